@@ -1,0 +1,248 @@
+"""fp64 CPU oracle for QLM plan scoring (arXiv 2407.00047, Secs. 6-7).
+
+TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` may import this package.  It shares no code
+with the HIP path and never imports it.
+
+The arithmetic lives in ``qlm_oracle.c`` (plain C, double precision); this
+module compiles it with gcc and marshals numpy arrays through ctypes.
+
+Inputs are plain mappings of numpy arrays (the same arrays the GPU reads):
+
+problem: n_groups, n_instances, n_models, n_classes, grp_count[G] int32,
+         grp_mu[G] f32, grp_var[G] f32, grp_model[G] int32, grp_slo[G] f32,
+         inst_tput[I] f32, inst_class[I] int32, inst_model0[I] int32 or None,
+         swap_cost[C*M*M] f32 or None, evict_cost float
+plans:   n_plans, perm[G, ld] int32, qoff[I+1, ld] int32,
+         evict_bits[ceil(G/32), ld] uint32 or None      (slot-major)
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+import threading
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "qlm_oracle.c")
+_LIB = os.path.join(_HERE, "libqlm_oracle.so")
+_lock = threading.Lock()
+_default = None
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (IEEE double, no contraction, OpenMP)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-O2", "-fopenmp", "-ffp-contract=off", "-fno-fast-math",
+               "-std=c11", "-Wall", "-Wextra", "-shared", "-fPIC", "-o", tmp, _SRC, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+class _Problem(ctypes.Structure):
+    _fields_ = [("n_groups", ctypes.c_int32), ("n_instances", ctypes.c_int32),
+                ("n_models", ctypes.c_int32), ("n_classes", ctypes.c_int32),
+                ("grp_count", ctypes.c_void_p), ("grp_mu", ctypes.c_void_p),
+                ("grp_var", ctypes.c_void_p), ("grp_model", ctypes.c_void_p),
+                ("grp_slo", ctypes.c_void_p), ("inst_tput", ctypes.c_void_p),
+                ("inst_class", ctypes.c_void_p), ("inst_model0", ctypes.c_void_p),
+                ("swap_cost", ctypes.c_void_p), ("evict_cost", ctypes.c_float)]
+
+
+class _Plans(ctypes.Structure):
+    _fields_ = [("n_plans", ctypes.c_int64), ("ld", ctypes.c_int64),
+                ("perm", ctypes.c_void_p), ("qoff", ctypes.c_void_p),
+                ("evict_bits", ctypes.c_void_p)]
+
+
+class Oracle:
+    """A loaded oracle library.  ``Oracle()`` is the committed source built by
+    ``build()``; tests may load another build of it (for mutation checks)."""
+
+    def __init__(self, path: str | None = None):
+        if path is None:
+            if not os.path.exists(_LIB):
+                build(force=False)
+            path = _LIB
+        lib = ctypes.CDLL(path)
+        dp = ctypes.POINTER(ctypes.c_double)
+        lib.oracle_plan.argtypes = [ctypes.POINTER(_Problem), ctypes.POINTER(_Plans),
+                                    ctypes.c_int64, dp, dp, dp, dp, dp]
+        lib.oracle_plan.restype = ctypes.c_int
+        lib.oracle_score_plans.argtypes = [ctypes.POINTER(_Problem), ctypes.POINTER(_Plans),
+                                           ctypes.c_int64, ctypes.c_int64, dp, dp, ctypes.c_int]
+        lib.oracle_score_plans.restype = ctypes.c_int64
+        lib.oracle_argmin.argtypes = [dp, ctypes.c_int64, dp]
+        lib.oracle_argmin.restype = ctypes.c_int64
+        lib.oracle_max_threads.restype = ctypes.c_int
+        self.lib = lib
+        self.path = path
+
+    def max_threads(self) -> int:
+        return int(self.lib.oracle_max_threads())
+
+    def score_plans(self, problem, plans, p0: int = 0, count: int | None = None,
+                    threads: int = 0):
+        """fp64 score and penalty of plans [p0, p0+count).  Returns (score, penalty)."""
+        b = _Bound(problem, plans)
+        if count is None:
+            count = b.n_plans - p0
+        if p0 < 0 or count < 0 or p0 + count > b.n_plans:
+            raise ValueError("plan range out of bounds")
+        score = np.empty(count, np.float64)
+        pen = np.empty(count, np.float64)
+        bad = self.lib.oracle_score_plans(ctypes.byref(b.problem), ctypes.byref(b.plans), p0,
+                                          count, _dp(score), _dp(pen), int(threads))
+        if bad:
+            raise ValueError("%d malformed plans" % bad)
+        return score, pen
+
+    def plan_detail(self, problem, plans, p: int):
+        """Per-slot E[W], SD[W], P and the plan's score and penalty, for plan p."""
+        b = _Bound(problem, plans)
+        if not 0 <= p < b.n_plans:
+            raise ValueError("plan index out of range")
+        wm = np.full(b.G, np.nan)
+        ws = np.full(b.G, np.nan)
+        pr = np.full(b.G, np.nan)
+        sc = np.zeros(1)
+        pe = np.zeros(1)
+        rc = self.lib.oracle_plan(ctypes.byref(b.problem), ctypes.byref(b.plans), p,
+                                  _dp(wm), _dp(ws), _dp(pr), _dp(sc), _dp(pe))
+        if rc != 0:
+            raise ValueError("malformed plan %d" % p)
+        return {"wait_mean": wm, "wait_sd": ws, "prob": pr, "score": float(sc[0]),
+                "penalty": float(pe[0])}
+
+    def argmin(self, score) -> tuple[int, float]:
+        """Lowest score, lowest index on ties."""
+        s = np.ascontiguousarray(score, dtype=np.float64)
+        bs = np.zeros(1)
+        idx = self.lib.oracle_argmin(_dp(s), s.size, _dp(bs))
+        return int(idx), float(bs[0])
+
+    def best_plan(self, problem, plans, threads: int = 0) -> tuple[int, float]:
+        """argmin_p score_p over all plans, lowest index on ties."""
+        score, _ = self.score_plans(problem, plans, threads=threads)
+        return self.argmin(score)
+
+
+def default() -> Oracle:
+    global _default
+    with _lock:
+        if _default is None:
+            _default = Oracle()
+    return _default
+
+
+def _arr(a, dtype):
+    if a is None:
+        return None
+    a = np.ascontiguousarray(a, dtype=dtype)
+    return a
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data
+
+
+def _dp(a):
+    return None if a is None else a.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+
+
+class _Bound:
+    """Keeps the numpy buffers alive while ctypes structs point at them."""
+
+    def __init__(self, problem, plans):
+        G = int(problem["n_groups"])
+        I = int(problem["n_instances"])
+        self.keep = []
+
+        def k(x, dt):
+            x = _arr(x, dt)
+            self.keep.append(x)
+            return x
+
+        pr = _Problem()
+        pr.n_groups = G
+        pr.n_instances = I
+        pr.n_models = int(problem["n_models"])
+        pr.n_classes = int(problem["n_classes"])
+        pr.grp_count = _ptr(k(problem["grp_count"], np.int32))
+        pr.grp_mu = _ptr(k(problem["grp_mu"], np.float32))
+        pr.grp_var = _ptr(k(problem["grp_var"], np.float32))
+        pr.grp_model = _ptr(k(problem["grp_model"], np.int32))
+        pr.grp_slo = _ptr(k(problem["grp_slo"], np.float32))
+        pr.inst_tput = _ptr(k(problem["inst_tput"], np.float32))
+        pr.inst_class = _ptr(k(problem["inst_class"], np.int32))
+        pr.inst_model0 = _ptr(k(problem.get("inst_model0"), np.int32))
+        pr.swap_cost = _ptr(k(problem.get("swap_cost"), np.float32))
+        pr.evict_cost = float(problem.get("evict_cost", 0.0))
+        self.problem = pr
+        # the C code trusts sizes and ranges; check them here
+        M, C = pr.n_models, pr.n_classes
+        for name in ("grp_count", "grp_mu", "grp_var", "grp_model", "grp_slo"):
+            if np.asarray(problem[name]).size != G:
+                raise ValueError(name + " must have n_groups entries")
+        for name in ("inst_tput", "inst_class"):
+            if np.asarray(problem[name]).size != I:
+                raise ValueError(name + " must have n_instances entries")
+        model = np.asarray(problem["grp_model"])
+        cls = np.asarray(problem["inst_class"])
+        if G < 1 or I < 1 or M < 1 or C < 1:
+            raise ValueError("sizes must be positive")
+        if model.min() < 0 or model.max() >= M or cls.min() < 0 or cls.max() >= C:
+            raise ValueError("model or class index out of range")
+        if problem.get("inst_model0") is not None:
+            m0 = np.asarray(problem["inst_model0"])
+            if m0.size != I or m0.min() < -1 or m0.max() >= M:
+                raise ValueError("inst_model0 must be [I] in [-1, M)")
+        if problem.get("swap_cost") is not None and np.asarray(problem["swap_cost"]).size != C * M * M:
+            raise ValueError("swap_cost must have C*M*M entries")
+
+        perm = k(plans["perm"], np.int32)
+        qoff = k(plans["qoff"], np.int32)
+        ev = k(plans.get("evict_bits"), np.uint32)
+        if perm.ndim != 2 or perm.shape[0] != G:
+            raise ValueError("perm must be [G, ld]")
+        ld = perm.shape[1]
+        if qoff.shape != (I + 1, ld):
+            raise ValueError("qoff must be [I+1, ld]")
+        if ev is not None and ev.shape != ((G + 31) // 32, ld):
+            raise ValueError("evict_bits must be [ceil(G/32), ld]")
+        n_plans = int(plans.get("n_plans", ld))
+        if not 0 <= n_plans <= ld:
+            raise ValueError("n_plans must be in [0, ld]")
+        pl = _Plans()
+        pl.n_plans = n_plans
+        pl.ld = ld
+        pl.perm = _ptr(perm)
+        pl.qoff = _ptr(qoff)
+        pl.evict_bits = _ptr(ev)
+        self.plans = pl
+        self.n_plans = n_plans
+        self.G = G
+
+
+def max_threads() -> int:
+    return default().max_threads()
+
+
+def score_plans(problem, plans, p0: int = 0, count: int | None = None, threads: int = 0):
+    return default().score_plans(problem, plans, p0, count, threads)
+
+
+def plan_detail(problem, plans, p: int):
+    return default().plan_detail(problem, plans, p)
+
+
+def argmin(score) -> tuple[int, float]:
+    return default().argmin(score)
+
+
+def best_plan(problem, plans, threads: int = 0) -> tuple[int, float]:
+    return default().best_plan(problem, plans, threads)

@@ -1,0 +1,389 @@
+"""Pins of the fp64 oracle against what the paper and the mathematics fix.
+
+Each ``pin_*`` takes a loaded oracle (``oracle.Oracle``) and raises
+AssertionError when the oracle disagrees.  They are run against the committed
+oracle by ``test_oracle_pins.py`` and against deliberately broken builds of it
+by ``test_oracle_mutants.py`` (every planted mistake must fail at least one).
+
+Expected values are hand-derived for hand-built inputs, textbook normal-table
+values (tests/golden/normal_upper_tail.txt), invariants, a Monte Carlo of the
+stated Normal model, or brute force over all orderings of tiny inputs.
+"""
+from __future__ import annotations
+
+import os
+
+import numpy as np
+
+from cases import all_orders, plans, problem
+
+_GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def normal_table():
+    rows = []
+    with open(os.path.join(_GOLDEN, "normal_upper_tail.txt")) as f:
+        for line in f:
+            line = line.strip()
+            if line and not line.startswith("#"):
+                z, q = line.split()
+                rows.append((float(z), float(q)))
+    return rows
+
+
+# ---------------------------------------------------------------------------
+# Closed forms on hand-built queues
+
+
+def pin_deterministic_queue(orc):
+    """One queue, sigma^2 = 0 (Sec. 6, Eq. base_equation with known tokens).
+    Each group carries n*mu = 400 tokens and Theta = 400 tok/s, so the group at
+    position j waits exactly j seconds (the tokens of the j groups ahead)."""
+    n = [4, 2, 8, 1, 5]
+    mu = [100, 200, 50, 400, 80]
+    slo = [0.5, 0.5, 2.5, 3.0, 10.0]
+    pr = problem([(n[k], mu[k], 0.0, 0, slo[k]) for k in range(5)], [(400.0, 0)])
+    pl = plans([[[0, 1, 2, 3, 4]]], 5)
+    d = orc.plan_detail(pr, pl, 0)
+    assert np.array_equal(d["wait_mean"], [0.0, 1.0, 2.0, 3.0, 4.0]), d["wait_mean"]
+    assert np.array_equal(d["wait_sd"], [0.0] * 5), d["wait_sd"]
+    # SD = 0: violated iff the wait strictly exceeds the SLO; 3.0 > 3.0 is met
+    assert np.array_equal(d["prob"], [0.0, 1.0, 0.0, 0.0, 0.0]), d["prob"]
+    assert d["score"] == 2.0, d["score"]          # n of the violated group
+    assert d["penalty"] == -6.5, d["penalty"]     # sum of (wait - slo), Eq. penalty
+    # a different order moves the waits with the groups
+    pl2 = plans([[[4, 3, 2, 1, 0]]], 5)
+    d2 = orc.plan_detail(pr, pl2, 0)
+    assert np.array_equal(d2["wait_mean"], [0.0, 1.0, 2.0, 3.0, 4.0])
+    # slots hold groups 4,3,2,1,0 (slo 10, 3, 2.5, .5, .5) waiting 0..4 s: groups 1 and 0
+    # (n = 2 and 4) miss their SLO
+    assert np.array_equal(d2["prob"], [0.0, 0.0, 0.0, 1.0, 1.0]), d2["prob"]
+    assert d2["score"] == 2.0 + 4.0
+
+
+def pin_variance_queue(orc):
+    """Same queue with n*sigma^2 = 40000 per group (Eq. output_token_dist): the
+    variance of the tokens ahead adds up, so SD[W_j] = sqrt(40000 j)/400 = sqrt(j)/2.
+    SLOs are placed at exact z-scores, so P(W > slo) = Q(z) from the normal table."""
+    n = [4, 2, 8, 1, 5]
+    mu = [100, 200, 50, 400, 80]
+    var = [10000, 20000, 5000, 40000, 8000]
+    table = dict(normal_table())
+    # wait = 0,1,2,3,4 ; sd = 0, .5, .707, .866, 1
+    slo = [10.0, 2.0, 2.0, 1.0e9, 5.0]            # z: -, 2, 0, huge, 1
+    pr = problem([(n[k], mu[k], var[k], 0, slo[k]) for k in range(5)], [(400.0, 0)])
+    pl = plans([[[0, 1, 2, 3, 4]]], 5)
+    d = orc.plan_detail(pr, pl, 0)
+    sd = np.array([0.0, 0.5, np.sqrt(2.0) / 2, np.sqrt(3.0) / 2, 1.0])
+    assert np.allclose(d["wait_sd"], sd, rtol=1e-15, atol=0), d["wait_sd"]
+    want = [0.0, table[2.0], 0.5, 0.0, table[1.0]]
+    assert np.allclose(d["prob"], want, rtol=1e-12, atol=1e-15), (d["prob"], want)
+    assert abs(d["score"] - (2 * table[2.0] + 8 * 0.5 + 5 * table[1.0])) < 1e-12
+    # mirrored SLOs: z = -2 at slot 1 and z = -1 at slot 4 give 1 - Q(z)
+    slo_m = [10.0, 0.0, 2.0, 1.0e9, 3.0]
+    pr_m = problem([(n[k], mu[k], var[k], 0, slo_m[k]) for k in range(5)], [(400.0, 0)])
+    dm = orc.plan_detail(pr_m, pl, 0)
+    assert abs(dm["prob"][1] - (1 - table[2.0])) < 1e-13, dm["prob"]
+    assert abs(dm["prob"][4] - (1 - table[1.0])) < 1e-13, dm["prob"]
+
+
+def pin_normal_table(orc):
+    """P(W > slo) against the textbook Q(z) at every tabulated z, both signs.
+    A head group of 400 tokens with variance 160000 on Theta = 400 gives the
+    second group W ~ N(1, 1) (seconds), so slo = 1 + z puts it at z."""
+    rows = normal_table()
+    for z, q in rows:
+        for sign in (+1, -1):
+            slo = 1.0 + sign * z
+            pr = problem([(1, 400.0, 160000.0, 0, 100.0), (3, 7.0, 9.0, 0, slo)], [(400.0, 0)])
+            d = orc.plan_detail(pr, plans([[[0, 1]]], 2), 0)
+            assert d["wait_mean"][1] == 1.0 and d["wait_sd"][1] == 1.0
+            want = q if sign > 0 else 1.0 - q
+            got = d["prob"][1]
+            assert abs(got - want) <= 1e-12 * max(want, 1e-300) + 1e-15, (z, sign, got, want)
+            assert abs(d["score"] - 3 * want) <= 1e-12 * 3 * max(want, 1e-300) + 1e-15
+
+
+def _swap_table():
+    """[C=2][M=3][M=3] swap costs, from-model row, to-model column; every
+    off-diagonal entry distinct (100c + 10a + b + 1) so that a transposed or
+    misplaced lookup shows; the diagonal is never a swap and holds 5000."""
+    S = np.zeros((2, 3, 3), np.float32)
+    for c in range(2):
+        for a in range(3):
+            for b in range(3):
+                S[c, a, b] = 5000.0 if a == b else 100 * c + 10 * a + b + 1
+    return S
+
+
+def pin_swap_costs(orc):
+    """Model transitions (Sec. 7, Eq. transition_time) add the swap time to the
+    waiting time of the group whose model is loaded and of every group behind it.
+    No tokens (mu = 0), so the wait is the swap sum alone."""
+    models = [0, 1, 1, 2, 0, 2, 2, 0]
+    groups = [(1, 0.0, 0.0, m, 1e6) for m in models]
+    pr = problem(groups, [(400.0, 1), (250.0, 0)], n_models=3, n_classes=2,
+                 swap=_swap_table(), model0=[-1, 1])
+    pl = plans([[[0, 1, 2, 3, 4], [5, 6, 7]]], 8)
+    d = orc.plan_detail(pr, pl, 0)
+    # queue 0 (class 1, nothing loaded): 0->1 costs 102, 1->2 costs 113, 2->0 costs 121
+    # queue 1 (class 0, model 1 loaded): head 1->2 costs 13, then 2->2 free, 2->0 costs 21
+    want = [0.0, 102.0, 102.0, 215.0, 336.0, 13.0, 13.0, 34.0]
+    assert np.array_equal(d["wait_mean"], want), d["wait_mean"]
+
+
+def pin_eviction_costs(orc):
+    """An evicted slot adds the eviction cost to its own wait and to every later
+    wait on the same queue, never to another queue."""
+    groups = [(1, 0.0, 0.0, 0, 1e6)] * 8
+    pr = problem(groups, [(400.0, 0), (400.0, 0)], evict_cost=2.5)
+    pl = plans([[[0, 1, 2, 3, 4], [5, 6, 7]]], 8, evict=[[1, 3, 7]])
+    d = orc.plan_detail(pr, pl, 0)
+    want = [0.0, 2.5, 2.5, 5.0, 5.0, 0.0, 0.0, 2.5]
+    assert np.array_equal(d["wait_mean"], want), d["wait_mean"]
+
+
+def pin_throughput_per_queue(orc):
+    """Each queue divides its own tokens by its own throughput (Eq. base_equation
+    with Theta per instance), and variances by Theta^2."""
+    groups = [(2, 300.0, 800.0, 0, 1e6)] * 4     # 600 tokens, variance 1600 each
+    pr = problem(groups, [(600.0, 0), (150.0, 0)])
+    pl = plans([[[0, 1], [2, 3]]], 4)
+    d = orc.plan_detail(pr, pl, 0)
+    assert np.array_equal(d["wait_mean"], [0.0, 1.0, 0.0, 4.0]), d["wait_mean"]
+    assert np.allclose(d["wait_sd"], [0.0, 40.0 / 600.0, 0.0, 40.0 / 150.0], rtol=1e-15)
+
+
+# ---------------------------------------------------------------------------
+# Invariants on random inputs
+
+
+def _random_case(rng, G=12, I=3, M=3, C=2, P=40, evict=True, model0=True):
+    groups = []
+    for _ in range(G):
+        n = int(rng.integers(1, 20))
+        mu = float(np.float32(rng.uniform(50, 500)))
+        var = float(np.float32(rng.uniform(0, 4e4)))
+        groups.append((n, mu, var, int(rng.integers(0, M)), float(np.float32(rng.uniform(1, 60)))))
+    inst = [(float(np.float32(rng.choice([800.0, 1500.0, 3000.0]))), int(rng.integers(0, C)))
+            for _ in range(I)]
+    S = rng.uniform(0.5, 10.0, (C, M, M)).astype(np.float32)
+    m0 = [int(x) for x in rng.integers(-1, M, I)] if model0 else None
+    pr = problem(groups, inst, n_models=M, n_classes=C, swap=S, evict_cost=1.5, model0=m0)
+    qls, evs = [], []
+    for _ in range(P):
+        order = rng.permutation(G)
+        owner = rng.integers(0, I, G)
+        qls.append([[int(i) for i in order if owner[i] == g] for g in range(I)])
+        evs.append(list(rng.choice(G, size=2, replace=False)) if evict else [])
+    pl = plans(qls, G, evict=evs if evict else None)
+    return pr, pl
+
+
+def pin_invariants(orc):
+    rng = np.random.default_rng(1234)
+    pr, pl = _random_case(rng)
+    for p in range(pl["n_plans"]):
+        d = orc.plan_detail(pr, pl, p)
+        q = pl["qoff"][:, p]
+        for g in range(pr["n_instances"]):
+            w = d["wait_mean"][q[g]:q[g + 1]]
+            s = d["wait_sd"][q[g]:q[g + 1]]
+            assert np.all(np.diff(w) >= 0) and np.all(np.diff(s) >= 0)
+            if q[g + 1] > q[g]:
+                assert s[0] == 0.0                     # nothing ahead of the head
+        assert np.all((d["prob"] >= 0) & (d["prob"] <= 1))
+    # P is non-increasing in the SLO, and 1/2 exactly at slo = E[W] (SD > 0)
+    d = orc.plan_detail(pr, pl, 0)
+    s = int(np.argmax(d["wait_sd"]))
+    i = int(pl["perm"][s, 0])
+    last = 2.0
+    for slo in np.linspace(d["wait_mean"][s] - 4 * d["wait_sd"][s],
+                           d["wait_mean"][s] + 4 * d["wait_sd"][s], 17):
+        pr2 = dict(pr)
+        pr2["grp_slo"] = pr["grp_slo"].copy()
+        pr2["grp_slo"][i] = np.float32(slo)
+        pv = orc.plan_detail(pr2, pl, 0)["prob"][s]
+        assert pv <= last + 1e-300
+        last = pv
+    # an SLO no wait can reach: nothing is violated
+    pr3 = dict(pr)
+    pr3["grp_slo"] = np.full(pr["n_groups"], 3.0e38, np.float32)
+    sc, _ = orc.score_plans(pr3, pl)
+    assert np.all(sc == 0.0)
+    # an SLO far below every wait: everything is violated
+    pr4 = dict(pr)
+    pr4["grp_slo"] = np.full(pr["n_groups"], -3.0e38, np.float32)
+    sc4, _ = orc.score_plans(pr4, pl)
+    assert np.all(sc4 == float(pr["grp_count"].sum()))
+
+
+def pin_half_at_mean(orc):
+    """P = 1/2 when the SLO equals the mean wait and SD > 0 (Normal symmetry)."""
+    pr = problem([(2, 300.0, 500.0, 0, 99.0), (1, 10.0, 10.0, 0, 1.5)], [(400.0, 0)])
+    d = orc.plan_detail(pr, plans([[[0, 1]]], 2), 0)
+    assert d["wait_mean"][1] == 1.5 and d["prob"][1] == 0.5
+
+
+def pin_identical_instances_symmetry(orc):
+    """Swapping the whole queues of two identical instances leaves every wait,
+    probability and the score unchanged (the score is a sum over queues)."""
+    rng = np.random.default_rng(7)
+    pr, pl = _random_case(rng, I=2, C=1, model0=False, evict=False)
+    pr["inst_tput"][:] = np.float32(1500.0)
+    for p in range(10):
+        q = pl["qoff"][:, p]
+        a = [int(x) for x in pl["perm"][q[0]:q[1], p]]
+        b = [int(x) for x in pl["perm"][q[1]:q[2], p]]
+        pl2 = plans([[a, b], [b, a]], pr["n_groups"])
+        s, _ = orc.score_plans(pr, pl2)
+        assert abs(s[0] - s[1]) <= 1e-12 * max(1.0, abs(s[0]))
+
+
+# ---------------------------------------------------------------------------
+# Monte Carlo of the stated model
+
+
+def _simulate(pr, queues, evicted, rng, n_samples):
+    """Draw every request's output tokens from N(mu, sigma^2) (the per-request
+    model of Sec. 6), serve each queue in order on its own throughput, and add
+    swap and eviction seconds as the queue is walked.  Returns W[sample, slot]
+    with slots in plan order."""
+    G = pr["n_groups"]
+    W = np.zeros((n_samples, G))
+    s = 0
+    S = pr["swap_cost"]
+    M = pr["n_models"]
+    for g, q in enumerate(queues):
+        theta = float(pr["inst_tput"][g])
+        c = int(pr["inst_class"][g])
+        prev = -1 if pr["inst_model0"] is None else int(pr["inst_model0"][g])
+        tokens = np.zeros(n_samples)
+        fixed = 0.0
+        for i in q:
+            m = int(pr["grp_model"][i])
+            if prev >= 0 and prev != m:
+                fixed += float(S[(c * M + prev) * M + m])
+            if s in evicted:
+                fixed += pr["evict_cost"]
+            W[:, s] = tokens / theta + fixed
+            n = int(pr["grp_count"][i])
+            draws = rng.normal(float(pr["grp_mu"][i]), np.sqrt(float(pr["grp_var"][i])),
+                               (n_samples, n))
+            tokens = tokens + draws.sum(axis=1)
+            prev = m
+            s += 1
+    return W
+
+
+def pin_monte_carlo(orc):
+    rng = np.random.default_rng(99)
+    groups = [(3, 200.0, 9000.0, 0, 0.0), (5, 120.0, 2500.0, 1, 0.0), (2, 400.0, 20000.0, 1, 0.0),
+              (4, 150.0, 4000.0, 0, 0.0), (6, 90.0, 1000.0, 1, 0.0), (3, 250.0, 12000.0, 0, 0.0)]
+    S = np.array([[[0, 2.0], [3.0, 0]], [[0, 0.5], [0.75, 0]]], np.float32)
+    pr = problem(groups, [(1000.0, 0), (600.0, 1)], n_models=2, n_classes=2, swap=S,
+                 evict_cost=0.4, model0=[1, -1])
+    queues = [[4, 0, 2], [1, 5, 3]]
+    evicted = {1, 4}
+    # SLOs at quantiles of an independent draw (so they sit inside each W's spread)
+    W0 = _simulate(pr, queues, evicted, rng, 20000)
+    levels = [0.15, 0.35, 0.5, 0.65, 0.85, 0.25]
+    slo_slot = [np.float32(np.quantile(W0[:, s], levels[s])) for s in range(6)]
+    perm = [i for q in queues for i in q]
+    for s, i in enumerate(perm):
+        pr["grp_slo"][i] = slo_slot[s]
+    pl = plans([queues], 6, evict=[sorted(evicted)])
+    d = orc.plan_detail(pr, pl, 0)
+    N = 400000
+    W = _simulate(pr, queues, evicted, rng, N)
+    slo = np.array([pr["grp_slo"][i] for i in perm], np.float64)
+    hat = (W > slo[None, :]).mean(axis=0)
+    se = np.sqrt(np.maximum(d["prob"] * (1 - d["prob"]), 1e-12) / N)
+    assert np.all(np.abs(hat - d["prob"]) <= 5 * se), (hat, d["prob"], se)
+    mean = W.mean(axis=0)
+    sd = W.std(axis=0)
+    assert np.allclose(mean, d["wait_mean"], rtol=0, atol=5 * sd.max() / np.sqrt(N) + 1e-9)
+    assert np.allclose(sd, d["wait_sd"], rtol=0.01, atol=1e-9), (sd, d["wait_sd"])
+    n = np.array([pr["grp_count"][i] for i in perm], np.float64)
+    score_hat = ((W > slo[None, :]) * n[None, :]).sum(axis=1)
+    assert abs(score_hat.mean() - d["score"]) <= 5 * score_hat.std() / np.sqrt(N)
+
+
+# ---------------------------------------------------------------------------
+# Brute force over orderings
+
+
+def pin_edf_special_case(orc):
+    """Sec. 2 Insight #3: with negligible swap cost EDF is the order to use.
+    With deterministic, equal-size groups the waiting time is the start time, and
+    Jackson's rule says EDF order minimises the maximum lateness max_j(W_j - slo_j);
+    so EDF also meets every SLO whenever any order does (score 0)."""
+    rng = np.random.default_rng(3)
+    for trial in range(6):
+        G = 6
+        slo = np.sort(rng.uniform(0.0, 6.0, G)).astype(np.float32)
+        rng.shuffle(slo)
+        groups = [(2, 200.0, 0.0, 0, float(slo[k])) for k in range(G)]   # 1 s each
+        pr = problem(groups, [(400.0, 0)])
+        pl = plans(all_orders(G), G)
+        score, _ = orc.score_plans(pr, pl)
+        lateness = []
+        for p in range(pl["n_plans"]):
+            d = orc.plan_detail(pr, pl, p)
+            sl = pr["grp_slo"][pl["perm"][:, p]].astype(np.float64)
+            lateness.append(np.max(d["wait_mean"] - sl))
+        edf = [[int(i) for i in np.argsort(slo, kind="stable")]]
+        ed = orc.plan_detail(pr, plans([edf], G), 0)
+        sl = pr["grp_slo"][edf[0]].astype(np.float64)
+        assert abs(np.max(ed["wait_mean"] - sl) - min(lateness)) < 1e-12
+        if score.min() == 0.0:
+            assert ed["score"] == 0.0
+        # brute-force argmin agrees with the oracle's argmin (first minimum)
+        best, bs = orc.argmin(score)
+        assert bs == score.min() and best == int(np.flatnonzero(score == score.min())[0])
+
+
+def pin_grouping_special_case(orc):
+    """Sec. 2 Insight #3: grouping same-model requests minimises the queue drain
+    time.  With no tokens, the last group's wait is the total swap time, which is
+    least (models - 1 swaps) exactly for the orders that keep each model together."""
+    models = [0, 0, 1, 1, 2, 2]
+    groups = [(1, 0.0, 0.0, m, 1e6) for m in models]
+    pr = problem(groups, [(400.0, 0)], n_models=3, swap=7.0)
+    pl = plans(all_orders(6), 6)
+    last = []
+    contiguous = []
+    for p in range(pl["n_plans"]):
+        d = orc.plan_detail(pr, pl, p)
+        last.append(d["wait_mean"][-1])
+        ms = [models[i] for i in pl["perm"][:, p]]
+        runs = 1 + sum(1 for k in range(1, 6) if ms[k] != ms[k - 1])
+        contiguous.append(runs == 3)
+    last = np.array(last)
+    assert last.min() == 14.0
+    assert np.array_equal(last == 14.0, np.array(contiguous))
+    assert int(np.sum(contiguous)) == 48          # 3! model orders x 2!^3 within
+
+
+def pin_argmin_ties(orc):
+    """Equal scores (duplicate plans) go to the lowest plan index."""
+    pr = problem([(3, 100.0, 500.0, 0, 0.2), (2, 50.0, 300.0, 0, 0.3), (4, 80.0, 100.0, 0, 0.5)],
+                 [(400.0, 0)])
+    orders = [[[2, 1, 0]], [[1, 0, 2]], [[0, 1, 2]], [[1, 0, 2]], [[0, 2, 1]], [[1, 0, 2]]]
+    pl = plans(orders, 3)
+    score, _ = orc.score_plans(pr, pl)
+    assert score[1] == score[3] == score[5]
+    best, bs = orc.argmin(score)
+    assert bs == score.min()
+    assert best == int(np.flatnonzero(score == bs)[0])
+    # put the best order first, then later duplicates of it: index 0 must win
+    b = orders[best]
+    pl2 = plans([b, orders[0], b, b], 3)
+    s2, _ = orc.score_plans(pr, pl2)
+    assert orc.argmin(s2)[0] == (0 if s2[0] <= s2[1] else 1)
+
+
+ALL_PINS = [pin_deterministic_queue, pin_variance_queue, pin_normal_table, pin_swap_costs,
+            pin_eviction_costs, pin_throughput_per_queue, pin_invariants, pin_half_at_mean,
+            pin_identical_instances_symmetry, pin_monte_carlo, pin_edf_special_case,
+            pin_grouping_special_case, pin_argmin_ties]

@@ -1,0 +1,108 @@
+"""The pins must catch plausible mistakes in the oracle.
+
+Each case below plants one mistake in a copy of oracle/qlm_oracle.c (on the CPU,
+in a temporary directory), builds it with gcc, and runs every pin against it; at
+least one pin must fail.  A mutant that survives means a blind spot in the pins.
+"""
+import os
+import subprocess
+
+import pytest
+
+import oracle
+import pins
+
+_SRC = os.path.join(os.path.dirname(oracle.__file__), "qlm_oracle.c")
+
+# (name, text in the committed source, replacement)
+MUTANTS = [
+    ("inclusive_token_prefix",
+     "const double EW = A / theta + K;",
+     "A += n * mu; const double EW = A / theta + K; A -= n * mu;"),
+    ("tokens_not_scaled_by_count", "A += n * mu;", "A += mu;"),
+    ("variance_not_scaled_by_count", "V += n * var;", "V += var;"),
+    ("variance_scaled_by_count_squared", "V += n * var;", "V += n * n * var;"),
+    ("sd_without_sqrt", "const double SD = sqrt(V) / theta;", "const double SD = V / theta;"),
+    ("sd_divided_by_theta_squared", "const double SD = sqrt(V) / theta;",
+     "const double SD = sqrt(V) / (theta * theta);"),
+    ("tokens_times_theta", "const double EW = A / theta + K;", "const double EW = A * theta + K;"),
+    ("z_sign_flipped", "erfc((slo - EW) / (SD * sqrt(2.0)))", "erfc((EW - slo) / (SD * sqrt(2.0)))"),
+    ("missing_sqrt2", "erfc((slo - EW) / (SD * sqrt(2.0)))", "erfc((slo - EW) / SD)"),
+    ("missing_half", "P = 0.5 * erfc(", "P = erfc("),
+    ("erf_instead_of_erfc", "P = 0.5 * erfc(", "P = 0.5 * erf("),
+    ("sd_zero_non_strict", "P = (EW > slo) ? 1.0 : 0.0;", "P = (EW >= slo) ? 1.0 : 0.0;"),
+    ("swap_dropped",
+     "K += (double)pr->swap_cost[((int64_t)cls * M + m_prev) * M + m];", "(void)cls;"),
+    ("swap_transposed",
+     "pr->swap_cost[((int64_t)cls * M + m_prev) * M + m]",
+     "pr->swap_cost[((int64_t)cls * M + m) * M + m_prev]"),
+    ("swap_class_ignored",
+     "pr->swap_cost[((int64_t)cls * M + m_prev) * M + m]",
+     "pr->swap_cost[((int64_t)0 * M + m_prev) * M + m]"),
+    ("swap_paid_after_the_group",     # the literal sum over k < j of the LP
+     "            if (m_prev >= 0 && m_prev != m && pr->swap_cost)\n"
+     "                K += (double)pr->swap_cost[((int64_t)cls * M + m_prev) * M + m];\n",
+     "            const double K_before = K;\n"
+     "            if (m_prev >= 0 && m_prev != m && pr->swap_cost)\n"
+     "                K += (double)pr->swap_cost[((int64_t)cls * M + m_prev) * M + m];\n"
+     "            const double K_swap = K - K_before; K = K_before;\n"),
+    ("head_model_ignored", "int m_prev = pr->inst_model0 ? pr->inst_model0[g] : -1;",
+     "int m_prev = -1;"),
+    ("eviction_dropped", "K += (double)pr->evict_cost;", "(void)0;"),
+    ("eviction_bit_off_by_one", "return (int)((w >> (s % 32)) & 1u);",
+     "return (int)((w >> ((s + 1) % 32)) & 1u);"),
+    ("costs_not_carried", "double K = 0.0;   /* swap", "double K = 0.0; double K0 = 0.0; /* swap"),
+    ("score_not_weighted_by_count", "score_g   += n * P;", "score_g   += P;"),
+    ("penalty_sign", "penalty_g += EW - slo;", "penalty_g += slo - EW;"),
+    ("prefix_not_reset_per_queue", "        double A = 0.0;   /* tokens",
+     "        static double A_carry = 0.0; double A = A_carry; (void)A_carry;   /* tokens"),
+    ("argmin_last_on_ties", "if (score[p] < bs) {", "if (score[p] <= bs) {"),
+    ("theta_of_first_queue", "const double theta = (double)pr->inst_tput[g];",
+     "const double theta = (double)pr->inst_tput[0];"),
+]
+
+
+def _fix_costs_not_carried(src):
+    # make the eviction/swap total restart at every position (K not carried)
+    return src.replace("            if (m_prev >= 0 && m_prev != m && pr->swap_cost)",
+                       "            K = K0;\n            if (m_prev >= 0 && m_prev != m && pr->swap_cost)")
+
+
+def _fix_swap_after(src):
+    # the swap reaches the waits of later groups only
+    return src.replace("            A += n * mu;\n", "            A += n * mu; K += K_swap;\n")
+
+
+def _fix_prefix_carry(src):
+    return src.replace("            A += n * mu;\n", "            A += n * mu; A_carry = A;\n")
+
+
+def _mutant_source(name, old, new):
+    src = open(_SRC).read()
+    assert src.count(old) >= 1, name
+    src = src.replace(old, new, 1)
+    if name == "costs_not_carried":
+        src = _fix_costs_not_carried(src)
+    if name == "swap_paid_after_the_group":
+        src = _fix_swap_after(src)
+    if name == "prefix_not_reset_per_queue":
+        src = _fix_prefix_carry(src)
+    return src
+
+
+@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_mutant_is_caught(tmp_path, name, old, new):
+    src = _mutant_source(name, old, new)
+    c = tmp_path / "mutant.c"
+    so = tmp_path / "libmutant.so"
+    c.write_text(src)
+    subprocess.run(["gcc", "-O1", "-fopenmp", "-ffp-contract=off", "-std=c11", "-shared", "-fPIC",
+                    "-w", "-o", str(so), str(c), "-lm"], check=True)
+    orc = oracle.Oracle(str(so))
+    failed = []
+    for pin in pins.ALL_PINS:
+        try:
+            pin(orc)
+        except (AssertionError, ValueError, FloatingPointError):
+            failed.append(pin.__name__)
+    assert failed, "mutant %s survived every pin" % name
