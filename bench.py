@@ -1,0 +1,178 @@
+#!/usr/bin/env python3
+"""Benchmark: candidate plans scored per second (RWT + SLO-violation
+probability + exact argmin) on one MI355X, with the HBM roofline of the
+scoring kernel and the fp64 CPU oracle timed beside it.
+
+One step = one qlm_best_plan call over the whole plan batch, inputs already
+resident in HBM: stage the tables, stream every plan, gather group statistics,
+transitions and costs, running prefix sums, normal tail, per-plan reduction,
+then the exact re-score of the screened candidates and the argmin.
+
+Prints one JSON line (the last line of stdout).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+METRIC = "candidate plans scored/sec (RWT + SLO prob) and % of HBM roofline, 1 GPU"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes_per_plan(problem) -> int:
+    """What the method must move per plan: every slot's group id, the queue
+    offsets, the eviction bits (when present), and the plan's score."""
+    G, I = problem["n_groups"], problem["n_instances"]
+    ev = 4 * ((G + 31) // 32) if problem.get("n_evict", 0) > 0 else 0
+    return 4 * G + 4 * (I + 1) + ev + 8
+
+
+def kernel_source_hash() -> str:
+    with open(os.path.join(ROOT, "paper_2407_00047_amd", "csrc", "qlm.hip"), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic(config: str, plans: int):
+    """HBM bytes per scoring launch from the committed rocprofv3 counter summary,
+    when it was taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", "k_score_%s_traffic.json" % config)
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    if t.get("source_sha256") != kernel_source_hash() or t.get("plans") != plans:
+        return None
+    return float(t["hbm_bytes_per_launch"])
+
+
+def cpu_baseline(problem, plans, seconds: float):
+    import oracle
+    orc = oracle.default()
+    P = plans["n_plans"]
+    n0 = min(P, 256)
+    t0 = time.perf_counter()
+    orc.score_plans(problem, plans, 0, n0)
+    dt = max(time.perf_counter() - t0, 1e-6)
+    count = int(min(P, max(n0, seconds * n0 / dt)))
+    t0 = time.perf_counter()
+    orc.score_plans(problem, plans, 0, count)
+    dt = time.perf_counter() - t0
+    return {"value": count / dt, "unit": "plans/s", "cores": orc.max_threads(), "kind": "oracle",
+            "sample": "plans 0..%d of the same batch (%d of %d), all host threads, fp64 C oracle,"
+                      " %.1f s" % (count - 1, count, P, dt)}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="large",
+                    help="workload: tiny, mixed, hetero, heavy, large (default)")
+    ap.add_argument("--plans", type=int, default=None, help="override the plan count")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print("bench.py: this build scores plans on one GPU; --gpus %d is not supported "
+              "(plans shard across GPUs by range, see the design notes)" % args.gpus,
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2407_00047_amd import qlm, workload
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    qlm.library()
+
+    cfg = workload.CONFIGS[args.config]
+    P = cfg["P"] if args.plans is None else args.plans
+    t0 = time.perf_counter()
+    pr = workload.make_problem(args.config)
+    pl = workload.make_plans(pr, 0, P)
+    log("generated %s: G=%d I=%d P=%d in %.1f s" % (args.config, pr["n_groups"],
+                                                     pr["n_instances"], P,
+                                                     time.perf_counter() - t0))
+    dpr = qlm.DeviceProblem(pr, device=dev)
+    dpl = qlm.DevicePlans.from_host(pl, device=dev)
+    ws = qlm.workspace(dpr, P, device=dev)
+    bi = torch.empty(1, dtype=torch.int64, device=dev)
+    bs = torch.empty(1, dtype=torch.float64, device=dev)
+    torch.cuda.synchronize()
+
+    for _ in range(args.warmup):
+        qlm.best_plan(dpr, dpl, ws=ws, out=(bi, bs))
+    torch.cuda.synchronize()
+
+    qlm.timing_enable(True)
+    qlm.timing_read()                      # reset
+    stream = torch.cuda.current_stream()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(args.steps):
+        qlm.best_plan(dpr, dpl, ws=ws, out=(bi, bs))
+    e1.record(stream)
+    torch.cuda.synchronize()
+    qlm.timing_enable(False)
+    n_launch, k_ms = qlm.timing_read()
+    total_ms = e0.elapsed_time(e1)
+    ms_step = total_ms / args.steps
+    plans_per_s = P / (ms_step / 1e3)
+    best_index = int(bi.item())
+    best_score = float(bs.item())
+
+    bpp = algorithmic_bytes_per_plan(pr)
+    k_avg_ms = k_ms / max(n_launch, 1)
+    achieved = bpp * P / (k_avg_ms / 1e3) / 1e9
+    traffic = measured_traffic(args.config, P)
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
+                "traffic": traffic, "kernel": "k_score", "kernel_avg_ms": round(k_avg_ms, 4),
+                "algorithmic_bytes_per_launch": bpp * P}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle ...")
+        cpu = cpu_baseline(pr, pl, args.cpu_seconds)
+
+    N = workload.total_requests(pr)
+    out = {
+        "metric": METRIC, "value": round(plans_per_s, 1), "unit": "plans/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32+f64", "data": "synthetic",
+        "config": {"workload": "%s: %d groups (%d requests), %d instances in %d classes, "
+                               "%d models, %d plans" % (args.config, pr["n_groups"], N,
+                                                        pr["n_instances"], pr["n_classes"],
+                                                        pr["n_models"], P),
+                   "plans": P, "groups": pr["n_groups"], "instances": pr["n_instances"],
+                   "requests": N},
+        "requests_per_s": round(plans_per_s * N, 1),
+        "best_index": best_index, "best_score": best_score,
+        "roofline": roofline, "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

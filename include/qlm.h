@@ -1,0 +1,192 @@
+/*
+ * qlm.h -- C interface of libqlm: batched request waiting time (RWT) estimation
+ * and SLO-violation scoring of candidate virtual-queue plans on an MI355X
+ * (gfx950), after "Queue Management for SLO-Oriented Large Language Model
+ * Serving" (QLM, arXiv 2407.00047).
+ *
+ * Model (paper Secs. 6 and 7).  Request groups (Sec. 4, Definition "Request
+ * Group") carry n_i requests of one model whose output tokens have mean mu_i
+ * and variance sigma_i^2, and one TTFT SLO.  A plan places every group in
+ * exactly one position of exactly one virtual queue (Sec. 7, Eq.
+ * slot_assignment); queue g is served by an instance of token throughput
+ * Theta_g.  For the group at position j of queue g:
+ *
+ *   E[W] = (sum_{k<j} n_k mu_k) / Theta_g + K_j          (Eq. base_equation;
+ *   SD[W] = sqrt(sum_{k<j} n_k sigma_k^2) / Theta_g       Eq. output_token_dist)
+ *   K_j  = sum_{k<=j} ( t_k * S[class_g][m_{k-1}][m_k] + evicted_k * E )
+ *          with t_k = (m_{k-1} != m_k)                    (Eq. transition_time,
+ *          and m_{-1} = inst_model0[g] (none if -1)        swap term of Eq.
+ *                                                          completion_time)
+ *   P    = P(W > slo), W ~ N(E[W], SD^2); for SD = 0, P = [E[W] > slo]
+ *   score_p = sum over queues, then positions, of n * P   (expected number of
+ *                                                          requests missing their SLO)
+ *   penalty_p = sum of (E[W] - slo)                        (Eq. penalty, objective)
+ *
+ * The group's own incoming model swap and its own eviction count in its wait;
+ * an eviction adds a fixed cost and no variance.
+ *
+ * Conventions for every entry point:
+ *  - All array pointers are DEVICE pointers owned by the caller, unless stated.
+ *    The library allocates no device memory.  Scalars and the structs themselves
+ *    live in host memory and are read during the call only.
+ *  - Work is enqueued on `stream` (0 = the null stream) and is asynchronous:
+ *    outputs are valid once the stream reaches that point.  Calls keep no state
+ *    between them, may run concurrently on different streams, and are
+ *    thread-safe (the error text is per host thread).
+ *  - The return value is a status (QLM_OK = 0).  Nothing is enqueued when a call
+ *    returns an argument, capacity or workspace error.  No exception crosses
+ *    the interface.
+ *  - Plan contents are not checked by the scoring calls (use
+ *    qlm_validate_plans): a malformed plan yields an unspecified score for that
+ *    plan, never an out-of-bounds access.  Group ids are clamped to [0, G],
+ *    models and classes to their ranges, counts to 24 bits.
+ */
+#ifndef QLM_H
+#define QLM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* A HIP stream (hipStream_t); 0 is the null stream. */
+typedef void *qlm_stream;
+
+enum {
+    QLM_OK = 0,
+    QLM_ERR_ARG = 1,        /* null required pointer, bad size or stride      */
+    QLM_ERR_CAPACITY = 2,   /* tables exceed the on-chip (LDS) budget         */
+    QLM_ERR_WORKSPACE = 3,  /* workspace missing, too small or misaligned     */
+    QLM_ERR_HIP = 4         /* a HIP call or kernel launch failed             */
+};
+
+/* Request groups, instances and swap costs (Sec. 7, table of LP symbols:
+ * models_i, slos_i, S; Sec. 6: mu_o, sigma_o, Theta).                       */
+typedef struct qlm_problem {
+    int32_t n_groups;            /* G >= 1                                       */
+    int32_t n_instances;         /* I >= 1 (one virtual queue per instance)      */
+    int32_t n_models;            /* M, 1 <= M <= 255                             */
+    int32_t n_classes;           /* C >= 1 hardware classes                      */
+    const int32_t *grp_count;    /* [G] requests per group, 0 <= n < 2^24        */
+    const float   *grp_mu;       /* [G] mean output tokens per request           */
+    const float   *grp_var;      /* [G] variance of output tokens, >= 0          */
+    const int32_t *grp_model;    /* [G] model of the group, in [0, M)            */
+    const float   *grp_slo;      /* [G] TTFT SLO, seconds                        */
+    const float   *inst_tput;    /* [I] token throughput Theta, tokens/s, > 0    */
+    const int32_t *inst_class;   /* [I] class of the instance, in [0, C)         */
+    const int32_t *inst_model0;  /* [I] model loaded before the head, -1 = none;
+                                    NULL = none for every instance               */
+    const float   *swap_cost;    /* [C][M][M] seconds to swap from model a (row)
+                                    to model b (column) on class c; the diagonal
+                                    is ignored; NULL = no swap cost              */
+    float          evict_cost;   /* seconds added at an evicted slot             */
+} qlm_problem;
+
+/* A batch of candidate plans, slot-major ("structure of arrays" over plans):
+ * entry (s, p) of perm is perm[s * plan_stride + p].  Consecutive plans are
+ * contiguous, so a wavefront reading one slot of 64 plans reads 256 bytes.    */
+typedef struct qlm_plans {
+    int64_t n_plans;             /* P >= 0                                      */
+    int64_t plan_stride;         /* elements between slot rows, >= P            */
+    const int32_t  *perm;        /* [G][stride]: group at slot s of plan p; each
+                                    plan's column is a permutation of 0..G-1   */
+    const int32_t  *qoff;        /* [I+1][stride]: queue g holds slots
+                                    [qoff[g], qoff[g+1]); 0 = qoff[0] <= ... <=
+                                    qoff[I] = G; empty queues allowed           */
+    const uint32_t *evict_bits;  /* [ceil(G/32)][stride]: slot s is evicted when
+                                    bit s%32 of word s/32 is set; NULL = none   */
+} qlm_plans;
+
+/* Per-slot outputs for plans [plan_begin, plan_begin + plan_count), each array
+ * [G][plan_count] slot-major (entry (s, q) at s * plan_count + q, where plan
+ * p = plan_begin + q); any of the three pointers may be NULL.                */
+typedef struct qlm_detail {
+    int64_t plan_begin, plan_count;
+    float *wait_mean;            /* E[W], seconds                                */
+    float *wait_sd;              /* SD[W], seconds                               */
+    float *prob;                 /* P(W > slo)                                   */
+} qlm_detail;
+
+/*
+ * Scores every plan (Secs. 6-7, the model above).
+ *   score   [P] out: score_p = expected requests missing their SLO
+ *   penalty [P] out or NULL: sum of (E[W] - slo) (Eq. penalty)
+ *   detail  NULL or per-slot outputs for a plan range (must lie in [0, P))
+ * Accuracy: per slot |dP| <= 1e-5 and E[W], SD[W] within 1e-5 relative of the
+ * double-precision definition; |d score_p| <= 1e-5 * (total requests).  The
+ * result is bit-for-bit reproducible for the same inputs.
+ */
+int qlm_rwt_score(const qlm_problem *problem, const qlm_plans *plans, double *score,
+                  double *penalty, const qlm_detail *detail, qlm_stream stream);
+
+/*
+ * Exact (double precision) scores of selected plans: plan_index[k] (device
+ * array of n, each in [0, P)) -> score[k] (device).  Every step is the
+ * definition above in double precision, summed in queue order then position
+ * order, with IEEE division and square root and the device erfc.
+ */
+int qlm_rwt_score_exact(const qlm_problem *problem, const qlm_plans *plans,
+                        const int64_t *plan_index, int64_t n, double *score,
+                        qlm_stream stream);
+
+/* Bytes of device workspace qlm_best_plan needs for n_plans plans (>= 256). */
+size_t qlm_best_plan_workspace_bytes(const qlm_problem *problem, int64_t n_plans);
+
+/*
+ * The plan the scheduler should pick (Sec. 7, objective; the scoring above in
+ * place of the LP): argmin over p of the exact score, the lowest index on ties.
+ * Screens every plan with the qlm_rwt_score arithmetic, then re-scores exactly
+ * every plan that can still be the minimum given the screening error bound.
+ *   ws          device workspace of at least qlm_best_plan_workspace_bytes,
+ *               256-byte aligned; its contents are scratch
+ *   best_index  [1] device out: index of the best plan (-1 when P = 0)
+ *   best_score  [1] device out: its exact score (+inf when P = 0)
+ */
+int qlm_best_plan(const qlm_problem *problem, const qlm_plans *plans, void *ws,
+                  size_t ws_bytes, int64_t *best_index, double *best_score,
+                  qlm_stream stream);
+
+/*
+ * Checks plan structure (Eq. slot_assignment): qoff starts at 0, ends at G and
+ * never decreases; perm is a permutation of 0..G-1; no eviction bit is set
+ * beyond slot G-1.
+ *   n_invalid   [1] device out: number of malformed plans
+ *   plan_status [P] device out or NULL: 0 ok, 1 bad qoff, 2 bad perm, 4 bad
+ *               eviction bits (bitwise or)
+ */
+int qlm_validate_plans(const qlm_problem *problem, const qlm_plans *plans,
+                       int64_t *n_invalid, int32_t *plan_status, qlm_stream stream);
+
+/*
+ * Checks the tables: 0 <= n < 2^24, var >= 0, models in [0, M), classes in
+ * [0, C), throughputs finite and > 0, inst_model0 in [-1, M).
+ *   n_invalid   [1] device out: number of bad entries
+ */
+int qlm_validate_problem(const qlm_problem *problem, int64_t *n_invalid,
+                         qlm_stream stream);
+
+/* Largest G the scoring kernels accept for these M, C, I (on-chip budget). */
+int32_t qlm_max_groups(int32_t n_models, int32_t n_classes, int32_t n_instances,
+                       int32_t with_eviction);
+
+/* Text of a status code; the last error's detail for this host thread. */
+const char *qlm_status_string(int status);
+const char *qlm_last_error(void);
+
+/*
+ * Optional launch timing for benchmarks: when enabled, the scoring kernel of
+ * every qlm_rwt_score / qlm_best_plan call is bracketed by HIP events on the
+ * call's stream.  qlm_timing_read waits for the recorded events and returns
+ * the number of scoring launches and their summed duration in milliseconds
+ * since the last reset, then resets.
+ */
+int qlm_timing_enable(int on);
+int qlm_timing_read(int64_t *launches, double *total_ms);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* QLM_H */

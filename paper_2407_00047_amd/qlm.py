@@ -1,0 +1,255 @@
+"""Python binding of libqlm (include/qlm.h): argument marshalling only.
+
+Every step of the scoring path runs in the HIP kernels of ``csrc/qlm.hip``;
+PyTorch supplies device memory and the current stream.  The binding refuses to
+run when the library is not built (there is no fallback of any kind).
+
+Function names follow the C interface: ``rwt_score``, ``rwt_score_exact``,
+``best_plan`` (with ``best_plan_workspace_bytes``), ``validate_plans``,
+``validate_problem``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libqlm.so")
+_lock = threading.Lock()
+_lib = None
+
+QLM_OK, QLM_ERR_ARG, QLM_ERR_CAPACITY, QLM_ERR_WORKSPACE, QLM_ERR_HIP = range(5)
+
+
+class QlmError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__("qlm status %d: %s" % (status, message))
+        self.status = status
+
+
+class Problem(ctypes.Structure):
+    _fields_ = [("n_groups", ctypes.c_int32), ("n_instances", ctypes.c_int32),
+                ("n_models", ctypes.c_int32), ("n_classes", ctypes.c_int32),
+                ("grp_count", ctypes.c_void_p), ("grp_mu", ctypes.c_void_p),
+                ("grp_var", ctypes.c_void_p), ("grp_model", ctypes.c_void_p),
+                ("grp_slo", ctypes.c_void_p), ("inst_tput", ctypes.c_void_p),
+                ("inst_class", ctypes.c_void_p), ("inst_model0", ctypes.c_void_p),
+                ("swap_cost", ctypes.c_void_p), ("evict_cost", ctypes.c_float)]
+
+
+class Plans(ctypes.Structure):
+    _fields_ = [("n_plans", ctypes.c_int64), ("plan_stride", ctypes.c_int64),
+                ("perm", ctypes.c_void_p), ("qoff", ctypes.c_void_p),
+                ("evict_bits", ctypes.c_void_p)]
+
+
+class Detail(ctypes.Structure):
+    _fields_ = [("plan_begin", ctypes.c_int64), ("plan_count", ctypes.c_int64),
+                ("wait_mean", ctypes.c_void_p), ("wait_sd", ctypes.c_void_p),
+                ("prob", ctypes.c_void_p)]
+
+
+def library():
+    """The loaded libqlm; raises when it has not been built."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                raise RuntimeError("libqlm.so is not built (run __graft_entry__.build() or "
+                                   "python -m paper_2407_00047_amd.build)")
+            lib = ctypes.CDLL(LIB_PATH)
+            P, PL, D = ctypes.POINTER(Problem), ctypes.POINTER(Plans), ctypes.POINTER(Detail)
+            vp, i64 = ctypes.c_void_p, ctypes.c_int64
+            lib.qlm_rwt_score.argtypes = [P, PL, vp, vp, D, vp]
+            lib.qlm_rwt_score_exact.argtypes = [P, PL, vp, i64, vp, vp]
+            lib.qlm_best_plan_workspace_bytes.argtypes = [P, i64]
+            lib.qlm_best_plan_workspace_bytes.restype = ctypes.c_size_t
+            lib.qlm_best_plan.argtypes = [P, PL, vp, ctypes.c_size_t, vp, vp, vp]
+            lib.qlm_validate_plans.argtypes = [P, PL, vp, vp, vp]
+            lib.qlm_validate_problem.argtypes = [P, vp, vp]
+            lib.qlm_max_groups.argtypes = [ctypes.c_int32] * 4
+            lib.qlm_max_groups.restype = ctypes.c_int32
+            lib.qlm_status_string.argtypes = [ctypes.c_int]
+            lib.qlm_status_string.restype = ctypes.c_char_p
+            lib.qlm_last_error.restype = ctypes.c_char_p
+            lib.qlm_timing_enable.argtypes = [ctypes.c_int]
+            lib.qlm_timing_read.argtypes = [ctypes.POINTER(ctypes.c_int64),
+                                            ctypes.POINTER(ctypes.c_double)]
+            for name in ("qlm_rwt_score", "qlm_rwt_score_exact", "qlm_best_plan",
+                         "qlm_validate_plans", "qlm_validate_problem", "qlm_timing_enable",
+                         "qlm_timing_read"):
+                getattr(lib, name).restype = ctypes.c_int
+            _lib = lib
+    return _lib
+
+
+def _check(rc: int):
+    if rc != QLM_OK:
+        lib = library()
+        raise QlmError(rc, lib.qlm_last_error().decode())
+
+
+def _stream(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+class DeviceProblem:
+    """Problem tables in device memory (torch tensors) plus the C struct."""
+
+    def __init__(self, problem, device="cuda"):
+        import torch
+
+        def dev(x, dt):
+            if x is None:
+                return None
+            return torch.as_tensor(np.ascontiguousarray(x)).to(device=device, dtype=dt)
+
+        self.n_groups = int(problem["n_groups"])
+        self.n_instances = int(problem["n_instances"])
+        self.n_models = int(problem["n_models"])
+        self.n_classes = int(problem["n_classes"])
+        self.grp_count = dev(problem["grp_count"], torch.int32)
+        self.grp_mu = dev(problem["grp_mu"], torch.float32)
+        self.grp_var = dev(problem["grp_var"], torch.float32)
+        self.grp_model = dev(problem["grp_model"], torch.int32)
+        self.grp_slo = dev(problem["grp_slo"], torch.float32)
+        self.inst_tput = dev(problem["inst_tput"], torch.float32)
+        self.inst_class = dev(problem["inst_class"], torch.int32)
+        self.inst_model0 = dev(problem.get("inst_model0"), torch.int32)
+        self.swap_cost = dev(problem.get("swap_cost"), torch.float32)
+        self.evict_cost = float(problem.get("evict_cost", 0.0))
+        self.total_requests = int(np.asarray(problem["grp_count"], np.int64).sum())
+        self.struct = Problem(self.n_groups, self.n_instances, self.n_models, self.n_classes,
+                              _ptr(self.grp_count), _ptr(self.grp_mu), _ptr(self.grp_var),
+                              _ptr(self.grp_model), _ptr(self.grp_slo), _ptr(self.inst_tput),
+                              _ptr(self.inst_class), _ptr(self.inst_model0),
+                              _ptr(self.swap_cost), self.evict_cost)
+
+
+class DevicePlans:
+    """A slot-major plan batch in device memory plus the C struct.  ``perm`` is
+    [G, stride] int32, ``qoff`` [I+1, stride] int32, ``evict_bits``
+    [ceil(G/32), stride] int32 (bit patterns) or None."""
+
+    def __init__(self, perm, qoff, evict_bits=None, n_plans=None):
+        self.perm = perm
+        self.qoff = qoff
+        self.evict_bits = evict_bits
+        stride = int(perm.shape[1])
+        self.n_plans = stride if n_plans is None else int(n_plans)
+        self.struct = Plans(self.n_plans, stride, _ptr(perm), _ptr(qoff), _ptr(evict_bits))
+
+    @classmethod
+    def from_host(cls, plans, device="cuda"):
+        import torch
+        perm = torch.from_numpy(np.ascontiguousarray(plans["perm"])).to(device)
+        qoff = torch.from_numpy(np.ascontiguousarray(plans["qoff"])).to(device)
+        ev = plans.get("evict_bits")
+        if ev is not None:
+            ev = torch.from_numpy(np.ascontiguousarray(ev).view(np.int32)).to(device)
+        return cls(perm, qoff, ev, plans.get("n_plans"))
+
+
+def rwt_score(problem: DeviceProblem, plans: DevicePlans, penalty: bool = False,
+              detail: tuple[int, int] | None = None, stream=None, out=None):
+    """Screening scores (and optionally penalties and per-slot detail for plans
+    [begin, begin+count)).  Returns dict of device tensors."""
+    import torch
+    dev = plans.perm.device
+    P = plans.n_plans
+    score = out if out is not None else torch.empty(P, dtype=torch.float64, device=dev)
+    pen = torch.empty(P, dtype=torch.float64, device=dev) if penalty else None
+    det = None
+    res = {"score": score, "penalty": pen}
+    if detail is not None:
+        b, c = detail
+        G = problem.n_groups
+        wm = torch.full((G, c), float("nan"), dtype=torch.float32, device=dev)
+        ws = torch.full((G, c), float("nan"), dtype=torch.float32, device=dev)
+        pr = torch.full((G, c), float("nan"), dtype=torch.float32, device=dev)
+        det = Detail(b, c, _ptr(wm), _ptr(ws), _ptr(pr))
+        res.update(wait_mean=wm, wait_sd=ws, prob=pr)
+    _check(library().qlm_rwt_score(ctypes.byref(problem.struct), ctypes.byref(plans.struct),
+                                   _ptr(score), _ptr(pen),
+                                   ctypes.byref(det) if det is not None else None,
+                                   _stream(stream)))
+    return res
+
+
+def rwt_score_exact(problem: DeviceProblem, plans: DevicePlans, plan_index, stream=None):
+    import torch
+    idx = torch.as_tensor(plan_index, dtype=torch.int64).to(plans.perm.device)
+    out = torch.empty(idx.numel(), dtype=torch.float64, device=plans.perm.device)
+    _check(library().qlm_rwt_score_exact(ctypes.byref(problem.struct), ctypes.byref(plans.struct),
+                                         _ptr(idx), idx.numel(), _ptr(out), _stream(stream)))
+    return out
+
+
+def best_plan_workspace_bytes(problem: DeviceProblem, n_plans: int) -> int:
+    return int(library().qlm_best_plan_workspace_bytes(ctypes.byref(problem.struct), n_plans))
+
+
+def workspace(problem: DeviceProblem, n_plans: int, device="cuda"):
+    import torch
+    nbytes = best_plan_workspace_bytes(problem, n_plans)
+    return torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+
+def best_plan(problem: DeviceProblem, plans: DevicePlans, ws=None, stream=None, out=None):
+    """(best_index, best_score) as device tensors of shape [1]."""
+    import torch
+    dev = plans.perm.device
+    if ws is None:
+        ws = workspace(problem, plans.n_plans, dev)
+    if out is None:
+        bi = torch.empty(1, dtype=torch.int64, device=dev)
+        bs = torch.empty(1, dtype=torch.float64, device=dev)
+    else:
+        bi, bs = out
+    _check(library().qlm_best_plan(ctypes.byref(problem.struct), ctypes.byref(plans.struct),
+                                   _ptr(ws), ws.numel(), _ptr(bi), _ptr(bs), _stream(stream)))
+    return bi, bs
+
+
+def validate_plans(problem: DeviceProblem, plans: DevicePlans, stream=None):
+    """(n_invalid tensor [1], per-plan status tensor [P])."""
+    import torch
+    dev = plans.perm.device
+    n = torch.empty(1, dtype=torch.int64, device=dev)
+    st = torch.empty(max(plans.n_plans, 1), dtype=torch.int32, device=dev)
+    _check(library().qlm_validate_plans(ctypes.byref(problem.struct), ctypes.byref(plans.struct),
+                                        _ptr(n), _ptr(st), _stream(stream)))
+    return n, st[:plans.n_plans]
+
+
+def validate_problem(problem: DeviceProblem, stream=None):
+    import torch
+    n = torch.empty(1, dtype=torch.int64, device=problem.grp_count.device)
+    _check(library().qlm_validate_problem(ctypes.byref(problem.struct), _ptr(n), _stream(stream)))
+    return n
+
+
+def max_groups(n_models: int, n_classes: int, n_instances: int, with_eviction: bool) -> int:
+    return int(library().qlm_max_groups(n_models, n_classes, n_instances, int(with_eviction)))
+
+
+def timing_enable(on: bool = True):
+    _check(library().qlm_timing_enable(int(on)))
+
+
+def timing_read():
+    """(number of scoring launches, total milliseconds) since the last read."""
+    n = ctypes.c_int64(0)
+    ms = ctypes.c_double(0.0)
+    _check(library().qlm_timing_read(ctypes.byref(n), ctypes.byref(ms)))
+    return int(n.value), float(ms.value)

@@ -1,0 +1,98 @@
+"""The C interface without a GPU: the library loads, exports every function
+include/qlm.h declares, and its host-side argument checks reject bad calls
+before anything reaches the device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "qlm.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"\b(qlm_[a-z0-9_]+)\s*\(", text)
+    return sorted(set(names))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2407_00047_amd import qlm
+    return qlm.library()
+
+
+def test_header_declares_entry_points():
+    names = declared_functions()
+    for must in ("qlm_rwt_score", "qlm_best_plan", "qlm_best_plan_workspace_bytes",
+                 "qlm_rwt_score_exact", "qlm_validate_plans", "qlm_validate_problem",
+                 "qlm_status_string", "qlm_last_error"):
+        assert must in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    missing = [n for n in declared_functions() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_status_strings(lib):
+    from paper_2407_00047_amd import qlm
+    for code in range(5):
+        assert lib.qlm_status_string(code)
+    assert lib.qlm_status_string(99) == b"unknown status"
+    assert qlm.QLM_ERR_CAPACITY == 2
+
+
+def _problem(qlm, G=4, I=1, M=1, C=1):
+    # pointers are never dereferenced by the host-side checks that fail first
+    fake = 0x1000
+    return qlm.Problem(G, I, M, C, fake, fake, fake, fake, fake, fake, fake, None, None, 0.0)
+
+
+def test_argument_errors_before_launch(lib):
+    from paper_2407_00047_amd import qlm
+    pr = _problem(qlm)
+    pl = qlm.Plans(4, 4, 0x1000, 0x1000, None)
+    P, PL = ctypes.byref, ctypes.byref
+    assert lib.qlm_rwt_score(None, PL(pl), 0x1000, None, None, None) == qlm.QLM_ERR_ARG
+    assert b"NULL" in lib.qlm_last_error()
+    assert lib.qlm_rwt_score(P(pr), None, 0x1000, None, None, None) == qlm.QLM_ERR_ARG
+    assert lib.qlm_rwt_score(P(pr), PL(pl), None, None, None, None) == qlm.QLM_ERR_ARG
+    bad = _problem(qlm, G=0)
+    assert lib.qlm_rwt_score(P(bad), PL(pl), 0x1000, None, None, None) == qlm.QLM_ERR_ARG
+    bad = _problem(qlm, M=256)
+    assert lib.qlm_rwt_score(P(bad), PL(pl), 0x1000, None, None, None) == qlm.QLM_ERR_ARG
+    stride_bad = qlm.Plans(8, 4, 0x1000, 0x1000, None)
+    assert lib.qlm_rwt_score(P(pr), PL(stride_bad), 0x1000, None, None, None) == qlm.QLM_ERR_ARG
+    neg = qlm.Plans(-1, 4, 0x1000, 0x1000, None)
+    assert lib.qlm_rwt_score(P(pr), PL(neg), 0x1000, None, None, None) == qlm.QLM_ERR_ARG
+    det = qlm.Detail(2, 5, 0x1000, None, None)                 # beyond n_plans
+    assert lib.qlm_rwt_score(P(pr), PL(pl), 0x1000, None, ctypes.byref(det), None) == qlm.QLM_ERR_ARG
+    # zero plans: nothing to do, no device work
+    zero = qlm.Plans(0, 1, None, None, None)
+    assert lib.qlm_rwt_score(P(pr), PL(zero), None, None, None, None) == qlm.QLM_OK
+
+
+def test_workspace_checks(lib):
+    from paper_2407_00047_amd import qlm
+    pr = _problem(qlm)
+    pl = qlm.Plans(1000, 1000, 0x1000, 0x1000, None)
+    need = lib.qlm_best_plan_workspace_bytes(ctypes.byref(pr), 1000)
+    assert need >= 8 * 1000
+    assert lib.qlm_best_plan_workspace_bytes(ctypes.byref(pr), 2000) > need
+    P = ctypes.byref
+    assert lib.qlm_best_plan(P(pr), P(pl), None, need, 0x1000, 0x1000, None) == qlm.QLM_ERR_WORKSPACE
+    assert lib.qlm_best_plan(P(pr), P(pl), 0x1010, need, 0x1000, 0x1000, None) == qlm.QLM_ERR_WORKSPACE
+    assert lib.qlm_best_plan(P(pr), P(pl), 0x1000, need - 1, 0x1000, 0x1000, None) == qlm.QLM_ERR_WORKSPACE
+    assert lib.qlm_best_plan(P(pr), P(pl), 0x1000, need, None, 0x1000, None) == qlm.QLM_ERR_ARG
+
+
+def test_max_groups(lib):
+    # LDS budget 160 KiB: 16-byte group records plus cost and instance tables
+    mg = lib.qlm_max_groups(8, 4, 64, 1)
+    assert 9000 < mg < 10240
+    assert lib.qlm_max_groups(1, 1, 1, 0) > mg
+    assert lib.qlm_max_groups(0, 1, 1, 0) == 0
+    assert lib.qlm_max_groups(256, 1, 1, 0) == 0
