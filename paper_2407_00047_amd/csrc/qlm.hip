@@ -30,6 +30,7 @@
 #include <cstring>
 #include <mutex>
 #include <string>
+#include <type_traits>
 #include <vector>
 
 #include "qlm.h"
@@ -62,11 +63,10 @@ constexpr float kQ6 = (float)(kRoot16of2 * 0.0000053830);
 
 struct ScoreArgs {
     int32_t G, I, M, C;
-    int32_t row_shift;        // log2(bytes per LUT row)
-    uint32_t ev_off;          // bytes between the plain and the evicted LUT halves
-    int32_t lut_words;        // words of LUT staged in LDS
-    uint32_t lds_lut;         // byte offset of the LUT in LDS
-    uint32_t lds_inst;        // byte offset of the instance table in LDS
+    int32_t row_shift;        // log2(bytes per cost-table row)
+    int32_t ev_shift;         // log2(bytes from a cost entry to its evicted twin)
+    uint32_t lut_align;       // alignment of the cost table in LDS (power of two)
+    uint32_t lut_region;      // bytes of the cost table (both halves)
     const int32_t *grp_count;
     const float *grp_mu, *grp_var, *grp_slo;
     const int32_t *grp_model;
@@ -86,15 +86,44 @@ struct ScoreArgs {
 
 __device__ inline int clampi(int v, int lo, int hi) { return v < lo ? lo : (v > hi ? hi : v); }
 
-// Stage the group records, the cost table and the instance table into LDS.
-//   group i   : {mu, var, slo, (n << 8) | model}, entry G is an all-zero record
-//   LUT word  : ((ev * C + c) * (M + 1) + row) * Mp + col, row M = no model loaded;
-//               value = swap(c, row -> col) (0 on the diagonal and in row M)
-//               + ev * evict_cost
-//   instance  : theta (double), class row base, head row (bytes into the LUT)
-__device__ void stage_tables(const ScoreArgs &a, unsigned char *lds)
+// LDS layout of the scoring kernel (byte addresses; `base` = the dynamic LDS
+// pointer):
+//   group table   base, 16 (G + 1) bytes: group i -> {mu, var, slo, (n << 8) | model};
+//                 entry G is an all-zero record (clamped out-of-range ids land there)
+//   cost table    at `lut`, the first multiple of lut_align after the group table:
+//                 byte (row << row_shift) | (col << 2) holds the seconds of swapping
+//                 from model `row` to model `col` on class c, where row = c (M + 1) +
+//                 previous model (previous model = M: none loaded; diagonal 0).  The
+//                 twin at + (1 << ev_shift) adds the eviction cost.  Both shifts are
+//                 powers of two and the table is aligned, so the address of a slot's
+//                 cost is a bitwise OR of its row, its column and its eviction bit.
+//   instances     theta (double) [I], class row base [I], head row [I] (LDS addresses)
+//   scratch       8 doubles for workgroup reductions
+struct Lds {
+    uint32_t grp, lut, inst, red;
+};
+
+__device__ inline Lds lds_layout(const ScoreArgs &a, const unsigned char *base)
 {
-    uint4 *grp = reinterpret_cast<uint4 *>(lds);
+    Lds l;
+    l.grp = (uint32_t)(uintptr_t)base;
+    l.lut = (l.grp + 16u * (uint32_t)(a.G + 1) + a.lut_align - 1u) & ~(a.lut_align - 1u);
+    l.inst = l.lut + a.lut_region;
+    l.red = l.inst + 16u * (uint32_t)a.I;
+    return l;
+}
+
+// Generic pointer to LDS byte address `addr` (an address-space cast from the
+// local address space, so loads and stores through it stay ds_* instructions).
+template <typename T>
+__device__ inline T *lds_ptr(uint32_t addr)
+{
+    return (T *)((__attribute__((address_space(3))) T *)(uintptr_t)addr);
+}
+
+__device__ void stage_tables(const ScoreArgs &a, const Lds &l)
+{
+    uint4 *grp = lds_ptr<uint4>(l.grp);
     for (int i = threadIdx.x; i <= a.G; i += blockDim.x) {
         uint4 r = make_uint4(0u, 0u, 0u, 0u);
         if (i < a.G) {
@@ -107,30 +136,34 @@ __device__ void stage_tables(const ScoreArgs &a, unsigned char *lds)
         }
         grp[i] = r;
     }
-    float *lut = reinterpret_cast<float *>(lds + a.lds_lut);
+    float *lut = lds_ptr<float>(l.lut);
     const int Mp = 1 << (a.row_shift - 2);
     const int rows = a.M + 1;
-    const int half = a.C * rows * Mp;
-    for (int w = threadIdx.x; w < a.lut_words; w += blockDim.x) {
-        const int ev = w >= half;
-        const int k = ev ? w - half : w;
-        const int col = k % Mp;
-        const int row = (k / Mp) % rows;
-        const int c = k / (Mp * rows);
+    const int half_words = a.C * rows * Mp;
+    const int twin_words = 1 << (a.ev_shift - 2);
+    const int words = (int)(a.lut_region / 4u);
+    for (int w = threadIdx.x; w < words; w += blockDim.x) {
+        const int ev = w >= twin_words;
+        const int k = ev ? w - twin_words : w;
         float v = 0.0f;
-        if (a.swap_cost && row < a.M && col < a.M && row != col)
-            v = a.swap_cost[((int64_t)c * a.M + row) * a.M + col];
-        if (ev) v += a.evict_cost;
+        if (k < half_words) {
+            const int col = k % Mp;
+            const int row = (k / Mp) % rows;
+            const int c = k / (Mp * rows);
+            if (a.swap_cost && row < a.M && col < a.M && row != col)
+                v = a.swap_cost[((int64_t)c * a.M + row) * a.M + col];
+            if (ev) v += a.evict_cost;
+        }
         lut[w] = v;
     }
-    double *theta = reinterpret_cast<double *>(lds + a.lds_inst);
+    double *theta = lds_ptr<double>(l.inst);
     uint32_t *cbase = reinterpret_cast<uint32_t *>(theta + a.I);
     uint32_t *head = cbase + a.I;
     for (int g = threadIdx.x; g < a.I; g += blockDim.x) {
         const int c = clampi(a.inst_class[g], 0, a.C - 1);
         const int m0 = a.inst_model0 ? clampi(a.inst_model0[g], -1, a.M - 1) : -1;
         theta[g] = (double)a.inst_tput[g];
-        const uint32_t cb = (uint32_t)(c * rows) << a.row_shift;
+        const uint32_t cb = l.lut + ((uint32_t)(c * rows) << a.row_shift);
         cbase[g] = cb;
         head[g] = cb + ((uint32_t)(m0 >= 0 ? m0 : a.M) << a.row_shift);
     }
@@ -145,11 +178,12 @@ __device__ inline double wave_min(double v)
 // Screening score of every plan.  One lane = one plan; the slots of a plan are
 // walked in order, so every prefix sum is a running sum.
 template <bool EVICT, bool PEN, bool DETAIL>
-__global__ __launch_bounds__(kScoreThreads) void k_score(ScoreArgs a)
+__global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_score(ScoreArgs a)
 {
     extern __shared__ __align__(16) unsigned char lds[];
-    stage_tables(a, lds);
-    __shared__ double red[kScoreThreads / kWave];
+    const Lds L = lds_layout(a, lds);
+    stage_tables(a, L);
+    double *red = lds_ptr<double>(L.red);
     if (a.wg_nsum && blockIdx.x == 0) {
         double t = 0.0;
         for (int i = threadIdx.x; i < a.G; i += blockDim.x)
@@ -165,72 +199,282 @@ __global__ __launch_bounds__(kScoreThreads) void k_score(ScoreArgs a)
     }
     __syncthreads();
 
-    const uint4 *grp = reinterpret_cast<const uint4 *>(lds);
-    const unsigned char *lut = lds + a.lds_lut;
-    const double *s_theta = reinterpret_cast<const double *>(lds + a.lds_inst);
+    const double *s_theta = lds_ptr<double>(L.inst);
     const uint32_t *s_cbase = reinterpret_cast<const uint32_t *>(s_theta + a.I);
     const uint32_t *s_head = s_cbase + a.I;
+    const uint32_t grp0 = L.grp;
 
     const int lane = threadIdx.x & (kWave - 1);
-    const int wave = threadIdx.x / kWave;
+    // the wavefront index is uniform within a wavefront; say so, so that the
+    // tile, its row addresses and the buffer resources live in scalar registers
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int wpb = blockDim.x / kWave;
     const int64_t ntiles = (a.P + kWave - 1) / kWave;
     const int G = a.G;
+    const int I1 = a.I - 1;
     const int64_t ld = a.ld;
+    const int ev_shift = a.ev_shift;
+    const int row_shift = a.row_shift;
     double lane_min = INFINITY;
 
     for (int64_t t = (int64_t)blockIdx.x * wpb + wave; t < ntiles; t += (int64_t)gridDim.x * wpb) {
-        const int64_t p_raw = t * kWave + lane;
-        const bool live = p_raw < a.P;
-        const int64_t p = live ? p_raw : a.P - 1;
-        const int32_t *col = a.perm + p;
-        const int32_t *qcol = a.qoff + p;
-        const uint32_t *ecol = EVICT ? a.evict + p : nullptr;
+        const int64_t tb = t * kWave;               // first plan of the tile (uniform)
+        const bool live = tb + lane < a.P;
+        const int lp = live ? lane : (int)(a.P - 1 - tb);   // lane's plan, relative to tb
+        const uint32_t lpb = (uint32_t)lp * 4u;     // its byte offset within a row
+        const int32_t *qrow = a.qoff + tb;
+        const int64_t p = tb + lp;
         const bool det = DETAIL && live && p >= a.d_begin && p < a.d_begin + a.d_count;
         const int64_t dq = p - a.d_begin;
+        // Row r of a slot-major array, lane's column: a plain global load (used
+        // for the queue offsets, once per block), and buffer loads from a
+        // resource based at a block's first row (group ids, eviction words),
+        // whose row offset is a scalar operand: no per-load vector arithmetic.
+        const int64_t ld4 = ld * 4;
+        auto at = [&](const void *base, int row) __attribute__((always_inline)) {
+            const unsigned char *rp =
+                reinterpret_cast<const unsigned char *>(base) + (int64_t)row * ld4 + tb * 4;
+            return *reinterpret_cast<const uint32_t *>(rp + lpb);
+        };
+        auto rsrc_at = [&](const void *base, int row) __attribute__((always_inline)) {
+            const unsigned char *rp =
+                reinterpret_cast<const unsigned char *>(base) + (int64_t)row * ld4 + tb * 4;
+            return __builtin_amdgcn_make_buffer_rsrc((void *)rp, (short)0, 0x7FFFFFFF, 0x00020000);
+        };
+        auto ld_rel = [&](__amdgpu_buffer_rsrc_t r, int rel_row) __attribute__((always_inline)) {
+            return (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(r, (int)lpb, rel_row * (int)ld4, 0);
+        };
 
-        double Y = 0.0;        // tokens ahead + theta * (swap and eviction seconds)
+        double Y = 0.0;        // tokens ahead + theta * (swap and eviction seconds so far)
         double V = 0.0;        // variance of the tokens ahead
         double S = 0.0;        // sum of n * P
         double PE = 0.0;       // sum of (E[W] - slo)
         double theta = 1.0, inv_theta = 1.0;
-        uint32_t cbase = 0, rowb = 0, evw = 0;
+        uint32_t cbase = 0, rowb = 0;
+        // Queue bookkeeping.  g is the queue of the current slot and nb the slot
+        // where the next queue starts.  Parameters of upcoming queues reach a
+        // queue head through a two-stage prefetch, so that a head never waits for
+        // a load younger than one block (32 slots):
+        //   f1, f2   queues q0+1 and q0+2, q0 = g at the start of the previous
+        //            block; loaded at that start
+        //   x_*      the next queue's parameters for the current block, chosen at
+        //            its start from f1 or f2 by how many queues the previous block
+        //            entered (two or more: not available, `need`)
+        struct QP {
+            int nb;               // end boundary of the queue
+            double theta;
+            uint32_t cbase, head;
+        };
         int g = -1, nb = 0;
+        QP x{0, 1.0, 0u, 0u}, f1{0, 1.0, 0u, 0u}, f2{0, 1.0, 0u, 0u};
+        int q0 = -1;
+        bool need = true;             // x belongs to a queue already entered
 
-        for (int s = 0; s < G; ++s) {
-            if (s == nb && g < a.I - 1) {   // queue head: move to the queue owning slot s
-                do {
-                    ++g;
-                    nb = qcol[(int64_t)(g + 1) * ld];
-                } while (nb <= s && g < a.I - 1);
-                theta = s_theta[g];
-                inv_theta = 1.0 / theta;
-                cbase = s_cbase[g];
-                rowb = s_head[g];
-                Y = 0.0;
-                V = 0.0;
+        // Issued for every lane, never under a per-lane condition (clamped
+        // index), so that the compiler counts the outstanding loads exactly.
+        auto load_qp = [&](int h) __attribute__((always_inline)) {
+            h = min(max(h, 0), I1);
+            QP q;
+            q.nb = (int)at(a.qoff, h + 1);
+            q.theta = s_theta[h];
+            q.cbase = s_cbase[h];
+            q.head = s_head[h];
+            return q;
+        };
+        auto block_start = [&]() __attribute__((always_inline)) {
+            const int c = g - q0;     // queues entered since the previous start
+            x.nb = c == 0 ? f1.nb : f2.nb;
+            x.theta = c == 0 ? f1.theta : f2.theta;
+            x.cbase = c == 0 ? f1.cbase : f2.cbase;
+            x.head = c == 0 ? f1.head : f2.head;
+            need = c > 1;
+            q0 = g;
+            __builtin_amdgcn_sched_barrier(0);        // select before the reload
+            f1 = load_qp(g + 1);
+            f2 = load_qp(g + 2);
+        };
+
+        // Enter the queue that owns slot s (called when s == nb).  The common
+        // case uses x_*, fetched at the start of the block; a second head in one
+        // block, or an empty queue, loads what it needs and waits for it on the
+        // spot, so that no wait on the common path covers a load issued after
+        // the block's group-id refills.
+        auto enter = [&](int s) __attribute__((always_inline)) {
+            int e_nb;
+            double e_theta;
+            uint32_t e_cbase, e_head;
+            if (!need) {
+                e_nb = x.nb;
+                e_theta = x.theta;
+                e_cbase = x.cbase;
+                e_head = x.head;
+            } else {
+                const int h = g + 1;
+                e_nb = (int)at(a.qoff, h + 1);
+                e_theta = s_theta[h];
+                e_cbase = s_cbase[h];
+                e_head = s_head[h];
+                __builtin_amdgcn_s_waitcnt(0x0070);   // vmcnt(0) lgkmcnt(0)
             }
-            const uint32_t i = min((uint32_t)col[(int64_t)s * ld], (uint32_t)G);
-            const uint4 r = grp[i];
+            ++g;
+            nb = e_nb;
+            theta = e_theta;
+            cbase = e_cbase;
+            rowb = e_head;
+            need = true;
+            while (nb <= s && g < I1) {   // empty queues: skip them (rare)
+                const int h = g + 1;
+                nb = (int)at(a.qoff, h + 1);
+                theta = s_theta[h];
+                cbase = s_cbase[h];
+                rowb = s_head[h];
+                __builtin_amdgcn_s_waitcnt(0x0070);
+                ++g;
+            }
+            if (g >= I1) nb = INT_MAX;    // last queue: no further head
+            inv_theta = 1.0 / theta;
+            Y = 0.0;
+            V = 0.0;
+        };
+
+        // Software pipeline over the slots of the plan:
+        //   ring[32]  group ids of the next 32 slots (global loads, 32 slots ahead)
+        //   rec[4]    LDS records of slots s..s+3 (gathered 4 slots ahead)
+        //   cost      swap/eviction seconds of slot s (looked up one slot ahead)
+        // Slot s: (A) waits and variances with its cost, (B) resolve whether s+1
+        // starts a queue and look up the cost of s+1, (C) the normal tail of s,
+        // which overlaps that lookup.
+        constexpr int D = 3;          // records gathered D slots ahead
+        int32_t ring[32];
+        uint4 rec[4];                 // rec[s % 4] holds slot s's record
+        __amdgpu_buffer_rsrc_t rp = rsrc_at(a.perm, 0);
+#pragma unroll
+        for (int k = 0; k < 32; ++k) ring[k] = (int32_t)ld_rel(rp, min(k, G - 1));
+        auto gather = [&](int32_t gid) __attribute__((always_inline)) {
+            return *lds_ptr<const uint4>((min((uint32_t)gid, (uint32_t)G) << 4) + grp0);
+        };
+        // prologue: records of slots 0..D-1 (their ring entries refilled with
+        // slots 32..32+D-1), the head of slot 0 and its cost
+#pragma unroll
+        for (int k = 0; k < D; ++k) {
+            rec[k] = gather(ring[k]);
+            ring[k] = (int32_t)ld_rel(rp, min(k + 32, G - 1));
+        }
+        rec[D] = rec[0];
+        uint32_t ev = EVICT ? ld_rel(rsrc_at(a.evict, 0), 0) : 0u;   // word of the block
+        uint32_t ev_nx = 0u;                              // word of the next block
+        // prefetch relative to q0 = -1 (queues 0 and 1), issued before enter(0),
+        // whose full wait leaves no load of the prologue pending at the loop
+        q0 = -1;
+        f1 = load_qp(0);
+        f2 = load_qp(1);
+        enter(0);                     // need: loads and waits (once per tile)
+        float cost = *lds_ptr<const float>(rowb | ((rec[0].w & 0xFFu) << 2) |
+                                           (EVICT ? (ev & 1u) << ev_shift : 0u));
+
+        // Full 32-slot blocks: no per-slot guard, so every refill is unconditional
+        // and the compiler's counting of outstanding loads stays exact.
+        const int G32 = G & ~31;
+        const int Gx = __builtin_amdgcn_readfirstlane(G);
+        for (int sb = 0; sb < G32; sb += 32) {
+            block_start();
+            if (EVICT) ev_nx = ld_rel(rsrc_at(a.evict, min((sb >> 5) + 1, (G - 1) >> 5)), 0);
+            rp = rsrc_at(a.perm, sb);
+#pragma unroll
+            for (int k = 0; k < 32; ++k) {
+                const int s = sb + k;
+                // ring entry of slot s+D: turned into its LDS address, then refilled
+                // with slot s+D+32 (unconditionally: rows past the end clamp to the
+                // last row), so both share one register and every wait on the ring
+                // counts loads exactly
+                const int j = (k + D) & 31;
+                rec[(k + D) & 3] = gather(ring[j]);   // record of slot s+D
+                __builtin_amdgcn_sched_barrier(0);    // consume before the refill
+                ring[j] = (int32_t)ld_rel(rp, min(s + D + 32, G - 1) - sb);
+                // always true here; an opaque bound keeps each slot a region of its
+                // own, which keeps the record pipeline in fixed registers
+                if (s >= Gx) continue;
+                const uint4 r = rec[k & 3];
+                const float mu = __uint_as_float(r.x);
+                const float var = __uint_as_float(r.y);
+                const float slo = __uint_as_float(r.z);
+                const uint32_t m = r.w & 0xFFu;
+                const double n = (double)(r.w >> 8);
+
+                // (A) waits of slot s
+                Y = fma((double)cost, theta, Y);                  // its swap / eviction
+                const double num = fma((double)slo, theta, -Y);   // theta (slo - E[W])
+                const float rs = __builtin_amdgcn_rsqf((float)V); // 1/sqrt(V); inf if V = 0
+                // |z|; a zero margin with zero variance gives +inf (no violation)
+                const float x = fmaxf(fabsf((float)num), 1e-38f) * rs;
+                if (PEN) PE = fma(-num, inv_theta, PE);
+                if (DETAIL && det) {
+                    const int64_t o = (int64_t)s * a.d_count + dq;
+                    if (a.d_mean) a.d_mean[o] = (float)(Y * inv_theta);
+                    if (a.d_sd) a.d_sd[o] = (float)(sqrt(V) * inv_theta);
+                }
+                Y = fma(n, (double)mu, Y);
+                V = fma(n, (double)var, V);
+                rowb = cbase + (m << row_shift);
+
+                // (B) queue head at s+1?  Then the cost of slot s+1
+                if (s + 1 == nb) enter(s + 1);
+                {
+                    const uint32_t m1 = rec[(k + 1) & 3].w & 0xFFu;
+                    uint32_t idx = rowb | (m1 << 2);
+                    if (EVICT) {
+                        const uint32_t w = k == 31 ? ev_nx : ev;
+                        idx |= __builtin_amdgcn_ubfe(w, (uint32_t)((k + 1) & 31), 1u) << ev_shift;
+                    }
+                    cost = *lds_ptr<const float>(idx);
+                }
+
+                // (C) normal tail of slot s (A&S 26.2.19)
+                float y = fmaf(x, kQ6, kQ5);
+                y = fmaf(y, x, kQ4);
+                y = fmaf(y, x, kQ3);
+                y = fmaf(y, x, kQ2);
+                y = fmaf(y, x, kQ1);
+                y = fmaf(y, x, kQ0);
+                y = y * y;
+                y = y * y;
+                y = y * y;
+                y = y * y;
+                const float q = __builtin_amdgcn_rcpf(y);         // Q(|z|)
+                const float prob = num < 0.0 ? 1.0f - q : q;
+                S = fma(n, (double)prob, S);
+                if (DETAIL && det && a.d_prob) a.d_prob[(int64_t)s * a.d_count + dq] = prob;
+            }
+            if (EVICT) ev = ev_nx;
+        }
+        // Remaining G % 32 slots, one at a time (plain loads; small G only).  The
+        // pipeline has already resolved the head and the cost of slot G32.
+        for (int s = G32; s < G; ++s) {
+            const uint4 r = gather((int32_t)at(a.perm, s));
+            const uint32_t m = r.w & 0xFFu;
+            if (s > G32) {
+                if (s == nb) enter(s);
+                uint32_t idx = rowb | (m << 2);
+                if (EVICT) idx |= __builtin_amdgcn_ubfe(ev, (uint32_t)(s & 31), 1u) << ev_shift;
+                cost = *lds_ptr<const float>(idx);
+            }
             const float mu = __uint_as_float(r.x);
             const float var = __uint_as_float(r.y);
             const float slo = __uint_as_float(r.z);
-            const uint32_t m = r.w & 0xFFu;
             const double n = (double)(r.w >> 8);
-            uint32_t idx = rowb + (m << 2);
-            if (EVICT) {
-                if ((s & 31) == 0) evw = ecol[(int64_t)(s >> 5) * ld];
-                idx += ((evw >> (s & 31)) & 1u) * a.ev_off;
-            }
-            const float cost = *reinterpret_cast<const float *>(lut + idx);
-            rowb = cbase + (m << a.row_shift);
-
-            Y = fma((double)cost, theta, Y);                  // this slot's swap / eviction
-            const double num = fma((double)slo, theta, -Y);   // theta * (slo - E[W])
-            const float v32 = (float)V;
-            const float rs = __builtin_amdgcn_rsqf(v32);      // 1/sqrt(V); +inf when V = 0
-            // |z|; a zero margin with zero variance gives +inf (no violation)
+            Y = fma((double)cost, theta, Y);
+            const double num = fma((double)slo, theta, -Y);
+            const float rs = __builtin_amdgcn_rsqf((float)V);
             const float x = fmaxf(fabsf((float)num), 1e-38f) * rs;
+            if (PEN) PE = fma(-num, inv_theta, PE);
+            if (DETAIL && det) {
+                const int64_t o = (int64_t)s * a.d_count + dq;
+                if (a.d_mean) a.d_mean[o] = (float)(Y * inv_theta);
+                if (a.d_sd) a.d_sd[o] = (float)(sqrt(V) * inv_theta);
+            }
+            Y = fma(n, (double)mu, Y);
+            V = fma(n, (double)var, V);
+            rowb = cbase + (m << row_shift);
             float y = fmaf(x, kQ6, kQ5);
             y = fmaf(y, x, kQ4);
             y = fmaf(y, x, kQ3);
@@ -241,18 +485,10 @@ __global__ __launch_bounds__(kScoreThreads) void k_score(ScoreArgs a)
             y = y * y;
             y = y * y;
             y = y * y;
-            const float q = __builtin_amdgcn_rcpf(y);         // Q(|z|)
+            const float q = __builtin_amdgcn_rcpf(y);
             const float prob = num < 0.0 ? 1.0f - q : q;
             S = fma(n, (double)prob, S);
-            if (PEN) PE = fma(-num, inv_theta, PE);
-            if (DETAIL && det) {
-                const int64_t o = (int64_t)s * a.d_count + dq;
-                if (a.d_mean) a.d_mean[o] = (float)(Y * inv_theta);
-                if (a.d_sd) a.d_sd[o] = (float)(sqrt(V) * inv_theta);
-                if (a.d_prob) a.d_prob[o] = prob;
-            }
-            Y = fma(n, (double)mu, Y);
-            V = fma(n, (double)var, V);
+            if (DETAIL && det && a.d_prob) a.d_prob[(int64_t)s * a.d_count + dq] = prob;
         }
         if (live) {
             a.score[p] = S;
@@ -584,31 +820,35 @@ int hip_fail(hipError_t e, const char *what)
 constexpr size_t kLdsLimit = 160 * 1024;   // gfx950 LDS per workgroup
 
 struct Geometry {
-    int row_shift;
-    uint32_t ev_off;
-    int lut_words;
-    uint32_t lds_lut, lds_inst;
+    int row_shift, ev_shift;
+    uint32_t lut_align, lut_region;
     size_t lds_bytes;
 };
 
-int ceil_log2(int v)
+int ceil_log2(uint32_t v)
 {
     int s = 0;
-    while ((1 << s) < v) ++s;
+    while ((1u << s) < v) ++s;
     return s;
 }
 
 Geometry geometry(int G, int I, int M, int C, bool evict)
 {
     Geometry g;
-    const int Mp = 1 << ceil_log2(M);
+    const uint32_t Mp = 1u << ceil_log2((uint32_t)M);
     g.row_shift = ceil_log2(Mp) + 2;
-    const int half = C * (M + 1) * Mp;
-    g.ev_off = (uint32_t)half * 4u;
-    g.lut_words = evict ? 2 * half : half;
-    g.lds_lut = (uint32_t)(16 * (size_t)(G + 1));
-    g.lds_inst = g.lds_lut + (uint32_t)((4 * (size_t)g.lut_words + 15) / 16 * 16);
-    g.lds_bytes = g.lds_inst + 16 * (size_t)I;
+    const uint32_t half = (uint32_t)(C * (M + 1)) << g.row_shift;   // bytes of one half
+    g.ev_shift = ceil_log2(half < 16u ? 16u : half);
+    if (evict) {
+        g.lut_region = 2u << g.ev_shift;
+        g.lut_align = 2u << g.ev_shift;
+    } else {
+        g.lut_region = (half + 15u) / 16u * 16u;
+        g.lut_align = (1u << g.row_shift) < 16u ? 16u : (1u << g.row_shift);
+    }
+    // group table, worst-case alignment padding, cost table, instances, scratch
+    g.lds_bytes = 16 * (size_t)(G + 1) + (g.lut_align - 1) + g.lut_region + 16 * (size_t)I + 64;
+    g.lds_bytes = (g.lds_bytes + 15) / 16 * 16;
     return g;
 }
 
@@ -645,10 +885,9 @@ ScoreArgs score_args(const qlm_problem *pr, const qlm_plans *pl, const Geometry 
     a.M = pr->n_models;
     a.C = pr->n_classes;
     a.row_shift = geo.row_shift;
-    a.ev_off = geo.ev_off;
-    a.lut_words = geo.lut_words;
-    a.lds_lut = geo.lds_lut;
-    a.lds_inst = geo.lds_inst;
+    a.ev_shift = geo.ev_shift;
+    a.lut_align = geo.lut_align;
+    a.lut_region = geo.lut_region;
     a.grp_count = pr->grp_count;
     a.grp_mu = pr->grp_mu;
     a.grp_var = pr->grp_var;
