@@ -566,9 +566,10 @@ __device__ double exact_queue(const ExactArgs &a, int64_t p, int g)
     return sc;
 }
 
-// Exact score of plan p by a whole workgroup: threads take queues, thread 0
-// adds the per-queue sums in queue order.
-__device__ double exact_plan(const ExactArgs &a, int64_t p, double *part)
+// Exact score of plan p by a whole workgroup, serial per queue (threads take
+// queues, thread 0 adds the per-queue sums in queue order).  Used when the
+// slot-parallel form below does not fit in LDS.
+__device__ double exact_plan_serial(const ExactArgs &a, int64_t p, double *part)
 {
     double total = 0.0;
     for (int g0 = 0; g0 < a.I; g0 += blockDim.x) {
@@ -583,17 +584,153 @@ __device__ double exact_plan(const ExactArgs &a, int64_t p, double *part)
     }
     return total;   // valid in thread 0
 }
+
+// The same exact score, slot-parallel, with the same arithmetic and the same
+// summation order.  Inputs are first gathered into LDS by independent loads
+// (no chains of dependent global loads):
+//   0. every thread takes slots: a = n mu and b = n var (exact products) and
+//      the model of the slot's group; the eviction words; the swap table
+//   1. per queue (one thread each), the running sums in position order give
+//      every slot's E[W] = A/Theta + K and SD = sqrt(V)/Theta (in place of a, b)
+//   2. every thread takes slots: P and the term n P (in place of E[W])
+//   3. per queue, the terms are added in position order; thread 0 adds the
+//      queue sums in queue order.
+struct ExactLds {
+    double *x, *y;            // [G] each
+    uint32_t *evw;            // [ceil(G/32)]
+    float *swap;              // [C M M] or null (then read from global memory)
+    unsigned char *mdl;       // [G]
+};
+
+__device__ double exact_plan(const ExactArgs &a, int64_t p, const ExactLds &L, double *part)
+{
+    const int G = a.G;
+    const int W = (G + 31) >> 5;
+    const int64_t ld = a.ld;
+    // 0. gather (8 independent slots per thread per step)
+    for (int s0 = threadIdx.x; s0 < G; s0 += 8 * blockDim.x) {
+        int i[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int s = s0 + u * blockDim.x;
+            i[u] = s < G ? (int)min((uint32_t)a.perm[(int64_t)s * ld + p], (uint32_t)(G - 1)) : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int s = s0 + u * blockDim.x;
+            if (s < G) {
+                const double n = (double)(uint32_t)clampi(a.grp_count[i[u]], 0, (int)kCountMask);
+                L.x[s] = n * (double)a.grp_mu[i[u]];
+                L.y[s] = n * (double)a.grp_var[i[u]];
+                L.mdl[s] = (unsigned char)clampi(a.grp_model[i[u]], 0, a.M - 1);
+            }
+        }
+    }
+    for (int w = threadIdx.x; w < W; w += blockDim.x)
+        L.evw[w] = a.evict ? a.evict[(int64_t)w * ld + p] : 0u;
+    if (L.swap && a.swap_cost)
+        for (int k = threadIdx.x; k < a.C * a.M * a.M; k += blockDim.x) L.swap[k] = a.swap_cost[k];
+    __syncthreads();
+    // 1. running sums per queue
+    for (int g = threadIdx.x; g < a.I; g += blockDim.x) {
+        const int32_t b = clampi(a.qoff[(int64_t)g * ld + p], 0, G);
+        const int32_t e = clampi(a.qoff[(int64_t)(g + 1) * ld + p], b, G);
+        const double theta = (double)a.inst_tput[g];
+        const int cls = clampi(a.inst_class[g], 0, a.C - 1);
+        int m_prev = a.inst_model0 ? clampi(a.inst_model0[g], -1, a.M - 1) : -1;
+        const double ecost = (double)a.evict_cost;
+        double A = 0.0, V = 0.0, K = 0.0;
+        for (int s = b; s < e; ++s) {
+            const int m = L.mdl[s];
+            if (m_prev >= 0 && m_prev != m && a.swap_cost) {
+                const int64_t k = ((int64_t)cls * a.M + m_prev) * a.M + m;
+                K += (double)(L.swap ? L.swap[k] : a.swap_cost[k]);
+            }
+            if ((L.evw[s >> 5] >> (s & 31)) & 1u) K += ecost;
+            const double xa = L.x[s], yb = L.y[s];
+            L.x[s] = A / theta + K;            // E[W]
+            L.y[s] = sqrt(V) / theta;          // SD[W]
+            A += xa;
+            V += yb;
+            m_prev = m;
+        }
+    }
+    __syncthreads();
+    // 2. probability and term per slot
+    for (int s0 = threadIdx.x; s0 < G; s0 += 8 * blockDim.x) {
+        int i[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int s = s0 + u * blockDim.x;
+            i[u] = s < G ? (int)min((uint32_t)a.perm[(int64_t)s * ld + p], (uint32_t)(G - 1)) : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int s = s0 + u * blockDim.x;
+            if (s < G) {
+                const double n = (double)(uint32_t)clampi(a.grp_count[i[u]], 0, (int)kCountMask);
+                const double slo = (double)a.grp_slo[i[u]];
+                const double EW = L.x[s], SD = L.y[s];
+                double P;
+                if (SD > 0.0)
+                    P = 0.5 * erfc((slo - EW) / (SD * 1.4142135623730951));
+                else
+                    P = (EW > slo) ? 1.0 : 0.0;
+                L.x[s] = n * P;
+            }
+        }
+    }
+    __syncthreads();
+    // 3. sums per queue, then over queues
+    double total = 0.0;
+    for (int g0 = 0; g0 < a.I; g0 += blockDim.x) {
+        const int g = g0 + threadIdx.x;
+        if (g < a.I) {
+            const int32_t b = clampi(a.qoff[(int64_t)g * ld + p], 0, G);
+            const int32_t e = clampi(a.qoff[(int64_t)(g + 1) * ld + p], b, G);
+            double sc = 0.0;
+            for (int s = b; s < e; ++s) sc += L.x[s];
+            part[threadIdx.x] = sc;
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            const int n = min((int)blockDim.x, a.I - g0);
+            for (int k = 0; k < n; ++k) total += part[k];
+        }
+        __syncthreads();
+    }
+    return total;   // valid in thread 0
+}
+
+// Exact score with whichever form fits: `big` = 1 the kernel got the LDS of
+// the staged form, 2 the same plus room for the swap table.
+__device__ double exact_score(const ExactArgs &a, int64_t p, unsigned char *dyn, int big,
+                              double *part)
+{
+    if (big) {
+        ExactLds L;
+        L.x = reinterpret_cast<double *>(dyn);
+        L.y = L.x + a.G;
+        L.evw = reinterpret_cast<uint32_t *>(L.y + a.G);
+        float *after = reinterpret_cast<float *>(L.evw + ((a.G + 31) >> 5));
+        L.swap = big == 2 ? after : nullptr;
+        L.mdl = reinterpret_cast<unsigned char *>(after + (big == 2 ? a.C * a.M * a.M : 0));
+        return exact_plan(a, p, L, part);
+    }
+    return exact_plan_serial(a, p, part);
+}
 #pragma clang fp contract(on)
 
 __global__ __launch_bounds__(kRefineThreads) void k_exact(ExactArgs a, const int64_t *idx,
-                                                          int64_t n, double *out)
+                                                          int64_t n, double *out, int big)
 {
+    extern __shared__ __align__(16) unsigned char dyn[];
     __shared__ double part[kRefineThreads];
     for (int64_t k = blockIdx.x; k < n; k += gridDim.x) {
         int64_t p = idx[k];
         const bool ok = p >= 0 && p < a.P;
         p = ok ? p : 0;
-        const double s = exact_plan(a, p, part);
+        const double s = exact_score(a, p, dyn, big, part);
         if (threadIdx.x == 0) out[k] = ok ? s : NAN;
     }
 }
@@ -650,8 +787,10 @@ __device__ double block_min(double v, double *ls)
 __global__ __launch_bounds__(kRefineThreads) void k_refine(ExactArgs a, const double *fast,
                                                            const double *wg_min, int n_wg,
                                                            const double *nsum,
-                                                           double *best_s, int64_t *best_i)
+                                                           double *best_s, int64_t *best_i,
+                                                           int big)
 {
+    extern __shared__ __align__(16) unsigned char dyn[];
     __shared__ double part[kRefineThreads];
     __shared__ double ls[kRefineThreads / kWave];
     __shared__ int64_t li[kRefineThreads / kWave];
@@ -687,7 +826,7 @@ __global__ __launch_bounds__(kRefineThreads) void k_refine(ExactArgs a, const do
             for (int w = 0; w < (int)(blockDim.x / kWave); ++w) q = li[w] < q ? li[w] : q;
             __syncthreads();
             if (q == INT64_MAX) break;
-            const double e = exact_plan(a, q, part);
+            const double e = exact_score(a, q, dyn, big, part);
             if (threadIdx.x == 0 && e < bs) {     // ascending index: the first minimum wins
                 bs = e;
                 bi = q;
@@ -1062,6 +1201,33 @@ int launch_score(const qlm_problem *pr, const qlm_plans *pl, double *score, doub
     return QLM_OK;
 }
 
+// Dynamic LDS of the exact re-score: the staged form when it fits (with the
+// swap table when that fits too), else none (serial form).
+int exact_lds(const void *kernel, const qlm_problem *pr, size_t *lds, int *big)
+{
+    const size_t G = (size_t)pr->n_groups;
+    const size_t base = 16 * G + 4 * ((G + 31) / 32) + G;
+    const size_t swap = 4 * (size_t)pr->n_classes * pr->n_models * pr->n_models;
+    const size_t static_lds = 8 * (size_t)kRefineThreads + 256;
+    size_t want = (base + 15) / 16 * 16;
+    int kind = 1;
+    if (pr->swap_cost && ((base + swap + 15) / 16 * 16) + static_lds <= kLdsLimit) {
+        want = (base + swap + 15) / 16 * 16;
+        kind = 2;
+    }
+    if (want + static_lds <= kLdsLimit) {
+        hipError_t e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                           (int)want);
+        if (e != hipSuccess) return hip_fail(e, "hipFuncSetAttribute");
+        *lds = want;
+        *big = kind;
+    } else {
+        *lds = 0;
+        *big = 0;
+    }
+    return QLM_OK;
+}
+
 size_t align256(size_t v) { return (v + 255) / 256 * 256; }
 
 }  // namespace
@@ -1102,8 +1268,12 @@ int qlm_rwt_score_exact(const qlm_problem *problem, const qlm_plans *plans,
     if (plans->n_plans == 0) return fail(QLM_ERR_ARG, "no plans to index");
     ExactArgs a = exact_args(problem, plans);
     const int grid = (int)(n < 65535 ? n : 65535);
-    hipLaunchKernelGGL(k_exact, dim3(grid), dim3(kRefineThreads), 0, (hipStream_t)stream, a,
-                       plan_index, n, score);
+    size_t lds = 0;
+    int big = 0;
+    rc = exact_lds((const void *)k_exact, problem, &lds, &big);
+    if (rc) return rc;
+    hipLaunchKernelGGL(k_exact, dim3(grid), dim3(kRefineThreads), lds, (hipStream_t)stream, a,
+                       plan_index, n, score, big);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "k_exact launch");
     return QLM_OK;
@@ -1153,8 +1323,12 @@ int qlm_best_plan(const qlm_problem *problem, const qlm_plans *plans, void *ws, 
     ExactArgs a = exact_args(problem, plans);
     int rgrid = (int)((P + kRefineThreads - 1) / kRefineThreads);
     if (rgrid > kRefineBlocks) rgrid = kRefineBlocks;
-    hipLaunchKernelGGL(k_refine, dim3(rgrid), dim3(kRefineThreads), 0, stream, a, fast, wg_min,
-                       grid, nsum, bs, bi);
+    size_t lds = 0;
+    int big = 0;
+    rc = exact_lds((const void *)k_refine, problem, &lds, &big);
+    if (rc) return rc;
+    hipLaunchKernelGGL(k_refine, dim3(rgrid), dim3(kRefineThreads), lds, stream, a, fast, wg_min,
+                       grid, nsum, bs, bi, big);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "k_refine launch");
     hipLaunchKernelGGL(k_final, dim3(1), dim3(256), 0, stream, bs, bi, rgrid, best_index,
