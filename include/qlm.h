@@ -39,7 +39,7 @@
  *  - Plan contents are not checked by the scoring calls (use
  *    qlm_validate_plans): a malformed plan yields an unspecified score for that
  *    plan, never an out-of-bounds access.  Group ids are clamped to [0, G],
- *    models and classes to their ranges, counts to 24 bits.
+ *    models and classes to their ranges, counts to 21 bits.
  */
 #ifndef QLM_H
 #define QLM_H
@@ -69,7 +69,7 @@ typedef struct qlm_problem {
     int32_t n_instances;         /* I >= 1 (one virtual queue per instance)      */
     int32_t n_models;            /* M, 1 <= M <= 255                             */
     int32_t n_classes;           /* C >= 1 hardware classes                      */
-    const int32_t *grp_count;    /* [G] requests per group, 0 <= n < 2^24        */
+    const int32_t *grp_count;    /* [G] requests per group, 0 <= n < 2^21        */
     const float   *grp_mu;       /* [G] mean output tokens per request           */
     const float   *grp_var;      /* [G] variance of output tokens, >= 0          */
     const int32_t *grp_model;    /* [G] model of the group, in [0, M)            */
@@ -116,7 +116,10 @@ typedef struct qlm_detail {
  *   detail  NULL or per-slot outputs for a plan range (must lie in [0, P))
  * Accuracy: per slot |dP| <= 1e-5 and E[W], SD[W] within 1e-5 relative of the
  * double-precision definition; |d score_p| <= 1e-5 * (total requests).  The
- * result is bit-for-bit reproducible for the same inputs.
+ * result is bit-for-bit reproducible for the same inputs.  Method: waits in
+ * double precision, variances in single precision per block of 32 positions
+ * on top of a double sum, and P from a 1024-cell linear table of the normal
+ * tail over |z| <= 6 (error below 2.2e-6; beyond, P is exactly 0 or 1).
  */
 int qlm_rwt_score(const qlm_problem *problem, const qlm_plans *plans, double *score,
                   double *penalty, const qlm_detail *detail, qlm_stream stream);
@@ -160,7 +163,7 @@ int qlm_validate_plans(const qlm_problem *problem, const qlm_plans *plans,
                        int64_t *n_invalid, int32_t *plan_status, qlm_stream stream);
 
 /*
- * Checks the tables: 0 <= n < 2^24, var >= 0, models in [0, M), classes in
+ * Checks the tables: 0 <= n < 2^21, var >= 0, models in [0, M), classes in
  * [0, C), throughputs finite and > 0, inst_model0 in [-1, M).
  *   n_invalid   [1] device out: number of bad entries
  */

@@ -12,9 +12,11 @@
 //             running sums in registers (no scan), reset at each queue head.
 //             Group statistics, the swap/eviction cost table and the instance
 //             table are staged once per workgroup in LDS; each slot gathers its
-//             group's 16-byte record with one ds_read_b128.  The violation
-//             probability is a fused single-precision normal tail (Abramowitz &
-//             Stegun 26.2.19); waits and variances accumulate in double.
+//             group's 16-byte record with one ds_read_b128.  Waits accumulate in
+//             double, variances in single precision within blocks of 32 slots on
+//             top of a double sum; the violation probability is read from a
+//             linear-cell table of the normal tail in LDS.  LDS reads are
+//             software-pipelined one slot ahead of their use.
 //   k_refine  exact double-precision re-score (same definition as the oracle,
 //             summed per queue then over queues) of every plan whose screened
 //             score is within the screening error bound of the minimum.
@@ -42,31 +44,40 @@ constexpr int kScoreThreads = 512;      // 8 wavefronts per workgroup
 constexpr int kRefineThreads = 256;
 constexpr int kMaxScoreBlocks = 4096;
 constexpr int kRefineBlocks = 1024;
-constexpr uint32_t kCountMask = 0xFFFFFFu;  // counts are 24-bit in the LDS record
+// Request counts share the 32-bit record word with the model's cost-table
+// column (bits 3..10), so they are 21-bit.
+constexpr uint32_t kCountMask = (1u << 21) - 1u;
+constexpr int kCountShift = 11;
+constexpr uint32_t kColMask = 0x7F8u;     // model * 8: byte column of the cost table
 
 // Screening error bound per slot of the single-precision probability: the
-// approximation error of A&S 26.2.19 (1.5e-7) plus single-precision rounding of
-// the standardised margin and of the evaluation (below 4e-6), with margin.
+// tabulated tail (below 2.2e-6), single-precision rounding of the standardised
+// margin and of the block-wise variance (below 1e-6), with margin.
 constexpr double kEpsP = 8e-6;
 
-// A&S 26.2.19: Q(x) ~ 1/2 (1 + d1 x + ... + d6 x^6)^-16 for x >= 0, |error| <
-// 1.5e-7.  Every coefficient is scaled by 2^(1/16) so that the sixteenth power
-// carries the factor 2 and Q = 1 / y^16.
-constexpr double kRoot16of2 = 1.0442737824274138403;
-constexpr float kQ0 = (float)(kRoot16of2);
-constexpr float kQ1 = (float)(kRoot16of2 * 0.0498673470);
-constexpr float kQ2 = (float)(kRoot16of2 * 0.0211410061);
-constexpr float kQ3 = (float)(kRoot16of2 * 0.0032776263);
-constexpr float kQ4 = (float)(kRoot16of2 * 0.0000380036);
-constexpr float kQ5 = (float)(kRoot16of2 * 0.0000488906);
-constexpr float kQ6 = (float)(kRoot16of2 * 0.0000053830);
+// Normal upper tail Q(z) = erfc(z / sqrt 2) / 2 as a table of 1024 linear
+// cells over z in [-6, 6] (beyond, Q is within 1e-9 of 0 or 1).  The kernel
+// forms t = 1536 - (1024 / 12) z in single precision and clamps it to
+// [1024, 2048): there every float has exponent 10, so the ten leading mantissa
+// bits are the cell and fract(t) the position in it.  Cell k holds the line
+// (c0, c1) that best fits Q over its width (the chord, moved by half its
+// largest deviation); the two end cells are the constants 0 and 1.
+constexpr int kTailCells = 1024;
+constexpr double kTailZ = 6.0;
+constexpr double kTailScale = kTailCells / (2.0 * kTailZ);          // cells per unit z
+constexpr float kTailMid = 1536.0f;
+constexpr float kTailLo = 1024.0f;
+constexpr float kTailHi = 2047.9998779296875f;                     // 2048 - 2^-13
+constexpr uint32_t kTailCellBits = 0x7FE000u;                      // mantissa bits 22..13
+// Variances are staged multiplied by 1 / kTailScale^2, so that the reciprocal
+// square root of the running sum is already in cells per unit of margin.
+constexpr double kVarScale = 1.0 / (kTailScale * kTailScale);
 
 struct ScoreArgs {
     int32_t G, I, M, C;
-    int32_t row_shift;        // log2(bytes per cost-table row)
+    int32_t col_shift;        // log2(entries per cost-table row)
     int32_t ev_shift;         // log2(bytes from a cost entry to its evicted twin)
-    uint32_t lut_align;       // alignment of the cost table in LDS (power of two)
-    uint32_t lut_region;      // bytes of the cost table (both halves)
+    uint32_t lut_bytes;       // bytes of the cost table (both halves), multiple of 16
     const int32_t *grp_count;
     const float *grp_mu, *grp_var, *grp_slo;
     const int32_t *grp_model;
@@ -86,29 +97,37 @@ struct ScoreArgs {
 
 __device__ inline int clampi(int v, int lo, int hi) { return v < lo ? lo : (v > hi ? hi : v); }
 
-// LDS layout of the scoring kernel (byte addresses; `base` = the dynamic LDS
-// pointer):
-//   group table   base, 16 (G + 1) bytes: group i -> {mu, var, slo, (n << 8) | model};
-//                 entry G is an all-zero record (clamped out-of-range ids land there)
-//   cost table    at `lut`, the first multiple of lut_align after the group table:
-//                 byte (row << row_shift) | (col << 2) holds the seconds of swapping
-//                 from model `row` to model `col` on class c, where row = c (M + 1) +
-//                 previous model (previous model = M: none loaded; diagonal 0).  The
-//                 twin at + (1 << ev_shift) adds the eviction cost.  Both shifts are
-//                 powers of two and the table is aligned, so the address of a slot's
-//                 cost is a bitwise OR of its row, its column and its eviction bit.
-//   instances     theta (double) [I], class row base [I], head row [I] (LDS addresses)
+// LDS of the scoring kernel.  The normal-tail table is a static array (8 KiB at
+// the start of LDS).  Dynamic part, byte addresses from `base`:
+//   group table   16 (G + 1) bytes: group i -> {mu, n var / kTailScale^2, slo,
+//                 (n << 11) | (model << 3)}; entry G is an all-zero record
+//                 (clamped out-of-range ids land there)
+//   cost table    lut_bytes of doubles.  Row r = c (M + 1) + previous model
+//                 (previous = M: none loaded) starts at byte r << (col_shift + 3);
+//                 its entry at + model * 8 holds the seconds of swapping to
+//                 `model` on class c (0 for the same model or none loaded).  The
+//                 twin at + (1 << ev_shift) adds the eviction cost.  A row offset is
+//                 the previous model's column offset shifted by col_shift.
+//   instances     16 bytes each: theta (double), the cost-table row base of its
+//                 class, the row of its head (initial model, or none)
 //   scratch       8 doubles for workgroup reductions
 struct Lds {
     uint32_t grp, lut, inst, red;
 };
 
+// LDS byte address of a pointer into LDS (a cast to the local address space:
+// no generic-pointer null check, so the address folds to a constant)
+__device__ inline uint32_t lds_addr(const void *p)
+{
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) unsigned char *)p;
+}
+
 __device__ inline Lds lds_layout(const ScoreArgs &a, const unsigned char *base)
 {
     Lds l;
-    l.grp = (uint32_t)(uintptr_t)base;
-    l.lut = (l.grp + 16u * (uint32_t)(a.G + 1) + a.lut_align - 1u) & ~(a.lut_align - 1u);
-    l.inst = l.lut + a.lut_region;
+    l.grp = lds_addr(base);
+    l.lut = l.grp + 16u * (uint32_t)(a.G + 1);
+    l.inst = l.lut + a.lut_bytes;
     l.red = l.inst + 16u * (uint32_t)a.I;
     return l;
 }
@@ -130,42 +149,72 @@ __device__ void stage_tables(const ScoreArgs &a, const Lds &l)
             const uint32_t n = (uint32_t)clampi(a.grp_count[i], 0, (int)kCountMask);
             const uint32_t m = (uint32_t)clampi(a.grp_model[i], 0, a.M - 1);
             r.x = __float_as_uint(a.grp_mu[i]);
-            r.y = __float_as_uint(a.grp_var[i]);
+            r.y = __float_as_uint((float)((double)n * (double)a.grp_var[i] * kVarScale));
             r.z = __float_as_uint(a.grp_slo[i]);
-            r.w = (n << 8) | m;
+            r.w = (n << kCountShift) | (m << 3);
         }
         grp[i] = r;
     }
-    float *lut = lds_ptr<float>(l.lut);
-    const int Mp = 1 << (a.row_shift - 2);
+    double *lut = lds_ptr<double>(l.lut);
+    const int Mp = 1 << a.col_shift;
     const int rows = a.M + 1;
-    const int half_words = a.C * rows * Mp;
-    const int twin_words = 1 << (a.ev_shift - 2);
-    const int words = (int)(a.lut_region / 4u);
-    for (int w = threadIdx.x; w < words; w += blockDim.x) {
-        const int ev = w >= twin_words;
-        const int k = ev ? w - twin_words : w;
-        float v = 0.0f;
-        if (k < half_words) {
+    const int half = a.C * rows * Mp;
+    const int twin = 1 << (a.ev_shift - 3);
+    const int entries = (int)(a.lut_bytes / 8u);
+    for (int w = threadIdx.x; w < entries; w += blockDim.x) {
+        const int ev = w >= twin;
+        const int k = ev ? w - twin : w;
+        double v = 0.0;
+        if (k < half) {
             const int col = k % Mp;
             const int row = (k / Mp) % rows;
             const int c = k / (Mp * rows);
             if (a.swap_cost && row < a.M && col < a.M && row != col)
-                v = a.swap_cost[((int64_t)c * a.M + row) * a.M + col];
-            if (ev) v += a.evict_cost;
+                v = (double)a.swap_cost[((int64_t)c * a.M + row) * a.M + col];
+            if (ev) v += (double)a.evict_cost;
         }
         lut[w] = v;
     }
-    double *theta = lds_ptr<double>(l.inst);
-    uint32_t *cbase = reinterpret_cast<uint32_t *>(theta + a.I);
-    uint32_t *head = cbase + a.I;
+    const uint32_t row_bytes = 8u << a.col_shift;
     for (int g = threadIdx.x; g < a.I; g += blockDim.x) {
         const int c = clampi(a.inst_class[g], 0, a.C - 1);
         const int m0 = a.inst_model0 ? clampi(a.inst_model0[g], -1, a.M - 1) : -1;
-        theta[g] = (double)a.inst_tput[g];
-        const uint32_t cb = l.lut + ((uint32_t)(c * rows) << a.row_shift);
-        cbase[g] = cb;
-        head[g] = cb + ((uint32_t)(m0 >= 0 ? m0 : a.M) << a.row_shift);
+        const uint32_t cb = l.lut + (uint32_t)(c * rows) * row_bytes;
+        const double th = (double)a.inst_tput[g];
+        uint4 r;
+        r.x = (uint32_t)__double_as_longlong(th);
+        r.y = (uint32_t)((uint64_t)__double_as_longlong(th) >> 32);
+        r.z = cb;
+        r.w = cb + (uint32_t)(m0 >= 0 ? m0 : a.M) * row_bytes;
+        lds_ptr<uint4>(l.inst)[g] = r;
+    }
+}
+
+// The normal-tail table: cell k covers t in [1024 + k, 1025 + k), i.e. z from
+// (512 - k) / kTailScale down to (511 - k) / kTailScale, and holds the line in
+// the position f = t - (1024 + k) that fits Q best (the chord, moved by half its
+// deviation at the middle of the cell).
+__device__ void stage_tail(float2 *tab)
+{
+    // a fixed trip count (the kernel runs kScoreThreads threads): no loop whose
+    // exit depends on the thread, after which uniform values would turn divergent
+    static_assert(kTailCells % kScoreThreads == 0, "tail cells per thread");
+#pragma unroll
+    for (int k0 = 0; k0 < kTailCells; k0 += kScoreThreads) {
+        const int k = k0 + (int)threadIdx.x;
+        const double r2 = 0.70710678118654752440;
+        const double p0 = 0.5 * erfc((512.0 - k) / kTailScale * r2);
+        const double p1 = 0.5 * erfc((511.0 - k) / kTailScale * r2);
+        const double pm = 0.5 * erfc((511.5 - k) / kTailScale * r2);
+        double c1 = p1 - p0;
+        double c0 = p0 + 0.5 * (pm - 0.5 * (p0 + p1));
+        // the end cells are flat at exactly 0 and 1 (their Q is within 2e-9 of it),
+        // so that clamped margins give exact zero and one terms
+        if (k == 0 || k == kTailCells - 1) {
+            c0 = k == 0 ? 0.0 : 1.0;
+            c1 = 0.0;
+        }
+        tab[k] = make_float2((float)c0, (float)c1);
     }
 }
 
@@ -176,13 +225,20 @@ __device__ inline double wave_min(double v)
 }
 
 // Screening score of every plan.  One lane = one plan; the slots of a plan are
-// walked in order, so every prefix sum is a running sum.
+// walked in order, so every prefix sum is a running sum.  Per slot: the
+// group's record (one LDS gather), the tokens ahead and the swap/eviction
+// seconds in double (Y = tokens + theta * seconds), the variance ahead in
+// single precision within a block of 32 slots on top of a double sum of the
+// earlier blocks, the standardised margin, and the violation probability from
+// the tail table.
 template <bool EVICT, bool PEN, bool DETAIL>
 __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_score(ScoreArgs a)
 {
+    __shared__ __align__(16) float2 s_tail[kTailCells];
     extern __shared__ __align__(16) unsigned char lds[];
     const Lds L = lds_layout(a, lds);
     stage_tables(a, L);
+    stage_tail(s_tail);
     double *red = lds_ptr<double>(L.red);
     if (a.wg_nsum && blockIdx.x == 0) {
         double t = 0.0;
@@ -199,10 +255,9 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
     }
     __syncthreads();
 
-    const double *s_theta = lds_ptr<double>(L.inst);
-    const uint32_t *s_cbase = reinterpret_cast<const uint32_t *>(s_theta + a.I);
-    const uint32_t *s_head = s_cbase + a.I;
     const uint32_t grp0 = L.grp;
+    const uint32_t inst0 = L.inst;
+    const uint32_t tail0 = lds_addr(s_tail);
 
     const int lane = threadIdx.x & (kWave - 1);
     // the wavefront index is uniform within a wavefront; say so, so that the
@@ -214,7 +269,7 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
     const int I1 = a.I - 1;
     const int64_t ld = a.ld;
     const int ev_shift = a.ev_shift;
-    const int row_shift = a.row_shift;
+    const int col_shift = a.col_shift;
     double lane_min = INFINITY;
 
     for (int64_t t = (int64_t)blockIdx.x * wpb + wave; t < ntiles; t += (int64_t)gridDim.x * wpb) {
@@ -222,14 +277,13 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
         const bool live = tb + lane < a.P;
         const int lp = live ? lane : (int)(a.P - 1 - tb);   // lane's plan, relative to tb
         const uint32_t lpb = (uint32_t)lp * 4u;     // its byte offset within a row
-        const int32_t *qrow = a.qoff + tb;
         const int64_t p = tb + lp;
         const bool det = DETAIL && live && p >= a.d_begin && p < a.d_begin + a.d_count;
         const int64_t dq = p - a.d_begin;
-        // Row r of a slot-major array, lane's column: a plain global load (used
-        // for the queue offsets, once per block), and buffer loads from a
-        // resource based at a block's first row (group ids, eviction words),
-        // whose row offset is a scalar operand: no per-load vector arithmetic.
+        // Row r of a slot-major array, lane's column: a plain global load (queue
+        // offsets, rare), and buffer loads from a resource based at a block's
+        // first row (group ids, eviction words), whose row offset is a scalar
+        // operand: no per-load vector arithmetic.
         const int64_t ld4 = ld * 4;
         auto at = [&](const void *base, int row) __attribute__((always_inline)) {
             const unsigned char *rp =
@@ -246,29 +300,31 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
         };
 
         double Y = 0.0;        // tokens ahead + theta * (swap and eviction seconds so far)
-        double V = 0.0;        // variance of the tokens ahead
+        double V = 0.0;        // scaled variance ahead, through the previous block
+        float vb = 0.0f;       // V rounded to single precision
+        float vblk = 0.0f;     // scaled variance ahead added within the current block
         double S = 0.0;        // sum of n * P
         double PE = 0.0;       // sum of (E[W] - slo)
         double theta = 1.0, inv_theta = 1.0;
-        uint32_t cbase = 0, rowb = 0;
+        uint32_t cbase = 0u;   // cost-table row base of the current queue's class
         // Queue bookkeeping.  g is the queue of the current slot and nb the slot
         // where the next queue starts.  Parameters of upcoming queues reach a
-        // queue head through a two-stage prefetch, so that a head never waits for
-        // a load younger than one block (32 slots):
-        //   f1, f2   queues q0+1 and q0+2, q0 = g at the start of the previous
-        //            block; loaded at that start
-        //   x_*      the next queue's parameters for the current block, chosen at
-        //            its start from f1 or f2 by how many queues the previous block
-        //            entered (two or more: not available, `need`)
+        // queue head through a prefetch at the start of every block of 32 slots:
+        //   f1, f2   queues q0+1 and q0+2, q0 = g at the start of the block
+        //   x        at the start of a block, the next queue's parameters from the
+        //            previous block's f1 or f2 (by how many queues that block
+        //            entered); `fast` marks lanes for which x is valid and the
+        //            queue not empty.  A block's first head uses x; a second one
+        //            uses this block's f2; anything else loads on the spot.
         struct QP {
-            int nb;               // end boundary of the queue
-            double theta;
+            int nb;               // end boundary of the queue (INT_MAX for the last)
+            double theta, inv;
             uint32_t cbase, head;
         };
-        int g = -1, nb = 0;
-        QP x{0, 1.0, 0u, 0u}, f1{0, 1.0, 0u, 0u}, f2{0, 1.0, 0u, 0u};
-        int q0 = -1;
-        bool need = true;             // x belongs to a queue already entered
+        int g = -1, nb = 0, q0 = -1;
+        int base = 0, nbr = 0;    // current block start, nb - base
+        QP x{0, 1.0, 1.0, 0u, 0u}, f1 = x, f2 = x;
+        bool fast = false;
 
         // Issued for every lane, never under a per-lane condition (clamped
         // index), so that the compiler counts the outstanding loads exactly.
@@ -276,9 +332,11 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
             h = min(max(h, 0), I1);
             QP q;
             q.nb = (int)at(a.qoff, h + 1);
-            q.theta = s_theta[h];
-            q.cbase = s_cbase[h];
-            q.head = s_head[h];
+            const uint4 r = *lds_ptr<const uint4>(inst0 + 16u * (uint32_t)h);
+            q.theta = __longlong_as_double((long long)(((uint64_t)r.y << 32) | r.x));
+            q.inv = 1.0;
+            q.cbase = r.z;
+            q.head = r.w;
             return q;
         };
         auto block_start = [&]() __attribute__((always_inline)) {
@@ -287,64 +345,78 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
             x.theta = c == 0 ? f1.theta : f2.theta;
             x.cbase = c == 0 ? f1.cbase : f2.cbase;
             x.head = c == 0 ? f1.head : f2.head;
-            need = c > 1;
+            if (g + 1 >= I1) x.nb = INT_MAX;
+            if (PEN || DETAIL) x.inv = 1.0 / x.theta;
+            fast = c <= 1 && g < I1 && x.nb > nb;
             q0 = g;
             __builtin_amdgcn_sched_barrier(0);        // select before the reload
             f1 = load_qp(g + 1);
             f2 = load_qp(g + 2);
         };
-
-        // Enter the queue that owns slot s (called when s == nb).  The common
-        // case uses x_*, fetched at the start of the block; a second head in one
-        // block, or an empty queue, loads what it needs and waits for it on the
-        // spot, so that no wait on the common path covers a load issued after
-        // the block's group-id refills.
-        auto enter = [&](int s) __attribute__((always_inline)) {
-            int e_nb;
-            double e_theta;
-            uint32_t e_cbase, e_head;
-            if (!need) {
-                e_nb = x.nb;
-                e_theta = x.theta;
-                e_cbase = x.cbase;
-                e_head = x.head;
+        // Enter queue g + 1 (or the first non-empty queue after it) at slot s,
+        // loading its parameters on the spot and waiting for them.
+        auto enter_slow = [&](int s, uint32_t &rowb) __attribute__((always_inline)) {
+            int h = g + 1;
+            int e_nb = (int)at(a.qoff, h + 1);
+            uint4 r = *lds_ptr<const uint4>(inst0 + 16u * (uint32_t)h);
+            __builtin_amdgcn_s_waitcnt(0x0070);   // vmcnt(0) lgkmcnt(0)
+            g = h;
+            // empty queues: skip them.  The loop runs while any lane needs it (a
+            // wavefront-uniform exit), the lanes that are done idle in it.
+            bool more = e_nb <= s && g < I1;
+            while (__builtin_amdgcn_ballot_w64(more)) {
+                if (more) {
+                    h = g + 1;
+                    e_nb = (int)at(a.qoff, h + 1);
+                    r = *lds_ptr<const uint4>(inst0 + 16u * (uint32_t)h);
+                    __builtin_amdgcn_s_waitcnt(0x0070);
+                    g = h;
+                    more = e_nb <= s && g < I1;
+                }
+            }
+            nb = g >= I1 ? INT_MAX : e_nb;
+            theta = __longlong_as_double((long long)(((uint64_t)r.y << 32) | r.x));
+            if (PEN || DETAIL) inv_theta = 1.0 / theta;
+            cbase = r.z;
+            rowb = r.w;
+        };
+        // Slot s is the head of the next queue: switch to it, reset the sums.
+        auto enter = [&](int s, uint32_t &rowb) __attribute__((always_inline)) {
+            if (fast) {
+                g += 1;
+                nb = x.nb;
+                theta = x.theta;
+                if (PEN || DETAIL) inv_theta = x.inv;
+                cbase = x.cbase;
+                rowb = x.head;
+                fast = false;
+            } else if (g == q0 + 1 && q0 + 2 <= I1 && (q0 + 2 >= I1 || f2.nb > s)) {
+                g = q0 + 2;
+                nb = g >= I1 ? INT_MAX : f2.nb;
+                theta = f2.theta;
+                if (PEN || DETAIL) inv_theta = 1.0 / theta;
+                cbase = f2.cbase;
+                rowb = f2.head;
             } else {
-                const int h = g + 1;
-                e_nb = (int)at(a.qoff, h + 1);
-                e_theta = s_theta[h];
-                e_cbase = s_cbase[h];
-                e_head = s_head[h];
-                __builtin_amdgcn_s_waitcnt(0x0070);   // vmcnt(0) lgkmcnt(0)
+                enter_slow(s, rowb);
             }
-            ++g;
-            nb = e_nb;
-            theta = e_theta;
-            cbase = e_cbase;
-            rowb = e_head;
-            need = true;
-            while (nb <= s && g < I1) {   // empty queues: skip them (rare)
-                const int h = g + 1;
-                nb = (int)at(a.qoff, h + 1);
-                theta = s_theta[h];
-                cbase = s_cbase[h];
-                rowb = s_head[h];
-                __builtin_amdgcn_s_waitcnt(0x0070);
-                ++g;
-            }
-            if (g >= I1) nb = INT_MAX;    // last queue: no further head
-            inv_theta = 1.0 / theta;
+            nbr = nb - base;
             Y = 0.0;
             V = 0.0;
+            vb = 0.0f;
+            vblk = 0.0f;
         };
 
         // Software pipeline over the slots of the plan:
         //   ring[32]  group ids of the next 32 slots (global loads, 32 slots ahead)
-        //   rec[4]    LDS records of slots s..s+3 (gathered 4 slots ahead)
-        //   cost      swap/eviction seconds of slot s (looked up one slot ahead)
-        // Slot s: (A) waits and variances with its cost, (B) resolve whether s+1
-        // starts a queue and look up the cost of s+1, (C) the normal tail of s,
-        // which overlaps that lookup.
-        constexpr int D = 3;          // records gathered D slots ahead
+        //   rec[4]    LDS records of slots s..s+3 (gathered D slots ahead)
+        //   cost      swap/eviction seconds of slot s, read during slot s-1
+        //   tc, tf    tail-table cell and position of slot s-1, read during s-1
+        // Slot s: (0) the probability of slot s-1, (1) the cost of s+1 read on the
+        // current queue's row, (2) waits and variances of slot s, (3) its tail cell,
+        // (4) if s+1 starts a queue: switch, and read the cost of s+1 again on the
+        // head row.  Every LDS read is consumed one slot after it is issued.
+        constexpr int D = 3;
         int32_t ring[32];
         uint4 rec[4];                 // rec[s % 4] holds slot s's record
         __amdgpu_buffer_rsrc_t rp = rsrc_at(a.perm, 0);
@@ -353,8 +425,6 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
         auto gather = [&](int32_t gid) __attribute__((always_inline)) {
             return *lds_ptr<const uint4>((min((uint32_t)gid, (uint32_t)G) << 4) + grp0);
         };
-        // prologue: records of slots 0..D-1 (their ring entries refilled with
-        // slots 32..32+D-1), the head of slot 0 and its cost
 #pragma unroll
         for (int k = 0; k < D; ++k) {
             rec[k] = gather(ring[k]);
@@ -363,133 +433,119 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
         rec[D] = rec[0];
         uint32_t ev = EVICT ? ld_rel(rsrc_at(a.evict, 0), 0) : 0u;   // word of the block
         uint32_t ev_nx = 0u;                              // word of the next block
-        // prefetch relative to q0 = -1 (queues 0 and 1), issued before enter(0),
-        // whose full wait leaves no load of the prologue pending at the loop
+        // prefetch relative to q0 = -1 (queues 0 and 1), issued before the
+        // entry into queue 0, whose full wait leaves no prologue load pending
         q0 = -1;
         f1 = load_qp(0);
         f2 = load_qp(1);
-        enter(0);                     // need: loads and waits (once per tile)
-        float cost = *lds_ptr<const float>(rowb | ((rec[0].w & 0xFFu) << 2) |
-                                           (EVICT ? (ev & 1u) << ev_shift : 0u));
+        uint32_t rowb0 = 0u;
+        enter_slow(0, rowb0);
+        uint32_t colc = rec[0].w & kColMask;   // cost-table column of the current slot
+        double cost = *lds_ptr<const double>(rowb0 + colc + (EVICT ? (ev & 1u) << ev_shift : 0u));
+        float2 tc = make_float2(0.0f, 0.0f);   // tail cell of the previous slot (none yet)
+        float tf = 0.0f;
+        double tn = 0.0;
+
+        // The probability of the previous slot from its tail cell.
+        auto finish = [&](int s_prev) __attribute__((always_inline)) {
+            const float prob = fmaf(tc.y, tf, tc.x);
+            S = fma(tn, (double)prob, S);
+            if (DETAIL && det && a.d_prob && s_prev >= 0)
+                a.d_prob[(int64_t)s_prev * a.d_count + dq] = prob;
+        };
+
+        // One slot.  w1: record word of slot s + 1; evw, b1: its eviction word and bit.
+        auto step = [&](int s, const uint4 r, uint32_t w1, uint32_t evw, uint32_t b1)
+                        __attribute__((always_inline)) {
+            // (0) slot s-1
+            finish(s - 1);
+            // (1) cost of slot s+1 if it stays in this queue
+            const uint32_t col1 = w1 & kColMask;
+            const uint32_t evb = EVICT ? __builtin_amdgcn_ubfe(evw, b1, 1u) << ev_shift : 0u;
+            double cost1 = *lds_ptr<const double>(cbase + (colc << col_shift) + col1 + evb);
+
+            // (2) slot s
+            const float mu = __uint_as_float(r.x);
+            const float nv = __uint_as_float(r.y);
+            const float slo = __uint_as_float(r.z);
+            const double n = (double)(r.w >> kCountShift);
+            Y = fma(cost, theta, Y);
+            const double num = fma((double)slo, theta, -Y);   // theta (slo - E[W])
+            const float vz = vb + vblk;                       // scaled variance ahead
+            if (DETAIL && det) {
+                const int64_t o = (int64_t)s * a.d_count + dq;
+                if (a.d_mean) a.d_mean[o] = (float)(Y * inv_theta);
+                if (a.d_sd) a.d_sd[o] = (float)(sqrt(V + (double)vblk) * kTailScale * inv_theta);
+            }
+            vblk += nv;
+            if (PEN) PE = fma(-num, inv_theta, PE);
+            Y = fma(n, (double)mu, Y);
+
+            // (3) tail cell of slot s
+            const float rs = __builtin_amdgcn_rsqf(vz);       // cells per unit margin; inf if 0
+            float tt = fmaf(-(float)num, rs, kTailMid);
+            tt = __builtin_amdgcn_fmed3f(tt, kTailLo, kTailHi);   // NaN (0 / 0) -> low end
+            const uint32_t cell = (__float_as_uint(tt) & kTailCellBits) >> 10;   // cell * 8
+            tf = __builtin_amdgcn_fractf(tt);
+            tc = *lds_ptr<const float2>(tail0 + cell);
+            tn = n;
+            // settled before the branch: nothing of slot s may sink into it
+            asm volatile("" : "+v"(tf), "+v"(vblk));
+
+            // (4) queue head at s+1?
+            if (s + 1 - base == nbr) {       // s + 1 == nb, compared block-relative
+                uint32_t rowb;
+                enter(s + 1, rowb);
+                cost1 = *lds_ptr<const double>(rowb + col1 + evb);
+            }
+            cost = cost1;
+            colc = col1;
+        };
 
         // Full 32-slot blocks: no per-slot guard, so every refill is unconditional
         // and the compiler's counting of outstanding loads stays exact.
         const int G32 = G & ~31;
-        const int Gx = __builtin_amdgcn_readfirstlane(G);
-        for (int sb = 0; sb < G32; sb += 32) {
+        for (int sb0 = 0; sb0 < G32; sb0 += 32) {
+            // uniform by construction; said explicitly so that the row offsets and
+            // buffer resources below stay scalar
+            const int sb = __builtin_amdgcn_readfirstlane(sb0);
             block_start();
             if (EVICT) ev_nx = ld_rel(rsrc_at(a.evict, min((sb >> 5) + 1, (G - 1) >> 5)), 0);
             rp = rsrc_at(a.perm, sb);
+            const int lim = G - 1 - sb;           // last row, relative to the block
+            base = sb;
+            nbr = nb - sb;
 #pragma unroll
             for (int k = 0; k < 32; ++k) {
                 const int s = sb + k;
-                // ring entry of slot s+D: turned into its LDS address, then refilled
+                // ring entry of slot s+D: turned into its LDS record, then refilled
                 // with slot s+D+32 (unconditionally: rows past the end clamp to the
-                // last row), so both share one register and every wait on the ring
-                // counts loads exactly
+                // last row), so both share one register
                 const int j = (k + D) & 31;
-                rec[(k + D) & 3] = gather(ring[j]);   // record of slot s+D
+                rec[(k + D) & 3] = gather(ring[j]);
                 __builtin_amdgcn_sched_barrier(0);    // consume before the refill
-                ring[j] = (int32_t)ld_rel(rp, min(s + D + 32, G - 1) - sb);
-                // always true here; an opaque bound keeps each slot a region of its
-                // own, which keeps the record pipeline in fixed registers
-                if (s >= Gx) continue;
-                const uint4 r = rec[k & 3];
-                const float mu = __uint_as_float(r.x);
-                const float var = __uint_as_float(r.y);
-                const float slo = __uint_as_float(r.z);
-                const uint32_t m = r.w & 0xFFu;
-                const double n = (double)(r.w >> 8);
-
-                // (A) waits of slot s
-                Y = fma((double)cost, theta, Y);                  // its swap / eviction
-                const double num = fma((double)slo, theta, -Y);   // theta (slo - E[W])
-                const float rs = __builtin_amdgcn_rsqf((float)V); // 1/sqrt(V); inf if V = 0
-                // |z|; a zero margin with zero variance gives +inf (no violation)
-                const float x = fmaxf(fabsf((float)num), 1e-38f) * rs;
-                if (PEN) PE = fma(-num, inv_theta, PE);
-                if (DETAIL && det) {
-                    const int64_t o = (int64_t)s * a.d_count + dq;
-                    if (a.d_mean) a.d_mean[o] = (float)(Y * inv_theta);
-                    if (a.d_sd) a.d_sd[o] = (float)(sqrt(V) * inv_theta);
-                }
-                Y = fma(n, (double)mu, Y);
-                V = fma(n, (double)var, V);
-                rowb = cbase + (m << row_shift);
-
-                // (B) queue head at s+1?  Then the cost of slot s+1
-                if (s + 1 == nb) enter(s + 1);
-                {
-                    const uint32_t m1 = rec[(k + 1) & 3].w & 0xFFu;
-                    uint32_t idx = rowb | (m1 << 2);
-                    if (EVICT) {
-                        const uint32_t w = k == 31 ? ev_nx : ev;
-                        idx |= __builtin_amdgcn_ubfe(w, (uint32_t)((k + 1) & 31), 1u) << ev_shift;
-                    }
-                    cost = *lds_ptr<const float>(idx);
-                }
-
-                // (C) normal tail of slot s (A&S 26.2.19)
-                float y = fmaf(x, kQ6, kQ5);
-                y = fmaf(y, x, kQ4);
-                y = fmaf(y, x, kQ3);
-                y = fmaf(y, x, kQ2);
-                y = fmaf(y, x, kQ1);
-                y = fmaf(y, x, kQ0);
-                y = y * y;
-                y = y * y;
-                y = y * y;
-                y = y * y;
-                const float q = __builtin_amdgcn_rcpf(y);         // Q(|z|)
-                const float prob = num < 0.0 ? 1.0f - q : q;
-                S = fma(n, (double)prob, S);
-                if (DETAIL && det && a.d_prob) a.d_prob[(int64_t)s * a.d_count + dq] = prob;
+                ring[j] = (int32_t)ld_rel(rp, min(k + D + 32, lim));
+                step(s, rec[k & 3], rec[(k + 1) & 3].w, k == 31 ? ev_nx : ev, (uint32_t)((k + 1) & 31));
             }
             if (EVICT) ev = ev_nx;
+            V += (double)vblk;        // fold the block into the double sum
+            vb = (float)V;
+            vblk = 0.0f;
         }
-        // Remaining G % 32 slots, one at a time (plain loads; small G only).  The
-        // pipeline has already resolved the head and the cost of slot G32.
-        for (int s = G32; s < G; ++s) {
-            const uint4 r = gather((int32_t)at(a.perm, s));
-            const uint32_t m = r.w & 0xFFu;
-            if (s > G32) {
-                if (s == nb) enter(s);
-                uint32_t idx = rowb | (m << 2);
-                if (EVICT) idx |= __builtin_amdgcn_ubfe(ev, (uint32_t)(s & 31), 1u) << ev_shift;
-                cost = *lds_ptr<const float>(idx);
+        // Remaining G % 32 slots, one at a time (plain loads).  The pipeline has
+        // already resolved the head and the cost of slot G32, whose record is
+        // rec[0] (G32 is a multiple of 4).
+        {
+            uint4 r = rec[0];
+            base = G32;
+            nbr = nb - G32;
+            for (int s = G32; s < G; ++s) {
+                const uint4 rn = gather((int32_t)at(a.perm, min(s + 1, G - 1)));
+                step(s, r, rn.w, ev, (uint32_t)((s + 1) & 31));
+                r = rn;
             }
-            const float mu = __uint_as_float(r.x);
-            const float var = __uint_as_float(r.y);
-            const float slo = __uint_as_float(r.z);
-            const double n = (double)(r.w >> 8);
-            Y = fma((double)cost, theta, Y);
-            const double num = fma((double)slo, theta, -Y);
-            const float rs = __builtin_amdgcn_rsqf((float)V);
-            const float x = fmaxf(fabsf((float)num), 1e-38f) * rs;
-            if (PEN) PE = fma(-num, inv_theta, PE);
-            if (DETAIL && det) {
-                const int64_t o = (int64_t)s * a.d_count + dq;
-                if (a.d_mean) a.d_mean[o] = (float)(Y * inv_theta);
-                if (a.d_sd) a.d_sd[o] = (float)(sqrt(V) * inv_theta);
-            }
-            Y = fma(n, (double)mu, Y);
-            V = fma(n, (double)var, V);
-            rowb = cbase + (m << row_shift);
-            float y = fmaf(x, kQ6, kQ5);
-            y = fmaf(y, x, kQ4);
-            y = fmaf(y, x, kQ3);
-            y = fmaf(y, x, kQ2);
-            y = fmaf(y, x, kQ1);
-            y = fmaf(y, x, kQ0);
-            y = y * y;
-            y = y * y;
-            y = y * y;
-            y = y * y;
-            const float q = __builtin_amdgcn_rcpf(y);
-            const float prob = num < 0.0 ? 1.0f - q : q;
-            S = fma(n, (double)prob, S);
-            if (DETAIL && det && a.d_prob) a.d_prob[(int64_t)s * a.d_count + dq] = prob;
         }
+        finish(G - 1);
         if (live) {
             a.score[p] = S;
             if (PEN) a.penalty[p] = PE;
@@ -958,10 +1014,13 @@ int hip_fail(hipError_t e, const char *what)
 
 constexpr size_t kLdsLimit = 160 * 1024;   // gfx950 LDS per workgroup
 
+// Dynamic LDS of the scoring kernel: everything but its static tail table.
+constexpr size_t kScoreLdsLimit = kLdsLimit - sizeof(float) * 2 * kTailCells;
+
 struct Geometry {
-    int row_shift, ev_shift;
-    uint32_t lut_align, lut_region;
-    size_t lds_bytes;
+    int col_shift, ev_shift;
+    uint32_t lut_bytes;
+    size_t lds_bytes;         // dynamic LDS of the scoring kernel
 };
 
 int ceil_log2(uint32_t v)
@@ -974,20 +1033,13 @@ int ceil_log2(uint32_t v)
 Geometry geometry(int G, int I, int M, int C, bool evict)
 {
     Geometry g;
-    const uint32_t Mp = 1u << ceil_log2((uint32_t)M);
-    g.row_shift = ceil_log2(Mp) + 2;
-    const uint32_t half = (uint32_t)(C * (M + 1)) << g.row_shift;   // bytes of one half
+    g.col_shift = ceil_log2((uint32_t)M);
+    const uint32_t half = (uint32_t)(C * (M + 1)) << (g.col_shift + 3);   // bytes of one half
     g.ev_shift = ceil_log2(half < 16u ? 16u : half);
-    if (evict) {
-        g.lut_region = 2u << g.ev_shift;
-        g.lut_align = 2u << g.ev_shift;
-    } else {
-        g.lut_region = (half + 15u) / 16u * 16u;
-        g.lut_align = (1u << g.row_shift) < 16u ? 16u : (1u << g.row_shift);
-    }
-    // group table, worst-case alignment padding, cost table, instances, scratch
-    g.lds_bytes = 16 * (size_t)(G + 1) + (g.lut_align - 1) + g.lut_region + 16 * (size_t)I + 64;
-    g.lds_bytes = (g.lds_bytes + 15) / 16 * 16;
+    const uint32_t bytes = evict ? (1u << g.ev_shift) + half : half;
+    g.lut_bytes = (bytes + 15u) / 16u * 16u;
+    // group table, cost table, instances, scratch
+    g.lds_bytes = 16 * (size_t)(G + 1) + g.lut_bytes + 16 * (size_t)I + 64;
     return g;
 }
 
@@ -1023,10 +1075,9 @@ ScoreArgs score_args(const qlm_problem *pr, const qlm_plans *pl, const Geometry 
     a.I = pr->n_instances;
     a.M = pr->n_models;
     a.C = pr->n_classes;
-    a.row_shift = geo.row_shift;
+    a.col_shift = geo.col_shift;
     a.ev_shift = geo.ev_shift;
-    a.lut_align = geo.lut_align;
-    a.lut_region = geo.lut_region;
+    a.lut_bytes = geo.lut_bytes;
     a.grp_count = pr->grp_count;
     a.grp_mu = pr->grp_mu;
     a.grp_var = pr->grp_var;
@@ -1159,10 +1210,11 @@ int launch_score(const qlm_problem *pr, const qlm_plans *pl, double *score, doub
 {
     const bool ev = pl->evict_bits != nullptr;
     const Geometry geo = geometry(pr->n_groups, pr->n_instances, pr->n_models, pr->n_classes, ev);
-    if (geo.lds_bytes > kLdsLimit)
+    if (geo.lds_bytes > kScoreLdsLimit)
         return fail(QLM_ERR_CAPACITY, "group, cost and instance tables need " +
                                           std::to_string(geo.lds_bytes) +
-                                          " bytes of LDS; the limit is 163840");
+                                          " bytes of LDS; the limit is " +
+                                          std::to_string(kScoreLdsLimit));
     ScoreArgs a = score_args(pr, pl, geo);
     a.score = score;
     a.penalty = penalty;
@@ -1387,8 +1439,8 @@ int32_t qlm_max_groups(int32_t n_models, int32_t n_classes, int32_t n_instances,
 {
     if (n_models < 1 || n_models > 255 || n_classes < 1 || n_instances < 1) return 0;
     const Geometry g0 = geometry(0, n_instances, n_models, n_classes, with_eviction != 0);
-    if (g0.lds_bytes > kLdsLimit) return 0;
-    return (int32_t)((kLdsLimit - g0.lds_bytes) / 16);
+    if (g0.lds_bytes > kScoreLdsLimit) return 0;
+    return (int32_t)((kScoreLdsLimit - g0.lds_bytes) / 16);
 }
 
 const char *qlm_status_string(int status)
