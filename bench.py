@@ -56,6 +56,88 @@ def measured_traffic(config: str, plans: int):
     return float(t["hbm_bytes_per_launch"])
 
 
+COPY_BYTES = 1 << 30
+
+
+def copy_calibration():
+    """A plain 1 GiB device-to-device copy (three times), for scaling the HBM
+    counters: rocprofv3's FETCH_SIZE / WRITE_SIZE of this copy, against its
+    known size, give the bytes each counter unit stands for."""
+    import torch
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.int32, device="cuda:0")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": COPY_BYTES, "copies": 3}), flush=True)
+
+
+def _counter_rows(path, counter):
+    import csv
+    import glob
+    files = glob.glob(os.path.join(path, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit("no counter_collection.csv under %s" % path)
+    out = []
+    for r in csv.DictReader(open(files[0])):
+        if r["Counter_Name"] == counter:
+            out.append((r["Kernel_Name"], int(r["Dispatch_Id"]), float(r["Counter_Value"])))
+    return out
+
+
+def summarize_counters(args):
+    """Per-launch HBM bytes of the scoring kernel from two rocprofv3 --pmc runs
+    of bench.py (FETCH_SIZE, then WRITE_SIZE) and two of --copy-calibration;
+    writes profiles/k_score_<config>_traffic.json and prints a summary."""
+    fetch_dir, write_dir, cfetch_dir, cwrite_dir = args.summarize_counters
+
+    def per_dispatch(rows, pred):
+        vals = {}
+        for name, d, v in rows:
+            if pred(name):
+                vals[d] = vals.get(d, 0.0) + v
+        return list(vals.values())
+
+    def is_score(n):
+        return "k_score" in n
+
+    def is_copy(n):
+        return "copy" in n.lower()
+
+    kf = per_dispatch(_counter_rows(fetch_dir, "FETCH_SIZE"), is_score)
+    kw = per_dispatch(_counter_rows(write_dir, "WRITE_SIZE"), is_score)
+    cf = per_dispatch(_counter_rows(cfetch_dir, "FETCH_SIZE"), is_copy)
+    cw = per_dispatch(_counter_rows(cwrite_dir, "WRITE_SIZE"), is_copy)
+    if not (kf and kw and cf and cw):
+        raise SystemExit("missing dispatches: k_score %d/%d, copy %d/%d" % (len(kf), len(kw), len(cf), len(cw)))
+    # counters are in KiB per dispatch; the largest copy dispatches are the 1 GiB copies
+    cf_k, cw_k = max(cf), max(cw)
+    f_scale = COPY_BYTES / (cf_k * 1024.0)
+    w_scale = COPY_BYTES / (cw_k * 1024.0)
+    kf_avg = sum(kf) / len(kf)
+    kw_avg = sum(kw) / len(kw)
+    fetch_b = kf_avg * 1024.0 * f_scale
+    write_b = kw_avg * 1024.0 * w_scale
+    from paper_2407_00047_amd import workload
+    cfg = workload.CONFIGS[args.config]
+    P = cfg["P"] if args.plans is None else args.plans
+    pr = workload.make_problem(args.config)
+    alg = algorithmic_bytes_per_plan(pr) * P
+    out = {"config": args.config, "plans": P, "source_sha256": kernel_source_hash(),
+           "fetch_kib_per_launch": kf_avg, "write_kib_per_launch": kw_avg,
+           "copy_fetch_kib": cf_k, "copy_write_kib": cw_k,
+           "fetch_scale": f_scale, "write_scale": w_scale,
+           "hbm_bytes_per_launch": fetch_b + write_b,
+           "algorithmic_bytes_per_launch": alg,
+           "traffic_over_algorithmic": (fetch_b + write_b) / alg}
+    path = os.path.join(ROOT, "profiles", "k_score_%s_traffic.json" % args.config)
+    with open(path, "w") as f:
+        json.dump(out, f, indent=1)
+        f.write("\n")
+    print(json.dumps(out, indent=1))
+
+
 def cpu_baseline(problem, plans, seconds: float):
     import oracle
     orc = oracle.default()
@@ -83,7 +165,15 @@ def main():
     ap.add_argument("--plans", type=int, default=None, help="override the plan count")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run a plain 1 GiB device copy (for HBM counter scaling) and exit")
+    ap.add_argument("--summarize-counters", nargs=4, metavar=("FETCH", "WRITE", "COPY_FETCH", "COPY_WRITE"),
+                    help="rocprofv3 --pmc output folders: write the traffic summary and exit")
     args = ap.parse_args()
+
+    if args.summarize_counters:
+        summarize_counters(args)
+        return
 
     if args.gpus != 1:
         print("bench.py: this build scores plans on one GPU; --gpus %d is not supported "
@@ -99,6 +189,9 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
+    if args.copy_calibration:
+        copy_calibration()
+        return
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     qlm.library()

@@ -380,8 +380,26 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
             cbase = r.z;
             rowb = r.w;
         };
-        // Slot s is the head of the next queue: switch to it, reset the sums.
-        auto enter = [&](int s, uint32_t &rowb) __attribute__((always_inline)) {
+        // Slot s is the head of the next queue: switch to it and reset the sums.
+        // enter_fast is the common case, where the next queue is x (prefetched a
+        // block ago, not empty); enter_any takes every case.
+        auto reset_sums = [&]() __attribute__((always_inline)) {
+            Y = 0.0;
+            V = 0.0;
+            vb = 0.0f;
+            vblk = 0.0f;
+        };
+        auto enter_fast = [&](uint32_t &rowb) __attribute__((always_inline)) {
+            g += 1;
+            nb = x.nb;
+            theta = x.theta;
+            if (PEN || DETAIL) inv_theta = x.inv;
+            cbase = x.cbase;
+            rowb = x.head;
+            nbr = nb - base;
+            reset_sums();
+        };
+        auto enter_any = [&](int s, uint32_t &rowb) __attribute__((always_inline)) {
             if (fast) {
                 g += 1;
                 nb = x.nb;
@@ -401,10 +419,7 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
                 enter_slow(s, rowb);
             }
             nbr = nb - base;
-            Y = 0.0;
-            V = 0.0;
-            vb = 0.0f;
-            vblk = 0.0f;
+            reset_sums();
         };
 
         // Software pipeline over the slots of the plan:
@@ -416,6 +431,9 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
         // current queue's row, (2) waits and variances of slot s, (3) its tail cell,
         // (4) if s+1 starts a queue: switch, and read the cost of s+1 again on the
         // head row.  Every LDS read is consumed one slot after it is issued.
+        // At the start of a block at slot sb: ring[j] holds the group id of slot
+        // sb + j (j >= D) or sb + 32 + j (j < D), rec[k] the record of slot sb + k
+        // (k < D), cost and colc those of slot sb.
         constexpr int D = 3;
         int32_t ring[32];
         uint4 rec[4];                 // rec[s % 4] holds slot s's record
@@ -450,13 +468,18 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
         auto finish = [&](int s_prev) __attribute__((always_inline)) {
             const float prob = fmaf(tc.y, tf, tc.x);
             S = fma(tn, (double)prob, S);
+            // settled here: sunk to the end of the block, the sums of all 32 slots
+            // would keep their tail cells live in registers
+            asm volatile("" : "+v"(S));
             if (DETAIL && det && a.d_prob && s_prev >= 0)
                 a.d_prob[(int64_t)s_prev * a.d_count + dq] = prob;
         };
 
-        // One slot.  w1: record word of slot s + 1; evw, b1: its eviction word and bit.
-        auto step = [&](int s, const uint4 r, uint32_t w1, uint32_t evw, uint32_t b1)
-                        __attribute__((always_inline)) {
+        // One slot.  w1: record word of slot s + 1; evw, b1: its eviction word and
+        // bit.  fast_block (std::true_type / false_type): only the common queue
+        // switch can happen here.
+        auto step = [&](auto fast_block, int s, const uint4 r, uint32_t w1, uint32_t evw,
+                        uint32_t b1) __attribute__((always_inline)) {
             // (0) slot s-1
             finish(s - 1);
             // (1) cost of slot s+1 if it stays in this queue
@@ -495,15 +518,21 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
             // (4) queue head at s+1?
             if (s + 1 - base == nbr) {       // s + 1 == nb, compared block-relative
                 uint32_t rowb;
-                enter(s + 1, rowb);
+                if constexpr (decltype(fast_block)::value)
+                    enter_fast(rowb);
+                else
+                    enter_any(s + 1, rowb);
                 cost1 = *lds_ptr<const double>(rowb + col1 + evb);
             }
             cost = cost1;
             colc = col1;
         };
 
-        // Full 32-slot blocks: no per-slot guard, so every refill is unconditional
-        // and the compiler's counting of outstanding loads stays exact.
+        // Full 32-slot blocks.  A block runs unrolled and pipelined when every
+        // lane enters at most the one queue x in it; otherwise (a second queue
+        // head in the block, an empty queue, a queue not prefetched) the whole
+        // wavefront takes the generic path for that block, slot by slot with
+        // plain loads, and then refills the pipeline for the next block.
         const int G32 = G & ~31;
         for (int sb0 = 0; sb0 < G32; sb0 += 32) {
             // uniform by construction; said explicitly so that the row offsets and
@@ -511,21 +540,44 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
             const int sb = __builtin_amdgcn_readfirstlane(sb0);
             block_start();
             if (EVICT) ev_nx = ld_rel(rsrc_at(a.evict, min((sb >> 5) + 1, (G - 1) >> 5)), 0);
-            rp = rsrc_at(a.perm, sb);
-            const int lim = G - 1 - sb;           // last row, relative to the block
             base = sb;
             nbr = nb - sb;
+            const bool odd = nbr >= 1 && nbr <= 32 && (!fast || x.nb <= sb + 32);
+            if (__builtin_amdgcn_ballot_w64(odd) == 0) {
+                rp = rsrc_at(a.perm, sb);
+                const int lim = G - 1 - sb;           // last row, relative to the block
 #pragma unroll
-            for (int k = 0; k < 32; ++k) {
-                const int s = sb + k;
-                // ring entry of slot s+D: turned into its LDS record, then refilled
-                // with slot s+D+32 (unconditionally: rows past the end clamp to the
-                // last row), so both share one register
-                const int j = (k + D) & 31;
-                rec[(k + D) & 3] = gather(ring[j]);
-                __builtin_amdgcn_sched_barrier(0);    // consume before the refill
-                ring[j] = (int32_t)ld_rel(rp, min(k + D + 32, lim));
-                step(s, rec[k & 3], rec[(k + 1) & 3].w, k == 31 ? ev_nx : ev, (uint32_t)((k + 1) & 31));
+                for (int k = 0; k < 32; ++k) {
+                    const int s = sb + k;
+                    // ring entry of slot s+D: turned into its LDS record, then
+                    // refilled with slot s+D+32 (rows past the end clamp to the last
+                    // row), so both share one register
+                    const int j = (k + D) & 31;
+                    rec[(k + D) & 3] = gather(ring[j]);
+                    __builtin_amdgcn_sched_barrier(0);    // consume before the refill
+                    ring[j] = (int32_t)ld_rel(rp, min(k + D + 32, lim));
+                    step(std::true_type{}, s, rec[k & 3], rec[(k + 1) & 3].w,
+                         k == 31 ? ev_nx : ev, (uint32_t)((k + 1) & 31));
+                }
+            } else {
+                uint4 r = rec[0];                     // slot sb (sb % 4 == 0)
+                for (int k = 0; k < 32; ++k) {
+                    const int s = sb + k;
+                    const uint4 rn = gather((int32_t)at(a.perm, min(s + 1, G - 1)));
+                    step(std::false_type{}, s, r, rn.w, k == 31 ? ev_nx : ev,
+                         (uint32_t)((k + 1) & 31));
+                    r = rn;
+                }
+                // refill the pipeline for the block at nx = sb + 32
+                const int nx = sb + 32;
+                const __amdgpu_buffer_rsrc_t rn = rsrc_at(a.perm, nx);
+                const int nlim = G - 1 - nx;
+#pragma unroll
+                for (int j = 0; j < 32; ++j)
+                    ring[j] = (int32_t)ld_rel(rn, max(min(j < D ? j + 32 : j, nlim), 0));
+#pragma unroll
+                for (int k = 0; k < D; ++k)
+                    rec[k] = gather((int32_t)at(a.perm, min(nx + k, G - 1)));
             }
             if (EVICT) ev = ev_nx;
             V += (double)vblk;        // fold the block into the double sum
@@ -541,7 +593,7 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
             nbr = nb - G32;
             for (int s = G32; s < G; ++s) {
                 const uint4 rn = gather((int32_t)at(a.perm, min(s + 1, G - 1)));
-                step(s, r, rn.w, ev, (uint32_t)((s + 1) & 31));
+                step(std::false_type{}, s, r, rn.w, ev, (uint32_t)((s + 1) & 31));
                 r = rn;
             }
         }
