@@ -89,7 +89,7 @@ typedef struct qlm_problem {
  * contiguous, so a wavefront reading one slot of 64 plans reads 256 bytes.    */
 typedef struct qlm_plans {
     int64_t n_plans;             /* P >= 0                                      */
-    int64_t plan_stride;         /* elements between slot rows, >= P            */
+    int64_t plan_stride;         /* elements between slot rows, P <= . <= 2^22   */
     const int32_t  *perm;        /* [G][stride]: group at slot s of plan p; each
                                     plan's column is a permutation of 0..G-1   */
     const int32_t  *qoff;        /* [I+1][stride]: queue g holds slots

@@ -43,6 +43,9 @@ constexpr int kWave = 64;
 constexpr int kScoreThreads = 512;      // 8 wavefronts per workgroup
 constexpr int kRefineThreads = 256;
 constexpr int kMaxScoreBlocks = 4096;
+// Row offsets of a block's prefetch (up to 67 rows of 4 * plan_stride bytes)
+// are 32-bit register operands.
+constexpr int64_t kMaxPlanStride = 1 << 22;
 constexpr int kRefineBlocks = 1024;
 // Request counts share the 32-bit record word with the model's cost-table
 // column (bits 3..10), so they are 21-bit.
@@ -59,9 +62,9 @@ constexpr double kEpsP = 8e-6;
 // cells over z in [-6, 6] (beyond, Q is within 1e-9 of 0 or 1).  The kernel
 // forms t = 1536 - (1024 / 12) z in single precision and clamps it to
 // [1024, 2048): there every float has exponent 10, so the ten leading mantissa
-// bits are the cell and fract(t) the position in it.  Cell k holds the line
-// (c0, c1) that best fits Q over its width (the chord, moved by half its
-// largest deviation); the two end cells are the constants 0 and 1.
+// bits are the cell.  Cell k holds the line that best fits Q over its width
+// (the chord, moved by half its largest deviation), as (a, b) with
+// Q ~ a + b t; the two end cells are the constants 0 and 1.
 constexpr int kTailCells = 1024;
 constexpr double kTailZ = 6.0;
 constexpr double kTailScale = kTailCells / (2.0 * kTailZ);          // cells per unit z
@@ -191,9 +194,9 @@ __device__ void stage_tables(const ScoreArgs &a, const Lds &l)
 }
 
 // The normal-tail table: cell k covers t in [1024 + k, 1025 + k), i.e. z from
-// (512 - k) / kTailScale down to (511 - k) / kTailScale, and holds the line in
-// the position f = t - (1024 + k) that fits Q best (the chord, moved by half its
-// deviation at the middle of the cell).
+// (512 - k) / kTailScale down to (511 - k) / kTailScale, and holds the line
+// that fits Q best there (the chord, moved by half its deviation at the middle
+// of the cell).
 __device__ void stage_tail(float2 *tab)
 {
     // a fixed trip count (the kernel runs kScoreThreads threads): no loop whose
@@ -214,7 +217,10 @@ __device__ void stage_tail(float2 *tab)
             c0 = k == 0 ? 0.0 : 1.0;
             c1 = 0.0;
         }
-        tab[k] = make_float2((float)c0, (float)c1);
+        // the line in t itself (c0 - c1 (1024 + k) + c1 t): no fraction to form
+        // in the kernel; the constant is at most 9.6 in size, so its rounding adds
+        // below 6e-7
+        tab[k] = make_float2((float)(c0 - c1 * (kTailLo + k)), (float)c1);
     }
 }
 
@@ -297,6 +303,10 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
         };
         auto ld_rel = [&](__amdgpu_buffer_rsrc_t r, int rel_row) __attribute__((always_inline)) {
             return (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(r, (int)lpb, rel_row * (int)ld4, 0);
+        };
+        // the same with the whole offset in a vector register (no scalar work)
+        auto ld_voff = [&](__amdgpu_buffer_rsrc_t r, uint32_t voff) __attribute__((always_inline)) {
+            return (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, 0, 0);
         };
 
         double Y = 0.0;        // tokens ahead + theta * (swap and eviction seconds so far)
@@ -389,15 +399,19 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
             vb = 0.0f;
             vblk = 0.0f;
         };
+        // (In a fast block g, nb and the double variance sum are brought up to
+        // date at the end of the block, from whether nbr moved.)
+        int xnbr = 0;             // x.nb - base, set at the start of a fast block
         auto enter_fast = [&](uint32_t &rowb) __attribute__((always_inline)) {
-            g += 1;
-            nb = x.nb;
             theta = x.theta;
             if (PEN || DETAIL) inv_theta = x.inv;
             cbase = x.cbase;
             rowb = x.head;
-            nbr = nb - base;
-            reset_sums();
+            nbr = xnbr;
+            Y = 0.0;
+            if (DETAIL) V = 0.0;
+            vb = 0.0f;
+            vblk = 0.0f;
         };
         auto enter_any = [&](int s, uint32_t &rowb) __attribute__((always_inline)) {
             if (fast) {
@@ -437,6 +451,11 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
         constexpr int D = 3;
         int32_t ring[32];
         uint4 rec[4];                 // rec[s % 4] holds slot s's record
+        // byte offsets of the refill rows of a block (rows sb + D + 32 + k),
+        // relative to its first row, with the lane's column
+        uint32_t voff[32];
+#pragma unroll
+        for (int k = 0; k < 32; ++k) voff[k] = lpb + (uint32_t)(k + D + 32) * (uint32_t)ld4;
         __amdgpu_buffer_rsrc_t rp = rsrc_at(a.perm, 0);
 #pragma unroll
         for (int k = 0; k < 32; ++k) ring[k] = (int32_t)ld_rel(rp, min(k, G - 1));
@@ -461,7 +480,7 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
         uint32_t colc = rec[0].w & kColMask;   // cost-table column of the current slot
         double cost = *lds_ptr<const double>(rowb0 + colc + (EVICT ? (ev & 1u) << ev_shift : 0u));
         float2 tc = make_float2(0.0f, 0.0f);   // tail cell of the previous slot (none yet)
-        float tf = 0.0f;
+        float tf = 0.0f;                       // and its t
         double tn = 0.0;
 
         // The probability of the previous slot from its tail cell.
@@ -501,7 +520,10 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
                 if (a.d_sd) a.d_sd[o] = (float)(sqrt(V + (double)vblk) * kTailScale * inv_theta);
             }
             vblk += nv;
-            if (PEN) PE = fma(-num, inv_theta, PE);
+            if (PEN) {
+                PE = fma(-num, inv_theta, PE);
+                asm volatile("" : "+v"(PE));     // not sunk to the end of the block
+            }
             Y = fma(n, (double)mu, Y);
 
             // (3) tail cell of slot s
@@ -509,7 +531,7 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
             float tt = fmaf(-(float)num, rs, kTailMid);
             tt = __builtin_amdgcn_fmed3f(tt, kTailLo, kTailHi);   // NaN (0 / 0) -> low end
             const uint32_t cell = (__float_as_uint(tt) & kTailCellBits) >> 10;   // cell * 8
-            tf = __builtin_amdgcn_fractf(tt);
+            tf = tt;
             tc = *lds_ptr<const float2>(tail0 + cell);
             tn = n;
             // settled before the branch: nothing of slot s may sink into it
@@ -544,21 +566,34 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
             nbr = nb - sb;
             const bool odd = nbr >= 1 && nbr <= 32 && (!fast || x.nb <= sb + 32);
             if (__builtin_amdgcn_ballot_w64(odd) == 0) {
+                if (sb + D + 64 > G) {
+                    // the last blocks: refill rows past the end clamp to the last
+                    // row (the offsets are recomputed at the next tile)
+#pragma unroll
+                    for (int k = 0; k < 32; ++k)
+                        voff[k] = lpb + (uint32_t)min(k + D + 32, G - 1 - sb) * (uint32_t)ld4;
+                }
                 rp = rsrc_at(a.perm, sb);
-                const int lim = G - 1 - sb;           // last row, relative to the block
+                const int nbr0 = nbr;
+                xnbr = x.nb - sb;
 #pragma unroll
                 for (int k = 0; k < 32; ++k) {
                     const int s = sb + k;
                     // ring entry of slot s+D: turned into its LDS record, then
-                    // refilled with slot s+D+32 (rows past the end clamp to the last
-                    // row), so both share one register
+                    // refilled with slot s+D+32, so both share one register
                     const int j = (k + D) & 31;
                     rec[(k + D) & 3] = gather(ring[j]);
                     __builtin_amdgcn_sched_barrier(0);    // consume before the refill
-                    ring[j] = (int32_t)ld_rel(rp, min(k + D + 32, lim));
+                    ring[j] = (int32_t)ld_voff(rp, voff[k]);
                     step(std::true_type{}, s, rec[k & 3], rec[(k + 1) & 3].w,
                          k == 31 ? ev_nx : ev, (uint32_t)((k + 1) & 31));
                 }
+                // at most one queue entered in this block: bring g, nb and the
+                // double variance sum up to date
+                const bool moved = nbr != nbr0;
+                g += moved ? 1 : 0;
+                nb = moved ? x.nb : nb;
+                if (!DETAIL) V = moved ? 0.0 : V;
             } else {
                 uint4 r = rec[0];                     // slot sb (sb % 4 == 0)
                 for (int k = 0; k < 32; ++k) {
@@ -568,13 +603,15 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
                          (uint32_t)((k + 1) & 31));
                     r = rn;
                 }
-                // refill the pipeline for the block at nx = sb + 32
+                // refill the pipeline for the block at nx = sb + 32 (nx may be G:
+                // every row is clamped to the last one, G - 1, and the resource is
+                // based at a row that exists)
                 const int nx = sb + 32;
-                const __amdgpu_buffer_rsrc_t rn = rsrc_at(a.perm, nx);
-                const int nlim = G - 1 - nx;
+                const int rb = min(nx, G - 1);
+                const __amdgpu_buffer_rsrc_t rn = rsrc_at(a.perm, rb);
 #pragma unroll
                 for (int j = 0; j < 32; ++j)
-                    ring[j] = (int32_t)ld_rel(rn, max(min(j < D ? j + 32 : j, nlim), 0));
+                    ring[j] = (int32_t)ld_rel(rn, min(nx + (j < D ? j + 32 : j), G - 1) - rb);
 #pragma unroll
                 for (int k = 0; k < D; ++k)
                     rec[k] = gather((int32_t)at(a.perm, min(nx + k, G - 1)));
@@ -1114,6 +1151,8 @@ int check_plans(const qlm_problem *pr, const qlm_plans *pl)
     if (pl->n_plans < 0) return fail(QLM_ERR_ARG, "n_plans must be >= 0");
     if (pl->plan_stride < pl->n_plans || pl->plan_stride < 1)
         return fail(QLM_ERR_ARG, "plan_stride must be >= max(n_plans, 1)");
+    if (pl->plan_stride > kMaxPlanStride)
+        return fail(QLM_ERR_ARG, "plan_stride must be <= 4194304");
     if (pl->n_plans > 0 && (!pl->perm || !pl->qoff))
         return fail(QLM_ERR_ARG, "perm and qoff are required");
     (void)pr;
