@@ -40,7 +40,7 @@
 namespace {
 
 constexpr int kWave = 64;
-constexpr int kScoreThreads = 512;      // 8 wavefronts per workgroup
+constexpr int kScoreThreads = 1024;     // 16 wavefronts per workgroup, 4 per SIMD
 constexpr int kRefineThreads = 256;
 constexpr int kMaxScoreBlocks = 4096;
 // Row offsets of a block's prefetch (up to 67 rows of 4 * plan_stride bytes)
@@ -91,6 +91,7 @@ struct ScoreArgs {
     int64_t P, ld;
     const int32_t *perm, *qoff;
     const uint32_t *evict;
+    int32_t split;            // slot where the second half of every plan starts, or G
     double *score, *penalty;
     int64_t d_begin, d_count;
     float *d_mean, *d_sd, *d_prob;
@@ -113,7 +114,7 @@ __device__ inline int clampi(int v, int lo, int hi) { return v < lo ? lo : (v > 
 //                 the previous model's column offset shifted by col_shift.
 //   instances     16 bytes each: theta (double), the cost-table row base of its
 //                 class, the row of its head (initial model, or none)
-//   scratch       8 doubles for workgroup reductions
+//   scratch       16 doubles for workgroup reductions
 struct Lds {
     uint32_t grp, lut, inst, red;
 };
@@ -238,7 +239,7 @@ __device__ inline double wave_min(double v)
 // earlier blocks, the standardised margin, and the violation probability from
 // the tail table.
 template <bool EVICT, bool PEN, bool DETAIL>
-__global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_score(ScoreArgs a)
+__global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4, 4))) void k_score(ScoreArgs a)
 {
     __shared__ __align__(16) float2 s_tail[kTailCells];
     extern __shared__ __align__(16) unsigned char lds[];
@@ -278,7 +279,23 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
     const int col_shift = a.col_shift;
     double lane_min = INFINITY;
 
-    for (int64_t t = (int64_t)blockIdx.x * wpb + wave; t < ntiles; t += (int64_t)gridDim.x * wpb) {
+    // When a.split < G every tile (64 plans) is scored by two wavefronts of the
+    // workgroup: the front one takes slots [0, split), the back one [split, G),
+    // after a warm-up that rebuilds the running sums of the queue holding slot
+    // split.  The back one leaves its partial sums in the outputs; after a
+    // barrier the front one adds its own.  Tiles are taken in rounds, the same
+    // number for every wavefront of the workgroup.
+    const bool halves = a.split < G;
+    const int per_round = halves ? wpb / 2 : wpb;
+    const int in_round = halves ? (wave >> 1) : wave;
+    const bool back = halves && (wave & 1);
+    const int s_begin = back ? a.split : 0;
+    const int s_end = halves && !back ? a.split : G;
+    for (int64_t r0 = (int64_t)blockIdx.x * per_round; r0 < ntiles; r0 += (int64_t)gridDim.x * per_round) {
+      const int64_t t = r0 + in_round;
+      double S_out = 0.0, PE_out = 0.0;
+      int64_t p_out = -1;                           // the lane's plan when live
+      if (t < ntiles) {
         const int64_t tb = t * kWave;               // first plan of the tile (uniform)
         const bool live = tb + lane < a.P;
         const int lp = live ? lane : (int)(a.P - 1 - tb);   // lane's plan, relative to tb
@@ -303,10 +320,6 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
         };
         auto ld_rel = [&](__amdgpu_buffer_rsrc_t r, int rel_row) __attribute__((always_inline)) {
             return (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(r, (int)lpb, rel_row * (int)ld4, 0);
-        };
-        // the same with the whole offset in a vector register (no scalar work)
-        auto ld_voff = [&](__amdgpu_buffer_rsrc_t r, uint32_t voff) __attribute__((always_inline)) {
-            return (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, 0, 0);
         };
 
         double Y = 0.0;        // tokens ahead + theta * (swap and eviction seconds so far)
@@ -437,7 +450,7 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
         };
 
         // Software pipeline over the slots of the plan:
-        //   ring[32]  group ids of the next 32 slots (global loads, 32 slots ahead)
+        //   ring[16]  group ids of the next 16 slots (global loads, 16 slots ahead)
         //   rec[4]    LDS records of slots s..s+3 (gathered D slots ahead)
         //   cost      swap/eviction seconds of slot s, read during slot s-1
         //   tc, tf    tail-table cell and position of slot s-1, read during s-1
@@ -446,37 +459,107 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
         // (4) if s+1 starts a queue: switch, and read the cost of s+1 again on the
         // head row.  Every LDS read is consumed one slot after it is issued.
         // At the start of a block at slot sb: ring[j] holds the group id of slot
-        // sb + j (j >= D) or sb + 32 + j (j < D), rec[k] the record of slot sb + k
+        // sb + j (j >= D) or sb + 16 + j (j < D), rec[k] the record of slot sb + k
         // (k < D), cost and colc those of slot sb.
         constexpr int D = 3;
-        int32_t ring[32];
+        constexpr int R = 16;
+        int32_t ring[R];
         uint4 rec[4];                 // rec[s % 4] holds slot s's record
-        // byte offsets of the refill rows of a block (rows sb + D + 32 + k),
-        // relative to its first row, with the lane's column
-        uint32_t voff[32];
-#pragma unroll
-        for (int k = 0; k < 32; ++k) voff[k] = lpb + (uint32_t)(k + D + 32) * (uint32_t)ld4;
-        __amdgpu_buffer_rsrc_t rp = rsrc_at(a.perm, 0);
-#pragma unroll
-        for (int k = 0; k < 32; ++k) ring[k] = (int32_t)ld_rel(rp, min(k, G - 1));
         auto gather = [&](int32_t gid) __attribute__((always_inline)) {
             return *lds_ptr<const uint4>((min((uint32_t)gid, (uint32_t)G) << 4) + grp0);
         };
+        // Back half: the state of the plan at slot s_begin (a multiple of 32,
+        // > 0).  The queue holding it is the last one starting at or before it
+        // (found from a scan of the queue offsets); its running sums are rebuilt
+        // from its first slot qs over the rows [min qs, s_begin), read in
+        // lockstep (a lane skips the rows before its own qs).  rowb: the
+        // cost-table row of slot s_begin.
+        auto warm_up = [&](uint32_t &rowb) __attribute__((always_inline)) {
+            const int Gs = s_begin;
+            int c = 0, qs = 0, nxt = INT_MAX;
+            for (int h0 = 0; h0 <= I1 + 1; h0 += 8) {
+                uint32_t qv[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) qv[u] = at(a.qoff, min(h0 + u, I1 + 1));
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    const int q = (int)qv[u];
+                    const bool in = h0 + u <= I1 + 1;
+                    if (in && q <= Gs) {
+                        c = h0 + u + 1;
+                        qs = q;
+                    }
+                    if (in && q > Gs) nxt = min(nxt, q);
+                }
+            }
+            g = clampi(c - 1, 0, I1);
+            nb = g >= I1 ? INT_MAX : nxt;
+            const uint4 ir = *lds_ptr<const uint4>(inst0 + 16u * (uint32_t)g);
+            theta = __longlong_as_double((long long)(((uint64_t)ir.y << 32) | ir.x));
+            if (PEN || DETAIL) inv_theta = 1.0 / theta;
+            cbase = ir.z;
+            qs = clampi(qs, 0, Gs);
+            int qmin = qs;
+            for (int o = 32; o > 0; o >>= 1) qmin = min(qmin, __shfl_xor(qmin, o, kWave));
+            const int s0 = __builtin_amdgcn_readfirstlane(qmin) & ~15;
+            double Yw = 0.0, Vw = 0.0;
+            uint32_t colp = 0u;
+            for (int c0 = s0; c0 < Gs; c0 += 16) {      // Gs - s0 is a multiple of 16
+                const __amdgpu_buffer_rsrc_t rw = rsrc_at(a.perm, c0);
+                uint32_t id[16];
+#pragma unroll
+                for (int k = 0; k < 16; ++k) id[k] = ld_rel(rw, k);
+                const uint32_t evw = EVICT ? at(a.evict, c0 >> 5) : 0u;
+#pragma unroll
+                for (int k = 0; k < 16; ++k) {
+                    const int s = c0 + k;
+                    const uint4 r = gather((int32_t)id[k]);
+                    const uint32_t col = r.w & kColMask;
+                    if (s >= qs) {
+                        const uint32_t evb =
+                            EVICT ? __builtin_amdgcn_ubfe(evw, (uint32_t)(s & 31), 1u) << ev_shift : 0u;
+                        const uint32_t rb = s == qs ? ir.w : cbase + (colp << col_shift);
+                        const double cst = *lds_ptr<const double>(rb + col + evb);
+                        Yw = fma(cst, theta, Yw);
+                        Yw = fma((double)(r.w >> kCountShift), (double)__uint_as_float(r.x), Yw);
+                        Vw += (double)__uint_as_float(r.y);
+                    }
+                    colp = col;
+                }
+            }
+            Y = Yw;
+            V = Vw;
+            vb = (float)V;
+            vblk = 0.0f;
+            rowb = qs == Gs ? ir.w : cbase + (colp << col_shift);
+            // prefetch as if queue g had been entered during the block before
+            q0 = g - 1;
+            f1 = load_qp(g);
+            f2 = load_qp(g + 1);
+        };
+        uint32_t rowb0 = 0u;          // cost-table row of slot s_begin
+        if (!back) {
+            // prefetch relative to q0 = -1 (queues 0 and 1), issued before the
+            // entry into queue 0, whose full wait leaves nothing pending
+            q0 = -1;
+            f1 = load_qp(0);
+            f2 = load_qp(1);
+            enter_slow(0, rowb0);
+        } else {
+            warm_up(rowb0);
+        }
+        // the pipeline at s_begin (a multiple of 32)
+        __amdgpu_buffer_rsrc_t rp = rsrc_at(a.perm, s_begin);
+#pragma unroll
+        for (int k = 0; k < R; ++k) ring[k] = (int32_t)ld_rel(rp, min(s_begin + k, G - 1) - s_begin);
 #pragma unroll
         for (int k = 0; k < D; ++k) {
             rec[k] = gather(ring[k]);
-            ring[k] = (int32_t)ld_rel(rp, min(k + 32, G - 1));
+            ring[k] = (int32_t)ld_rel(rp, min(s_begin + k + R, G - 1) - s_begin);
         }
         rec[D] = rec[0];
-        uint32_t ev = EVICT ? ld_rel(rsrc_at(a.evict, 0), 0) : 0u;   // word of the block
+        uint32_t ev = EVICT ? ld_rel(rsrc_at(a.evict, s_begin >> 5), 0) : 0u;   // word of the block
         uint32_t ev_nx = 0u;                              // word of the next block
-        // prefetch relative to q0 = -1 (queues 0 and 1), issued before the
-        // entry into queue 0, whose full wait leaves no prologue load pending
-        q0 = -1;
-        f1 = load_qp(0);
-        f2 = load_qp(1);
-        uint32_t rowb0 = 0u;
-        enter_slow(0, rowb0);
         uint32_t colc = rec[0].w & kColMask;   // cost-table column of the current slot
         double cost = *lds_ptr<const double>(rowb0 + colc + (EVICT ? (ev & 1u) << ev_shift : 0u));
         float2 tc = make_float2(0.0f, 0.0f);   // tail cell of the previous slot (none yet)
@@ -556,7 +639,8 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
         // wavefront takes the generic path for that block, slot by slot with
         // plain loads, and then refills the pipeline for the next block.
         const int G32 = G & ~31;
-        for (int sb0 = 0; sb0 < G32; sb0 += 32) {
+        const int s_full = s_end & ~31;       // split is a multiple of 32
+        for (int sb0 = s_begin; sb0 < s_full; sb0 += 32) {
             // uniform by construction; said explicitly so that the row offsets and
             // buffer resources below stay scalar
             const int sb = __builtin_amdgcn_readfirstlane(sb0);
@@ -566,25 +650,20 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
             nbr = nb - sb;
             const bool odd = nbr >= 1 && nbr <= 32 && (!fast || x.nb <= sb + 32);
             if (__builtin_amdgcn_ballot_w64(odd) == 0) {
-                if (sb + D + 64 > G) {
-                    // the last blocks: refill rows past the end clamp to the last
-                    // row (the offsets are recomputed at the next tile)
-#pragma unroll
-                    for (int k = 0; k < 32; ++k)
-                        voff[k] = lpb + (uint32_t)min(k + D + 32, G - 1 - sb) * (uint32_t)ld4;
-                }
                 rp = rsrc_at(a.perm, sb);
+                const int lim = G - 1 - sb;           // last row, relative to the block
                 const int nbr0 = nbr;
                 xnbr = x.nb - sb;
 #pragma unroll
                 for (int k = 0; k < 32; ++k) {
                     const int s = sb + k;
                     // ring entry of slot s+D: turned into its LDS record, then
-                    // refilled with slot s+D+32, so both share one register
-                    const int j = (k + D) & 31;
+                    // refilled with slot s+D+R (rows past the end clamp to the
+                    // last row), so both share one register
+                    const int j = (k + D) & (R - 1);
                     rec[(k + D) & 3] = gather(ring[j]);
                     __builtin_amdgcn_sched_barrier(0);    // consume before the refill
-                    ring[j] = (int32_t)ld_voff(rp, voff[k]);
+                    ring[j] = (int32_t)ld_rel(rp, min(k + D + R, lim));
                     step(std::true_type{}, s, rec[k & 3], rec[(k + 1) & 3].w,
                          k == 31 ? ev_nx : ev, (uint32_t)((k + 1) & 31));
                 }
@@ -610,8 +689,8 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
                 const int rb = min(nx, G - 1);
                 const __amdgpu_buffer_rsrc_t rn = rsrc_at(a.perm, rb);
 #pragma unroll
-                for (int j = 0; j < 32; ++j)
-                    ring[j] = (int32_t)ld_rel(rn, min(nx + (j < D ? j + 32 : j), G - 1) - rb);
+                for (int j = 0; j < R; ++j)
+                    ring[j] = (int32_t)ld_rel(rn, min(nx + (j < D ? j + R : j), G - 1) - rb);
 #pragma unroll
                 for (int k = 0; k < D; ++k)
                     rec[k] = gather((int32_t)at(a.perm, min(nx + k, G - 1)));
@@ -624,7 +703,7 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
         // Remaining G % 32 slots, one at a time (plain loads).  The pipeline has
         // already resolved the head and the cost of slot G32, whose record is
         // rec[0] (G32 is a multiple of 4).
-        {
+        if (s_end == G) {
             uint4 r = rec[0];
             base = G32;
             nbr = nb - G32;
@@ -634,12 +713,30 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
                 r = rn;
             }
         }
-        finish(G - 1);
+        finish(s_end - 1);
         if (live) {
-            a.score[p] = S;
-            if (PEN) a.penalty[p] = PE;
-            lane_min = fmin(lane_min, S);
+            S_out = S;
+            PE_out = PE;
+            p_out = p;
         }
+      }
+      if (halves) {
+          // the back half's sums go through the outputs to the front half
+          if (back && p_out >= 0) {
+              a.score[p_out] = S_out;
+              if (PEN) a.penalty[p_out] = PE_out;
+          }
+          __syncthreads();
+          if (!back && p_out >= 0) {
+              S_out += a.score[p_out];
+              if (PEN) PE_out += a.penalty[p_out];
+          }
+      }
+      if (!back && p_out >= 0) {
+          a.score[p_out] = S_out;
+          if (PEN) a.penalty[p_out] = PE_out;
+          lane_min = fmin(lane_min, S_out);
+      }
     }
     if (a.wg_min) {
         const double m = wave_min(lane_min);
@@ -1128,7 +1225,7 @@ Geometry geometry(int G, int I, int M, int C, bool evict)
     const uint32_t bytes = evict ? (1u << g.ev_shift) + half : half;
     g.lut_bytes = (bytes + 15u) / 16u * 16u;
     // group table, cost table, instances, scratch
-    g.lds_bytes = 16 * (size_t)(G + 1) + g.lut_bytes + 16 * (size_t)I + 64;
+    g.lds_bytes = 16 * (size_t)(G + 1) + g.lut_bytes + 16 * (size_t)I + 128;
     return g;
 }
 
@@ -1280,13 +1377,21 @@ int occupancy(ScoreKernel k, size_t lds, int *cus, int *per_cu)
 }
 
 // Grid of the scoring kernel: persistent, at most as many workgroups as fit.
-int score_grid(ScoreKernel k, size_t lds, int64_t P, int *grid)
+// When the tiles (64 plans each) fill at most half of the wavefronts the chip
+// holds at once, every tile is split between two wavefronts at *split (a
+// multiple of 32); otherwise *split = G.
+int score_grid(ScoreKernel k, size_t lds, int64_t P, int G, int *grid, int *split)
 {
     int cus = 0, per_cu = 0;
     int rc = occupancy(k, lds, &cus, &per_cu);
     if (rc) return rc;
+    const int wpb = kScoreThreads / kWave;
     const int64_t tiles = (P + kWave - 1) / kWave;
-    const int64_t need = (tiles + kScoreThreads / kWave - 1) / (kScoreThreads / kWave);
+    const int64_t resident = (int64_t)per_cu * cus * wpb;
+    const bool halves = G >= 256 && 2 * tiles <= resident;
+    *split = halves ? (G / 2) & ~31 : G;
+    const int per_round = halves ? wpb / 2 : wpb;
+    const int64_t need = (tiles + per_round - 1) / per_round;
     int64_t g = (int64_t)per_cu * cus;
     if (g > need) g = need;
     if (g > kMaxScoreBlocks) g = kMaxScoreBlocks;
@@ -1322,7 +1427,9 @@ int launch_score(const qlm_problem *pr, const qlm_plans *pl, double *score, doub
                          (det->wait_mean || det->wait_sd || det->prob);
     ScoreKernel k = pick_kernel(ev, penalty != nullptr, use_det);
     int grid = 1;
-    int rc = score_grid(k, geo.lds_bytes, pl->n_plans, &grid);
+    int split = pr->n_groups;
+    int rc = score_grid(k, geo.lds_bytes, pl->n_plans, pr->n_groups, &grid, &split);
+    a.split = split;
     if (rc) return rc;
     if (grid_out) *grid_out = grid;
 
