@@ -53,9 +53,10 @@ constexpr uint32_t kCountMask = (1u << 21) - 1u;
 constexpr int kCountShift = 11;
 constexpr uint32_t kColMask = 0x7F8u;     // model * 8: byte column of the cost table
 
-// Screening error bound per slot of the single-precision probability: the
-// tabulated tail (below 2.2e-6), single-precision rounding of the standardised
-// margin and of the block-wise variance (below 1e-6), with margin.
+// Screening error bound per request: the tabulated tail (below 2.2e-6),
+// single-precision rounding of the standardised margin and of the block-wise
+// variance (below 1e-6) and of the block-wise sums of n P (32 terms at most:
+// below 1.9e-6 of their total), with margin.
 constexpr double kEpsP = 8e-6;
 
 // Normal upper tail Q(z) = erfc(z / sqrt 2) / 2 as a table of 1024 linear
@@ -326,7 +327,8 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
         double V = 0.0;        // scaled variance ahead, through the previous block
         float vb = 0.0f;       // V rounded to single precision
         float vblk = 0.0f;     // scaled variance ahead added within the current block
-        double S = 0.0;        // sum of n * P
+        double S = 0.0;        // sum of n * P, through the previous block
+        float S32 = 0.0f;      // sum of n * P within the current block
         double PE = 0.0;       // sum of (E[W] - slo)
         double theta = 1.0, inv_theta = 1.0;
         uint32_t cbase = 0u;   // cost-table row base of the current queue's class
@@ -564,15 +566,15 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
         double cost = *lds_ptr<const double>(rowb0 + colc + (EVICT ? (ev & 1u) << ev_shift : 0u));
         float2 tc = make_float2(0.0f, 0.0f);   // tail cell of the previous slot (none yet)
         float tf = 0.0f;                       // and its t
-        double tn = 0.0;
+        float tn = 0.0f;                       // and its count
 
         // The probability of the previous slot from its tail cell.
         auto finish = [&](int s_prev) __attribute__((always_inline)) {
             const float prob = fmaf(tc.y, tf, tc.x);
-            S = fma(tn, (double)prob, S);
+            S32 = fmaf(tn, prob, S32);
             // settled here: sunk to the end of the block, the sums of all 32 slots
             // would keep their tail cells live in registers
-            asm volatile("" : "+v"(S));
+            asm volatile("" : "+v"(S32));
             if (DETAIL && det && a.d_prob && s_prev >= 0)
                 a.d_prob[(int64_t)s_prev * a.d_count + dq] = prob;
         };
@@ -616,7 +618,7 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
             const uint32_t cell = (__float_as_uint(tt) & kTailCellBits) >> 10;   // cell * 8
             tf = tt;
             tc = *lds_ptr<const float2>(tail0 + cell);
-            tn = n;
+            tn = (float)(r.w >> kCountShift);
             // settled before the branch: nothing of slot s may sink into it
             asm volatile("" : "+v"(tf), "+v"(vblk));
 
@@ -696,9 +698,11 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
                     rec[k] = gather((int32_t)at(a.perm, min(nx + k, G - 1)));
             }
             if (EVICT) ev = ev_nx;
-            V += (double)vblk;        // fold the block into the double sum
+            V += (double)vblk;        // fold the block into the double sums
             vb = (float)V;
             vblk = 0.0f;
+            S += (double)S32;
+            S32 = 0.0f;
         }
         // Remaining G % 32 slots, one at a time (plain loads).  The pipeline has
         // already resolved the head and the cost of slot G32, whose record is
@@ -714,6 +718,7 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
             }
         }
         finish(s_end - 1);
+        S += (double)S32;
         if (live) {
             S_out = S;
             PE_out = PE;
@@ -1380,7 +1385,7 @@ int occupancy(ScoreKernel k, size_t lds, int *cus, int *per_cu)
 // When the tiles (64 plans each) fill at most half of the wavefronts the chip
 // holds at once, every tile is split between two wavefronts at *split (a
 // multiple of 32); otherwise *split = G.
-int score_grid(ScoreKernel k, size_t lds, int64_t P, int G, int *grid, int *split)
+int score_grid(ScoreKernel k, size_t lds, int64_t P, int G, int I, int *grid, int *split)
 {
     int cus = 0, per_cu = 0;
     int rc = occupancy(k, lds, &cus, &per_cu);
@@ -1389,7 +1394,10 @@ int score_grid(ScoreKernel k, size_t lds, int64_t P, int G, int *grid, int *spli
     const int64_t tiles = (P + kWave - 1) / kWave;
     const int64_t resident = (int64_t)per_cu * cus * wpb;
     const bool halves = G >= 256 && 2 * tiles <= resident;
-    *split = halves ? (G / 2) & ~31 : G;
+    // the back half also rebuilds about one queue's running sums: give it a
+    // little less
+    const int mean_queue = G / I;
+    *split = halves ? min((G + mean_queue) / 2, G - 64) & ~31 : G;
     const int per_round = halves ? wpb / 2 : wpb;
     const int64_t need = (tiles + per_round - 1) / per_round;
     int64_t g = (int64_t)per_cu * cus;
@@ -1428,7 +1436,7 @@ int launch_score(const qlm_problem *pr, const qlm_plans *pl, double *score, doub
     ScoreKernel k = pick_kernel(ev, penalty != nullptr, use_det);
     int grid = 1;
     int split = pr->n_groups;
-    int rc = score_grid(k, geo.lds_bytes, pl->n_plans, pr->n_groups, &grid, &split);
+    int rc = score_grid(k, geo.lds_bytes, pl->n_plans, pr->n_groups, pr->n_instances, &grid, &split);
     a.split = split;
     if (rc) return rc;
     if (grid_out) *grid_out = grid;
