@@ -79,6 +79,17 @@ class Oracle:
         lib.oracle_argmin.argtypes = [dp, ctypes.c_int64, dp]
         lib.oracle_argmin.restype = ctypes.c_int64
         lib.oracle_max_threads.restype = ctypes.c_int
+        vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
+        lib.oracle_n_moves.argtypes = [i32, i32, i32]
+        lib.oracle_n_moves.restype = i64
+        lib.oracle_move_apply.argtypes = [ctypes.POINTER(_Problem), i32, i64, vp, vp, vp, vp, vp, vp]
+        lib.oracle_move_apply.restype = ctypes.c_int
+        lib.oracle_move_scores.argtypes = [ctypes.POINTER(_Problem), ctypes.POINTER(_Plans), i64,
+                                           i32, vp, i64, dp, ctypes.c_int]
+        lib.oracle_move_scores.restype = ctypes.c_int
+        lib.oracle_local_search.argtypes = [ctypes.POINTER(_Problem), ctypes.POINTER(_Plans), i64,
+                                            i32, i32, vp, vp, vp, dp, vp, vp, ctypes.c_int]
+        lib.oracle_local_search.restype = ctypes.c_int
         self.lib = lib
         self.path = path
 
@@ -129,6 +140,71 @@ class Oracle:
         """argmin_p score_p over all plans, lowest index on ties."""
         score, _ = self.score_plans(problem, plans, threads=threads)
         return self.argmin(score)
+
+    # -- plan search -------------------------------------------------------
+
+    def n_moves(self, G: int, I: int, window: int) -> int:
+        return int(self.lib.oracle_n_moves(G, I, window))
+
+    def move_apply(self, problem, perm, qoff, flag, window: int, k: int):
+        """Move k applied to one plan given as arrays (perm[G], qoff[I+1],
+        flag[G] 0/1).  Returns (perm, qoff, flag) of the new plan, or None when
+        k names no move."""
+        b = _Bound(problem, {"perm": np.asarray(perm, np.int32).reshape(-1, 1),
+                             "qoff": np.asarray(qoff, np.int32).reshape(-1, 1)})
+        G, I = b.G, int(problem["n_instances"])
+        perm = np.ascontiguousarray(perm, np.int32)
+        qoff = np.ascontiguousarray(qoff, np.int32)
+        flag = np.ascontiguousarray(flag, np.uint8)
+        p2 = np.empty(G, np.int32)
+        q2 = np.empty(I + 1, np.int32)
+        f2 = np.empty(G, np.uint8)
+        ok = self.lib.oracle_move_apply(ctypes.byref(b.problem), int(window), int(k), _ptr(perm),
+                                        _ptr(qoff), _ptr(flag), _ptr(p2), _ptr(q2), _ptr(f2))
+        return (p2, q2, f2) if ok else None
+
+    def move_scores(self, problem, plans, p: int, window: int, ks=None, threads: int = 0):
+        """Exact scores of the moves ks (default: every move, in index order) of
+        plan p; +inf where a number names no move."""
+        b = _Bound(problem, plans)
+        if not 0 <= p < b.n_plans:
+            raise ValueError("plan index out of range")
+        if window < 0:
+            raise ValueError("window must be >= 0")
+        if ks is None:
+            n = self.n_moves(b.G, int(problem["n_instances"]), window)
+            kp = None
+        else:
+            ks = np.ascontiguousarray(ks, np.int64)
+            n = ks.size
+            kp = ks
+        out = np.empty(n, np.float64)
+        self.lib.oracle_move_scores(ctypes.byref(b.problem), ctypes.byref(b.plans), p, window,
+                                    _ptr(kp), n, _dp(out), int(threads))
+        return out
+
+    def local_search(self, problem, plans, p: int, window: int, max_steps: int,
+                     threads: int = 0):
+        """Steepest-descent search from plan p.  Returns a dict with the final
+        perm[G], qoff[I+1], evict_bits[ceil(G/32)] (None without flags), its
+        score, the number of steps applied and trace[max_steps]."""
+        b = _Bound(problem, plans)
+        if not 0 <= p < b.n_plans:
+            raise ValueError("plan index out of range")
+        if window < 0 or max_steps < 0:
+            raise ValueError("window and max_steps must be >= 0")
+        G, I = b.G, int(problem["n_instances"])
+        perm = np.empty(G, np.int32)
+        qoff = np.empty(I + 1, np.int32)
+        ev = np.empty((G + 31) // 32, np.uint32) if plans.get("evict_bits") is not None else None
+        sc = np.zeros(1)
+        steps = np.zeros(1, np.int32)
+        trace = np.full(max(max_steps, 1), -1, np.int64)
+        self.lib.oracle_local_search(ctypes.byref(b.problem), ctypes.byref(b.plans), p, window,
+                                     max_steps, _ptr(perm), _ptr(qoff), _ptr(ev), _dp(sc),
+                                     _ptr(steps), _ptr(trace), int(threads))
+        return {"perm": perm, "qoff": qoff, "evict_bits": ev, "score": float(sc[0]),
+                "steps": int(steps[0]), "trace": trace[:max_steps]}
 
 
 def default() -> Oracle:
@@ -246,3 +322,11 @@ def argmin(score) -> tuple[int, float]:
 
 def best_plan(problem, plans, threads: int = 0) -> tuple[int, float]:
     return default().best_plan(problem, plans, threads)
+
+
+def move_scores(problem, plans, p: int, window: int, ks=None, threads: int = 0):
+    return default().move_scores(problem, plans, p, window, ks, threads)
+
+
+def local_search(problem, plans, p: int, window: int, max_steps: int, threads: int = 0):
+    return default().local_search(problem, plans, p, window, max_steps, threads)

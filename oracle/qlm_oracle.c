@@ -37,6 +37,10 @@
  *                                                        the optimisation goal)
  *   best plan         argmin_p score_p, lowest p on ties.
  *
+ * The plan search at the end of the file (local search with the scheduler's
+ * reorder and reassign actions as moves) scores each move by building the
+ * moved plan and scoring it with the definition above, from scratch.
+ *
  * The readings behind the choices that the paper leaves open (probability of
  * violation as the score, the group's own swap counted in its waiting time,
  * eviction as a fixed cost, the exclusive token prefix) are listed in the
@@ -44,11 +48,15 @@
  *
  * Parity status: every function here is pinned by tests (closed forms,
  * textbook normal-table values, invariants, Monte Carlo of the stated Normal
- * model, brute force over orderings on tiny inputs).
+ * model, brute force over orderings on tiny inputs; for the search, moves
+ * worked by hand, an independent re-implementation of the moves, and brute
+ * force over every move of tiny plans).
  */
 #include <math.h>
 #include <stddef.h>
 #include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
 
 #ifdef _OPENMP
 #include <omp.h>
@@ -204,4 +212,217 @@ int oracle_max_threads(void)
 #else
     return 1;
 #endif
+}
+
+/* ------------------------------------------------------------------------
+ * Plan search: a local search over plans.
+ *
+ * The paper's global scheduler places groups by solving the assignment
+ * x_{g,i,j} of Sec. 7 as an LP and compares with EDF and with same-model
+ * grouping (Secs. 2 and 8).  This library searches plans directly with the
+ * scheduler's own actions on virtual queues as moves:
+ *
+ *   SWAP(s, d)  reordering within a queue: the groups at slots s and s + d
+ *               (1 <= d <= W) trade places when both slots lie in one queue;
+ *   MOVE(s, h)  reassignment (load balancing, Sec. 5): the group at slot s
+ *               leaves its queue g and joins queue h != g, placed before the
+ *               first group of h whose SLO is strictly later than its own
+ *               (at the end of h when there is none).
+ *
+ * A moved group keeps its eviction flag (the flag belongs to the group's
+ * placement, not to the slot number).  Moves are numbered
+ *   SWAP(s, d):  k = s*W + (d - 1)            s in [0, G), d in [1, W]
+ *   MOVE(s, h):  k = G*W + s*I + h            s in [0, G), h in [0, I)
+ * and a number whose partner slot lies in another queue (or beyond G), or
+ * whose h is the group's own queue, names no move.
+ *
+ * One step scores every move (the exact score above of the plan the move
+ * makes), takes the lowest score, the lowest k on ties, and applies that move
+ * when its score is strictly below the current plan's; otherwise the search
+ * has converged and stops.
+ */
+int64_t oracle_n_moves(int32_t G, int32_t I, int32_t W)
+{
+    return (int64_t)G * W + (int64_t)G * I;
+}
+
+/* queue holding slot s: the g with qoff[g] <= s < qoff[g+1] */
+static int queue_of(const int32_t *qoff, int I, int32_t s)
+{
+    for (int g = 0; g < I; ++g)
+        if (qoff[g] <= s && s < qoff[g + 1]) return g;
+    return -1;
+}
+
+/* Applies move k to the plan (perm, qoff, flag) of one plan; writes the new
+ * plan to (perm2, qoff2, flag2).  Returns 1 when k names a move, else 0
+ * (outputs untouched).  The new plan is built queue by queue as lists. */
+int oracle_move_apply(const oracle_problem *pr, int32_t W, int64_t k,
+                      const int32_t *perm, const int32_t *qoff, const uint8_t *flag,
+                      int32_t *perm2, int32_t *qoff2, uint8_t *flag2)
+{
+    const int G = pr->n_groups, I = pr->n_instances;
+    if (k < 0 || k >= oracle_n_moves(G, I, W)) return 0;
+    if (k < (int64_t)G * W) {                                  /* SWAP */
+        const int32_t s = (int32_t)(k / W), t = s + (int32_t)(k % W) + 1;
+        if (t >= G) return 0;
+        const int g = queue_of(qoff, I, s);
+        if (t >= qoff[g + 1]) return 0;
+        memcpy(perm2, perm, sizeof(int32_t) * G);
+        memcpy(qoff2, qoff, sizeof(int32_t) * (I + 1));
+        memcpy(flag2, flag, G);
+        perm2[s] = perm[t];  perm2[t] = perm[s];
+        flag2[s] = flag[t];  flag2[t] = flag[s];
+        return 1;
+    }
+    const int64_t r = k - (int64_t)G * W;                        /* MOVE */
+    const int32_t s = (int32_t)(r / I);
+    const int h = (int)(r % I);
+    const int g = queue_of(qoff, I, s);
+    if (h == g) return 0;
+    const int32_t gi = perm[s];
+    const float slo_i = pr->grp_slo[gi];
+    int32_t out = 0;
+    for (int q = 0; q < I; ++q) {
+        qoff2[q] = out;
+        int placed = (q != h);
+        for (int32_t u = qoff[q]; u < qoff[q + 1]; ++u) {
+            if (u == s) continue;                       /* the group leaves g */
+            if (!placed && pr->grp_slo[perm[u]] > slo_i) {
+                perm2[out] = gi;  flag2[out] = flag[s];  ++out;  placed = 1;
+            }
+            perm2[out] = perm[u];  flag2[out] = flag[u];  ++out;
+        }
+        if (!placed) { perm2[out] = gi;  flag2[out] = flag[s];  ++out; }
+    }
+    qoff2[I] = out;
+    return 1;
+}
+
+/* Exact score of one plan given as arrays (flags one byte per slot). */
+static double score_one(const oracle_problem *pr, const int32_t *perm, const int32_t *qoff,
+                        const uint8_t *flag, int with_flags, uint32_t *words)
+{
+    const int G = pr->n_groups;
+    oracle_plans one;
+    one.n_plans = 1;
+    one.ld = 1;
+    one.perm = perm;
+    one.qoff = qoff;
+    one.evict_bits = NULL;
+    if (with_flags) {
+        memset(words, 0, sizeof(uint32_t) * (size_t)((G + 31) / 32));
+        for (int s = 0; s < G; ++s)
+            if (flag[s]) words[s / 32] |= 1u << (s % 32);
+        one.evict_bits = words;
+    }
+    double sc = NAN;
+    if (oracle_plan(pr, &one, 0, NULL, NULL, NULL, &sc, NULL) != 0) return NAN;
+    return sc;
+}
+
+/* The plan p of a batch as arrays. */
+static void take_plan(const oracle_problem *pr, const oracle_plans *pl, int64_t p,
+                      int32_t *perm, int32_t *qoff, uint8_t *flag)
+{
+    for (int s = 0; s < pr->n_groups; ++s) {
+        perm[s] = pl->perm[(int64_t)s * pl->ld + p];
+        flag[s] = (uint8_t)evicted(pl, p, s);
+    }
+    for (int g = 0; g <= pr->n_instances; ++g) qoff[g] = pl->qoff[(int64_t)g * pl->ld + p];
+}
+
+/* Scores of moves of one plan given as arrays: ks[0..n) (NULL = every move,
+ * n = oracle_n_moves).  A number that names no move scores +inf. */
+static void move_scores_of(const oracle_problem *pr, int32_t W, const int32_t *perm,
+                           const int32_t *qoff, const uint8_t *flag, int with_flags,
+                           const int64_t *ks, int64_t n, double *out, int n_threads)
+{
+    const int G = pr->n_groups, I = pr->n_instances;
+#ifdef _OPENMP
+    if (n_threads <= 0) n_threads = omp_get_max_threads();
+#pragma omp parallel num_threads(n_threads)
+#endif
+    {
+        int32_t *perm2 = malloc(sizeof(int32_t) * G);
+        int32_t *qoff2 = malloc(sizeof(int32_t) * (I + 1));
+        uint8_t *flag2 = malloc(G);
+        uint32_t *words = malloc(sizeof(uint32_t) * ((G + 31) / 32));
+#ifdef _OPENMP
+#pragma omp for schedule(dynamic, 64)
+#endif
+        for (int64_t j = 0; j < n; ++j) {
+            const int64_t k = ks ? ks[j] : j;
+            if (oracle_move_apply(pr, W, k, perm, qoff, flag, perm2, qoff2, flag2))
+                out[j] = score_one(pr, perm2, qoff2, flag2, with_flags, words);
+            else
+                out[j] = INFINITY;
+        }
+        free(perm2); free(qoff2); free(flag2); free(words);
+    }
+    (void)n_threads;
+}
+
+/* Scores of moves ks[0..n) (NULL = all) of plan p of the batch. */
+int oracle_move_scores(const oracle_problem *pr, const oracle_plans *pl, int64_t p, int32_t W,
+                       const int64_t *ks, int64_t n, double *out, int n_threads)
+{
+    const int G = pr->n_groups, I = pr->n_instances;
+    int32_t *perm = malloc(sizeof(int32_t) * G);
+    int32_t *qoff = malloc(sizeof(int32_t) * (I + 1));
+    uint8_t *flag = malloc(G);
+    take_plan(pr, pl, p, perm, qoff, flag);
+    if (!ks) n = oracle_n_moves(G, I, W);
+    move_scores_of(pr, W, perm, qoff, flag, pl->evict_bits != NULL, ks, n, out, n_threads);
+    free(perm); free(qoff); free(flag);
+    return 0;
+}
+
+/* Local search from plan p of the batch, at most max_steps steps.  Writes the
+ * final plan (perm_out[G], qoff_out[I+1], evict_out[ceil(G/32)] or NULL), its
+ * exact score, the number of moves applied, and trace[max_steps] (the move
+ * applied at each step, -1 from the step that found no improving move on). */
+int oracle_local_search(const oracle_problem *pr, const oracle_plans *pl, int64_t p, int32_t W,
+                        int32_t max_steps, int32_t *perm_out, int32_t *qoff_out,
+                        uint32_t *evict_out, double *score, int32_t *steps, int64_t *trace,
+                        int n_threads)
+{
+    const int G = pr->n_groups, I = pr->n_instances;
+    const int with_flags = pl->evict_bits != NULL;
+    const int64_t nm = oracle_n_moves(G, I, W);
+    int32_t *perm = malloc(sizeof(int32_t) * G), *perm2 = malloc(sizeof(int32_t) * G);
+    int32_t *qoff = malloc(sizeof(int32_t) * (I + 1)), *qoff2 = malloc(sizeof(int32_t) * (I + 1));
+    uint8_t *flag = malloc(G), *flag2 = malloc(G);
+    uint32_t *words = malloc(sizeof(uint32_t) * ((G + 31) / 32));
+    double *sc = malloc(sizeof(double) * (size_t)(nm > 0 ? nm : 1));
+    take_plan(pr, pl, p, perm, qoff, flag);
+    double cur = score_one(pr, perm, qoff, flag, with_flags, words);
+    int32_t done = 0;
+    for (int32_t t = 0; t < max_steps; ++t) trace[t] = -1;
+    for (int32_t t = 0; t < max_steps; ++t) {
+        move_scores_of(pr, W, perm, qoff, flag, with_flags, NULL, nm, sc, n_threads);
+        int64_t best = -1;
+        double bs = INFINITY;
+        for (int64_t k = 0; k < nm; ++k)
+            if (sc[k] < bs) { bs = sc[k]; best = k; }
+        if (best < 0 || !(bs < cur)) break;             /* converged */
+        oracle_move_apply(pr, W, best, perm, qoff, flag, perm2, qoff2, flag2);
+        memcpy(perm, perm2, sizeof(int32_t) * G);
+        memcpy(qoff, qoff2, sizeof(int32_t) * (I + 1));
+        memcpy(flag, flag2, G);
+        cur = score_one(pr, perm, qoff, flag, with_flags, words);
+        trace[t] = best;
+        ++done;
+    }
+    memcpy(perm_out, perm, sizeof(int32_t) * G);
+    memcpy(qoff_out, qoff, sizeof(int32_t) * (I + 1));
+    if (evict_out) {
+        memset(evict_out, 0, sizeof(uint32_t) * (size_t)((G + 31) / 32));
+        for (int s = 0; s < G; ++s)
+            if (flag[s]) evict_out[s / 32] |= 1u << (s % 32);
+    }
+    *score = cur;
+    *steps = done;
+    free(perm); free(perm2); free(qoff); free(qoff2); free(flag); free(flag2); free(words); free(sc);
+    return 0;
 }

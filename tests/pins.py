@@ -383,7 +383,205 @@ def pin_argmin_ties(orc):
     assert orc.argmin(s2)[0] == (0 if s2[0] <= s2[1] else 1)
 
 
+# ---------------------------------------------------------------------------
+# Plan search (local search with reorder and reassign moves)
+#
+# SWAP(s, d), k = s*W + d - 1: the groups at slots s and s+d trade places when
+# both are in one queue.  MOVE(s, h), k = G*W + s*I + h: the group at slot s
+# leaves its queue for queue h != g, placed before the first group of h with a
+# strictly later SLO (else at the end).  Eviction flags go with their group.
+
+
+def _queues_of(perm, qoff):
+    return [list(perm[qoff[g]:qoff[g + 1]]) for g in range(len(qoff) - 1)]
+
+
+def _apply_move_py(pr, perm, qoff, flag, W, k):
+    """The moves restated on Python lists (independent of the oracle's code):
+    returns (perm, qoff, flag) or None."""
+    G, I = int(pr["n_groups"]), int(pr["n_instances"])
+    slo = pr["grp_slo"]
+    owner = {}
+    for g in range(I):
+        for s in range(qoff[g], qoff[g + 1]):
+            owner[s] = g
+    # carry (group, flag) pairs per queue
+    qs = [[(int(perm[s]), int(flag[s])) for s in range(qoff[g], qoff[g + 1])] for g in range(I)]
+    if k < G * W:
+        s, d = divmod(k, W)
+        t = s + d + 1
+        if t >= G or owner[s] != owner[t]:
+            return None
+        g = owner[s]
+        a, b = s - qoff[g], t - qoff[g]
+        qs[g][a], qs[g][b] = qs[g][b], qs[g][a]
+    else:
+        s, h = divmod(k - G * W, I)
+        g = owner[s]
+        if h == g:
+            return None
+        item = qs[g].pop(s - qoff[g])
+        later = [j for j, (i, _) in enumerate(qs[h]) if slo[i] > slo[item[0]]]
+        qs[h].insert(later[0] if later else len(qs[h]), item)
+    flat = [x for q in qs for x in q]
+    lens = [len(q) for q in qs]
+    return (np.array([x[0] for x in flat], np.int32),
+            np.concatenate([[0], np.cumsum(lens)]).astype(np.int32),
+            np.array([x[1] for x in flat], np.uint8))
+
+
+def _flags_of(pl, p, G):
+    if pl.get("evict_bits") is None:
+        return np.zeros(G, np.uint8)
+    w = pl["evict_bits"][:, p]
+    return np.array([(int(w[s // 32]) >> (s % 32)) & 1 for s in range(G)], np.uint8)
+
+
+def _one_plan(perm, qoff, flag, with_flags):
+    G = len(perm)
+    ev = None
+    if with_flags:
+        ev = np.zeros(((G + 31) // 32, 1), np.uint32)
+        for s in range(G):
+            if flag[s]:
+                ev[s // 32, 0] |= np.uint32(1) << np.uint32(s % 32)
+    return {"n_plans": 1, "perm": np.asarray(perm, np.int32).reshape(G, 1),
+            "qoff": np.asarray(qoff, np.int32).reshape(-1, 1), "evict_bits": ev}
+
+
+def pin_moves_by_hand(orc):
+    """Moves worked by hand on one plan: queues [[0, 1, 2], [3], [4, 5, 6]] with
+    SLOs 0:5 1:1 2:9 3:3 4:5 5:1 6:9, group 2 flagged (slot 2), W = 2."""
+    slo = [5, 1, 9, 3, 5, 1, 9]
+    pr = problem([(1, 10.0, 0.0, 0, float(x)) for x in slo], [(100.0, 0)] * 3)
+    perm = np.array([0, 1, 2, 3, 4, 5, 6], np.int32)
+    qoff = np.array([0, 3, 4, 7], np.int32)
+    flag = np.array([0, 0, 1, 0, 0, 0, 0], np.uint8)
+    G, I, W = 7, 3, 2
+
+    def mv(k):
+        return orc.move_apply(pr, perm, qoff, flag, W, k)
+    # SWAP(0, 2) = k 1: groups 0 and 2 trade places, and the flag goes with group 2
+    p2, q2, f2 = mv(0 * W + 1)
+    assert list(p2) == [2, 1, 0, 3, 4, 5, 6] and list(q2) == [0, 3, 4, 7]
+    assert list(f2) == [1, 0, 0, 0, 0, 0, 0]
+    # SWAP(2, 1) = k 4: slot 3 is in the next queue, no move; SWAP(6, 1): beyond G
+    assert mv(2 * W + 0) is None and mv(6 * W + 0) is None
+    # MOVE(slot 3 = group 3, SLO 3, to queue 2 = [4(5), 5(1), 6(9)]): before group 4
+    p2, q2, f2 = mv(G * W + 3 * I + 2)
+    assert list(p2) == [0, 1, 2, 3, 4, 5, 6] and list(q2) == [0, 3, 3, 7]
+    # MOVE(slot 0 = group 0, SLO 5, to queue 2): 5 is not later than group 4's 5,
+    # nor 1; group 6 (9) is the first later one
+    p2, q2, f2 = mv(G * W + 0 * I + 2)
+    assert list(p2) == [1, 2, 3, 4, 5, 0, 6] and list(q2) == [0, 2, 3, 7]
+    assert list(f2) == [0, 1, 0, 0, 0, 0, 0]
+    # MOVE(slot 2 = flagged group 2, SLO 9, to queue 1 = [3(3)]): at the end, flag kept
+    p2, q2, f2 = mv(G * W + 2 * I + 1)
+    assert list(p2) == [0, 1, 3, 2, 4, 5, 6] and list(q2) == [0, 2, 4, 7]
+    assert list(f2) == [0, 0, 0, 1, 0, 0, 0]
+    # MOVE(slot 5 = group 5, SLO 1, to queue 0 = [0(5), 1(1), 2(9)]): at the head
+    p2, q2, f2 = mv(G * W + 5 * I + 0)
+    assert list(p2) == [5, 0, 1, 2, 3, 4, 6] and list(q2) == [0, 4, 5, 7]
+    assert list(f2) == [0, 0, 0, 1, 0, 0, 0]
+    # MOVE to the group's own queue: no move
+    assert mv(G * W + 4 * I + 2) is None
+    assert orc.n_moves(G, I, W) == G * W + G * I
+
+
+def _search_case(rng, G, I, M=2, C=2, evict=True):
+    pr, pl = _random_case(rng, G=G, I=I, M=M, C=C, P=3, evict=evict)
+    return pr, pl
+
+
+def pin_moves_independent(orc):
+    """Every move of random tiny plans, against the moves restated in Python,
+    and every move's score against the plan score of the moved plan."""
+    rng = np.random.default_rng(77)
+    for G, I, W, evict in [(7, 3, 3, True), (9, 2, 9, False), (5, 4, 1, True)]:
+        pr, pl = _search_case(rng, G, I, evict=evict)
+        for p in range(pl["n_plans"]):
+            perm = pl["perm"][:, p].copy()
+            qoff = pl["qoff"][:, p].copy()
+            flag = _flags_of(pl, p, G)
+            sc = orc.move_scores(pr, pl, p, W)
+            assert sc.size == G * W + G * I
+            for k in range(G * W + G * I):
+                a = orc.move_apply(pr, perm, qoff, flag, W, k)
+                b = _apply_move_py(pr, perm, qoff, flag, W, k)
+                if b is None:
+                    assert a is None and sc[k] == np.inf, (G, I, W, p, k)
+                    continue
+                assert a is not None, (G, I, W, p, k)
+                for x, y in zip(a, b):
+                    assert np.array_equal(x, y), (G, I, W, p, k, a, b)
+                ref = orc.plan_detail(pr, _one_plan(*b, evict), 0)["score"]
+                assert sc[k] == ref, (k, sc[k], ref)
+            # a sample of moves by number gives the same scores
+            ks = np.array([0, G * W + 1, G * W + G * I - 1, 2], np.int64)
+            assert np.array_equal(orc.move_scores(pr, pl, p, W, ks=ks), sc[ks])
+
+
+def pin_search_by_hand(orc):
+    """Two identical instances (400 tok/s); queue 0 holds group 0 (2 x 200
+    tokens, 1 s) then group 1 (3 x 100 tokens), both with a 0.5 s SLO; queue 1
+    is empty.  Group 1 waits 1 s and misses: score 3.  With G = 2, W = 1, I = 2:
+    k0 SWAP(0,1): group 0 now waits 0.75 s and misses, score 2; k1 SWAP(1,1):
+    beyond G; k2 MOVE(0,0), k4 MOVE(1,0): own queue; k3 MOVE(0,1) and k5
+    MOVE(1,1): one group per queue, nobody waits, score 0.  The tie goes to
+    k3; after it nothing improves on 0."""
+    pr = problem([(2, 200.0, 0.0, 0, 0.5), (3, 100.0, 0.0, 0, 0.5)], [(400.0, 0), (400.0, 0)])
+    pl = plans([[[0, 1], []]], 2)
+    sc = orc.move_scores(pr, pl, 0, 1)
+    assert list(sc) == [2.0, np.inf, np.inf, 0.0, np.inf, 0.0], sc
+    r = orc.local_search(pr, pl, 0, 1, 4)
+    assert r["steps"] == 1 and list(r["trace"]) == [3, -1, -1, -1]
+    assert list(r["perm"]) == [1, 0] and list(r["qoff"]) == [0, 1, 2] and r["score"] == 0.0
+    # a plan that meets every SLO does not move; neither does one with no moves
+    r = orc.local_search(pr, plans([[[0], [1]]], 2), 0, 1, 4)
+    assert r["steps"] == 0 and list(r["perm"]) == [0, 1] and r["score"] == 0.0
+    pr1 = problem([(2, 200.0, 0.0, 0, 0.5), (3, 100.0, 0.0, 0, 0.5)], [(400.0, 0)])
+    r = orc.local_search(pr1, plans([[[0, 1]]], 2), 0, 0, 3)
+    assert r["steps"] == 0 and r["score"] == 3.0 and list(r["trace"]) == [-1, -1, -1]
+
+
+def pin_search_steepest(orc):
+    """Brute force: at every step of the search on tiny random plans, the move
+    taken is the first minimum over every move (each scored by building the
+    moved plan in Python and scoring it), it strictly improves, and the search
+    stops exactly when no move improves."""
+    rng = np.random.default_rng(5)
+    for G, I, W, evict in [(7, 3, 2, True), (6, 2, 6, False)]:
+        pr, pl = _search_case(rng, G, I, evict=evict)
+        for p in range(pl["n_plans"]):
+            r = orc.local_search(pr, pl, p, W, 12)
+            perm = pl["perm"][:, p].copy()
+            qoff = pl["qoff"][:, p].copy()
+            flag = _flags_of(pl, p, G)
+            cur = orc.plan_detail(pr, _one_plan(perm, qoff, flag, evict), 0)["score"]
+            for t in range(13):
+                best, bs = -1, np.inf
+                for k in range(G * W + G * I):
+                    b = _apply_move_py(pr, perm, qoff, flag, W, k)
+                    if b is None:
+                        continue
+                    v = orc.plan_detail(pr, _one_plan(*b, evict), 0)["score"]
+                    if v < bs:
+                        best, bs = k, v
+                if t == 12 or not bs < cur:
+                    break
+                assert r["trace"][t] == best, (p, t, r["trace"], best)
+                perm, qoff, flag = _apply_move_py(pr, perm, qoff, flag, W, best)
+                cur = bs
+            assert r["steps"] == t, (r["steps"], t)
+            assert np.array_equal(r["perm"], perm) and np.array_equal(r["qoff"], qoff)
+            assert r["score"] == cur
+            if evict:
+                assert np.array_equal(_flags_of({"evict_bits": r["evict_bits"].reshape(-1, 1)},
+                                                0, G), flag)
+
+
 ALL_PINS = [pin_deterministic_queue, pin_variance_queue, pin_normal_table, pin_swap_costs,
             pin_eviction_costs, pin_throughput_per_queue, pin_invariants, pin_half_at_mean,
             pin_identical_instances_symmetry, pin_monte_carlo, pin_edf_special_case,
-            pin_grouping_special_case, pin_argmin_ties]
+            pin_grouping_special_case, pin_argmin_ties, pin_moves_by_hand, pin_moves_independent,
+            pin_search_by_hand, pin_search_steepest]

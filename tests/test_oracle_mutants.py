@@ -59,6 +59,23 @@ MUTANTS = [
     ("argmin_last_on_ties", "if (score[p] < bs) {", "if (score[p] <= bs) {"),
     ("theta_of_first_queue", "const double theta = (double)pr->inst_tput[g];",
      "const double theta = (double)pr->inst_tput[0];"),
+    # plan search
+    ("insert_before_equal_slo", "if (!placed && pr->grp_slo[perm[u]] > slo_i) {",
+     "if (!placed && pr->grp_slo[perm[u]] >= slo_i) {"),
+    ("insert_before_earlier_slo", "if (!placed && pr->grp_slo[perm[u]] > slo_i) {",
+     "if (!placed && pr->grp_slo[perm[u]] < slo_i) {"),
+    ("swap_flags_stay", "flag2[s] = flag[t];  flag2[t] = flag[s];", "(void)0;"),
+    ("move_flag_dropped", "perm2[out] = gi;  flag2[out] = flag[s];  ++out;  placed = 1;",
+     "perm2[out] = gi;  flag2[out] = 0;  ++out;  placed = 1;"),
+    ("swap_across_queues", "if (t >= qoff[g + 1]) return 0;", "(void)g;"),
+    ("swap_distance_short", "t = s + (int32_t)(k % W) + 1;", "t = s + (int32_t)(k % W);"),
+    ("move_index_transposed",
+     "const int32_t s = (int32_t)(r / I);\n    const int h = (int)(r % I);",
+     "const int32_t s = (int32_t)(r % G);\n    const int h = (int)(r / G);"),
+    ("last_move_on_ties", "if (sc[k] < bs) { bs = sc[k]; best = k; }",
+     "if (sc[k] <= bs) { bs = sc[k]; best = k; }"),
+    ("move_on_equal_score", "if (best < 0 || !(bs < cur)) break;",
+     "if (best < 0 || !(bs <= cur)) break;"),
 ]
 
 
