@@ -170,6 +170,71 @@ int qlm_validate_plans(const qlm_problem *problem, const qlm_plans *plans,
 int qlm_validate_problem(const qlm_problem *problem, int64_t *n_invalid,
                          qlm_stream stream);
 
+/* Writable plans (the output of qlm_local_search), laid out as qlm_plans.   */
+typedef struct qlm_plans_out {
+    int64_t plan_stride;         /* elements between slot rows, >= n_plans      */
+    int32_t  *perm;              /* [G][stride]                                  */
+    int32_t  *qoff;              /* [I+1][stride]                                */
+    uint32_t *evict_bits;        /* [ceil(G/32)][stride]; required when the start
+                                    plans have eviction bits, else ignored      */
+} qlm_plans_out;
+
+/*
+ * Plan search.  The paper's scheduler places groups by solving an LP over the
+ * assignment of groups to queue positions (Sec. 7) and is compared with EDF
+ * and same-model grouping (Secs. 2, 8).  This library instead improves plans
+ * by local search whose moves are the scheduler's actions on virtual queues
+ * (Sec. 5: reordering within a queue, reassigning a group to another
+ * instance), each scored exactly by the plan score above:
+ *
+ *   SWAP(s, d)  k = s*W + d - 1     (s in [0,G), d in [1,W]): the groups at
+ *               slots s and s + d trade places, if both slots lie in one queue;
+ *   MOVE(s, h)  k = G*W + s*I + h   (h in [0,I)): the group at slot s leaves
+ *               its queue g for queue h != g, placed before the first group of
+ *               h whose SLO is strictly later than its own (else at the end).
+ *
+ * A moved group keeps its eviction flag.  A number k whose partner slot lies
+ * in another queue or beyond G, or whose h is the group's own queue, names no
+ * move.  A move's score is the exact plan score (the arithmetic and summation
+ * order of qlm_rwt_score_exact) of the plan the move makes; the library
+ * computes it incrementally, from the first position the move changes.
+ *
+ * Limits: G <= 65536, I <= 4096, 0 <= W <= 1024.  SLOs must not be NaN.
+ * Malformed start plans give unspecified results, never out-of-bounds access.
+ */
+int64_t qlm_search_n_moves(int32_t n_groups, int32_t n_instances, int32_t window);
+
+/* Bytes of device workspace for n_plans plans with window W (0 on bad sizes). */
+size_t qlm_search_workspace_bytes(const qlm_problem *problem, int64_t n_plans,
+                                  int32_t window);
+
+/*
+ * Scores every move of every plan: move_score [P][qlm_search_n_moves] device
+ * out, plan-major (entry (p, k) at p * n_moves + k); +inf where k names no
+ * move.  ws: device workspace of at least qlm_search_workspace_bytes, 256-byte
+ * aligned, scratch.
+ */
+int qlm_search_moves(const qlm_problem *problem, const qlm_plans *plans, int32_t window,
+                     void *ws, size_t ws_bytes, double *move_score, qlm_stream stream);
+
+/*
+ * Steepest-descent local search from every start plan, independently: each
+ * step scores every move, takes the lowest score (the lowest k on ties) and
+ * applies it when it is strictly below the current plan's score; otherwise
+ * that plan has converged and stops.  At most max_steps steps.
+ *   start   the start plans (read before any output is written, so `out` may
+ *           name the same arrays)
+ *   out     the final plans
+ *   score   [P] device out or NULL: exact score of each final plan
+ *   steps   [P] device out or NULL: moves applied
+ *   trace   [P][max_steps] device out or NULL: the move applied at each step,
+ *           -1 from the step that found no improving move
+ */
+int qlm_local_search(const qlm_problem *problem, const qlm_plans *start,
+                     const qlm_plans_out *out, int32_t window, int32_t max_steps,
+                     void *ws, size_t ws_bytes, double *score, int32_t *steps,
+                     int64_t *trace, qlm_stream stream);
+
 /* Largest G the scoring kernels accept for these M, C, I (on-chip budget). */
 int32_t qlm_max_groups(int32_t n_models, int32_t n_classes, int32_t n_instances,
                        int32_t with_eviction);

@@ -14,6 +14,7 @@ ROOT = os.path.dirname(HERE)
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 LIB = os.path.join(HERE, "libqlm.so")
 ARCH = "gfx950"
+SOURCES = ["qlm.hip", "search.hip"]
 
 HIP_FLAGS = [
     "-O3", "-std=c++17", "--offload-arch=" + ARCH, "-fPIC", "-shared",
@@ -25,9 +26,9 @@ HIP_FLAGS = [
 
 
 def build_hip(verbose: bool = False, extra=()) -> str:
-    src = os.path.join(HERE, "csrc", "qlm.hip")
+    srcs = [os.path.join(HERE, "csrc", f) for f in SOURCES]
     tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [HIPCC, *HIP_FLAGS, *extra, "-o", tmp, src]
+    cmd = [HIPCC, *HIP_FLAGS, *extra, "-o", tmp, *srcs]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)

@@ -35,6 +35,7 @@
 #include <type_traits>
 #include <vector>
 
+#include "internal.h"
 #include "qlm.h"
 
 namespace {
@@ -1187,8 +1188,12 @@ __global__ void k_validate_problem(ExactArgs a, int64_t *n_invalid)
     if (bad) atomicAdd((unsigned long long *)n_invalid, (unsigned long long)bad);
 }
 
+}  // namespace
+
 // ---------------------------------------------------------------------------
 // Host side
+
+namespace qlm_internal {
 
 thread_local std::string t_err;
 
@@ -1202,6 +1207,42 @@ int hip_fail(hipError_t e, const char *what)
 {
     return fail(QLM_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
 }
+
+int check_problem(const qlm_problem *pr)
+{
+    if (!pr) return fail(QLM_ERR_ARG, "problem is NULL");
+    if (pr->n_groups < 1 || pr->n_instances < 1 || pr->n_models < 1 || pr->n_classes < 1)
+        return fail(QLM_ERR_ARG, "n_groups, n_instances, n_models and n_classes must be >= 1");
+    if (pr->n_models > 255) return fail(QLM_ERR_ARG, "n_models must be <= 255");
+    if (pr->n_groups > (1 << 24)) return fail(QLM_ERR_ARG, "n_groups too large");
+    if (!pr->grp_count || !pr->grp_mu || !pr->grp_var || !pr->grp_model || !pr->grp_slo ||
+        !pr->inst_tput || !pr->inst_class)
+        return fail(QLM_ERR_ARG, "a required problem array is NULL");
+    return QLM_OK;
+}
+
+int check_plans(const qlm_problem *pr, const qlm_plans *pl)
+{
+    if (!pl) return fail(QLM_ERR_ARG, "plans is NULL");
+    if (pl->n_plans < 0) return fail(QLM_ERR_ARG, "n_plans must be >= 0");
+    if (pl->plan_stride < pl->n_plans || pl->plan_stride < 1)
+        return fail(QLM_ERR_ARG, "plan_stride must be >= max(n_plans, 1)");
+    if (pl->plan_stride > kMaxPlanStride)
+        return fail(QLM_ERR_ARG, "plan_stride must be <= 4194304");
+    if (pl->n_plans > 0 && (!pl->perm || !pl->qoff))
+        return fail(QLM_ERR_ARG, "perm and qoff are required");
+    (void)pr;
+    return QLM_OK;
+}
+
+}  // namespace qlm_internal
+
+namespace {
+
+using qlm_internal::check_plans;
+using qlm_internal::check_problem;
+using qlm_internal::fail;
+using qlm_internal::hip_fail;
 
 constexpr size_t kLdsLimit = 160 * 1024;   // gfx950 LDS per workgroup
 
@@ -1232,33 +1273,6 @@ Geometry geometry(int G, int I, int M, int C, bool evict)
     // group table, cost table, instances, scratch
     g.lds_bytes = 16 * (size_t)(G + 1) + g.lut_bytes + 16 * (size_t)I + 128;
     return g;
-}
-
-int check_problem(const qlm_problem *pr)
-{
-    if (!pr) return fail(QLM_ERR_ARG, "problem is NULL");
-    if (pr->n_groups < 1 || pr->n_instances < 1 || pr->n_models < 1 || pr->n_classes < 1)
-        return fail(QLM_ERR_ARG, "n_groups, n_instances, n_models and n_classes must be >= 1");
-    if (pr->n_models > 255) return fail(QLM_ERR_ARG, "n_models must be <= 255");
-    if (pr->n_groups > (1 << 24)) return fail(QLM_ERR_ARG, "n_groups too large");
-    if (!pr->grp_count || !pr->grp_mu || !pr->grp_var || !pr->grp_model || !pr->grp_slo ||
-        !pr->inst_tput || !pr->inst_class)
-        return fail(QLM_ERR_ARG, "a required problem array is NULL");
-    return QLM_OK;
-}
-
-int check_plans(const qlm_problem *pr, const qlm_plans *pl)
-{
-    if (!pl) return fail(QLM_ERR_ARG, "plans is NULL");
-    if (pl->n_plans < 0) return fail(QLM_ERR_ARG, "n_plans must be >= 0");
-    if (pl->plan_stride < pl->n_plans || pl->plan_stride < 1)
-        return fail(QLM_ERR_ARG, "plan_stride must be >= max(n_plans, 1)");
-    if (pl->plan_stride > kMaxPlanStride)
-        return fail(QLM_ERR_ARG, "plan_stride must be <= 4194304");
-    if (pl->n_plans > 0 && (!pl->perm || !pl->qoff))
-        return fail(QLM_ERR_ARG, "perm and qoff are required");
-    (void)pr;
-    return QLM_OK;
 }
 
 ScoreArgs score_args(const qlm_problem *pr, const qlm_plans *pl, const Geometry &geo)
@@ -1661,7 +1675,7 @@ const char *qlm_status_string(int status)
     }
 }
 
-const char *qlm_last_error(void) { return t_err.c_str(); }
+const char *qlm_last_error(void) { return qlm_internal::t_err.c_str(); }
 
 int qlm_timing_enable(int on)
 {

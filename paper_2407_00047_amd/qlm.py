@@ -6,7 +6,8 @@ run when the library is not built (there is no fallback of any kind).
 
 Function names follow the C interface: ``rwt_score``, ``rwt_score_exact``,
 ``best_plan`` (with ``best_plan_workspace_bytes``), ``validate_plans``,
-``validate_problem``.
+``validate_problem``, ``search_n_moves``, ``search_workspace_bytes``,
+``search_moves``, ``local_search``.
 """
 from __future__ import annotations
 
@@ -46,6 +47,11 @@ class Plans(ctypes.Structure):
                 ("evict_bits", ctypes.c_void_p)]
 
 
+class PlansOut(ctypes.Structure):
+    _fields_ = [("plan_stride", ctypes.c_int64), ("perm", ctypes.c_void_p),
+                ("qoff", ctypes.c_void_p), ("evict_bits", ctypes.c_void_p)]
+
+
 class Detail(ctypes.Structure):
     _fields_ = [("plan_begin", ctypes.c_int64), ("plan_count", ctypes.c_int64),
                 ("wait_mean", ctypes.c_void_p), ("wait_sd", ctypes.c_void_p),
@@ -78,9 +84,17 @@ def library():
             lib.qlm_timing_enable.argtypes = [ctypes.c_int]
             lib.qlm_timing_read.argtypes = [ctypes.POINTER(ctypes.c_int64),
                                             ctypes.POINTER(ctypes.c_double)]
+            i32 = ctypes.c_int32
+            lib.qlm_search_n_moves.argtypes = [i32, i32, i32]
+            lib.qlm_search_n_moves.restype = i64
+            lib.qlm_search_workspace_bytes.argtypes = [P, i64, i32]
+            lib.qlm_search_workspace_bytes.restype = ctypes.c_size_t
+            lib.qlm_search_moves.argtypes = [P, PL, i32, vp, ctypes.c_size_t, vp, vp]
+            lib.qlm_local_search.argtypes = [P, PL, ctypes.POINTER(PlansOut), i32, i32, vp,
+                                             ctypes.c_size_t, vp, vp, vp, vp]
             for name in ("qlm_rwt_score", "qlm_rwt_score_exact", "qlm_best_plan",
                          "qlm_validate_plans", "qlm_validate_problem", "qlm_timing_enable",
-                         "qlm_timing_read"):
+                         "qlm_timing_read", "qlm_search_moves", "qlm_local_search"):
                 getattr(lib, name).restype = ctypes.c_int
             _lib = lib
     return _lib
@@ -253,3 +267,63 @@ def timing_read():
     ms = ctypes.c_double(0.0)
     _check(library().qlm_timing_read(ctypes.byref(n), ctypes.byref(ms)))
     return int(n.value), float(ms.value)
+
+
+# -- plan search --------------------------------------------------------------
+
+def search_n_moves(n_groups: int, n_instances: int, window: int) -> int:
+    return int(library().qlm_search_n_moves(n_groups, n_instances, window))
+
+
+def search_workspace_bytes(problem: DeviceProblem, n_plans: int, window: int) -> int:
+    return int(library().qlm_search_workspace_bytes(ctypes.byref(problem.struct), n_plans,
+                                                    window))
+
+
+def search_workspace(problem: DeviceProblem, n_plans: int, window: int, device="cuda"):
+    import torch
+    nbytes = search_workspace_bytes(problem, n_plans, window)
+    return torch.empty(max(nbytes, 1), dtype=torch.uint8, device=device)
+
+
+def search_moves(problem: DeviceProblem, plans: DevicePlans, window: int, ws=None, stream=None,
+                 out=None):
+    """Exact score of every move of every plan: device tensor [P, n_moves]
+    (+inf where a move number names no move)."""
+    import torch
+    dev = plans.perm.device
+    nm = search_n_moves(problem.n_groups, problem.n_instances, window)
+    if ws is None:
+        ws = search_workspace(problem, plans.n_plans, window, dev)
+    if out is None:
+        out = torch.empty((plans.n_plans, nm), dtype=torch.float64, device=dev)
+    _check(library().qlm_search_moves(ctypes.byref(problem.struct), ctypes.byref(plans.struct),
+                                      window, _ptr(ws), ws.numel(), _ptr(out), _stream(stream)))
+    return out
+
+
+def local_search(problem: DeviceProblem, plans: DevicePlans, window: int, max_steps: int,
+                 trace: bool = False, ws=None, stream=None, out: DevicePlans | None = None):
+    """Steepest-descent search from every plan.  Returns a dict with the final
+    plans (a DevicePlans), their exact scores [P] f64, the steps applied [P]
+    int32 and, when asked, the trace [P, max_steps] int64."""
+    import torch
+    dev = plans.perm.device
+    P = plans.n_plans
+    if ws is None:
+        ws = search_workspace(problem, P, window, dev)
+    if out is None:
+        out = DevicePlans(torch.empty_like(plans.perm), torch.empty_like(plans.qoff),
+                          None if plans.evict_bits is None else torch.empty_like(plans.evict_bits),
+                          P)
+    o = PlansOut(int(out.perm.shape[1]), _ptr(out.perm), _ptr(out.qoff), _ptr(out.evict_bits))
+    score = torch.empty(P, dtype=torch.float64, device=dev)
+    steps = torch.empty(P, dtype=torch.int32, device=dev)
+    tr = torch.empty((P, max(max_steps, 1)), dtype=torch.int64, device=dev) if trace else None
+    _check(library().qlm_local_search(ctypes.byref(problem.struct), ctypes.byref(plans.struct),
+                                      ctypes.byref(o), window, max_steps, _ptr(ws), ws.numel(),
+                                      _ptr(score), _ptr(steps), _ptr(tr), _stream(stream)))
+    res = {"plans": out, "score": score, "steps": steps}
+    if trace:
+        res["trace"] = tr[:, :max_steps]
+    return res

@@ -88,3 +88,33 @@ def subset_plans(pl, idx):
             "qoff": np.ascontiguousarray(pl["qoff"][:, idx]),
             "evict_bits": None if pl.get("evict_bits") is None
             else np.ascontiguousarray(pl["evict_bits"][:, idx])}
+
+
+def hand_case(rng, G, I, M=3, C=2, P=70, model0=True, evict=True, empty_queues=False,
+              skewed=False):
+    """Random groups, instances and plans drawn from rng (uniform sizes, SLOs
+    and costs; optional empty queues, skewed queue lengths, eviction flags)."""
+    groups = []
+    for _ in range(G):
+        groups.append((int(rng.integers(0, 30)), float(rng.uniform(1, 600)),
+                       float(rng.uniform(0, 5e4)), int(rng.integers(0, M)),
+                       float(rng.uniform(0.1, 300))))
+    inst = [(float(rng.choice([400.0, 1000.0, 5000.0])), int(rng.integers(0, C))) for _ in range(I)]
+    S = rng.uniform(0.5, 30.0, (C, M, M)).astype(np.float32)
+    m0 = [int(x) for x in rng.integers(-1, M, I)] if model0 else None
+    pr = problem(groups, inst, n_models=M, n_classes=C, swap=S, evict_cost=1.25, model0=m0)
+    qls, evs = [], []
+    for p in range(P):
+        order = rng.permutation(G)
+        k = I if not empty_queues else max(1, I // 3)
+        if skewed:
+            # a few long queues and many short ones: 32-slot blocks with one queue
+            # head per plan and blocks with several, in the same plan
+            w = np.where(np.arange(I) < 3, 30.0, 1.0)
+            owner = rng.choice(I, size=G, p=w / w.sum())
+        else:
+            owner = rng.integers(0, k, G)
+        qls.append([[int(i) for i in order if owner[i] == g] for g in range(I)])
+        evs.append(list(rng.choice(G, size=min(G, 3), replace=False)))
+    pl = plans(qls, G, evict=evs if evict else None)
+    return pr, pl

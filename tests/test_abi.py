@@ -28,7 +28,8 @@ def test_header_declares_entry_points():
     names = declared_functions()
     for must in ("qlm_rwt_score", "qlm_best_plan", "qlm_best_plan_workspace_bytes",
                  "qlm_rwt_score_exact", "qlm_validate_plans", "qlm_validate_problem",
-                 "qlm_status_string", "qlm_last_error"):
+                 "qlm_status_string", "qlm_last_error", "qlm_search_n_moves",
+                 "qlm_search_workspace_bytes", "qlm_search_moves", "qlm_local_search"):
         assert must in names
 
 
@@ -96,3 +97,42 @@ def test_max_groups(lib):
     assert lib.qlm_max_groups(1, 1, 1, 0) > mg
     assert lib.qlm_max_groups(0, 1, 1, 0) == 0
     assert lib.qlm_max_groups(256, 1, 1, 0) == 0
+
+
+def test_search_argument_checks(lib):
+    """The plan search rejects bad windows, sizes, workspaces and outputs on
+    the host, before any launch."""
+    from paper_2407_00047_amd import qlm
+    P = ctypes.byref
+    pr = _problem(qlm, G=8, I=2)
+    pl = qlm.Plans(3, 3, 0x1000, 0x1000, None)
+    assert lib.qlm_search_n_moves(8, 2, 3) == 8 * 3 + 8 * 2
+    assert lib.qlm_search_n_moves(8, 2, -1) == 0
+    need = lib.qlm_search_workspace_bytes(P(pr), 3, 4)
+    assert need > 0 and lib.qlm_search_workspace_bytes(P(pr), 6, 4) > need
+    assert lib.qlm_search_workspace_bytes(P(pr), 3, -1) == 0
+    ws = 0x10000
+    out = qlm.PlansOut(3, 0x1000, 0x1000, None)
+    ms = lib.qlm_search_moves
+    assert ms(P(pr), P(pl), -1, ws, need, 0x1000, None) == qlm.QLM_ERR_ARG
+    assert ms(P(pr), P(pl), 1025, ws, need, 0x1000, None) == qlm.QLM_ERR_ARG
+    assert ms(P(pr), P(pl), 4, ws, need, None, None) == qlm.QLM_ERR_ARG
+    assert ms(P(pr), P(pl), 4, None, need, 0x1000, None) == qlm.QLM_ERR_WORKSPACE
+    assert ms(P(pr), P(pl), 4, ws + 16, need, 0x1000, None) == qlm.QLM_ERR_WORKSPACE
+    assert ms(P(pr), P(pl), 4, ws, need - 1, 0x1000, None) == qlm.QLM_ERR_WORKSPACE
+    big = _problem(qlm, G=65537, I=2)
+    assert ms(P(big), P(pl), 4, ws, need, 0x1000, None) == qlm.QLM_ERR_ARG
+    many = _problem(qlm, G=8, I=4097)
+    assert ms(P(many), P(pl), 4, ws, need, 0x1000, None) == qlm.QLM_ERR_ARG
+    ls = lib.qlm_local_search
+    assert ls(P(pr), P(pl), None, 4, 5, ws, need, None, None, None, None) == qlm.QLM_ERR_ARG
+    assert ls(P(pr), P(pl), P(out), 4, -1, ws, need, None, None, None, None) == qlm.QLM_ERR_ARG
+    short = qlm.PlansOut(2, 0x1000, 0x1000, None)
+    assert ls(P(pr), P(pl), P(short), 4, 5, ws, need, None, None, None, None) == qlm.QLM_ERR_ARG
+    plev = qlm.Plans(3, 3, 0x1000, 0x1000, 0x1000)
+    assert ls(P(pr), P(plev), P(out), 4, 5, ws, need, None, None, None, None) == qlm.QLM_ERR_ARG
+    assert ls(P(pr), P(pl), P(out), 4, 5, ws, need - 1, None, None, None, None) == \
+        qlm.QLM_ERR_WORKSPACE
+    # no plans: nothing to do
+    zero = qlm.Plans(0, 1, None, None, None)
+    assert ms(P(pr), P(zero), 4, ws, need, 0x1000, None) == qlm.QLM_OK

@@ -1,0 +1,273 @@
+"""Parity of the GPU plan search with the oracle.
+
+  - every move score of every plan (qlm_search_moves) against the oracle,
+    which builds each moved plan and scores it from scratch: both are double
+    precision in the same order, so they agree to the last bits of erfc;
+  - the search itself (qlm_local_search): the moves taken step by step, the
+    steps, the final plans (bit-exact) and their scores.  Where both sides are
+    at a near-tie (two moves whose scores differ only in erfc's last bits) the
+    GPU may take the other move; that step is then checked for being a valid
+    choice, and the comparison ends there;
+  - at full workload sizes, a sample of move scores and a few search steps,
+    each checked by the oracle on the plan the search holds at that step.
+"""
+import zlib
+
+import numpy as np
+import pytest
+
+from cases import hand_case
+from gpu_util import device_inputs
+
+pytestmark = pytest.mark.gpu
+
+# Both sides are double precision with the same operations in the same order;
+# only the device and host erfc differ, in their last bits.
+MOVE_REL = 1e-12
+
+
+@pytest.fixture(scope="module")
+def qlm():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2407_00047_amd import qlm as q
+    q.library()
+    return q
+
+
+def _close(a, b):
+    a = np.atleast_1d(np.asarray(a, np.float64))
+    b = np.atleast_1d(np.asarray(b, np.float64))
+    same_inf = np.isinf(a) & np.isinf(b) & (np.sign(a) == np.sign(b))
+    fin = np.isfinite(a) & np.isfinite(b)
+    ok = same_inf.copy()
+    ok[fin] = np.abs(a[fin] - b[fin]) <= MOVE_REL * (np.abs(b[fin]) + 1.0)
+    return ok
+
+
+def _flags(pl, p, G):
+    if pl.get("evict_bits") is None:
+        return np.zeros(G, np.uint8)
+    w = pl["evict_bits"][:, p]
+    return ((w[np.arange(G) // 32] >> (np.arange(G) % 32)) & 1).astype(np.uint8)
+
+
+def _one(perm, qoff, flag, with_flags):
+    G = len(perm)
+    ev = None
+    if with_flags:
+        ev = np.zeros(((G + 31) // 32, 1), np.uint32)
+        for s in np.flatnonzero(flag):
+            ev[s // 32, 0] |= np.uint32(1) << np.uint32(s % 32)
+    return {"n_plans": 1, "perm": np.asarray(perm, np.int32).reshape(G, 1),
+            "qoff": np.asarray(qoff, np.int32).reshape(-1, 1), "evict_bits": ev}
+
+
+SEARCH_CASES = [
+    dict(G=1, I=1, P=2, W=1),                       # no move at all
+    dict(G=5, I=3, P=9, W=2),
+    dict(G=33, I=2, P=8, W=4, evict=False),
+    dict(G=70, I=4, P=6, W=8, empty_queues=True),
+    dict(G=97, I=1, P=3, W=5, model0=False),        # one queue: no reassignment
+    dict(G=40, I=5, P=5, W=0),                      # no swaps
+    dict(G=64, I=64, P=4, W=3),                     # about one group per queue
+    dict(G=300, I=12, P=4, W=16, skewed=True),      # two rank blocks per queue
+    dict(G=160, I=3, P=3, W=200),                   # window beyond every queue
+]
+
+
+def _case(kw):
+    kw = dict(kw)
+    W = kw.pop("W")
+    rng = np.random.default_rng(zlib.crc32(("search" + str(sorted(kw.items()))).encode()))
+    pr, pl = hand_case(rng, **kw)
+    return pr, pl, W
+
+
+@pytest.mark.parametrize("kw", SEARCH_CASES, ids=[str(c) for c in SEARCH_CASES])
+def test_move_scores(qlm, orc, kw):
+    import torch
+    pr, pl, W = _case(kw)
+    print("case", kw, flush=True)
+    dpr, dpl = device_inputs(pr, pl)
+    ms = qlm.search_moves(dpr, dpl, W)
+    torch.cuda.synchronize()
+    ms = ms.cpu().numpy()
+    G, I = pr["n_groups"], pr["n_instances"]
+    assert ms.shape == (pl["n_plans"], G * W + G * I)
+    exact = 0
+    for p in range(pl["n_plans"]):
+        ref = orc.move_scores(pr, pl, p, W)
+        ok = _close(ms[p], ref)
+        bad = np.flatnonzero(~ok)
+        assert ok.all(), (p, bad[:5], ms[p][bad[:5]], ref[bad[:5]])
+        exact += int(np.sum(ms[p] == ref))
+    print("bit-identical move scores: %d of %d" % (exact, ms.size))
+
+
+def _check_search(orc, pr, pl, p, W, T, g_trace, g_steps, g_perm, g_qoff, g_ev, g_score):
+    """Compares one chain's search with the oracle's; returns the step where a
+    near-tie let the two sides part (None when they agree throughout)."""
+    G = pr["n_groups"]
+    with_flags = pl.get("evict_bits") is not None
+    o = orc.local_search(pr, pl, p, W, T)
+    ot = o["trace"]
+    diff = np.flatnonzero(g_trace != ot)
+    if diff.size == 0:
+        assert g_steps == o["steps"]
+        assert np.array_equal(g_perm, o["perm"]) and np.array_equal(g_qoff, o["qoff"])
+        if with_flags:
+            assert np.array_equal(g_ev, o["evict_bits"])
+        assert _close(g_score, o["score"]), (g_score, o["score"])
+        return None
+    t = int(diff[0])
+    # replay the common steps, then judge the GPU's choice at step t
+    perm, qoff, flag = pl["perm"][:, p].copy(), pl["qoff"][:, p].copy(), _flags(pl, p, G)
+    for k in ot[:t]:
+        perm, qoff, flag = orc.move_apply(pr, perm, qoff, flag, W, int(k))
+    one = _one(perm, qoff, flag, with_flags)
+    cur = orc.plan_detail(pr, one, 0)["score"]
+    allm = orc.move_scores(pr, one, 0, W)
+    best = float(allm.min())
+    gk = int(g_trace[t])
+    if gk >= 0:
+        # the GPU's move must be a minimum up to erfc's last bits, and an improvement
+        assert _close(allm[gk], best), (t, gk, allm[gk], best)
+        assert allm[gk] < cur or _close(allm[gk], cur)
+    else:
+        # the GPU stopped: no move may improve beyond erfc's last bits
+        assert _close(best, cur) or best >= cur, (t, best, cur)
+    return t
+
+
+@pytest.mark.parametrize("kw", SEARCH_CASES, ids=[str(c) for c in SEARCH_CASES])
+def test_local_search(qlm, orc, kw):
+    import torch
+    pr, pl, W = _case(kw)
+    T = 25
+    print("case", kw, "steps", T, flush=True)
+    dpr, dpl = device_inputs(pr, pl)
+    r = qlm.local_search(dpr, dpl, W, T, trace=True)
+    torch.cuda.synchronize()
+    out = r["plans"]
+    g_perm = out.perm.cpu().numpy()
+    g_qoff = out.qoff.cpu().numpy()
+    g_ev = None if out.evict_bits is None else out.evict_bits.cpu().numpy().view(np.uint32)
+    g_trace = r["trace"].cpu().numpy()
+    g_steps = r["steps"].cpu().numpy()
+    g_score = r["score"].cpu().numpy()
+    moved = 0
+    for p in range(pl["n_plans"]):
+        t = _check_search(orc, pr, pl, p, W, T, g_trace[p], int(g_steps[p]), g_perm[:, p],
+                          g_qoff[:, p], None if g_ev is None else g_ev[:, p], float(g_score[p]))
+        if t is not None:
+            print("plan %d: near-tie at step %d" % (p, t))
+        moved += int(g_steps[p])
+    print("moves applied over all plans:", moved)
+    # scores never rise, and the final scores are those of the final plans
+    ex = qlm.rwt_score_exact(dpr, out, np.arange(pl["n_plans"]))
+    assert np.array_equal(ex.cpu().numpy(), g_score)
+
+
+def test_search_edge_calls(qlm, orc):
+    """No steps: the start plans and their scores come back unchanged; a search
+    in place (output arrays = start arrays); plans that already meet every SLO
+    do not move."""
+    import torch
+    rng = np.random.default_rng(11)
+    pr, pl = hand_case(rng, G=50, I=4, P=5)
+    dpr, dpl = device_inputs(pr, pl)
+    r = qlm.local_search(dpr, dpl, 4, 0, trace=True)
+    torch.cuda.synchronize()
+    assert np.array_equal(r["plans"].perm.cpu().numpy(), pl["perm"])
+    assert np.array_equal(r["plans"].qoff.cpu().numpy(), pl["qoff"])
+    assert np.array_equal(r["plans"].evict_bits.cpu().numpy().view(np.uint32), pl["evict_bits"])
+    assert np.all(r["steps"].cpu().numpy() == 0)
+    osc, _ = orc.score_plans(pr, pl)
+    assert np.all(_close(r["score"].cpu().numpy(), osc))
+    # in place
+    dpl2 = device_inputs(pr, pl)[1]
+    r2 = qlm.local_search(dpr, dpl2, 4, 6, out=dpl2)
+    ref = qlm.local_search(dpr, dpl, 4, 6)
+    torch.cuda.synchronize()
+    assert torch.equal(dpl2.perm, ref["plans"].perm) and torch.equal(dpl2.qoff, ref["plans"].qoff)
+    assert torch.equal(r2["score"], ref["score"])
+    # SLOs no wait reaches: score 0, nothing moves
+    pr3 = dict(pr)
+    pr3["grp_slo"] = np.full(pr["n_groups"], 3.0e38, np.float32)
+    dpr3 = device_inputs(pr3, pl)[0]
+    r3 = qlm.local_search(dpr3, dpl, 4, 5)
+    torch.cuda.synchronize()
+    assert np.all(r3["steps"].cpu().numpy() == 0) and np.all(r3["score"].cpu().numpy() == 0.0)
+
+
+def test_search_workloads(qlm, orc):
+    """Two plans of each generated workload small enough for the oracle's
+    full neighbourhoods: all move scores, then five search steps."""
+    import torch
+    from paper_2407_00047_amd import workload
+    for name, W in (("tiny", 4), ("mixed", 8), ("hetero", 8)):
+        pr = workload.make_problem(name)
+        pl = workload.make_plans(pr, 0, 2)
+        print("workload", name, flush=True)
+        dpr, dpl = device_inputs(pr, pl)
+        ms = qlm.search_moves(dpr, dpl, W).cpu().numpy()
+        for p in range(2):
+            ref = orc.move_scores(pr, pl, p, W)
+            assert _close(ms[p], ref).all(), (name, p)
+        r = qlm.local_search(dpr, dpl, W, 5, trace=True)
+        torch.cuda.synchronize()
+        out = r["plans"]
+        for p in range(2):
+            _check_search(orc, pr, pl, p, W, 5, r["trace"].cpu().numpy()[p],
+                          int(r["steps"][p]), out.perm.cpu().numpy()[:, p],
+                          out.qoff.cpu().numpy()[:, p],
+                          None if out.evict_bits is None
+                          else out.evict_bits.cpu().numpy().view(np.uint32)[:, p],
+                          float(r["score"][p]))
+
+
+FULL = [("hetero", 16), ("heavy", 16), ("large", 16)]
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name,W", FULL, ids=[f[0] for f in FULL])
+def test_search_full_size(qlm, orc, name, W):
+    """One plan of the full workload: a sample of move scores (and the best
+    one) against the oracle, and three search steps, each move re-scored by
+    the oracle on the plan the search held at that step."""
+    import torch
+    from paper_2407_00047_amd import workload
+    pr = workload.make_problem(name)
+    pl = workload.make_plans(pr, 0, 1)
+    G, I = pr["n_groups"], pr["n_instances"]
+    print("full size", name, "G", G, "I", I, "W", W, flush=True)
+    dpr, dpl = device_inputs(pr, pl)
+    ms = qlm.search_moves(dpr, dpl, W).cpu().numpy()[0]
+    valid = np.flatnonzero(np.isfinite(ms))
+    rng = np.random.default_rng(1)
+    ks = np.concatenate([rng.choice(valid, 200, replace=False), [int(np.argmin(ms))],
+                         np.flatnonzero(~np.isfinite(ms))[:20]])
+    ref = orc.move_scores(pr, pl, 0, W, ks=ks)
+    assert _close(ms[ks], ref).all()
+    T = 3
+    r = qlm.local_search(dpr, dpl, W, T, trace=True)
+    torch.cuda.synchronize()
+    tr = r["trace"].cpu().numpy()[0]
+    assert tr[0] == int(np.argmin(ms))          # the first step takes the best move
+    perm, qoff, flag = pl["perm"][:, 0].copy(), pl["qoff"][:, 0].copy(), _flags(pl, 0, G)
+    with_flags = pl.get("evict_bits") is not None
+    cur = orc.plan_detail(pr, _one(perm, qoff, flag, with_flags), 0)["score"]
+    for t in range(T):
+        k = int(tr[t])
+        if k < 0:
+            break
+        v = orc.move_scores(pr, _one(perm, qoff, flag, with_flags), 0, W, ks=[k])[0]
+        assert v < cur
+        perm, qoff, flag = orc.move_apply(pr, perm, qoff, flag, W, k)
+        cur = v
+    out = r["plans"]
+    assert np.array_equal(out.perm.cpu().numpy()[:, 0], perm)
+    assert np.array_equal(out.qoff.cpu().numpy()[:, 0], qoff)
+    assert _close(float(r["score"][0]), cur)
