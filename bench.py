@@ -24,6 +24,14 @@ sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0
 METRIC = "candidate plans scored/sec (RWT + SLO prob) and % of HBM roofline, 1 GPU"
+SEARCH_METRIC = "plan-search moves scored/sec (exact, incremental) and % of fp64 roofline, 1 GPU"
+# MI355X vector fp64: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz instructions per
+# second (78.6 TFLOP/s counts a fused multiply-add as two).
+PEAK_F64_INSTR = 256 * 4 * 16 * 2.4e9
+# fp64 instructions of one visited position in the walk of the reassignment
+# kernel (IEEE divisions, square root, erfc and the running sums), counted in
+# its compiled loop.
+F64_PER_VISIT = 125
 
 
 def log(*a):
@@ -155,6 +163,137 @@ def cpu_baseline(problem, plans, seconds: float):
                       " %.1f s" % (count - 1, count, P, dt)}
 
 
+def move_counts(problem, plans, p, window):
+    """Valid moves of plan p (swaps within a queue, reassignments) and the
+    positions the reassignment kernel visits for them: for a group moving to
+    queue h, the walk starts at its insertion point (one position earlier when
+    that is the end of a non-empty queue) and runs to the end of h."""
+    import numpy as np
+    G, I = problem["n_groups"], problem["n_instances"]
+    perm = plans["perm"][:, p]
+    qoff = plans["qoff"][:, p]
+    slo = np.asarray(problem["grp_slo"], np.float32)
+    lens = np.diff(qoff)
+    swaps = int(sum(max(int(L) - d, 0) for L in lens for d in range(1, window + 1)))
+    moves = G * (I - 1)
+    owner = np.repeat(np.arange(I), lens)
+    g_of = np.empty(G, np.int64)
+    g_of[perm] = owner
+    visits = 0
+    for h in range(I):
+        b, e = int(qoff[h]), int(qoff[h + 1])
+        x = slo[g_of != h]
+        if e == b:
+            visits += x.size
+            continue
+        pmax = np.maximum.accumulate(slo[perm[b:e]])
+        pos = np.searchsorted(pmax, x, side="right")          # first pmax > slo
+        visits += int(np.sum((e - b) - pos + 1 + (pos == e - b)))
+    return swaps + moves, moves, visits
+
+
+def cpu_search_baseline(problem, plans, window, seconds: float):
+    import numpy as np
+    import oracle
+    orc = oracle.default()
+    ms = np.arange(orc.n_moves(problem["n_groups"], problem["n_instances"], window))
+    rng = np.random.default_rng(0)
+    n0 = 64
+    t0 = time.perf_counter()
+    orc.move_scores(problem, plans, 0, window, ks=rng.choice(ms, n0, replace=False))
+    dt = max(time.perf_counter() - t0, 1e-6)
+    n = int(min(ms.size, max(n0, seconds * n0 / dt)))
+    ks = rng.choice(ms, n, replace=False)
+    t0 = time.perf_counter()
+    sc = orc.move_scores(problem, plans, 0, window, ks=ks)
+    dt = time.perf_counter() - t0
+    valid = int(np.sum(np.isfinite(sc)))
+    return {"value": valid / dt, "unit": "moves/s", "cores": orc.max_threads(), "kind": "oracle",
+            "sample": "%d move numbers drawn at random from plan 0's neighbourhood (%d valid "
+                      "moves), each moved plan built and scored from scratch by the fp64 C oracle, "
+                      "all host threads, %.1f s" % (n, valid, dt)}
+
+
+def bench_search(args):
+    """One step = one step of the local search on every chain: cache the plan,
+    score every move exactly (swaps, then reassignments), pick and apply."""
+    import torch
+    from paper_2407_00047_amd import qlm, workload
+    dev = torch.device("cuda:0")
+    B, W, K = args.chains, args.window, args.steps
+    pr = workload.make_problem(args.config)
+    pl = workload.make_plans(pr, 0, B)
+    G, I = pr["n_groups"], pr["n_instances"]
+    dpr = qlm.DeviceProblem(pr, device=dev)
+    dpl = qlm.DevicePlans.from_host(pl, device=dev)
+    ws = qlm.search_workspace(dpr, B, W, device=dev)
+    nm = qlm.search_n_moves(G, I, W)
+    counts = [move_counts(pr, pl, p, W) for p in range(B)]
+    valid = sum(c[0] for c in counts)
+    visits = sum(c[2] for c in counts)
+    log("search %s: G=%d I=%d chains=%d window=%d, %d valid moves per step" % (
+        args.config, G, I, B, W, valid))
+    out = qlm.DevicePlans(torch.empty_like(dpl.perm), torch.empty_like(dpl.qoff),
+                          None if dpl.evict_bits is None else torch.empty_like(dpl.evict_bits), B)
+    for _ in range(max(args.warmup, 1)):
+        r = qlm.local_search(dpr, dpl, W, K, ws=ws, out=out)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    qlm.timing_enable(True)
+    qlm.timing_read()
+    e0.record(stream)
+    r = qlm.local_search(dpr, dpl, W, K, ws=ws, out=out)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    n_search, ms_search = qlm.timing_read()
+    total_ms = e0.elapsed_time(e1)
+    steps = r["steps"].cpu().numpy()
+    applied = int(steps.sum())
+    # the reassignment kernel on the start plans (the positions it visits are
+    # known exactly there), timed over repeated launches
+    ms_scores = torch.empty((B, nm), dtype=torch.float64, device=dev)
+    reps = 10
+    qlm.search_moves(dpr, dpl, W, ws=ws, out=ms_scores)
+    torch.cuda.synchronize()
+    qlm.timing_read()
+    for _ in range(reps):
+        qlm.search_moves(dpr, dpl, W, ws=ws, out=ms_scores)
+    torch.cuda.synchronize()
+    n_launch, k_ms = qlm.timing_read()
+    qlm.timing_enable(False)
+    k_avg = k_ms / max(n_launch, 1)
+    achieved = visits / (k_avg / 1e3) / 1e9
+    peak = PEAK_F64_INSTR / F64_PER_VISIT / 1e9
+    roofline = {"bound": "alu", "achieved": round(achieved, 2), "peak": round(peak, 2),
+                "unit": "Gvisits/s", "frac": round(achieved / peak, 4), "traffic": None,
+                "kernel": "k_smove", "kernel_avg_ms": round(k_avg, 4),
+                "kernel_avg_ms_in_search": round(ms_search / max(n_search, 1), 4),
+                "visits_per_launch": visits, "f64_instr_per_visit": F64_PER_VISIT}
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle ...")
+        cpu = cpu_search_baseline(pr, pl, W, args.cpu_seconds)
+    ms_step = total_ms / K
+    N = workload.total_requests(pr)
+    res = {
+        "metric": SEARCH_METRIC, "value": round(valid * K / (total_ms / 1e3), 1),
+        "unit": "moves/s", "n_gpus": 1, "steps": K, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+        "config": {"workload": "plan search on %s: %d groups (%d requests), %d instances, "
+                               "%d start plans, window %d, %d valid moves per plan and step"
+                               % (args.config, G, N, I, B, W, valid // B),
+                   "chains": B, "window": W, "groups": G, "instances": I,
+                   "moves_per_step": valid},
+        "moves_applied": applied,
+        "score_start_to_end": [float(x) for x in r["score"].cpu().numpy()[:4]],
+        "roofline": roofline, "cpu_baseline": cpu,
+    }
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -167,6 +306,10 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run a plain 1 GiB device copy (for HBM counter scaling) and exit")
+    ap.add_argument("--search", action="store_true",
+                    help="benchmark the plan search (local search steps) instead")
+    ap.add_argument("--chains", type=int, default=1, help="--search: start plans")
+    ap.add_argument("--window", type=int, default=16, help="--search: swap window")
     ap.add_argument("--summarize-counters", nargs=4, metavar=("FETCH", "WRITE", "COPY_FETCH", "COPY_WRITE"),
                     help="rocprofv3 --pmc output folders: write the traffic summary and exit")
     args = ap.parse_args()
@@ -195,6 +338,9 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     qlm.library()
+    if args.search:
+        bench_search(args)
+        return
 
     cfg = workload.CONFIGS[args.config]
     P = cfg["P"] if args.plans is None else args.plans

@@ -244,11 +244,13 @@ const char *qlm_status_string(int status);
 const char *qlm_last_error(void);
 
 /*
- * Optional launch timing for benchmarks: when enabled, the scoring kernel of
- * every qlm_rwt_score / qlm_best_plan call is bracketed by HIP events on the
- * call's stream.  qlm_timing_read waits for the recorded events and returns
- * the number of scoring launches and their summed duration in milliseconds
- * since the last reset, then resets.
+ * Optional launch timing for benchmarks: when enabled, the dominant kernel of
+ * each call is bracketed by HIP events on the call's stream: the plan-scoring
+ * kernel of every qlm_rwt_score / qlm_best_plan call, and the kernel that
+ * scores the reassignment moves in every qlm_search_moves call and every step
+ * of qlm_local_search.  qlm_timing_read waits for the recorded events and
+ * returns the number of timed launches and their summed duration in
+ * milliseconds since the last reset, then resets.
  */
 int qlm_timing_enable(int on);
 int qlm_timing_read(int64_t *launches, double *total_ms);

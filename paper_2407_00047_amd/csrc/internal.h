@@ -18,4 +18,12 @@ int hip_fail(hipError_t e, const char *what);
 int check_problem(const qlm_problem *pr);
 int check_plans(const qlm_problem *pr, const qlm_plans *pl);
 
+// Launch timing (qlm_timing_enable): a launch bracketed by two HIP events on
+// its stream when timing is on; the pair is queued for qlm_timing_read.
+struct TimedLaunch {
+    hipEvent_t e0, e1;
+};
+int timing_begin(hipStream_t stream, TimedLaunch *t);
+void timing_end(hipStream_t stream, TimedLaunch *t);
+
 }  // namespace qlm_internal

@@ -1235,6 +1235,29 @@ int check_plans(const qlm_problem *pr, const qlm_plans *pl)
     return QLM_OK;
 }
 
+// Launch timing (benchmarks only)
+std::atomic<bool> g_timing{false};
+std::mutex g_timing_mu;
+std::vector<std::pair<hipEvent_t, hipEvent_t>> g_events;
+
+int timing_begin(hipStream_t stream, TimedLaunch *t)
+{
+    t->e0 = t->e1 = nullptr;
+    if (!g_timing.load()) return QLM_OK;
+    if (hipEventCreate(&t->e0) != hipSuccess || hipEventCreate(&t->e1) != hipSuccess)
+        return fail(QLM_ERR_HIP, "hipEventCreate");
+    (void)hipEventRecord(t->e0, stream);
+    return QLM_OK;
+}
+
+void timing_end(hipStream_t stream, TimedLaunch *t)
+{
+    if (!t->e0) return;
+    (void)hipEventRecord(t->e1, stream);
+    std::lock_guard<std::mutex> lk(g_timing_mu);
+    g_events.emplace_back(t->e0, t->e1);
+}
+
 }  // namespace qlm_internal
 
 namespace {
@@ -1330,10 +1353,6 @@ ExactArgs exact_args(const qlm_problem *pr, const qlm_plans *pl)
     return a;
 }
 
-// Launch timing (benchmarks only)
-std::atomic<bool> g_timing{false};
-std::mutex g_timing_mu;
-std::vector<std::pair<hipEvent_t, hipEvent_t>> g_events;
 
 using ScoreKernel = void (*)(ScoreArgs);
 
@@ -1455,21 +1474,13 @@ int launch_score(const qlm_problem *pr, const qlm_plans *pl, double *score, doub
     if (rc) return rc;
     if (grid_out) *grid_out = grid;
 
-    hipEvent_t e0 = nullptr, e1 = nullptr;
-    const bool timing = g_timing.load();
-    if (timing) {
-        if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess)
-            return fail(QLM_ERR_HIP, "hipEventCreate");
-        (void)hipEventRecord(e0, stream);
-    }
+    qlm_internal::TimedLaunch tl;
+    rc = qlm_internal::timing_begin(stream, &tl);
+    if (rc) return rc;
     hipLaunchKernelGGL(k, dim3(grid), dim3(kScoreThreads), geo.lds_bytes, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "k_score launch");
-    if (timing) {
-        (void)hipEventRecord(e1, stream);
-        std::lock_guard<std::mutex> lk(g_timing_mu);
-        g_events.emplace_back(e0, e1);
-    }
+    qlm_internal::timing_end(stream, &tl);
     return QLM_OK;
 }
 
@@ -1679,7 +1690,7 @@ const char *qlm_last_error(void) { return qlm_internal::t_err.c_str(); }
 
 int qlm_timing_enable(int on)
 {
-    g_timing.store(on != 0);
+    qlm_internal::g_timing.store(on != 0);
     return QLM_OK;
 }
 
@@ -1687,8 +1698,8 @@ int qlm_timing_read(int64_t *launches, double *total_ms)
 {
     std::vector<std::pair<hipEvent_t, hipEvent_t>> ev;
     {
-        std::lock_guard<std::mutex> lk(g_timing_mu);
-        ev.swap(g_events);
+        std::lock_guard<std::mutex> lk(qlm_internal::g_timing_mu);
+        ev.swap(qlm_internal::g_events);
     }
     double tot = 0.0;
     int rc = QLM_OK;

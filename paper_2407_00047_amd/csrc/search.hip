@@ -805,9 +805,13 @@ int score_moves(SearchArgs &a, hipStream_t stream)
     hipLaunchKernelGGL(k_sswap, dim3((unsigned)(a.nwg_a * a.B)), dim3(kTaskThreads), 0, stream, a);
     int rc = launched("k_sswap launch");
     if (rc) return rc;
+    qlm_internal::TimedLaunch tl;
+    if ((rc = qlm_internal::timing_begin(stream, &tl))) return rc;
     hipLaunchKernelGGL(k_smove, dim3((unsigned)((int64_t)a.I * a.nwg_b * a.B)), dim3(kTaskThreads),
                        0, stream, a);
-    return launched("k_smove launch");
+    if ((rc = launched("k_smove launch"))) return rc;
+    qlm_internal::timing_end(stream, &tl);
+    return QLM_OK;
 }
 
 }  // namespace
