@@ -218,10 +218,28 @@ int qlm_search_moves(const qlm_problem *problem, const qlm_plans *plans, int32_t
                      void *ws, size_t ws_bytes, double *move_score, qlm_stream stream);
 
 /*
+ * Screened scores of every move, the first stage of every qlm_local_search
+ * step: score [P][n_moves] and bound [P][n_moves] device out, plan-major like
+ * qlm_search_moves.  For every move |score - exact score| <= bound, where the
+ * exact score is the one qlm_search_moves returns.  The screen walks a move's
+ * target queue from cached waits and variances with the normal tail read from
+ * the table of qlm_rwt_score; its bound is 8e-6 times the requests of that
+ * queue plus 1e-12 of the scores.  bound = +inf marks a move the screen cannot
+ * bound (a spread too small for the rounding of its margin; the search scores
+ * it exactly); score = +inf with bound 0 where k names no move.
+ */
+int qlm_search_screen(const qlm_problem *problem, const qlm_plans *plans, int32_t window,
+                      void *ws, size_t ws_bytes, double *score, double *bound,
+                      qlm_stream stream);
+
+/*
  * Steepest-descent local search from every start plan, independently: each
  * step scores every move, takes the lowest score (the lowest k on ties) and
  * applies it when it is strictly below the current plan's score; otherwise
- * that plan has converged and stops.  At most max_steps steps.
+ * that plan has converged and stops.  At most max_steps steps.  Each step
+ * screens every move (qlm_search_screen), scores exactly only the moves that
+ * can still be the lowest and improve, and decides on the exact scores, so
+ * the steps are those of a search that scores every move exactly.
  *   start   the start plans (read before any output is written, so `out` may
  *           name the same arrays)
  *   out     the final plans

@@ -37,6 +37,7 @@
 
 #include "internal.h"
 #include "qlm.h"
+#include "tail.h"
 
 namespace {
 
@@ -60,23 +61,16 @@ constexpr uint32_t kColMask = 0x7F8u;     // model * 8: byte column of the cost 
 // below 1.9e-6 of their total), with margin.
 constexpr double kEpsP = 8e-6;
 
-// Normal upper tail Q(z) = erfc(z / sqrt 2) / 2 as a table of 1024 linear
-// cells over z in [-6, 6] (beyond, Q is within 1e-9 of 0 or 1).  The kernel
-// forms t = 1536 - (1024 / 12) z in single precision and clamps it to
-// [1024, 2048): there every float has exponent 10, so the ten leading mantissa
-// bits are the cell.  Cell k holds the line that best fits Q over its width
-// (the chord, moved by half its largest deviation), as (a, b) with
-// Q ~ a + b t; the two end cells are the constants 0 and 1.
-constexpr int kTailCells = 1024;
-constexpr double kTailZ = 6.0;
-constexpr double kTailScale = kTailCells / (2.0 * kTailZ);          // cells per unit z
-constexpr float kTailMid = 1536.0f;
-constexpr float kTailLo = 1024.0f;
-constexpr float kTailHi = 2047.9998779296875f;                     // 2048 - 2^-13
-constexpr uint32_t kTailCellBits = 0x7FE000u;                      // mantissa bits 22..13
+// Normal upper tail as a table of linear cells (tail.h).
+constexpr int kTailCells = qlm_tail::kCells;
+constexpr double kTailScale = qlm_tail::kScale;
+constexpr float kTailMid = qlm_tail::kMid;
+constexpr float kTailLo = qlm_tail::kLo;
+constexpr float kTailHi = qlm_tail::kHi;
+constexpr uint32_t kTailCellBits = qlm_tail::kCellBits;
 // Variances are staged multiplied by 1 / kTailScale^2, so that the reciprocal
 // square root of the running sum is already in cells per unit of margin.
-constexpr double kVarScale = 1.0 / (kTailScale * kTailScale);
+constexpr double kVarScale = qlm_tail::kVarScale;
 
 struct ScoreArgs {
     int32_t G, I, M, C;
@@ -204,27 +198,7 @@ __device__ void stage_tail(float2 *tab)
 {
     // a fixed trip count (the kernel runs kScoreThreads threads): no loop whose
     // exit depends on the thread, after which uniform values would turn divergent
-    static_assert(kTailCells % kScoreThreads == 0, "tail cells per thread");
-#pragma unroll
-    for (int k0 = 0; k0 < kTailCells; k0 += kScoreThreads) {
-        const int k = k0 + (int)threadIdx.x;
-        const double r2 = 0.70710678118654752440;
-        const double p0 = 0.5 * erfc((512.0 - k) / kTailScale * r2);
-        const double p1 = 0.5 * erfc((511.0 - k) / kTailScale * r2);
-        const double pm = 0.5 * erfc((511.5 - k) / kTailScale * r2);
-        double c1 = p1 - p0;
-        double c0 = p0 + 0.5 * (pm - 0.5 * (p0 + p1));
-        // the end cells are flat at exactly 0 and 1 (their Q is within 2e-9 of it),
-        // so that clamped margins give exact zero and one terms
-        if (k == 0 || k == kTailCells - 1) {
-            c0 = k == 0 ? 0.0 : 1.0;
-            c1 = 0.0;
-        }
-        // the line in t itself (c0 - c1 (1024 + k) + c1 t): no fraction to form
-        // in the kernel; the constant is at most 9.6 in size, so its rounding adds
-        // below 6e-7
-        tab[k] = make_float2((float)(c0 - c1 * (kTailLo + k)), (float)c1);
-    }
+    qlm_tail::build<kScoreThreads>(tab);
 }
 
 __device__ inline double wave_min(double v)

@@ -1,6 +1,6 @@
 // search.hip -- plan search on the GPU: steepest-descent local search over
-// virtual-queue plans, every move scored exactly (double precision) and
-// incrementally.  Interface: qlm_search_* and qlm_local_search in include/qlm.h.
+// virtual-queue plans.  Interface: qlm_search_* and qlm_local_search in
+// include/qlm.h.
 //
 // Moves are the scheduler's actions on virtual queues (reordering within a
 // queue, reassignment to another instance: Sec. 5); the paper itself places
@@ -12,30 +12,61 @@
 //                                   is strictly later (else at the end)
 // A moved group keeps its eviction flag.
 //
-// Incremental scoring.  A move changes at most two queues, each from one
-// position on.  For every chain (a plan being improved) k_sstate caches, per
-// slot, the running sums ahead of it (tokens A, variance V, fixed costs K up
-// to the previous slot, and the score C of the slots ahead in its queue), and
-// the score of every queue.  A move restarts the sums at its first changed
-// position and walks the rest of the queue; the operations and their order are
-// those of scoring the moved plan from its first slot (positions in order,
-// then queues in order), so a move's score is exactly the plan score of the
-// moved plan.
+// Exact scores.  A move changes at most two queues, each from one position
+// on.  For every chain (a plan being improved) k_sstate caches, per slot, the
+// running sums ahead of it (tokens A, variance V, fixed costs K, the score C
+// of the slots ahead in its queue) and the score of every queue.  An exact
+// move score restarts the sums at the first changed position and walks the
+// rest of the queue with the operations, in the order, of scoring the moved
+// plan from its first slot (positions in order, then queues in order): it is
+// the plan score of the moved plan, bit for bit.
+//
+// Screened steps.  A search step needs the exact score of the best move only.
+// Every move is first screened: past the positions it changes, a queue is the
+// old queue shifted by constants (the moved group's tokens and variance, the
+// change of fixed costs), so each later position costs one subtraction from
+// its cached margin slo - E[W] and one lookup in the linear-cell table of the
+// normal tail (tail.h).  The screened score F has a proven bound D on its
+// distance to the exact score (below); the moves whose exact score can still
+// be the lowest, F - D <= min(F + D), and can still improve on the plan, are
+// re-scored exactly, one wavefront per move, and the lowest exact score (the
+// lowest k on ties) decides.  The search takes the same steps as one that
+// scores every move exactly.
+//
+// Screening bound, per request of the queue the screen walks: the table is
+// within 2.2e-6 of Q; single-precision rounding of the margin, the scaled
+// variance, the cell coordinate and n P adds below 1.5e-6; so D = 8e-6 times
+// the requests of that queue, plus 1e-12 of the scores for double rounding.
+// The margin itself is formed in double precision from cached sums, which may
+// differ from the exact score's own sums in their last bits; a move whose
+// smallest spread is so small that this could move z by more than 1e-7 gets
+// D = infinity (re-scored exactly), as does one whose walk meets a variance
+// that single precision cannot hold.  A queue that loses the moved group is
+// screened with its variance ahead in double precision (no cancellation), and
+// a MOVE's bound adds the bounds of both its queues.  Exact scores (of the
+// candidates) walk both queues exactly.
 //
 // Kernels
-//   k_sprep    once per call: 32-byte group records; the groups ranked by SLO
-//   k_sload    the start plans, slot-major -> chain-major working copies
-//   k_sstate   one workgroup per chain: the cache above, per-queue scores and
-//              their running sum over queues (= the plan score)
-//   k_sswap    one lane per (chain, slot s, d = 0..W): d = 0 scores the queue
-//              of s without s (a MOVE's source queue), d >= 1 SWAP(s, d)
-//   k_smove    one lane per (chain, target queue h, group rank r by SLO):
-//              MOVE(slot of that group, h).  Adjacent lanes hold groups of
-//              adjacent SLOs, so their insertion points and walks are alike.
-//   k_spick    one workgroup per chain: lowest (score, k) over all moves;
-//              applied when strictly below the plan's score, else the chain
-//              has converged and every later kernel skips it
+//   k_srank    once per call: group records; the groups ranked by SLO
+//   k_stail    once per call: the normal-tail table, which the screens copy
+//              into LDS
+//   k_sload    start plans, slot-major -> chain-major working copies
+//   k_sstate   one wavefront per queue: slot records, the exact running sums,
+//              the cached margins, the queue score (k_stotal: their sum)
+//   k_fswap    one lane per task: the screened score of the queue of each slot
+//              s without s (for the MOVEs of s), and screened SWAP(s, d); the
+//              positions past the changes are walked in step by the wavefront
+//   k_fmove    one wavefront per (target queue h, 64 groups adjacent in SLO
+//              order): screened MOVE; the positions past the insertion points
+//              are walked in step by the whole wavefront (one record read per
+//              position for all 64 moves)
+//   k_sbound / k_sselect / k_sexact   the bound min(F + D), the candidates,
+//              their exact scores
+//   k_spick    lowest (exact score, k) of the candidates; applied when it
+//              improves on the plan, else the chain has converged
 //   k_sout     final plans back to the caller's slot-major layout
+//   k_sswap / k_smove   exact scores of every move, one lane per move
+//              (qlm_search_moves)
 #include <hip/hip_runtime.h>
 
 #include <climits>
@@ -45,6 +76,7 @@
 
 #include "internal.h"
 #include "qlm.h"
+#include "tail.h"
 
 namespace {
 
@@ -52,17 +84,19 @@ using qlm_internal::fail;
 using qlm_internal::hip_fail;
 
 constexpr int kWave = 64;
-constexpr int kStateThreads = 1024;
-constexpr int kTaskThreads = 256;
-constexpr int kPickThreads = 256;
-constexpr int kPrepThreads = 256;
+constexpr int kThreads = 256;              // every search kernel: 4 wavefronts
+constexpr int kWaves = kThreads / kWave;
 constexpr int kRankTile = 1024;
+constexpr int kExactBlocks = 64;           // per chain, for the exact re-scores
+constexpr int kStage = 1024;               // tail records staged in LDS at a time
 constexpr int32_t kMaxSearchGroups = 1 << 16;
 constexpr int32_t kMaxSearchInstances = 4096;
 constexpr int32_t kMaxWindow = 1024;
 constexpr uint32_t kCountMask = (1u << 21) - 1u;
 constexpr uint32_t kFlagBit = 1u << 8;
 constexpr int kCountShift = 9;
+constexpr double kEpsP = 8e-6;             // screening bound per request
+constexpr double kZErr = 1e-7;             // largest z error from the margin's rounding
 
 // Group record: n mu and n sigma^2 (exact products of the fp32 inputs in
 // double), SLO, and n << 9 | model.
@@ -91,6 +125,15 @@ struct SSt {
     double A, V, K, C;
 };
 
+// What a screen reads at a position past the change: the margin slo - E[W]
+// (seconds), the variance ahead scaled for the tail table (V / Theta^2 times
+// kVarScale, single precision), and the request count.
+struct TRec {
+    double m;
+    float vz;
+    float n;
+};
+
 struct SearchArgs {
     int32_t G, I, M, C, W;
     int64_t B;                    // chains
@@ -103,6 +146,7 @@ struct SearchArgs {
     float evict_cost;
     GRec *grec;                   // [G]
     int32_t *by_slo;              // [G] groups in SLO order
+    float2 *tail;                 // [kCells] the normal-tail table (tail.h)
     // per chain, chain b at b * (per-chain size)
     int32_t *perm;                // [G]
     uint8_t *flag;                // [G]
@@ -110,17 +154,29 @@ struct SearchArgs {
     int32_t *inv;                 // [G] slot of each group
     SRec *srec;                   // [G]
     SSt *sst;                     // [G]
-    double *R;                    // [G] score of the queue of s without s
+    TRec *trec;                   // [G]
+    double *R;                    // [G] score of the queue of s without s (exact in
+                                  // the exact kernels, screened in the screens)
+    double *RD;                   // [G] bound of the screened one
     double *Q;                    // [I] queue scores
+    double *Nq;                   // [I] requests per queue
+    double *Es;                   // [I] largest |E[W]| + |slo| in the queue
     double *T;                    // [I + 1] running sum of queue scores
     double *cur;                  // [1] plan score
     int32_t *done, *steps;        // [1] each
-    double *wmin_s;               // [nwg] workgroup minima of the move scores
+    double *wmin_s;               // [nwg] exact kernels: workgroup minima
     int64_t *wmin_i;              // [nwg] and their move numbers
+    double *smin;                 // [nws] screens: workgroup minima of F + D
+    double *F, *D;                // [n_moves] screened scores and their bounds
+    int32_t *cand;                // [n_moves] candidate moves
+    double *cex;                  // [n_moves] their exact scores
+    int32_t *ncand;               // [1]
+    double *U;                    // [1] min(F + D)
     int32_t *scratch;             // [2 G] shifts of k_spick
     int32_t nwg_a, nwg_b, nwg;    // per chain: k_sswap, k_smove (per queue), total
+    int32_t nwg_f, nws;           // per chain: k_fswap (d = 0..W), all screen workgroups
     int64_t n_moves;
-    double *move_score;           // [B][n_moves] or null
+    double *move_score;           // [B][n_moves] or null (exact kernels)
     int64_t *trace;               // [B][max_steps] or null
     int32_t max_steps;
 };
@@ -137,6 +193,58 @@ __device__ inline uint32_t order_key(float f)
 {
     const uint32_t u = __float_as_uint(f);
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// Lane j's value (j the same in every lane).
+__device__ inline double lane_value(double v, int j)
+{
+    const int hi = __builtin_amdgcn_readlane(__double2hiint(v), j);
+    const int lo = __builtin_amdgcn_readlane(__double2loint(v), j);
+    return __hiloint2double(hi, lo);
+}
+
+// This thread's wavefront within its workgroup, as a value the compiler
+// knows to be the same in every lane (loops over it stay scalar).
+__device__ inline int wave_id() { return __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave)); }
+
+__device__ inline double wave_min(double v)
+{
+    for (int o = kWave / 2; o > 0; o >>= 1) v = fmin(v, __shfl_xor(v, o, kWave));
+    return v;
+}
+
+__device__ inline double wave_max(double v)
+{
+    for (int o = kWave / 2; o > 0; o >>= 1) v = fmax(v, __shfl_xor(v, o, kWave));
+    return v;
+}
+
+__device__ inline double wave_sum(double v)
+{
+    for (int o = kWave / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+    return v;
+}
+
+// Workgroup minimum; the result is valid in thread 0.
+__device__ inline double block_min(double v, double *lmin)
+{
+    v = wave_min(v);
+    if ((threadIdx.x & (kWave - 1)) == 0) lmin[threadIdx.x / kWave] = v;
+    __syncthreads();
+    if (threadIdx.x == 0)
+        for (int w = 1; w < kWaves; ++w) v = fmin(v, lmin[w]);
+    return v;
+}
+
+// Workgroup minimum of an int, valid in every thread.
+__device__ inline int block_min_int(int v, int *lint)
+{
+    for (int o = kWave / 2; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o, kWave));
+    __syncthreads();
+    if ((threadIdx.x & (kWave - 1)) == 0) lint[threadIdx.x / kWave] = v;
+    __syncthreads();
+    for (int w = 0; w < kWaves; ++w) v = min(v, lint[w]);
+    return v;
 }
 
 #pragma clang fp contract(off)
@@ -213,7 +321,6 @@ __device__ inline bool better(double s, int64_t k, double s2, int64_t k2)
 }
 
 // Workgroup minimum of (score, k); the result is valid in thread 0.
-template <int kThreads>
 __device__ void block_best(double &s, int64_t &k, double *ls, int64_t *lk)
 {
     for (int o = kWave / 2; o > 0; o >>= 1) {
@@ -231,7 +338,7 @@ __device__ void block_best(double &s, int64_t &k, double *ls, int64_t *lk)
     }
     __syncthreads();
     if (threadIdx.x == 0) {
-        for (int w = 1; w < kThreads / kWave; ++w)
+        for (int w = 1; w < kWaves; ++w)
             if (better(ls[w], lk[w], s, k)) {
                 s = ls[w];
                 k = lk[w];
@@ -239,50 +346,179 @@ __device__ void block_best(double &s, int64_t &k, double *ls, int64_t *lk)
     }
 }
 
-// ---------------------------------------------------------------------------
-
-__global__ __launch_bounds__(kPrepThreads) void k_sprep(SearchArgs a)
+// Lane l receives lane l - 1's value (DPP wave_shr:1); lane 0 keeps its own.
+__device__ inline double from_left(double v)
 {
-    __shared__ uint32_t keys[kRankTile];
+    const int lo = __double2loint(v), hi = __double2hiint(v);
+    return __hiloint2double(__builtin_amdgcn_update_dpp(hi, hi, 0x138, 0xF, 0xF, false),
+                            __builtin_amdgcn_update_dpp(lo, lo, 0x138, 0xF, 0xF, false));
+}
+
+// The same, with zero in lane 0.
+__device__ inline double from_left0(double v)
+{
+    const int lo = __double2loint(v), hi = __double2hiint(v);
+    return __hiloint2double(__builtin_amdgcn_update_dpp(0, hi, 0x138, 0xF, 0xF, false),
+                            __builtin_amdgcn_update_dpp(0, lo, 0x138, 0xF, 0xF, false));
+}
+
+// The exact walk of nv positions by one wavefront (visit() in effect for each
+// position in turn, with the same operations in the same order).  Position v
+// holds the record rec(v); the sums start from r, which every lane holds, and
+// end there.  64 positions at a time, one per lane: the running sums ripple
+// from lane to lane (at each of up to 63 steps every lane takes its left
+// neighbour's sum and adds its left neighbour's input), which forms each
+// lane's sums in position order exactly as a serial walk does; then each lane
+// forms its probability, and the terms ripple the same way.  A lane adds its
+// own model-change and eviction costs to the costs it receives (adding a zero
+// cost leaves a sum unchanged).  out(v, x, A, V, K, C, E) receives each
+// position's sums on entry, its score ahead C and its E[W] (in the lane that
+// holds the position).
+template <class RecOf, class Out>
+__device__ void wave_walk(Run &r, int nv, const RecOf &rec, double theta, int cls,
+                          const SearchArgs &a, const Out &out)
+{
+    const int lane = threadIdx.x & (kWave - 1);
+    const double ecost = (double)a.evict_cost;
+    for (int v0 = 0; v0 < nv; v0 += kWave) {
+        const int cnt = min(kWave, nv - v0);
+        const bool on = lane < cnt;
+        SRec x{};
+        if (on) x = rec(v0 + lane);
+        const int m = (int)(x.nmf & 0xFFu);
+        int pm = __shfl_up(m, 1, kWave);
+        if (lane == 0) pm = r.prev;
+        double c1 = 0.0;
+        if (on && pm >= 0 && pm != m && a.swap_cost)
+            c1 = (double)a.swap_cost[((int64_t)cls * a.M + pm) * a.M + m];
+        const double c2 = (on && (x.nmf & kFlagBit)) ? ecost : 0.0;
+        // inputs of the left neighbour (zero in lane 0, whose sums stay at r)
+        const double la = from_left0(x.a);
+        const double lb = from_left0(x.b);
+        const double l1 = from_left0(c1);
+        const double l2 = from_left0(c2);
+        double A = r.A, V = r.V, K0 = r.K;     // K0: costs before this position's own
+        for (int j = 1; j < cnt; ++j) {
+            A = from_left(A) + la;
+            V = from_left(V) + lb;
+            K0 = (from_left(K0) + l1) + l2;
+        }
+        double K = K0 + c1;
+        K = K + c2;
+        double term = 0.0, E = 0.0;
+        if (on) {
+            E = A / theta + K;
+            const double SD = sqrt(V) / theta;
+            const double slo = (double)x.slo;
+            double P;
+            if (SD > 0.0)
+                P = 0.5 * erfc((slo - E) / (SD * 1.4142135623730951));
+            else
+                P = (E > slo) ? 1.0 : 0.0;
+            term = (double)(x.nmf >> kCountShift) * P;
+        }
+        const double lt = from_left0(term);
+        double C = r.sc;
+        for (int j = 1; j < cnt; ++j) C = from_left(C) + lt;
+        const int last = cnt - 1;
+        r.A = lane_value(A, last) + lane_value(x.a, last);
+        r.V = lane_value(V, last) + lane_value(x.b, last);
+        r.K = lane_value(K, last);
+        r.sc = lane_value(C, last) + lane_value(term, last);
+        r.prev = __builtin_amdgcn_readlane(m, last);
+        if (on) out(v0 + lane, x, A, V, K, C, E);
+    }
+}
+
+struct NoOut {
+    __device__ void operator()(int, const SRec &, double, double, double, double, double) const {}
+};
+
+// Plan score with queue g's score replaced by qg (queues summed in order).
+__device__ inline double total_with(const double *T, const double *Q, int I, int g, double qg)
+{
+    double t = T[g] + qg;
+    for (int q = g + 1; q < I; ++q) t += Q[q];
+    return t;
+}
+
+// Plan score with queues g and h (g != h) replaced by rg and nh.
+__device__ inline double total_with2(const double *T, const double *Q, int I, int g, double rg,
+                                     int h, double nh)
+{
+    const int lo = g < h ? g : h;
+    double t = T[lo];
+    for (int q = lo; q < I; ++q) t += q == g ? rg : (q == h ? nh : Q[q]);
+    return t;
+}
+
+// ---------------------------------------------------------------------------
+// Set-up
+
+// Group records, and each group's rank in (SLO, id) order.  A workgroup takes
+// 64 groups; its four wavefronts count a quarter of the keys each.
+__global__ __launch_bounds__(kThreads) void k_srank(SearchArgs a)
+{
+    __shared__ __align__(16) uint32_t keys[kRankTile];
+    __shared__ int part[kThreads];
     const int G = a.G;
-    const int i = blockIdx.x * kPrepThreads + threadIdx.x;
+    const int li = threadIdx.x & (kWave - 1), quarter = threadIdx.x / kWave;
+    const int i = blockIdx.x * kWave + li;
     uint32_t mine = 0;
     if (i < G) {
-        const uint32_t n = (uint32_t)clampi(a.grp_count[i], 0, (int)kCountMask);
-        const double dn = (double)n;
-        GRec r;
-        r.a = dn * (double)a.grp_mu[i];
-        r.b = dn * (double)a.grp_var[i];
-        r.slo = a.grp_slo[i];
-        r.nm = (n << kCountShift) | (uint32_t)clampi(a.grp_model[i], 0, a.M - 1);
-        r.pad[0] = r.pad[1] = 0u;
-        a.grec[i] = r;
-        mine = order_key(r.slo);
-    }
-    // rank = groups ordered before i by (SLO, id)
-    int rank = 0;
-    for (int t0 = 0; t0 < G; t0 += kRankTile) {
-        __syncthreads();
-        for (int k = threadIdx.x; k < kRankTile; k += kPrepThreads)
-            keys[k] = t0 + k < G ? order_key(a.grp_slo[t0 + k]) : 0xFFFFFFFFu;
-        __syncthreads();
-        const int n = min(kRankTile, G - t0);
-        for (int k = 0; k < n; ++k) {
-            const uint32_t o = keys[k];
-            rank += (o < mine || (o == mine && t0 + k < i)) ? 1 : 0;
+        mine = order_key(a.grp_slo[i]);
+        if (quarter == 0) {
+            const uint32_t n = (uint32_t)clampi(a.grp_count[i], 0, (int)kCountMask);
+            const double dn = (double)n;
+            GRec r;
+            r.a = dn * (double)a.grp_mu[i];
+            r.b = dn * (double)a.grp_var[i];
+            r.slo = a.grp_slo[i];
+            r.nm = (n << kCountShift) | (uint32_t)clampi(a.grp_model[i], 0, a.M - 1);
+            r.pad[0] = r.pad[1] = 0u;
+            a.grec[i] = r;
         }
     }
-    if (i < G) a.by_slo[rank] = i;
+    int cnt = 0;
+    for (int t0 = 0; t0 < G; t0 += kRankTile) {
+        __syncthreads();
+        for (int k = threadIdx.x; k < kRankTile; k += kThreads)
+            keys[k] = t0 + k < G ? order_key(a.grp_slo[t0 + k]) : 0xFFFFFFFFu;
+        __syncthreads();
+        const int base = quarter * (kRankTile / kWaves);
+#pragma unroll 4
+        for (int k = 0; k < kRankTile / kWaves; k += 4) {
+            const uint4 o = *reinterpret_cast<const uint4 *>(&keys[base + k]);
+            const int id = t0 + base + k;      // ids past G hold the largest key
+            cnt += (o.x < mine || (o.x == mine && id < i)) ? 1 : 0;
+            cnt += (o.y < mine || (o.y == mine && id + 1 < i)) ? 1 : 0;
+            cnt += (o.z < mine || (o.z == mine && id + 2 < i)) ? 1 : 0;
+            cnt += (o.w < mine || (o.w == mine && id + 3 < i)) ? 1 : 0;
+        }
+    }
+    part[threadIdx.x] = cnt;
+    __syncthreads();
+    if (quarter == 0 && i < G)
+        a.by_slo[part[li] + part[li + kWave] + part[li + 2 * kWave] + part[li + 3 * kWave]] = i;
+}
+
+// The normal-tail table, once per call, for the screens to copy into LDS.
+__global__ __launch_bounds__(kThreads) void k_stail(SearchArgs a)
+{
+    __shared__ float2 tab[qlm_tail::kCells];
+    qlm_tail::build<kThreads>(tab);
+    __syncthreads();
+    for (int k = threadIdx.x; k < qlm_tail::kCells; k += kThreads) a.tail[k] = tab[k];
 }
 
 // Start plans into the working copies; qoff is forced to a monotone split of
 // [0, G] and group ids to [0, G) so that every later access stays in bounds.
-__global__ __launch_bounds__(kPrepThreads) void k_sload(SearchArgs a, qlm_plans pl)
+__global__ __launch_bounds__(kThreads) void k_sload(SearchArgs a, qlm_plans pl)
 {
     const int G = a.G, I = a.I;
-    const int nblk = (G + kPrepThreads - 1) / kPrepThreads;
+    const int nblk = (G + kThreads - 1) / kThreads;
     const int64_t b = blockIdx.x / nblk;
-    const int s = (blockIdx.x % nblk) * kPrepThreads + threadIdx.x;
+    const int s = (blockIdx.x % nblk) * kThreads + threadIdx.x;
     if (s < G) {
         const int64_t e = (int64_t)s * pl.plan_stride + b;
         a.perm[b * G + s] = clampi(pl.perm[e], 0, G - 1);
@@ -307,132 +543,110 @@ __global__ __launch_bounds__(kPrepThreads) void k_sload(SearchArgs a, qlm_plans 
     }
 }
 
-// The cache of one chain's plan (one workgroup per chain).
-__global__ __launch_bounds__(kStateThreads) void k_sstate(SearchArgs a, int force)
+// The cache of one queue of one chain (one wavefront per queue).
+__global__ __launch_bounds__(kThreads) void k_sstate(SearchArgs a, int force)
 {
-    __shared__ int32_t qo[kMaxSearchInstances + 1];
-    const int64_t b = blockIdx.x;
-    if (!force && a.done[b]) return;
-    const int G = a.G, I = a.I;
+    const int I = a.I, G = a.G;
+    const int nblk = (I + kWaves - 1) / kWaves;
+    const int64_t b = blockIdx.x / nblk;
+    const int g = (blockIdx.x % nblk) * kWaves + wave_id();
+    const int lane = threadIdx.x & (kWave - 1);
+    if (g >= I || (!force && a.done[b])) return;
     const int32_t *__restrict__ perm = a.perm + b * G;
     const uint8_t *__restrict__ flag = a.flag + b * G;
     SRec *__restrict__ sr = a.srec + b * G;
     SSt *__restrict__ ss = a.sst + b * G;
+    TRec *__restrict__ tr = a.trec + b * G;
     int32_t *__restrict__ inv = a.inv + b * G;
-    double *__restrict__ Q = a.Q + b * I;
-    for (int g = threadIdx.x; g <= I; g += kStateThreads) qo[g] = a.qof[b * (I + 1) + g];
-    __syncthreads();
-    // 0. slot records in slot order
-    for (int s = threadIdx.x; s < G; s += kStateThreads) {
-        int lo = 0, hi = I;                     // last g with qo[g] <= s
-        while (hi - lo > 1) {
-            const int mid = (lo + hi) >> 1;
-            if (qo[mid] <= s)
-                lo = mid;
-            else
-                hi = mid;
+    const int bq = a.qof[b * (I + 1) + g], eq = a.qof[b * (I + 1) + g + 1];
+    // slot records, with the running maximum of the SLOs
+    float pm = -INFINITY;
+    for (int u0 = bq; u0 < eq; u0 += kWave) {
+        const int u = u0 + lane;
+        SRec x{};
+        float mx = -INFINITY;
+        if (u < eq) {
+            const int i = perm[u];
+            const GRec r = a.grec[i];
+            x.a = r.a;
+            x.b = r.b;
+            x.slo = r.slo;
+            x.nmf = r.nm | (flag[u] ? kFlagBit : 0u);
+            x.q = (uint32_t)g;
+            mx = r.slo;
+            inv[i] = u;
         }
-        const int i = perm[s];
-        const GRec r = a.grec[i];
-        SRec x;
-        x.a = r.a;
-        x.b = r.b;
-        x.slo = r.slo;
-        x.nmf = r.nm | (flag[s] ? kFlagBit : 0u);
-        x.pmax = 0.0f;
-        x.q = (uint32_t)lo;
-        sr[s] = x;
-        inv[i] = s;
-    }
-    __syncthreads();
-    // 1. running sums per queue, in position order (8 records fetched ahead)
-    for (int g = threadIdx.x; g < I; g += kStateThreads) {
-        const int bq = qo[g], eq = qo[g + 1];
-        const int cls = clampi(a.inst_class[g], 0, a.C - 1);
-        Run r{0.0, 0.0, 0.0, 0.0, model0_of(a, g)};
-        float pm = -INFINITY;
-        for (int s0 = bq; s0 < eq; s0 += 8) {
-            SRec x[8];
-#pragma unroll
-            for (int u = 0; u < 8; ++u)
-                if (s0 + u < eq) x[u] = sr[s0 + u];
-#pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                if (s0 + u >= eq) break;
-                const int m = (int)(x[u].nmf & 0xFFu);
-                if (r.prev >= 0 && r.prev != m && a.swap_cost)
-                    r.K += (double)a.swap_cost[((int64_t)cls * a.M + r.prev) * a.M + m];
-                if (x[u].nmf & kFlagBit) r.K += (double)a.evict_cost;
-                pm = x[u].slo > pm ? x[u].slo : pm;
-                ss[s0 + u] = SSt{r.A, r.V, r.K, 0.0};
-                sr[s0 + u].pmax = pm;
-                r.A += x[u].a;
-                r.V += x[u].b;
-                r.prev = m;
-            }
+        for (int o = 1; o < kWave; o <<= 1) {
+            const float y = __shfl_up(mx, o, kWave);
+            if (lane >= o) mx = y > mx ? y : mx;
         }
+        mx = pm > mx ? pm : mx;
+        x.pmax = mx;
+        if (u < eq) sr[u] = x;
+        pm = __shfl(mx, kWave - 1, kWave);
     }
-    __syncthreads();
-    // 2. each slot's term n P
-    for (int s = threadIdx.x; s < G; s += kStateThreads) {
-        const SRec x = sr[s];
-        const SSt t = ss[s];
-        const double theta = (double)a.inst_tput[x.q];
-        const double EW = t.A / theta + t.K;
-        const double SD = sqrt(t.V) / theta;
-        const double slo = (double)x.slo;
-        double P;
-        if (SD > 0.0)
-            P = 0.5 * erfc((slo - EW) / (SD * 1.4142135623730951));
-        else
-            P = (EW > slo) ? 1.0 : 0.0;
-        ss[s].C = (double)(x.nmf >> kCountShift) * P;
-    }
-    __syncthreads();
-    // 3. scores ahead of each slot, and per queue, in position order
-    for (int g = threadIdx.x; g < I; g += kStateThreads) {
-        const int bq = qo[g], eq = qo[g + 1];
-        double c = 0.0;
-        for (int s0 = bq; s0 < eq; s0 += 8) {
-            double t[8];
-#pragma unroll
-            for (int u = 0; u < 8; ++u)
-                if (s0 + u < eq) t[u] = ss[s0 + u].C;
-#pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                if (s0 + u >= eq) break;
-                ss[s0 + u].C = c;
-                c += t[u];
-            }
-        }
-        Q[g] = c;
-    }
-    __syncthreads();
-    // 4. queue scores summed in queue order
-    if (threadIdx.x == 0) {
-        double *T = a.T + b * (I + 1);
-        double t = 0.0;
-        T[0] = 0.0;
-        for (int g = 0; g < I; ++g) {
-            t += Q[g];
-            T[g + 1] = t;
-        }
-        a.cur[b] = t;
+    // the exact running sums and the screens' margins
+    const double theta = (double)a.inst_tput[g];
+    const int cls = clampi(a.inst_class[g], 0, a.C - 1);
+    const double vscale = qlm_tail::kVarScale / (theta * theta);
+    Run r{0.0, 0.0, 0.0, 0.0, model0_of(a, g)};
+    double nsum = 0.0, emax = 0.0;
+    wave_walk(r, eq - bq, [&](int v) { return sr[bq + v]; }, theta, cls, a,
+              [&](int v, const SRec &x, double A, double V, double K, double C, double E) {
+                  const int u = bq + v;
+                  ss[u] = SSt{A, V, K, C};
+                  const double slo = (double)x.slo;
+                  TRec t;
+                  t.m = slo - E;
+                  t.vz = (float)(V * vscale);
+                  t.n = (float)(x.nmf >> kCountShift);
+                  tr[u] = t;
+                  nsum += (double)(x.nmf >> kCountShift);
+                  emax = fmax(emax, fabs(E) + fabs(slo));
+              });
+    nsum = wave_sum(nsum);
+    emax = wave_max(emax);
+    if (lane == 0) {
+        a.Q[b * I + g] = r.sc;
+        a.Nq[b * I + g] = nsum;
+        a.Es[b * I + g] = emax;
     }
 }
 
-// Plan score with queue g's score replaced by qg (queues summed in order).
-__device__ inline double total_with(const double *T, const double *Q, int I, int g, double qg)
+// Queue scores summed in queue order: the plan score (the scores are staged
+// in LDS by all threads, then added in order by one).
+__global__ __launch_bounds__(kThreads) void k_stotal(SearchArgs a, int force)
 {
-    double t = T[g] + qg;
-    for (int q = g + 1; q < I; ++q) t += Q[q];
-    return t;
+    __shared__ double q[kThreads];
+    const int64_t b = blockIdx.x;
+    if (!force && a.done[b]) return;
+    const int I = a.I;
+    const double *Q = a.Q + b * I;
+    double *T = a.T + b * (I + 1);
+    double t = 0.0;
+    if (threadIdx.x == 0) T[0] = 0.0;
+    for (int g0 = 0; g0 < I; g0 += kThreads) {
+        if (g0 + (int)threadIdx.x < I) q[threadIdx.x] = Q[g0 + threadIdx.x];
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            const int n = min(kThreads, I - g0);
+            for (int k = 0; k < n; ++k) {
+                t += q[k];
+                T[g0 + k + 1] = t;
+            }
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) a.cur[b] = t;
 }
 
-__global__ __launch_bounds__(kTaskThreads) void k_sswap(SearchArgs a)
+// ---------------------------------------------------------------------------
+// Exact scores of every move, one lane per move (qlm_search_moves)
+
+__global__ __launch_bounds__(kThreads) void k_sswap(SearchArgs a)
 {
-    __shared__ double ls[kTaskThreads / kWave];
-    __shared__ int64_t lk[kTaskThreads / kWave];
+    __shared__ double ls[kWaves];
+    __shared__ int64_t lk[kWaves];
     const int64_t b = blockIdx.x / a.nwg_a;
     const int wg = blockIdx.x % a.nwg_a;
     if (a.done[b]) return;
@@ -440,7 +654,7 @@ __global__ __launch_bounds__(kTaskThreads) void k_sswap(SearchArgs a)
     const SRec *__restrict__ sr = a.srec + b * G;
     const SSt *__restrict__ ss = a.sst + b * G;
     const int32_t *__restrict__ qof = a.qof + b * (I + 1);
-    const int t = wg * kTaskThreads + threadIdx.x;
+    const int t = wg * kThreads + threadIdx.x;
     const int s = t / (W + 1);
     const int d = t - s * (W + 1);
     double best = INFINITY;
@@ -472,17 +686,17 @@ __global__ __launch_bounds__(kTaskThreads) void k_sswap(SearchArgs a)
             if (a.move_score) a.move_score[b * a.n_moves + k] = score;
         }
     }
-    block_best<kTaskThreads>(best, bk, ls, lk);
+    block_best(best, bk, ls, lk);
     if (threadIdx.x == 0) {
         a.wmin_s[b * a.nwg + wg] = best;
         a.wmin_i[b * a.nwg + wg] = bk;
     }
 }
 
-__global__ __launch_bounds__(kTaskThreads) void k_smove(SearchArgs a)
+__global__ __launch_bounds__(kThreads) void k_smove(SearchArgs a)
 {
-    __shared__ double ls[kTaskThreads / kWave];
-    __shared__ int64_t lk[kTaskThreads / kWave];
+    __shared__ double ls[kWaves];
+    __shared__ int64_t lk[kWaves];
     const int G = a.G, I = a.I;
     const int per_chain = I * a.nwg_b;
     const int64_t b = blockIdx.x / per_chain;
@@ -492,7 +706,7 @@ __global__ __launch_bounds__(kTaskThreads) void k_smove(SearchArgs a)
     const SRec *__restrict__ sr = a.srec + b * G;
     const SSt *__restrict__ ss = a.sst + b * G;
     const int32_t *__restrict__ qof = a.qof + b * (I + 1);
-    const int r = wg * kTaskThreads + threadIdx.x;
+    const int r = wg * kThreads + threadIdx.x;
     double best = INFINITY;
     int64_t bk = INT64_MAX;
     if (r < G) {
@@ -522,13 +736,7 @@ __global__ __launch_bounds__(kTaskThreads) void k_smove(SearchArgs a)
                     for (int u = p; u < eq; ++u) visit(w, sr[u], theta, cls, a);
                 }
             }
-            const double *T = a.T + b * (I + 1);
-            const double *Q = a.Q + b * I;
-            const double Rs = a.R[b * G + s];
-            const int lo = g < h ? g : h;
-            double t = T[lo];
-            for (int q = lo; q < I; ++q) t += q == g ? Rs : (q == h ? w.sc : Q[q]);
-            score = t;
+            score = total_with2(a.T + b * (I + 1), a.Q + b * I, I, g, a.R[b * G + s], h, w.sc);
             if (better(score, k, best, bk)) {
                 best = score;
                 bk = k;
@@ -536,7 +744,7 @@ __global__ __launch_bounds__(kTaskThreads) void k_smove(SearchArgs a)
         }
         if (a.move_score) a.move_score[b * a.n_moves + k] = score;
     }
-    block_best<kTaskThreads>(best, bk, ls, lk);
+    block_best(best, bk, ls, lk);
     if (threadIdx.x == 0) {
         const int64_t o = b * a.nwg + a.nwg_a + (int64_t)h * a.nwg_b + wg;
         a.wmin_s[o] = best;
@@ -544,29 +752,479 @@ __global__ __launch_bounds__(kTaskThreads) void k_smove(SearchArgs a)
     }
 }
 
+// ---------------------------------------------------------------------------
+// Screened steps
+
+// The z error a margin error of eps_rel * scale may cause stays below kZErr
+// when the scaled variance is at least the returned value (rsq of the scaled
+// variance is in cells per second of margin).
+__device__ inline double vz_floor(double eps_rel, double scale)
+{
+    const double t = eps_rel * scale / (kZErr * qlm_tail::kScale);
+    return fmax(t * t, 1.1754943508222875e-38);
+}
+
+// Relative rounding of a margin formed from sums over a queue of L positions.
+__device__ inline double margin_eps(int L) { return (8.0 + 2.0 * L) * 2.220446049250313e-16; }
+
+// One position of a screened walk: the running sums as in visit(), then P from
+// the tail table (or exactly [E > slo] where nothing ahead has variance, with
+// E formed as the exact score forms it).  A position whose spread is too small
+// for the rounding of its margin sets `force`.
+__device__ inline void screen_visit(Run &r, const SRec &x, double theta, double inv_theta, int cls,
+                                    double vscale, double eps_rel, const float2 *tab,
+                                    const SearchArgs &a, bool &force)
+{
+    const int m = (int)(x.nmf & 0xFFu);
+    if (r.prev >= 0 && r.prev != m && a.swap_cost)
+        r.K += (double)a.swap_cost[((int64_t)cls * a.M + r.prev) * a.M + m];
+    if (x.nmf & kFlagBit) r.K += (double)a.evict_cost;
+    const double slo = (double)x.slo;
+    double P;
+    if (r.V == 0.0) {
+        const double EW = r.A / theta + r.K;
+        P = (EW > slo) ? 1.0 : 0.0;
+    } else {
+        const double EW = fma(r.A, inv_theta, r.K);
+        const float vz = (float)(r.V * vscale);
+        force = force || !((double)vz >= vz_floor(eps_rel, fabs(EW) + fabs(slo)));
+        P = (double)qlm_tail::q_of(tab, (float)(slo - EW), vz);
+    }
+    r.sc += (double)(x.nmf >> kCountShift) * P;
+    r.A += x.a;
+    r.V += x.b;
+    r.prev = m;
+}
+
+// The in-step walks read one tail record per position for a whole wavefront,
+// at an address every lane shares, through the scalar cache (the records are
+// not written while the screens run).
+typedef const __attribute__((address_space(4))) TRec CTRec;
+typedef const __attribute__((address_space(4))) SSt CSSt;
+
+template <class T>
+__device__ inline const __attribute__((address_space(4))) T *as_const(const T *p)
+{
+    return reinterpret_cast<const __attribute__((address_space(4))) T *>(
+        reinterpret_cast<uintptr_t>(p));
+}
+
+// Sum over the positions u in [lo, hi) of each lane of n_u Q(z), the margin
+// m_u - dE and the scaled variance either the cached one plus dvz or, with
+// `exactv`, (V_u - db) vscale from the double-precision variances (which a
+// removal needs: no cancellation).  The wavefront walks the union of its
+// lanes' ranges in step.  Lanes with on = false add nothing.
+__device__ inline double tail_walk(const TRec *tr, const SSt *ss, const float2 *tab, bool on,
+                                   int lo, int hi, double dE, float dvz, double db, double vscale,
+                                   bool exactv)
+{
+    const int ulo = __builtin_amdgcn_readfirstlane((int)wave_min(on ? (double)lo : 1e9));
+    const int uhi = __builtin_amdgcn_readfirstlane((int)wave_max(on ? (double)hi : -1.0));
+    const auto ct = as_const(tr);
+    const auto cs = as_const(ss);
+    double acc = 0.0;
+    int u = ulo;
+    if (exactv) {
+        for (; u < uhi; u += 8) {
+            float s32 = 0.0f;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int uu = min(u + j, uhi - 1);
+                const double m = ct[uu].m;
+                const float n = ct[uu].n;
+                const double v = cs[uu].V;
+                const float q = qlm_tail::q_of(tab, (float)(m - dE), (float)((v - db) * vscale));
+                const float w = (on && u + j >= lo && u + j < hi) ? n : 0.0f;
+                s32 = fmaf(w, q, s32);
+            }
+            acc += (double)s32;
+        }
+    } else {
+        for (; u < uhi; u += 8) {
+            float s32 = 0.0f;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int uu = min(u + j, uhi - 1);
+                const double m = ct[uu].m;
+                const float vz = ct[uu].vz, n = ct[uu].n;
+                const float q = qlm_tail::q_of(tab, (float)(m - dE), vz + dvz);
+                const float w = (on && u + j >= lo && u + j < hi) ? n : 0.0f;
+                s32 = fmaf(w, q, s32);
+            }
+            acc += (double)s32;
+        }
+    }
+    return acc;
+}
+
+// Screened removals and SWAPs, one lane per task: tasks [0, G) are the
+// queues of each slot s without s (which the MOVE screens of s take up),
+// tasks G + s*W + d - 1 the moves SWAP(s, d).
+__global__ __launch_bounds__(kThreads) void k_fswap(SearchArgs a)
+{
+    __shared__ float2 tab[qlm_tail::kCells];
+    __shared__ double lmin[kWaves];
+    for (int k = threadIdx.x; k < qlm_tail::kCells; k += kThreads) tab[k] = a.tail[k];
+    __syncthreads();
+    const int64_t b = blockIdx.x / a.nwg_f;
+    const int wg = blockIdx.x % a.nwg_f;
+    if (a.done[b]) return;
+    const int G = a.G, I = a.I, W = a.W;
+    const SRec *__restrict__ sr = a.srec + b * G;
+    const SSt *__restrict__ ss = a.sst + b * G;
+    const TRec *__restrict__ tr = a.trec + b * G;
+    const int32_t *__restrict__ qof = a.qof + b * (I + 1);
+    const int t = wg * kThreads + threadIdx.x;
+    const bool removal = t < G;
+    const bool swap = !removal && t < G + G * W;
+    const int s = removal ? t : (swap ? (t - G) / W : 0);
+    const int d = swap ? (t - G) - s * W + 1 : 0;
+    int g = 0, eq = 0, lo = 0;
+    bool on = false, force = false, valid = false;
+    double q = 0.0, dE = 0.0, db = 0.0, vscale = 0.0;
+    if (removal || swap) {
+        g = (int)sr[s].q;
+        const int bq = qof[g];
+        eq = qof[g + 1];
+        const double theta = (double)a.inst_tput[g];
+        const double inv_theta = 1.0 / theta;
+        vscale = qlm_tail::kVarScale / (theta * theta);
+        const int cls = clampi(a.inst_class[g], 0, a.C - 1);
+        const double eps = margin_eps(eq - bq);
+        Run r = start_at(a, sr, ss, s, bq, g);
+        if (removal) {
+            // without s: the group after it moves up one position; past that the
+            // queue is the old one less s's tokens and variance, with its costs
+            // shifted
+            valid = true;
+            q = r.sc;
+            if (s + 1 < eq) {
+                screen_visit(r, sr[s + 1], theta, inv_theta, cls, vscale, eps, tab, a, force);
+                q = r.sc;
+                lo = s + 2;
+                if (lo < eq) {
+                    const SRec xs = sr[s];
+                    dE = (r.K - ss[s + 1].K) - xs.a * inv_theta;
+                    db = xs.b;
+                    // the variance left ahead keeps most of its bits and a spread wide
+                    // enough for the margin's rounding (both grow along the queue)
+                    const double v0 = ss[lo].V, v1 = v0 - db;
+                    force = force || !(v1 >= 0x1p-20 * v0) ||
+                            !((double)(float)(v1 * vscale) >=
+                              vz_floor(eps, a.Es[b * I + g] + fabs(dE)));
+                    on = true;
+                }
+            }
+        } else if (s + d < eq) {
+            valid = true;
+            screen_visit(r, sr[s + d], theta, inv_theta, cls, vscale, eps, tab, a, force);
+            for (int u = s + 1; u < s + d; ++u)
+                screen_visit(r, sr[u], theta, inv_theta, cls, vscale, eps, tab, a, force);
+            screen_visit(r, sr[s], theta, inv_theta, cls, vscale, eps, tab, a, force);
+            q = r.sc;
+            const int u1 = s + d + 1;
+            if (u1 < eq) {
+                screen_visit(r, sr[u1], theta, inv_theta, cls, vscale, eps, tab, a, force);
+                q = r.sc;
+                lo = u1 + 1;
+                if (lo < eq) {
+                    // past u1 the queue is the old one with its costs shifted by dK
+                    const double dK = r.K - ss[u1].K;
+                    force = force || !((double)tr[lo].vz >=
+                                       vz_floor(eps, a.Es[b * I + g] + fabs(dK)));
+                    if (dK == 0.0)
+                        q += a.Q[b * I + g] - ss[lo].C;
+                    else {
+                        dE = dK;
+                        on = true;
+                    }
+                }
+            }
+        }
+    }
+    const bool exactv = __ballot(on && removal) != 0;
+    q += tail_walk(tr, ss, tab, on, lo, eq, dE, 0.0f, db, vscale, exactv);
+    double F = INFINITY, D = 0.0;
+    if (valid) {
+        const double nq = a.Nq[b * I + g];
+        if (removal) {
+            a.R[b * G + s] = q;
+            a.RD[b * G + s] = force ? INFINITY : kEpsP * nq + 1e-12 * (fabs(a.Q[b * I + g]) + nq);
+        } else {
+            const double cur = a.cur[b];
+            F = cur - a.Q[b * I + g] + q;
+            D = force ? INFINITY : kEpsP * nq + 1e-12 * (fabs(cur) + nq);
+        }
+    }
+    if (swap) {
+        const int64_t k = (int64_t)s * W + (d - 1);
+        a.F[b * a.n_moves + k] = F;
+        a.D[b * a.n_moves + k] = D;
+    }
+    const double m = block_min(F + D, lmin);
+    if (threadIdx.x == 0) a.smin[b * a.nws + wg] = m;
+}
+
+// Screened MOVE: one wavefront per (target queue h, 64 groups adjacent in SLO
+// order).  Each lane scores its group's insertion point and the position after
+// it with running sums; past that, the queue is the old one shifted by the
+// group's tokens, variance and the change of costs, walked by the whole
+// wavefront in step from the earliest insertion point.
+__global__ __launch_bounds__(kThreads) void k_fmove(SearchArgs a)
+{
+    __shared__ float2 tab[qlm_tail::kCells];
+    __shared__ double lmin[kWaves];
+    __shared__ int lint[kWaves];
+    __shared__ TRec stage[kStage];
+    for (int k = threadIdx.x; k < qlm_tail::kCells; k += kThreads) tab[k] = a.tail[k];
+    __syncthreads();
+    const int G = a.G, I = a.I;
+    const int per_chain = I * a.nwg_b;
+    const int64_t b = blockIdx.x / per_chain;
+    const int h = (blockIdx.x % per_chain) / a.nwg_b;
+    const int wg = blockIdx.x % a.nwg_b;
+    if (a.done[b]) return;
+    const SRec *__restrict__ sr = a.srec + b * G;
+    const SSt *__restrict__ ss = a.sst + b * G;
+    const TRec *__restrict__ tr = a.trec + b * G;
+    const int32_t *__restrict__ qof = a.qof + b * (I + 1);
+    const int bq = qof[h], eq = qof[h + 1];
+    const double theta = (double)a.inst_tput[h];
+    const double inv_theta = 1.0 / theta;
+    const double vscale = qlm_tail::kVarScale / (theta * theta);
+    const int cls = clampi(a.inst_class[h], 0, a.C - 1);
+    const double eps = margin_eps(eq - bq + 1);
+    const double Qh = a.Q[b * I + h];
+    const int r = wg * kThreads + threadIdx.x;
+    bool valid = false, tail = false, force = false;
+    int s = 0, g = 0, p = eq;
+    double N = 0.0, dE = 0.0;
+    float dvz = 0.0f;
+    if (r < G) {
+        const int i = a.by_slo[r];
+        s = clampi(a.inv[b * G + i], 0, G - 1);
+        const SRec x = sr[s];
+        g = (int)x.q;
+        valid = g != h;
+        if (valid) {
+            Run w;
+            if (bq == eq) {
+                w = Run{0.0, 0.0, 0.0, 0.0, model0_of(a, h)};
+                screen_visit(w, x, theta, inv_theta, cls, vscale, eps, tab, a, force);
+            } else {
+                p = insertion_point(sr, bq, eq, x.slo);
+                if (p == eq) {
+                    const SSt t = ss[eq - 1];
+                    const SRec y = sr[eq - 1];
+                    w = Run{t.A + y.a, t.V + y.b, t.K, Qh, (int)(y.nmf & 0xFFu)};
+                    screen_visit(w, x, theta, inv_theta, cls, vscale, eps, tab, a, force);
+                } else {
+                    w = start_at(a, sr, ss, p, bq, h);
+                    screen_visit(w, x, theta, inv_theta, cls, vscale, eps, tab, a, force);
+                    screen_visit(w, sr[p], theta, inv_theta, cls, vscale, eps, tab, a, force);
+                    const double dK = w.K - ss[p].K;
+                    dE = x.a * inv_theta + dK;
+                    dvz = (float)(x.b * vscale);
+                    tail = p + 1 < eq;
+                    if (tail) {
+                        const double floor = vz_floor(eps, a.Es[b * I + h] + fabs(dE));
+                        force = force || !((double)(tr[p + 1].vz + dvz) >= floor);
+                    }
+                }
+            }
+            N = w.sc;
+        }
+    }
+    // the shifted tails: queue h's tail records pass through LDS in chunks
+    // (every wavefront of the workgroup targets h); each wavefront walks its
+    // lanes' tails in step, masked until its last lane's tail has begun
+    {
+        const int lo = tail ? p + 1 : eq;
+        const int ulo = __builtin_amdgcn_readfirstlane((int)wave_min((double)lo));
+        const int umask = __builtin_amdgcn_readfirstlane(
+            (int)wave_max(tail ? (double)lo : -1.0));            // from here no lane waits
+        const int wlo = __builtin_amdgcn_readfirstlane(block_min_int(ulo, lint));   // the workgroup's earliest
+        double acc = 0.0;
+        for (int c0 = wlo; c0 < eq; c0 += kStage) {
+            const int c1 = min(c0 + kStage, eq);
+            __syncthreads();
+            for (int u = c0 + (int)threadIdx.x; u < c1; u += kThreads) stage[u - c0] = tr[u];
+            __syncthreads();
+            int u = max(c0, ulo);
+            // masked part: some lanes' tails start later
+            for (; u < c1 && u <= umask; ++u) {
+                const TRec x = stage[u - c0];
+                const float q = qlm_tail::q_of(tab, (float)(x.m - dE), x.vz + dvz);
+                acc += (double)((tail && u > p) ? x.n * q : 0.0f);
+            }
+            // every lane with a tail is in it now
+            for (; u < c1; u += 8) {
+                float s32 = 0.0f;
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const int uu = min(u + j, c1 - 1);
+                    const TRec x = stage[uu - c0];
+                    const float q = qlm_tail::q_of(tab, (float)(x.m - dE), x.vz + dvz);
+                    s32 = fmaf(u + j < c1 ? x.n : 0.0f, q, s32);
+                }
+                acc += (double)s32;
+            }
+        }
+        N += tail ? acc : 0.0;
+    }
+    double F = INFINITY, D = 0.0;
+    if (valid) {
+        const double cur = a.cur[b];
+        const double nq = a.Nq[b * I + h];
+        F = cur + (a.R[b * G + s] - a.Q[b * I + g]) + (N - Qh);
+        D = force ? INFINITY : a.RD[b * G + s] + kEpsP * nq + 1e-12 * (fabs(cur) + nq);
+    }
+    if (r < G) {
+        const int64_t k = (int64_t)G * a.W + (int64_t)s * I + h;
+        a.F[b * a.n_moves + k] = F;
+        a.D[b * a.n_moves + k] = D;
+    }
+    const double m = block_min(F + D, lmin);
+    if (threadIdx.x == 0) a.smin[b * a.nws + a.nwg_f + (int64_t)h * a.nwg_b + wg] = m;
+}
+
+// The bound of the chain's lowest exact score, min(F + D); the candidate list
+// starts empty.
+__global__ __launch_bounds__(kThreads) void k_sbound(SearchArgs a)
+{
+    __shared__ double lmin[kWaves];
+    const int64_t b = blockIdx.x;
+    if (a.done[b]) return;
+    double m = INFINITY;
+    for (int w = threadIdx.x; w < a.nws; w += kThreads) m = fmin(m, a.smin[b * a.nws + w]);
+    m = block_min(m, lmin);
+    if (threadIdx.x == 0) {
+        a.U[b] = m;
+        a.ncand[b] = 0;
+    }
+}
+
+// Candidates: moves whose exact score may be the lowest and below the plan's.
+__global__ __launch_bounds__(kThreads) void k_sselect(SearchArgs a)
+{
+    const int nblk = (int)((a.n_moves + kThreads - 1) / kThreads);
+    const int64_t b = blockIdx.x / nblk;
+    if (a.done[b]) return;
+    const int64_t k = (int64_t)(blockIdx.x % nblk) * kThreads + threadIdx.x;
+    bool c = false;
+    if (k < a.n_moves) {
+        const double lo = a.F[b * a.n_moves + k] - a.D[b * a.n_moves + k];
+        c = lo <= a.U[b] && lo < a.cur[b];
+    }
+    const uint64_t mask = __ballot(c);
+    if (!mask) return;
+    const int lane = threadIdx.x & (kWave - 1);
+    int base = 0;
+    if (lane == 0) base = atomicAdd(&a.ncand[b], __popcll(mask));
+    base = __shfl(base, 0, kWave);
+    if (c) {
+        const int below = __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                                     __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+        a.cand[b * a.n_moves + base + below] = (int32_t)k;
+    }
+}
+
+// Exact scores of the candidates, one wavefront per candidate.
+__global__ __launch_bounds__(kThreads) void k_sexact(SearchArgs a)
+{
+    const int64_t b = blockIdx.x / kExactBlocks;
+    if (a.done[b]) return;
+    const int G = a.G, I = a.I, W = a.W;
+    const SRec *__restrict__ sr = a.srec + b * G;
+    const SSt *__restrict__ ss = a.sst + b * G;
+    const int32_t *__restrict__ qof = a.qof + b * (I + 1);
+    const double *T = a.T + b * (I + 1);
+    const double *Q = a.Q + b * I;
+    const int nc = a.ncand[b];
+    const int lane = threadIdx.x & (kWave - 1);
+    for (int c = (int)(blockIdx.x % kExactBlocks) * kWaves + wave_id(); c < nc;
+         c += kExactBlocks * kWaves) {
+        const int64_t k = __builtin_amdgcn_readfirstlane(a.cand[b * a.n_moves + c]);
+        double score = INFINITY;              // for a number that names no move
+        if (k < (int64_t)G * W) {
+            const int s = (int)(k / W), d = (int)(k % W) + 1;
+            const int g = (int)sr[s].q;
+            const int bq = qof[g], eq = qof[g + 1];
+            if (s + d >= eq) {
+                if (lane == 0) a.cex[b * a.n_moves + c] = score;
+                continue;
+            }
+            Run r = start_at(a, sr, ss, s, bq, g);
+            wave_walk(r, eq - s,
+                      [&](int v) { return sr[v == 0 ? s + d : (v == d ? s : s + v)]; },
+                      (double)a.inst_tput[g], clampi(a.inst_class[g], 0, a.C - 1), a,
+                      NoOut{});
+            score = total_with(T, Q, I, g, r.sc);
+        } else {
+            const int64_t rr = k - (int64_t)G * W;
+            const int s = (int)(rr / I), h = (int)(rr % I);
+            const SRec x = sr[s];
+            const int g = (int)x.q;
+            if (g == h) {
+                if (lane == 0) a.cex[b * a.n_moves + c] = score;
+                continue;
+            }
+            const int bq = qof[h], eq = qof[h + 1];
+            const double theta = (double)a.inst_tput[h];
+            const int cls = clampi(a.inst_class[h], 0, a.C - 1);
+            Run r;
+            if (bq == eq) {
+                r = Run{0.0, 0.0, 0.0, 0.0, model0_of(a, h)};
+                wave_walk(r, 1, [&](int) { return x; }, theta, cls, a, NoOut{});
+            } else {
+                const int p = insertion_point(sr, bq, eq, x.slo);
+                if (p == eq) {
+                    r = start_at(a, sr, ss, eq - 1, bq, h);
+                    wave_walk(r, 2, [&](int v) { return v == 0 ? sr[eq - 1] : x; }, theta, cls,
+                              a, NoOut{});
+                } else {
+                    r = start_at(a, sr, ss, p, bq, h);
+                    wave_walk(r, eq - p + 1, [&](int v) { return v == 0 ? x : sr[p + v - 1]; },
+                              theta, cls, a, NoOut{});
+                }
+            }
+            const double nh = r.sc;
+            const int bg = qof[g], eg = qof[g + 1];
+            Run rg = start_at(a, sr, ss, s, bg, g);
+            wave_walk(rg, eg - s - 1, [&](int v) { return sr[s + 1 + v]; },
+                      (double)a.inst_tput[g], clampi(a.inst_class[g], 0, a.C - 1), a,
+                      NoOut{});
+            score = total_with2(T, Q, I, g, rg.sc, h, nh);
+        }
+        if (lane == 0) a.cex[b * a.n_moves + c] = score;
+    }
+}
+
 #pragma clang fp contract(on)
 
-// Best move of each chain; applied when it improves on the plan.
-__global__ __launch_bounds__(kPickThreads) void k_spick(SearchArgs a, int step)
+// The lowest exact score among the candidates (lowest k on ties); applied when
+// it improves on the plan.
+__global__ __launch_bounds__(kThreads) void k_spick(SearchArgs a, int step)
 {
-    __shared__ double ls[kPickThreads / kWave];
-    __shared__ int64_t lk[kPickThreads / kWave];
+    __shared__ double ls[kWaves];
+    __shared__ int64_t lk[kWaves];
     __shared__ int apply;
     __shared__ int64_t kk;
     const int64_t b = blockIdx.x;
     if (a.done[b]) return;
     const int G = a.G, I = a.I, W = a.W;
+    const int nc = a.ncand[b];
     double best = INFINITY;
     int64_t bk = INT64_MAX;
-    for (int w = threadIdx.x; w < a.nwg; w += kPickThreads) {
-        const double s = a.wmin_s[b * a.nwg + w];
-        const int64_t k = a.wmin_i[b * a.nwg + w];
+    for (int c = threadIdx.x; c < nc; c += kThreads) {
+        const double s = a.cex[b * a.n_moves + c];
+        const int64_t k = a.cand[b * a.n_moves + c];
         if (better(s, k, best, bk)) {
             best = s;
             bk = k;
         }
     }
-    block_best<kPickThreads>(best, bk, ls, lk);
+    block_best(best, bk, ls, lk);
     if (threadIdx.x == 0) {
         apply = (best < a.cur[b] && bk >= 0 && bk < a.n_moves) ? 1 : 0;
         kk = bk;
@@ -606,12 +1264,12 @@ __global__ __launch_bounds__(kPickThreads) void k_spick(SearchArgs a, int step)
     const int hi = h > g ? p - 1 : s;
     int32_t *sp = a.scratch + b * 2 * G;
     int32_t *sf = sp + G;
-    for (int u = lo + threadIdx.x; u <= hi; u += kPickThreads) {
+    for (int u = lo + threadIdx.x; u <= hi; u += kThreads) {
         sp[u] = perm[u];
         sf[u] = flag[u];
     }
     __syncthreads();
-    for (int u = lo + threadIdx.x; u <= hi; u += kPickThreads) {
+    for (int u = lo + threadIdx.x; u <= hi; u += kThreads) {
         int v;
         if (h > g)
             v = u == hi ? s : u + 1;          // left by one, the group at the end
@@ -621,22 +1279,22 @@ __global__ __launch_bounds__(kPickThreads) void k_spick(SearchArgs a, int step)
         flag[u] = (uint8_t)sf[v];
     }
     if (h > g) {
-        for (int q = g + 1 + threadIdx.x; q <= h; q += kPickThreads) qof[q] -= 1;
+        for (int q = g + 1 + threadIdx.x; q <= h; q += kThreads) qof[q] -= 1;
     } else {
-        for (int q = h + 1 + threadIdx.x; q <= g; q += kPickThreads) qof[q] += 1;
+        for (int q = h + 1 + threadIdx.x; q <= g; q += kThreads) qof[q] += 1;
     }
 }
 
 // Final plans to the caller's slot-major arrays, with their scores and steps.
-__global__ __launch_bounds__(kPrepThreads) void k_sout(SearchArgs a, qlm_plans_out out,
-                                                       double *score, int32_t *steps)
+__global__ __launch_bounds__(kThreads) void k_sout(SearchArgs a, qlm_plans_out out,
+                                                   double *score, int32_t *steps)
 {
     const int G = a.G, I = a.I;
     const int64_t B = a.B;
     const int nw = (G + 31) >> 5;
     const int64_t rows = (int64_t)G + (I + 1) + (out.evict_bits ? nw : 0) + 1;
-    for (int64_t x = (int64_t)blockIdx.x * kPrepThreads + threadIdx.x; x < rows * B;
-         x += (int64_t)gridDim.x * kPrepThreads) {
+    for (int64_t x = (int64_t)blockIdx.x * kThreads + threadIdx.x; x < rows * B;
+         x += (int64_t)gridDim.x * kThreads) {
         const int64_t row = x / B, b = x % B;
         if (row < G) {
             out.perm[row * out.plan_stride + b] = a.perm[b * G + row];
@@ -662,17 +1320,21 @@ __global__ __launch_bounds__(kPrepThreads) void k_sout(SearchArgs a, qlm_plans_o
 size_t align256(size_t v) { return (v + 255) / 256 * 256; }
 
 struct Layout {
-    int nwg_a, nwg_b, nwg;
-    size_t grec, by_slo, perm, flag, qof, inv, srec, sst, R, Q, T, cur, done, steps, wmin_s,
-        wmin_i, scratch, total;
+    int nwg_a, nwg_b, nwg, nwg_f, nws;
+    int64_t n_moves;
+    size_t grec, by_slo, perm, flag, qof, inv, srec, sst, trec, R, RD, Q, Nq, Es, T, cur, done, steps,
+        wmin_s, wmin_i, smin, F, D, cand, cex, ncand, U, scratch, tail, total;
 };
 
 Layout layout(int G, int I, int W, int64_t B)
 {
     Layout L{};
-    L.nwg_a = (int)(((int64_t)G * (W + 1) + kTaskThreads - 1) / kTaskThreads);
-    L.nwg_b = (G + kTaskThreads - 1) / kTaskThreads;
+    L.nwg_a = (int)(((int64_t)G * (W + 1) + kThreads - 1) / kThreads);
+    L.nwg_b = (G + kThreads - 1) / kThreads;
     L.nwg = L.nwg_a + I * L.nwg_b;
+    L.nwg_f = (int)(((int64_t)G * (W + 1) + kThreads - 1) / kThreads);
+    L.nws = L.nwg_f + I * L.nwg_b;
+    L.n_moves = (int64_t)G * W + (int64_t)G * I;
     size_t o = 0;
     auto take = [&](size_t bytes) {
         const size_t at = o;
@@ -680,6 +1342,7 @@ Layout layout(int G, int I, int W, int64_t B)
         return at;
     };
     const size_t b = (size_t)B;
+    const size_t nm = (size_t)L.n_moves;
     L.grec = take(sizeof(GRec) * G);
     L.by_slo = take(4 * (size_t)G);
     L.perm = take(4 * (size_t)G * b);
@@ -688,15 +1351,27 @@ Layout layout(int G, int I, int W, int64_t B)
     L.inv = take(4 * (size_t)G * b);
     L.srec = take(sizeof(SRec) * G * b);
     L.sst = take(sizeof(SSt) * G * b);
+    L.trec = take(sizeof(TRec) * G * b);
     L.R = take(8 * (size_t)G * b);
+    L.RD = take(8 * (size_t)G * b);
     L.Q = take(8 * (size_t)I * b);
+    L.Nq = take(8 * (size_t)I * b);
+    L.Es = take(8 * (size_t)I * b);
     L.T = take(8 * (size_t)(I + 1) * b);
     L.cur = take(8 * b);
     L.done = take(4 * b);
     L.steps = take(4 * b);
     L.wmin_s = take(8 * (size_t)L.nwg * b);
     L.wmin_i = take(8 * (size_t)L.nwg * b);
+    L.smin = take(8 * (size_t)L.nws * b);
+    L.F = take(8 * nm * b);
+    L.D = take(8 * nm * b);
+    L.cand = take(4 * nm * b);
+    L.cex = take(8 * nm * b);
+    L.ncand = take(4 * b);
+    L.U = take(8 * b);
     L.scratch = take(8 * (size_t)G * b);
+    L.tail = take(sizeof(float2) * qlm_tail::kCells);
     L.total = o;
     return L;
 }
@@ -710,9 +1385,14 @@ int check_search(const qlm_problem *pr, int64_t B, int32_t W)
         return fail(QLM_ERR_ARG, "search: n_instances must be <= 4096");
     if (W < 0 || W > kMaxWindow) return fail(QLM_ERR_ARG, "search: window must be in [0, 1024]");
     if (B < 0) return fail(QLM_ERR_ARG, "search: n_plans must be >= 0");
-    const Layout L = layout(pr->n_groups, pr->n_instances, W, B > 0 ? B : 1);
-    if ((int64_t)L.nwg * B > INT_MAX || (int64_t)pr->n_instances * L.nwg_b * B > INT_MAX ||
-        (int64_t)L.nwg_a * B > INT_MAX)
+    const Layout L = layout(pr->n_groups, pr->n_instances, W, 1);
+    const int64_t Bc = B > 0 ? B : 1;
+    const int64_t sel = (L.n_moves + kThreads - 1) / kThreads;
+    if ((int64_t)L.nwg * Bc > INT_MAX || sel * Bc > INT_MAX || (int64_t)L.nws * Bc > INT_MAX ||
+        (int64_t)kExactBlocks * Bc > INT_MAX ||
+        (int64_t)((pr->n_groups + kWaves - 1) / kWaves) * Bc > INT_MAX ||
+        (int64_t)((pr->n_instances + kWaves - 1) / kWaves) * Bc > INT_MAX ||
+        (int64_t)((pr->n_groups + kThreads - 1) / kThreads) * Bc > INT_MAX)
         return fail(QLM_ERR_ARG, "search: too many plans for one launch");
     return QLM_OK;
 }
@@ -745,19 +1425,33 @@ SearchArgs search_args(const qlm_problem *pr, int64_t B, int32_t W, unsigned cha
     a.inv = (int32_t *)(ws + L.inv);
     a.srec = (SRec *)(ws + L.srec);
     a.sst = (SSt *)(ws + L.sst);
+    a.trec = (TRec *)(ws + L.trec);
     a.R = (double *)(ws + L.R);
+    a.RD = (double *)(ws + L.RD);
     a.Q = (double *)(ws + L.Q);
+    a.Nq = (double *)(ws + L.Nq);
+    a.Es = (double *)(ws + L.Es);
     a.T = (double *)(ws + L.T);
     a.cur = (double *)(ws + L.cur);
     a.done = (int32_t *)(ws + L.done);
     a.steps = (int32_t *)(ws + L.steps);
     a.wmin_s = (double *)(ws + L.wmin_s);
     a.wmin_i = (int64_t *)(ws + L.wmin_i);
+    a.smin = (double *)(ws + L.smin);
+    a.F = (double *)(ws + L.F);
+    a.D = (double *)(ws + L.D);
+    a.cand = (int32_t *)(ws + L.cand);
+    a.cex = (double *)(ws + L.cex);
+    a.ncand = (int32_t *)(ws + L.ncand);
+    a.U = (double *)(ws + L.U);
     a.scratch = (int32_t *)(ws + L.scratch);
+    a.tail = (float2 *)(ws + L.tail);
     a.nwg_a = L.nwg_a;
     a.nwg_b = L.nwg_b;
     a.nwg = L.nwg;
-    a.n_moves = (int64_t)a.G * W + (int64_t)a.G * a.I;
+    a.nwg_f = L.nwg_f;
+    a.nws = L.nws;
+    a.n_moves = L.n_moves;
     return a;
 }
 
@@ -767,8 +1461,7 @@ int launched(const char *what)
     return e == hipSuccess ? QLM_OK : hip_fail(e, what);
 }
 
-// Set-up shared by both entry points: checks, the group records and ranks, the
-// start plans, and the cache of every chain.
+// Checks, and the group records and ranks.
 int search_begin(const qlm_problem *pr, const qlm_plans *pl, int32_t W, void *ws, size_t ws_bytes,
                  SearchArgs *out, hipStream_t stream)
 {
@@ -784,34 +1477,75 @@ int search_begin(const qlm_problem *pr, const qlm_plans *pl, int32_t W, void *ws
     SearchArgs a = search_args(pr, B, W, (unsigned char *)ws, L);
     *out = a;
     if (B == 0) return QLM_OK;
-    const int G = a.G;
-    hipLaunchKernelGGL(k_sprep, dim3((G + kPrepThreads - 1) / kPrepThreads), dim3(kPrepThreads), 0,
-                       stream, a);
-    return launched("k_sprep launch");
+    hipLaunchKernelGGL(k_srank, dim3((a.G + kWave - 1) / kWave), dim3(kThreads), 0, stream, a);
+    rc = launched("k_srank launch");
+    if (rc) return rc;
+    hipLaunchKernelGGL(k_stail, dim3(1), dim3(kThreads), 0, stream, a);
+    return launched("k_stail launch");
+}
+
+int launch_state(SearchArgs &a, int force, hipStream_t stream)
+{
+    const int nblk = (a.I + kWaves - 1) / kWaves;
+    hipLaunchKernelGGL(k_sstate, dim3((unsigned)(nblk * a.B)), dim3(kThreads), 0, stream, a, force);
+    int rc = launched("k_sstate launch");
+    if (rc) return rc;
+    hipLaunchKernelGGL(k_stotal, dim3((unsigned)a.B), dim3(kThreads), 0, stream, a, force);
+    return launched("k_stotal launch");
 }
 
 int load_and_state(SearchArgs &a, const qlm_plans *pl, hipStream_t stream)
 {
-    const int nblk = (a.G + kPrepThreads - 1) / kPrepThreads;
-    hipLaunchKernelGGL(k_sload, dim3((unsigned)(nblk * a.B)), dim3(kPrepThreads), 0, stream, a, *pl);
+    const int nblk = (a.G + kThreads - 1) / kThreads;
+    hipLaunchKernelGGL(k_sload, dim3((unsigned)(nblk * a.B)), dim3(kThreads), 0, stream, a, *pl);
     int rc = launched("k_sload launch");
     if (rc) return rc;
-    hipLaunchKernelGGL(k_sstate, dim3((unsigned)a.B), dim3(kStateThreads), 0, stream, a, 1);
-    return launched("k_sstate launch");
+    return launch_state(a, 1, stream);
 }
 
-int score_moves(SearchArgs &a, hipStream_t stream)
+// Exact scores of every move (one lane per move).
+int exact_moves(SearchArgs &a, hipStream_t stream)
 {
-    hipLaunchKernelGGL(k_sswap, dim3((unsigned)(a.nwg_a * a.B)), dim3(kTaskThreads), 0, stream, a);
+    hipLaunchKernelGGL(k_sswap, dim3((unsigned)(a.nwg_a * a.B)), dim3(kThreads), 0, stream, a);
     int rc = launched("k_sswap launch");
     if (rc) return rc;
     qlm_internal::TimedLaunch tl;
     if ((rc = qlm_internal::timing_begin(stream, &tl))) return rc;
-    hipLaunchKernelGGL(k_smove, dim3((unsigned)((int64_t)a.I * a.nwg_b * a.B)), dim3(kTaskThreads),
-                       0, stream, a);
+    hipLaunchKernelGGL(k_smove, dim3((unsigned)((int64_t)a.I * a.nwg_b * a.B)), dim3(kThreads), 0,
+                       stream, a);
     if ((rc = launched("k_smove launch"))) return rc;
     qlm_internal::timing_end(stream, &tl);
     return QLM_OK;
+}
+
+// The screens of every move (removals and swaps, then reassignments).
+int screen_moves(SearchArgs &a, hipStream_t stream)
+{
+    hipLaunchKernelGGL(k_fswap, dim3((unsigned)(a.nwg_f * a.B)), dim3(kThreads), 0, stream, a);
+    int rc = launched("k_fswap launch");
+    if (rc) return rc;
+    qlm_internal::TimedLaunch tl;
+    if ((rc = qlm_internal::timing_begin(stream, &tl))) return rc;
+    hipLaunchKernelGGL(k_fmove, dim3((unsigned)((int64_t)a.I * a.nwg_b * a.B)), dim3(kThreads), 0,
+                       stream, a);
+    if ((rc = launched("k_fmove launch"))) return rc;
+    qlm_internal::timing_end(stream, &tl);
+    return QLM_OK;
+}
+
+// One search step after the screens: candidates, their exact scores, the pick.
+int pick_step(SearchArgs &a, int step, hipStream_t stream)
+{
+    hipLaunchKernelGGL(k_sbound, dim3((unsigned)a.B), dim3(kThreads), 0, stream, a);
+    int rc = launched("k_sbound launch");
+    if (rc) return rc;
+    const int64_t sel = (a.n_moves + kThreads - 1) / kThreads;
+    hipLaunchKernelGGL(k_sselect, dim3((unsigned)(sel * a.B)), dim3(kThreads), 0, stream, a);
+    if ((rc = launched("k_sselect launch"))) return rc;
+    hipLaunchKernelGGL(k_sexact, dim3((unsigned)(kExactBlocks * a.B)), dim3(kThreads), 0, stream, a);
+    if ((rc = launched("k_sexact launch"))) return rc;
+    hipLaunchKernelGGL(k_spick, dim3((unsigned)a.B), dim3(kThreads), 0, stream, a, step);
+    return launched("k_spick launch");
 }
 
 }  // namespace
@@ -847,7 +1581,23 @@ int qlm_search_moves(const qlm_problem *problem, const qlm_plans *plans, int32_t
     a.move_score = move_score;
     rc = load_and_state(a, plans, stream);
     if (rc) return rc;
-    return score_moves(a, stream);
+    return exact_moves(a, stream);
+}
+
+int qlm_search_screen(const qlm_problem *problem, const qlm_plans *plans, int32_t window,
+                      void *ws, size_t ws_bytes, double *score, double *bound, qlm_stream stream_)
+{
+    hipStream_t stream = (hipStream_t)stream_;
+    if (!score || !bound) return fail(QLM_ERR_ARG, "score and bound are required");
+    SearchArgs a;
+    int rc = search_begin(problem, plans, window, ws, ws_bytes, &a, stream);
+    if (rc) return rc;
+    if (a.B == 0) return QLM_OK;
+    rc = load_and_state(a, plans, stream);
+    if (rc) return rc;
+    a.F = score;
+    a.D = bound;
+    return screen_moves(a, stream);
 }
 
 int qlm_local_search(const qlm_problem *problem, const qlm_plans *start, const qlm_plans_out *out,
@@ -873,25 +1623,17 @@ int qlm_local_search(const qlm_problem *problem, const qlm_plans *start, const q
     rc = load_and_state(a, start, stream);
     if (rc) return rc;
     for (int t = 0; t < max_steps; ++t) {
-        if (t > 0) {
-            hipLaunchKernelGGL(k_sstate, dim3((unsigned)a.B), dim3(kStateThreads), 0, stream, a, 0);
-            if ((rc = launched("k_sstate launch"))) return rc;
-        }
-        if ((rc = score_moves(a, stream))) return rc;
-        hipLaunchKernelGGL(k_spick, dim3((unsigned)a.B), dim3(kPickThreads), 0, stream, a, t);
-        if ((rc = launched("k_spick launch"))) return rc;
+        if (t > 0 && (rc = launch_state(a, 0, stream))) return rc;
+        if ((rc = screen_moves(a, stream))) return rc;
+        if ((rc = pick_step(a, t, stream))) return rc;
     }
-    if (max_steps > 0) {
-        hipLaunchKernelGGL(k_sstate, dim3((unsigned)a.B), dim3(kStateThreads), 0, stream, a, 1);
-        if ((rc = launched("k_sstate launch"))) return rc;
-    }
+    if (max_steps > 0 && (rc = launch_state(a, 1, stream))) return rc;
     qlm_plans_out o = *out;
     if (!start->evict_bits) o.evict_bits = nullptr;
     const int64_t rows = (int64_t)a.G + a.I + 1 + (o.evict_bits ? (a.G + 31) / 32 : 0) + 1;
-    int64_t grid = (rows * a.B + kPrepThreads - 1) / kPrepThreads;
+    int64_t grid = (rows * a.B + kThreads - 1) / kThreads;
     if (grid > 65536) grid = 65536;
-    hipLaunchKernelGGL(k_sout, dim3((unsigned)grid), dim3(kPrepThreads), 0, stream, a, o, score,
-                       steps);
+    hipLaunchKernelGGL(k_sout, dim3((unsigned)grid), dim3(kThreads), 0, stream, a, o, score, steps);
     return launched("k_sout launch");
 }
 

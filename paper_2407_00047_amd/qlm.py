@@ -7,7 +7,7 @@ run when the library is not built (there is no fallback of any kind).
 Function names follow the C interface: ``rwt_score``, ``rwt_score_exact``,
 ``best_plan`` (with ``best_plan_workspace_bytes``), ``validate_plans``,
 ``validate_problem``, ``search_n_moves``, ``search_workspace_bytes``,
-``search_moves``, ``local_search``.
+``search_moves``, ``search_screen``, ``local_search``.
 """
 from __future__ import annotations
 
@@ -90,11 +90,13 @@ def library():
             lib.qlm_search_workspace_bytes.argtypes = [P, i64, i32]
             lib.qlm_search_workspace_bytes.restype = ctypes.c_size_t
             lib.qlm_search_moves.argtypes = [P, PL, i32, vp, ctypes.c_size_t, vp, vp]
+            lib.qlm_search_screen.argtypes = [P, PL, i32, vp, ctypes.c_size_t, vp, vp, vp]
             lib.qlm_local_search.argtypes = [P, PL, ctypes.POINTER(PlansOut), i32, i32, vp,
                                              ctypes.c_size_t, vp, vp, vp, vp]
             for name in ("qlm_rwt_score", "qlm_rwt_score_exact", "qlm_best_plan",
                          "qlm_validate_plans", "qlm_validate_problem", "qlm_timing_enable",
-                         "qlm_timing_read", "qlm_search_moves", "qlm_local_search"):
+                         "qlm_timing_read", "qlm_search_moves", "qlm_search_screen",
+                         "qlm_local_search"):
                 getattr(lib, name).restype = ctypes.c_int
             _lib = lib
     return _lib
@@ -300,6 +302,23 @@ def search_moves(problem: DeviceProblem, plans: DevicePlans, window: int, ws=Non
     _check(library().qlm_search_moves(ctypes.byref(problem.struct), ctypes.byref(plans.struct),
                                       window, _ptr(ws), ws.numel(), _ptr(out), _stream(stream)))
     return out
+
+
+def search_screen(problem: DeviceProblem, plans: DevicePlans, window: int, ws=None, stream=None):
+    """Screened score and its error bound for every move of every plan: two
+    device tensors [P, n_moves] (score +inf, bound 0 where a move number names
+    no move; bound +inf where the screen cannot bound the move)."""
+    import torch
+    dev = plans.perm.device
+    nm = search_n_moves(problem.n_groups, problem.n_instances, window)
+    if ws is None:
+        ws = search_workspace(problem, plans.n_plans, window, dev)
+    score = torch.empty((plans.n_plans, nm), dtype=torch.float64, device=dev)
+    bound = torch.empty((plans.n_plans, nm), dtype=torch.float64, device=dev)
+    _check(library().qlm_search_screen(ctypes.byref(problem.struct), ctypes.byref(plans.struct),
+                                       window, _ptr(ws), ws.numel(), _ptr(score), _ptr(bound),
+                                       _stream(stream)))
+    return score, bound
 
 
 def local_search(problem: DeviceProblem, plans: DevicePlans, window: int, max_steps: int,

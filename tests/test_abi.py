@@ -29,7 +29,8 @@ def test_header_declares_entry_points():
     for must in ("qlm_rwt_score", "qlm_best_plan", "qlm_best_plan_workspace_bytes",
                  "qlm_rwt_score_exact", "qlm_validate_plans", "qlm_validate_problem",
                  "qlm_status_string", "qlm_last_error", "qlm_search_n_moves",
-                 "qlm_search_workspace_bytes", "qlm_search_moves", "qlm_local_search"):
+                 "qlm_search_workspace_bytes", "qlm_search_moves", "qlm_search_screen",
+                 "qlm_local_search"):
         assert must in names
 
 
@@ -133,6 +134,11 @@ def test_search_argument_checks(lib):
     assert ls(P(pr), P(plev), P(out), 4, 5, ws, need, None, None, None, None) == qlm.QLM_ERR_ARG
     assert ls(P(pr), P(pl), P(out), 4, 5, ws, need - 1, None, None, None, None) == \
         qlm.QLM_ERR_WORKSPACE
+    sc = lib.qlm_search_screen
+    assert sc(P(pr), P(pl), 4, ws, need, 0x1000, None, None) == qlm.QLM_ERR_ARG
+    assert sc(P(pr), P(pl), 4, ws, need - 1, 0x1000, 0x1000, None) == qlm.QLM_ERR_WORKSPACE
+    assert sc(P(pr), P(pl), -2, ws, need, 0x1000, 0x1000, None) == qlm.QLM_ERR_ARG
     # no plans: nothing to do
     zero = qlm.Plans(0, 1, None, None, None)
     assert ms(P(pr), P(zero), 4, ws, need, 0x1000, None) == qlm.QLM_OK
+    assert sc(P(pr), P(zero), 4, ws, need, 0x1000, 0x1000, None) == qlm.QLM_OK

@@ -106,6 +106,40 @@ def test_move_scores(qlm, orc, kw):
     print("bit-identical move scores: %d of %d" % (exact, ms.size))
 
 
+def _check_screen(F, D, ref, label):
+    """Screened scores within their bounds of the exact ones; +inf where no move."""
+    F = np.asarray(F)
+    D = np.asarray(D)
+    nomove = np.isinf(ref)
+    assert np.all(np.isinf(F[nomove])) and np.all(D[nomove] == 0), label
+    mv = ~nomove
+    assert np.all(np.isfinite(F[mv])) and np.all(D[mv] >= 0), label
+    fin = mv & np.isfinite(D)
+    err = np.abs(F[fin] - ref[fin])
+    assert np.all(err <= D[fin]), (label, int(np.argmax(err - D[fin])), float(np.max(err - D[fin])))
+    return int(np.sum(mv & np.isinf(D))), float(np.max(err / np.maximum(D[fin], 1e-300))) if err.size else 0.0
+
+
+@pytest.mark.parametrize("kw", SEARCH_CASES, ids=[str(c) for c in SEARCH_CASES])
+def test_screen_bounds(qlm, orc, kw):
+    """Every screened move score lies within its bound of the oracle's score."""
+    import torch
+    pr, pl, W = _case(kw)
+    print("case", kw, flush=True)
+    dpr, dpl = device_inputs(pr, pl)
+    F, D = qlm.search_screen(dpr, dpl, W)
+    torch.cuda.synchronize()
+    F = F.cpu().numpy()
+    D = D.cpu().numpy()
+    forced, worst = 0, 0.0
+    for p in range(pl["n_plans"]):
+        ref = orc.move_scores(pr, pl, p, W)
+        f, w = _check_screen(F[p], D[p], ref, (kw, p))
+        forced += f
+        worst = max(worst, w)
+    print("unbounded (scored exactly): %d of %d; largest error / bound %.3g" % (forced, F.size, worst))
+
+
 def _check_search(orc, pr, pl, p, W, T, g_trace, g_steps, g_perm, g_qoff, g_ev, g_score):
     """Compares one chain's search with the oracle's; returns the step where a
     near-tie let the two sides part (None when they agree throughout)."""
@@ -213,9 +247,13 @@ def test_search_workloads(qlm, orc):
         print("workload", name, flush=True)
         dpr, dpl = device_inputs(pr, pl)
         ms = qlm.search_moves(dpr, dpl, W).cpu().numpy()
+        F, D = qlm.search_screen(dpr, dpl, W)
+        F = F.cpu().numpy()
+        D = D.cpu().numpy()
         for p in range(2):
             ref = orc.move_scores(pr, pl, p, W)
             assert _close(ms[p], ref).all(), (name, p)
+            print(name, "screen: unbounded, worst error/bound", _check_screen(F[p], D[p], ref, (name, p)))
         r = qlm.local_search(dpr, dpl, W, 5, trace=True)
         torch.cuda.synchronize()
         out = r["plans"]
@@ -251,6 +289,13 @@ def test_search_full_size(qlm, orc, name, W):
                          np.flatnonzero(~np.isfinite(ms))[:20]])
     ref = orc.move_scores(pr, pl, 0, W, ks=ks)
     assert _close(ms[ks], ref).all()
+    F, D = qlm.search_screen(dpr, dpl, W)
+    F = F.cpu().numpy()[0]
+    D = D.cpu().numpy()[0]
+    print("screen on the sample: unbounded, worst error/bound", _check_screen(F[ks], D[ks], ref, name))
+    # every move: the screen against the exact scores of the GPU's exact kernels
+    # (both checked against the oracle above on the sample)
+    print("screen on all moves (against the exact kernels):", _check_screen(F, D, ms, name))
     T = 3
     r = qlm.local_search(dpr, dpl, W, T, trace=True)
     torch.cuda.synchronize()
