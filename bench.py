@@ -24,14 +24,13 @@ sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0
 METRIC = "candidate plans scored/sec (RWT + SLO prob) and % of HBM roofline, 1 GPU"
-SEARCH_METRIC = "plan-search moves scored/sec (exact, incremental) and % of fp64 roofline, 1 GPU"
-# MI355X vector fp64: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz instructions per
-# second (78.6 TFLOP/s counts a fused multiply-add as two).
-PEAK_F64_INSTR = 256 * 4 * 16 * 2.4e9
-# fp64 instructions of one visited position in the walk of the reassignment
-# kernel (IEEE divisions, square root, erfc and the running sums), counted in
-# its compiled loop.
-F64_PER_VISIT = 125
+SEARCH_METRIC = "plan-search moves scored/sec (screened + exact best) and % of VALU roofline, 1 GPU"
+# MI355X vector issue: 256 CUs x 4 SIMDs, one wave64 VALU instruction per SIMD
+# every 4 cycles (16 lanes a cycle) at 2.4 GHz.
+PEAK_VALU_LANES = 256 * 4 * 16 * 2.4e9
+# VALU instructions per visited position in the main loop of the reassignment
+# screen (k_fmove), counted in its compiled loop body.
+VALU_PER_VISIT = 13
 
 
 def log(*a):
@@ -165,9 +164,9 @@ def cpu_baseline(problem, plans, seconds: float):
 
 def move_counts(problem, plans, p, window):
     """Valid moves of plan p (swaps within a queue, reassignments) and the
-    positions the reassignment kernel visits for them: for a group moving to
-    queue h, the walk starts at its insertion point (one position earlier when
-    that is the end of a non-empty queue) and runs to the end of h."""
+    positions the reassignment screen visits for them: for a group moving to
+    queue h, itself at its insertion point and every position of h from there
+    on (one position when it goes to the end or into an empty queue)."""
     import numpy as np
     G, I = problem["n_groups"], problem["n_instances"]
     perm = plans["perm"][:, p]
@@ -188,7 +187,7 @@ def move_counts(problem, plans, p, window):
             continue
         pmax = np.maximum.accumulate(slo[perm[b:e]])
         pos = np.searchsorted(pmax, x, side="right")          # first pmax > slo
-        visits += int(np.sum((e - b) - pos + 1 + (pos == e - b)))
+        visits += int(np.sum(np.where(pos == e - b, 1, (e - b) - pos + 1)))
     return swaps + moves, moves, visits
 
 
@@ -216,7 +215,8 @@ def cpu_search_baseline(problem, plans, window, seconds: float):
 
 def bench_search(args):
     """One step = one step of the local search on every chain: cache the plan,
-    score every move exactly (swaps, then reassignments), pick and apply."""
+    screen every move (removals, swaps, reassignments), re-score exactly the
+    moves that can still be the best, pick and apply."""
     import torch
     from paper_2407_00047_amd import qlm, workload
     dev = torch.device("cuda:0")
@@ -251,26 +251,25 @@ def bench_search(args):
     total_ms = e0.elapsed_time(e1)
     steps = r["steps"].cpu().numpy()
     applied = int(steps.sum())
-    # the reassignment kernel on the start plans (the positions it visits are
+    # the reassignment screen on the start plans (the positions it visits are
     # known exactly there), timed over repeated launches
-    ms_scores = torch.empty((B, nm), dtype=torch.float64, device=dev)
     reps = 10
-    qlm.search_moves(dpr, dpl, W, ws=ws, out=ms_scores)
+    qlm.search_screen(dpr, dpl, W, ws=ws)
     torch.cuda.synchronize()
     qlm.timing_read()
     for _ in range(reps):
-        qlm.search_moves(dpr, dpl, W, ws=ws, out=ms_scores)
+        qlm.search_screen(dpr, dpl, W, ws=ws)
     torch.cuda.synchronize()
     n_launch, k_ms = qlm.timing_read()
     qlm.timing_enable(False)
     k_avg = k_ms / max(n_launch, 1)
     achieved = visits / (k_avg / 1e3) / 1e9
-    peak = PEAK_F64_INSTR / F64_PER_VISIT / 1e9
-    roofline = {"bound": "alu", "achieved": round(achieved, 2), "peak": round(peak, 2),
+    peak = PEAK_VALU_LANES / VALU_PER_VISIT / 1e9
+    roofline = {"bound": "alu", "achieved": round(achieved, 1), "peak": round(peak, 1),
                 "unit": "Gvisits/s", "frac": round(achieved / peak, 4), "traffic": None,
-                "kernel": "k_smove", "kernel_avg_ms": round(k_avg, 4),
+                "kernel": "k_fmove", "kernel_avg_ms": round(k_avg, 4),
                 "kernel_avg_ms_in_search": round(ms_search / max(n_search, 1), 4),
-                "visits_per_launch": visits, "f64_instr_per_visit": F64_PER_VISIT}
+                "visits_per_launch": visits, "valu_per_visit": VALU_PER_VISIT}
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle ...")
@@ -281,7 +280,7 @@ def bench_search(args):
         "metric": SEARCH_METRIC, "value": round(valid * K / (total_ms / 1e3), 1),
         "unit": "moves/s", "n_gpus": 1, "steps": K, "warmup": args.warmup,
         "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+        "vs_baseline": None, "dtype": "f32+f64", "data": "synthetic",
         "config": {"workload": "plan search on %s: %d groups (%d requests), %d instances, "
                                "%d start plans, window %d, %d valid moves per plan and step"
                                % (args.config, G, N, I, B, W, valid // B),
