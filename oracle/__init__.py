@@ -90,6 +90,8 @@ class Oracle:
         lib.oracle_local_search.argtypes = [ctypes.POINTER(_Problem), ctypes.POINTER(_Plans), i64,
                                             i32, i32, vp, vp, vp, dp, vp, vp, ctypes.c_int]
         lib.oracle_local_search.restype = ctypes.c_int
+        lib.oracle_seed_plan.argtypes = [ctypes.POINTER(_Problem), i32, vp, vp]
+        lib.oracle_seed_plan.restype = ctypes.c_int
         self.lib = lib
         self.path = path
 
@@ -182,6 +184,17 @@ class Oracle:
         self.lib.oracle_move_scores(ctypes.byref(b.problem), ctypes.byref(b.plans), p, window,
                                     _ptr(kp), n, _dp(out), int(threads))
         return out
+
+    def seed_plan(self, problem, policy: int):
+        """Seed plan of a policy (0 EDF, 1 same-model grouped): (perm[G], qoff[I+1])."""
+        G, I = int(problem["n_groups"]), int(problem["n_instances"])
+        b = _Bound(problem, {"perm": np.zeros((G, 1), np.int32),
+                             "qoff": np.zeros((I + 1, 1), np.int32)})
+        perm = np.empty(G, np.int32)
+        qoff = np.empty(I + 1, np.int32)
+        if self.lib.oracle_seed_plan(ctypes.byref(b.problem), int(policy), _ptr(perm), _ptr(qoff)):
+            raise ValueError("policy must be 0 (EDF) or 1 (grouped)")
+        return perm, qoff
 
     def local_search(self, problem, plans, p: int, window: int, max_steps: int,
                      threads: int = 0):
@@ -330,3 +343,7 @@ def move_scores(problem, plans, p: int, window: int, ks=None, threads: int = 0):
 
 def local_search(problem, plans, p: int, window: int, max_steps: int, threads: int = 0):
     return default().local_search(problem, plans, p, window, max_steps, threads)
+
+
+def seed_plan(problem, policy: int):
+    return default().seed_plan(problem, policy)

@@ -426,3 +426,87 @@ int oracle_local_search(const oracle_problem *pr, const oracle_plans *pl, int64_
     free(perm); free(perm2); free(qoff); free(qoff2); free(flag); free(flag2); free(words); free(sc);
     return 0;
 }
+
+/* ------------------------------------------------------------------------
+ * Seed plans for the search: the paper's reference orders.
+ *
+ *   policy 0, EDF: groups taken by SLO (earliest deadline first, the EDF
+ *             baseline of Sec. 8), ties by group id;
+ *   policy 1, grouped: groups taken by model, then SLO, then id (same-model
+ *             requests kept together to avoid repeated model swaps, Sec. 2,
+ *             Insight #3).
+ *
+ * Groups are placed one at a time, in that order, at the end of the queue
+ * whose drain time after taking the group is smallest (load balancing by
+ * queue drain time, Sec. 8's load-balancing study): for queue q holding
+ * tokens A_q and fixed costs K_q, whose last model is l_q (the loaded model
+ * inst_model0[q] while empty, -1 = none),
+ *   drain_q(i) = (A_q + n_i mu_i) / Theta_q + (K_q + s),
+ *   s = S[class_q][l_q][m_i] if l_q >= 0 and l_q != m_i, else 0,
+ * the lowest q on ties.  Seeds evict nothing.
+ */
+static const oracle_problem *g_seed_pr;
+static int g_seed_policy;
+
+static int seed_cmp(const void *pa, const void *pb)
+{
+    const int32_t a = *(const int32_t *)pa, b = *(const int32_t *)pb;
+    const oracle_problem *pr = g_seed_pr;
+    if (g_seed_policy == 1 && pr->grp_model[a] != pr->grp_model[b])
+        return pr->grp_model[a] < pr->grp_model[b] ? -1 : 1;
+    if (pr->grp_slo[a] < pr->grp_slo[b]) return -1;
+    if (pr->grp_slo[a] > pr->grp_slo[b]) return 1;
+    return a < b ? -1 : (a > b ? 1 : 0);
+}
+
+/* One seed plan: perm_out[G], qoff_out[I+1].  Returns 0, or -1 on a bad policy. */
+int oracle_seed_plan(const oracle_problem *pr, int32_t policy, int32_t *perm_out,
+                     int32_t *qoff_out)
+{
+    const int G = pr->n_groups, I = pr->n_instances, M = pr->n_models;
+    if (policy != 0 && policy != 1) return -1;
+    int32_t *order = malloc(sizeof(int32_t) * G);
+    int32_t *owner = malloc(sizeof(int32_t) * G);
+    double *A = calloc((size_t)I, sizeof(double)), *K = calloc((size_t)I, sizeof(double));
+    int32_t *last = malloc(sizeof(int32_t) * I), *count = calloc((size_t)I, sizeof(int32_t));
+    for (int i = 0; i < G; ++i) order[i] = i;
+    g_seed_pr = pr;
+    g_seed_policy = policy;
+    qsort(order, (size_t)G, sizeof(int32_t), seed_cmp);
+    for (int q = 0; q < I; ++q) last[q] = pr->inst_model0 ? pr->inst_model0[q] : -1;
+    for (int k = 0; k < G; ++k) {
+        const int i = order[k];
+        const int m = pr->grp_model[i];
+        const double a = (double)pr->grp_count[i] * (double)pr->grp_mu[i];
+        int best = -1;
+        double bd = INFINITY;
+        for (int q = 0; q < I; ++q) {
+            double s = 0.0;
+            if (last[q] >= 0 && last[q] != m && pr->swap_cost)
+                s = (double)pr->swap_cost[((int64_t)pr->inst_class[q] * M + last[q]) * M + m];
+            const double d = (A[q] + a) / (double)pr->inst_tput[q] + (K[q] + s);
+            if (d < bd) { bd = d; best = q; }
+        }
+        if (best < 0) best = 0;                        /* all NaN: the first queue */
+        {
+            double s = 0.0;
+            if (last[best] >= 0 && last[best] != m && pr->swap_cost)
+                s = (double)pr->swap_cost[((int64_t)pr->inst_class[best] * M + last[best]) * M + m];
+            A[best] += a;
+            K[best] += s;
+        }
+        last[best] = m;
+        owner[k] = best;
+        count[best] += 1;
+    }
+    qoff_out[0] = 0;
+    for (int q = 0; q < I; ++q) qoff_out[q + 1] = qoff_out[q] + count[q];
+    for (int q = 0; q < I; ++q) count[q] = 0;
+    for (int k = 0; k < G; ++k) {
+        const int q = owner[k];
+        perm_out[qoff_out[q] + count[q]] = order[k];
+        count[q] += 1;
+    }
+    free(order); free(owner); free(A); free(K); free(last); free(count);
+    return 0;
+}

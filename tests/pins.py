@@ -580,8 +580,108 @@ def pin_search_steepest(orc):
                                                 0, G), flag)
 
 
+# ---------------------------------------------------------------------------
+# Seed plans (EDF order / same-model grouping, each group at the end of the
+# queue with the smallest drain time after taking it, the lowest queue on ties)
+
+
+def _seed_py(pr, policy):
+    """The seed construction restated in Python (float64, same operations)."""
+    G, I, M = int(pr["n_groups"]), int(pr["n_instances"]), int(pr["n_models"])
+    slo = pr["grp_slo"]
+    model = pr["grp_model"]
+    ids = list(range(G))
+    if policy == 0:
+        ids.sort(key=lambda i: (float(slo[i]), i))
+    else:
+        ids.sort(key=lambda i: (int(model[i]), float(slo[i]), i))
+    m0 = pr.get("inst_model0")
+    last = [int(m0[q]) if m0 is not None else -1 for q in range(I)]
+    A = [0.0] * I
+    K = [0.0] * I
+    queues = [[] for _ in range(I)]
+    S = pr.get("swap_cost")
+    for i in ids:
+        m = int(model[i])
+        a = float(pr["grp_count"][i]) * float(pr["grp_mu"][i])
+        best, bd = -1, np.inf
+        for q in range(I):
+            sw = 0.0
+            if last[q] >= 0 and last[q] != m and S is not None:
+                sw = float(S[(int(pr["inst_class"][q]) * M + last[q]) * M + m])
+            d = (A[q] + a) / float(pr["inst_tput"][q]) + (K[q] + sw)
+            if d < bd:
+                best, bd = q, d
+        sw = 0.0
+        if last[best] >= 0 and last[best] != m and S is not None:
+            sw = float(S[(int(pr["inst_class"][best]) * M + last[best]) * M + m])
+        A[best] += a
+        K[best] += sw
+        last[best] = m
+        queues[best].append(i)
+    perm = np.array([i for q in queues for i in q], np.int32)
+    qoff = np.concatenate([[0], np.cumsum([len(q) for q in queues])]).astype(np.int32)
+    return perm, qoff
+
+
+def pin_seed_by_hand(orc):
+    """Four 1-s groups on two 100 tok/s instances, 10 s per model change.
+    EDF order 1 (m1), 3 (m1), 2 (m0), 0 (m0): 1 -> q0 (tie, 1 s each); 3 -> q1
+    (2 s on q0, 1 s on q1); 2 -> q0 (2 + 10 = 12 s either way, tie); 0 -> q1
+    (13 s on q0, 12 s on q1).  Grouped order 2, 0 (m0), 1, 3 (m1): 2 -> q0,
+    0 -> q1, 1 -> q0 (12 s both), 3 -> q1 (13 s against 12 s)."""
+    pr = problem([(1, 100.0, 0.0, 0, 5.0), (1, 100.0, 0.0, 1, 1.0), (1, 100.0, 0.0, 0, 3.0),
+                  (1, 100.0, 0.0, 1, 2.0)], [(100.0, 0), (100.0, 0)], n_models=2, swap=10.0)
+    p, q = orc.seed_plan(pr, 0)
+    assert list(p) == [1, 2, 3, 0] and list(q) == [0, 2, 4], (p, q)
+    p, q = orc.seed_plan(pr, 1)
+    assert list(p) == [2, 1, 0, 3] and list(q) == [0, 2, 4], (p, q)
+
+
+def pin_seed_special_cases(orc):
+    """One queue: the EDF seed is the SLO order (ties by id), the grouped seed
+    the (model, SLO) order.  Equal groups on identical instances go round-robin.
+    On instances of 100 and 300 tok/s, equal 1-s groups split 1 : 3 (the faster
+    instance drains three groups in the time of one)."""
+    rng = np.random.default_rng(8)
+    G = 9
+    slo = np.float32(rng.choice([3.0, 1.0, 7.0], G))
+    model = rng.integers(0, 3, G)
+    pr = problem([(2, 50.0, 10.0, int(model[k]), float(slo[k])) for k in range(G)], [(400.0, 0)],
+                 n_models=3, swap=5.0)
+    p, q = orc.seed_plan(pr, 0)
+    assert list(p) == list(np.lexsort((np.arange(G), slo))) and list(q) == [0, G]
+    p, q = orc.seed_plan(pr, 1)
+    assert list(p) == list(np.lexsort((np.arange(G), slo, model)))
+    # SLOs falling as the ids rise: EDF reverses the ids
+    pr = problem([(1, 10.0, 1.0, 0, float(20 - k)) for k in range(12)], [(400.0, 0)])
+    p, q = orc.seed_plan(pr, 0)
+    assert list(p) == list(range(11, -1, -1)), p
+    pr = problem([(1, 100.0, 0.0, 0, float(k)) for k in range(8)], [(100.0, 0)] * 3)
+    p, q = orc.seed_plan(pr, 0)
+    assert list(p) == [0, 3, 6, 1, 4, 7, 2, 5] and list(q) == [0, 3, 6, 8], (p, q)
+    pr = problem([(1, 100.0, 0.0, 0, float(k)) for k in range(8)], [(100.0, 0), (300.0, 0)])
+    p, q = orc.seed_plan(pr, 0)
+    assert list(q) == [0, 2, 8] and list(p) == [2, 6, 0, 1, 3, 4, 5, 7], (p, q)
+
+
+def pin_seed_restated(orc):
+    """Random problems (heterogeneous instances, swap costs, loaded models):
+    both seeds equal the construction restated in Python, and are plans."""
+    rng = np.random.default_rng(21)
+    for G, I in [(12, 3), (30, 5), (7, 7), (20, 1)]:
+        pr, _ = _random_case(rng, G=G, I=I, M=3, C=2, P=1)
+        for policy in (0, 1):
+            p, q = orc.seed_plan(pr, policy)
+            rp, rq = _seed_py(pr, policy)
+            assert np.array_equal(p, rp) and np.array_equal(q, rq), (G, I, policy)
+            assert sorted(p) == list(range(G)) and q[0] == 0 and q[-1] == G
+            assert np.all(np.diff(q) >= 0)
+
+
 ALL_PINS = [pin_deterministic_queue, pin_variance_queue, pin_normal_table, pin_swap_costs,
             pin_eviction_costs, pin_throughput_per_queue, pin_invariants, pin_half_at_mean,
             pin_identical_instances_symmetry, pin_monte_carlo, pin_edf_special_case,
             pin_grouping_special_case, pin_argmin_ties, pin_moves_by_hand, pin_moves_independent,
-            pin_search_by_hand, pin_search_steepest]
+            pin_search_by_hand, pin_search_steepest, pin_seed_by_hand, pin_seed_special_cases,
+            pin_seed_restated]

@@ -76,6 +76,18 @@ MUTANTS = [
      "if (sc[k] <= bs) { bs = sc[k]; best = k; }"),
     ("move_on_equal_score", "if (best < 0 || !(bs < cur)) break;",
      "if (best < 0 || !(bs <= cur)) break;"),
+    # seed plans
+    ("seed_last_queue_on_ties", "if (d < bd) { bd = d; best = q; }",
+     "if (d <= bd) { bd = d; best = q; }"),
+    ("seed_grouping_ignores_model", "if (g_seed_policy == 1 && pr->grp_model[a] != pr->grp_model[b])",
+     "if (g_seed_policy == 2 && pr->grp_model[a] != pr->grp_model[b])"),
+    ("seed_latest_deadline_first",
+     "if (pr->grp_slo[a] < pr->grp_slo[b]) return -1;\n    if (pr->grp_slo[a] > pr->grp_slo[b]) return 1;",
+     "if (pr->grp_slo[a] > pr->grp_slo[b]) return -1;\n    if (pr->grp_slo[a] < pr->grp_slo[b]) return 1;"),
+    ("seed_drain_without_own_tokens",
+     "const double d = (A[q] + a) / (double)pr->inst_tput[q] + (K[q] + s);",
+     "const double d = A[q] / (double)pr->inst_tput[q] + (K[q] + s);"),
+    ("seed_swap_not_kept", "            K[best] += s;", "            (void)s;"),
 ]
 
 
