@@ -253,6 +253,24 @@ int qlm_local_search(const qlm_problem *problem, const qlm_plans *start,
                      void *ws, size_t ws_bytes, double *score, int32_t *steps,
                      int64_t *trace, qlm_stream stream);
 
+/*
+ * Seed plans for the search: the paper's reference orders, EDF (Sec. 8
+ * baselines) and same-model grouping (Sec. 2, Insight #3).  Groups are taken
+ * in EDF order (SLO, then group id) for policy 0, or by model, then SLO, then
+ * id for policy 1; each is appended to the queue whose drain time after taking
+ * it is smallest, (A_q + n mu) / Theta_q + (K_q + S[class_q][last model][model])
+ * with A_q the queue's tokens and K_q its model-change costs so far (load
+ * balancing by drain time, Sec. 8), the lowest queue on ties.  Seeds evict
+ * nothing.  Limits as for the search; SLOs must not be NaN.
+ *   policy  host array [n], 0 <= n <= 64: the policy of plan k of out
+ *   out     plans 0..n-1 are written (eviction bits, when given, cleared)
+ *   ws      device workspace of at least qlm_seed_workspace_bytes, 256-byte
+ *           aligned, scratch
+ */
+size_t qlm_seed_workspace_bytes(const qlm_problem *problem, int32_t n_seeds);
+int qlm_seed_plans(const qlm_problem *problem, int32_t n, const int32_t *policy,
+                   const qlm_plans_out *out, void *ws, size_t ws_bytes, qlm_stream stream);
+
 /* Largest G the scoring kernels accept for these M, C, I (on-chip budget). */
 int32_t qlm_max_groups(int32_t n_models, int32_t n_classes, int32_t n_instances,
                        int32_t with_eviction);

@@ -67,6 +67,9 @@
 //   k_sout     final plans back to the caller's slot-major layout
 //   k_sswap / k_smove   exact scores of every move, one lane per move
 //              (qlm_search_moves)
+//   k_seedrank / k_seedassign / k_seedwrite   seed plans (qlm_seed_plans):
+//              EDF or same-model order, each group to the queue with the
+//              smallest drain time after it (one wavefront per seed)
 #include <hip/hip_runtime.h>
 
 #include <climits>
@@ -1315,6 +1318,180 @@ __global__ __launch_bounds__(kThreads) void k_sout(SearchArgs a, qlm_plans_out o
 }
 
 // ---------------------------------------------------------------------------
+// Seed plans: groups taken in EDF order (SLO, id) or grouped by model (model,
+// SLO, id), each appended to the queue whose drain time after taking it,
+// (A_q + n mu) / Theta_q + (K_q + model-change cost), is smallest (the lowest
+// queue on ties).  No evictions.
+
+constexpr int kMaxSeeds = 64;
+constexpr size_t kSeedSwapLds = 48 * 1024;     // largest swap table staged in LDS
+
+struct SeedArgs {
+    int32_t G, I, M, C;
+    const int32_t *grp_count;
+    const float *grp_mu, *grp_slo;
+    const int32_t *grp_model;
+    const float *inst_tput;
+    const int32_t *inst_class, *inst_model0;
+    const float *swap_cost;
+    int32_t n;                    // seeds
+    int32_t swap_in_lds;          // the swap table is staged in LDS
+    int8_t policy[kMaxSeeds];     // 0 EDF, 1 grouped
+    int32_t *order, *owner, *pos; // [n][G]: groups in order, their queue and position
+    int32_t *qcount;              // [n][I]
+    qlm_plans_out out;
+};
+
+// Order key of group i: model (when grouping), then the SLO as a number (-0
+// counts as +0); ties go to the lower id.
+__device__ inline uint64_t seed_key(const SeedArgs &a, int pol, int i)
+{
+    float f = a.grp_slo[i];
+    if (f == 0.0f) f = 0.0f;
+    const uint64_t hi = pol == 1 ? (uint64_t)(uint32_t)a.grp_model[i] : 0u;
+    return (hi << 32) | order_key(f);
+}
+
+// Each group's rank in its seed's order (grid: 64 groups x seeds).
+__global__ __launch_bounds__(kThreads) void k_seedrank(SeedArgs a)
+{
+    __shared__ uint64_t keys[kRankTile];
+    __shared__ int part[kThreads];
+    const int seed = blockIdx.y;
+    const int pol = a.policy[seed];
+    const int G = a.G;
+    const int li = threadIdx.x & (kWave - 1), quarter = threadIdx.x / kWave;
+    const int i = blockIdx.x * kWave + li;
+    const uint64_t mine = i < G ? seed_key(a, pol, i) : 0u;
+    int cnt = 0;
+    for (int t0 = 0; t0 < G; t0 += kRankTile) {
+        __syncthreads();
+        for (int k = threadIdx.x; k < kRankTile; k += kThreads)
+            keys[k] = t0 + k < G ? seed_key(a, pol, t0 + k) : ~0ull;
+        __syncthreads();
+        const int base = quarter * (kRankTile / kWaves);
+#pragma unroll 4
+        for (int k = 0; k < kRankTile / kWaves; ++k) {
+            const uint64_t o = keys[base + k];
+            const int id = t0 + base + k;       // ids past G hold the largest key
+            cnt += (o < mine || (o == mine && id < i)) ? 1 : 0;
+        }
+    }
+    part[threadIdx.x] = cnt;
+    __syncthreads();
+    if (quarter == 0 && i < G)
+        a.order[(int64_t)seed * G + part[li] + part[li + kWave] + part[li + 2 * kWave] +
+                part[li + 3 * kWave]] = i;
+}
+
+#pragma clang fp contract(off)
+
+// Placement, one wavefront per seed: groups in order; each lane evaluates the
+// drain time of its queues (q = lane, lane + 64, ...), the lowest drain time
+// (then the lowest queue) wins, and the winning queue takes the group.
+__global__ __launch_bounds__(kWave) void k_seedassign(SeedArgs a)
+{
+    extern __shared__ __align__(16) unsigned char dyn[];
+    const int seed = blockIdx.x;
+    const int G = a.G, I = a.I, M = a.M;
+    const int lane = threadIdx.x;
+    double *qA = reinterpret_cast<double *>(dyn);
+    double *qK = qA + I;
+    int *qlast = reinterpret_cast<int *>(qK + I);
+    int *qcnt = qlast + I;
+    float *sw = reinterpret_cast<float *>(qcnt + I);
+    for (int q = lane; q < I; q += kWave) {
+        qA[q] = 0.0;
+        qK[q] = 0.0;
+        qlast[q] = a.inst_model0 ? clampi(a.inst_model0[q], -1, M - 1) : -1;
+        qcnt[q] = 0;
+    }
+    if (a.swap_in_lds)
+        for (int k = lane; k < a.C * M * M; k += kWave) sw[k] = a.swap_cost[k];
+    const float *swt = a.swap_in_lds ? sw : a.swap_cost;
+    __syncthreads();
+    const int32_t *order = a.order + (int64_t)seed * G;
+    int32_t *owner = a.owner + (int64_t)seed * G;
+    int32_t *pos = a.pos + (int64_t)seed * G;
+    for (int k0 = 0; k0 < G; k0 += kWave) {
+        const int cnt = min(kWave, G - k0);
+        const int il = lane < cnt ? order[k0 + lane] : 0;
+        const double al = (double)a.grp_count[il] * (double)a.grp_mu[il];
+        const int ml = clampi(a.grp_model[il], 0, M - 1);
+        for (int j = 0; j < cnt; ++j) {
+            const double ag = lane_value(al, j);
+            const int mg = __builtin_amdgcn_readlane(ml, j);
+            double bd = INFINITY;
+            int bq = INT_MAX;
+            for (int q = lane; q < I; q += kWave) {
+                const int l = qlast[q];
+                double sc = 0.0;
+                if (l >= 0 && l != mg && a.swap_cost)
+                    sc = (double)swt[((int64_t)clampi(a.inst_class[q], 0, a.C - 1) * M + l) * M + mg];
+                const double d = (qA[q] + ag) / (double)a.inst_tput[q] + (qK[q] + sc);
+                if (d < bd) {
+                    bd = d;
+                    bq = q;
+                }
+            }
+            for (int o = kWave / 2; o > 0; o >>= 1) {
+                const double d2 = __shfl_xor(bd, o, kWave);
+                const int q2 = __shfl_xor(bq, o, kWave);
+                if (d2 < bd || (d2 == bd && q2 < bq)) {
+                    bd = d2;
+                    bq = q2;
+                }
+            }
+            int best = __builtin_amdgcn_readfirstlane(bq);
+            if (best == INT_MAX) best = 0;          // every drain time NaN: the first queue
+            if (lane == (best & (kWave - 1))) {
+                const int l = qlast[best];
+                double sc = 0.0;
+                if (l >= 0 && l != mg && a.swap_cost)
+                    sc = (double)swt[((int64_t)clampi(a.inst_class[best], 0, a.C - 1) * M + l) * M + mg];
+                qA[best] += ag;
+                qK[best] += sc;
+                qlast[best] = mg;
+                owner[k0 + j] = best;
+                pos[k0 + j] = qcnt[best];
+                qcnt[best] += 1;
+            }
+            __syncthreads();
+        }
+    }
+    for (int q = lane; q < I; q += kWave) a.qcount[(int64_t)seed * I + q] = qcnt[q];
+}
+
+#pragma clang fp contract(on)
+
+// The seed plans into the caller's slot-major arrays (one workgroup per seed).
+__global__ __launch_bounds__(kThreads) void k_seedwrite(SeedArgs a)
+{
+    __shared__ int32_t qo[kMaxSearchInstances + 1];
+    const int seed = blockIdx.x;
+    const int G = a.G, I = a.I;
+    const int64_t st = a.out.plan_stride;
+    if (threadIdx.x == 0) {
+        int t = 0;
+        qo[0] = 0;
+        for (int q = 0; q < I; ++q) {
+            t += a.qcount[(int64_t)seed * I + q];
+            qo[q + 1] = t;
+        }
+    }
+    __syncthreads();
+    for (int q = threadIdx.x; q <= I; q += kThreads) a.out.qoff[(int64_t)q * st + seed] = qo[q];
+    for (int k = threadIdx.x; k < G; k += kThreads) {
+        const int64_t o = (int64_t)seed * G + k;
+        const int slot = clampi(qo[clampi(a.owner[o], 0, I - 1)] + a.pos[o], 0, G - 1);
+        a.out.perm[(int64_t)slot * st + seed] = a.order[o];
+    }
+    if (a.out.evict_bits)
+        for (int w = threadIdx.x; w < (G + 31) / 32; w += kThreads)
+            a.out.evict_bits[(int64_t)w * st + seed] = 0u;
+}
+
+// ---------------------------------------------------------------------------
 // Host side
 
 size_t align256(size_t v) { return (v + 255) / 256 * 256; }
@@ -1548,12 +1725,94 @@ int pick_step(SearchArgs &a, int step, hipStream_t stream)
     return launched("k_spick launch");
 }
 
+struct SeedLayout {
+    size_t order, owner, pos, qcount, total;
+};
+
+SeedLayout seed_layout(int G, int I, int n)
+{
+    SeedLayout L{};
+    size_t o = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = o;
+        o += align256(bytes);
+        return at;
+    };
+    L.order = take(4 * (size_t)G * n);
+    L.owner = take(4 * (size_t)G * n);
+    L.pos = take(4 * (size_t)G * n);
+    L.qcount = take(4 * (size_t)I * n);
+    L.total = o;
+    return L;
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------------------
 // C interface
 
 extern "C" {
+
+size_t qlm_seed_workspace_bytes(const qlm_problem *problem, int32_t n_seeds)
+{
+    if (!problem || problem->n_groups < 1 || problem->n_instances < 1 || n_seeds < 0)
+        return 0;
+    return seed_layout(problem->n_groups, problem->n_instances, n_seeds > 0 ? n_seeds : 1).total;
+}
+
+int qlm_seed_plans(const qlm_problem *problem, int32_t n, const int32_t *policy,
+                   const qlm_plans_out *out, void *ws, size_t ws_bytes, qlm_stream stream_)
+{
+    hipStream_t stream = (hipStream_t)stream_;
+    int rc = check_search(problem, 1, 0);
+    if (rc) return rc;
+    if (n < 0 || n > kMaxSeeds) return fail(QLM_ERR_ARG, "seeds: n must be in [0, 64]");
+    if (n == 0) return QLM_OK;
+    if (!policy) return fail(QLM_ERR_ARG, "seeds: policy is NULL");
+    for (int k = 0; k < n; ++k)
+        if (policy[k] != 0 && policy[k] != 1)
+            return fail(QLM_ERR_ARG, "seeds: a policy is neither 0 (EDF) nor 1 (grouped)");
+    if (!out || !out->perm || !out->qoff) return fail(QLM_ERR_ARG, "seeds: out perm and qoff are required");
+    if (out->plan_stride < n) return fail(QLM_ERR_ARG, "seeds: out plan_stride must be >= n");
+    const int G = problem->n_groups, I = problem->n_instances;
+    const SeedLayout L = seed_layout(G, I, n);
+    if (!ws || ((uintptr_t)ws & 255u))
+        return fail(QLM_ERR_WORKSPACE, "workspace must be non-NULL and 256-byte aligned");
+    if (ws_bytes < L.total) return fail(QLM_ERR_WORKSPACE, "workspace too small");
+    SeedArgs a{};
+    a.G = G;
+    a.I = I;
+    a.M = problem->n_models;
+    a.C = problem->n_classes;
+    a.grp_count = problem->grp_count;
+    a.grp_mu = problem->grp_mu;
+    a.grp_slo = problem->grp_slo;
+    a.grp_model = problem->grp_model;
+    a.inst_tput = problem->inst_tput;
+    a.inst_class = problem->inst_class;
+    a.inst_model0 = problem->inst_model0;
+    a.swap_cost = problem->swap_cost;
+    a.n = n;
+    for (int k = 0; k < n; ++k) a.policy[k] = (int8_t)policy[k];
+    unsigned char *w = (unsigned char *)ws;
+    a.order = (int32_t *)(w + L.order);
+    a.owner = (int32_t *)(w + L.owner);
+    a.pos = (int32_t *)(w + L.pos);
+    a.qcount = (int32_t *)(w + L.qcount);
+    a.out = *out;
+    const size_t swap_bytes = problem->swap_cost ? sizeof(float) * (size_t)a.C * a.M * a.M : 0;
+    a.swap_in_lds = swap_bytes > 0 && swap_bytes <= kSeedSwapLds;
+    const size_t lds = 24 * (size_t)I + (a.swap_in_lds ? swap_bytes : 0);
+    hipError_t e = hipFuncSetAttribute((const void *)k_seedassign,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return hip_fail(e, "hipFuncSetAttribute");
+    hipLaunchKernelGGL(k_seedrank, dim3((G + kWave - 1) / kWave, n), dim3(kThreads), 0, stream, a);
+    if ((rc = launched("k_seedrank launch"))) return rc;
+    hipLaunchKernelGGL(k_seedassign, dim3(n), dim3(kWave), lds, stream, a);
+    if ((rc = launched("k_seedassign launch"))) return rc;
+    hipLaunchKernelGGL(k_seedwrite, dim3(n), dim3(kThreads), 0, stream, a);
+    return launched("k_seedwrite launch");
+}
 
 int64_t qlm_search_n_moves(int32_t n_groups, int32_t n_instances, int32_t window)
 {

@@ -7,7 +7,7 @@ run when the library is not built (there is no fallback of any kind).
 Function names follow the C interface: ``rwt_score``, ``rwt_score_exact``,
 ``best_plan`` (with ``best_plan_workspace_bytes``), ``validate_plans``,
 ``validate_problem``, ``search_n_moves``, ``search_workspace_bytes``,
-``search_moves``, ``search_screen``, ``local_search``.
+``search_moves``, ``search_screen``, ``local_search``, ``seed_plans``.
 """
 from __future__ import annotations
 
@@ -91,12 +91,16 @@ def library():
             lib.qlm_search_workspace_bytes.restype = ctypes.c_size_t
             lib.qlm_search_moves.argtypes = [P, PL, i32, vp, ctypes.c_size_t, vp, vp]
             lib.qlm_search_screen.argtypes = [P, PL, i32, vp, ctypes.c_size_t, vp, vp, vp]
+            lib.qlm_seed_workspace_bytes.argtypes = [P, i32]
+            lib.qlm_seed_workspace_bytes.restype = ctypes.c_size_t
+            lib.qlm_seed_plans.argtypes = [P, i32, ctypes.POINTER(ctypes.c_int32),
+                                           ctypes.POINTER(PlansOut), vp, ctypes.c_size_t, vp]
             lib.qlm_local_search.argtypes = [P, PL, ctypes.POINTER(PlansOut), i32, i32, vp,
                                              ctypes.c_size_t, vp, vp, vp, vp]
             for name in ("qlm_rwt_score", "qlm_rwt_score_exact", "qlm_best_plan",
                          "qlm_validate_plans", "qlm_validate_problem", "qlm_timing_enable",
                          "qlm_timing_read", "qlm_search_moves", "qlm_search_screen",
-                         "qlm_local_search"):
+                         "qlm_local_search", "qlm_seed_plans"):
                 getattr(lib, name).restype = ctypes.c_int
             _lib = lib
     return _lib
@@ -346,3 +350,29 @@ def local_search(problem: DeviceProblem, plans: DevicePlans, window: int, max_st
     if trace:
         res["trace"] = tr[:, :max_steps]
     return res
+
+
+EDF, GROUPED = 0, 1
+
+
+def seed_workspace_bytes(problem: DeviceProblem, n_seeds: int) -> int:
+    return int(library().qlm_seed_workspace_bytes(ctypes.byref(problem.struct), n_seeds))
+
+
+def seed_plans(problem: DeviceProblem, policies=(EDF, GROUPED), evict: bool = False, ws=None,
+               stream=None, device="cuda"):
+    """Seed plans (one per policy: EDF = 0, GROUPED = 1) as a DevicePlans; with
+    evict=True the plans carry (cleared) eviction bits."""
+    import torch
+    n = len(policies)
+    G, I = problem.n_groups, problem.n_instances
+    perm = torch.empty((G, max(n, 1)), dtype=torch.int32, device=device)
+    qoff = torch.empty((I + 1, max(n, 1)), dtype=torch.int32, device=device)
+    ev = torch.empty(((G + 31) // 32, max(n, 1)), dtype=torch.int32, device=device) if evict else None
+    if ws is None:
+        ws = torch.empty(max(seed_workspace_bytes(problem, n), 1), dtype=torch.uint8, device=device)
+    pol = (ctypes.c_int32 * max(n, 1))(*policies)
+    o = PlansOut(int(perm.shape[1]), _ptr(perm), _ptr(qoff), _ptr(ev))
+    _check(library().qlm_seed_plans(ctypes.byref(problem.struct), n, pol, ctypes.byref(o),
+                                    _ptr(ws), ws.numel(), _stream(stream)))
+    return DevicePlans(perm, qoff, ev, n)

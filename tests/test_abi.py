@@ -30,7 +30,7 @@ def test_header_declares_entry_points():
                  "qlm_rwt_score_exact", "qlm_validate_plans", "qlm_validate_problem",
                  "qlm_status_string", "qlm_last_error", "qlm_search_n_moves",
                  "qlm_search_workspace_bytes", "qlm_search_moves", "qlm_search_screen",
-                 "qlm_local_search"):
+                 "qlm_local_search", "qlm_seed_workspace_bytes", "qlm_seed_plans"):
         assert must in names
 
 
@@ -142,3 +142,26 @@ def test_search_argument_checks(lib):
     zero = qlm.Plans(0, 1, None, None, None)
     assert ms(P(pr), P(zero), 4, ws, need, 0x1000, None) == qlm.QLM_OK
     assert sc(P(pr), P(zero), 4, ws, need, 0x1000, 0x1000, None) == qlm.QLM_OK
+
+
+def test_seed_argument_checks(lib):
+    """Seed plans: policy, count, output and workspace are checked on the host."""
+    from paper_2407_00047_amd import qlm
+    P = ctypes.byref
+    pr = _problem(qlm, G=8, I=2)
+    need = lib.qlm_seed_workspace_bytes(P(pr), 2)
+    assert need > 0 and lib.qlm_seed_workspace_bytes(P(pr), -1) == 0
+    out = qlm.PlansOut(2, 0x1000, 0x1000, None)
+    pol = (ctypes.c_int32 * 2)(0, 1)
+    bad = (ctypes.c_int32 * 2)(0, 2)
+    ws = 0x10000
+    sp = lib.qlm_seed_plans
+    assert sp(P(pr), 2, bad, P(out), ws, need, None) == qlm.QLM_ERR_ARG
+    assert sp(P(pr), 65, pol, P(out), ws, need, None) == qlm.QLM_ERR_ARG
+    assert sp(P(pr), 2, None, P(out), ws, need, None) == qlm.QLM_ERR_ARG
+    assert sp(P(pr), 2, pol, None, ws, need, None) == qlm.QLM_ERR_ARG
+    short = qlm.PlansOut(1, 0x1000, 0x1000, None)
+    assert sp(P(pr), 2, pol, P(short), ws, need, None) == qlm.QLM_ERR_ARG
+    assert sp(P(pr), 2, pol, P(out), ws, need - 1, None) == qlm.QLM_ERR_WORKSPACE
+    assert sp(P(pr), 2, pol, P(out), ws + 8, need, None) == qlm.QLM_ERR_WORKSPACE
+    assert sp(P(pr), 0, pol, P(out), ws, need, None) == qlm.QLM_OK

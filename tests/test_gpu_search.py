@@ -316,3 +316,43 @@ def test_search_full_size(qlm, orc, name, W):
     assert np.array_equal(out.perm.cpu().numpy()[:, 0], perm)
     assert np.array_equal(out.qoff.cpu().numpy()[:, 0], qoff)
     assert _close(float(r["score"][0]), cur)
+
+
+SEED_CASES = [dict(G=1, I=1), dict(G=5, I=3), dict(G=40, I=5, model0=False), dict(G=97, I=1),
+              dict(G=300, I=12), dict(G=64, I=64), dict(G=200, I=70)]
+
+
+@pytest.mark.parametrize("kw", SEED_CASES, ids=[str(c) for c in SEED_CASES])
+def test_seed_plans(qlm, orc, kw):
+    """Seed plans bit-exact against the oracle's, both policies."""
+    import torch
+    rng = np.random.default_rng(zlib.crc32(("seed" + str(sorted(kw.items()))).encode()))
+    pr, pl = hand_case(rng, P=1, **kw)
+    print("case", kw, flush=True)
+    dpr = device_inputs(pr, pl)[0]
+    sp = qlm.seed_plans(dpr, (0, 1, 0), evict=True)
+    torch.cuda.synchronize()
+    perm = sp.perm.cpu().numpy()
+    qoff = sp.qoff.cpu().numpy()
+    assert np.all(sp.evict_bits.cpu().numpy() == 0)
+    for k, policy in enumerate((0, 1, 0)):
+        p, q = orc.seed_plan(pr, policy)
+        assert np.array_equal(perm[:, k], p), (kw, policy)
+        assert np.array_equal(qoff[:, k], q), (kw, policy)
+
+
+def test_seed_plans_workloads(qlm, orc):
+    """Seed plans of every generated workload, bit-exact, and a search from them."""
+    import torch
+    from paper_2407_00047_amd import workload
+    for name in ("tiny", "mixed", "hetero", "heavy", "large"):
+        pr = workload.make_problem(name)
+        dpr = qlm.DeviceProblem(pr)
+        sp = qlm.seed_plans(dpr, (0, 1))
+        torch.cuda.synchronize()
+        for k in (0, 1):
+            p, q = orc.seed_plan(pr, k)
+            assert np.array_equal(sp.perm.cpu().numpy()[:, k], p), (name, k)
+            assert np.array_equal(sp.qoff.cpu().numpy()[:, k], q), (name, k)
+        sc = qlm.rwt_score_exact(dpr, sp, [0, 1]).cpu().numpy()
+        print(name, "seed scores EDF %.6g grouped %.6g" % tuple(sc), flush=True)
