@@ -92,6 +92,9 @@ class Oracle:
         lib.oracle_local_search.restype = ctypes.c_int
         lib.oracle_seed_plan.argtypes = [ctypes.POINTER(_Problem), i32, vp, vp]
         lib.oracle_seed_plan.restype = ctypes.c_int
+        lib.oracle_place_group.argtypes = [ctypes.POINTER(_Problem), ctypes.POINTER(_Plans), i64,
+                                           i32, vp, vp, vp, dp, vp]
+        lib.oracle_place_group.restype = ctypes.c_int
         self.lib = lib
         self.path = path
 
@@ -195,6 +198,26 @@ class Oracle:
         if self.lib.oracle_seed_plan(ctypes.byref(b.problem), int(policy), _ptr(perm), _ptr(qoff)):
             raise ValueError("policy must be 0 (EDF) or 1 (grouped)")
         return perm, qoff
+
+    def place_group(self, problem, plans, p: int, group: int):
+        """Plan p with `group` moved to the EDF position of the queue giving the
+        lowest exact score (lowest queue on ties): dict perm, qoff, evict_bits,
+        score, queue."""
+        b = _Bound(problem, plans)
+        if not 0 <= p < b.n_plans:
+            raise ValueError("plan index out of range")
+        G, I = b.G, int(problem["n_instances"])
+        perm = np.empty(G, np.int32)
+        qoff = np.empty(I + 1, np.int32)
+        ev = np.empty((G + 31) // 32, np.uint32) if plans.get("evict_bits") is not None else None
+        sc = np.zeros(1)
+        q = np.zeros(1, np.int32)
+        if self.lib.oracle_place_group(ctypes.byref(b.problem), ctypes.byref(b.plans), p,
+                                       int(group), _ptr(perm), _ptr(qoff), _ptr(ev), _dp(sc),
+                                       _ptr(q)):
+            raise ValueError("group not in the plan")
+        return {"perm": perm, "qoff": qoff, "evict_bits": ev, "score": float(sc[0]),
+                "queue": int(q[0])}
 
     def local_search(self, problem, plans, p: int, window: int, max_steps: int,
                      threads: int = 0):
@@ -347,3 +370,7 @@ def local_search(problem, plans, p: int, window: int, max_steps: int, threads: i
 
 def seed_plan(problem, policy: int):
     return default().seed_plan(problem, policy)
+
+
+def place_group(problem, plans, p: int, group: int):
+    return default().place_group(problem, plans, p, group)

@@ -510,3 +510,74 @@ int oracle_seed_plan(const oracle_problem *pr, int32_t policy, int32_t *perm_out
     free(order); free(owner); free(A); free(K); free(last); free(count);
     return 0;
 }
+
+/* ------------------------------------------------------------------------
+ * Placement of one group (a new arrival parked anywhere in the plan, or a
+ * group whose wait violates its SLO): the scheduler call of Sec. 5 for one
+ * group.  The group leaves its queue and is put into queue h before the first
+ * group of h (as h stands after the removal) whose SLO is strictly later (at
+ * the end when there is none), keeping its eviction flag; the h giving the
+ * lowest exact plan score wins, the lowest h on ties.
+ */
+static void place_into(const oracle_problem *pr, const int32_t *perm, const int32_t *qoff,
+                       const uint8_t *flag, int32_t s, int h, int32_t *perm2, int32_t *qoff2,
+                       uint8_t *flag2)
+{
+    const int I = pr->n_instances;
+    const int32_t gi = perm[s];
+    const float slo_i = pr->grp_slo[gi];
+    int32_t out = 0;
+    for (int q = 0; q < I; ++q) {
+        qoff2[q] = out;
+        int placed = (q != h);
+        for (int32_t u = qoff[q]; u < qoff[q + 1]; ++u) {
+            if (u == s) continue;
+            if (!placed && pr->grp_slo[perm[u]] > slo_i) {
+                perm2[out] = gi;  flag2[out] = flag[s];  ++out;  placed = 1;
+            }
+            perm2[out] = perm[u];  flag2[out] = flag[u];  ++out;
+        }
+        if (!placed) { perm2[out] = gi;  flag2[out] = flag[s];  ++out; }
+    }
+    qoff2[I] = out;
+}
+
+/* Places group `group` of plan p; writes the new plan, its exact score and the
+ * chosen queue.  Returns 0, or -1 when the group is not in the plan. */
+int oracle_place_group(const oracle_problem *pr, const oracle_plans *pl, int64_t p, int32_t group,
+                       int32_t *perm_out, int32_t *qoff_out, uint32_t *evict_out, double *score,
+                       int32_t *queue)
+{
+    const int G = pr->n_groups, I = pr->n_instances;
+    const int with_flags = pl->evict_bits != NULL;
+    int32_t *perm = malloc(sizeof(int32_t) * G), *perm2 = malloc(sizeof(int32_t) * G);
+    int32_t *qoff = malloc(sizeof(int32_t) * (I + 1)), *qoff2 = malloc(sizeof(int32_t) * (I + 1));
+    uint8_t *flag = malloc(G), *flag2 = malloc(G);
+    uint32_t *words = malloc(sizeof(uint32_t) * ((G + 31) / 32));
+    take_plan(pr, pl, p, perm, qoff, flag);
+    int32_t s = -1;
+    for (int u = 0; u < G; ++u)
+        if (perm[u] == group) s = u;
+    int best = -1;
+    double bs = INFINITY;
+    if (s >= 0) {
+        for (int h = 0; h < I; ++h) {
+            place_into(pr, perm, qoff, flag, s, h, perm2, qoff2, flag2);
+            const double sc = score_one(pr, perm2, qoff2, flag2, with_flags, words);
+            if (sc < bs) { bs = sc; best = h; }
+        }
+        if (best < 0) best = 0;
+        place_into(pr, perm, qoff, flag, s, best, perm2, qoff2, flag2);
+        memcpy(perm_out, perm2, sizeof(int32_t) * G);
+        memcpy(qoff_out, qoff2, sizeof(int32_t) * (I + 1));
+        if (evict_out) {
+            memset(evict_out, 0, sizeof(uint32_t) * (size_t)((G + 31) / 32));
+            for (int u = 0; u < G; ++u)
+                if (flag2[u]) evict_out[u / 32] |= 1u << (u % 32);
+        }
+        *score = score_one(pr, perm2, qoff2, flag2, with_flags, words);
+        *queue = best;
+    }
+    free(perm); free(perm2); free(qoff); free(qoff2); free(flag); free(flag2); free(words);
+    return s >= 0 ? 0 : -1;
+}

@@ -679,9 +679,82 @@ def pin_seed_restated(orc):
             assert np.all(np.diff(q) >= 0)
 
 
+# ---------------------------------------------------------------------------
+# Placement of one group (arrival / violation trigger)
+
+
+def _place_py(pr, perm, qoff, flag, s, h):
+    """Group at slot s out of its queue, into queue h before the first later SLO
+    (as h stands after the removal), restated on Python lists."""
+    I = int(pr["n_instances"])
+    slo = pr["grp_slo"]
+    qs = [[(int(perm[u]), int(flag[u])) for u in range(qoff[g], qoff[g + 1])] for g in range(I)]
+    g = next(q for q in range(I) if qoff[q] <= s < qoff[q + 1])
+    item = qs[g].pop(s - qoff[g])
+    later = [j for j, (i, _) in enumerate(qs[h]) if slo[i] > slo[item[0]]]
+    qs[h].insert(later[0] if later else len(qs[h]), item)
+    flat = [x for q in qs for x in q]
+    return (np.array([x[0] for x in flat], np.int32),
+            np.concatenate([[0], np.cumsum([len(q) for q in qs])]).astype(np.int32),
+            np.array([x[1] for x in flat], np.uint8))
+
+
+def pin_place_by_hand(orc):
+    """Queue 0 holds groups 0, 1, 2 (1 s each, SLOs 0.5, 0.6, 0.7 s), queue 1 is
+    empty: groups 1 and 2 wait 1 and 2 s and miss.  Placing group 2: in queue 0
+    it goes back to the end (no later SLO), still missing (score 3 + 4); alone in
+    queue 1 it waits 0 s (score 3): queue 1.  With one instance, a group with a
+    0.5 s SLO behind two 10 s groups moves to the head and everything is met."""
+    pr = problem([(2, 200.0, 0.0, 0, 0.5), (3, 100.0, 0.0, 0, 0.6), (4, 100.0, 0.0, 0, 0.7)],
+                 [(300.0, 0), (300.0, 0)])
+    pl = plans([[[0, 1, 2], []]], 3)
+    r = orc.place_group(pr, pl, 0, 2)
+    assert r["queue"] == 1 and list(r["perm"]) == [0, 1, 2] and list(r["qoff"]) == [0, 2, 3]
+    assert r["score"] == 3.0, r["score"]
+    pr = problem([(1, 100.0, 0.0, 0, 10.0), (1, 100.0, 0.0, 0, 10.0), (5, 20.0, 0.0, 0, 0.5)],
+                 [(100.0, 0)])
+    r = orc.place_group(pr, plans([[[0, 1, 2]]], 3), 0, 2)
+    assert r["queue"] == 0 and list(r["perm"]) == [2, 0, 1] and r["score"] == 0.0
+    # equal SLOs are not later: a group goes behind the groups that share its SLO
+    pr = problem([(1, 100.0, 0.0, 0, 1.0)] * 3, [(100.0, 0)])
+    r = orc.place_group(pr, plans([[[2, 0, 1]]], 3), 0, 2)
+    assert list(r["perm"]) == [0, 1, 2], r["perm"]
+
+
+def pin_place_restated(orc):
+    """Random plans: the placed plan is the first minimum over every queue of
+    the placement restated in Python and scored as a plan; for other queues the
+    candidate is the reassignment move MOVE(s, h)."""
+    rng = np.random.default_rng(31)
+    for G, I, evict in [(9, 3, True), (12, 4, False), (6, 1, True)]:
+        pr, pl = _random_case(rng, G=G, I=I, M=2, C=2, P=3, evict=evict)
+        for p in range(pl["n_plans"]):
+            perm = pl["perm"][:, p].copy()
+            qoff = pl["qoff"][:, p].copy()
+            flag = _flags_of(pl, p, G)
+            ms = orc.move_scores(pr, pl, p, 0)
+            for group in (0, G - 1, G // 2):
+                s = int(np.flatnonzero(perm == group)[0])
+                g = next(q for q in range(I) if qoff[q] <= s < qoff[q + 1])
+                best, bs, bplan = -1, np.inf, None
+                for h in range(I):
+                    c = _place_py(pr, perm, qoff, flag, s, h)
+                    v = orc.plan_detail(pr, _one_plan(*c, evict), 0)["score"]
+                    if h != g:
+                        assert v == ms[s * I + h], (h, v, ms[s * I + h])
+                    if v < bs:
+                        best, bs, bplan = h, v, c
+                r = orc.place_group(pr, pl, p, group)
+                assert r["queue"] == best and r["score"] == bs, (r["queue"], best, r["score"], bs)
+                assert np.array_equal(r["perm"], bplan[0]) and np.array_equal(r["qoff"], bplan[1])
+                if evict:
+                    assert np.array_equal(_flags_of({"evict_bits": r["evict_bits"].reshape(-1, 1)},
+                                                    0, G), bplan[2])
+
+
 ALL_PINS = [pin_deterministic_queue, pin_variance_queue, pin_normal_table, pin_swap_costs,
             pin_eviction_costs, pin_throughput_per_queue, pin_invariants, pin_half_at_mean,
             pin_identical_instances_symmetry, pin_monte_carlo, pin_edf_special_case,
             pin_grouping_special_case, pin_argmin_ties, pin_moves_by_hand, pin_moves_independent,
             pin_search_by_hand, pin_search_steepest, pin_seed_by_hand, pin_seed_special_cases,
-            pin_seed_restated]
+            pin_seed_restated, pin_place_by_hand, pin_place_restated]

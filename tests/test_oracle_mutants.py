@@ -88,6 +88,16 @@ MUTANTS = [
      "const double d = (A[q] + a) / (double)pr->inst_tput[q] + (K[q] + s);",
      "const double d = A[q] / (double)pr->inst_tput[q] + (K[q] + s);"),
     ("seed_swap_not_kept", "            K[best] += s;", "            (void)s;"),
+    # placement of one group
+    ("place_last_queue_on_ties", "if (sc < bs) { bs = sc; best = h; }",
+     "if (sc <= bs) { bs = sc; best = h; }"),
+    ("place_own_queue_skipped",
+     "            place_into(pr, perm, qoff, flag, s, h, perm2, qoff2, flag2);\n            const double sc",
+     "            if (qoff[h] <= s && s < qoff[h + 1]) continue;\n"
+     "            place_into(pr, perm, qoff, flag, s, h, perm2, qoff2, flag2);\n            const double sc"),
+    ("place_before_equal_slo",
+     "            if (!placed && pr->grp_slo[perm[u]] > slo_i) {\n                perm2[out] = gi;  flag2[out] = flag[s];  ++out;  placed = 1;\n            }\n            perm2[out] = perm[u];  flag2[out] = flag[u];  ++out;\n        }\n        if (!placed) { perm2[out] = gi;  flag2[out] = flag[s];  ++out; }\n    }\n    qoff2[I] = out;\n}\n\n/* Places",
+     "            if (!placed && pr->grp_slo[perm[u]] >= slo_i) {\n                perm2[out] = gi;  flag2[out] = flag[s];  ++out;  placed = 1;\n            }\n            perm2[out] = perm[u];  flag2[out] = flag[u];  ++out;\n        }\n        if (!placed) { perm2[out] = gi;  flag2[out] = flag[s];  ++out; }\n    }\n    qoff2[I] = out;\n}\n\n/* Places"),
 ]
 
 
