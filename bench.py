@@ -293,6 +293,78 @@ def bench_search(args):
     print(json.dumps(res), flush=True)
 
 
+PLACE_METRIC = "group placements per second (arrival / violation re-score, exact), 1 GPU"
+
+
+def cpu_place_baseline(problem, plans, groups, seconds: float):
+    import oracle
+    orc = oracle.default()
+    G = problem["n_groups"]
+    t0 = time.perf_counter()
+    n = 0
+    while n == 0 or time.perf_counter() - t0 < seconds:
+        orc.place_group(problem, plans, 0, groups[n % len(groups)] % G)
+        n += 1
+    dt = time.perf_counter() - t0
+    return {"value": n / dt, "unit": "updates/s", "cores": 1, "kind": "oracle",
+            "sample": "%d placements of the timed groups into plan 0 of the same batch, each "
+                      "candidate plan built and scored from scratch by the fp64 C oracle (one "
+                      "thread), %.1f s" % (n, dt)}
+
+
+def bench_place(args):
+    """One update = one qlm_place_group call on every plan: the cache of each
+    plan, the group scored exactly in every queue, the best placement applied."""
+    import torch
+    from paper_2407_00047_amd import qlm, workload
+    dev = torch.device("cuda:0")
+    B, K = args.chains, args.steps
+    pr = workload.make_problem(args.config)
+    pl = workload.make_plans(pr, 0, B)
+    G, I = pr["n_groups"], pr["n_instances"]
+    dpr = qlm.DeviceProblem(pr, device=dev)
+    dpl = qlm.DevicePlans.from_host(pl, device=dev)
+    ws = qlm.search_workspace(dpr, B, 0, device=dev)
+    groups = [(g * 7919) % G for g in range(K)]
+    for _ in range(max(args.warmup, 1)):
+        qlm.place_group(dpr, dpl, groups[0], ws=ws)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    qlm.timing_enable(True)
+    qlm.timing_read()
+    e0.record(stream)
+    for g in groups:
+        qlm.place_group(dpr, dpl, g, ws=ws)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    n_launch, k_ms = qlm.timing_read()
+    qlm.timing_enable(False)
+    ms = e0.elapsed_time(e1) / K
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle ...")
+        cpu = cpu_place_baseline(pr, pl, groups, args.cpu_seconds)
+    N = workload.total_requests(pr)
+    res = {
+        "metric": PLACE_METRIC, "value": round(B / (ms / 1e3), 1), "unit": "updates/s",
+        "n_gpus": 1, "steps": K, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "us_per_update": round(1e3 * ms, 2), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+        "config": {"workload": "placement of one group in %d plan(s) of %s: %d groups (%d "
+                               "requests), %d instances" % (B, args.config, G, N, I),
+                   "plans": B, "groups": G, "instances": I},
+        "candidate_kernel_avg_ms": round(k_ms / max(n_launch, 1), 4),
+        "roofline": {"bound": "latency", "achieved": round(1e3 * ms, 2), "peak": None,
+                     "unit": "us/update", "frac": None, "traffic": None,
+                     "kernel": "k_place_eval",
+                     "note": "a chain of dependent launches; the latency, not a rate, bounds it"},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -307,7 +379,9 @@ def main():
                     help="run a plain 1 GiB device copy (for HBM counter scaling) and exit")
     ap.add_argument("--search", action="store_true",
                     help="benchmark the plan search (local search steps) instead")
-    ap.add_argument("--chains", type=int, default=1, help="--search: start plans")
+    ap.add_argument("--place", action="store_true",
+                    help="benchmark the placement of one group (arrival re-score) instead")
+    ap.add_argument("--chains", type=int, default=1, help="--search / --place: plans")
     ap.add_argument("--window", type=int, default=16, help="--search: swap window")
     ap.add_argument("--summarize-counters", nargs=4, metavar=("FETCH", "WRITE", "COPY_FETCH", "COPY_WRITE"),
                     help="rocprofv3 --pmc output folders: write the traffic summary and exit")
@@ -339,6 +413,9 @@ def main():
     qlm.library()
     if args.search:
         bench_search(args)
+        return
+    if args.place:
+        bench_place(args)
         return
 
     cfg = workload.CONFIGS[args.config]

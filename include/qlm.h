@@ -254,6 +254,26 @@ int qlm_local_search(const qlm_problem *problem, const qlm_plans *start,
                      int64_t *trace, qlm_stream stream);
 
 /*
+ * Placement of one group in every plan: the scheduler call of Sec. 5 when a
+ * group arrives (the caller parks it anywhere in the plan first) or when its
+ * wait violates its SLO.  In plan p the group leaves its queue and goes into
+ * queue h before the first group of h (as h stands after the removal) whose
+ * SLO is strictly later, at the end when there is none, keeping its eviction
+ * flag; of the I choices (its own queue included) the one with the lowest
+ * exact plan score wins, the lowest h on ties.  Only the two queues that
+ * change are walked, from the first position that changes.
+ *   start/out  as for qlm_local_search (out may name the start arrays)
+ *   group      the group's id; every plan holds it
+ *   ws         device workspace of at least qlm_search_workspace_bytes(problem,
+ *              P, 0), 256-byte aligned, scratch
+ *   score [P]  device out or NULL: exact score of each placed plan
+ *   queue [P]  device out or NULL: the queue chosen
+ */
+int qlm_place_group(const qlm_problem *problem, const qlm_plans *start,
+                    const qlm_plans_out *out, int32_t group, void *ws, size_t ws_bytes,
+                    double *score, int32_t *queue, qlm_stream stream);
+
+/*
  * Seed plans for the search: the paper's reference orders, EDF (Sec. 8
  * baselines) and same-model grouping (Sec. 2, Insight #3).  Groups are taken
  * in EDF order (SLO, then group id) for policy 0, or by model, then SLO, then
@@ -282,9 +302,10 @@ const char *qlm_last_error(void);
 /*
  * Optional launch timing for benchmarks: when enabled, the dominant kernel of
  * each call is bracketed by HIP events on the call's stream: the plan-scoring
- * kernel of every qlm_rwt_score / qlm_best_plan call, and the kernel that
- * scores the reassignment moves in every qlm_search_moves call and every step
- * of qlm_local_search.  qlm_timing_read waits for the recorded events and
+ * kernel of every qlm_rwt_score / qlm_best_plan call, the kernel that scores
+ * the reassignment moves in every qlm_search_moves / qlm_search_screen call
+ * and every step of qlm_local_search, and the candidate kernel of every
+ * qlm_place_group call.  qlm_timing_read waits for the recorded events and
  * returns the number of timed launches and their summed duration in
  * milliseconds since the last reset, then resets.
  */

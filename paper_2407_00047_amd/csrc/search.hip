@@ -67,6 +67,9 @@
 //   k_sout     final plans back to the caller's slot-major layout
 //   k_sswap / k_smove   exact scores of every move, one lane per move
 //              (qlm_search_moves)
+//   k_place_eval / k_place_pick   placement of one group (qlm_place_group):
+//              one wavefront per (plan, queue) scores the group placed there
+//              exactly; the lowest score is applied
 //   k_seedrank / k_seedassign / k_seedwrite   seed plans (qlm_seed_plans):
 //              EDF or same-model order, each group to the queue with the
 //              smallest drain time after it (one wavefront per seed)
@@ -503,6 +506,22 @@ __global__ __launch_bounds__(kThreads) void k_srank(SearchArgs a)
     __syncthreads();
     if (quarter == 0 && i < G)
         a.by_slo[part[li] + part[li + kWave] + part[li + 2 * kWave] + part[li + 3 * kWave]] = i;
+}
+
+// Group records only (when no screen runs).
+__global__ __launch_bounds__(kThreads) void k_sgrec(SearchArgs a)
+{
+    const int i = blockIdx.x * kThreads + threadIdx.x;
+    if (i >= a.G) return;
+    const uint32_t n = (uint32_t)clampi(a.grp_count[i], 0, (int)kCountMask);
+    const double dn = (double)n;
+    GRec r;
+    r.a = dn * (double)a.grp_mu[i];
+    r.b = dn * (double)a.grp_var[i];
+    r.slo = a.grp_slo[i];
+    r.nm = (n << kCountShift) | (uint32_t)clampi(a.grp_model[i], 0, a.M - 1);
+    r.pad[0] = r.pad[1] = 0u;
+    a.grec[i] = r;
 }
 
 // The normal-tail table, once per call, for the screens to copy into LDS.
@@ -1205,6 +1224,42 @@ __global__ __launch_bounds__(kThreads) void k_sexact(SearchArgs a)
 
 #pragma clang fp contract(on)
 
+// Moves the group at slot s of chain b to queue h, before the first group of h
+// whose SLO is strictly later (a reassignment, or with h its own queue a
+// re-insertion): the slots between its old and new place rotate by one, and
+// the queue offsets between the two queues shift.  Run by a whole workgroup.
+__device__ void place_apply(const SearchArgs &a, int64_t b, int s, int h)
+{
+    const int G = a.G, I = a.I;
+    int32_t *perm = a.perm + b * G;
+    uint8_t *flag = a.flag + b * G;
+    int32_t *qof = a.qof + b * (I + 1);
+    const SRec *sr = a.srec + b * G;
+    const int g = (int)sr[s].q;
+    const int p = insertion_point(sr, qof[h], qof[h + 1], sr[s].slo);
+    // left: the group goes later (to slot p - 1); right: earlier (to slot p)
+    const bool left = h > g || (h == g && p > s);
+    const int lo = left ? s : p;
+    const int hi = left ? p - 1 : s;
+    int32_t *sp = a.scratch + b * 2 * G;
+    int32_t *sf = sp + G;
+    for (int u = lo + threadIdx.x; u <= hi; u += kThreads) {
+        sp[u] = perm[u];
+        sf[u] = flag[u];
+    }
+    __syncthreads();
+    for (int u = lo + threadIdx.x; u <= hi; u += kThreads) {
+        const int v = left ? (u == hi ? s : u + 1) : (u == lo ? s : u - 1);
+        perm[u] = sp[v];
+        flag[u] = (uint8_t)sf[v];
+    }
+    if (h > g) {
+        for (int q = g + 1 + threadIdx.x; q <= h; q += kThreads) qof[q] -= 1;
+    } else if (h < g) {
+        for (int q = h + 1 + threadIdx.x; q <= g; q += kThreads) qof[q] += 1;
+    }
+}
+
 // The lowest exact score among the candidates (lowest k on ties); applied when
 // it improves on the plan.
 __global__ __launch_bounds__(kThreads) void k_spick(SearchArgs a, int step)
@@ -1243,7 +1298,6 @@ __global__ __launch_bounds__(kThreads) void k_spick(SearchArgs a, int step)
     if (!apply) return;
     int32_t *perm = a.perm + b * G;
     uint8_t *flag = a.flag + b * G;
-    int32_t *qof = a.qof + b * (I + 1);
     const int64_t k = kk;
     if (k < (int64_t)G * W) {
         if (threadIdx.x == 0) {
@@ -1258,34 +1312,7 @@ __global__ __launch_bounds__(kThreads) void k_spick(SearchArgs a, int step)
         return;
     }
     const int64_t r = k - (int64_t)G * W;
-    const int s = (int)(r / I), h = (int)(r % I);
-    const SRec *sr = a.srec + b * G;
-    const int g = (int)sr[s].q;
-    const int p = insertion_point(sr, qof[h], qof[h + 1], sr[s].slo);
-    // the slots from s to the insertion point rotate by one
-    const int lo = h > g ? s : p;
-    const int hi = h > g ? p - 1 : s;
-    int32_t *sp = a.scratch + b * 2 * G;
-    int32_t *sf = sp + G;
-    for (int u = lo + threadIdx.x; u <= hi; u += kThreads) {
-        sp[u] = perm[u];
-        sf[u] = flag[u];
-    }
-    __syncthreads();
-    for (int u = lo + threadIdx.x; u <= hi; u += kThreads) {
-        int v;
-        if (h > g)
-            v = u == hi ? s : u + 1;          // left by one, the group at the end
-        else
-            v = u == lo ? s : u - 1;          // right by one, the group at the front
-        perm[u] = sp[v];
-        flag[u] = (uint8_t)sf[v];
-    }
-    if (h > g) {
-        for (int q = g + 1 + threadIdx.x; q <= h; q += kThreads) qof[q] -= 1;
-    } else {
-        for (int q = h + 1 + threadIdx.x; q <= g; q += kThreads) qof[q] += 1;
-    }
+    place_apply(a, b, (int)(r / I), (int)(r % I));
 }
 
 // Final plans to the caller's slot-major arrays, with their scores and steps.
@@ -1315,6 +1342,99 @@ __global__ __launch_bounds__(kThreads) void k_sout(SearchArgs a, qlm_plans_out o
             if (steps) steps[b] = a.steps[b];
         }
     }
+}
+
+// ---------------------------------------------------------------------------
+// Placement of one group (qlm_place_group)
+
+#pragma clang fp contract(off)
+
+// Exact score of each plan with its group `group` placed in queue h, one
+// wavefront per (plan, h).
+__global__ __launch_bounds__(kThreads) void k_place_eval(SearchArgs a, int group)
+{
+    const int G = a.G, I = a.I;
+    const int nblk = (I + kWaves - 1) / kWaves;
+    const int64_t b = blockIdx.x / nblk;
+    const int h = (blockIdx.x % nblk) * kWaves + wave_id();
+    if (h >= I) return;
+    const SRec *__restrict__ sr = a.srec + b * G;
+    const SSt *__restrict__ ss = a.sst + b * G;
+    const int32_t *__restrict__ qof = a.qof + b * (I + 1);
+    const double *T = a.T + b * (I + 1);
+    const double *Q = a.Q + b * I;
+    const int s = __builtin_amdgcn_readfirstlane(clampi(a.inv[b * G + group], 0, G - 1));
+    const SRec x = sr[s];
+    const int g = (int)x.q;
+    const int bq = qof[h], eq = qof[h + 1];
+    const double theta = (double)a.inst_tput[h];
+    const int cls = clampi(a.inst_class[h], 0, a.C - 1);
+    const int p = insertion_point(sr, bq, eq, x.slo);
+    double score;
+    if (h == g) {
+        // its own queue: from the first position that changes, the queue without
+        // s with the group at the insertion point
+        const int st = min(s, p);
+        Run r = start_at(a, sr, ss, st, bq, g);
+        if (p <= s)
+            wave_walk(r, eq - st, [&](int v) { return v == 0 ? x : (v <= s - p ? sr[p + v - 1] : sr[p + v]); },
+                      theta, cls, a, NoOut{});
+        else
+            wave_walk(r, eq - st, [&](int v) {
+                return v < p - s - 1 ? sr[s + 1 + v] : (v == p - s - 1 ? x : sr[s + v]);
+            }, theta, cls, a, NoOut{});
+        score = total_with(T, Q, I, g, r.sc);
+    } else {
+        Run r;
+        if (bq == eq) {
+            r = Run{0.0, 0.0, 0.0, 0.0, model0_of(a, h)};
+            wave_walk(r, 1, [&](int) { return x; }, theta, cls, a, NoOut{});
+        } else if (p == eq) {
+            r = start_at(a, sr, ss, eq - 1, bq, h);
+            wave_walk(r, 2, [&](int v) { return v == 0 ? sr[eq - 1] : x; }, theta, cls, a, NoOut{});
+        } else {
+            r = start_at(a, sr, ss, p, bq, h);
+            wave_walk(r, eq - p + 1, [&](int v) { return v == 0 ? x : sr[p + v - 1]; }, theta, cls,
+                      a, NoOut{});
+        }
+        const double nh = r.sc;
+        const int bg = qof[g], eg = qof[g + 1];
+        Run rg = start_at(a, sr, ss, s, bg, g);
+        wave_walk(rg, eg - s - 1, [&](int v) { return sr[s + 1 + v]; }, (double)a.inst_tput[g],
+                  clampi(a.inst_class[g], 0, a.C - 1), a, NoOut{});
+        score = total_with2(T, Q, I, g, rg.sc, h, nh);
+    }
+    if ((threadIdx.x & (kWave - 1)) == 0) a.cex[b * a.n_moves + h] = score;
+}
+
+#pragma clang fp contract(on)
+
+// The queue with the lowest exact score (lowest h on ties), applied.
+__global__ __launch_bounds__(kThreads) void k_place_pick(SearchArgs a, int group, int32_t *queue)
+{
+    __shared__ double ls[kWaves];
+    __shared__ int64_t lk[kWaves];
+    __shared__ int64_t kk;
+    const int64_t b = blockIdx.x;
+    const int G = a.G, I = a.I;
+    double best = INFINITY;
+    int64_t bk = INT64_MAX;
+    for (int h = threadIdx.x; h < I; h += kThreads) {
+        const double v = a.cex[b * a.n_moves + h];
+        if (better(v, h, best, bk)) {
+            best = v;
+            bk = h;
+        }
+    }
+    block_best(best, bk, ls, lk);
+    if (threadIdx.x == 0) {
+        if (bk < 0 || bk >= I) bk = 0;            // every score NaN: the first queue
+        kk = bk;
+        a.cur[b] = a.cex[b * a.n_moves + bk];
+        if (queue) queue[b] = (int32_t)bk;
+    }
+    __syncthreads();
+    place_apply(a, b, clampi(a.inv[b * G + group], 0, G - 1), (int)kk);
 }
 
 // ---------------------------------------------------------------------------
@@ -1638,9 +1758,10 @@ int launched(const char *what)
     return e == hipSuccess ? QLM_OK : hip_fail(e, what);
 }
 
-// Checks, and the group records and ranks.
+// Checks, the group records, and (for the screens) the SLO ranks and the tail
+// table.
 int search_begin(const qlm_problem *pr, const qlm_plans *pl, int32_t W, void *ws, size_t ws_bytes,
-                 SearchArgs *out, hipStream_t stream)
+                 SearchArgs *out, hipStream_t stream, bool screens = true)
 {
     int rc = check_search(pr, pl ? pl->n_plans : 0, W);
     if (rc) return rc;
@@ -1654,6 +1775,10 @@ int search_begin(const qlm_problem *pr, const qlm_plans *pl, int32_t W, void *ws
     SearchArgs a = search_args(pr, B, W, (unsigned char *)ws, L);
     *out = a;
     if (B == 0) return QLM_OK;
+    if (!screens) {
+        hipLaunchKernelGGL(k_sgrec, dim3((a.G + kThreads - 1) / kThreads), dim3(kThreads), 0, stream, a);
+        return launched("k_sgrec launch");
+    }
     hipLaunchKernelGGL(k_srank, dim3((a.G + kWave - 1) / kWave), dim3(kThreads), 0, stream, a);
     rc = launched("k_srank launch");
     if (rc) return rc;
@@ -1812,6 +1937,47 @@ int qlm_seed_plans(const qlm_problem *problem, int32_t n, const int32_t *policy,
     if ((rc = launched("k_seedassign launch"))) return rc;
     hipLaunchKernelGGL(k_seedwrite, dim3(n), dim3(kThreads), 0, stream, a);
     return launched("k_seedwrite launch");
+}
+
+int qlm_place_group(const qlm_problem *problem, const qlm_plans *start, const qlm_plans_out *out,
+                    int32_t group, void *ws, size_t ws_bytes, double *score, int32_t *queue,
+                    qlm_stream stream_)
+{
+    hipStream_t stream = (hipStream_t)stream_;
+    if (!out) return fail(QLM_ERR_ARG, "out is NULL");
+    if (!problem || group < 0 || group >= problem->n_groups)
+        return fail(QLM_ERR_ARG, "group must be in [0, n_groups)");
+    if (start && start->n_plans > 0) {
+        if (!out->perm || !out->qoff) return fail(QLM_ERR_ARG, "out perm and qoff are required");
+        if (out->plan_stride < start->n_plans)
+            return fail(QLM_ERR_ARG, "out plan_stride must be >= n_plans");
+        if (start->evict_bits && !out->evict_bits)
+            return fail(QLM_ERR_ARG, "out evict_bits is required when the plans have eviction bits");
+    }
+    SearchArgs a;
+    int rc = search_begin(problem, start, 0, ws, ws_bytes, &a, stream, false);
+    if (rc) return rc;
+    if (a.B == 0) return QLM_OK;
+    rc = load_and_state(a, start, stream);
+    if (rc) return rc;
+    const int nblk = (a.I + kWaves - 1) / kWaves;
+    qlm_internal::TimedLaunch tl;
+    if ((rc = qlm_internal::timing_begin(stream, &tl))) return rc;
+    hipLaunchKernelGGL(k_place_eval, dim3((unsigned)(nblk * a.B)), dim3(kThreads), 0, stream, a,
+                       group);
+    if ((rc = launched("k_place_eval launch"))) return rc;
+    qlm_internal::timing_end(stream, &tl);
+    hipLaunchKernelGGL(k_place_pick, dim3((unsigned)a.B), dim3(kThreads), 0, stream, a, group,
+                       queue);
+    if ((rc = launched("k_place_pick launch"))) return rc;
+    qlm_plans_out o = *out;
+    if (!start->evict_bits) o.evict_bits = nullptr;
+    const int64_t rows = (int64_t)a.G + a.I + 1 + (o.evict_bits ? (a.G + 31) / 32 : 0) + 1;
+    int64_t grid = (rows * a.B + kThreads - 1) / kThreads;
+    if (grid > 65536) grid = 65536;
+    hipLaunchKernelGGL(k_sout, dim3((unsigned)grid), dim3(kThreads), 0, stream, a, o, score,
+                       (int32_t *)nullptr);
+    return launched("k_sout launch");
 }
 
 int64_t qlm_search_n_moves(int32_t n_groups, int32_t n_instances, int32_t window)

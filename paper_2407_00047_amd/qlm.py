@@ -7,7 +7,8 @@ run when the library is not built (there is no fallback of any kind).
 Function names follow the C interface: ``rwt_score``, ``rwt_score_exact``,
 ``best_plan`` (with ``best_plan_workspace_bytes``), ``validate_plans``,
 ``validate_problem``, ``search_n_moves``, ``search_workspace_bytes``,
-``search_moves``, ``search_screen``, ``local_search``, ``seed_plans``.
+``search_moves``, ``search_screen``, ``local_search``, ``seed_plans``,
+``place_group``.
 """
 from __future__ import annotations
 
@@ -91,6 +92,8 @@ def library():
             lib.qlm_search_workspace_bytes.restype = ctypes.c_size_t
             lib.qlm_search_moves.argtypes = [P, PL, i32, vp, ctypes.c_size_t, vp, vp]
             lib.qlm_search_screen.argtypes = [P, PL, i32, vp, ctypes.c_size_t, vp, vp, vp]
+            lib.qlm_place_group.argtypes = [P, PL, ctypes.POINTER(PlansOut), i32, vp,
+                                            ctypes.c_size_t, vp, vp, vp]
             lib.qlm_seed_workspace_bytes.argtypes = [P, i32]
             lib.qlm_seed_workspace_bytes.restype = ctypes.c_size_t
             lib.qlm_seed_plans.argtypes = [P, i32, ctypes.POINTER(ctypes.c_int32),
@@ -100,7 +103,7 @@ def library():
             for name in ("qlm_rwt_score", "qlm_rwt_score_exact", "qlm_best_plan",
                          "qlm_validate_plans", "qlm_validate_problem", "qlm_timing_enable",
                          "qlm_timing_read", "qlm_search_moves", "qlm_search_screen",
-                         "qlm_local_search", "qlm_seed_plans"):
+                         "qlm_local_search", "qlm_seed_plans", "qlm_place_group"):
                 getattr(lib, name).restype = ctypes.c_int
             _lib = lib
     return _lib
@@ -376,3 +379,26 @@ def seed_plans(problem: DeviceProblem, policies=(EDF, GROUPED), evict: bool = Fa
     _check(library().qlm_seed_plans(ctypes.byref(problem.struct), n, pol, ctypes.byref(o),
                                     _ptr(ws), ws.numel(), _stream(stream)))
     return DevicePlans(perm, qoff, ev, n)
+
+
+def place_group(problem: DeviceProblem, plans: DevicePlans, group: int, ws=None, stream=None,
+                out: DevicePlans | None = None):
+    """Every plan with `group` moved to the EDF position of its best queue:
+    dict with the placed plans (DevicePlans), their exact scores [P] f64 and
+    the chosen queues [P] int32."""
+    import torch
+    dev = plans.perm.device
+    P = plans.n_plans
+    if ws is None:
+        ws = search_workspace(problem, P, 0, dev)
+    if out is None:
+        out = DevicePlans(torch.empty_like(plans.perm), torch.empty_like(plans.qoff),
+                          None if plans.evict_bits is None else torch.empty_like(plans.evict_bits),
+                          P)
+    o = PlansOut(int(out.perm.shape[1]), _ptr(out.perm), _ptr(out.qoff), _ptr(out.evict_bits))
+    score = torch.empty(P, dtype=torch.float64, device=dev)
+    queue = torch.empty(P, dtype=torch.int32, device=dev)
+    _check(library().qlm_place_group(ctypes.byref(problem.struct), ctypes.byref(plans.struct),
+                                     ctypes.byref(o), int(group), _ptr(ws), ws.numel(),
+                                     _ptr(score), _ptr(queue), _stream(stream)))
+    return {"plans": out, "score": score, "queue": queue}

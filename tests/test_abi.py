@@ -30,7 +30,8 @@ def test_header_declares_entry_points():
                  "qlm_rwt_score_exact", "qlm_validate_plans", "qlm_validate_problem",
                  "qlm_status_string", "qlm_last_error", "qlm_search_n_moves",
                  "qlm_search_workspace_bytes", "qlm_search_moves", "qlm_search_screen",
-                 "qlm_local_search", "qlm_seed_workspace_bytes", "qlm_seed_plans"):
+                 "qlm_local_search", "qlm_seed_workspace_bytes", "qlm_seed_plans",
+                 "qlm_place_group"):
         assert must in names
 
 
@@ -165,3 +166,19 @@ def test_seed_argument_checks(lib):
     assert sp(P(pr), 2, pol, P(out), ws, need - 1, None) == qlm.QLM_ERR_WORKSPACE
     assert sp(P(pr), 2, pol, P(out), ws + 8, need, None) == qlm.QLM_ERR_WORKSPACE
     assert sp(P(pr), 0, pol, P(out), ws, need, None) == qlm.QLM_OK
+
+
+def test_place_argument_checks(lib):
+    from paper_2407_00047_amd import qlm
+    P = ctypes.byref
+    pr = _problem(qlm, G=8, I=2)
+    pl = qlm.Plans(3, 3, 0x1000, 0x1000, None)
+    need = lib.qlm_search_workspace_bytes(P(pr), 3, 0)
+    out = qlm.PlansOut(3, 0x1000, 0x1000, None)
+    pg = lib.qlm_place_group
+    assert pg(P(pr), P(pl), None, 0, 0x10000, need, None, None, None) == qlm.QLM_ERR_ARG
+    assert pg(P(pr), P(pl), P(out), 8, 0x10000, need, None, None, None) == qlm.QLM_ERR_ARG
+    assert pg(P(pr), P(pl), P(out), -1, 0x10000, need, None, None, None) == qlm.QLM_ERR_ARG
+    assert pg(P(pr), P(pl), P(out), 1, 0x10000, need - 1, None, None, None) == qlm.QLM_ERR_WORKSPACE
+    zero = qlm.Plans(0, 1, None, None, None)
+    assert pg(P(pr), P(zero), P(out), 1, 0x10000, need, None, None, None) == qlm.QLM_OK

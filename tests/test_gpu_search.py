@@ -356,3 +356,76 @@ def test_seed_plans_workloads(qlm, orc):
             assert np.array_equal(sp.qoff.cpu().numpy()[:, k], q), (name, k)
         sc = qlm.rwt_score_exact(dpr, sp, [0, 1]).cpu().numpy()
         print(name, "seed scores EDF %.6g grouped %.6g" % tuple(sc), flush=True)
+
+
+PLACE_CASES = [dict(G=1, I=1, P=2), dict(G=5, I=3, P=9), dict(G=33, I=2, P=8, evict=False),
+               dict(G=70, I=4, P=6, empty_queues=True), dict(G=97, I=1, P=3),
+               dict(G=64, I=64, P=4), dict(G=300, I=12, P=4, skewed=True)]
+
+
+@pytest.mark.parametrize("kw", PLACE_CASES, ids=[str(c) for c in PLACE_CASES])
+def test_place_group(qlm, orc, kw):
+    """Placed plans bit-exact, chosen queues and exact scores against the oracle
+    (a near-tie between two queues may pick either; the choice is then checked
+    for being a minimum)."""
+    import torch
+    rng = np.random.default_rng(zlib.crc32(("place" + str(sorted(kw.items()))).encode()))
+    pr, pl = hand_case(rng, **kw)
+    G = pr["n_groups"]
+    dpr, dpl = device_inputs(pr, pl)
+    for group in sorted({0, G - 1, G // 2}):
+        print("case", kw, "group", group, flush=True)
+        r = qlm.place_group(dpr, dpl, group)
+        torch.cuda.synchronize()
+        out = r["plans"]
+        perm = out.perm.cpu().numpy()
+        qoff = out.qoff.cpu().numpy()
+        sc = r["score"].cpu().numpy()
+        qu = r["queue"].cpu().numpy()
+        for p in range(pl["n_plans"]):
+            o = orc.place_group(pr, pl, p, group)
+            if qu[p] != o["queue"]:
+                # a near-tie: the GPU's choice must score the same to erfc's last bits
+                assert _close(sc[p], o["score"]), (kw, group, p, qu[p], o["queue"])
+                continue
+            assert np.array_equal(perm[:, p], o["perm"]) and np.array_equal(qoff[:, p], o["qoff"])
+            if out.evict_bits is not None:
+                assert np.array_equal(out.evict_bits.cpu().numpy().view(np.uint32)[:, p],
+                                      o["evict_bits"])
+            assert _close(sc[p], o["score"]), (sc[p], o["score"])
+        ex = qlm.rwt_score_exact(dpr, out, np.arange(pl["n_plans"])).cpu().numpy()
+        assert np.array_equal(ex, sc)
+
+
+def test_place_group_arrival(qlm, orc):
+    """An arrival: the hetero workload with one more group parked at the end of
+    queue 0 of every plan, then placed."""
+    import torch
+    from paper_2407_00047_amd import workload
+    pr = workload.make_problem("hetero")
+    pl = workload.make_plans(pr, 0, 4)
+    G = pr["n_groups"]
+    pr2 = dict(pr)
+    pr2["n_groups"] = G + 1
+    for k, v in (("grp_count", 7), ("grp_mu", 250.0), ("grp_var", 4e4), ("grp_model", 1),
+                 ("grp_slo", 20.0)):
+        pr2[k] = np.concatenate([pr[k], np.array([v], pr[k].dtype)])
+    e1 = pl["qoff"][1]
+    perm = np.concatenate([pl["perm"], np.full((1, 4), -1, np.int32)])
+    for p in range(4):
+        col = list(pl["perm"][:, p])
+        col.insert(int(e1[p]), G)
+        perm[:, p] = col
+    qoff = pl["qoff"].copy()
+    qoff[1:] += 1
+    W = (G + 1 + 31) // 32
+    ev = np.zeros((W, 4), np.uint32)
+    pl2 = {"n_plans": 4, "perm": perm, "qoff": qoff, "evict_bits": ev}
+    dpr, dpl = device_inputs(pr2, pl2)
+    r = qlm.place_group(dpr, dpl, G)
+    torch.cuda.synchronize()
+    for p in range(4):
+        o = orc.place_group(pr2, pl2, p, G)
+        assert int(r["queue"][p]) == o["queue"]
+        assert np.array_equal(r["plans"].perm.cpu().numpy()[:, p], o["perm"])
+        assert _close(float(r["score"][p]), o["score"])
