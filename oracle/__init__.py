@@ -95,6 +95,12 @@ class Oracle:
         lib.oracle_place_group.argtypes = [ctypes.POINTER(_Problem), ctypes.POINTER(_Plans), i64,
                                            i32, vp, vp, vp, dp, vp]
         lib.oracle_place_group.restype = ctypes.c_int
+        lib.oracle_plan_fcfs.argtypes = [ctypes.POINTER(_Problem), ctypes.POINTER(_Plans), i64,
+                                         vp, i64, dp, dp]
+        lib.oracle_plan_fcfs.restype = ctypes.c_int
+        lib.oracle_score_plans_fcfs.argtypes = [ctypes.POINTER(_Problem), ctypes.POINTER(_Plans),
+                                                vp, i64, i64, i64, dp, ctypes.c_int]
+        lib.oracle_score_plans_fcfs.restype = ctypes.c_int64
         self.lib = lib
         self.path = path
 
@@ -145,6 +151,45 @@ class Oracle:
         """argmin_p score_p over all plans, lowest index on ties."""
         score, _ = self.score_plans(problem, plans, threads=threads)
         return self.argmin(score)
+
+    # -- per-request (FCFS within each group) variant ------------------------
+
+    def score_plans_fcfs(self, problem, plans, req_slo, p0: int = 0, count: int | None = None,
+                         threads: int = 0):
+        """fp64 per-request scores of plans [p0, p0+count); req_slo holds every
+        group's request SLOs in arrival order, group by group."""
+        b = _Bound(problem, plans)
+        slo = np.ascontiguousarray(req_slo, dtype=np.float32)
+        if count is None:
+            count = b.n_plans - p0
+        if p0 < 0 or count < 0 or p0 + count > b.n_plans:
+            raise ValueError("plan range out of bounds")
+        if slo.size != int(np.asarray(problem["grp_count"], np.int64).sum()):
+            raise ValueError("req_slo must hold sum(grp_count) entries")
+        score = np.empty(count, np.float64)
+        bad = self.lib.oracle_score_plans_fcfs(ctypes.byref(b.problem), ctypes.byref(b.plans),
+                                               _ptr(slo), slo.size, p0, count, _dp(score),
+                                               int(threads))
+        if bad:
+            raise ValueError("%d malformed plans" % bad)
+        return score
+
+    def plan_fcfs(self, problem, plans, req_slo, p: int):
+        """Per-request P (indexed as req_slo) and the score of plan p."""
+        b = _Bound(problem, plans)
+        slo = np.ascontiguousarray(req_slo, dtype=np.float32)
+        if not 0 <= p < b.n_plans:
+            raise ValueError("plan index out of range")
+        prob = np.full(slo.size, np.nan)
+        sc = np.zeros(1)
+        if self.lib.oracle_plan_fcfs(ctypes.byref(b.problem), ctypes.byref(b.plans), p,
+                                     _ptr(slo), slo.size, _dp(prob), _dp(sc)):
+            raise ValueError("malformed plan %d or req_slo size" % p)
+        return {"prob": prob, "score": float(sc[0])}
+
+    def best_plan_fcfs(self, problem, plans, req_slo, threads: int = 0) -> tuple[int, float]:
+        """argmin_p of the per-request score, lowest index on ties."""
+        return self.argmin(self.score_plans_fcfs(problem, plans, req_slo, threads=threads))
 
     # -- plan search -------------------------------------------------------
 
@@ -374,3 +419,16 @@ def seed_plan(problem, policy: int):
 
 def place_group(problem, plans, p: int, group: int):
     return default().place_group(problem, plans, p, group)
+
+
+def score_plans_fcfs(problem, plans, req_slo, p0: int = 0, count: int | None = None,
+                     threads: int = 0):
+    return default().score_plans_fcfs(problem, plans, req_slo, p0, count, threads)
+
+
+def plan_fcfs(problem, plans, req_slo, p: int):
+    return default().plan_fcfs(problem, plans, req_slo, p)
+
+
+def best_plan_fcfs(problem, plans, req_slo, threads: int = 0) -> tuple[int, float]:
+    return default().best_plan_fcfs(problem, plans, req_slo, threads)

@@ -215,6 +215,117 @@ int oracle_max_threads(void)
 }
 
 /* ------------------------------------------------------------------------
+ * Per-request variant: first-come-first-served order inside each group.
+ *
+ * The requests of a group are served in their arrival order (Sec. 4, request
+ * group creation; Sec. 5, request pulling takes the head group's requests
+ * first come, first served), and every request carries its own TTFT SLO
+ * (Sec. 3, Definition "SLO").  Request r of the group at position j of queue g
+ * (r = 0 is the first to arrive) has ahead of it the requests of the groups
+ * before position j and the r earlier requests of its own group.  By Eq.
+ * output_token_dist its tokens ahead are Normal with mean A + r mu_i and
+ * variance V + r sigma_i^2, so with E[W] = A / Theta_g + K as above:
+ *
+ *   E[W_r]  = E[W] + r * (mu_i / Theta_g)
+ *   SD[W_r] = sqrt(V + r * sigma_i^2) / Theta_g
+ *   P_r     = 0.5 erfc((slo_{i,r} - E[W_r]) / (SD[W_r] sqrt 2)),   SD > 0
+ *           = [E[W_r] > slo_{i,r}],                                SD = 0
+ *   score_p = sum over queues, then positions, then requests, of P_r
+ *             (the expected number of requests that miss their own SLO;
+ *             the group's slot sum starts at 0 and adds P_0, P_1, ... in
+ *             order, the queue sum adds the slot sums in position order,
+ *             the plan sum adds the queue sums in queue order)
+ *
+ * req_slo[n_requests] holds the SLOs of group 0's requests in arrival order,
+ * then group 1's, and so on: group i's start at n_0 + ... + n_{i-1}.  With one
+ * request per group (and its SLO equal to the group's) this is the group
+ * model above.
+ */
+int oracle_plan_fcfs(const oracle_problem *pr, const oracle_plans *pl, int64_t p,
+                     const float *req_slo, int64_t n_requests, double *prob,
+                     double *score_out)
+{
+    const int G = pr->n_groups, I = pr->n_instances, M = pr->n_models;
+    int64_t *first = (int64_t *)malloc(sizeof(int64_t) * (size_t)(G + 1));
+    if (!first) return -1;
+    first[0] = 0;
+    for (int i = 0; i < G; ++i) first[i + 1] = first[i] + pr->grp_count[i];
+    int rc = 0;
+    double score = 0.0;
+    if (first[G] != n_requests) rc = -1;
+    if (pl->qoff[p] != 0 || pl->qoff[(int64_t)I * pl->ld + p] != G) rc = -1;
+
+    for (int g = 0; g < I && rc == 0; ++g) {                 /* queues ascending */
+        const int32_t begin = pl->qoff[(int64_t)g * pl->ld + p];
+        const int32_t end   = pl->qoff[(int64_t)(g + 1) * pl->ld + p];
+        if (begin > end) { rc = -1; break; }
+        const double theta = (double)pr->inst_tput[g];
+        const int    cls   = pr->inst_class[g];
+        int m_prev = pr->inst_model0 ? pr->inst_model0[g] : -1;
+        double A = 0.0, V = 0.0, K = 0.0;
+        double score_g = 0.0;
+
+        for (int32_t s = begin; s < end; ++s) {             /* positions ascending */
+            const int32_t i = pl->perm[(int64_t)s * pl->ld + p];
+            if (i < 0 || i >= G) { rc = -1; break; }
+            const int    m   = pr->grp_model[i];
+            const int32_t n  = pr->grp_count[i];
+            const double mu  = (double)pr->grp_mu[i];
+            const double var = (double)pr->grp_var[i];
+
+            if (m_prev >= 0 && m_prev != m && pr->swap_cost)
+                K += (double)pr->swap_cost[((int64_t)cls * M + m_prev) * M + m];
+            if (evicted(pl, p, s))
+                K += (double)pr->evict_cost;
+
+            const double EW = A / theta + K;                 /* the group's start */
+            double slot = 0.0;
+            for (int32_t r = 0; r < n; ++r) {                /* arrival order */
+                const double slo = (double)req_slo[first[i] + r];
+                const double Er  = EW + (double)r * (mu / theta);
+                const double SDr = sqrt(V + (double)r * var) / theta;
+                double P;
+                if (SDr > 0.0)
+                    P = 0.5 * erfc((slo - Er) / (SDr * sqrt(2.0)));
+                else
+                    P = (Er > slo) ? 1.0 : 0.0;
+                if (prob) prob[first[i] + r] = P;
+                slot += P;
+            }
+            score_g += slot;
+
+            A += (double)n * mu;
+            V += (double)n * var;
+            m_prev = m;
+        }
+        score += score_g;
+    }
+    free(first);
+    if (score_out) *score_out = (rc == 0) ? score : NAN;
+    return rc;
+}
+
+/* FCFS scores of plans [p0, p0+count), spread over threads by plan.  Returns
+ * the number of malformed plans (their score is NaN).                       */
+int64_t oracle_score_plans_fcfs(const oracle_problem *pr, const oracle_plans *pl,
+                                const float *req_slo, int64_t n_requests,
+                                int64_t p0, int64_t count, double *score, int n_threads)
+{
+    int64_t bad = 0;
+#ifdef _OPENMP
+    if (n_threads <= 0) n_threads = omp_get_max_threads();
+#pragma omp parallel for schedule(dynamic, 1) num_threads(n_threads) reduction(+ : bad)
+#endif
+    for (int64_t k = 0; k < count; ++k) {
+        double sc = 0.0;
+        if (oracle_plan_fcfs(pr, pl, p0 + k, req_slo, n_requests, NULL, &sc) != 0) bad += 1;
+        if (score) score[k] = sc;
+    }
+    (void)n_threads;
+    return bad;
+}
+
+/* ------------------------------------------------------------------------
  * Plan search: a local search over plans.
  *
  * The paper's global scheduler places groups by solving the assignment

@@ -210,3 +210,25 @@ def make(name: str, n_plans: int | None = None, seed: int | None = None, threads
 
 def total_requests(problem) -> int:
     return int(np.asarray(problem["grp_count"], np.int64).sum())
+
+
+ARRIVAL_WINDOW = 0.25
+
+
+def make_request_slos(problem, seed: int | None = None):
+    """Per-request TTFT SLOs for the first-come-first-served variant: every
+    request carries its group's SLO target, less the time it has already waited
+    since it arrived.  A group's requests arrived as a Poisson stream over about
+    ARRIVAL_WINDOW of its SLO, the last one just now; they are listed group by
+    group, each group's in arrival order (oldest first).  float32 [sum n_i]."""
+    seed = (int(problem["seed"]) ^ 0xFCF5) if seed is None else seed
+    rng = np.random.default_rng(seed)
+    n = np.asarray(problem["grp_count"], np.int64)
+    slo = np.asarray(problem["grp_slo"], np.float64)
+    N = int(n.sum())
+    grp = np.repeat(np.arange(n.size), n)
+    gap = rng.exponential(1.0, N) * (ARRIVAL_WINDOW * slo / np.maximum(n, 1))[grp]
+    end = np.cumsum(n)[grp]                          # one past each request's group
+    c = np.cumsum(gap)
+    age = c[end - 1] - c                             # gaps of the later requests
+    return (slo[grp] - age).astype(np.float32)

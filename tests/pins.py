@@ -752,9 +752,163 @@ def pin_place_restated(orc):
                                                     0, G), bplan[2])
 
 
+# ---------------------------------------------------------------------------
+# Per-request variant: first come, first served inside each group
+
+
+def _req_first(pr):
+    return np.concatenate([[0], np.cumsum(np.asarray(pr["grp_count"], np.int64))])
+
+
+def pin_fcfs_by_hand(orc):
+    """One queue at Theta = 100 tok/s.  Group 0 holds 3 requests of 100 tokens
+    (1 s each), group 1 two of 50 (0.5 s each).  Deterministic (sigma = 0):
+    request r of group 0 waits r s; group 1 starts after the 300 tokens of
+    group 0, so its requests wait 3 and 3.5 s.  With SD = 0 a request misses
+    its SLO when its wait is strictly later."""
+    pr = problem([(3, 100.0, 0.0, 0, 9.0), (2, 50.0, 0.0, 0, 9.0)], [(100.0, 0)])
+    pl = plans([[[0, 1]]], 2)
+    req = np.array([0.5, 0.5, 2.5, 3.0, 3.4], np.float32)
+    d = orc.plan_fcfs(pr, pl, req, 0)
+    assert np.array_equal(d["prob"], [0.0, 1.0, 0.0, 0.0, 1.0]), d["prob"]
+    assert d["score"] == 2.0
+    # the other order: group 1 first (waits 0, 0.5 s), then group 0 (1, 2, 3 s)
+    d2 = orc.plan_fcfs(pr, plans([[[1, 0]]], 2), req, 0)
+    assert np.array_equal(d2["prob"], [1.0, 1.0, 1.0, 0.0, 0.0]), d2["prob"]
+    # sigma = 100 tokens = 1 s per request: request r of group 0 has SD sqrt(r) s;
+    # SLOs at z = 2 for r = 1 (1 + 2) and z = 1 for r = 2 (2 + sqrt 2); r = 0 has
+    # SD 0 and a wait of 0 > -1
+    table = dict(normal_table())
+    pr3 = problem([(3, 100.0, 10000.0, 0, 9.0)], [(100.0, 0)])
+    req3 = np.array([-1.0, 3.0, 2.0 + np.sqrt(2.0)], np.float32)
+    d3 = orc.plan_fcfs(pr3, plans([[[0]]], 1), req3, 0)
+    z2 = (float(req3[2]) - 2.0) / np.sqrt(2.0)      # 1 up to the float rounding of the SLO
+    want = [1.0, table[2.0], table[1.0] - (z2 - 1.0) * np.exp(-0.5) / np.sqrt(2 * np.pi)]
+    assert np.allclose(d3["prob"], want, rtol=0, atol=1e-8), (d3["prob"], want)
+
+
+def _explode(pr, queues, req, evicted):
+    """Every request as a group of its own (n = 1, its own SLO), in arrival order
+    at its group's place; a group's eviction goes to its first request."""
+    first = _req_first(pr)
+    groups, qs, ev, slot = [], [], [], 0
+    for q in queues:
+        out = []
+        for i in q:
+            s_here = slot
+            slot += 1
+            for r in range(int(pr["grp_count"][i])):
+                if r == 0 and s_here in evicted:
+                    ev.append(len(groups))
+                out.append(len(groups))
+                groups.append((1, float(pr["grp_mu"][i]), float(pr["grp_var"][i]),
+                               int(pr["grp_model"][i]), float(req[first[i] + r])))
+        qs.append(out)
+    G = len(groups)
+    # group ids = exploded positions, so the plan's slot s holds exploded group s
+    pe = problem(groups, np.stack([pr["inst_tput"], pr["inst_class"]], 1).tolist(),
+                 n_models=pr["n_models"], n_classes=pr["n_classes"],
+                 swap=None if pr["swap_cost"] is None else
+                 pr["swap_cost"].reshape(pr["n_classes"], pr["n_models"], pr["n_models"]),
+                 evict_cost=pr["evict_cost"], model0=pr["inst_model0"])
+    return pe, plans([qs], G, evict=[ev])
+
+
+def pin_fcfs_exploded(orc):
+    """Request r of a group has ahead of it the groups before the group and the
+    group's r earlier requests (Eq. output_token_dist counts every request
+    ahead): the per-request score of a plan equals the group score of the plan
+    in which every request is a group of one, with its own SLO, at its place in
+    arrival order.  One request per group, with the group's SLO, gives the group
+    score itself, exactly."""
+    rng = np.random.default_rng(41)
+    for trial in range(5):
+        G, I, M, C = 7, 3, 3, 2
+        groups = [(int(rng.integers(0, 6)), float(rng.uniform(20, 400)),
+                   float(rng.uniform(0, 3e4)), int(rng.integers(0, M)), 0.0) for _ in range(G)]
+        S = rng.uniform(0.5, 8.0, (C, M, M)).astype(np.float32)
+        pr = problem(groups, [(float(rng.choice([300.0, 800.0])), int(rng.integers(0, C)))
+                              for _ in range(I)], n_models=M, n_classes=C, swap=S,
+                     evict_cost=0.7, model0=[int(x) for x in rng.integers(-1, M, I)])
+        order = rng.permutation(G)
+        owner = rng.integers(0, I, G)
+        queues = [[int(i) for i in order if owner[i] == g] for g in range(I)]
+        evicted = set(int(x) for x in rng.choice(G, 2, replace=False))
+        pl = plans([queues], G, evict=[sorted(evicted)])
+        N = int(sum(g[0] for g in groups))
+        # SLOs near each request's wait, so that P spreads over (0, 1)
+        waits = rng.uniform(0.0, 60.0, N)
+        req = waits.astype(np.float32)
+        f = orc.score_plans_fcfs(pr, pl, req)[0]
+        pe, ple = _explode(pr, queues, req, evicted)
+        g, _ = orc.score_plans(pe, ple)
+        assert abs(f - g[0]) <= 1e-12 * max(1.0, abs(g[0])), (trial, f, g[0])
+        assert 0.0 < f < N
+        # one request per group: the group model, bit for bit
+        pr1 = dict(pr)
+        pr1["grp_count"] = np.ones(G, np.int32)
+        req1 = pr1["grp_slo"] = rng.uniform(0, 30, G).astype(np.float32)
+        assert orc.score_plans_fcfs(pr1, pl, req1)[0] == orc.score_plans(pr1, pl)[0][0]
+
+
+def _simulate_requests(pr, queues, evicted, rng, n_samples):
+    """Every request's tokens drawn from N(mu, sigma^2); each queue served in
+    order, each group's requests in arrival order.  Returns W[sample, request]
+    with requests indexed as the SLO array."""
+    first = _req_first(pr)
+    W = np.zeros((n_samples, int(first[-1])))
+    S, M, s = pr["swap_cost"], pr["n_models"], 0
+    for g, q in enumerate(queues):
+        theta = float(pr["inst_tput"][g])
+        c = int(pr["inst_class"][g])
+        prev = -1 if pr["inst_model0"] is None else int(pr["inst_model0"][g])
+        tokens = np.zeros(n_samples)
+        fixed = 0.0
+        for i in q:
+            m = int(pr["grp_model"][i])
+            if prev >= 0 and prev != m:
+                fixed += float(S[(c * M + prev) * M + m])
+            if s in evicted:
+                fixed += pr["evict_cost"]
+            for r in range(int(pr["grp_count"][i])):
+                W[:, first[i] + r] = tokens / theta + fixed
+                tokens = tokens + rng.normal(float(pr["grp_mu"][i]),
+                                             np.sqrt(float(pr["grp_var"][i])), n_samples)
+            prev = m
+            s += 1
+    return W
+
+
+def pin_fcfs_monte_carlo(orc):
+    """Per-request violation probabilities against a simulation of the stated
+    model: each request's tokens drawn, requests served one after another."""
+    rng = np.random.default_rng(7)
+    groups = [(3, 200.0, 9000.0, 0, 0.0), (4, 120.0, 2500.0, 1, 0.0), (2, 400.0, 20000.0, 1, 0.0),
+              (3, 150.0, 4000.0, 0, 0.0)]
+    S = np.array([[[0, 2.0], [3.0, 0]]], np.float32)
+    pr = problem(groups, [(1000.0, 0), (600.0, 0)], n_models=2, n_classes=1, swap=S,
+                 evict_cost=0.4, model0=[1, -1])
+    queues = [[3, 0], [1, 2]]
+    evicted = {2}
+    W0 = _simulate_requests(pr, queues, evicted, rng, 20000)
+    levels = np.linspace(0.1, 0.9, W0.shape[1])
+    req = np.array([np.quantile(W0[:, k], levels[k]) for k in range(W0.shape[1])], np.float32)
+    req[0] = -1.0                       # group 0's first request waits behind group 3
+    pl = plans([queues], 4, evict=[sorted(evicted)])
+    d = orc.plan_fcfs(pr, pl, req, 0)
+    N = 200000
+    W = _simulate_requests(pr, queues, evicted, rng, N)
+    hat = (W > req[None, :].astype(np.float64)).mean(axis=0)
+    se = np.sqrt(np.maximum(d["prob"] * (1 - d["prob"]), 1e-12) / N)
+    assert np.all(np.abs(hat - d["prob"]) <= 5 * se), (hat, d["prob"], se)
+    tot = (W > req[None, :].astype(np.float64)).sum(axis=1)
+    assert abs(tot.mean() - d["score"]) <= 5 * tot.std() / np.sqrt(N)
+
+
 ALL_PINS = [pin_deterministic_queue, pin_variance_queue, pin_normal_table, pin_swap_costs,
             pin_eviction_costs, pin_throughput_per_queue, pin_invariants, pin_half_at_mean,
             pin_identical_instances_symmetry, pin_monte_carlo, pin_edf_special_case,
             pin_grouping_special_case, pin_argmin_ties, pin_moves_by_hand, pin_moves_independent,
             pin_search_by_hand, pin_search_steepest, pin_seed_by_hand, pin_seed_special_cases,
-            pin_seed_restated, pin_place_by_hand, pin_place_restated]
+            pin_seed_restated, pin_place_by_hand, pin_place_restated, pin_fcfs_by_hand,
+            pin_fcfs_exploded, pin_fcfs_monte_carlo]

@@ -98,13 +98,32 @@ MUTANTS = [
     ("place_before_equal_slo",
      "            if (!placed && pr->grp_slo[perm[u]] > slo_i) {\n                perm2[out] = gi;  flag2[out] = flag[s];  ++out;  placed = 1;\n            }\n            perm2[out] = perm[u];  flag2[out] = flag[u];  ++out;\n        }\n        if (!placed) { perm2[out] = gi;  flag2[out] = flag[s];  ++out; }\n    }\n    qoff2[I] = out;\n}\n\n/* Places",
      "            if (!placed && pr->grp_slo[perm[u]] >= slo_i) {\n                perm2[out] = gi;  flag2[out] = flag[s];  ++out;  placed = 1;\n            }\n            perm2[out] = perm[u];  flag2[out] = flag[u];  ++out;\n        }\n        if (!placed) { perm2[out] = gi;  flag2[out] = flag[s];  ++out; }\n    }\n    qoff2[I] = out;\n}\n\n/* Places"),
+    # per-request (FCFS) variant
+    ("fcfs_own_requests_dropped", "const double Er  = EW + (double)r * (mu / theta);",
+     "const double Er  = EW;"),
+    ("fcfs_own_variance_dropped", "sqrt(V + (double)r * var)", "sqrt(V)"),
+    ("fcfs_own_request_counted", "(double)r * (mu / theta)", "(double)(r + 1) * (mu / theta)"),
+    ("fcfs_variance_times_r_squared", "sqrt(V + (double)r * var)", "sqrt(V + (double)r * r * var)"),
+    ("fcfs_mean_over_theta_squared", "(double)r * (mu / theta)", "(double)r * (mu / (theta * theta))"),
+    ("fcfs_group_slo_for_all", "(double)req_slo[first[i] + r];", "(double)req_slo[first[i]];"),
+    ("fcfs_reversed_arrival", "(double)req_slo[first[i] + r];", "(double)req_slo[first[i] + (n - 1 - r)];"),
+    ("fcfs_sd_zero_non_strict", "P = (Er > slo) ? 1.0 : 0.0;", "P = (Er >= slo) ? 1.0 : 0.0;"),
+    ("fcfs_weighted_by_count", "slot += P;", "slot += (double)n * P;"),
+    ("fcfs_eviction_dropped",
+     "                K += (double)pr->evict_cost;\n\n            const double EW = A / theta + K;  "
+     "               /* the group's start */",
+     "                (void)0;\n\n            const double EW = A / theta + K;"),
+    ("fcfs_head_model_ignored",
+     "int m_prev = pr->inst_model0 ? pr->inst_model0[g] : -1;\n        double A = 0.0, V = 0.0, K = 0.0;",
+     "int m_prev = -1;\n        double A = 0.0, V = 0.0, K = 0.0;"),
 ]
 
 
 def _fix_costs_not_carried(src):
     # make the eviction/swap total restart at every position (K not carried)
     return src.replace("            if (m_prev >= 0 && m_prev != m && pr->swap_cost)",
-                       "            K = K0;\n            if (m_prev >= 0 && m_prev != m && pr->swap_cost)")
+                       "            K = K0;\n            if (m_prev >= 0 && m_prev != m && pr->swap_cost)",
+                       1)
 
 
 def _fix_swap_after(src):
