@@ -293,6 +293,95 @@ def bench_search(args):
     print(json.dumps(res), flush=True)
 
 
+FCFS_METRIC = "plans scored per second, per-request FCFS variant (exact argmin), 1 GPU"
+FCFS_PLANS = 16384
+# VALU instructions per request in k_fscreen's unrolled loop (compiled code):
+# margin (v_add_f64, v_fmac_f64, v_cvt_f32_f64), variance (v_fmamk_f32),
+# v_rsq_f32, cell coordinate (v_fma_f32, v_med3_f32), cell address
+# (v_lshrrev_b32, v_and_b32), the line (v_fmac_f32), the sum (v_add_f32)
+VALU_PER_REQUEST = 11
+
+
+def cpu_fcfs_baseline(problem, plans, req, seconds: float):
+    import oracle
+    orc = oracle.default()
+    threads = orc.max_threads()
+    P = plans["n_plans"]
+    n, dt, t0 = 0, 0.0, time.perf_counter()
+    while n < P and (n == 0 or dt < seconds):
+        c = min(threads, P - n)
+        orc.score_plans_fcfs(problem, plans, req, n, c)
+        n += c
+        dt = time.perf_counter() - t0
+    N = int(req.size)
+    return {"value": n / dt, "unit": "plans/s", "requests_per_s": n * N / dt, "cores": threads,
+            "kind": "oracle",
+            "sample": "the first %d plans of the same batch, exact fp64 per-request scores by the "
+                      "C oracle on %d threads, %.1f s" % (n, threads, dt)}
+
+
+def bench_fcfs(args):
+    """One step = qlm_fcfs_best_plan over the batch: every plan screened (each
+    group's start once per plan, each request's tail), the plans within the
+    bound re-scored exactly, the lowest exact score."""
+    import torch
+    from paper_2407_00047_amd import qlm, workload
+    dev = torch.device("cuda:0")
+    K = args.steps
+    P = args.plans or FCFS_PLANS
+    pr = workload.make_problem(args.config)
+    pl = workload.make_plans(pr, 0, P)
+    req = workload.make_request_slos(pr)
+    G, I, N = pr["n_groups"], pr["n_instances"], int(req.size)
+    dpr = qlm.DeviceProblem(pr, device=dev)
+    dpl = qlm.DevicePlans.from_host(pl, device=dev)
+    dreq = qlm.device_requests(req, device=dev)
+    ws = qlm.fcfs_workspace(dpr, P, N, device=dev, chunk_plans=args.chunk)
+    log("fcfs %s: G=%d I=%d requests=%d plans=%d chunk=%d" % (args.config, G, I, N, P, args.chunk))
+    for _ in range(max(args.warmup, 1)):
+        bi, bs = qlm.fcfs_best_plan(dpr, dpl, dreq, ws=ws)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    qlm.timing_enable(True)
+    qlm.timing_read()
+    e0.record(stream)
+    for _ in range(K):
+        bi, bs = qlm.fcfs_best_plan(dpr, dpl, dreq, ws=ws, out=(bi, bs))
+    e1.record(stream)
+    torch.cuda.synchronize()
+    n_launch, k_ms = qlm.timing_read()
+    qlm.timing_enable(False)
+    ms = e0.elapsed_time(e1) / K
+    k_avg = k_ms / max(n_launch, 1)
+    per_launch = N * P * K / max(n_launch, 1)          # requests screened per launch
+    achieved = per_launch / (k_avg / 1e3) / 1e9
+    peak = PEAK_VALU_LANES / VALU_PER_REQUEST / 1e9
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle ...")
+        cpu = cpu_fcfs_baseline(pr, pl, req, args.cpu_seconds)
+    res = {
+        "metric": FCFS_METRIC, "value": round(P / (ms / 1e3), 1), "unit": "plans/s",
+        "requests_per_s": round(P * N / (ms / 1e3), 1),
+        "n_gpus": 1, "steps": K, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32+f64",
+        "data": "synthetic",
+        "config": {"workload": "per-request FCFS scoring on %s: %d groups, %d requests (each with "
+                               "its own SLO), %d instances, %d plans" % (args.config, G, N, I, P),
+                   "plans": P, "groups": G, "requests": N, "instances": I},
+        "best": [int(bi.item()), float(bs.item())],
+        "roofline": {"bound": "alu", "achieved": round(achieved, 1), "peak": round(peak, 1),
+                     "unit": "Grequests/s", "frac": round(achieved / peak, 4), "traffic": None,
+                     "kernel": "k_fscreen", "kernel_avg_ms": round(k_avg, 4),
+                     "requests_per_launch": int(per_launch),
+                     "valu_per_request": VALU_PER_REQUEST},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(res), flush=True)
+
+
 PLACE_METRIC = "group placements per second (arrival / violation re-score, exact), 1 GPU"
 
 
@@ -381,6 +470,10 @@ def main():
                     help="benchmark the plan search (local search steps) instead")
     ap.add_argument("--place", action="store_true",
                     help="benchmark the placement of one group (arrival re-score) instead")
+    ap.add_argument("--fcfs", action="store_true",
+                    help="benchmark the per-request FCFS variant instead")
+    ap.add_argument("--chunk", type=int, default=0,
+                    help="--fcfs: plans per screening chunk (0 = the library's default)")
     ap.add_argument("--chains", type=int, default=1, help="--search / --place: plans")
     ap.add_argument("--window", type=int, default=16, help="--search: swap window")
     ap.add_argument("--summarize-counters", nargs=4, metavar=("FETCH", "WRITE", "COPY_FETCH", "COPY_WRITE"),
@@ -416,6 +509,9 @@ def main():
         return
     if args.place:
         bench_place(args)
+        return
+    if args.fcfs:
+        bench_fcfs(args)
         return
 
     cfg = workload.CONFIGS[args.config]

@@ -291,6 +291,76 @@ size_t qlm_seed_workspace_bytes(const qlm_problem *problem, int32_t n_seeds);
 int qlm_seed_plans(const qlm_problem *problem, int32_t n, const int32_t *policy,
                    const qlm_plans_out *out, void *ws, size_t ws_bytes, qlm_stream stream);
 
+/*
+ * Per-request variant: first come, first served inside each group, every
+ * request with its own TTFT SLO (Sec. 3, Definition "SLO"; Sec. 4, requests
+ * of a group are served first come, first served; Sec. 5, request pulling).
+ * Request r (r = 0 the first to arrive) of the group at position j of queue g
+ * has ahead of it the groups before j and the r earlier requests of its own
+ * group, so by Eq. output_token_dist, with E[W] and K as above:
+ *
+ *   E[W_r]  = E[W] + r * (mu_i / Theta_g)
+ *   SD[W_r] = sqrt(sum_{k<j} n_k sigma_k^2 + r sigma_i^2) / Theta_g
+ *   P_r     = P(W_r > slo_{i,r}), W_r ~ N(E[W_r], SD[W_r]^2); [E[W_r] > slo] at SD = 0
+ *   score_p = sum over queues, then positions, then requests in arrival order,
+ *             of P_r (expected number of requests missing their own SLO)
+ *
+ * req_slo [n_requests] (device) holds the SLOs (seconds) of group 0's requests
+ * in arrival order, then group 1's, and so on: group i's start at
+ * n_0 + ... + n_{i-1}.  n_requests must equal sum n_i; the calls clamp every
+ * group's requests to the array, so a mismatch gives unspecified scores, never
+ * an out-of-bounds read.
+ * With one request per group and req_slo = grp_slo this is the group score.
+ *
+ * Every call takes a device workspace, 256-byte aligned, used as scratch.
+ * The plans are screened in chunks: a chunk of c plans needs 16 bytes per
+ * group and plan for the groups' starts, and every call 8 bytes per request
+ * and 8 (I + 2) bytes per plan.  qlm_fcfs_workspace_bytes(problem, n_plans,
+ * n_requests, chunk_plans) is the size for chunks of chunk_plans plans
+ * (rounded up to a multiple of 64; 0 = as many as 1 GiB of starts holds, the
+ * size to use), 0 for an invalid problem.  A call uses the largest chunk the
+ * workspace it is given holds, so any workspace of at least the size for
+ * chunk_plans = 64 works; smaller chunks only take more launches.  Calls that
+ * share a workspace must not overlap.
+ */
+size_t qlm_fcfs_workspace_bytes(const qlm_problem *problem, int64_t n_plans, int64_t n_requests,
+                                int64_t chunk_plans);
+
+/*
+ * Screened per-request scores of every plan: score [P] device out.
+ * Accuracy: |score_p - exact| <= 8e-6 * n_requests, when every request with
+ * SD[W_r] > 0 has E[W_r] <= 2^30 SD[W_r] (any plan whose token variances are
+ * zero or not vanishingly small); requests with SD = 0 are decided exactly at
+ * r = 0 and throughout groups without variance.  Method: per group and plan,
+ * the start E[W] in double (one walk of each queue); per request, the margin
+ * in double, the variance in single precision and the normal tail from the
+ * 1024-cell table; single-precision sums of at most 32 terms.
+ */
+int qlm_fcfs_score(const qlm_problem *problem, const qlm_plans *plans, const float *req_slo,
+                   int64_t n_requests, void *ws, size_t ws_bytes, double *score,
+                   qlm_stream stream);
+
+/*
+ * Exact (double precision) per-request scores of selected plans: plan_index
+ * [n] (device, each in [0, P), n <= P) -> score [n] (device).  The
+ * definition above in double precision, in the order stated, with IEEE
+ * division and square root and the device erfc.
+ */
+int qlm_fcfs_score_exact(const qlm_problem *problem, const qlm_plans *plans, const float *req_slo,
+                         int64_t n_requests, const int64_t *plan_index, int64_t n, void *ws,
+                         size_t ws_bytes, double *score, qlm_stream stream);
+
+/*
+ * argmin over plans of the exact per-request score, the lowest index on ties
+ * (a NaN score never wins; -1 and +inf when there is no plan): every plan is
+ * screened, the plans whose screened score lies within twice the bound of the
+ * lowest are scored exactly, and the lowest exact score wins.
+ *   best_index [1], best_score [1]: device out
+ */
+int qlm_fcfs_best_plan(const qlm_problem *problem, const qlm_plans *plans, const float *req_slo,
+                       int64_t n_requests, void *ws, size_t ws_bytes, int64_t *best_index,
+                       double *best_score, qlm_stream stream);
+
 /* Largest G the scoring kernels accept for these M, C, I (on-chip budget). */
 int32_t qlm_max_groups(int32_t n_models, int32_t n_classes, int32_t n_instances,
                        int32_t with_eviction);
@@ -304,8 +374,9 @@ const char *qlm_last_error(void);
  * each call is bracketed by HIP events on the call's stream: the plan-scoring
  * kernel of every qlm_rwt_score / qlm_best_plan call, the kernel that scores
  * the reassignment moves in every qlm_search_moves / qlm_search_screen call
- * and every step of qlm_local_search, and the candidate kernel of every
- * qlm_place_group call.  qlm_timing_read waits for the recorded events and
+ * and every step of qlm_local_search, the candidate kernel of every
+ * qlm_place_group call, and the per-request screening kernel of every plan
+ * chunk of qlm_fcfs_score / qlm_fcfs_best_plan.  qlm_timing_read waits for the recorded events and
  * returns the number of timed launches and their summed duration in
  * milliseconds since the last reset, then resets.
  */

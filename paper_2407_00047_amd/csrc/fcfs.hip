@@ -1,0 +1,1084 @@
+// fcfs.hip -- the per-request variant of the plan score: first come, first
+// served inside each group, every request with its own SLO.  Interface:
+// qlm_fcfs_* in include/qlm.h.
+//
+// Request r (r = 0 the first to arrive) of the group i at position j of queue
+// g has ahead of it the groups before j and the r earlier requests of group i
+// (Sec. 4 request groups are served first come, first served; Sec. 6, Eq.
+// output_token_dist counts every request ahead), and carries its own TTFT SLO
+// (Sec. 3, Definition "SLO"):
+//
+//   E[W_r]  = A / Theta_g + K + r (mu_i / Theta_g)
+//   SD[W_r] = sqrt(V + r sigma_i^2) / Theta_g
+//   P_r     = Q((slo_r - E[W_r]) / SD[W_r]),  [E[W_r] > slo_r] at SD = 0
+//   score_p = sum of P_r over every request of the plan
+//
+// A, V are the tokens and the token variance of the groups ahead of position
+// j, K the swap and eviction seconds up to and including it.  At 8192 groups
+// of 128 requests a plan holds 1,048,576 requests, each with its own tail: the
+// work is arithmetic, one tail per request, and the kernels are laid out for
+// that, not for memory traffic.
+//
+// Screen.  The running sums are per position (one walk of each plan), the
+// tails are per request.  The walk produces, for every group and plan, the
+// group's start E[W] = A/Theta + K (double), its variance ahead (single,
+// scaled for the tail table) and its queue, stored group-major; the screen
+// then takes one lane per plan and one wavefront per (64 plans, 64 groups):
+// all 64 lanes work on the same group at a time, so the request SLOs are the
+// same across the wavefront and come through the scalar cache, the request's
+// position in its group is a constant of the unrolled loop, and each request
+// costs a margin in double, a variance in single and one read of the
+// normal-tail table (11 vector instructions).
+//
+// The walk reads the plans slot-major with every lane (plan) of a wavefront at
+// the same slot, so its reads are coalesced.  It is cut into segments of 128
+// slots: k_fseg sums each segment's trailing queue piece, k_fstart chains the
+// pieces into each segment's starting sums, and k_frec walks each segment
+// again from them and stores the records.  Its stores land in the rows of the
+// groups, a different row in every lane: this transposition from the plans'
+// slot order to group order is the price of the screen's shared SLOs.
+//
+// Screening bound, per request: table error below 2.2e-6; single-precision
+// rounding of the cell coordinate, of the line's evaluation, of the margin and
+// of the variance below 1.7e-6; the sum of at most 32 terms in single
+// precision below 1.9e-6 per term; so |screened - exact| <= 8e-6 per request.
+// The margin is formed in double from the start E[W], whose rounding stays
+// below 2^-50 E[W_r]: negligible while E[W_r] <= 2^30 SD[W_r] (true of any
+// plan whose variances are not zero or vanishingly small).  A request with
+// SD = 0 at r = 0 (a queue's first group, or one behind groups without
+// variance) takes the exact comparison with the oracle's E[W] (formed in the
+// oracle's order: where a segment starts with nothing varying ahead, its sums
+// are formed again from the queue's first slot); a group without variance is
+// walked with exact comparisons throughout.
+//
+// Exact argmin.  Plans whose screened score is within twice the bound of the
+// lowest are re-scored exactly (k_fexact: one wavefront per queue, the running
+// sums rippled from lane to lane in position order, each request's term in
+// double with erfc, in the oracle's order), and the lowest exact score, the
+// lowest index on ties, wins.
+//
+// Kernels
+//   k_fprep     per group: clamped count, request offset, statistics; the
+//               request total; k_fslo: the SLOs widened to double; k_ftail:
+//               the normal-tail table
+//   k_fseg      one lane per plan, one wavefront per (64 plans, segment):
+//               each segment's trailing queue piece
+//   k_fstart    one lane per plan: the sums at each segment's first slot
+//   k_frec      as k_fseg: the records of the segment's groups
+//   k_fscreen   one lane per plan, one wavefront per (64 plans, 64 groups):
+//               partial screened scores
+//   k_fsum      partial scores -> screened plan scores, and the per-block
+//               minimum
+//   k_fselect   the plans within the bound of the lowest -> candidates
+//   k_fexact    one wavefront per (candidate, queue): exact queue scores
+//   k_fpick / k_fplan   exact plan scores; the lowest (score, index)
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+
+#include "internal.h"
+#include "qlm.h"
+#include "ripple.h"
+#include "tail.h"
+
+namespace {
+
+using qlm_internal::check_plans;
+using qlm_internal::check_problem;
+using qlm_internal::fail;
+using qlm_internal::hip_fail;
+using qlm_ripple::from_left;
+using qlm_ripple::from_left0;
+using qlm_ripple::lane_value;
+using qlm_ripple::wave_id;
+
+constexpr int kWave = 64;
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / kWave;
+constexpr int kGroupsPerWave = 64;          // groups of one k_fscreen wavefront
+constexpr int kSeg = 128;                   // slots per segment of the queue walks
+constexpr int kRecPad = 24;                 // plans of padding per record row
+constexpr int kSumBlocks = 1024;            // k_fsum blocks (per-block minima)
+constexpr int kExactBlocks = 256;
+constexpr int kPickThreads = 256;
+constexpr uint32_t kCountMask = (1u << 21) - 1u;
+constexpr uint32_t kNoVar = 1u << 31;       // record flag: no variance ahead
+constexpr double kEpsP = 8e-6;              // screening bound per request
+constexpr int64_t kMaxRequests = (int64_t)1 << 31;
+constexpr size_t kRecBudget = (size_t)1 << 30;    // bytes of group records per chunk
+
+// Per group, built once per call: for the walks (the count clamped to 21 bits,
+// the model clamped to [0, M)) ...
+struct FGrp {
+    float mu, var;
+    uint32_t cnt;
+    uint32_t model;
+};
+
+// ... and for the requests: how many are scored (clamped to n_requests).
+struct FReq {
+    float mu, var;
+    uint32_t n;
+    uint32_t pad;
+};
+
+// A slot's group start in one plan: E[W] of its first request, its variance
+// ahead V / Theta^2 times the table's scale, and its queue (| kNoVar when
+// V = 0).
+struct FRec {
+    double c0;
+    float v0;
+    uint32_t q;
+};
+
+// Sums over the slots of one segment of a plan that belong to the queue open
+// at the segment's end (tokens, variance, fixed costs), whether that queue
+// starts inside the segment, and the queue open at the segment's start.
+struct Piece {
+    double A, V, K;
+    int32_t head, q0;
+};
+
+// The running sums at a segment's first slot (those of its queue so far).
+struct Start {
+    double A, V, K;
+    int32_t pad[2];
+};
+
+struct FArgs {
+    int32_t G, I, M, C;
+    const int32_t *grp_count;
+    const float *grp_mu, *grp_var;
+    const int32_t *grp_model;
+    const float *inst_tput;
+    const int32_t *inst_class, *inst_model0;
+    const float *swap_cost;
+    float evict_cost;
+    int64_t P, ld;
+    const int32_t *perm, *qoff;
+    const uint32_t *evict_bits;
+    const float *req_slo;
+    int64_t n_req;
+    // workspace
+    FGrp *grp;                // [G]
+    FReq *req;                // [G]
+    int32_t *first;           // [G + 1] request offsets in req_slo
+    double *slo64;            // [n_req] the SLOs in double
+    float2 *tail;             // [kCells]
+    double *nreq;             // [1] requests scored
+    FRec *rec;                // [G slots][chunk]
+    Piece *piece;             // [nseg][chunk]
+    Start *start;             // [nseg][chunk]
+    double *part;             // [ceil(G / kGroupsPerWave)][chunk]
+    double *F;                // [P] screened scores
+    double *bmin;             // [kSumBlocks]
+    int32_t *ncand;           // [1]
+    int64_t *cand;            // [P]
+    double *Q;                // [P][I] exact queue scores
+    int64_t chunk;
+    int64_t rld;              // row stride of rec: chunk plus a pad, so that the
+                              // rows a scattered store touches fall on different
+                              // memory channels
+};
+
+__device__ inline int clampi(int v, int lo, int hi) { return v < lo ? lo : (v > hi ? hi : v); }
+
+template <class T>
+__device__ inline const __attribute__((address_space(4))) T *as_const(const T *p)
+{
+    return (const __attribute__((address_space(4))) T *)p;
+}
+
+__device__ inline double wave_min(double v)
+{
+    for (int o = kWave / 2; o > 0; o >>= 1) v = fmin(v, __shfl_xor(v, o, kWave));
+    return v;
+}
+
+__device__ inline int wave_max_int(int v)
+{
+    for (int o = kWave / 2; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o, kWave));
+    return v;
+}
+
+// (score, index) is better than (s2, i2): lower score, then lower index; a NaN
+// score is never better.
+__device__ inline bool better(double s, int64_t i, double s2, int64_t i2)
+{
+    return s < s2 || (s == s2 && i < i2);
+}
+
+#pragma clang fp contract(off)
+
+// ---------------------------------------------------------------------------
+// Per-call tables
+
+// One workgroup: clamped counts, request offsets (an exclusive scan), group
+// statistics, the request total.
+__global__ __launch_bounds__(kThreads) void k_fprep(FArgs a)
+{
+    __shared__ int64_t part[kThreads];
+    const int t = threadIdx.x;
+    const int per = (a.G + kThreads - 1) / kThreads;
+    const int b = t * per, e = min(a.G, b + per);
+    int64_t s = 0;
+    for (int i = b; i < e; ++i) s += (int64_t)((uint32_t)a.grp_count[i] & kCountMask);
+    part[t] = s;
+    __syncthreads();
+    if (t == 0) {
+        int64_t run = 0;
+        for (int k = 0; k < kThreads; ++k) {
+            const int64_t v = part[k];
+            part[k] = run;
+            run += v;
+        }
+    }
+    __syncthreads();
+    int64_t off = part[t];
+    for (int i = b; i < e; ++i) {
+        const int64_t want = (int64_t)((uint32_t)a.grp_count[i] & kCountMask);
+        const int64_t lo = off < a.n_req ? off : a.n_req;
+        const int64_t hi = off + want < a.n_req ? off + want : a.n_req;
+        a.first[i] = (int32_t)lo;
+        FGrp g;
+        g.mu = a.grp_mu[i];
+        g.var = a.grp_var[i];
+        g.cnt = (uint32_t)want;
+        g.model = (uint32_t)clampi(a.grp_model[i], 0, a.M - 1);
+        a.grp[i] = g;
+        FReq r;
+        r.mu = g.mu;
+        r.var = g.var;
+        r.n = (uint32_t)(hi - lo);
+        r.pad = 0u;
+        a.req[i] = r;
+        off += want;
+    }
+    // the last thread's range ends at G: its offset is then the total
+    if (t == kThreads - 1) {
+        a.first[a.G] = (int32_t)(off < a.n_req ? off : a.n_req);
+        a.nreq[0] = (double)(off < a.n_req ? off : a.n_req);
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void k_fslo(FArgs a)
+{
+    for (int64_t k = (int64_t)blockIdx.x * kThreads + threadIdx.x; k < a.n_req;
+         k += (int64_t)gridDim.x * kThreads)
+        a.slo64[k] = (double)a.req_slo[k];
+}
+
+__global__ __launch_bounds__(kThreads) void k_ftail(FArgs a)
+{
+    __shared__ float2 tab[qlm_tail::kCells];
+    qlm_tail::build<kThreads>(tab);
+    __syncthreads();
+    for (int k = threadIdx.x; k < qlm_tail::kCells; k += kThreads) a.tail[k] = tab[k];
+}
+
+// ---------------------------------------------------------------------------
+// Screen
+
+// The walk of one plan's slots in order, one lane per plan, every lane of a
+// wavefront at the same slot (so the reads of the plan rows are coalesced).
+// Queues are contiguous slot ranges; at a queue's first slot the running sums
+// restart.  The sums and costs are formed with the oracle's operations in the
+// oracle's order.
+struct Walk {
+    int q, nh;                 // open queue, first slot of the next queue
+    double theta, vscale;
+    int cls, prev;
+    double A, V, K;
+};
+
+__device__ inline void open_queue(const FArgs &a, int64_t p, int q, Walk &w)
+{
+    w.q = q;
+    w.nh = a.qoff[(int64_t)(q + 1) * a.ld + p];
+    w.theta = (double)a.inst_tput[q];
+    w.vscale = qlm_tail::kVarScale / (w.theta * w.theta);
+    w.cls = clampi(a.inst_class[q], 0, a.C - 1);
+    w.prev = a.inst_model0 ? clampi(a.inst_model0[q], -1, a.M - 1) : -1;
+    w.A = w.V = w.K = 0.0;
+}
+
+// The queue holding slot s: the largest q with qoff[q] <= s.
+__device__ inline int queue_at(const FArgs &a, int64_t p, int s)
+{
+    int lo = 0, hi = a.I - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (a.qoff[(int64_t)mid * a.ld + p] <= s)
+            lo = mid;
+        else
+            hi = mid - 1;
+    }
+    return lo;
+}
+
+// Slots [s0, s1) of the walk, B at a time: a batch's reads (group ids, one
+// eviction word, the group records) are issued together, and with kPipe the
+// next batch's reads are issued while a batch is walked.  Batches start at
+// multiples of B (so one eviction word covers a batch); slots before s0 are
+// passed over.  At a queue's first slot (the next queue's first slot reached,
+// empty queues skipped) the sums restart; then the slot's model-change and
+// eviction costs; visit(s, i, w) sees the sums on entry to the slot (fixed
+// costs included); then the group's tokens and variance join the sums.  Ids
+// out of range (a malformed plan) are skipped.
+template <int B>
+struct Batch {
+    int ids[B];
+    uint32_t ev;
+};
+
+template <int B>
+__device__ inline void batch_ids(const FArgs &a, int64_t p, int sb, int s1, Batch<B> &b)
+{
+#pragma unroll
+    for (int u = 0; u < B; ++u) {
+        const int s = sb + u;
+        b.ids[u] = s < s1 ? a.perm[(int64_t)s * a.ld + p] : -1;
+    }
+    b.ev = a.evict_bits ? a.evict_bits[(int64_t)(sb >> 5) * a.ld + p] : 0u;
+}
+
+template <int B>
+__device__ inline void batch_groups(const FArgs &a, const Batch<B> &b, FGrp *gr)
+{
+#pragma unroll
+    for (int u = 0; u < B; ++u) {
+        const int i = b.ids[u];
+        gr[u] = (i >= 0 && i < a.G) ? a.grp[i] : FGrp{0.0f, 0.0f, 0u, 0u};
+    }
+}
+
+template <int B, bool kPipe, class Visit>
+__device__ inline void walk(const FArgs &a, int64_t p, int s0, int s1, Walk &w, bool *fresh,
+                            const Visit &visit)
+{
+    static_assert(B <= 32 && (B & (B - 1)) == 0, "a batch lies in one eviction word");
+    if (s0 >= s1) return;
+    int sb = s0 & ~(B - 1);
+    Batch<B> cur;
+    FGrp gr[B];
+    batch_ids<B>(a, p, sb, s1, cur);
+    batch_groups<B>(a, cur, gr);
+    for (; sb < s1; sb += B) {
+        Batch<B> nxt;
+        const bool more = sb + B < s1;
+        if (kPipe && more) batch_ids<B>(a, p, sb + B, s1, nxt);
+#pragma unroll
+        for (int u = 0; u < B; ++u) {
+            const int s = sb + u;
+            if (s < s0) continue;
+            if (s >= s1) break;
+            if (s >= w.nh) {
+                int q = w.q;
+                while (q + 1 < a.I && a.qoff[(int64_t)(q + 1) * a.ld + p] <= s) ++q;
+                open_queue(a, p, q, w);
+                *fresh = true;
+            }
+            const int i = cur.ids[u];
+            if (i < 0 || i >= a.G) continue;
+            const int m = (int)gr[u].model;
+            if (w.prev >= 0 && w.prev != m && a.swap_cost)
+                w.K += (double)a.swap_cost[((int64_t)w.cls * a.M + w.prev) * a.M + m];
+            if ((cur.ev >> (s & 31)) & 1u) w.K += (double)a.evict_cost;
+            visit(s, i, w);
+            const double n = (double)gr[u].cnt;
+            w.A += n * (double)gr[u].mu;
+            w.V += n * (double)gr[u].var;
+            w.prev = m;
+        }
+        if (more) {
+            if (kPipe)
+                cur = nxt;
+            else
+                batch_ids<B>(a, p, sb + B, s1, cur);
+            batch_groups<B>(a, cur, gr);
+        }
+    }
+}
+
+struct NoVisit {
+    __device__ void operator()(int, int, const Walk &) const {}
+};
+
+// Grid: ceil(chunk/64) tiles x ceil(nseg/4); wavefront = (tile, segment).
+// Pass 1: each segment's trailing piece (the sums of its last queue over the
+// segment's slots).
+__global__ __launch_bounds__(kThreads) void k_fseg(FArgs a, int64_t p0, int64_t pc)
+{
+    const int nseg = (a.G + kSeg - 1) / kSeg;
+    const int sq = (nseg + kWaves - 1) / kWaves;
+    const int64_t tile = blockIdx.x / sq;
+    const int k = (int)(blockIdx.x % sq) * kWaves + wave_id();
+    if (k >= nseg) return;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t col = tile * kWave + lane;
+    const bool on = col < pc;
+    const int64_t p = p0 + (on ? col : pc - 1);
+    const int s0 = k * kSeg, s1 = min(a.G, s0 + kSeg);
+    Walk w;
+    const int q0 = queue_at(a, p, s0);
+    open_queue(a, p, q0, w);
+    bool fresh = s0 == 0 || a.qoff[(int64_t)q0 * a.ld + p] >= s0;
+    if (!fresh) {
+        const int i = a.perm[(int64_t)(s0 - 1) * a.ld + p];
+        if (i >= 0 && i < a.G) w.prev = (int)a.grp[i].model;
+    }
+    walk<8, true>(a, p, s0, s1, w, &fresh, NoVisit{});
+    if (on) {
+        Piece t;
+        t.A = w.A;
+        t.V = w.V;
+        t.K = w.K;
+        t.head = fresh ? 1 : 0;
+        t.q0 = q0;
+        a.piece[(int64_t)k * a.chunk + col] = t;
+    }
+}
+
+// Pass 2: one lane per plan, the segments in order: the sums at each
+// segment's first slot.
+__global__ __launch_bounds__(kThreads) void k_fstart(FArgs a, int64_t pc)
+{
+    const int64_t col = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (col >= pc) return;
+    const int nseg = (a.G + kSeg - 1) / kSeg;
+    double A = 0.0, V = 0.0, K = 0.0;
+    for (int k = 0; k < nseg; ++k) {
+        Start st;
+        st.A = A;
+        st.V = V;
+        st.K = K;
+        st.pad[0] = st.pad[1] = 0;
+        a.start[(int64_t)k * a.chunk + col] = st;
+        const Piece t = a.piece[(int64_t)k * a.chunk + col];
+        if (t.head) {
+            A = t.A;
+            V = t.V;
+            K = t.K;
+        } else {
+            A = A + t.A;
+            V = V + t.V;
+            K = K + t.K;
+        }
+    }
+}
+
+// Pass 3: each slot's record (its group's start E[W] = A/Theta + K, its
+// variance ahead, its queue), written to the slot's row.  A queue open at
+// the segment's start continues from the sums of pass 2; where nothing
+// varies ahead (V = 0) those sums are formed again slot by slot from the
+// queue's first slot, so that E[W] is the oracle's bit for bit wherever an
+// exact comparison uses it.
+__global__ __launch_bounds__(kThreads) void k_frec(FArgs a, int64_t p0, int64_t pc)
+{
+    const int nseg = (a.G + kSeg - 1) / kSeg;
+    const int sq = (nseg + kWaves - 1) / kWaves;
+    const int64_t tile = blockIdx.x / sq;
+    const int k = (int)(blockIdx.x % sq) * kWaves + wave_id();
+    if (k >= nseg) return;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t col = tile * kWave + lane;
+    const bool on = col < pc;
+    const int64_t c = on ? col : pc - 1;
+    const int64_t p = p0 + c;
+    const int s0 = k * kSeg, s1 = min(a.G, s0 + kSeg);
+    Walk w;
+    const int q0 = a.piece[(int64_t)k * a.chunk + c].q0;
+    open_queue(a, p, q0, w);
+    const int b = a.qoff[(int64_t)q0 * a.ld + p];
+    if (s0 > 0 && b < s0) {
+        const Start st = a.start[(int64_t)k * a.chunk + c];
+        if (st.V == 0.0) {
+            // nothing varies ahead: form the sums again in the oracle's order
+            bool f = false;
+            walk<8, true>(a, p, max(b, 0), s0, w, &f, NoVisit{});
+        } else {
+            w.A = st.A;
+            w.V = st.V;
+            w.K = st.K;
+            const int i = a.perm[(int64_t)(s0 - 1) * a.ld + p];
+            if (i >= 0 && i < a.G) w.prev = (int)a.grp[i].model;
+        }
+    }
+    bool f = false;
+    // (the scattered record stores run best with fewer wavefronts in flight:
+    // larger batches, no overlap)
+    walk<16, false>(a, p, s0, s1, w, &f, [&](int, int i, const Walk &x) {
+        if (on) {
+            FRec r;
+            r.c0 = x.A / x.theta + x.K;
+            r.v0 = (float)(x.V * x.vscale);
+            r.q = (uint32_t)x.q | (x.V == 0.0 ? kNoVar : 0u);
+            a.rec[(int64_t)i * a.rld + col] = r;
+        }
+    });
+}
+
+// Q of the margin m (seconds) at scaled variance vz, from the table in LDS.
+__device__ inline float tail_q(const float2 *tab, float m, float vz)
+{
+    return qlm_tail::q_of(tab, m, vz);
+}
+
+// Grid: ceil(G / 64) group blocks x ceil(tiles / 4), group block major (the
+// wavefronts running at one time share their groups' SLOs in the caches).
+// Lane = plan; every lane of a wavefront is at the same request of the same
+// group, whose SLO is read through the scalar cache.
+__global__ __launch_bounds__(kThreads) void k_fscreen(FArgs a, int64_t p0, int64_t pc)
+{
+    __shared__ float2 tab[qlm_tail::kCells];
+    for (int k = threadIdx.x; k < qlm_tail::kCells; k += kThreads) tab[k] = a.tail[k];
+    __syncthreads();
+    const int64_t tiles = (pc + kWave - 1) / kWave;
+    const int64_t quads = (tiles + kWaves - 1) / kWaves;
+    const int gb = (int)(blockIdx.x / quads);
+    const int64_t tile = (blockIdx.x % quads) * kWaves + wave_id();
+    if (tile >= tiles) return;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t col0 = tile * kWave + lane;
+    const bool on = col0 < pc;
+    const int64_t col = on ? col0 : pc - 1;
+    const int i0 = gb * kGroupsPerWave, i1 = min(a.G, i0 + kGroupsPerWave);
+    const auto req = as_const(a.req);
+    const auto first = as_const(a.first);
+    double tot = 0.0;
+    for (int i = i0; i < i1; ++i) {
+        const int n = (int)req[i].n;
+        if (n == 0) continue;
+        const float mu = req[i].mu, var = req[i].var;
+        const auto slo = as_const(a.slo64 + first[i]);
+        const FRec rc = a.rec[(int64_t)i * a.rld + col];
+        const int g = min((int)(rc.q & ~kNoVar), a.I - 1);
+        const bool novar = (rc.q & kNoVar) != 0u;
+        const double theta = (double)a.inst_tput[g];
+        const double c1 = (double)mu / theta;
+        const float v1 = (float)((double)var * (qlm_tail::kVarScale / (theta * theta)));
+        const double c0 = rc.c0;
+        const float v0 = rc.v0;
+        const double s0 = slo[0];
+        double Sg = novar ? (c0 > s0 ? 1.0 : 0.0) : (double)tail_q(tab, (float)(s0 - c0), v0);
+        if (var == 0.0f) {
+            for (int r = 1; r < n; ++r) {
+                const double Er = c0 + (double)r * c1;
+                const double sr = slo[r];
+                Sg += novar ? (Er > sr ? 1.0 : 0.0) : (double)tail_q(tab, (float)(sr - Er), v0);
+            }
+        } else {
+            int r = 1;
+            for (; r + 32 <= n; r += 32) {
+                const double eb = c0 + (double)r * c1;
+                const float vb = fmaf((float)r, v1, v0);
+                float S = 0.0f;
+#pragma unroll
+                for (int k = 0; k < 32; ++k) {
+                    const float m = (float)fma(-(double)k, c1, slo[r + k] - eb);
+                    const float v = fmaf((float)k, v1, vb);
+                    S += tail_q(tab, m, v);
+                }
+                Sg += (double)S;
+            }
+            float S = 0.0f;
+            for (; r < n; ++r) {
+                const double e = c0 + (double)r * c1;
+                const float m = (float)(slo[r] - e);
+                const float v = fmaf((float)r, v1, v0);
+                S += tail_q(tab, m, v);
+            }
+            Sg += (double)S;
+        }
+        tot += Sg;
+    }
+    if (on) a.part[(int64_t)gb * a.chunk + col0] = tot;
+}
+
+// Screened plan scores of the chunk (partials in group-block order) and the
+// running minimum per block (grid-stride over plans, fixed grid).
+__global__ __launch_bounds__(kThreads) void k_fsum(FArgs a, int64_t p0, int64_t pc, int first_chunk)
+{
+    __shared__ double lmin[kWaves];
+    const int nb = (a.G + kGroupsPerWave - 1) / kGroupsPerWave;
+    double mn = first_chunk ? INFINITY : a.bmin[blockIdx.x];
+    for (int64_t c = (int64_t)blockIdx.x * kThreads + threadIdx.x; c < pc;
+         c += (int64_t)gridDim.x * kThreads) {
+        double s = 0.0;
+        for (int b = 0; b < nb; ++b) s += a.part[(int64_t)b * a.chunk + c];
+        a.F[p0 + c] = s;
+        mn = fmin(mn, s);
+    }
+    mn = wave_min(mn);
+    if ((threadIdx.x & (kWave - 1)) == 0) lmin[threadIdx.x / kWave] = mn;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int w = 1; w < kWaves; ++w) mn = fmin(mn, lmin[w]);
+        a.bmin[blockIdx.x] = mn;
+    }
+}
+
+// Candidates: plans whose screened score lies within twice the bound of the
+// lowest (their exact score can be the lowest), and plans with a NaN score.
+// Block 0 clears the counter first in a kernel of its own (k_fzero).
+__global__ void k_fzero(FArgs a) { if (threadIdx.x == 0) a.ncand[0] = 0; }
+
+__global__ __launch_bounds__(kThreads) void k_fselect(FArgs a, int nbmin)
+{
+    __shared__ double smin;
+    if (threadIdx.x < kWave) {
+        double m = INFINITY;
+        for (int b = threadIdx.x; b < nbmin; b += kWave) m = fmin(m, a.bmin[b]);
+        m = wave_min(m);
+        if (threadIdx.x == 0) smin = m;
+    }
+    __syncthreads();
+    const double lim = smin + 2.0 * kEpsP * a.nreq[0] + 1e-9 * fabs(smin);
+    for (int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x; p < a.P;
+         p += (int64_t)gridDim.x * kThreads) {
+        const double f = a.F[p];
+        if (f <= lim || f != f) {
+            const int k = atomicAdd(a.ncand, 1);
+            a.cand[k] = p;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Exact scores
+
+// The oracle's terms for one group in double: the slot sum starts at 0 and
+// adds P_0, P_1, ... in arrival order.
+__device__ inline double slot_exact(const FArgs &a, int i, double A, double V, double K,
+                                    double theta)
+{
+    const int n = (int)a.req[i].n;
+    const double mu = (double)a.grp[i].mu;
+    const double var = (double)a.grp[i].var;
+    const float *slo = a.req_slo + a.first[i];
+    const double EW = A / theta + K;
+    double slot = 0.0;
+    for (int r = 0; r < n; ++r) {
+        const double sl = (double)slo[r];
+        const double Er = EW + (double)r * (mu / theta);
+        const double SDr = sqrt(V + (double)r * var) / theta;
+        double P;
+        if (SDr > 0.0)
+            P = 0.5 * erfc((sl - Er) / (SDr * 1.4142135623730951));
+        else
+            P = (Er > sl) ? 1.0 : 0.0;
+        slot += P;
+    }
+    return slot;
+}
+
+// One wavefront per (candidate k, queue g), over a fixed grid: the queue's
+// positions 64 at a time, one per lane; the running sums ripple from lane to
+// lane in position order, then each lane forms its group's requests' terms,
+// and the slot sums ripple into the queue score the same way.
+__global__ __launch_bounds__(kThreads) void k_fexact(FArgs a, const int64_t *plan_index,
+                                                      const int32_t *count_dev, int64_t count)
+{
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t n = count_dev ? (int64_t)__builtin_amdgcn_readfirstlane(count_dev[0]) : count;
+    const int64_t tasks = n * a.I;
+    const int64_t nw = (int64_t)gridDim.x * kWaves;
+    const double ecost = (double)a.evict_cost;
+    for (int64_t t = (int64_t)blockIdx.x * kWaves + wave_id(); t < tasks; t += nw) {
+        const int64_t k = t / a.I;
+        const int g = (int)(t % a.I);
+        int64_t p = plan_index[k];
+        p = p < 0 ? 0 : (p >= a.P ? a.P - 1 : p);
+        const int G = a.G;
+        const int bq = clampi(a.qoff[(int64_t)g * a.ld + p], 0, G);
+        const int eq = clampi(a.qoff[(int64_t)(g + 1) * a.ld + p], bq, G);
+        const double theta = (double)a.inst_tput[g];
+        const int cls = clampi(a.inst_class[g], 0, a.C - 1);
+        int prev = a.inst_model0 ? clampi(a.inst_model0[g], -1, a.M - 1) : -1;
+        double rA = 0.0, rV = 0.0, rK = 0.0, rC = 0.0;
+        for (int v0 = bq; v0 < eq; v0 += kWave) {
+            const int cnt = min(kWave, eq - v0);
+            const bool on = lane < cnt;
+            int i = -1;
+            if (on) {
+                i = a.perm[(int64_t)(v0 + lane) * a.ld + p];
+                if (i < 0 || i >= G) i = -1;
+            }
+            const int m = i >= 0 ? (int)a.grp[i].model : -1;
+            // an invalid id (malformed plan) keeps the model before it
+            int pm = __shfl_up(m, 1, kWave);
+            if (lane == 0) pm = prev;
+            const int mm = m >= 0 ? m : pm;
+            double xa = 0.0, xb = 0.0, c1 = 0.0, c2 = 0.0;
+            if (i >= 0) {
+                const double nn = (double)a.grp[i].cnt;
+                xa = nn * (double)a.grp[i].mu;
+                xb = nn * (double)a.grp[i].var;
+                if (pm >= 0 && pm != m && a.swap_cost)
+                    c1 = (double)a.swap_cost[((int64_t)cls * a.M + pm) * a.M + m];
+                const int s = v0 + lane;
+                if (a.evict_bits && ((a.evict_bits[(int64_t)(s >> 5) * a.ld + p] >> (s & 31)) & 1u))
+                    c2 = ecost;
+            }
+            const double la = from_left0(xa), lb = from_left0(xb);
+            const double l1 = from_left0(c1), l2 = from_left0(c2);
+            double A = rA, V = rV, K0 = rK;
+            for (int j = 1; j < cnt; ++j) {
+                A = from_left(A) + la;
+                V = from_left(V) + lb;
+                K0 = (from_left(K0) + l1) + l2;
+            }
+            double K = K0 + c1;
+            K = K + c2;
+            const double term = i >= 0 ? slot_exact(a, i, A, V, K, theta) : 0.0;
+            const double lt = from_left0(term);
+            double C = rC;
+            for (int j = 1; j < cnt; ++j) C = from_left(C) + lt;
+            const int last = cnt - 1;
+            rA = lane_value(A, last) + lane_value(xa, last);
+            rV = lane_value(V, last) + lane_value(xb, last);
+            rK = lane_value(K, last);
+            rC = lane_value(C, last) + lane_value(term, last);
+            // the model the next round starts from: the last valid one
+            int carry = __builtin_amdgcn_readlane(mm, last);
+            prev = carry;
+        }
+        if (lane == 0) a.Q[k * a.I + g] = rC;
+    }
+}
+
+// Exact plan scores of the listed plans (queue scores summed in order).
+__global__ __launch_bounds__(kThreads) void k_fplan(FArgs a, int64_t n, double *score)
+{
+    for (int64_t k = (int64_t)blockIdx.x * kThreads + threadIdx.x; k < n;
+         k += (int64_t)gridDim.x * kThreads) {
+        double s = 0.0;
+        for (int g = 0; g < a.I; ++g) s += a.Q[k * a.I + g];
+        score[k] = s;
+    }
+}
+
+// The lowest (exact score, plan index) over the candidates.
+__global__ __launch_bounds__(kPickThreads) void k_fpick(FArgs a, int64_t *best_index,
+                                                        double *best_score)
+{
+    __shared__ double ls[kPickThreads / kWave];
+    __shared__ int64_t li[kPickThreads / kWave];
+    const int n = a.ncand[0];
+    double bs = INFINITY;
+    int64_t bi = -1;
+    for (int k = threadIdx.x; k < n; k += kPickThreads) {
+        double s = 0.0;
+        for (int g = 0; g < a.I; ++g) s += a.Q[(int64_t)k * a.I + g];
+        const int64_t p = a.cand[k];
+        if (s == s && (bi < 0 || better(s, p, bs, bi))) {   // a NaN score never wins
+            bs = s;
+            bi = p;
+        }
+    }
+    for (int o = kWave / 2; o > 0; o >>= 1) {
+        const double s2 = __shfl_xor(bs, o, kWave);
+        const int64_t i2 = __shfl_xor(bi, o, kWave);
+        if (i2 >= 0 && (bi < 0 || better(s2, i2, bs, bi))) {
+            bs = s2;
+            bi = i2;
+        }
+    }
+    const int w = threadIdx.x / kWave;
+    if ((threadIdx.x & (kWave - 1)) == 0) {
+        ls[w] = bs;
+        li[w] = bi;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int k = 1; k < kPickThreads / kWave; ++k)
+            if (li[k] >= 0 && (bi < 0 || better(ls[k], li[k], bs, bi))) {
+                bs = ls[k];
+                bi = li[k];
+            }
+        best_index[0] = bi;
+        best_score[0] = bi < 0 ? INFINITY : bs;
+    }
+}
+
+#pragma clang fp contract(on)
+
+// ---------------------------------------------------------------------------
+// Host side
+
+size_t align256(size_t v) { return (v + 255) / 256 * 256; }
+
+// Plans per chunk: as many as `want` asks for (0 = up to kRecBudget bytes of
+// group records), a multiple of 64, no more than the plans rounded up.
+int64_t chunk_of(int32_t G, int64_t P, int64_t want)
+{
+    int64_t c = (int64_t)(kRecBudget / (sizeof(FRec) * (size_t)(G > 0 ? G : 1)));
+    if (want > 0) c = want;
+    c = (c + kWave - 1) / kWave * kWave;
+    const int64_t all = (P + kWave - 1) / kWave * kWave;
+    if (all < c) c = all;
+    return c < kWave ? kWave : c;
+}
+
+struct FLayout {
+    size_t grp, req, first, slo64, tail, nreq, rec, piece, start, part, F, bmin, ncand, cand, Q,
+        total;
+    int64_t chunk;
+};
+
+FLayout flayout(const qlm_problem *pr, int64_t P, int64_t n_req, int64_t chunk)
+{
+    FLayout L{};
+    const int32_t G = pr->n_groups, I = pr->n_instances;
+    L.chunk = chunk_of(G, P, chunk);
+    const int64_t Pn = P > 0 ? P : 1;
+    const int nb = (G + kGroupsPerWave - 1) / kGroupsPerWave;
+    size_t o = 0;
+    auto put = [&](size_t &field, size_t bytes) {
+        field = o;
+        o += align256(bytes);
+    };
+    put(L.grp, sizeof(FGrp) * (size_t)G);
+    put(L.req, sizeof(FReq) * (size_t)G);
+    put(L.first, 4 * ((size_t)G + 1));
+    put(L.slo64, 8 * ((size_t)n_req + 1));
+    put(L.tail, 8 * (size_t)qlm_tail::kCells);
+    put(L.nreq, 8);
+    put(L.rec, sizeof(FRec) * (size_t)G * (size_t)(L.chunk + kRecPad));
+    const size_t nseg = (size_t)((G + kSeg - 1) / kSeg);
+    put(L.piece, sizeof(Piece) * nseg * (size_t)L.chunk);
+    put(L.start, sizeof(Start) * nseg * (size_t)L.chunk);
+    put(L.part, 8 * (size_t)nb * (size_t)L.chunk);
+    put(L.F, 8 * (size_t)Pn);
+    put(L.bmin, 8 * (size_t)kSumBlocks);
+    put(L.ncand, 256);
+    put(L.cand, 8 * (size_t)Pn);
+    put(L.Q, 8 * (size_t)Pn * (size_t)I);
+    L.total = o;
+    return L;
+}
+
+int check_requests(const qlm_problem *pr, const float *req_slo, int64_t n_req)
+{
+    (void)pr;
+    if (n_req < 0 || n_req >= kMaxRequests)
+        return fail(QLM_ERR_ARG, "n_requests must be in [0, 2^31)");
+    if (n_req > 0 && !req_slo) return fail(QLM_ERR_ARG, "req_slo is NULL");
+    return QLM_OK;
+}
+
+FArgs fargs(const qlm_problem *pr, const qlm_plans *pl, const float *req_slo, int64_t n_req,
+            void *ws, const FLayout &L)
+{
+    FArgs a{};
+    a.G = pr->n_groups;
+    a.I = pr->n_instances;
+    a.M = pr->n_models;
+    a.C = pr->n_classes;
+    a.grp_count = pr->grp_count;
+    a.grp_mu = pr->grp_mu;
+    a.grp_var = pr->grp_var;
+    a.grp_model = pr->grp_model;
+    a.inst_tput = pr->inst_tput;
+    a.inst_class = pr->inst_class;
+    a.inst_model0 = pr->inst_model0;
+    a.swap_cost = pr->swap_cost;
+    a.evict_cost = pr->evict_cost;
+    a.P = pl->n_plans;
+    a.ld = pl->plan_stride;
+    a.perm = pl->perm;
+    a.qoff = pl->qoff;
+    a.evict_bits = pl->evict_bits;
+    a.req_slo = req_slo;
+    a.n_req = n_req;
+    unsigned char *w = (unsigned char *)ws;
+    a.grp = (FGrp *)(w + L.grp);
+    a.req = (FReq *)(w + L.req);
+    a.first = (int32_t *)(w + L.first);
+    a.slo64 = (double *)(w + L.slo64);
+    a.tail = (float2 *)(w + L.tail);
+    a.nreq = (double *)(w + L.nreq);
+    a.rec = (FRec *)(w + L.rec);
+    a.piece = (Piece *)(w + L.piece);
+    a.start = (Start *)(w + L.start);
+    a.part = (double *)(w + L.part);
+    a.F = (double *)(w + L.F);
+    a.bmin = (double *)(w + L.bmin);
+    a.ncand = (int32_t *)(w + L.ncand);
+    a.cand = (int64_t *)(w + L.cand);
+    a.Q = (double *)(w + L.Q);
+    a.chunk = L.chunk;
+    a.rld = L.chunk + kRecPad;
+    return a;
+}
+
+int launched(const char *what)
+{
+    const hipError_t e = hipGetLastError();
+    return e == hipSuccess ? QLM_OK : hip_fail(e, what);
+}
+
+// Common start of every call: argument checks, the workspace, the per-call
+// tables.
+int fbegin(const qlm_problem *problem, const qlm_plans *plans, const float *req_slo,
+           int64_t n_req, void *ws, size_t ws_bytes, FArgs *out, FLayout *lay, bool need_tail,
+           bool prep, hipStream_t stream)
+{
+    int rc = check_problem(problem);
+    if (rc) return rc;
+    rc = check_plans(problem, plans);
+    if (rc) return rc;
+    rc = check_requests(problem, req_slo, n_req);
+    if (rc) return rc;
+    if (!ws || ((uintptr_t)ws & 255u))
+        return fail(QLM_ERR_WORKSPACE, "workspace must be non-NULL and 256-byte aligned");
+    // the largest chunk the workspace holds, from the default down to 64 plans
+    FLayout L = flayout(problem, plans->n_plans, n_req, 0);
+    if (ws_bytes < L.total) {
+        const FLayout L64 = flayout(problem, plans->n_plans, n_req, kWave);
+        if (ws_bytes < L64.total) return fail(QLM_ERR_WORKSPACE, "workspace too small");
+        const size_t per = (L.total - L64.total) / (size_t)(L.chunk - kWave);
+        int64_t c = kWave + (int64_t)((ws_bytes - L64.total) / (per > 0 ? per : 1));
+        c = c / kWave * kWave;
+        L = flayout(problem, plans->n_plans, n_req, c);
+        while (L.total > ws_bytes && c > kWave) L = flayout(problem, plans->n_plans, n_req, c -= kWave);
+    }
+    *out = fargs(problem, plans, req_slo, n_req, ws, L);
+    *lay = L;
+    if (plans->n_plans == 0 || !prep) return QLM_OK;
+    hipLaunchKernelGGL(k_fprep, dim3(1), dim3(kThreads), 0, stream, *out);
+    if ((rc = launched("k_fprep launch"))) return rc;
+    if (n_req > 0 && need_tail) {
+        int64_t blocks = (n_req + kThreads - 1) / kThreads;
+        if (blocks > 4096) blocks = 4096;
+        hipLaunchKernelGGL(k_fslo, dim3((unsigned)blocks), dim3(kThreads), 0, stream, *out);
+        if ((rc = launched("k_fslo launch"))) return rc;
+    }
+    if (need_tail) {
+        hipLaunchKernelGGL(k_ftail, dim3(1), dim3(kThreads), 0, stream, *out);
+        if ((rc = launched("k_ftail launch"))) return rc;
+    }
+    return QLM_OK;
+}
+
+// The screen over every plan, chunk by chunk: F and the per-block minima.
+int screen_all(const FArgs &a, hipStream_t stream)
+{
+    int rc;
+    const int nb = (a.G + kGroupsPerWave - 1) / kGroupsPerWave;
+    for (int64_t p0 = 0; p0 < a.P; p0 += a.chunk) {
+        const int64_t pc = a.P - p0 < a.chunk ? a.P - p0 : a.chunk;
+        const int64_t tiles = (pc + kWave - 1) / kWave;
+        const int64_t sq = ((a.G + kSeg - 1) / kSeg + kWaves - 1) / kWaves;
+        hipLaunchKernelGGL(k_fseg, dim3((unsigned)(tiles * sq)), dim3(kThreads), 0, stream, a, p0,
+                           pc);
+        if ((rc = launched("k_fseg launch"))) return rc;
+        hipLaunchKernelGGL(k_fstart, dim3((unsigned)((pc + kThreads - 1) / kThreads)),
+                           dim3(kThreads), 0, stream, a, pc);
+        if ((rc = launched("k_fstart launch"))) return rc;
+        hipLaunchKernelGGL(k_frec, dim3((unsigned)(tiles * sq)), dim3(kThreads), 0, stream, a, p0,
+                           pc);
+        if ((rc = launched("k_frec launch"))) return rc;
+        const int64_t quads = (tiles + kWaves - 1) / kWaves;
+        qlm_internal::TimedLaunch tl;
+        if ((rc = qlm_internal::timing_begin(stream, &tl))) return rc;
+        hipLaunchKernelGGL(k_fscreen, dim3((unsigned)(quads * nb)), dim3(kThreads), 0, stream, a,
+                           p0, pc);
+        if ((rc = launched("k_fscreen launch"))) return rc;
+        qlm_internal::timing_end(stream, &tl);
+        hipLaunchKernelGGL(k_fsum, dim3(kSumBlocks), dim3(kThreads), 0, stream, a, p0, pc,
+                           p0 == 0 ? 1 : 0);
+        if ((rc = launched("k_fsum launch"))) return rc;
+    }
+    return QLM_OK;
+}
+
+int exact_grid(int64_t tasks)
+{
+    int64_t b = (tasks + kWaves - 1) / kWaves;
+    if (b > kExactBlocks) b = kExactBlocks;
+    return (int)(b < 1 ? 1 : b);
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// C interface
+
+extern "C" {
+
+size_t qlm_fcfs_workspace_bytes(const qlm_problem *problem, int64_t n_plans, int64_t n_requests,
+                                int64_t chunk_plans)
+{
+    if (!problem || problem->n_groups < 1 || problem->n_instances < 1) return 0;
+    if (n_plans < 0) n_plans = 0;
+    if (n_requests < 0) n_requests = 0;
+    return flayout(problem, n_plans, n_requests, chunk_plans > 0 ? chunk_plans : 0).total;
+}
+
+int qlm_fcfs_score(const qlm_problem *problem, const qlm_plans *plans, const float *req_slo,
+                   int64_t n_requests, void *ws, size_t ws_bytes, double *score,
+                   qlm_stream stream_)
+{
+    hipStream_t stream = (hipStream_t)stream_;
+    FArgs a;
+    FLayout L;
+    if (plans && plans->n_plans > 0 && !score) return fail(QLM_ERR_ARG, "score is NULL");
+    int rc = fbegin(problem, plans, req_slo, n_requests, ws, ws_bytes, &a, &L, true, true, stream);
+    if (rc) return rc;
+    if (plans->n_plans == 0) return QLM_OK;
+    a.F = score;
+    return screen_all(a, stream);
+}
+
+int qlm_fcfs_score_exact(const qlm_problem *problem, const qlm_plans *plans, const float *req_slo,
+                         int64_t n_requests, const int64_t *plan_index, int64_t n, void *ws,
+                         size_t ws_bytes, double *score, qlm_stream stream_)
+{
+    hipStream_t stream = (hipStream_t)stream_;
+    if (n < 0) return fail(QLM_ERR_ARG, "n must be >= 0");
+    FArgs a;
+    FLayout L;
+    if (n > 0 && (!plan_index || !score))
+        return fail(QLM_ERR_ARG, "plan_index and score are required");
+    if (plans && n > plans->n_plans) return fail(QLM_ERR_ARG, "n must be <= n_plans");
+    int rc = fbegin(problem, plans, req_slo, n_requests, ws, ws_bytes, &a, &L, false, n > 0,
+                    stream);
+    if (rc) return rc;
+    if (n == 0) return QLM_OK;
+    hipLaunchKernelGGL(k_fexact, dim3((unsigned)exact_grid(n * a.I)), dim3(kThreads), 0, stream, a,
+                       plan_index, (const int32_t *)nullptr, n);
+    if ((rc = launched("k_fexact launch"))) return rc;
+    int64_t blocks = (n + kThreads - 1) / kThreads;
+    if (blocks > 1024) blocks = 1024;
+    hipLaunchKernelGGL(k_fplan, dim3((unsigned)blocks), dim3(kThreads), 0, stream, a, n, score);
+    return launched("k_fplan launch");
+}
+
+int qlm_fcfs_best_plan(const qlm_problem *problem, const qlm_plans *plans, const float *req_slo,
+                       int64_t n_requests, void *ws, size_t ws_bytes, int64_t *best_index,
+                       double *best_score, qlm_stream stream_)
+{
+    hipStream_t stream = (hipStream_t)stream_;
+    if (!best_index || !best_score)
+        return fail(QLM_ERR_ARG, "best_index and best_score are required");
+    FArgs a;
+    FLayout L;
+    int rc = fbegin(problem, plans, req_slo, n_requests, ws, ws_bytes, &a, &L, true, true, stream);
+    if (rc) return rc;
+    hipLaunchKernelGGL(k_fzero, dim3(1), dim3(kWave), 0, stream, a);
+    if ((rc = launched("k_fzero launch"))) return rc;
+    if (plans->n_plans > 0) {
+        if ((rc = screen_all(a, stream))) return rc;
+        hipLaunchKernelGGL(k_fselect, dim3(kSumBlocks), dim3(kThreads), 0, stream, a, kSumBlocks);
+        if ((rc = launched("k_fselect launch"))) return rc;
+        hipLaunchKernelGGL(k_fexact, dim3(kExactBlocks), dim3(kThreads), 0, stream, a,
+                           (const int64_t *)a.cand, (const int32_t *)a.ncand, (int64_t)0);
+        if ((rc = launched("k_fexact launch"))) return rc;
+    }
+    hipLaunchKernelGGL(k_fpick, dim3(1), dim3(kPickThreads), 0, stream, a, best_index, best_score);
+    return launched("k_fpick launch");
+}
+
+}  // extern "C"

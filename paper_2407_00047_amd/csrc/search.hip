@@ -82,12 +82,17 @@
 
 #include "internal.h"
 #include "qlm.h"
+#include "ripple.h"
 #include "tail.h"
 
 namespace {
 
 using qlm_internal::fail;
 using qlm_internal::hip_fail;
+using qlm_ripple::from_left;
+using qlm_ripple::from_left0;
+using qlm_ripple::lane_value;
+using qlm_ripple::wave_id;
 
 constexpr int kWave = 64;
 constexpr int kThreads = 256;              // every search kernel: 4 wavefronts
@@ -200,18 +205,6 @@ __device__ inline uint32_t order_key(float f)
     const uint32_t u = __float_as_uint(f);
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
-
-// Lane j's value (j the same in every lane).
-__device__ inline double lane_value(double v, int j)
-{
-    const int hi = __builtin_amdgcn_readlane(__double2hiint(v), j);
-    const int lo = __builtin_amdgcn_readlane(__double2loint(v), j);
-    return __hiloint2double(hi, lo);
-}
-
-// This thread's wavefront within its workgroup, as a value the compiler
-// knows to be the same in every lane (loops over it stay scalar).
-__device__ inline int wave_id() { return __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave)); }
 
 __device__ inline double wave_min(double v)
 {
@@ -350,22 +343,6 @@ __device__ void block_best(double &s, int64_t &k, double *ls, int64_t *lk)
                 k = lk[w];
             }
     }
-}
-
-// Lane l receives lane l - 1's value (DPP wave_shr:1); lane 0 keeps its own.
-__device__ inline double from_left(double v)
-{
-    const int lo = __double2loint(v), hi = __double2hiint(v);
-    return __hiloint2double(__builtin_amdgcn_update_dpp(hi, hi, 0x138, 0xF, 0xF, false),
-                            __builtin_amdgcn_update_dpp(lo, lo, 0x138, 0xF, 0xF, false));
-}
-
-// The same, with zero in lane 0.
-__device__ inline double from_left0(double v)
-{
-    const int lo = __double2loint(v), hi = __double2hiint(v);
-    return __hiloint2double(__builtin_amdgcn_update_dpp(0, hi, 0x138, 0xF, 0xF, false),
-                            __builtin_amdgcn_update_dpp(0, lo, 0x138, 0xF, 0xF, false));
 }
 
 // The exact walk of nv positions by one wavefront (visit() in effect for each

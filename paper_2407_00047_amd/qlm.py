@@ -100,10 +100,17 @@ def library():
                                            ctypes.POINTER(PlansOut), vp, ctypes.c_size_t, vp]
             lib.qlm_local_search.argtypes = [P, PL, ctypes.POINTER(PlansOut), i32, i32, vp,
                                              ctypes.c_size_t, vp, vp, vp, vp]
+            sz = ctypes.c_size_t
+            lib.qlm_fcfs_workspace_bytes.argtypes = [P, i64, i64, i64]
+            lib.qlm_fcfs_workspace_bytes.restype = sz
+            lib.qlm_fcfs_score.argtypes = [P, PL, vp, i64, vp, sz, vp, vp]
+            lib.qlm_fcfs_score_exact.argtypes = [P, PL, vp, i64, vp, i64, vp, sz, vp, vp]
+            lib.qlm_fcfs_best_plan.argtypes = [P, PL, vp, i64, vp, sz, vp, vp, vp]
             for name in ("qlm_rwt_score", "qlm_rwt_score_exact", "qlm_best_plan",
                          "qlm_validate_plans", "qlm_validate_problem", "qlm_timing_enable",
                          "qlm_timing_read", "qlm_search_moves", "qlm_search_screen",
-                         "qlm_local_search", "qlm_seed_plans", "qlm_place_group"):
+                         "qlm_local_search", "qlm_seed_plans", "qlm_place_group",
+                         "qlm_fcfs_score", "qlm_fcfs_score_exact", "qlm_fcfs_best_plan"):
                 getattr(lib, name).restype = ctypes.c_int
             _lib = lib
     return _lib
@@ -402,3 +409,75 @@ def place_group(problem: DeviceProblem, plans: DevicePlans, group: int, ws=None,
                                      ctypes.byref(o), int(group), _ptr(ws), ws.numel(),
                                      _ptr(score), _ptr(queue), _stream(stream)))
     return {"plans": out, "score": score, "queue": queue}
+
+
+# -- per-request (first come, first served) variant ---------------------------
+
+def device_requests(req_slo, device="cuda"):
+    """Per-request SLOs (group by group, each group's in arrival order) as a
+    float32 device tensor."""
+    import torch
+    return torch.as_tensor(np.ascontiguousarray(req_slo, dtype=np.float32)).to(device)
+
+
+def fcfs_workspace_bytes(problem: DeviceProblem, n_plans: int, n_requests: int,
+                         chunk_plans: int = 0) -> int:
+    return int(library().qlm_fcfs_workspace_bytes(ctypes.byref(problem.struct), int(n_plans),
+                                                  int(n_requests), int(chunk_plans)))
+
+
+def fcfs_workspace(problem: DeviceProblem, n_plans: int, n_requests: int, device="cuda",
+                   chunk_plans: int = 0):
+    """A workspace for chunks of chunk_plans plans (0 = the default size)."""
+    import torch
+    nbytes = fcfs_workspace_bytes(problem, n_plans, n_requests, chunk_plans)
+    return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+
+
+def fcfs_score(problem: DeviceProblem, plans: DevicePlans, req_slo, ws=None, stream=None,
+               out=None):
+    """Screened per-request scores of every plan: device tensor [P] f64."""
+    import torch
+    dev = plans.perm.device
+    if ws is None:
+        ws = fcfs_workspace(problem, plans.n_plans, req_slo.numel(), dev)
+    if out is None:
+        out = torch.empty(max(plans.n_plans, 1), dtype=torch.float64, device=dev)
+    _check(library().qlm_fcfs_score(ctypes.byref(problem.struct), ctypes.byref(plans.struct),
+                                    _ptr(req_slo), req_slo.numel(), _ptr(ws), ws.numel(),
+                                    _ptr(out), _stream(stream)))
+    return out[:plans.n_plans]
+
+
+def fcfs_score_exact(problem: DeviceProblem, plans: DevicePlans, req_slo, plan_index, ws=None,
+                     stream=None):
+    """Exact per-request scores of the listed plans: device tensor [n] f64."""
+    import torch
+    dev = plans.perm.device
+    idx = torch.as_tensor(plan_index, dtype=torch.int64).to(dev)
+    if ws is None:
+        ws = fcfs_workspace(problem, plans.n_plans, req_slo.numel(), dev)
+    out = torch.empty(max(idx.numel(), 1), dtype=torch.float64, device=dev)
+    _check(library().qlm_fcfs_score_exact(ctypes.byref(problem.struct),
+                                          ctypes.byref(plans.struct), _ptr(req_slo),
+                                          req_slo.numel(), _ptr(idx), idx.numel(), _ptr(ws),
+                                          ws.numel(), _ptr(out), _stream(stream)))
+    return out[:idx.numel()]
+
+
+def fcfs_best_plan(problem: DeviceProblem, plans: DevicePlans, req_slo, ws=None, stream=None,
+                   out=None):
+    """(best_index, best_score) of the per-request score, device tensors [1]."""
+    import torch
+    dev = plans.perm.device
+    if ws is None:
+        ws = fcfs_workspace(problem, plans.n_plans, req_slo.numel(), dev)
+    if out is None:
+        bi = torch.empty(1, dtype=torch.int64, device=dev)
+        bs = torch.empty(1, dtype=torch.float64, device=dev)
+    else:
+        bi, bs = out
+    _check(library().qlm_fcfs_best_plan(ctypes.byref(problem.struct), ctypes.byref(plans.struct),
+                                        _ptr(req_slo), req_slo.numel(), _ptr(ws), ws.numel(),
+                                        _ptr(bi), _ptr(bs), _stream(stream)))
+    return bi, bs

@@ -31,7 +31,8 @@ def test_header_declares_entry_points():
                  "qlm_status_string", "qlm_last_error", "qlm_search_n_moves",
                  "qlm_search_workspace_bytes", "qlm_search_moves", "qlm_search_screen",
                  "qlm_local_search", "qlm_seed_workspace_bytes", "qlm_seed_plans",
-                 "qlm_place_group"):
+                 "qlm_place_group", "qlm_fcfs_workspace_bytes", "qlm_fcfs_score",
+                 "qlm_fcfs_score_exact", "qlm_fcfs_best_plan"):
         assert must in names
 
 
@@ -182,3 +183,41 @@ def test_place_argument_checks(lib):
     assert pg(P(pr), P(pl), P(out), 1, 0x10000, need - 1, None, None, None) == qlm.QLM_ERR_WORKSPACE
     zero = qlm.Plans(0, 1, None, None, None)
     assert pg(P(pr), P(zero), P(out), 1, 0x10000, need, None, None, None) == qlm.QLM_OK
+
+
+def test_fcfs_argument_checks(lib):
+    from paper_2407_00047_amd import qlm
+    P = ctypes.byref
+    pr = _problem(qlm, G=8, I=2)
+    pl = qlm.Plans(3, 3, 0x1000, 0x1000, None)
+    need = lib.qlm_fcfs_workspace_bytes(P(pr), 3, 40, 0)
+    assert need > 0 and need % 256 == 0
+    assert lib.qlm_fcfs_workspace_bytes(P(pr), 3, 4000, 0) > need
+    assert lib.qlm_fcfs_workspace_bytes(None, 3, 40, 0) == 0
+    assert lib.qlm_fcfs_workspace_bytes(P(pr), 3, 40, 64) == need     # 3 plans: one chunk of 64
+    big = qlm.Problem(8192, 64, 1, 1, 1, 1, 1, 1, 1, 1, 1, None, None, 0.0)
+    full = lib.qlm_fcfs_workspace_bytes(P(big), 20000, 100, 0)
+    small = lib.qlm_fcfs_workspace_bytes(P(big), 20000, 100, 100)
+    assert small < full and lib.qlm_fcfs_workspace_bytes(P(big), 20000, 100, 128) == small
+    ws, slo, out = 0x10000, 0x2000, 0x3000
+    fs, fx, fb = lib.qlm_fcfs_score, lib.qlm_fcfs_score_exact, lib.qlm_fcfs_best_plan
+    assert fs(P(pr), P(pl), None, 40, ws, need, out, None) == qlm.QLM_ERR_ARG
+    assert fs(P(pr), P(pl), slo, -1, ws, need, out, None) == qlm.QLM_ERR_ARG
+    assert fs(P(pr), P(pl), slo, 1 << 31, ws, need, out, None) == qlm.QLM_ERR_ARG
+    assert fs(P(pr), P(pl), slo, 40, ws, need, None, None) == qlm.QLM_ERR_ARG
+    assert fs(P(pr), P(pl), slo, 40, ws, need - 1, out, None) == qlm.QLM_ERR_WORKSPACE
+    assert fs(P(pr), P(pl), slo, 40, ws + 8, need, out, None) == qlm.QLM_ERR_WORKSPACE
+    assert fs(P(pr), P(pl), slo, 40, None, need, out, None) == qlm.QLM_ERR_WORKSPACE
+    assert fs(None, P(pl), slo, 40, ws, need, out, None) == qlm.QLM_ERR_ARG
+    idx = 0x4000
+    assert fx(P(pr), P(pl), slo, 40, None, 2, ws, need, out, None) == qlm.QLM_ERR_ARG
+    assert fx(P(pr), P(pl), slo, 40, idx, -1, ws, need, out, None) == qlm.QLM_ERR_ARG
+    assert fx(P(pr), P(pl), slo, 40, idx, 4, ws, need, out, None) == qlm.QLM_ERR_ARG
+    assert fx(P(pr), P(pl), slo, 40, idx, 2, ws, need - 1, out, None) == qlm.QLM_ERR_WORKSPACE
+    assert fx(P(pr), P(pl), slo, 40, idx, 0, ws, need, out, None) == qlm.QLM_OK
+    assert fb(P(pr), P(pl), slo, 40, ws, need, None, out, None) == qlm.QLM_ERR_ARG
+    assert fb(P(pr), P(pl), None, 40, ws, need, idx, out, None) == qlm.QLM_ERR_ARG
+    zero = qlm.Plans(0, 1, None, None, None)
+    need0 = lib.qlm_fcfs_workspace_bytes(P(pr), 0, 40, 0)
+    assert fs(P(pr), P(zero), slo, 40, ws, need0, None, None) == qlm.QLM_OK
+
