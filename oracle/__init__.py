@@ -59,6 +59,15 @@ class _Plans(ctypes.Structure):
                 ("evict_bits", ctypes.c_void_p)]
 
 
+class _Profile(ctypes.Structure):
+    _fields_ = [("prefill", ctypes.c_void_p), ("decode_time", ctypes.c_void_p),
+                ("ineff", ctypes.c_void_p), ("max_tokens", ctypes.c_void_p),
+                ("kv_tokens", ctypes.c_void_p), ("mean_tokens", ctypes.c_void_p)]
+
+
+PROFILE_FIELDS = ("prefill", "decode_time", "ineff", "max_tokens", "kv_tokens", "mean_tokens")
+
+
 class Oracle:
     """A loaded oracle library.  ``Oracle()`` is the committed source built by
     ``build()``; tests may load another build of it (for mutation checks)."""
@@ -101,6 +110,9 @@ class Oracle:
         lib.oracle_score_plans_fcfs.argtypes = [ctypes.POINTER(_Problem), ctypes.POINTER(_Plans),
                                                 vp, i64, i64, i64, dp, ctypes.c_int]
         lib.oracle_score_plans_fcfs.restype = ctypes.c_int64
+        lib.oracle_apply_profile.argtypes = [ctypes.POINTER(_Problem), ctypes.POINTER(_Profile),
+                                             vp, vp, vp, vp, vp, i64, vp]
+        lib.oracle_apply_profile.restype = None
         self.lib = lib
         self.path = path
 
@@ -190,6 +202,48 @@ class Oracle:
     def best_plan_fcfs(self, problem, plans, req_slo, threads: int = 0) -> tuple[int, float]:
         """argmin_p of the per-request score, lowest index on ties."""
         return self.argmin(self.score_plans_fcfs(problem, plans, req_slo, threads=threads))
+
+    # -- problem tables from a hardware profile -----------------------------
+
+    def apply_profile(self, problem, profile, inst_model=None, req_slo=None):
+        """The problem with its swap table (plus the drain before a model
+        change), SLOs (less the prefill) and throughputs (from the GPU's token
+        memory, the decode step and the inefficiency) derived from a hardware
+        profile: a dict of [M] or [C*M] float32 arrays, any of them None.
+        Returns (problem, req_slo or None)."""
+        G, I = int(problem["n_groups"]), int(problem["n_instances"])
+        M, C = int(problem["n_models"]), int(problem["n_classes"])
+        plans = {"n_plans": 0, "perm": np.zeros((G, 1), np.int32),
+                 "qoff": np.zeros((I + 1, 1), np.int32), "evict_bits": None}
+        b = _Bound(problem, plans)
+        keep = []
+        pf = _Profile()
+        sizes = {"prefill": M, "decode_time": C * M, "ineff": C * M, "max_tokens": M,
+                 "kv_tokens": C * M, "mean_tokens": M}
+        for f in PROFILE_FIELDS:
+            x = profile.get(f)
+            if x is not None:
+                x = np.ascontiguousarray(x, dtype=np.float32).reshape(-1)
+                if x.size != sizes[f]:
+                    raise ValueError(f + " has the wrong size")
+                keep.append(x)
+            setattr(pf, f, _ptr(x))
+        im = None if inst_model is None else np.ascontiguousarray(inst_model, np.int32)
+        if im is not None and (im.size != I or im.max() >= M or im.min() < -1):
+            raise ValueError("inst_model must be [I] in [-1, M)")
+        swap = np.empty(C * M * M, np.float32)
+        slo = np.empty(G, np.float32)
+        tput = np.empty(I, np.float32)
+        rs = None if req_slo is None else np.ascontiguousarray(req_slo, np.float32)
+        rso = None if rs is None else np.empty_like(rs)
+        self.lib.oracle_apply_profile(ctypes.byref(b.problem), ctypes.byref(pf), _ptr(im),
+                                      _ptr(swap), _ptr(slo), _ptr(tput), _ptr(rs),
+                                      0 if rs is None else rs.size, _ptr(rso))
+        out = dict(problem)
+        out["swap_cost"] = swap
+        out["grp_slo"] = slo
+        out["inst_tput"] = tput
+        return out, rso
 
     # -- plan search -------------------------------------------------------
 
@@ -432,3 +486,7 @@ def plan_fcfs(problem, plans, req_slo, p: int):
 
 def best_plan_fcfs(problem, plans, req_slo, threads: int = 0) -> tuple[int, float]:
     return default().best_plan_fcfs(problem, plans, req_slo, threads)
+
+
+def apply_profile(problem, profile, inst_model=None, req_slo=None):
+    return default().apply_profile(problem, profile, inst_model, req_slo)

@@ -326,6 +326,91 @@ int64_t oracle_score_plans_fcfs(const oracle_problem *pr, const oracle_plans *pl
 }
 
 /* ------------------------------------------------------------------------
+ * Problem tables from a hardware profile: prefill, drain and throughput.
+ *
+ * The completion time of a request is its wait, its prefill and its decode,
+ * C_q = W_q + P + D_q (Sec. 6, Eq. total_completion_time), with P constant per
+ * model, D_q = O_q * eps * d (Eq. total_decode_time; O_q taken as the
+ * model's largest output, the estimator's conservative choice) and a group's
+ * completion the latest of its requests' (Eq. group_completion_time).
+ *
+ *   prefill   The SLO bounds the time to the first token (Sec. 3, Definition
+ *             "SLO"), which is the wait plus the request's own prefill, so a
+ *             request misses it when W > slo - P[m].  The SLO table becomes
+ *             slo - P[m_i].
+ *   drain     Before an instance of class c changes from model a to model b,
+ *             the requests already running must complete: the latest of them,
+ *             admitted last, needs its prefill and up to O_max decode steps,
+ *             P[a] + O_max[a] * eps[c][a] * d[c][a].  This is the completion
+ *             time that Eq. completion_time charges at every model transition
+ *             (its third term), so the swap table becomes
+ *             S[c][a][b] + P[a] + O_max[a] * eps[c][a] * d[c][a] for a != b.
+ *   Theta     The token throughput of an instance is its batch over the time
+ *             of one decode step, Theta = B / (d * eps), and the batch is what
+ *             the GPU's token memory holds, B = GPU / E[I + O] (Appendix,
+ *             waiting time predictability).  Instance g of class c serving
+ *             model m gets Theta[c][m].
+ *
+ * Each value is formed in double precision and stored in single precision,
+ * the precision of the problem tables.  A NULL profile array leaves its term
+ * out (no prefill; no drain; the throughputs as given).
+ */
+typedef struct {
+    const float *prefill;      /* [M]    P, seconds                           */
+    const float *decode_time;  /* [C][M] d, seconds per output token          */
+    const float *ineff;        /* [C][M] eps, inefficiency factor             */
+    const float *max_tokens;   /* [M]    O_max, largest output of the model   */
+    const float *kv_tokens;    /* [C][M] GPU, tokens the memory holds         */
+    const float *mean_tokens;  /* [M]    E[I + O], tokens per request         */
+} oracle_profile;
+
+void oracle_apply_profile(const oracle_problem *pr, const oracle_profile *pf,
+                          const int32_t *inst_model, float *swap_out, float *slo_out,
+                          float *tput_out, const float *req_slo, int64_t n_requests,
+                          float *req_slo_out)
+{
+    const int G = pr->n_groups, I = pr->n_instances, M = pr->n_models, C = pr->n_classes;
+    const int drain = pf->prefill && pf->decode_time && pf->ineff && pf->max_tokens;
+    for (int c = 0; c < C; ++c)
+        for (int a = 0; a < M; ++a)
+            for (int b = 0; b < M; ++b) {
+                const int64_t k = ((int64_t)c * M + a) * M + b;
+                double S = pr->swap_cost ? (double)pr->swap_cost[k] : 0.0;
+                if (drain && a != b) {
+                    const int64_t ca = (int64_t)c * M + a;
+                    const double D = (double)pf->max_tokens[a] * (double)pf->ineff[ca] *
+                                     (double)pf->decode_time[ca];
+                    S = S + ((double)pf->prefill[a] + D);
+                }
+                swap_out[k] = (float)S;
+            }
+    for (int i = 0; i < G; ++i) {
+        double slo = (double)pr->grp_slo[i];
+        if (pf->prefill) slo = slo - (double)pf->prefill[pr->grp_model[i]];
+        slo_out[i] = (float)slo;
+    }
+    if (req_slo && req_slo_out) {
+        int64_t r = 0;
+        for (int i = 0; i < G && r < n_requests; ++i)
+            for (int32_t k = 0; k < pr->grp_count[i] && r < n_requests; ++k, ++r) {
+                double slo = (double)req_slo[r];
+                if (pf->prefill) slo = slo - (double)pf->prefill[pr->grp_model[i]];
+                req_slo_out[r] = (float)slo;
+            }
+    }
+    for (int g = 0; g < I; ++g) {
+        double theta = (double)pr->inst_tput[g];
+        const int m = inst_model ? inst_model[g] : -1;
+        if (pf->kv_tokens && pf->decode_time && pf->ineff && pf->mean_tokens && m >= 0) {
+            const int64_t cm = (int64_t)pr->inst_class[g] * M + m;
+            const double B = (double)pf->kv_tokens[cm] / (double)pf->mean_tokens[m];
+            theta = B / ((double)pf->decode_time[cm] * (double)pf->ineff[cm]);
+        }
+        tput_out[g] = (float)theta;
+    }
+}
+
+/* ------------------------------------------------------------------------
  * Plan search: a local search over plans.
  *
  * The paper's global scheduler places groups by solving the assignment

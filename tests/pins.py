@@ -905,10 +905,85 @@ def pin_fcfs_monte_carlo(orc):
     assert abs(tot.mean() - d["score"]) <= 5 * tot.std() / np.sqrt(N)
 
 
+# ---------------------------------------------------------------------------
+# Problem tables from a hardware profile
+
+
+def _profile_by_hand():
+    # two classes, two models; decode times and factors chosen so that the
+    # derived throughputs and drains are exact in binary
+    return {"prefill": [0.25, 0.5],
+            "decode_time": [1 / 32, 1 / 64, 1 / 16, 1 / 128],   # [c][m]
+            "ineff": [2.0, 1.5, 1.0, 2.0],
+            "max_tokens": [512.0, 256.0],
+            "kv_tokens": [4096.0, 8192.0, 2048.0, 65536.0],
+            "mean_tokens": [512.0, 256.0]}
+
+
+def pin_profile_by_hand(orc):
+    """Sec. 6 (completion = wait + prefill + decode, decode = O eps d, a group
+    completes with its last request) and the Appendix (Theta = B / (d eps),
+    B = GPU / E[I + O]), worked by hand:
+      Theta[0][0] = (4096/512) / (2/32) = 128 tok/s, Theta[1][1] = (65536/256) / (2/128) = 16384;
+      drain[0][0] = 0.25 + 512*2/32 = 32.25 s, drain[0][1] = 0.5 + 256*1.5/64 = 6.5 s,
+      drain[1][0] = 0.25 + 512/16 = 32.25 s, drain[1][1] = 0.5 + 256*2/128 = 4.5 s;
+    the swap table gains the drain of the model left behind; SLOs lose the
+    prefill of the group's model."""
+    S = np.array([[[99, 10], [20, 99]], [[99, 1], [2, 99]]], np.float32)
+    groups = [(1, 128.0, 0.0, 0, 100.0), (2, 64.0, 0.0, 1, 43.5), (1, 128.0, 0.0, 1, 45.0),
+              (1, 128.0, 0.0, 0, 50.0)]
+    pr = problem(groups, [(999.0, 0), (999.0, 1)], n_models=2, n_classes=2, swap=S)
+    out, _ = orc.apply_profile(pr, _profile_by_hand(), inst_model=[0, 1])
+    assert list(out["inst_tput"]) == [128.0, 16384.0], out["inst_tput"]
+    want = np.array([[[99, 42.25], [26.5, 99]], [[99, 33.25], [6.5, 99]]], np.float32)
+    assert np.array_equal(out["swap_cost"], want.reshape(-1)), out["swap_cost"]
+    assert list(out["grp_slo"]) == [99.75, 43.0, 44.5, 49.75], out["grp_slo"]
+    # queue 0 (Theta 128): groups 0 (model 0, 1 s of tokens), 1 and 2 (model 1,
+    # 1 s each): waits 0, 1 + 42.25, 44.25.  Group 1's TTFT (43.25 + 0.5) is
+    # past its SLO of 43.5, group 2's (44.25 + 0.5) is not
+    d = orc.plan_detail(out, plans([[[0, 1, 2], [3]]], 4), 0)
+    assert list(d["wait_mean"]) == [0.0, 43.25, 44.25, 0.0], d["wait_mean"]
+    assert list(d["prob"]) == [0.0, 1.0, 0.0, 0.0], d["prob"]
+    assert d["score"] == 2.0
+    # no profile: the tables as given
+    same, _ = orc.apply_profile(pr, {})
+    assert np.array_equal(same["swap_cost"], pr["swap_cost"])
+    assert np.array_equal(same["grp_slo"], pr["grp_slo"])
+    assert np.array_equal(same["inst_tput"], pr["inst_tput"])
+    # per-request SLOs lose the prefill of their group's model
+    req = np.arange(5, dtype=np.float32) + 10.0
+    _, rs = orc.apply_profile(pr, {"prefill": [0.25, 0.5]}, req_slo=req)
+    assert list(rs) == [9.75, 10.5, 11.5, 12.5, 13.75], rs
+
+
+def pin_profile_scaling(orc):
+    """Theta grows with the token memory and falls with the decode time, the
+    inefficiency and the tokens per request, each in proportion (Appendix):
+    random profiles, each factor doubled in turn."""
+    rng = np.random.default_rng(17)
+    C, M = 2, 3
+    pr = problem([(1, 100.0, 10.0, m % M, 50.0) for m in range(4)],
+                 [(1000.0, c % C) for c in range(4)], n_models=M, n_classes=C)
+    base = {"prefill": rng.uniform(0.05, 0.5, M), "decode_time": rng.uniform(0.01, 0.05, C * M),
+            "ineff": rng.uniform(1.0, 1.6, C * M), "max_tokens": rng.uniform(256, 4096, M),
+            "kv_tokens": rng.uniform(1e5, 1e6, C * M), "mean_tokens": rng.uniform(200, 900, M)}
+    base = {k: np.float32(v) for k, v in base.items()}
+    im = [0, 1, 2, 1]
+    t0 = orc.apply_profile(pr, base, inst_model=im)[0]["inst_tput"].astype(np.float64)
+    for f, power in (("kv_tokens", 1), ("decode_time", -1), ("ineff", -1), ("mean_tokens", -1)):
+        p2 = dict(base)
+        p2[f] = base[f] * np.float32(2)
+        t = orc.apply_profile(pr, p2, inst_model=im)[0]["inst_tput"].astype(np.float64)
+        assert np.allclose(t / t0, 2.0 ** power, rtol=2e-7), (f, t / t0)
+    # an instance without a model keeps its throughput
+    t = orc.apply_profile(pr, base, inst_model=[-1, 1, 2, 1])[0]["inst_tput"]
+    assert t[0] == 1000.0
+
+
 ALL_PINS = [pin_deterministic_queue, pin_variance_queue, pin_normal_table, pin_swap_costs,
             pin_eviction_costs, pin_throughput_per_queue, pin_invariants, pin_half_at_mean,
             pin_identical_instances_symmetry, pin_monte_carlo, pin_edf_special_case,
             pin_grouping_special_case, pin_argmin_ties, pin_moves_by_hand, pin_moves_independent,
             pin_search_by_hand, pin_search_steepest, pin_seed_by_hand, pin_seed_special_cases,
             pin_seed_restated, pin_place_by_hand, pin_place_restated, pin_fcfs_by_hand,
-            pin_fcfs_exploded, pin_fcfs_monte_carlo]
+            pin_fcfs_exploded, pin_fcfs_monte_carlo, pin_profile_by_hand, pin_profile_scaling]

@@ -116,6 +116,25 @@ MUTANTS = [
     ("fcfs_head_model_ignored",
      "int m_prev = pr->inst_model0 ? pr->inst_model0[g] : -1;\n        double A = 0.0, V = 0.0, K = 0.0;",
      "int m_prev = -1;\n        double A = 0.0, V = 0.0, K = 0.0;"),
+    # problem tables from a hardware profile
+    ("profile_drain_of_new_model", "const int64_t ca = (int64_t)c * M + a;",
+     "const int64_t ca = (int64_t)c * M + b;"),
+    ("profile_drain_without_prefill", "S = S + ((double)pf->prefill[a] + D);", "S = S + D;"),
+    ("profile_drain_on_diagonal", "if (drain && a != b) {", "if (drain) {"),
+    ("profile_drain_without_ineff",
+     "const double D = (double)pf->max_tokens[a] * (double)pf->ineff[ca] *",
+     "const double D = (double)pf->max_tokens[a] * 1.0 *"),
+    ("profile_prefill_added", "if (pf->prefill) slo = slo - (double)pf->prefill[pr->grp_model[i]];",
+     "if (pf->prefill) slo = slo + (double)pf->prefill[pr->grp_model[i]];"),
+    ("profile_theta_ineff_inverted",
+     "theta = B / ((double)pf->decode_time[cm] * (double)pf->ineff[cm]);",
+     "theta = B * (double)pf->ineff[cm] / (double)pf->decode_time[cm];"),
+    ("profile_batch_inverted",
+     "const double B = (double)pf->kv_tokens[cm] / (double)pf->mean_tokens[m];",
+     "const double B = (double)pf->mean_tokens[m] / (double)pf->kv_tokens[cm];"),
+    ("profile_class_of_first_instance",
+     "const int64_t cm = (int64_t)pr->inst_class[g] * M + m;",
+     "const int64_t cm = (int64_t)pr->inst_class[0] * M + m;"),
 ]
 
 
