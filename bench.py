@@ -474,6 +474,9 @@ def main():
                     help="benchmark the per-request FCFS variant instead")
     ap.add_argument("--chunk", type=int, default=0,
                     help="--fcfs: plans per screening chunk (0 = the library's default)")
+    ap.add_argument("--with-profile", action="store_true",
+                    help="fold a synthetic hardware profile (prefill, drain, throughput) into "
+                         "the problem tables first")
     ap.add_argument("--chains", type=int, default=1, help="--search / --place: plans")
     ap.add_argument("--window", type=int, default=16, help="--search: swap window")
     ap.add_argument("--summarize-counters", nargs=4, metavar=("FETCH", "WRITE", "COPY_FETCH", "COPY_WRITE"),
@@ -523,6 +526,24 @@ def main():
                                                      pr["n_instances"], P,
                                                      time.perf_counter() - t0))
     dpr = qlm.DeviceProblem(pr, device=dev)
+    profile_ms = None
+    if args.with_profile:
+        # the estimator's prefill, drain and throughput terms folded into the
+        # tables (instance g profiled for model g mod M); timed once
+        pf = workload.make_profile(pr)
+        im = [g % pr["n_models"] for g in range(pr["n_instances"])]
+        p0 = torch.cuda.Event(enable_timing=True)
+        p1 = torch.cuda.Event(enable_timing=True)
+        qlm.apply_profile(dpr, pf, inst_model=im)
+        torch.cuda.synchronize()
+        p0.record()
+        dpr, _ = qlm.apply_profile(dpr, pf, inst_model=im)
+        p1.record()
+        torch.cuda.synchronize()
+        profile_ms = p0.elapsed_time(p1)
+        if not args.no_cpu_baseline:
+            import oracle
+            pr = oracle.apply_profile(pr, pf, inst_model=im)[0]
     dpl = qlm.DevicePlans.from_host(pl, device=dev)
     ws = qlm.workspace(dpr, P, device=dev)
     bi = torch.empty(1, dtype=torch.int64, device=dev)
@@ -582,6 +603,9 @@ def main():
         "best_index": best_index, "best_score": best_score,
         "roofline": roofline, "cpu_baseline": cpu,
     }
+    if args.with_profile:
+        out["config"]["workload"] += ", tables from a hardware profile"
+        out["profile_ms"] = round(profile_ms, 4)
     print(json.dumps(out), flush=True)
 
 

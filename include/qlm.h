@@ -361,6 +361,52 @@ int qlm_fcfs_best_plan(const qlm_problem *problem, const qlm_plans *plans, const
                        int64_t n_requests, void *ws, size_t ws_bytes, int64_t *best_index,
                        double *best_score, qlm_stream stream);
 
+/*
+ * A hardware profile (Sec. 6, "Offline profiling": workload and hardware
+ * profiling of the estimator's constants), per model m and per (instance
+ * class c, model m), row-major [C][M].  Device arrays; any may be NULL, which
+ * leaves out the terms that need it.
+ */
+typedef struct qlm_profile {
+    const float *prefill;        /* [M]    P, prefill time of a request, seconds
+                                    (constant per model, Sec. 6)                */
+    const float *decode_time;    /* [C][M] d, seconds per output token          */
+    const float *ineff;          /* [C][M] eps, inefficiency of continuous batching */
+    const float *max_tokens;     /* [M]    O_max, the model's largest output     */
+    const float *kv_tokens;      /* [C][M] GPU, tokens the GPU memory holds      */
+    const float *mean_tokens;    /* [M]    E[I + O], tokens per request          */
+} qlm_profile;
+
+/*
+ * Problem tables with the estimator's prefill, drain and throughput terms
+ * folded in (Sec. 6, Eqs. total_completion_time, total_decode_time,
+ * group_completion_time; Sec. 7, Eq. completion_time; Appendix, waiting time
+ * predictability), for the scoring calls to read in place of the problem's own:
+ *   slo_out  [G]      grp_slo[i] - P[m_i]: the SLO bounds the time to the
+ *                     first token, the wait plus the request's own prefill
+ *   swap_out [C][M][M] S[c][a][b] + (P[a] + O_max[a] eps[c][a] d[c][a]) for
+ *                     a != b (the running requests of model a finish before
+ *                     the swap: the completion time Eq. completion_time
+ *                     charges at each transition); S = 0 where swap_cost is
+ *                     NULL; the diagonal is copied
+ *   tput_out [I]      Theta = (GPU[c][m] / E[I+O][m]) / (d[c][m] eps[c][m])
+ *                     for instance g of class c serving inst_model[g] = m (the
+ *                     batch the memory holds over one decode step); the
+ *                     problem's inst_tput where inst_model is NULL or -1
+ *   req_slo_out [n]   per-request SLOs (qlm_fcfs_* layout) less the prefill of
+ *                     their group's model; req_slo and req_slo_out both NULL
+ *                     or both given
+ * The drain needs prefill, decode_time, ineff and max_tokens; the throughput
+ * needs kv_tokens, decode_time, ineff, mean_tokens and inst_model.  Each value
+ * is formed in double precision in the order written and stored in single
+ * precision.  The outputs are device arrays of the caller and may not alias
+ * the inputs.
+ */
+int qlm_apply_profile(const qlm_problem *problem, const qlm_profile *profile,
+                      const int32_t *inst_model, float *swap_out, float *slo_out, float *tput_out,
+                      const float *req_slo, int64_t n_requests, float *req_slo_out,
+                      qlm_stream stream);
+
 /* Largest G the scoring kernels accept for these M, C, I (on-chip budget). */
 int32_t qlm_max_groups(int32_t n_models, int32_t n_classes, int32_t n_instances,
                        int32_t with_eviction);

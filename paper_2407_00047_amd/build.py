@@ -14,7 +14,7 @@ ROOT = os.path.dirname(HERE)
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 LIB = os.path.join(HERE, "libqlm.so")
 ARCH = "gfx950"
-SOURCES = ["qlm.hip", "search.hip", "fcfs.hip"]
+SOURCES = ["qlm.hip", "search.hip", "fcfs.hip", "profile.hip"]
 
 HIP_FLAGS = [
     "-O3", "-std=c++17", "--offload-arch=" + ARCH, "-fPIC", "-shared",

@@ -59,6 +59,15 @@ class Detail(ctypes.Structure):
                 ("prob", ctypes.c_void_p)]
 
 
+class Profile(ctypes.Structure):
+    _fields_ = [("prefill", ctypes.c_void_p), ("decode_time", ctypes.c_void_p),
+                ("ineff", ctypes.c_void_p), ("max_tokens", ctypes.c_void_p),
+                ("kv_tokens", ctypes.c_void_p), ("mean_tokens", ctypes.c_void_p)]
+
+
+PROFILE_FIELDS = ("prefill", "decode_time", "ineff", "max_tokens", "kv_tokens", "mean_tokens")
+
+
 def library():
     """The loaded libqlm; raises when it has not been built."""
     global _lib
@@ -106,11 +115,14 @@ def library():
             lib.qlm_fcfs_score.argtypes = [P, PL, vp, i64, vp, sz, vp, vp]
             lib.qlm_fcfs_score_exact.argtypes = [P, PL, vp, i64, vp, i64, vp, sz, vp, vp]
             lib.qlm_fcfs_best_plan.argtypes = [P, PL, vp, i64, vp, sz, vp, vp, vp]
+            lib.qlm_apply_profile.argtypes = [P, ctypes.POINTER(Profile), vp, vp, vp, vp, vp, i64,
+                                              vp, vp]
             for name in ("qlm_rwt_score", "qlm_rwt_score_exact", "qlm_best_plan",
                          "qlm_validate_plans", "qlm_validate_problem", "qlm_timing_enable",
                          "qlm_timing_read", "qlm_search_moves", "qlm_search_screen",
                          "qlm_local_search", "qlm_seed_plans", "qlm_place_group",
-                         "qlm_fcfs_score", "qlm_fcfs_score_exact", "qlm_fcfs_best_plan"):
+                         "qlm_fcfs_score", "qlm_fcfs_score_exact", "qlm_fcfs_best_plan",
+                         "qlm_apply_profile"):
                 getattr(lib, name).restype = ctypes.c_int
             _lib = lib
     return _lib
@@ -481,3 +493,50 @@ def fcfs_best_plan(problem: DeviceProblem, plans: DevicePlans, req_slo, ws=None,
                                         _ptr(req_slo), req_slo.numel(), _ptr(ws), ws.numel(),
                                         _ptr(bi), _ptr(bs), _stream(stream)))
     return bi, bs
+
+
+# -- problem tables from a hardware profile -----------------------------------
+
+def apply_profile(problem: DeviceProblem, profile, inst_model=None, req_slo=None, stream=None):
+    """The problem with the profile's prefill, drain and throughput folded into
+    its SLO, swap and throughput tables (a new DeviceProblem sharing the other
+    arrays), and the per-request SLOs less the prefill when req_slo is given.
+    ``profile`` maps the qlm_profile field names to arrays (or None)."""
+    import copy
+    import torch
+    dev = problem.grp_count.device
+    M, C = problem.n_models, problem.n_classes
+    keep = {}
+    for f in PROFILE_FIELDS:
+        x = profile.get(f)
+        keep[f] = None if x is None else torch.as_tensor(
+            np.ascontiguousarray(x, dtype=np.float32).reshape(-1)).to(dev)
+    sizes = {"prefill": M, "decode_time": C * M, "ineff": C * M, "max_tokens": M,
+             "kv_tokens": C * M, "mean_tokens": M}
+    for f, x in keep.items():
+        if x is not None and x.numel() != sizes[f]:
+            raise ValueError(f + " has the wrong size")
+    im = None if inst_model is None else torch.as_tensor(
+        np.ascontiguousarray(inst_model, dtype=np.int32)).to(dev)
+    if im is not None and im.numel() != problem.n_instances:
+        raise ValueError("inst_model must have n_instances entries")
+    pf = Profile(*[_ptr(keep[f]) for f in PROFILE_FIELDS])
+    out = copy.copy(problem)
+    out.swap_cost = torch.empty(C * M * M, dtype=torch.float32, device=dev)
+    out.grp_slo = torch.empty(problem.n_groups, dtype=torch.float32, device=dev)
+    out.inst_tput = torch.empty(problem.n_instances, dtype=torch.float32, device=dev)
+    rs = None
+    if req_slo is not None:
+        rs = torch.empty_like(req_slo)
+    _check(library().qlm_apply_profile(ctypes.byref(problem.struct), ctypes.byref(pf), _ptr(im),
+                                       _ptr(out.swap_cost), _ptr(out.grp_slo),
+                                       _ptr(out.inst_tput), _ptr(req_slo),
+                                       0 if req_slo is None else req_slo.numel(), _ptr(rs),
+                                       _stream(stream)))
+    out._profile_keep = (keep, im)
+    out.struct = Problem(out.n_groups, out.n_instances, out.n_models, out.n_classes,
+                         _ptr(out.grp_count), _ptr(out.grp_mu), _ptr(out.grp_var),
+                         _ptr(out.grp_model), _ptr(out.grp_slo), _ptr(out.inst_tput),
+                         _ptr(out.inst_class), _ptr(out.inst_model0), _ptr(out.swap_cost),
+                         out.evict_cost)
+    return out, rs

@@ -232,3 +232,22 @@ def make_request_slos(problem, seed: int | None = None):
     c = np.cumsum(gap)
     age = c[end - 1] - c                             # gaps of the later requests
     return (slo[grp] - age).astype(np.float32)
+
+
+def make_profile(problem, seed: int | None = None):
+    """A synthetic hardware profile for the problem's classes and models (the
+    constants the estimator profiles offline): prefill 0.05-0.5 s per model,
+    decode time per output token 8-40 ms and inefficiency 1.05-1.5 per (class,
+    model), the largest output 1024-4096 tokens per model, a token memory of
+    5e4-4e5 tokens per (class, model), 300-1200 tokens per request per model.
+    Arrays float32, [M] or [C*M] (class-major)."""
+    seed = (int(problem["seed"]) ^ 0x9F0F) if seed is None else seed
+    rng = np.random.default_rng(seed)
+    C, M = int(problem["n_classes"]), int(problem["n_models"])
+    f = np.float32
+    return {"prefill": rng.uniform(0.05, 0.5, M).astype(f),
+            "decode_time": rng.uniform(0.008, 0.040, C * M).astype(f),
+            "ineff": rng.uniform(1.05, 1.5, C * M).astype(f),
+            "max_tokens": np.floor(rng.uniform(1024, 4097, M)).astype(f),
+            "kv_tokens": np.floor(rng.uniform(5e4, 4e5, C * M)).astype(f),
+            "mean_tokens": np.floor(rng.uniform(300, 1201, M)).astype(f)}

@@ -32,7 +32,7 @@ def test_header_declares_entry_points():
                  "qlm_search_workspace_bytes", "qlm_search_moves", "qlm_search_screen",
                  "qlm_local_search", "qlm_seed_workspace_bytes", "qlm_seed_plans",
                  "qlm_place_group", "qlm_fcfs_workspace_bytes", "qlm_fcfs_score",
-                 "qlm_fcfs_score_exact", "qlm_fcfs_best_plan"):
+                 "qlm_fcfs_score_exact", "qlm_fcfs_best_plan", "qlm_apply_profile"):
         assert must in names
 
 
@@ -220,4 +220,21 @@ def test_fcfs_argument_checks(lib):
     zero = qlm.Plans(0, 1, None, None, None)
     need0 = lib.qlm_fcfs_workspace_bytes(P(pr), 0, 40, 0)
     assert fs(P(pr), P(zero), slo, 40, ws, need0, None, None) == qlm.QLM_OK
+
+
+def test_profile_argument_checks(lib):
+    from paper_2407_00047_amd import qlm
+    P = ctypes.byref
+    pr = _problem(qlm, G=8, I=2, M=2, C=1)
+    pf = qlm.Profile(None, None, None, None, None, None)
+    out = 0x5000
+    ap = lib.qlm_apply_profile
+    assert ap(P(pr), None, None, out, out, out, None, 0, None, None) == qlm.QLM_ERR_ARG
+    assert ap(P(pr), P(pf), None, None, out, out, None, 0, None, None) == qlm.QLM_ERR_ARG
+    assert ap(P(pr), P(pf), None, out, None, out, None, 0, None, None) == qlm.QLM_ERR_ARG
+    assert ap(P(pr), P(pf), None, out, out, None, None, 0, None, None) == qlm.QLM_ERR_ARG
+    assert ap(P(pr), P(pf), None, out, out, out, 0x6000, -1, out, None) == qlm.QLM_ERR_ARG
+    assert ap(P(pr), P(pf), None, out, out, out, 0x6000, 4, None, None) == qlm.QLM_ERR_ARG
+    assert ap(P(pr), P(pf), None, out, out, out, None, 4, out, None) == qlm.QLM_ERR_ARG
+    assert ap(None, P(pf), None, out, out, out, None, 0, None, None) == qlm.QLM_ERR_ARG
 
