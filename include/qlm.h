@@ -274,6 +274,33 @@ int qlm_place_group(const qlm_problem *problem, const qlm_plans *start,
                     double *score, int32_t *queue, qlm_stream stream);
 
 /*
+ * A placement session: the plans stay in the workspace between placements, so
+ * that a stream of arrivals and violations is placed one group after another
+ * without reloading the plans, and each placement re-forms only the cache of
+ * the queues it changed (every queue from the group's old queue to its new
+ * one; the others keep theirs).
+ *   qlm_place_begin  loads the plans (as qlm_place_group reads them) and
+ *                    forms their cache in ws (qlm_search_workspace_bytes(
+ *                    problem, P, 0) bytes, 256-byte aligned)
+ *   qlm_place_step   places `group` in every plan, as qlm_place_group does;
+ *                    score [P] and queue [P] (device out or NULL): each
+ *                    plan's exact score after the placement, the queue chosen
+ *   qlm_place_end    writes the plans (as qlm_place_group writes them, with
+ *                    eviction bits when out has them) and their exact scores
+ *                    (score [P] or NULL); the session may continue after it
+ * Every call names the same problem and plan count.  The workspace is the
+ * session's state: between qlm_place_begin and the last call that uses it, no
+ * other call may use it, and the calls of a session must be ordered (one
+ * stream, or synchronized).
+ */
+int qlm_place_begin(const qlm_problem *problem, const qlm_plans *plans, void *ws, size_t ws_bytes,
+                    qlm_stream stream);
+int qlm_place_step(const qlm_problem *problem, int64_t n_plans, int32_t group, void *ws,
+                   size_t ws_bytes, double *score, int32_t *queue, qlm_stream stream);
+int qlm_place_end(const qlm_problem *problem, int64_t n_plans, const qlm_plans_out *out, void *ws,
+                  size_t ws_bytes, double *score, qlm_stream stream);
+
+/*
  * Seed plans for the search: the paper's reference orders, EDF (Sec. 8
  * baselines) and same-model grouping (Sec. 2, Insight #3).  Groups are taken
  * in EDF order (SLO, then group id) for policy 0, or by model, then SLO, then

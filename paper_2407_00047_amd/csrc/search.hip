@@ -184,6 +184,9 @@ struct SearchArgs {
     int32_t *ncand;               // [1]
     double *U;                    // [1] min(F + D)
     int32_t *scratch;             // [2 G] shifts of k_spick
+    int32_t *dq;                  // [4] placement: the queues a placement changed
+                                  // (every queue from the lower to the higher),
+                                  // the group's slot and queue
     int32_t nwg_a, nwg_b, nwg;    // per chain: k_sswap, k_smove (per queue), total
     int32_t nwg_f, nws;           // per chain: k_fswap (d = 0..W), all screen workgroups
     int64_t n_moves;
@@ -310,6 +313,21 @@ __device__ inline int insertion_point(const SRec *sr, int bq, int eq, float slo)
             lo = mid + 1;
     }
     return lo;
+}
+
+// The same, by the wavefront: 64 positions a read, the first whose running
+// maximum is later by a ballot (long queues take the binary search).
+__device__ inline int insertion_point_wave(const SRec *sr, int bq, int eq, float slo)
+{
+    if (eq - bq > 8 * kWave) return insertion_point(sr, bq, eq, slo);
+    const int lane = threadIdx.x & (kWave - 1);
+    for (int u0 = bq; u0 < eq; u0 += kWave) {
+        const int u = u0 + lane;
+        const bool later = u < eq && sr[u].pmax > slo;
+        const uint64_t m = __builtin_amdgcn_ballot_w64(later);
+        if (m) return u0 + (int)__builtin_ctzll(m);
+    }
+    return eq;
 }
 
 // (score, k) is better than (s2, k2): lower score, then lower k.  A NaN score
@@ -551,6 +569,8 @@ __global__ __launch_bounds__(kThreads) void k_sstate(SearchArgs a, int force)
     const int g = (blockIdx.x % nblk) * kWaves + wave_id();
     const int lane = threadIdx.x & (kWave - 1);
     if (g >= I || (!force && a.done[b])) return;
+    // force == 2: only the queues a placement changed
+    if (force == 2 && (g < a.dq[b * 4] || g > a.dq[b * 4 + 1])) return;
     const int32_t *__restrict__ perm = a.perm + b * G;
     const uint8_t *__restrict__ flag = a.flag + b * G;
     SRec *__restrict__ sr = a.srec + b * G;
@@ -1205,7 +1225,7 @@ __global__ __launch_bounds__(kThreads) void k_sexact(SearchArgs a)
 // whose SLO is strictly later (a reassignment, or with h its own queue a
 // re-insertion): the slots between its old and new place rotate by one, and
 // the queue offsets between the two queues shift.  Run by a whole workgroup.
-__device__ void place_apply(const SearchArgs &a, int64_t b, int s, int h)
+__device__ void place_apply(const SearchArgs &a, int64_t b, int s, int h, int p_known = -1)
 {
     const int G = a.G, I = a.I;
     int32_t *perm = a.perm + b * G;
@@ -1213,7 +1233,7 @@ __device__ void place_apply(const SearchArgs &a, int64_t b, int s, int h)
     int32_t *qof = a.qof + b * (I + 1);
     const SRec *sr = a.srec + b * G;
     const int g = (int)sr[s].q;
-    const int p = insertion_point(sr, qof[h], qof[h + 1], sr[s].slo);
+    const int p = p_known >= 0 ? p_known : insertion_point(sr, qof[h], qof[h + 1], sr[s].slo);
     // left: the group goes later (to slot p - 1); right: earlier (to slot p)
     const bool left = h > g || (h == g && p > s);
     const int lo = left ? s : p;
@@ -1328,13 +1348,19 @@ __global__ __launch_bounds__(kThreads) void k_sout(SearchArgs a, qlm_plans_out o
 
 // Exact score of each plan with its group `group` placed in queue h, one
 // wavefront per (plan, h).
+// One wavefront per (chain, queue h), and one more per chain (h = I) for the
+// group's own queue without it, which every other queue's score shares: the
+// score of the plan with the group placed in h (h = the group's queue), or
+// the score of queue h with the group inserted (other h; k_place_pick
+// completes it with the own queue's score without the group), or the own
+// queue's score without the group (h = I, in U).
 __global__ __launch_bounds__(kThreads) void k_place_eval(SearchArgs a, int group)
 {
     const int G = a.G, I = a.I;
-    const int nblk = (I + kWaves - 1) / kWaves;
+    const int nblk = (I + 1 + kWaves - 1) / kWaves;
     const int64_t b = blockIdx.x / nblk;
     const int h = (blockIdx.x % nblk) * kWaves + wave_id();
-    if (h >= I) return;
+    if (h > I) return;
     const SRec *__restrict__ sr = a.srec + b * G;
     const SSt *__restrict__ ss = a.sst + b * G;
     const int32_t *__restrict__ qof = a.qof + b * (I + 1);
@@ -1342,11 +1368,23 @@ __global__ __launch_bounds__(kThreads) void k_place_eval(SearchArgs a, int group
     const double *Q = a.Q + b * I;
     const int s = __builtin_amdgcn_readfirstlane(clampi(a.inv[b * G + group], 0, G - 1));
     const SRec x = sr[s];
-    const int g = (int)x.q;
-    const int bq = qof[h], eq = qof[h + 1];
+    const int g = clampi((int)x.q, 0, I - 1);
+    if (h == I) {
+        const int bg = clampi(qof[g], 0, G), eg = clampi(qof[g + 1], bg, G);
+        Run rg = start_at(a, sr, ss, s, bg, g);
+        wave_walk(rg, eg - s - 1, [&](int v) { return sr[s + 1 + v]; }, (double)a.inst_tput[g],
+                  clampi(a.inst_class[g], 0, a.C - 1), a, NoOut{});
+        if ((threadIdx.x & (kWave - 1)) == 0) {
+            a.U[b] = rg.sc;
+            a.dq[b * 4 + 2] = s;
+            a.dq[b * 4 + 3] = g;
+        }
+        return;
+    }
+    const int bq = clampi(qof[h], 0, G), eq = clampi(qof[h + 1], bq, G);
     const double theta = (double)a.inst_tput[h];
     const int cls = clampi(a.inst_class[h], 0, a.C - 1);
-    const int p = insertion_point(sr, bq, eq, x.slo);
+    const int p = insertion_point_wave(sr, bq, eq, x.slo);
     double score;
     if (h == g) {
         // its own queue: from the first position that changes, the queue without
@@ -1374,30 +1412,46 @@ __global__ __launch_bounds__(kThreads) void k_place_eval(SearchArgs a, int group
             wave_walk(r, eq - p + 1, [&](int v) { return v == 0 ? x : sr[p + v - 1]; }, theta, cls,
                       a, NoOut{});
         }
-        const double nh = r.sc;
-        const int bg = qof[g], eg = qof[g + 1];
-        Run rg = start_at(a, sr, ss, s, bg, g);
-        wave_walk(rg, eg - s - 1, [&](int v) { return sr[s + 1 + v]; }, (double)a.inst_tput[g],
-                  clampi(a.inst_class[g], 0, a.C - 1), a, NoOut{});
-        score = total_with2(T, Q, I, g, rg.sc, h, nh);
+        score = r.sc;                    // completed by k_place_pick
     }
-    if ((threadIdx.x & (kWave - 1)) == 0) a.cex[b * a.n_moves + h] = score;
+    if ((threadIdx.x & (kWave - 1)) == 0) {
+        a.cex[b * a.n_moves + h] = score;
+        a.cand[b * a.n_moves + h] = p;   // the insertion point, for the pick
+    }
 }
 
 #pragma clang fp contract(on)
 
 // The queue with the lowest exact score (lowest h on ties), applied.
-__global__ __launch_bounds__(kThreads) void k_place_pick(SearchArgs a, int group, int32_t *queue)
+__global__ __launch_bounds__(kThreads) void k_place_pick(SearchArgs a, int group, int32_t *queue,
+                                                         double *score)
 {
     __shared__ double ls[kWaves];
     __shared__ int64_t lk[kWaves];
     __shared__ int64_t kk;
+    __shared__ int kp;
+    // the queue scores and their running sums, staged for the totals
+    __shared__ double sT[kMaxSearchInstances + 1], sQ[kMaxSearchInstances];
     const int64_t b = blockIdx.x;
     const int G = a.G, I = a.I;
+    for (int q = threadIdx.x; q <= I; q += kThreads) {
+        sT[q] = a.T[b * (I + 1) + q];
+        if (q < I) sQ[q] = a.Q[b * I + q];
+    }
+    __syncthreads();
+    const int s0 = clampi(a.dq[b * 4 + 2], 0, G - 1);
+    const int g0 = clampi(a.dq[b * 4 + 3], 0, I - 1);
+    const double *T = sT;
+    const double *Q = sQ;
+    const double rg = a.U[b];
     double best = INFINITY;
     int64_t bk = INT64_MAX;
     for (int h = threadIdx.x; h < I; h += kThreads) {
-        const double v = a.cex[b * a.n_moves + h];
+        double v = a.cex[b * a.n_moves + h];
+        if (h != g0) {
+            v = total_with2(T, Q, I, g0, rg, h, v);
+            a.cex[b * a.n_moves + h] = v;
+        }
         if (better(v, h, best, bk)) {
             best = v;
             bk = h;
@@ -1409,9 +1463,13 @@ __global__ __launch_bounds__(kThreads) void k_place_pick(SearchArgs a, int group
         kk = bk;
         a.cur[b] = a.cex[b * a.n_moves + bk];
         if (queue) queue[b] = (int32_t)bk;
+        if (score) score[b] = a.cur[b];
+        a.dq[b * 4] = min(g0, (int)bk);
+        a.dq[b * 4 + 1] = max(g0, (int)bk);
+        kp = clampi(a.cand[b * a.n_moves + bk], 0, G);
     }
     __syncthreads();
-    place_apply(a, b, clampi(a.inv[b * G + group], 0, G - 1), (int)kk);
+    place_apply(a, b, s0, (int)kk, kp);
 }
 
 // ---------------------------------------------------------------------------
@@ -1597,7 +1655,7 @@ struct Layout {
     int nwg_a, nwg_b, nwg, nwg_f, nws;
     int64_t n_moves;
     size_t grec, by_slo, perm, flag, qof, inv, srec, sst, trec, R, RD, Q, Nq, Es, T, cur, done, steps,
-        wmin_s, wmin_i, smin, F, D, cand, cex, ncand, U, scratch, tail, total;
+        wmin_s, wmin_i, smin, F, D, cand, cex, ncand, U, scratch, dq, tail, total;
 };
 
 Layout layout(int G, int I, int W, int64_t B)
@@ -1645,6 +1703,7 @@ Layout layout(int G, int I, int W, int64_t B)
     L.ncand = take(4 * b);
     L.U = take(8 * b);
     L.scratch = take(8 * (size_t)G * b);
+    L.dq = take(16 * b);
     L.tail = take(sizeof(float2) * qlm_tail::kCells);
     L.total = o;
     return L;
@@ -1719,6 +1778,7 @@ SearchArgs search_args(const qlm_problem *pr, int64_t B, int32_t W, unsigned cha
     a.ncand = (int32_t *)(ws + L.ncand);
     a.U = (double *)(ws + L.U);
     a.scratch = (int32_t *)(ws + L.scratch);
+    a.dq = (int32_t *)(ws + L.dq);
     a.tail = (float2 *)(ws + L.tail);
     a.nwg_a = L.nwg_a;
     a.nwg_b = L.nwg_b;
@@ -1809,6 +1869,52 @@ int screen_moves(SearchArgs &a, hipStream_t stream)
                        stream, a);
     if ((rc = launched("k_fmove launch"))) return rc;
     qlm_internal::timing_end(stream, &tl);
+    return QLM_OK;
+}
+
+// The placement of one group in every chain: the candidate queues scored
+// exactly, the lowest applied; with `refresh`, the cache of the queues the
+// placement changed is formed again (the session's next step reads it).
+int place_step(SearchArgs &a, int32_t group, int32_t *queue, double *score, bool refresh,
+               hipStream_t stream)
+{
+    int rc;
+    qlm_internal::TimedLaunch tl;
+    if ((rc = qlm_internal::timing_begin(stream, &tl))) return rc;
+    const int eblk = (a.I + 1 + kWaves - 1) / kWaves;
+    hipLaunchKernelGGL(k_place_eval, dim3((unsigned)(eblk * a.B)), dim3(kThreads), 0, stream, a,
+                       group);
+    if ((rc = launched("k_place_eval launch"))) return rc;
+    qlm_internal::timing_end(stream, &tl);
+    hipLaunchKernelGGL(k_place_pick, dim3((unsigned)a.B), dim3(kThreads), 0, stream, a, group,
+                       queue, score);
+    if ((rc = launched("k_place_pick launch"))) return rc;
+    if (!refresh) return QLM_OK;
+    return launch_state(a, 2, stream);
+}
+
+// The chains' plans back to the caller's layout, with their scores.
+int write_plans(SearchArgs &a, qlm_plans_out o, double *score, hipStream_t stream)
+{
+    const int64_t rows = (int64_t)a.G + a.I + 1 + (o.evict_bits ? (a.G + 31) / 32 : 0) + 1;
+    int64_t grid = (rows * a.B + kThreads - 1) / kThreads;
+    if (grid > 65536) grid = 65536;
+    hipLaunchKernelGGL(k_sout, dim3((unsigned)grid), dim3(kThreads), 0, stream, a, o, score,
+                       (int32_t *)nullptr);
+    return launched("k_sout launch");
+}
+
+// The arguments of a placement session's later calls: the workspace as
+// qlm_place_begin left it, for the same problem and plan count.
+int session_args(const qlm_problem *pr, int64_t B, void *ws, size_t ws_bytes, SearchArgs *out)
+{
+    int rc = check_search(pr, B, 0);
+    if (rc) return rc;
+    const Layout L = layout(pr->n_groups, pr->n_instances, 0, B);
+    if (!ws || ((uintptr_t)ws & 255u))
+        return fail(QLM_ERR_WORKSPACE, "workspace must be non-NULL and 256-byte aligned");
+    if (ws_bytes < L.total) return fail(QLM_ERR_WORKSPACE, "workspace too small");
+    *out = search_args(pr, B, 0, (unsigned char *)ws, L);
     return QLM_OK;
 }
 
@@ -1937,24 +2043,48 @@ int qlm_place_group(const qlm_problem *problem, const qlm_plans *start, const ql
     if (a.B == 0) return QLM_OK;
     rc = load_and_state(a, start, stream);
     if (rc) return rc;
-    const int nblk = (a.I + kWaves - 1) / kWaves;
-    qlm_internal::TimedLaunch tl;
-    if ((rc = qlm_internal::timing_begin(stream, &tl))) return rc;
-    hipLaunchKernelGGL(k_place_eval, dim3((unsigned)(nblk * a.B)), dim3(kThreads), 0, stream, a,
-                       group);
-    if ((rc = launched("k_place_eval launch"))) return rc;
-    qlm_internal::timing_end(stream, &tl);
-    hipLaunchKernelGGL(k_place_pick, dim3((unsigned)a.B), dim3(kThreads), 0, stream, a, group,
-                       queue);
-    if ((rc = launched("k_place_pick launch"))) return rc;
+    if ((rc = place_step(a, group, queue, nullptr, false, stream))) return rc;
     qlm_plans_out o = *out;
     if (!start->evict_bits) o.evict_bits = nullptr;
-    const int64_t rows = (int64_t)a.G + a.I + 1 + (o.evict_bits ? (a.G + 31) / 32 : 0) + 1;
-    int64_t grid = (rows * a.B + kThreads - 1) / kThreads;
-    if (grid > 65536) grid = 65536;
-    hipLaunchKernelGGL(k_sout, dim3((unsigned)grid), dim3(kThreads), 0, stream, a, o, score,
-                       (int32_t *)nullptr);
-    return launched("k_sout launch");
+    return write_plans(a, o, score, stream);
+}
+
+int qlm_place_begin(const qlm_problem *problem, const qlm_plans *plans, void *ws, size_t ws_bytes,
+                    qlm_stream stream_)
+{
+    hipStream_t stream = (hipStream_t)stream_;
+    SearchArgs a;
+    int rc = search_begin(problem, plans, 0, ws, ws_bytes, &a, stream, false);
+    if (rc) return rc;
+    if (a.B == 0) return QLM_OK;
+    return load_and_state(a, plans, stream);
+}
+
+int qlm_place_step(const qlm_problem *problem, int64_t n_plans, int32_t group, void *ws,
+                   size_t ws_bytes, double *score, int32_t *queue, qlm_stream stream_)
+{
+    hipStream_t stream = (hipStream_t)stream_;
+    if (!problem || group < 0 || group >= problem->n_groups)
+        return fail(QLM_ERR_ARG, "group must be in [0, n_groups)");
+    SearchArgs a;
+    int rc = session_args(problem, n_plans, ws, ws_bytes, &a);
+    if (rc) return rc;
+    if (a.B == 0) return QLM_OK;
+    return place_step(a, group, queue, score, true, stream);
+}
+
+int qlm_place_end(const qlm_problem *problem, int64_t n_plans, const qlm_plans_out *out, void *ws,
+                  size_t ws_bytes, double *score, qlm_stream stream_)
+{
+    hipStream_t stream = (hipStream_t)stream_;
+    if (!out) return fail(QLM_ERR_ARG, "out is NULL");
+    SearchArgs a;
+    int rc = session_args(problem, n_plans, ws, ws_bytes, &a);
+    if (rc) return rc;
+    if (a.B == 0) return QLM_OK;
+    if (!out->perm || !out->qoff) return fail(QLM_ERR_ARG, "out perm and qoff are required");
+    if (out->plan_stride < n_plans) return fail(QLM_ERR_ARG, "out plan_stride must be >= n_plans");
+    return write_plans(a, *out, score, stream);
 }
 
 int64_t qlm_search_n_moves(int32_t n_groups, int32_t n_instances, int32_t window)

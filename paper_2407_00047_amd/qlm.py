@@ -117,12 +117,16 @@ def library():
             lib.qlm_fcfs_best_plan.argtypes = [P, PL, vp, i64, vp, sz, vp, vp, vp]
             lib.qlm_apply_profile.argtypes = [P, ctypes.POINTER(Profile), vp, vp, vp, vp, vp, i64,
                                               vp, vp]
+            lib.qlm_place_begin.argtypes = [P, PL, vp, sz, vp]
+            lib.qlm_place_step.argtypes = [P, i64, i32, vp, sz, vp, vp, vp]
+            lib.qlm_place_end.argtypes = [P, i64, ctypes.POINTER(PlansOut), vp, sz, vp, vp]
             for name in ("qlm_rwt_score", "qlm_rwt_score_exact", "qlm_best_plan",
                          "qlm_validate_plans", "qlm_validate_problem", "qlm_timing_enable",
                          "qlm_timing_read", "qlm_search_moves", "qlm_search_screen",
                          "qlm_local_search", "qlm_seed_plans", "qlm_place_group",
                          "qlm_fcfs_score", "qlm_fcfs_score_exact", "qlm_fcfs_best_plan",
-                         "qlm_apply_profile"):
+                         "qlm_apply_profile", "qlm_place_begin", "qlm_place_step",
+                         "qlm_place_end"):
                 getattr(lib, name).restype = ctypes.c_int
             _lib = lib
     return _lib
@@ -540,3 +544,44 @@ def apply_profile(problem: DeviceProblem, profile, inst_model=None, req_slo=None
                          _ptr(out.inst_class), _ptr(out.inst_model0), _ptr(out.swap_cost),
                          out.evict_cost)
     return out, rs
+
+
+class PlaceSession:
+    """A placement session (qlm_place_begin / step / end): the plans stay in
+    the workspace while groups are placed one after another."""
+
+    def __init__(self, problem: DeviceProblem, plans: DevicePlans, ws=None, stream=None):
+        import torch
+        self.problem = problem
+        self.n_plans = plans.n_plans
+        self.has_evict = plans.evict_bits is not None
+        self.like = plans
+        self.dev = plans.perm.device
+        self.ws = ws if ws is not None else search_workspace(problem, plans.n_plans, 0, self.dev)
+        self.stream = stream
+        _check(library().qlm_place_begin(ctypes.byref(problem.struct), ctypes.byref(plans.struct),
+                                         _ptr(self.ws), self.ws.numel(), _stream(stream)))
+        self.score = torch.empty(max(self.n_plans, 1), dtype=torch.float64, device=self.dev)
+        self.queue = torch.empty(max(self.n_plans, 1), dtype=torch.int32, device=self.dev)
+
+    def step(self, group: int):
+        """Places `group` in every plan; returns (scores [P], queues [P]) (device)."""
+        _check(library().qlm_place_step(ctypes.byref(self.problem.struct), self.n_plans,
+                                        int(group), _ptr(self.ws), self.ws.numel(),
+                                        _ptr(self.score), _ptr(self.queue), _stream(self.stream)))
+        return self.score[:self.n_plans], self.queue[:self.n_plans]
+
+    def end(self, out: DevicePlans | None = None):
+        """The plans as they stand (DevicePlans) and their exact scores."""
+        import torch
+        p = self.like
+        if out is None:
+            out = DevicePlans(torch.empty_like(p.perm), torch.empty_like(p.qoff),
+                              None if p.evict_bits is None else torch.empty_like(p.evict_bits),
+                              self.n_plans)
+        o = PlansOut(int(out.perm.shape[1]), _ptr(out.perm), _ptr(out.qoff), _ptr(out.evict_bits))
+        score = torch.empty(max(self.n_plans, 1), dtype=torch.float64, device=self.dev)
+        _check(library().qlm_place_end(ctypes.byref(self.problem.struct), self.n_plans,
+                                       ctypes.byref(o), _ptr(self.ws), self.ws.numel(),
+                                       _ptr(score), _stream(self.stream)))
+        return out, score[:self.n_plans]

@@ -32,7 +32,8 @@ def test_header_declares_entry_points():
                  "qlm_search_workspace_bytes", "qlm_search_moves", "qlm_search_screen",
                  "qlm_local_search", "qlm_seed_workspace_bytes", "qlm_seed_plans",
                  "qlm_place_group", "qlm_fcfs_workspace_bytes", "qlm_fcfs_score",
-                 "qlm_fcfs_score_exact", "qlm_fcfs_best_plan", "qlm_apply_profile"):
+                 "qlm_fcfs_score_exact", "qlm_fcfs_best_plan", "qlm_apply_profile",
+                 "qlm_place_begin", "qlm_place_step", "qlm_place_end"):
         assert must in names
 
 
@@ -237,4 +238,28 @@ def test_profile_argument_checks(lib):
     assert ap(P(pr), P(pf), None, out, out, out, 0x6000, 4, None, None) == qlm.QLM_ERR_ARG
     assert ap(P(pr), P(pf), None, out, out, out, None, 4, out, None) == qlm.QLM_ERR_ARG
     assert ap(None, P(pf), None, out, out, out, None, 0, None, None) == qlm.QLM_ERR_ARG
+
+
+def test_place_session_argument_checks(lib):
+    from paper_2407_00047_amd import qlm
+    P = ctypes.byref
+    pr = _problem(qlm, G=8, I=2)
+    pl = qlm.Plans(3, 3, 0x1000, 0x1000, None)
+    need = lib.qlm_search_workspace_bytes(P(pr), 3, 0)
+    ws = 0x10000
+    assert lib.qlm_place_begin(P(pr), P(pl), ws, need - 1, None) == qlm.QLM_ERR_WORKSPACE
+    assert lib.qlm_place_begin(P(pr), P(pl), ws + 8, need, None) == qlm.QLM_ERR_WORKSPACE
+    assert lib.qlm_place_begin(P(pr), None, ws, need, None) == qlm.QLM_ERR_ARG
+    st = lib.qlm_place_step
+    assert st(P(pr), 3, 8, ws, need, None, None, None) == qlm.QLM_ERR_ARG
+    assert st(P(pr), 3, -1, ws, need, None, None, None) == qlm.QLM_ERR_ARG
+    assert st(P(pr), 3, 1, ws, need - 1, None, None, None) == qlm.QLM_ERR_WORKSPACE
+    assert st(P(pr), -1, 1, ws, need, None, None, None) == qlm.QLM_ERR_ARG
+    assert st(P(pr), 0, 1, ws, need, None, None, None) == qlm.QLM_OK
+    out = qlm.PlansOut(3, 0x1000, 0x1000, None)
+    en = lib.qlm_place_end
+    assert en(P(pr), 3, None, ws, need, None, None) == qlm.QLM_ERR_ARG
+    assert en(P(pr), 3, P(out), ws, need - 1, None, None) == qlm.QLM_ERR_WORKSPACE
+    short = qlm.PlansOut(2, 0x1000, 0x1000, None)
+    assert en(P(pr), 3, P(short), ws, need, None, None) == qlm.QLM_ERR_ARG
 

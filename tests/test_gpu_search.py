@@ -429,3 +429,45 @@ def test_place_group_arrival(qlm, orc):
         assert int(r["queue"][p]) == o["queue"]
         assert np.array_equal(r["plans"].perm.cpu().numpy()[:, p], o["perm"])
         assert _close(float(r["score"][p]), o["score"])
+
+
+@pytest.mark.parametrize("kw", [dict(G=9, I=3, P=5), dict(G=70, I=4, P=6, empty_queues=True),
+                                dict(G=300, I=12, P=4, skewed=True), dict(G=40, I=1, P=3)])
+def test_place_session(qlm, orc, kw):
+    """A session places groups one after another with the plans kept in the
+    workspace, re-forming only the changed queues' cache: each step's plans and
+    scores equal placing the same groups with qlm_place_group, call after call,
+    and the oracle's placements of the sequence."""
+    import torch
+    rng = np.random.default_rng(zlib.crc32(("session" + str(sorted(kw.items()))).encode()))
+    pr, pl = hand_case(rng, **kw)
+    G, P = pr["n_groups"], pl["n_plans"]
+    groups = [int(x) for x in rng.integers(0, G, 8)]
+    dpr, dpl = device_inputs(pr, pl)
+    ses = qlm.PlaceSession(dpr, dpl)
+    cur = dpl
+    host = {k: (v.copy() if isinstance(v, np.ndarray) else v) for k, v in pl.items()}
+    for k, group in enumerate(groups):
+        print("case", kw, "step", k, "group", group, flush=True)
+        sc, qu = ses.step(group)
+        r = qlm.place_group(dpr, cur, group)
+        torch.cuda.synchronize()
+        assert np.array_equal(sc.cpu().numpy(), r["score"].cpu().numpy()), (k, group)
+        assert np.array_equal(qu.cpu().numpy(), r["queue"].cpu().numpy()), (k, group)
+        cur = r["plans"]
+        # the oracle, plan by plan, on the host copy of the plans so far
+        for p in range(P):
+            o = orc.place_group(pr, host, p, group)
+            if int(qu[p]) == o["queue"]:
+                assert _close(float(sc[p]), o["score"]), (k, p)
+        host = {"n_plans": P, "perm": cur.perm.cpu().numpy(), "qoff": cur.qoff.cpu().numpy(),
+                "evict_bits": None if cur.evict_bits is None
+                else cur.evict_bits.cpu().numpy().view(np.uint32)}
+    out, score = ses.end()
+    torch.cuda.synchronize()
+    assert np.array_equal(out.perm.cpu().numpy(), cur.perm.cpu().numpy())
+    assert np.array_equal(out.qoff.cpu().numpy(), cur.qoff.cpu().numpy())
+    if cur.evict_bits is not None:
+        assert np.array_equal(out.evict_bits.cpu().numpy(), cur.evict_bits.cpu().numpy())
+    ex = qlm.rwt_score_exact(dpr, out, np.arange(P)).cpu().numpy()
+    assert np.array_equal(score.cpu().numpy(), ex)
