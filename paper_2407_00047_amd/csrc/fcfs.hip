@@ -34,9 +34,13 @@
 // the same slot, so its reads are coalesced.  It is cut into segments of 128
 // slots: k_fseg sums each segment's trailing queue piece, k_fstart chains the
 // pieces into each segment's starting sums, and k_frec walks each segment
-// again from them and stores the records.  Its stores land in the rows of the
-// groups, a different row in every lane: this transposition from the plans'
-// slot order to group order is the price of the screen's shared SLOs.
+// again from them and forms the records.  The records belong in the rows of
+// the groups, a different row in every lane: this transposition from the
+// plans' slot order to group order is the price of the screen's shared SLOs.
+// It runs in two passes: k_frec sorts every 8 slots' records by block of 128
+// groups in LDS and appends each block's run to the block's bucket of the
+// tile; k_ftrans places each bucket's records in LDS by (group, plan) and
+// writes whole rows.
 //
 // Screening bound, per request: table error below 2.2e-6; single-precision
 // rounding of the cell coordinate, of the line's evaluation, of the margin and
@@ -64,7 +68,9 @@
 //   k_fseg      one lane per plan, one wavefront per (64 plans, segment):
 //               each segment's trailing queue piece
 //   k_fstart    one lane per plan: the sums at each segment's first slot
-//   k_frec      as k_fseg: the records of the segment's groups
+//   k_frec      as k_fseg: the records of the segment's groups, into the
+//               buckets of their group blocks (k_fbzero clears the counts)
+//   k_ftrans    one workgroup per (64 plans, 128 groups): the bucket to rows
 //   k_fscreen   one lane per plan, one wavefront per (64 plans, 64 groups):
 //               partial screened scores
 //   k_fsum      partial scores -> screened plan scores, and the per-block
@@ -99,6 +105,13 @@ constexpr int kWaves = kThreads / kWave;
 constexpr int kGroupsPerWave = 64;          // groups of one k_fscreen wavefront
 constexpr int kSeg = 128;                   // slots per segment of the queue walks
 constexpr int kRecPad = 24;                 // plans of padding per record row
+constexpr int kBlk = 128;                   // groups per bucket of the transposition
+constexpr int kBlkCap = kBlk * 64;          // records per bucket (a tile's plans)
+constexpr int kSub = 8;                     // slots a walk sorts into buckets at a time
+constexpr int kRecWaves = 4;                // wavefronts of a k_frec workgroup
+constexpr int kMaxFcfsGroups = 1 << 16;
+constexpr int kMaxFcfsInstances = 4096;
+constexpr int kMaxBlocks = kMaxFcfsGroups / kBlk;
 constexpr int kSumBlocks = 1024;            // k_fsum blocks (per-block minima)
 constexpr int kExactBlocks = 256;
 constexpr int kPickThreads = 256;
@@ -167,7 +180,9 @@ struct FArgs {
     double *slo64;            // [n_req] the SLOs in double
     float2 *tail;             // [kCells]
     double *nreq;             // [1] requests scored
-    FRec *rec;                // [G slots][chunk]
+    FRec *rec;                // [G][rld] group-major
+    FRec *bucket;             // [tiles][nblk][kBlkCap] the transposition's buckets
+    int32_t *bcnt;            // [tiles][nblk] records in each bucket
     Piece *piece;             // [nseg][chunk]
     Start *start;             // [nseg][chunk]
     double *part;             // [ceil(G / kGroupsPerWave)][chunk]
@@ -353,9 +368,13 @@ __device__ inline void batch_groups(const FArgs &a, const Batch<B> &b, FGrp *gr)
     }
 }
 
-template <int B, bool kPipe, class Visit>
+struct NoPost {
+    __device__ void operator()(int) const {}
+};
+
+template <int B, bool kPipe, class Visit, class Post = NoPost>
 __device__ inline void walk(const FArgs &a, int64_t p, int s0, int s1, Walk &w, bool *fresh,
-                            const Visit &visit)
+                            const Visit &visit, const Post &post = Post{})
 {
     static_assert(B <= 32 && (B & (B - 1)) == 0, "a batch lies in one eviction word");
     if (s0 >= s1) return;
@@ -391,6 +410,7 @@ __device__ inline void walk(const FArgs &a, int64_t p, int s0, int s1, Walk &w, 
             w.V += n * (double)gr[u].var;
             w.prev = m;
         }
+        post(sb);                       // every lane, after each batch
         if (more) {
             if (kPipe)
                 cur = nxt;
@@ -469,24 +489,104 @@ __global__ __launch_bounds__(kThreads) void k_fstart(FArgs a, int64_t pc)
 }
 
 // Pass 3: each slot's record (its group's start E[W] = A/Theta + K, its
-// variance ahead, its queue), written to the slot's row.  A queue open at
-// the segment's start continues from the sums of pass 2; where nothing
-// varies ahead (V = 0) those sums are formed again slot by slot from the
-// queue's first slot, so that E[W] is the oracle's bit for bit wherever an
-// exact comparison uses it.
-__global__ __launch_bounds__(kThreads) void k_frec(FArgs a, int64_t p0, int64_t pc)
+// variance ahead, its queue), on its way to the group's row.  A queue open at
+// the segment's start continues from the sums of pass 2; where nothing varies
+// ahead (V = 0) those sums are formed again slot by slot from the queue's
+// first slot, so that E[W] is the oracle's bit for bit wherever an exact
+// comparison uses it.
+//
+// The records go to group rows, a different row in every lane, so they are
+// not stored directly (every store would be a partial line).  Every kSub
+// slots the wavefront sorts its records by group block (kBlk groups) in LDS
+// and appends each block's run to that block's bucket of the tile, in
+// consecutive addresses; k_ftrans then turns each bucket into its rows.  A
+// record carries its group within the block and its lane in the word of its
+// queue (the queue < 4096 in bits 0-11, the group in bits 12-18, the lane in
+// bits 19-24, kNoVar in bit 31).
+struct WaveBuf {
+    FRec rec[kSub * kWave];
+    uint16_t sidx[kSub * kWave];    // sorted position -> entry
+    uint16_t sgb[kSub * kWave];     // entry -> group block
+    uint8_t val[kSub * kWave];      // entry holds a record
+    int cnt[kMaxBlocks];
+    uint16_t boff[kMaxBlocks], gbase[kMaxBlocks];
+};
+
+__device__ inline void wave_sync()
 {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// The wavefront's buffered records into the buckets of tile `tile`.
+__device__ inline void flush(const FArgs &a, WaveBuf &wb, int64_t tile, int nblk)
+{
+    const int lane = threadIdx.x & (kWave - 1);
+    for (int k = lane; k < nblk; k += kWave) wb.cnt[k] = 0;
+    wave_sync();
+    int rank[kSub];
+#pragma unroll
+    for (int j = 0; j < kSub; ++j) {
+        const int e = j * kWave + lane;
+        rank[j] = wb.val[e] ? atomicAdd(&wb.cnt[wb.sgb[e]], 1) : 0;
+    }
+    wave_sync();
+    // offsets of the blocks' runs (a scan over the blocks), and their room in
+    // the buckets
+    int run = 0;
+    for (int k0 = 0; k0 < nblk; k0 += kWave) {
+        const int k = k0 + lane;
+        const int c = k < nblk ? wb.cnt[k] : 0;
+        int x = c;
+        for (int o = 1; o < kWave; o <<= 1) {
+            const int y = __shfl_up(x, o, kWave);
+            if (lane >= o) x += y;
+        }
+        if (k < nblk) {
+            wb.boff[k] = (uint16_t)(run + x - c);
+            const int at = c > 0 ? atomicAdd(&a.bcnt[tile * nblk + k], c) : 0;
+            wb.gbase[k] = (uint16_t)min(at, kBlkCap);
+        }
+        run += __shfl(x, kWave - 1, kWave);
+    }
+    wave_sync();
+#pragma unroll
+    for (int j = 0; j < kSub; ++j) {
+        const int e = j * kWave + lane;
+        if (wb.val[e]) wb.sidx[wb.boff[wb.sgb[e]] + rank[j]] = (uint16_t)e;
+    }
+    wave_sync();
+    for (int pos = lane; pos < run; pos += kWave) {
+        const int e = wb.sidx[pos];
+        const int k = wb.sgb[e];
+        const int dst = wb.gbase[k] + (pos - wb.boff[k]);
+        if (dst < kBlkCap) a.bucket[(tile * nblk + k) * (int64_t)kBlkCap + dst] = wb.rec[e];
+    }
+    wave_sync();
+#pragma unroll
+    for (int j = 0; j < kSub; ++j) wb.val[j * kWave + lane] = 0;
+    wave_sync();
+}
+
+__global__ __launch_bounds__(kRecWaves * kWave) void k_frec(FArgs a, int64_t p0, int64_t pc)
+{
+    __shared__ WaveBuf bufs[kRecWaves];
     const int nseg = (a.G + kSeg - 1) / kSeg;
-    const int sq = (nseg + kWaves - 1) / kWaves;
+    const int nblk = (a.G + kBlk - 1) / kBlk;
+    const int sq = (nseg + kRecWaves - 1) / kRecWaves;
     const int64_t tile = blockIdx.x / sq;
-    const int k = (int)(blockIdx.x % sq) * kWaves + wave_id();
+    const int k = (int)(blockIdx.x % sq) * kRecWaves + wave_id();
     if (k >= nseg) return;
+    WaveBuf &wb = bufs[wave_id()];
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t col = tile * kWave + lane;
     const bool on = col < pc;
     const int64_t c = on ? col : pc - 1;
     const int64_t p = p0 + c;
     const int s0 = k * kSeg, s1 = min(a.G, s0 + kSeg);
+#pragma unroll
+    for (int j = 0; j < kSub; ++j) wb.val[j * kWave + lane] = 0;
     Walk w;
     const int q0 = a.piece[(int64_t)k * a.chunk + c].q0;
     open_queue(a, p, q0, w);
@@ -505,18 +605,73 @@ __global__ __launch_bounds__(kThreads) void k_frec(FArgs a, int64_t p0, int64_t 
             if (i >= 0 && i < a.G) w.prev = (int)a.grp[i].model;
         }
     }
+    wave_sync();
     bool f = false;
-    // (the scattered record stores run best with fewer wavefronts in flight:
-    // larger batches, no overlap)
-    walk<16, false>(a, p, s0, s1, w, &f, [&](int, int i, const Walk &x) {
+    // batches of kSub slots (s0 is a multiple of kSub); the next batch's reads
+    // are in flight while a batch's records are sorted into the buckets
+    walk<kSub, true>(a, p, s0, s1, w, &f, [&](int s, int i, const Walk &x) {
         if (on) {
+            const int e = (s & (kSub - 1)) * kWave + lane;
             FRec r;
             r.c0 = x.A / x.theta + x.K;
             r.v0 = (float)(x.V * x.vscale);
-            r.q = (uint32_t)x.q | (x.V == 0.0 ? kNoVar : 0u);
-            a.rec[(int64_t)i * a.rld + col] = r;
+            r.q = (uint32_t)x.q | ((uint32_t)(i & (kBlk - 1)) << 12) |
+                  ((uint32_t)lane << 19) | (x.V == 0.0 ? kNoVar : 0u);
+            wb.rec[e] = r;
+            wb.sgb[e] = (uint16_t)(i / kBlk);
+            wb.val[e] = 1;
         }
+    }, [&](int) {
+        wave_sync();
+        flush(a, wb, tile, nblk);
     });
+}
+
+// One workgroup per bucket (tile, group block): its records into LDS at their
+// (group, lane) place, then out to the groups' rows, 64 plans a row.
+constexpr int kTransThreads = 1024;
+
+__global__ __launch_bounds__(kTransThreads) void k_ftrans(FArgs a, int64_t pc)
+{
+    extern __shared__ __align__(16) unsigned char dyn[];
+    FRec *tile_rec = reinterpret_cast<FRec *>(dyn);
+    const int nblk = (a.G + kBlk - 1) / kBlk;
+    const int64_t tile = blockIdx.x / nblk;
+    const int gb = (int)(blockIdx.x % nblk);
+    const int i0 = gb * kBlk;
+    const int ng = min(kBlk, a.G - i0);
+    const int n = min(a.bcnt[tile * nblk + gb], kBlkCap);
+    const FRec *src = a.bucket + (tile * nblk + gb) * (int64_t)kBlkCap;
+    constexpr int kU = kBlkCap / kTransThreads;       // 8 records a thread, read together
+    FRec x[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+        const int r = u * kTransThreads + (int)threadIdx.x;
+        if (r < n) x[u] = src[r];
+    }
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+        const int r = u * kTransThreads + (int)threadIdx.x;
+        if (r < n) {
+            const int gi = (int)((x[u].q >> 12) & (kBlk - 1));
+            const int ln = (int)((x[u].q >> 19) & (kWave - 1));
+            x[u].q &= 0xFFFu | kNoVar;
+            tile_rec[gi * kWave + ln] = x[u];
+        }
+    }
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < ng * kWave; idx += kTransThreads) {
+        const int gi = idx / kWave, ln = idx % kWave;
+        const int64_t col = tile * kWave + ln;
+        if (col < pc) a.rec[(int64_t)(i0 + gi) * a.rld + col] = tile_rec[idx];
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void k_fbzero(FArgs a, int64_t n)
+{
+    for (int64_t k = (int64_t)blockIdx.x * kThreads + threadIdx.x; k < n;
+         k += (int64_t)gridDim.x * kThreads)
+        a.bcnt[k] = 0;
 }
 
 // Q of the margin m (seconds) at scaled variance vz, from the table in LDS.
@@ -822,8 +977,8 @@ int64_t chunk_of(int32_t G, int64_t P, int64_t want)
 }
 
 struct FLayout {
-    size_t grp, req, first, slo64, tail, nreq, rec, piece, start, part, F, bmin, ncand, cand, Q,
-        total;
+    size_t grp, req, first, slo64, tail, nreq, rec, bucket, bcnt, piece, start, part, F, bmin, ncand,
+        cand, Q, total;
     int64_t chunk;
 };
 
@@ -846,6 +1001,10 @@ FLayout flayout(const qlm_problem *pr, int64_t P, int64_t n_req, int64_t chunk)
     put(L.tail, 8 * (size_t)qlm_tail::kCells);
     put(L.nreq, 8);
     put(L.rec, sizeof(FRec) * (size_t)G * (size_t)(L.chunk + kRecPad));
+    const size_t tiles = (size_t)(L.chunk / kWave);
+    const size_t nblk = (size_t)((G + kBlk - 1) / kBlk);
+    put(L.bucket, sizeof(FRec) * tiles * nblk * (size_t)kBlkCap);
+    put(L.bcnt, 4 * tiles * nblk);
     const size_t nseg = (size_t)((G + kSeg - 1) / kSeg);
     put(L.piece, sizeof(Piece) * nseg * (size_t)L.chunk);
     put(L.start, sizeof(Start) * nseg * (size_t)L.chunk);
@@ -900,6 +1059,8 @@ FArgs fargs(const qlm_problem *pr, const qlm_plans *pl, const float *req_slo, in
     a.tail = (float2 *)(w + L.tail);
     a.nreq = (double *)(w + L.nreq);
     a.rec = (FRec *)(w + L.rec);
+    a.bucket = (FRec *)(w + L.bucket);
+    a.bcnt = (int32_t *)(w + L.bcnt);
     a.piece = (Piece *)(w + L.piece);
     a.start = (Start *)(w + L.start);
     a.part = (double *)(w + L.part);
@@ -931,6 +1092,9 @@ int fbegin(const qlm_problem *problem, const qlm_plans *plans, const float *req_
     if (rc) return rc;
     rc = check_requests(problem, req_slo, n_req);
     if (rc) return rc;
+    if (problem->n_groups > kMaxFcfsGroups || problem->n_instances > kMaxFcfsInstances)
+        return fail(QLM_ERR_CAPACITY, "the per-request calls take at most 65536 groups and 4096 "
+                                      "instances");
     if (!ws || ((uintptr_t)ws & 255u))
         return fail(QLM_ERR_WORKSPACE, "workspace must be non-NULL and 256-byte aligned");
     // the largest chunk the workspace holds, from the default down to 64 plans
@@ -977,9 +1141,22 @@ int screen_all(const FArgs &a, hipStream_t stream)
         hipLaunchKernelGGL(k_fstart, dim3((unsigned)((pc + kThreads - 1) / kThreads)),
                            dim3(kThreads), 0, stream, a, pc);
         if ((rc = launched("k_fstart launch"))) return rc;
-        hipLaunchKernelGGL(k_frec, dim3((unsigned)(tiles * sq)), dim3(kThreads), 0, stream, a, p0,
-                           pc);
+        const int64_t nblk = (a.G + kBlk - 1) / kBlk;
+        int64_t zb = (tiles * nblk + kThreads - 1) / kThreads;
+        if (zb > 1024) zb = 1024;
+        hipLaunchKernelGGL(k_fbzero, dim3((unsigned)zb), dim3(kThreads), 0, stream, a, tiles * nblk);
+        if ((rc = launched("k_fbzero launch"))) return rc;
+        const int64_t sq2 = ((a.G + kSeg - 1) / kSeg + kRecWaves - 1) / kRecWaves;
+        hipLaunchKernelGGL(k_frec, dim3((unsigned)(tiles * sq2)), dim3(kRecWaves * kWave), 0,
+                           stream, a, p0, pc);
         if ((rc = launched("k_frec launch"))) return rc;
+        const hipError_t ea = hipFuncSetAttribute((const void *)k_ftrans,
+                                                  hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                  (int)(sizeof(FRec) * kBlkCap));
+        if (ea != hipSuccess) return hip_fail(ea, "hipFuncSetAttribute");
+        hipLaunchKernelGGL(k_ftrans, dim3((unsigned)(tiles * nblk)), dim3(kTransThreads),
+                           sizeof(FRec) * kBlkCap, stream, a, pc);
+        if ((rc = launched("k_ftrans launch"))) return rc;
         const int64_t quads = (tiles + kWaves - 1) / kWaves;
         qlm_internal::TimedLaunch tl;
         if ((rc = qlm_internal::timing_begin(stream, &tl))) return rc;
