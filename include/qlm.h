@@ -134,16 +134,24 @@ int qlm_rwt_score_exact(const qlm_problem *problem, const qlm_plans *plans,
                         const int64_t *plan_index, int64_t n, double *score,
                         qlm_stream stream);
 
-/* Bytes of device workspace qlm_best_plan needs for n_plans plans (>= 256). */
+/*
+ * Bytes of device workspace qlm_best_plan needs for n_plans plans: about 16
+ * bytes per plan, plus 8 bytes per instance for each candidate whose queue
+ * scores it holds (min(n_plans, max(256, 4Mi / n_instances)) candidates, 32
+ * MiB at most).  0 when problem is NULL or has no instances.
+ */
 size_t qlm_best_plan_workspace_bytes(const qlm_problem *problem, int64_t n_plans);
 
 /*
  * The plan the scheduler should pick (Sec. 7, objective; the scoring above in
  * place of the LP): argmin over p of the exact score, the lowest index on ties.
  * Screens every plan with the qlm_rwt_score arithmetic, then re-scores exactly
- * every plan that can still be the minimum given the screening error bound.
+ * every plan that can still be the minimum given the screening error bound
+ * (the candidates): one wavefront per (candidate, queue) while the workspace
+ * holds the candidates' queue scores, else one workgroup per candidate.
  *   ws          device workspace of at least qlm_best_plan_workspace_bytes,
- *               256-byte aligned; its contents are scratch
+ *               256-byte aligned; its contents are scratch.  A larger one
+ *               holds the queue scores of more candidates.
  *   best_index  [1] device out: index of the best plan (-1 when P = 0)
  *   best_score  [1] device out: its exact score (+inf when P = 0)
  */

@@ -17,11 +17,15 @@
 //             top of a double sum; the violation probability is read from a
 //             linear-cell table of the normal tail in LDS.  LDS reads are
 //             software-pipelined one slot ahead of their use.
-//   k_refine  exact double-precision re-score (same definition as the oracle,
-//             summed per queue then over queues) of every plan whose screened
-//             score is within the screening error bound of the minimum.
-//   k_final   lowest exact score, lowest index on ties.
-//   k_exact   exact re-score of a list of plans (qlm_rwt_score_exact).
+//   k_gselect the plans whose screened score is within the screening error
+//             bound of the minimum (the candidates of qlm_best_plan)
+//   k_gexact  exact double-precision re-score of the candidates (same
+//             definition as the oracle, summed per queue then over queues): one
+//             wavefront per (candidate, queue), the running sums rippling from
+//             lane to lane in position order
+//   k_gpick   lowest exact score, lowest index on ties.
+//   k_exact   exact re-score of a list of plans (qlm_rwt_score_exact), one
+//             workgroup per plan, its wavefronts over the plan's queues.
 //   k_validate_plans / k_validate_problem   structural checks.
 #include <hip/hip_runtime.h>
 
@@ -37,18 +41,31 @@
 
 #include "internal.h"
 #include "qlm.h"
+#include "ripple.h"
 #include "tail.h"
 
 namespace {
 
+using qlm_ripple::from_left;
+using qlm_ripple::from_left0;
+using qlm_ripple::lane_value;
+using qlm_ripple::wave_id;
+
 constexpr int kWave = 64;
 constexpr int kScoreThreads = 1024;     // 16 wavefronts per workgroup, 4 per SIMD
-constexpr int kRefineThreads = 256;
+constexpr int kExactThreads = 1024;     // qlm_rwt_score_exact: 16 wavefronts per plan
+constexpr int kExactPass = 1024;        // queue sums a workgroup holds in LDS at once
+constexpr int kSelThreads = 256;
+constexpr int kSelBlocks = 1024;
+constexpr int kGexThreads = 256;
+constexpr int kGexBlocks = 512;
+// Per-(candidate, queue) sums of qlm_best_plan's workspace by default (the
+// candidates beyond them are re-scored a workgroup each).
+constexpr size_t kCandSumBytes = size_t(32) << 20;
 constexpr int kMaxScoreBlocks = 4096;
 // Row offsets of a block's prefetch (up to 67 rows of 4 * plan_stride bytes)
 // are 32-bit register operands.
 constexpr int64_t kMaxPlanStride = 1 << 22;
-constexpr int kRefineBlocks = 1024;
 // Request counts share the 32-bit record word with the model's cost-table
 // column (bits 3..10), so they are 21-bit.
 constexpr uint32_t kCountMask = (1u << 21) - 1u;
@@ -93,6 +110,7 @@ struct ScoreArgs {
     float *d_mean, *d_sd, *d_prob;
     double *wg_min;           // best_plan: per-workgroup minimum score, or null
     double *wg_nsum;          // best_plan: total requests (written by block 0)
+    int32_t *ncand;           // best_plan: candidate count, zeroed by block 0
 };
 
 __device__ inline int clampi(int v, int lo, int hi) { return v < lo ? lo : (v > hi ? hi : v); }
@@ -224,6 +242,7 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
     stage_tail(s_tail);
     double *red = lds_ptr<double>(L.red);
     if (a.wg_nsum && blockIdx.x == 0) {
+        if (threadIdx.x == 0 && a.ncand) *a.ncand = 0;
         double t = 0.0;
         for (int i = threadIdx.x; i < a.G; i += blockDim.x)
             t += (double)(uint32_t)clampi(a.grp_count[i], 0, (int)kCountMask);
@@ -752,207 +771,149 @@ struct ExactArgs {
 };
 
 #pragma clang fp contract(off)
-__device__ double exact_queue(const ExactArgs &a, int64_t p, int g)
+// Exact score of queue g of plan p by one wavefront.  Each round takes the
+// next 64 positions, one per lane; the running sums (tokens n mu and variance
+// n var ahead, costs K) ripple from lane to lane in position order, so every
+// lane holds the same sums a serial walk forms at its position.  Each lane
+// then forms its position's E[W], SD and term n P, and the terms ripple into
+// the queue's sum the same way, one round later (in the steps of the next
+// round's running sums).  A ripple always takes 63 steps: lanes beyond the
+// queue's end hold zeros, which leave every sum unchanged, and the code has
+// no branch between steps.  Loads run ahead: the next round's group fields
+// and swap costs, and the group ids of the round after.  Returns the queue's
+// score in every lane.  Group ids are clamped to [0, G), offsets to [0, G]
+// (malformed plans never read out of bounds).
+struct RoundIn {
+    int m;                    // model (0 where the lane holds no position)
+    uint32_t n;               // requests (0 where none)
+    float mu, var, slo;
+    uint32_t ev;              // eviction word of the lane's position
+};
+
+__device__ double wave_queue_exact(const ExactArgs &a, int64_t p, int g)
 {
-    int32_t b = a.qoff[(int64_t)g * a.ld + p];
-    int32_t e = a.qoff[(int64_t)(g + 1) * a.ld + p];
-    b = clampi(b, 0, a.G);
-    e = clampi(e, b, a.G);
+    const int lane = threadIdx.x & (kWave - 1);
+    const int G = a.G;
+    const int64_t ld = a.ld;
+    const int bq = clampi(a.qoff[(int64_t)g * ld + p], 0, G);
+    const int eq = clampi(a.qoff[(int64_t)(g + 1) * ld + p], bq, G);
     const double theta = (double)a.inst_tput[g];
-    const int cls = clampi(a.inst_class[g], 0, a.C - 1);
-    int m_prev = a.inst_model0 ? clampi(a.inst_model0[g], -1, a.M - 1) : -1;
-    double A = 0.0, V = 0.0, K = 0.0, sc = 0.0;
-    for (int s = b; s < e; ++s) {
-        const int i = (int)min((uint32_t)a.perm[(int64_t)s * a.ld + p], (uint32_t)(a.G - 1));
-        const int m = clampi(a.grp_model[i], 0, a.M - 1);
-        const double n = (double)(uint32_t)clampi(a.grp_count[i], 0, (int)kCountMask);
-        const double mu = (double)a.grp_mu[i];
-        const double var = (double)a.grp_var[i];
-        const double slo = (double)a.grp_slo[i];
-        if (m_prev >= 0 && m_prev != m && a.swap_cost)
-            K += (double)a.swap_cost[((int64_t)cls * a.M + m_prev) * a.M + m];
-        if (a.evict && ((a.evict[(int64_t)(s >> 5) * a.ld + p] >> (s & 31)) & 1u))
-            K += (double)a.evict_cost;
+    const int64_t swap_row = (int64_t)clampi(a.inst_class[g], 0, a.C - 1) * a.M;
+    int prev = a.inst_model0 ? clampi(a.inst_model0[g], -1, a.M - 1) : -1;
+    const double ecost = (double)a.evict_cost;
+    // group id at position v0 + lane, -1 beyond the queue
+    auto ids = [&](int v0) -> int {
+        const int s = v0 + lane;
+        return s < eq ? (int)min((uint32_t)a.perm[(int64_t)s * ld + p], (uint32_t)(G - 1)) : -1;
+    };
+    auto fields = [&](int i, int v0) -> RoundIn {
+        RoundIn f{0, 0u, 0.f, 0.f, 0.f, 0u};
+        if (i >= 0) {
+            f.m = clampi(a.grp_model[i], 0, a.M - 1);
+            f.n = (uint32_t)clampi(a.grp_count[i], 0, (int)kCountMask);
+            f.mu = a.grp_mu[i];
+            f.var = a.grp_var[i];
+            f.slo = a.grp_slo[i];
+            if (a.evict) f.ev = a.evict[(int64_t)((v0 + lane) >> 5) * ld + p];
+        }
+        return f;
+    };
+    // swap cost into this lane's position from the one before (prev for lane 0)
+    auto swap_in = [&](const RoundIn &f, bool on) -> float {
+        int pm = __shfl_up(f.m, 1, kWave);
+        if (lane == 0) pm = prev;
+        return (on && pm >= 0 && pm != f.m && a.swap_cost)
+                   ? a.swap_cost[(swap_row + pm) * a.M + f.m] : 0.f;
+    };
+    int i0 = ids(bq);
+    RoundIn f = fields(i0, bq);
+    int i2 = ids(bq + kWave);
+    float sw = swap_in(f, i0 >= 0);
+    double rA = 0.0, rV = 0.0, rK = 0.0, rC = 0.0;
+    double tprev = 0.0;       // the previous round's terms (none before the first)
+    for (int v0 = bq; v0 < eq; v0 += kWave) {
+        const int cnt = min(kWave, eq - v0);
+        const bool on = lane < cnt;
+        // next round's fields, the ids of the round after
+        const int i1 = i2;
+        const RoundIn f1 = fields(i1, v0 + kWave);
+        i2 = ids(v0 + 2 * kWave);
+        const double n = (double)f.n;
+        const double xa = n * (double)f.mu;
+        const double xb = n * (double)f.var;
+        const double c1 = (double)sw;
+        const double c2 = (on && ((f.ev >> ((v0 + lane) & 31)) & 1u)) ? ecost : 0.0;
+        const double la = from_left0(xa), lb = from_left0(xb);
+        const double l1 = from_left0(c1), l2 = from_left0(c2);
+        const double lt = from_left0(tprev);
+        double A = rA, V = rV, K = rK, C = rC;
+#pragma unroll
+        for (int j = 1; j < kWave; ++j) {
+            A = from_left(A) + la;
+            V = from_left(V) + lb;
+            K = (from_left(K) + l1) + l2;
+            C = from_left(C) + lt;
+        }
+        rC = lane_value(C, kWave - 1) + lane_value(tprev, kWave - 1);
+        K = K + c1;               // this position's swap, then its eviction
+        K = K + c2;
         const double EW = A / theta + K;
         const double SD = sqrt(V) / theta;
+        const double slo = (double)f.slo;
         double P;
         if (SD > 0.0)
             P = 0.5 * erfc((slo - EW) / (SD * 1.4142135623730951));
         else
             P = (EW > slo) ? 1.0 : 0.0;
-        sc += n * P;
-        A += n * mu;
-        V += n * var;
-        m_prev = m;
+        tprev = on ? n * P : 0.0;
+        rA = lane_value(A, kWave - 1) + lane_value(xa, kWave - 1);
+        rV = lane_value(V, kWave - 1) + lane_value(xb, kWave - 1);
+        rK = lane_value(K, kWave - 1);
+        prev = __builtin_amdgcn_readlane(f.m, cnt - 1);
+        f = f1;
+        sw = swap_in(f, i1 >= 0);
     }
-    return sc;
+    if (eq > bq) {            // the last round's terms
+        const double lt = from_left0(tprev);
+        double C = rC;
+#pragma unroll
+        for (int j = 1; j < kWave; ++j) C = from_left(C) + lt;
+        rC = lane_value(C, kWave - 1) + lane_value(tprev, kWave - 1);
+    }
+    return rC;
 }
 
-// Exact score of plan p by a whole workgroup, serial per queue (threads take
-// queues, thread 0 adds the per-queue sums in queue order).  Used when the
-// slot-parallel form below does not fit in LDS.
-__device__ double exact_plan_serial(const ExactArgs &a, int64_t p, double *part)
+// Exact score of plan p by a whole workgroup: its wavefronts take queues, the
+// queue sums go to LDS, and thread 0 adds them in queue order.
+__device__ double block_plan_exact(const ExactArgs &a, int64_t p, double *qpart)
 {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int nw = blockDim.x / kWave;
     double total = 0.0;
-    for (int g0 = 0; g0 < a.I; g0 += blockDim.x) {
-        const int g = g0 + threadIdx.x;
-        if (g < a.I) part[threadIdx.x] = exact_queue(a, p, g);
-        __syncthreads();
-        if (threadIdx.x == 0) {
-            const int n = min((int)blockDim.x, a.I - g0);
-            for (int k = 0; k < n; ++k) total += part[k];
+    for (int g0 = 0; g0 < a.I; g0 += kExactPass) {
+        const int n = min(kExactPass, a.I - g0);
+        for (int j = wave_id(); j < n; j += nw) {
+            const double sc = wave_queue_exact(a, p, g0 + j);
+            if (lane == 0) qpart[j] = sc;
         }
+        __syncthreads();
+        if (threadIdx.x == 0)
+            for (int k = 0; k < n; ++k) total += qpart[k];
         __syncthreads();
     }
     return total;   // valid in thread 0
-}
-
-// The same exact score, slot-parallel, with the same arithmetic and the same
-// summation order.  Inputs are first gathered into LDS by independent loads
-// (no chains of dependent global loads):
-//   0. every thread takes slots: a = n mu and b = n var (exact products) and
-//      the model of the slot's group; the eviction words; the swap table
-//   1. per queue (one thread each), the running sums in position order give
-//      every slot's E[W] = A/Theta + K and SD = sqrt(V)/Theta (in place of a, b)
-//   2. every thread takes slots: P and the term n P (in place of E[W])
-//   3. per queue, the terms are added in position order; thread 0 adds the
-//      queue sums in queue order.
-struct ExactLds {
-    double *x, *y;            // [G] each
-    uint32_t *evw;            // [ceil(G/32)]
-    float *swap;              // [C M M] or null (then read from global memory)
-    unsigned char *mdl;       // [G]
-};
-
-__device__ double exact_plan(const ExactArgs &a, int64_t p, const ExactLds &L, double *part)
-{
-    const int G = a.G;
-    const int W = (G + 31) >> 5;
-    const int64_t ld = a.ld;
-    // 0. gather (8 independent slots per thread per step)
-    for (int s0 = threadIdx.x; s0 < G; s0 += 8 * blockDim.x) {
-        int i[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const int s = s0 + u * blockDim.x;
-            i[u] = s < G ? (int)min((uint32_t)a.perm[(int64_t)s * ld + p], (uint32_t)(G - 1)) : 0;
-        }
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const int s = s0 + u * blockDim.x;
-            if (s < G) {
-                const double n = (double)(uint32_t)clampi(a.grp_count[i[u]], 0, (int)kCountMask);
-                L.x[s] = n * (double)a.grp_mu[i[u]];
-                L.y[s] = n * (double)a.grp_var[i[u]];
-                L.mdl[s] = (unsigned char)clampi(a.grp_model[i[u]], 0, a.M - 1);
-            }
-        }
-    }
-    for (int w = threadIdx.x; w < W; w += blockDim.x)
-        L.evw[w] = a.evict ? a.evict[(int64_t)w * ld + p] : 0u;
-    if (L.swap && a.swap_cost)
-        for (int k = threadIdx.x; k < a.C * a.M * a.M; k += blockDim.x) L.swap[k] = a.swap_cost[k];
-    __syncthreads();
-    // 1. running sums per queue
-    for (int g = threadIdx.x; g < a.I; g += blockDim.x) {
-        const int32_t b = clampi(a.qoff[(int64_t)g * ld + p], 0, G);
-        const int32_t e = clampi(a.qoff[(int64_t)(g + 1) * ld + p], b, G);
-        const double theta = (double)a.inst_tput[g];
-        const int cls = clampi(a.inst_class[g], 0, a.C - 1);
-        int m_prev = a.inst_model0 ? clampi(a.inst_model0[g], -1, a.M - 1) : -1;
-        const double ecost = (double)a.evict_cost;
-        double A = 0.0, V = 0.0, K = 0.0;
-        for (int s = b; s < e; ++s) {
-            const int m = L.mdl[s];
-            if (m_prev >= 0 && m_prev != m && a.swap_cost) {
-                const int64_t k = ((int64_t)cls * a.M + m_prev) * a.M + m;
-                K += (double)(L.swap ? L.swap[k] : a.swap_cost[k]);
-            }
-            if ((L.evw[s >> 5] >> (s & 31)) & 1u) K += ecost;
-            const double xa = L.x[s], yb = L.y[s];
-            L.x[s] = A / theta + K;            // E[W]
-            L.y[s] = sqrt(V) / theta;          // SD[W]
-            A += xa;
-            V += yb;
-            m_prev = m;
-        }
-    }
-    __syncthreads();
-    // 2. probability and term per slot
-    for (int s0 = threadIdx.x; s0 < G; s0 += 8 * blockDim.x) {
-        int i[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const int s = s0 + u * blockDim.x;
-            i[u] = s < G ? (int)min((uint32_t)a.perm[(int64_t)s * ld + p], (uint32_t)(G - 1)) : 0;
-        }
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const int s = s0 + u * blockDim.x;
-            if (s < G) {
-                const double n = (double)(uint32_t)clampi(a.grp_count[i[u]], 0, (int)kCountMask);
-                const double slo = (double)a.grp_slo[i[u]];
-                const double EW = L.x[s], SD = L.y[s];
-                double P;
-                if (SD > 0.0)
-                    P = 0.5 * erfc((slo - EW) / (SD * 1.4142135623730951));
-                else
-                    P = (EW > slo) ? 1.0 : 0.0;
-                L.x[s] = n * P;
-            }
-        }
-    }
-    __syncthreads();
-    // 3. sums per queue, then over queues
-    double total = 0.0;
-    for (int g0 = 0; g0 < a.I; g0 += blockDim.x) {
-        const int g = g0 + threadIdx.x;
-        if (g < a.I) {
-            const int32_t b = clampi(a.qoff[(int64_t)g * ld + p], 0, G);
-            const int32_t e = clampi(a.qoff[(int64_t)(g + 1) * ld + p], b, G);
-            double sc = 0.0;
-            for (int s = b; s < e; ++s) sc += L.x[s];
-            part[threadIdx.x] = sc;
-        }
-        __syncthreads();
-        if (threadIdx.x == 0) {
-            const int n = min((int)blockDim.x, a.I - g0);
-            for (int k = 0; k < n; ++k) total += part[k];
-        }
-        __syncthreads();
-    }
-    return total;   // valid in thread 0
-}
-
-// Exact score with whichever form fits: `big` = 1 the kernel got the LDS of
-// the staged form, 2 the same plus room for the swap table.
-__device__ double exact_score(const ExactArgs &a, int64_t p, unsigned char *dyn, int big,
-                              double *part)
-{
-    if (big) {
-        ExactLds L;
-        L.x = reinterpret_cast<double *>(dyn);
-        L.y = L.x + a.G;
-        L.evw = reinterpret_cast<uint32_t *>(L.y + a.G);
-        float *after = reinterpret_cast<float *>(L.evw + ((a.G + 31) >> 5));
-        L.swap = big == 2 ? after : nullptr;
-        L.mdl = reinterpret_cast<unsigned char *>(after + (big == 2 ? a.C * a.M * a.M : 0));
-        return exact_plan(a, p, L, part);
-    }
-    return exact_plan_serial(a, p, part);
 }
 #pragma clang fp contract(on)
 
-__global__ __launch_bounds__(kRefineThreads) void k_exact(ExactArgs a, const int64_t *idx,
-                                                          int64_t n, double *out, int big)
+__global__ __launch_bounds__(kExactThreads) void k_exact(ExactArgs a, const int64_t *idx,
+                                                         int64_t n, double *out)
 {
-    extern __shared__ __align__(16) unsigned char dyn[];
-    __shared__ double part[kRefineThreads];
+    __shared__ double qpart[kExactPass];
     for (int64_t k = blockIdx.x; k < n; k += gridDim.x) {
         int64_t p = idx[k];
         const bool ok = p >= 0 && p < a.P;
         p = ok ? p : 0;
-        const double s = exact_score(a, p, dyn, big, part);
+        const double s = block_plan_exact(a, p, qpart);
         if (threadIdx.x == 0) out[k] = ok ? s : NAN;
     }
 }
@@ -1001,80 +962,102 @@ __device__ double block_min(double v, double *ls)
     return b;
 }
 
-// Candidate selection and exact re-score.  Every workgroup first reduces the
-// per-workgroup minima of the screening scores, then walks its own contiguous
-// range of plans in index order and re-scores exactly every plan whose
-// screening score is within twice the screening error bound of the minimum
-// (the exact minimum is always among them).
-__global__ __launch_bounds__(kRefineThreads) void k_refine(ExactArgs a, const double *fast,
-                                                           const double *wg_min, int n_wg,
-                                                           const double *nsum,
-                                                           double *best_s, int64_t *best_i,
-                                                           int big)
+// Candidate selection: every workgroup reduces the per-workgroup minima of the
+// screened scores, then appends the plans of its share whose screened score is
+// within twice the screening error bound of the minimum (the exact minimum is
+// always among them) to the candidate list, one atomic per wavefront.  The
+// scoring kernel zeroed the count.
+__global__ __launch_bounds__(kSelThreads) void k_gselect(const double *fast, const double *wg_min,
+                                                         int n_wg, const double *nsum, int64_t P,
+                                                         int64_t *cand, int32_t *ncand)
 {
-    extern __shared__ __align__(16) unsigned char dyn[];
-    __shared__ double part[kRefineThreads];
-    __shared__ double ls[kRefineThreads / kWave];
-    __shared__ int64_t li[kRefineThreads / kWave];
+    __shared__ double ls[kSelThreads / kWave];
     double m = INFINITY;
     for (int k = threadIdx.x; k < n_wg; k += blockDim.x) m = fmin(m, wg_min[k]);
     m = block_min(m, ls);
     // |screened - exact| <= eps * (total requests), plus the rounding of both sums
     const double delta = kEpsP * (*nsum) * (1.0 + 1e-9) + 1e-300;
     const double thr = m + 2.0 * delta;
-
-    const int64_t per = (a.P + gridDim.x - 1) / gridDim.x;
-    const int64_t lo = (int64_t)blockIdx.x * per;
-    const int64_t hi = min(a.P, lo + per);
-    double bs = INFINITY;
-    int64_t bi = -1;
-    for (int64_t base = lo; base < hi; base += blockDim.x) {
-        const int64_t p = base + threadIdx.x;
-        const bool cand = p < hi && fast[p] <= thr;
-        if (!__syncthreads_or(cand)) continue;
-        // candidates of this chunk, one at a time in index order
-        int64_t next = cand ? p : INT64_MAX;
-        while (true) {
-            int64_t q = next;
-            // lowest remaining candidate index in the block
-            for (int o = 32; o > 0; o >>= 1) {
-                const int64_t q2 = __shfl_xor(q, o, kWave);
-                q = q2 < q ? q2 : q;
-            }
-            __syncthreads();
-            if ((threadIdx.x & (kWave - 1)) == 0) li[threadIdx.x / kWave] = q;
-            __syncthreads();
-            q = INT64_MAX;
-            for (int w = 0; w < (int)(blockDim.x / kWave); ++w) q = li[w] < q ? li[w] : q;
-            __syncthreads();
-            if (q == INT64_MAX) break;
-            const double e = exact_score(a, q, dyn, big, part);
-            if (threadIdx.x == 0 && e < bs) {     // ascending index: the first minimum wins
-                bs = e;
-                bi = q;
-            }
-            if (next == q) next = INT64_MAX;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t stride = (int64_t)gridDim.x * kSelThreads;
+    for (int64_t base = (int64_t)blockIdx.x * kSelThreads + (threadIdx.x - lane); base < P;
+         base += stride) {
+        const int64_t p = base + lane;
+        const bool c = p < P && fast[p] <= thr;
+        const uint64_t bal = __ballot(c);
+        if (bal) {
+            int off = 0;
+            if (lane == 0) off = atomicAdd(ncand, __popcll(bal));
+            off = __shfl(off, 0, kWave);
+            if (c) cand[off + __popcll(bal & ((1ull << lane) - 1ull))] = p;
         }
-    }
-    if (threadIdx.x == 0) {
-        best_s[blockIdx.x] = bs;
-        best_i[blockIdx.x] = bi;
     }
 }
 
-__global__ __launch_bounds__(256) void k_final(const double *best_s, const int64_t *best_i, int n,
-                                               int64_t *out_i, double *out_s)
+// Exact scores of the candidates.  When the per-(candidate, queue) sums fit
+// (count <= cap), one wavefront per (candidate, queue) writes its queue's
+// score to Q; else every workgroup scores whole candidates and writes the
+// plan's score over its screened score in X.
+__global__ __launch_bounds__(kGexThreads) void k_gexact(ExactArgs a, const int64_t *cand,
+                                                        const int32_t *ncand, int64_t cap,
+                                                        double *Q, double *X)
+{
+    __shared__ double qpart[kExactPass];
+    const int64_t n = __builtin_amdgcn_readfirstlane(ncand[0]);
+    if (n <= cap) {
+        constexpr int nwv = kGexThreads / kWave;
+        const int64_t tasks = n * a.I;
+        for (int64_t t = (int64_t)blockIdx.x * nwv + wave_id(); t < tasks;
+             t += (int64_t)gridDim.x * nwv) {
+            const int64_t k = t / a.I;
+            const int g = (int)(t - k * a.I);
+            int64_t p = cand[k];
+            p = p < 0 ? 0 : (p >= a.P ? a.P - 1 : p);
+            const double sc = wave_queue_exact(a, p, g);
+            if ((threadIdx.x & (kWave - 1)) == 0) Q[k * a.I + g] = sc;
+        }
+    } else {
+        for (int64_t k = blockIdx.x; k < n; k += gridDim.x) {
+            int64_t p = cand[k];
+            p = p < 0 ? 0 : (p >= a.P ? a.P - 1 : p);
+            const double s = block_plan_exact(a, p, qpart);
+            if (threadIdx.x == 0) X[p] = s;
+        }
+    }
+}
+
+// The candidate with the lowest exact score, the lowest index on ties; a NaN
+// score never wins.  Plan scores are the queue sums added in queue order (or
+// the whole-plan scores of k_gexact's second form).  No candidates: index -1,
+// score +inf.
+__global__ __launch_bounds__(256) void k_gpick(const int64_t *cand, const int32_t *ncand,
+                                               int64_t cap, int I, const double *Q,
+                                               const double *X, int64_t *out_i, double *out_s)
 {
     __shared__ double ls[256 / kWave];
     __shared__ int64_t li[256 / kWave];
+    const int64_t n = ncand ? (int64_t)ncand[0] : 0;
     double s = INFINITY;
     int64_t i = -1;
-    for (int k = threadIdx.x; k < n; k += blockDim.x) {
-        const double s2 = best_s[k];
-        const int64_t i2 = best_i[k];
-        const bool take = i2 >= 0 && (i < 0 || s2 < s || (s2 == s && i2 < i));
-        s = take ? s2 : s;
-        i = take ? i2 : i;
+    // one wavefront per candidate: the lanes load its queue sums, which are
+    // added in queue order
+    const int lane = threadIdx.x & (kWave - 1);
+    const int nw = blockDim.x / kWave;
+    for (int64_t k = wave_id(); k < n; k += nw) {
+        const int64_t p = cand[k];
+        double t = 0.0;
+        if (n <= cap) {
+            for (int g0 = 0; g0 < I; g0 += kWave) {
+                const double q = g0 + lane < I ? Q[k * I + g0 + lane] : 0.0;
+                const int c = min(kWave, I - g0);
+                for (int j = 0; j < c; ++j) t += lane_value(q, j);
+            }
+        } else {
+            t = X[p];
+        }
+        const bool take = lane == 0 && t == t && (i < 0 || t < s || (t == s && p < i));
+        s = take ? t : s;
+        i = take ? p : i;
     }
     block_argmin(s, i, ls, li);
     if (threadIdx.x == 0) {
@@ -1416,8 +1399,8 @@ int score_grid(ScoreKernel k, size_t lds, int64_t P, int G, int I, int *grid, in
 }
 
 int launch_score(const qlm_problem *pr, const qlm_plans *pl, double *score, double *penalty,
-                 const qlm_detail *det, double *wg_min, double *wg_nsum, int *grid_out,
-                 hipStream_t stream)
+                 const qlm_detail *det, double *wg_min, double *wg_nsum, int32_t *ncand,
+                 int *grid_out, hipStream_t stream)
 {
     const bool ev = pl->evict_bits != nullptr;
     const Geometry geo = geometry(pr->n_groups, pr->n_instances, pr->n_models, pr->n_classes, ev);
@@ -1431,6 +1414,7 @@ int launch_score(const qlm_problem *pr, const qlm_plans *pl, double *score, doub
     a.penalty = penalty;
     a.wg_min = wg_min;
     a.wg_nsum = wg_nsum;
+    a.ncand = ncand;
     if (det) {
         a.d_begin = det->plan_begin;
         a.d_count = det->plan_count;
@@ -1458,34 +1442,16 @@ int launch_score(const qlm_problem *pr, const qlm_plans *pl, double *score, doub
     return QLM_OK;
 }
 
-// Dynamic LDS of the exact re-score: the staged form when it fits (with the
-// swap table when that fits too), else none (serial form).
-int exact_lds(const void *kernel, const qlm_problem *pr, size_t *lds, int *big)
-{
-    const size_t G = (size_t)pr->n_groups;
-    const size_t base = 16 * G + 4 * ((G + 31) / 32) + G;
-    const size_t swap = 4 * (size_t)pr->n_classes * pr->n_models * pr->n_models;
-    const size_t static_lds = 8 * (size_t)kRefineThreads + 256;
-    size_t want = (base + 15) / 16 * 16;
-    int kind = 1;
-    if (pr->swap_cost && ((base + swap + 15) / 16 * 16) + static_lds <= kLdsLimit) {
-        want = (base + swap + 15) / 16 * 16;
-        kind = 2;
-    }
-    if (want + static_lds <= kLdsLimit) {
-        hipError_t e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                           (int)want);
-        if (e != hipSuccess) return hip_fail(e, "hipFuncSetAttribute");
-        *lds = want;
-        *big = kind;
-    } else {
-        *lds = 0;
-        *big = 0;
-    }
-    return QLM_OK;
-}
-
 size_t align256(size_t v) { return (v + 255) / 256 * 256; }
+
+// qlm_best_plan's workspace before the per-(candidate, queue) sums: screened
+// scores [P], per-workgroup minima, total requests and candidate count,
+// candidates [P].
+size_t best_plan_fixed_bytes(int64_t P)
+{
+    return align256(8 * (size_t)P) + align256(8 * (size_t)kMaxScoreBlocks) + 256 +
+           align256(8 * (size_t)P);
+}
 
 }  // namespace
 
@@ -1508,7 +1474,7 @@ int qlm_rwt_score(const qlm_problem *problem, const qlm_plans *plans, double *sc
             detail->plan_begin + detail->plan_count > plans->n_plans)
             return fail(QLM_ERR_ARG, "detail plan range outside [0, n_plans)");
     }
-    return launch_score(problem, plans, score, penalty, detail, nullptr, nullptr, nullptr,
+    return launch_score(problem, plans, score, penalty, detail, nullptr, nullptr, nullptr, nullptr,
                         (hipStream_t)stream);
 }
 
@@ -1525,12 +1491,8 @@ int qlm_rwt_score_exact(const qlm_problem *problem, const qlm_plans *plans,
     if (plans->n_plans == 0) return fail(QLM_ERR_ARG, "no plans to index");
     ExactArgs a = exact_args(problem, plans);
     const int grid = (int)(n < 65535 ? n : 65535);
-    size_t lds = 0;
-    int big = 0;
-    rc = exact_lds((const void *)k_exact, problem, &lds, &big);
-    if (rc) return rc;
-    hipLaunchKernelGGL(k_exact, dim3(grid), dim3(kRefineThreads), lds, (hipStream_t)stream, a,
-                       plan_index, n, score, big);
+    hipLaunchKernelGGL(k_exact, dim3(grid), dim3(kExactThreads), 0, (hipStream_t)stream, a,
+                       plan_index, n, score);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "k_exact launch");
     return QLM_OK;
@@ -1538,10 +1500,13 @@ int qlm_rwt_score_exact(const qlm_problem *problem, const qlm_plans *plans,
 
 size_t qlm_best_plan_workspace_bytes(const qlm_problem *problem, int64_t n_plans)
 {
-    (void)problem;
+    if (!problem || problem->n_instances < 1) return 0;
     if (n_plans < 0) n_plans = 0;
-    return align256(8 * (size_t)n_plans) + align256(8 * (size_t)kMaxScoreBlocks) + 256 +
-           align256(8 * (size_t)kRefineBlocks) + align256(8 * (size_t)kRefineBlocks);
+    const size_t I = (size_t)problem->n_instances;
+    size_t rows = kCandSumBytes / (8 * I);
+    if (rows < 256) rows = 256;
+    if (rows > (size_t)n_plans) rows = (size_t)n_plans;
+    return best_plan_fixed_bytes(n_plans) + align256(8 * rows * I);
 }
 
 int qlm_best_plan(const qlm_problem *problem, const qlm_plans *plans, void *ws, size_t ws_bytes,
@@ -1554,44 +1519,52 @@ int qlm_best_plan(const qlm_problem *problem, const qlm_plans *plans, void *ws, 
     if (rc) return rc;
     if (!best_index || !best_score) return fail(QLM_ERR_ARG, "best_index and best_score are required");
     const int64_t P = plans->n_plans;
+    const int I = problem->n_instances;
     if (!ws || ((uintptr_t)ws & 255u))
         return fail(QLM_ERR_WORKSPACE, "workspace must be non-NULL and 256-byte aligned");
+    const size_t fixed = best_plan_fixed_bytes(P);
     if (ws_bytes < qlm_best_plan_workspace_bytes(problem, P))
         return fail(QLM_ERR_WORKSPACE, "workspace too small");
+    hipError_t e;
+    if (P == 0) {
+        hipLaunchKernelGGL(k_gpick, dim3(1), dim3(256), 0, stream, nullptr, nullptr, (int64_t)0, I,
+                           nullptr, nullptr, best_index, best_score);
+        e = hipGetLastError();
+        return e == hipSuccess ? QLM_OK : hip_fail(e, "k_gpick launch");
+    }
     unsigned char *w = (unsigned char *)ws;
     double *fast = (double *)w;
     w += align256(8 * (size_t)P);
     double *wg_min = (double *)w;
     w += align256(8 * (size_t)kMaxScoreBlocks);
     double *nsum = (double *)w;
+    int32_t *ncand = (int32_t *)(w + 128);
     w += 256;
-    double *bs = (double *)w;
-    w += align256(8 * (size_t)kRefineBlocks);
-    int64_t *bi = (int64_t *)w;
-    if (P == 0) {
-        hipLaunchKernelGGL(k_final, dim3(1), dim3(256), 0, stream, bs, bi, 0, best_index,
-                           best_score);
-        hipError_t e = hipGetLastError();
-        return e == hipSuccess ? QLM_OK : hip_fail(e, "k_final launch");
-    }
+    int64_t *cand = (int64_t *)w;
+    w += align256(8 * (size_t)P);
+    double *Q = (double *)w;
+    // candidates whose per-queue sums fit in the rest of the workspace
+    int64_t cap = (int64_t)((ws_bytes - fixed) / (8 * (size_t)I));
+    if (cap > P) cap = P;
     int grid = 0;
-    rc = launch_score(problem, plans, fast, nullptr, nullptr, wg_min, nsum, &grid, stream);
+    rc = launch_score(problem, plans, fast, nullptr, nullptr, wg_min, nsum, ncand, &grid, stream);
     if (rc) return rc;
-    ExactArgs a = exact_args(problem, plans);
-    int rgrid = (int)((P + kRefineThreads - 1) / kRefineThreads);
-    if (rgrid > kRefineBlocks) rgrid = kRefineBlocks;
-    size_t lds = 0;
-    int big = 0;
-    rc = exact_lds((const void *)k_refine, problem, &lds, &big);
-    if (rc) return rc;
-    hipLaunchKernelGGL(k_refine, dim3(rgrid), dim3(kRefineThreads), lds, stream, a, fast, wg_min,
-                       grid, nsum, bs, bi, big);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return hip_fail(e, "k_refine launch");
-    hipLaunchKernelGGL(k_final, dim3(1), dim3(256), 0, stream, bs, bi, rgrid, best_index,
-                       best_score);
+    int sgrid = (int)((P + kSelThreads - 1) / kSelThreads);
+    if (sgrid > kSelBlocks) sgrid = kSelBlocks;
+    hipLaunchKernelGGL(k_gselect, dim3(sgrid), dim3(kSelThreads), 0, stream, fast, wg_min, grid,
+                       nsum, P, cand, ncand);
     e = hipGetLastError();
-    if (e != hipSuccess) return hip_fail(e, "k_final launch");
+    if (e != hipSuccess) return hip_fail(e, "k_gselect launch");
+    ExactArgs a = exact_args(problem, plans);
+    hipLaunchKernelGGL(k_gexact, dim3(kGexBlocks), dim3(kGexThreads), 0, stream, a,
+                       (const int64_t *)cand, (const int32_t *)ncand, cap, Q, fast);
+    e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "k_gexact launch");
+    hipLaunchKernelGGL(k_gpick, dim3(1), dim3(256), 0, stream, (const int64_t *)cand,
+                       (const int32_t *)ncand, cap, I, (const double *)Q, (const double *)fast,
+                       best_index, best_score);
+    e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "k_gpick launch");
     return QLM_OK;
 }
 
