@@ -879,17 +879,27 @@ __global__ __launch_bounds__(kThreads) void k_fexact(FArgs a, const int64_t *pla
             const double la = from_left0(xa), lb = from_left0(xb);
             const double l1 = from_left0(c1), l2 = from_left0(c2);
             double A = rA, V = rV, K0 = rK;
-            for (int j = 1; j < cnt; ++j) {
-                A = from_left(A) + la;
-                V = from_left(V) + lb;
-                K0 = (from_left(K0) + l1) + l2;
+            // cnt - 1 steps, rounded up to blocks of 8 (a step past the last
+            // position leaves every position's sums unchanged), the count in
+            // a scalar register so that only a block ends in a branch
+            const int steps = __builtin_amdgcn_readfirstlane(cnt - 1);
+            for (int j = 0; j < steps; j += 8) {
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    A = from_left(A) + la;
+                    V = from_left(V) + lb;
+                    K0 = (from_left(K0) + l1) + l2;
+                }
             }
             double K = K0 + c1;
             K = K + c2;
             const double term = i >= 0 ? slot_exact(a, i, A, V, K, theta) : 0.0;
             const double lt = from_left0(term);
             double C = rC;
-            for (int j = 1; j < cnt; ++j) C = from_left(C) + lt;
+            for (int j = 0; j < steps; j += 8) {
+#pragma unroll
+                for (int u = 0; u < 8; ++u) C = from_left(C) + lt;
+            }
             const int last = cnt - 1;
             rA = lane_value(A, last) + lane_value(xa, last);
             rV = lane_value(V, last) + lane_value(xb, last);

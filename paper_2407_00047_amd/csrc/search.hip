@@ -103,6 +103,7 @@ constexpr int kStage = 1024;               // tail records staged in LDS at a ti
 constexpr int32_t kMaxSearchGroups = 1 << 16;
 constexpr int32_t kMaxSearchInstances = 4096;
 constexpr int32_t kMaxWindow = 1024;
+constexpr int kStageSlots = 8192;            // slots a placement moves through LDS
 constexpr uint32_t kCountMask = (1u << 21) - 1u;
 constexpr uint32_t kFlagBit = 1u << 8;
 constexpr int kCountShift = 9;
@@ -399,10 +400,17 @@ __device__ void wave_walk(Run &r, int nv, const RecOf &rec, double theta, int cl
         const double l1 = from_left0(c1);
         const double l2 = from_left0(c2);
         double A = r.A, V = r.V, K0 = r.K;     // K0: costs before this position's own
-        for (int j = 1; j < cnt; ++j) {
-            A = from_left(A) + la;
-            V = from_left(V) + lb;
-            K0 = (from_left(K0) + l1) + l2;
+        // cnt - 1 steps, rounded up to blocks of 8 (a step past the last
+        // position leaves every position's sums unchanged), the count in a
+        // scalar register so that only a block ends in a branch
+        const int steps = __builtin_amdgcn_readfirstlane(cnt - 1);
+        for (int j = 0; j < steps; j += 8) {
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                A = from_left(A) + la;
+                V = from_left(V) + lb;
+                K0 = (from_left(K0) + l1) + l2;
+            }
         }
         double K = K0 + c1;
         K = K + c2;
@@ -420,7 +428,10 @@ __device__ void wave_walk(Run &r, int nv, const RecOf &rec, double theta, int cl
         }
         const double lt = from_left0(term);
         double C = r.sc;
-        for (int j = 1; j < cnt; ++j) C = from_left(C) + lt;
+        for (int j = 0; j < steps; j += 8) {
+#pragma unroll
+            for (int u = 0; u < 8; ++u) C = from_left(C) + lt;
+        }
         const int last = cnt - 1;
         r.A = lane_value(A, last) + lane_value(x.a, last);
         r.V = lane_value(V, last) + lane_value(x.b, last);
@@ -1225,30 +1236,47 @@ __global__ __launch_bounds__(kThreads) void k_sexact(SearchArgs a)
 // whose SLO is strictly later (a reassignment, or with h its own queue a
 // re-insertion): the slots between its old and new place rotate by one, and
 // the queue offsets between the two queues shift.  Run by a whole workgroup.
-__device__ void place_apply(const SearchArgs &a, int64_t b, int s, int h, int p_known = -1)
+__device__ void place_apply(const SearchArgs &a, int64_t b, int s, int h, int p_known = -1,
+                            int g_known = -1)
 {
+    // the slots that move, staged in LDS when they fit (else in the workspace)
+    __shared__ int32_t st_perm[kStageSlots];
+    __shared__ uint8_t st_flag[kStageSlots];
     const int G = a.G, I = a.I;
     int32_t *perm = a.perm + b * G;
     uint8_t *flag = a.flag + b * G;
     int32_t *qof = a.qof + b * (I + 1);
     const SRec *sr = a.srec + b * G;
-    const int g = (int)sr[s].q;
+    const int g = g_known >= 0 ? g_known : (int)sr[s].q;
     const int p = p_known >= 0 ? p_known : insertion_point(sr, qof[h], qof[h + 1], sr[s].slo);
     // left: the group goes later (to slot p - 1); right: earlier (to slot p)
     const bool left = h > g || (h == g && p > s);
     const int lo = left ? s : p;
     const int hi = left ? p - 1 : s;
-    int32_t *sp = a.scratch + b * 2 * G;
-    int32_t *sf = sp + G;
-    for (int u = lo + threadIdx.x; u <= hi; u += kThreads) {
-        sp[u] = perm[u];
-        sf[u] = flag[u];
-    }
-    __syncthreads();
-    for (int u = lo + threadIdx.x; u <= hi; u += kThreads) {
-        const int v = left ? (u == hi ? s : u + 1) : (u == lo ? s : u - 1);
-        perm[u] = sp[v];
-        flag[u] = (uint8_t)sf[v];
+    if (hi - lo < kStageSlots) {
+        for (int u = lo + threadIdx.x; u <= hi; u += kThreads) {
+            st_perm[u - lo] = perm[u];
+            st_flag[u - lo] = flag[u];
+        }
+        __syncthreads();
+        for (int u = lo + threadIdx.x; u <= hi; u += kThreads) {
+            const int v = left ? (u == hi ? s : u + 1) : (u == lo ? s : u - 1);
+            perm[u] = st_perm[v - lo];
+            flag[u] = st_flag[v - lo];
+        }
+    } else {
+        int32_t *sp = a.scratch + b * 2 * G;
+        int32_t *sf = sp + G;
+        for (int u = lo + threadIdx.x; u <= hi; u += kThreads) {
+            sp[u] = perm[u];
+            sf[u] = flag[u];
+        }
+        __syncthreads();
+        for (int u = lo + threadIdx.x; u <= hi; u += kThreads) {
+            const int v = left ? (u == hi ? s : u + 1) : (u == lo ? s : u - 1);
+            perm[u] = sp[v];
+            flag[u] = (uint8_t)sf[v];
+        }
     }
     if (h > g) {
         for (int q = g + 1 + threadIdx.x; q <= h; q += kThreads) qof[q] -= 1;
@@ -1429,25 +1457,36 @@ __global__ __launch_bounds__(kThreads) void k_place_pick(SearchArgs a, int group
     __shared__ double ls[kWaves];
     __shared__ int64_t lk[kWaves];
     __shared__ int64_t kk;
-    __shared__ int kp;
+    __shared__ int kp, kg;
     // the queue scores and their running sums, staged for the totals
     __shared__ double sT[kMaxSearchInstances + 1], sQ[kMaxSearchInstances];
+    __shared__ int scand[kThreads];
     const int64_t b = blockIdx.x;
     const int G = a.G, I = a.I;
+    // every independent load at once: the queue scores, the moved group's
+    // slot and queue, and (up to kThreads queues) each thread's candidate
+    // score and insertion point
+    const bool one = I <= kThreads;
+    double v1 = 0.0;
+    if (one && threadIdx.x < I) {
+        v1 = a.cex[b * a.n_moves + threadIdx.x];
+        scand[threadIdx.x] = a.cand[b * a.n_moves + threadIdx.x];
+    }
     for (int q = threadIdx.x; q <= I; q += kThreads) {
         sT[q] = a.T[b * (I + 1) + q];
         if (q < I) sQ[q] = a.Q[b * I + q];
     }
-    __syncthreads();
     const int s0 = clampi(a.dq[b * 4 + 2], 0, G - 1);
     const int g0 = clampi(a.dq[b * 4 + 3], 0, I - 1);
+    if (threadIdx.x == 0) kg = (int)a.srec[b * G + s0].q;
+    __syncthreads();
     const double *T = sT;
     const double *Q = sQ;
     const double rg = a.U[b];
     double best = INFINITY;
     int64_t bk = INT64_MAX;
     for (int h = threadIdx.x; h < I; h += kThreads) {
-        double v = a.cex[b * a.n_moves + h];
+        double v = one ? v1 : a.cex[b * a.n_moves + h];
         if (h != g0) {
             v = total_with2(T, Q, I, g0, rg, h, v);
             a.cex[b * a.n_moves + h] = v;
@@ -1459,17 +1498,19 @@ __global__ __launch_bounds__(kThreads) void k_place_pick(SearchArgs a, int group
     }
     block_best(best, bk, ls, lk);
     if (threadIdx.x == 0) {
-        if (bk < 0 || bk >= I) bk = 0;            // every score NaN: the first queue
+        const bool none = bk < 0 || bk >= I;
+        if (none) bk = 0;                         // every score NaN: the first queue
         kk = bk;
-        a.cur[b] = a.cex[b * a.n_moves + bk];
+        const double cur = none ? a.cex[b * a.n_moves + bk] : best;
+        a.cur[b] = cur;
         if (queue) queue[b] = (int32_t)bk;
-        if (score) score[b] = a.cur[b];
+        if (score) score[b] = cur;
         a.dq[b * 4] = min(g0, (int)bk);
         a.dq[b * 4 + 1] = max(g0, (int)bk);
-        kp = clampi(a.cand[b * a.n_moves + bk], 0, G);
+        kp = clampi(one ? scand[bk] : a.cand[b * a.n_moves + bk], 0, G);
     }
     __syncthreads();
-    place_apply(a, b, s0, (int)kk, kp);
+    place_apply(a, b, s0, (int)kk, kp, kg);
 }
 
 // ---------------------------------------------------------------------------

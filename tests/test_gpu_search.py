@@ -431,6 +431,41 @@ def test_place_group_arrival(qlm, orc):
         assert _close(float(r["score"][p]), o["score"])
 
 
+@pytest.mark.parametrize("fast", [0, 2])
+def test_place_group_long_move(qlm, orc, fast):
+    """A placement that moves more slots than a workgroup stages in LDS (8192):
+    9000 groups on 3 queues, one instance 100 times faster than the others.
+    fast = 2: the group heads queue 0, which holds 8301 groups (the slots
+    shift left); fast = 0: the group ends queue 2 and queue 0 holds 100 groups
+    (they shift right)."""
+    import torch
+    from cases import plans as make_plans_by_hand, problem as make_problem_by_hand
+    rng = np.random.default_rng(31 + fast)
+    G = 9000
+    groups = [(int(rng.integers(1, 20)), float(rng.uniform(50, 600)), float(rng.uniform(0, 5e4)),
+               0, float(rng.uniform(1, 50))) for _ in range(G)]
+    inst = [(400.0, 0)] * 3
+    inst[fast] = (40000.0, 0)
+    pr = make_problem_by_hand(groups, inst)
+    order = [int(x) for x in rng.permutation(G)]
+    if fast == 2:
+        group = order[0]
+        queues = [order[:8301], order[8301:8311], order[8311:]]
+    else:
+        group = order[-1]
+        queues = [order[:100], order[100:4600], order[4600:]]
+    pl = make_plans_by_hand([queues], G)
+    dpr, dpl = device_inputs(pr, pl)
+    r = qlm.place_group(dpr, dpl, group)
+    torch.cuda.synchronize()
+    o = orc.place_group(pr, pl, 0, group)
+    span = abs(list(o["perm"]).index(group) - list(pl["perm"][:, 0]).index(group)) + 1
+    assert span > 8192 and int(r["queue"][0]) == o["queue"], (span, o["queue"])
+    assert np.array_equal(r["plans"].perm.cpu().numpy()[:, 0], o["perm"])
+    assert np.array_equal(r["plans"].qoff.cpu().numpy()[:, 0], o["qoff"])
+    assert _close(float(r["score"][0]), o["score"])
+
+
 @pytest.mark.parametrize("kw", [dict(G=9, I=3, P=5), dict(G=70, I=4, P=6, empty_queues=True),
                                 dict(G=300, I=12, P=4, skewed=True), dict(G=40, I=1, P=3)])
 def test_place_session(qlm, orc, kw):
