@@ -316,6 +316,20 @@ __device__ inline int insertion_point(const SRec *sr, int bq, int eq, float slo)
     return lo;
 }
 
+// The same over the running maxima of [bq, eq) staged in LDS (pm[u - bq]).
+__device__ inline int insertion_point_lds(const float *pm, int bq, int eq, float slo)
+{
+    int lo = bq, hi = eq;
+    while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (pm[mid - bq] > slo)
+            hi = mid;
+        else
+            lo = mid + 1;
+    }
+    return lo;
+}
+
 // The same, by the wavefront: 64 positions a read, the first whose running
 // maximum is later by a ballot (long queues take the binary search).
 __device__ inline int insertion_point_wave(const SRec *sr, int bq, int eq, float slo)
@@ -1006,19 +1020,26 @@ __global__ __launch_bounds__(kThreads) void k_fmove(SearchArgs a)
     __shared__ double lmin[kWaves];
     __shared__ int lint[kWaves];
     __shared__ TRec stage[kStage];
-    for (int k = threadIdx.x; k < qlm_tail::kCells; k += kThreads) tab[k] = a.tail[k];
-    __syncthreads();
     const int G = a.G, I = a.I;
     const int per_chain = I * a.nwg_b;
     const int64_t b = blockIdx.x / per_chain;
     const int h = (blockIdx.x % per_chain) / a.nwg_b;
     const int wg = blockIdx.x % a.nwg_b;
-    if (a.done[b]) return;
+    if (a.done[b]) return;                    // the same in the whole workgroup
     const SRec *__restrict__ sr = a.srec + b * G;
     const SSt *__restrict__ ss = a.sst + b * G;
     const TRec *__restrict__ tr = a.trec + b * G;
     const int32_t *__restrict__ qof = a.qof + b * (I + 1);
     const int bq = qof[h], eq = qof[h + 1];
+    // the target queue's running SLO maxima, for the insertion points, share
+    // the tail records' staging buffer (the tails are staged after a barrier)
+    float *pmax = reinterpret_cast<float *>(stage);
+    constexpr int kPmaxSlots = (int)(kStage * sizeof(TRec) / sizeof(float));
+    const bool pm_lds = eq - bq <= kPmaxSlots;
+    for (int k = threadIdx.x; k < qlm_tail::kCells; k += kThreads) tab[k] = a.tail[k];
+    if (pm_lds)
+        for (int u = bq + (int)threadIdx.x; u < eq; u += kThreads) pmax[u - bq] = sr[u].pmax;
+    __syncthreads();
     const double theta = (double)a.inst_tput[h];
     const double inv_theta = 1.0 / theta;
     const double vscale = qlm_tail::kVarScale / (theta * theta);
@@ -1042,7 +1063,8 @@ __global__ __launch_bounds__(kThreads) void k_fmove(SearchArgs a)
                 w = Run{0.0, 0.0, 0.0, 0.0, model0_of(a, h)};
                 screen_visit(w, x, theta, inv_theta, cls, vscale, eps, tab, a, force);
             } else {
-                p = insertion_point(sr, bq, eq, x.slo);
+                p = pm_lds ? insertion_point_lds(pmax, bq, eq, x.slo)
+                           : insertion_point(sr, bq, eq, x.slo);
                 if (p == eq) {
                     const SSt t = ss[eq - 1];
                     const SRec y = sr[eq - 1];

@@ -140,6 +140,22 @@ def test_screen_bounds(qlm, orc, kw):
     print("unbounded (scored exactly): %d of %d; largest error / bound %.3g" % (forced, F.size, worst))
 
 
+def test_screen_bounds_long_queue(qlm, orc):
+    """A queue of 4300 groups, longer than the reassignment screen stages in
+    LDS for its insertion points (4096): the screened scores of every move
+    within their bounds of the oracle's."""
+    import torch
+    rng = np.random.default_rng(52)
+    pr, pl = hand_case(rng, G=4500, I=2, P=1)
+    pl["qoff"][:, 0] = [0, 4300, 4500]
+    dpr, dpl = device_inputs(pr, pl)
+    F, D = qlm.search_screen(dpr, dpl, 4)
+    torch.cuda.synchronize()
+    ref = orc.move_scores(pr, pl, 0, 4)
+    f, w = _check_screen(F.cpu().numpy()[0], D.cpu().numpy()[0], ref, "long queue")
+    print("unbounded: %d; largest error / bound %.3g" % (f, w))
+
+
 def _check_search(orc, pr, pl, p, W, T, g_trace, g_steps, g_perm, g_qoff, g_ev, g_score):
     """Compares one chain's search with the oracle's; returns the step where a
     near-tie let the two sides part (None when they agree throughout)."""
