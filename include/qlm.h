@@ -126,9 +126,10 @@ int qlm_rwt_score(const qlm_problem *problem, const qlm_plans *plans, double *sc
 
 /*
  * Exact (double precision) scores of selected plans: plan_index[k] (device
- * array of n, each in [0, P)) -> score[k] (device).  Every step is the
- * definition above in double precision, summed in queue order then position
- * order, with IEEE division and square root and the device erfc.
+ * array of n, each in [0, P)) -> score[k] (device); an index outside [0, P)
+ * gives NaN.  Every step is the definition above in double precision, with
+ * IEEE division and square root and the device erfc; each queue's terms are
+ * added in position order, then the queue sums in queue order.
  */
 int qlm_rwt_score_exact(const qlm_problem *problem, const qlm_plans *plans,
                         const int64_t *plan_index, int64_t n, double *score,
