@@ -47,7 +47,9 @@
 // candidates) walk both queues exactly.
 //
 // Kernels
-//   k_srank    once per call: group records; the groups ranked by SLO
+//   k_srank    once per call: the groups ranked by SLO (partial counts per
+//              tile of 1024 groups; k_srankout sums them, places each group
+//              at its rank and writes the group records)
 //   k_stail    once per call: the normal-tail table, which the screens copy
 //              into LDS
 //   k_sload    start plans, slot-major -> chain-major working copies
@@ -158,6 +160,7 @@ struct SearchArgs {
     float evict_cost;
     GRec *grec;                   // [G]
     int32_t *by_slo;              // [G] groups in SLO order
+    int32_t *rank_part;           // [ceil(G / kRankTile)][G] partial ranks
     float2 *tail;                 // [kCells] the normal-tail table (tail.h)
     // per chain, chain b at b * (per-chain size)
     int32_t *perm;                // [G]
@@ -483,56 +486,10 @@ __device__ inline double total_with2(const double *T, const double *Q, int I, in
 
 // Group records, and each group's rank in (SLO, id) order.  A workgroup takes
 // 64 groups; its four wavefronts count a quarter of the keys each.
-__global__ __launch_bounds__(kThreads) void k_srank(SearchArgs a)
+// Group i's record: n mu and n var (exact products in double), SLO, and the
+// request count with the model.
+__device__ inline GRec group_record(const SearchArgs &a, int i)
 {
-    __shared__ __align__(16) uint32_t keys[kRankTile];
-    __shared__ int part[kThreads];
-    const int G = a.G;
-    const int li = threadIdx.x & (kWave - 1), quarter = threadIdx.x / kWave;
-    const int i = blockIdx.x * kWave + li;
-    uint32_t mine = 0;
-    if (i < G) {
-        mine = order_key(a.grp_slo[i]);
-        if (quarter == 0) {
-            const uint32_t n = (uint32_t)clampi(a.grp_count[i], 0, (int)kCountMask);
-            const double dn = (double)n;
-            GRec r;
-            r.a = dn * (double)a.grp_mu[i];
-            r.b = dn * (double)a.grp_var[i];
-            r.slo = a.grp_slo[i];
-            r.nm = (n << kCountShift) | (uint32_t)clampi(a.grp_model[i], 0, a.M - 1);
-            r.pad[0] = r.pad[1] = 0u;
-            a.grec[i] = r;
-        }
-    }
-    int cnt = 0;
-    for (int t0 = 0; t0 < G; t0 += kRankTile) {
-        __syncthreads();
-        for (int k = threadIdx.x; k < kRankTile; k += kThreads)
-            keys[k] = t0 + k < G ? order_key(a.grp_slo[t0 + k]) : 0xFFFFFFFFu;
-        __syncthreads();
-        const int base = quarter * (kRankTile / kWaves);
-#pragma unroll 4
-        for (int k = 0; k < kRankTile / kWaves; k += 4) {
-            const uint4 o = *reinterpret_cast<const uint4 *>(&keys[base + k]);
-            const int id = t0 + base + k;      // ids past G hold the largest key
-            cnt += (o.x < mine || (o.x == mine && id < i)) ? 1 : 0;
-            cnt += (o.y < mine || (o.y == mine && id + 1 < i)) ? 1 : 0;
-            cnt += (o.z < mine || (o.z == mine && id + 2 < i)) ? 1 : 0;
-            cnt += (o.w < mine || (o.w == mine && id + 3 < i)) ? 1 : 0;
-        }
-    }
-    part[threadIdx.x] = cnt;
-    __syncthreads();
-    if (quarter == 0 && i < G)
-        a.by_slo[part[li] + part[li + kWave] + part[li + 2 * kWave] + part[li + 3 * kWave]] = i;
-}
-
-// Group records only (when no screen runs).
-__global__ __launch_bounds__(kThreads) void k_sgrec(SearchArgs a)
-{
-    const int i = blockIdx.x * kThreads + threadIdx.x;
-    if (i >= a.G) return;
     const uint32_t n = (uint32_t)clampi(a.grp_count[i], 0, (int)kCountMask);
     const double dn = (double)n;
     GRec r;
@@ -541,7 +498,63 @@ __global__ __launch_bounds__(kThreads) void k_sgrec(SearchArgs a)
     r.slo = a.grp_slo[i];
     r.nm = (n << kCountShift) | (uint32_t)clampi(a.grp_model[i], 0, a.M - 1);
     r.pad[0] = r.pad[1] = 0u;
-    a.grec[i] = r;
+    return r;
+}
+
+// Ranks in (SLO, id) order, counted: workgroup (tile t, block of 64 groups)
+// counts, for each of its groups, the groups of tile t (kRankTile ids) that
+// order before it, its four wavefronts a quarter of the tile each, and leaves
+// the partial counts in rank_part[t][i].
+__global__ __launch_bounds__(kThreads) void k_srank(SearchArgs a)
+{
+    __shared__ __align__(16) uint32_t keys[kRankTile];
+    __shared__ int part[kThreads];
+    const int G = a.G;
+    const int nb = (G + kWave - 1) / kWave;
+    const int gb = blockIdx.x % nb, tile = blockIdx.x / nb;
+    const int li = threadIdx.x & (kWave - 1), quarter = threadIdx.x / kWave;
+    const int i = gb * kWave + li;
+    const uint32_t mine = i < G ? order_key(a.grp_slo[i]) : 0u;
+    const int t0 = tile * kRankTile;
+    for (int k = threadIdx.x; k < kRankTile; k += kThreads)
+        keys[k] = t0 + k < G ? order_key(a.grp_slo[t0 + k]) : 0xFFFFFFFFu;
+    __syncthreads();
+    int cnt = 0;
+    const int base = quarter * (kRankTile / kWaves);
+#pragma unroll 4
+    for (int k = 0; k < kRankTile / kWaves; k += 4) {
+        const uint4 o = *reinterpret_cast<const uint4 *>(&keys[base + k]);
+        const int id = t0 + base + k;          // ids past G hold the largest key
+        cnt += (o.x < mine || (o.x == mine && id < i)) ? 1 : 0;
+        cnt += (o.y < mine || (o.y == mine && id + 1 < i)) ? 1 : 0;
+        cnt += (o.z < mine || (o.z == mine && id + 2 < i)) ? 1 : 0;
+        cnt += (o.w < mine || (o.w == mine && id + 3 < i)) ? 1 : 0;
+    }
+    part[threadIdx.x] = cnt;
+    __syncthreads();
+    if (quarter == 0 && i < G)
+        a.rank_part[(int64_t)tile * G + i] =
+            part[li] + part[li + kWave] + part[li + 2 * kWave] + part[li + 3 * kWave];
+}
+
+// Group records, and each group at its rank (the sum of its partial counts)
+// in the SLO order.
+__global__ __launch_bounds__(kThreads) void k_srankout(SearchArgs a, int ntiles)
+{
+    const int i = blockIdx.x * kThreads + threadIdx.x;
+    if (i >= a.G) return;
+    int r = 0;
+    for (int t = 0; t < ntiles; ++t) r += a.rank_part[(int64_t)t * a.G + i];
+    a.by_slo[r] = i;
+    a.grec[i] = group_record(a, i);
+}
+
+// Group records only (when no screen runs).
+__global__ __launch_bounds__(kThreads) void k_sgrec(SearchArgs a)
+{
+    const int i = blockIdx.x * kThreads + threadIdx.x;
+    if (i >= a.G) return;
+    a.grec[i] = group_record(a, i);
 }
 
 // The normal-tail table, once per call, for the screens to copy into LDS.
@@ -1717,7 +1730,7 @@ size_t align256(size_t v) { return (v + 255) / 256 * 256; }
 struct Layout {
     int nwg_a, nwg_b, nwg, nwg_f, nws;
     int64_t n_moves;
-    size_t grec, by_slo, perm, flag, qof, inv, srec, sst, trec, R, RD, Q, Nq, Es, T, cur, done, steps,
+    size_t grec, by_slo, rank_part, perm, flag, qof, inv, srec, sst, trec, R, RD, Q, Nq, Es, T, cur, done, steps,
         wmin_s, wmin_i, smin, F, D, cand, cex, ncand, U, scratch, dq, tail, total;
 };
 
@@ -1740,6 +1753,7 @@ Layout layout(int G, int I, int W, int64_t B)
     const size_t nm = (size_t)L.n_moves;
     L.grec = take(sizeof(GRec) * G);
     L.by_slo = take(4 * (size_t)G);
+    L.rank_part = take(4 * (size_t)G * (size_t)((G + kRankTile - 1) / kRankTile));
     L.perm = take(4 * (size_t)G * b);
     L.flag = take((size_t)G * b);
     L.qof = take(4 * (size_t)(I + 1) * b);
@@ -1815,6 +1829,7 @@ SearchArgs search_args(const qlm_problem *pr, int64_t B, int32_t W, unsigned cha
     a.evict_cost = pr->evict_cost;
     a.grec = (GRec *)(ws + L.grec);
     a.by_slo = (int32_t *)(ws + L.by_slo);
+    a.rank_part = (int32_t *)(ws + L.rank_part);
     a.perm = (int32_t *)(ws + L.perm);
     a.flag = ws + L.flag;
     a.qof = (int32_t *)(ws + L.qof);
@@ -1879,8 +1894,16 @@ int search_begin(const qlm_problem *pr, const qlm_plans *pl, int32_t W, void *ws
         hipLaunchKernelGGL(k_sgrec, dim3((a.G + kThreads - 1) / kThreads), dim3(kThreads), 0, stream, a);
         return launched("k_sgrec launch");
     }
-    hipLaunchKernelGGL(k_srank, dim3((a.G + kWave - 1) / kWave), dim3(kThreads), 0, stream, a);
-    rc = launched("k_srank launch");
+    {
+        const int nb = (a.G + kWave - 1) / kWave;
+        const int ntiles = (a.G + kRankTile - 1) / kRankTile;
+        hipLaunchKernelGGL(k_srank, dim3((unsigned)(nb * ntiles)), dim3(kThreads), 0, stream, a);
+        rc = launched("k_srank launch");
+        if (rc) return rc;
+        hipLaunchKernelGGL(k_srankout, dim3((a.G + kThreads - 1) / kThreads), dim3(kThreads), 0,
+                           stream, a, ntiles);
+        rc = launched("k_srankout launch");
+    }
     if (rc) return rc;
     hipLaunchKernelGGL(k_stail, dim3(1), dim3(kThreads), 0, stream, a);
     return launched("k_stail launch");

@@ -156,6 +156,21 @@ def test_screen_bounds_long_queue(qlm, orc):
     print("unbounded: %d; largest error / bound %.3g" % (f, w))
 
 
+def test_screen_bounds_many_groups(qlm, orc):
+    """17,000 groups: the SLO ranks are counted over 17 tiles of 1024 groups,
+    the last one ragged; every move's screened score within its bound of the
+    oracle's."""
+    import torch
+    rng = np.random.default_rng(53)
+    pr, pl = hand_case(rng, G=17000, I=4, P=1)
+    dpr, dpl = device_inputs(pr, pl)
+    F, D = qlm.search_screen(dpr, dpl, 1)
+    torch.cuda.synchronize()
+    ref = orc.move_scores(pr, pl, 0, 1)
+    f, w = _check_screen(F.cpu().numpy()[0], D.cpu().numpy()[0], ref, "many groups")
+    print("unbounded: %d; largest error / bound %.3g" % (f, w))
+
+
 def _check_search(orc, pr, pl, p, W, T, g_trace, g_steps, g_perm, g_qoff, g_ev, g_score):
     """Compares one chain's search with the oracle's; returns the step where a
     near-tie let the two sides part (None when they agree throughout)."""
