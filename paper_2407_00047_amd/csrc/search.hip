@@ -100,6 +100,10 @@ constexpr int kWave = 64;
 constexpr int kThreads = 256;              // every search kernel: 4 wavefronts
 constexpr int kWaves = kThreads / kWave;
 constexpr int kRankTile = 1024;
+constexpr int kSwapStage = 512;              // tail records the removal/swap screen stages
+constexpr int kSwapStageBytes = kSwapStage * 24;   // 16-byte records and 8-byte variances
+constexpr int kSwapRecs = kSwapStageBytes / 32;    // or that many 32-byte slot records
+constexpr int kSwapCostStage = 1024;         // swap-cost entries it stages
 constexpr int kExactBlocks = 64;           // per chain, for the exact re-scores
 constexpr int kStage = 1024;               // tail records staged in LDS at a time
 constexpr int32_t kMaxSearchGroups = 1 << 16;
@@ -147,6 +151,7 @@ struct TRec {
     float vz;
     float n;
 };
+static_assert(sizeof(SRec) == 32 && sizeof(TRec) == 16, "the screens' LDS staging sizes");
 
 struct SearchArgs {
     int32_t G, I, M, C, W;
@@ -830,11 +835,11 @@ __device__ inline double margin_eps(int L) { return (8.0 + 2.0 * L) * 2.22044604
 // for the rounding of its margin sets `force`.
 __device__ inline void screen_visit(Run &r, const SRec &x, double theta, double inv_theta, int cls,
                                     double vscale, double eps_rel, const float2 *tab,
-                                    const SearchArgs &a, bool &force)
+                                    const SearchArgs &a, bool &force, const float *swc = nullptr)
 {
     const int m = (int)(x.nmf & 0xFFu);
     if (r.prev >= 0 && r.prev != m && a.swap_cost)
-        r.K += (double)a.swap_cost[((int64_t)cls * a.M + r.prev) * a.M + m];
+        r.K += (double)(swc ? swc : a.swap_cost)[((int64_t)cls * a.M + r.prev) * a.M + m];
     if (x.nmf & kFlagBit) r.K += (double)a.evict_cost;
     const double slo = (double)x.slo;
     double P;
@@ -871,14 +876,13 @@ __device__ inline const __attribute__((address_space(4))) T *as_const(const T *p
 // `exactv`, (V_u - db) vscale from the double-precision variances (which a
 // removal needs: no cancellation).  The wavefront walks the union of its
 // lanes' ranges in step.  Lanes with on = false add nothing.
-__device__ inline double tail_walk(const TRec *tr, const SSt *ss, const float2 *tab, bool on,
+template <class TrAt, class VAt>
+__device__ inline double tail_walk(const TrAt &tr_at, const VAt &v_at, const float2 *tab, bool on,
                                    int lo, int hi, double dE, float dvz, double db, double vscale,
                                    bool exactv)
 {
     const int ulo = __builtin_amdgcn_readfirstlane((int)wave_min(on ? (double)lo : 1e9));
     const int uhi = __builtin_amdgcn_readfirstlane((int)wave_max(on ? (double)hi : -1.0));
-    const auto ct = as_const(tr);
-    const auto cs = as_const(ss);
     double acc = 0.0;
     int u = ulo;
     if (exactv) {
@@ -887,11 +891,10 @@ __device__ inline double tail_walk(const TRec *tr, const SSt *ss, const float2 *
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
                 const int uu = min(u + j, uhi - 1);
-                const double m = ct[uu].m;
-                const float n = ct[uu].n;
-                const double v = cs[uu].V;
-                const float q = qlm_tail::q_of(tab, (float)(m - dE), (float)((v - db) * vscale));
-                const float w = (on && u + j >= lo && u + j < hi) ? n : 0.0f;
+                const TRec x = tr_at(uu);
+                const double v = v_at(uu);
+                const float q = qlm_tail::q_of(tab, (float)(x.m - dE), (float)((v - db) * vscale));
+                const float w = (on && u + j >= lo && u + j < hi) ? x.n : 0.0f;
                 s32 = fmaf(w, q, s32);
             }
             acc += (double)s32;
@@ -902,10 +905,9 @@ __device__ inline double tail_walk(const TRec *tr, const SSt *ss, const float2 *
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
                 const int uu = min(u + j, uhi - 1);
-                const double m = ct[uu].m;
-                const float vz = ct[uu].vz, n = ct[uu].n;
-                const float q = qlm_tail::q_of(tab, (float)(m - dE), vz + dvz);
-                const float w = (on && u + j >= lo && u + j < hi) ? n : 0.0f;
+                const TRec x = tr_at(uu);
+                const float q = qlm_tail::q_of(tab, (float)(x.m - dE), x.vz + dvz);
+                const float w = (on && u + j >= lo && u + j < hi) ? x.n : 0.0f;
                 s32 = fmaf(w, q, s32);
             }
             acc += (double)s32;
@@ -921,13 +923,44 @@ __global__ __launch_bounds__(kThreads) void k_fswap(SearchArgs a)
 {
     __shared__ float2 tab[qlm_tail::kCells];
     __shared__ double lmin[kWaves];
-    for (int k = threadIdx.x; k < qlm_tail::kCells; k += kThreads) tab[k] = a.tail[k];
-    __syncthreads();
+    __shared__ int lint_lo[kWaves], lint_hi[kWaves];
+    // one buffer: first the slot records the lanes visit, then their tails
+    // (records and variances ahead)
+    __shared__ __align__(16) unsigned char stbuf[kSwapStageBytes];
+    __shared__ float st_c[kSwapCostStage];
+    SRec *st_r = reinterpret_cast<SRec *>(stbuf);
+    TRec *st_t = reinterpret_cast<TRec *>(stbuf);
+    double *st_v = reinterpret_cast<double *>(stbuf + kSwapStage * sizeof(TRec));
     const int64_t b = blockIdx.x / a.nwg_f;
     const int wg = blockIdx.x % a.nwg_f;
-    if (a.done[b]) return;
+    if (a.done[b]) return;                    // the same in the whole workgroup
     const int G = a.G, I = a.I, W = a.W;
     const SRec *__restrict__ sr = a.srec + b * G;
+    // the slots this workgroup's tasks visit, [vlo, vhi): removals t < G visit
+    // t and t + 1, swaps s = (t - G) / W up to W + 1 past s; a workgroup can
+    // hold both kinds
+    const int t0 = wg * kThreads, t1 = min(t0 + kThreads, G + G * W) - 1;
+    int vlo = G, vhi = 0;
+    if (t0 < G) {
+        vlo = t0;
+        vhi = min(t1, G - 1) + 2;
+    }
+    if (t1 >= G) {
+        vlo = min(vlo, (max(t0, G) - G) / W);
+        vhi = max(vhi, (t1 - G) / W + W + 2);
+    }
+    vhi = min(vhi, G);
+    const bool rec_lds = vhi - vlo <= kSwapRecs;
+    const int ncost = a.swap_cost ? a.C * a.M * a.M : 0;
+    const bool cost_lds = ncost <= kSwapCostStage;
+    for (int k = threadIdx.x; k < qlm_tail::kCells; k += kThreads) tab[k] = a.tail[k];
+    if (rec_lds)
+        for (int u = vlo + (int)threadIdx.x; u < vhi; u += kThreads) st_r[u - vlo] = sr[u];
+    if (cost_lds)
+        for (int k = threadIdx.x; k < ncost; k += kThreads) st_c[k] = a.swap_cost[k];
+    __syncthreads();
+    auto rec = [&](int u) { return rec_lds ? st_r[u - vlo] : sr[u]; };
+    const float *swc = cost_lds ? st_c : nullptr;
     const SSt *__restrict__ ss = a.sst + b * G;
     const TRec *__restrict__ tr = a.trec + b * G;
     const int32_t *__restrict__ qof = a.qof + b * (I + 1);
@@ -940,7 +973,7 @@ __global__ __launch_bounds__(kThreads) void k_fswap(SearchArgs a)
     bool on = false, force = false, valid = false;
     double q = 0.0, dE = 0.0, db = 0.0, vscale = 0.0;
     if (removal || swap) {
-        g = (int)sr[s].q;
+        g = (int)min(rec(s).q, (uint32_t)(I - 1));
         const int bq = qof[g];
         eq = qof[g + 1];
         const double theta = (double)a.inst_tput[g];
@@ -956,11 +989,11 @@ __global__ __launch_bounds__(kThreads) void k_fswap(SearchArgs a)
             valid = true;
             q = r.sc;
             if (s + 1 < eq) {
-                screen_visit(r, sr[s + 1], theta, inv_theta, cls, vscale, eps, tab, a, force);
+                screen_visit(r, rec(s + 1), theta, inv_theta, cls, vscale, eps, tab, a, force, swc);
                 q = r.sc;
                 lo = s + 2;
                 if (lo < eq) {
-                    const SRec xs = sr[s];
+                    const SRec xs = rec(s);
                     dE = (r.K - ss[s + 1].K) - xs.a * inv_theta;
                     db = xs.b;
                     // the variance left ahead keeps most of its bits and a spread wide
@@ -974,14 +1007,14 @@ __global__ __launch_bounds__(kThreads) void k_fswap(SearchArgs a)
             }
         } else if (s + d < eq) {
             valid = true;
-            screen_visit(r, sr[s + d], theta, inv_theta, cls, vscale, eps, tab, a, force);
+            screen_visit(r, rec(s + d), theta, inv_theta, cls, vscale, eps, tab, a, force, swc);
             for (int u = s + 1; u < s + d; ++u)
-                screen_visit(r, sr[u], theta, inv_theta, cls, vscale, eps, tab, a, force);
-            screen_visit(r, sr[s], theta, inv_theta, cls, vscale, eps, tab, a, force);
+                screen_visit(r, rec(u), theta, inv_theta, cls, vscale, eps, tab, a, force, swc);
+            screen_visit(r, rec(s), theta, inv_theta, cls, vscale, eps, tab, a, force, swc);
             q = r.sc;
             const int u1 = s + d + 1;
             if (u1 < eq) {
-                screen_visit(r, sr[u1], theta, inv_theta, cls, vscale, eps, tab, a, force);
+                screen_visit(r, rec(u1), theta, inv_theta, cls, vscale, eps, tab, a, force, swc);
                 q = r.sc;
                 lo = u1 + 1;
                 if (lo < eq) {
@@ -1000,7 +1033,24 @@ __global__ __launch_bounds__(kThreads) void k_fswap(SearchArgs a)
         }
     }
     const bool exactv = __ballot(on && removal) != 0;
-    q += tail_walk(tr, ss, tab, on, lo, eq, dE, 0.0f, db, vscale, exactv);
+    // the tails of the workgroup's lanes lie in one range of slots: staged in
+    // LDS (records and variances ahead) when it fits, so that the walks read
+    // no global memory
+    const int wlo = block_min_int(on ? lo : INT_MAX, lint_lo);
+    const int whi = -block_min_int(on ? -eq : 0, lint_hi);
+    const bool staged = wlo < whi && whi - wlo <= kSwapStage;
+    if (staged)
+        for (int u = wlo + (int)threadIdx.x; u < whi; u += kThreads) {
+            st_t[u - wlo] = tr[u];
+            st_v[u - wlo] = ss[u].V;
+        }
+    __syncthreads();
+    if (staged)
+        q += tail_walk([&](int u) { return st_t[u - wlo]; }, [&](int u) { return st_v[u - wlo]; },
+                       tab, on, lo, eq, dE, 0.0f, db, vscale, exactv);
+    else
+        q += tail_walk([&](int u) { return tr[u]; }, [&](int u) { return ss[u].V; }, tab, on, lo,
+                       eq, dE, 0.0f, db, vscale, exactv);
     double F = INFINITY, D = 0.0;
     if (valid) {
         const double nq = a.Nq[b * I + g];

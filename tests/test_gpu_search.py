@@ -156,6 +156,24 @@ def test_screen_bounds_long_queue(qlm, orc):
     print("unbounded: %d; largest error / bound %.3g" % (f, w))
 
 
+@pytest.mark.parametrize("kw", [dict(G=600, I=3, P=2, W=500),
+                                dict(G=300, I=5, P=2, M=20, C=3, W=8)],
+                         ids=["window 500", "1200 swap costs"])
+def test_screen_bounds_unstaged(qlm, orc, kw):
+    """The removal and swap screen stages its lanes' slot records (up to 384
+    slots) and the swap-cost table (up to 1024 entries) in LDS: a window of 500
+    takes the records from global memory, 20 models in 3 classes the costs;
+    every move's screened score within its bound of the oracle's."""
+    import torch
+    pr, pl, W = _case(kw)
+    dpr, dpl = device_inputs(pr, pl)
+    F, D = qlm.search_screen(dpr, dpl, W)
+    torch.cuda.synchronize()
+    F, D = F.cpu().numpy(), D.cpu().numpy()
+    for p in range(pl["n_plans"]):
+        _check_screen(F[p], D[p], orc.move_scores(pr, pl, p, W), (kw, p))
+
+
 def test_screen_bounds_many_groups(qlm, orc):
     """17,000 groups: the SLO ranks are counted over 17 tiles of 1024 groups,
     the last one ragged; every move's screened score within its bound of the
