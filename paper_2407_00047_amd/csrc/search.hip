@@ -398,17 +398,19 @@ __device__ void block_best(double &s, int64_t &k, double *ls, int64_t *lk)
 // cost leaves a sum unchanged).  out(v, x, A, V, K, C, E) receives each
 // position's sums on entry, its score ahead C and its E[W] (in the lane that
 // holds the position).
-template <class RecOf, class Out>
-__device__ void wave_walk(Run &r, int nv, const RecOf &rec, double theta, int cls,
-                          const SearchArgs &a, const Out &out)
+// wave_walk_rounds takes each round's records from load(v0, on), called in
+// every lane (on: the lane holds position v0 + lane), so that a loader can
+// form them with wavefront operations.
+template <class LoadRound, class Out>
+__device__ void wave_walk_rounds(Run &r, int nv, const LoadRound &load, double theta, int cls,
+                                 const SearchArgs &a, const Out &out)
 {
     const int lane = threadIdx.x & (kWave - 1);
     const double ecost = (double)a.evict_cost;
     for (int v0 = 0; v0 < nv; v0 += kWave) {
         const int cnt = min(kWave, nv - v0);
         const bool on = lane < cnt;
-        SRec x{};
-        if (on) x = rec(v0 + lane);
+        const SRec x = load(v0, on);
         const int m = (int)(x.nmf & 0xFFu);
         int pm = __shfl_up(m, 1, kWave);
         if (lane == 0) pm = r.prev;
@@ -462,6 +464,18 @@ __device__ void wave_walk(Run &r, int nv, const RecOf &rec, double theta, int cl
         r.prev = __builtin_amdgcn_readlane(m, last);
         if (on) out(v0 + lane, x, A, V, K, C, E);
     }
+}
+
+template <class RecOf, class Out>
+__device__ void wave_walk(Run &r, int nv, const RecOf &rec, double theta, int cls,
+                          const SearchArgs &a, const Out &out)
+{
+    const int lane = threadIdx.x & (kWave - 1);
+    wave_walk_rounds(r, nv, [&](int v0, bool on) {
+        SRec x{};
+        if (on) x = rec(v0 + lane);
+        return x;
+    }, theta, cls, a, out);
 }
 
 struct NoOut {
@@ -621,21 +635,26 @@ __global__ __launch_bounds__(kThreads) void k_sstate(SearchArgs a, int force)
     TRec *__restrict__ tr = a.trec + b * G;
     int32_t *__restrict__ inv = a.inv + b * G;
     const int bq = a.qof[b * (I + 1) + g], eq = a.qof[b * (I + 1) + g + 1];
-    // slot records, with the running maximum of the SLOs
+    const double theta = (double)a.inst_tput[g];
+    const int cls = clampi(a.inst_class[g], 0, a.C - 1);
+    const double vscale = qlm_tail::kVarScale / (theta * theta);
+    // each round's slot records (with the running maximum of the SLOs) are
+    // formed, stored, and walked at once: the exact running sums and the
+    // screens' margins
     float pm = -INFINITY;
-    for (int u0 = bq; u0 < eq; u0 += kWave) {
-        const int u = u0 + lane;
+    auto load = [&](int v0, bool on) {
+        const int u = bq + v0 + lane;
         SRec x{};
         float mx = -INFINITY;
-        if (u < eq) {
+        if (on) {
             const int i = perm[u];
-            const GRec r = a.grec[i];
-            x.a = r.a;
-            x.b = r.b;
-            x.slo = r.slo;
-            x.nmf = r.nm | (flag[u] ? kFlagBit : 0u);
+            const GRec gr = a.grec[i];
+            x.a = gr.a;
+            x.b = gr.b;
+            x.slo = gr.slo;
+            x.nmf = gr.nm | (flag[u] ? kFlagBit : 0u);
             x.q = (uint32_t)g;
-            mx = r.slo;
+            mx = gr.slo;
             inv[i] = u;
         }
         for (int o = 1; o < kWave; o <<= 1) {
@@ -644,16 +663,13 @@ __global__ __launch_bounds__(kThreads) void k_sstate(SearchArgs a, int force)
         }
         mx = pm > mx ? pm : mx;
         x.pmax = mx;
-        if (u < eq) sr[u] = x;
+        if (on) sr[u] = x;
         pm = __shfl(mx, kWave - 1, kWave);
-    }
-    // the exact running sums and the screens' margins
-    const double theta = (double)a.inst_tput[g];
-    const int cls = clampi(a.inst_class[g], 0, a.C - 1);
-    const double vscale = qlm_tail::kVarScale / (theta * theta);
+        return x;
+    };
     Run r{0.0, 0.0, 0.0, 0.0, model0_of(a, g)};
     double nsum = 0.0, emax = 0.0;
-    wave_walk(r, eq - bq, [&](int v) { return sr[bq + v]; }, theta, cls, a,
+    wave_walk_rounds(r, eq - bq, load, theta, cls, a,
               [&](int v, const SRec &x, double A, double V, double K, double C, double E) {
                   const int u = bq + v;
                   ss[u] = SSt{A, V, K, C};
