@@ -28,6 +28,10 @@ SEARCH_METRIC = "plan-search moves scored/sec (screened + exact best) and % of V
 # MI355X vector issue: 256 CUs x 4 SIMDs, one wave64 VALU instruction per SIMD
 # every 4 cycles (16 lanes a cycle) at 2.4 GHz.
 PEAK_VALU_LANES = 256 * 4 * 16 * 2.4e9
+# VALU instructions per slot in k_score's unrolled 32-slot block (gfx950 code of
+# the benchmarked variant, eviction words on; the queue-head path and the
+# per-block work excluded)
+VALU_PER_SLOT = 26
 # VALU instructions per visited position in the main loop of the reassignment
 # screen (k_fmove), counted in its compiled loop body.
 VALU_PER_VISIT = 13
@@ -598,6 +602,13 @@ def main():
                 "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
                 "traffic": traffic, "kernel": "k_score", "kernel_avg_ms": round(k_avg_ms, 4),
                 "algorithmic_bytes_per_launch": bpp * P}
+    # the same kernel against its VALU issue bound (slot visits per second)
+    slots = P * pr["n_groups"]
+    s_achieved = slots / (k_avg_ms / 1e3) / 1e9
+    s_peak = PEAK_VALU_LANES / VALU_PER_SLOT / 1e9
+    valu_issue = {"bound": "alu", "achieved": round(s_achieved, 1), "peak": round(s_peak, 1),
+                  "unit": "Gslots/s", "frac": round(s_achieved / s_peak, 4), "kernel": "k_score",
+                  "slots_per_launch": slots, "valu_per_slot": VALU_PER_SLOT}
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -618,7 +629,7 @@ def main():
                    "requests": N},
         "requests_per_s": round(plans_per_s * N, 1),
         "best_index": best_index, "best_score": best_score,
-        "roofline": roofline, "cpu_baseline": cpu,
+        "roofline": roofline, "valu_issue": valu_issue, "cpu_baseline": cpu,
     }
     if args.with_profile:
         out["config"]["workload"] += ", tables from a hardware profile"
