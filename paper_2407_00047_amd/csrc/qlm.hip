@@ -776,13 +776,13 @@ struct ExactArgs {
 // n var ahead, costs K) ripple from lane to lane in position order, so every
 // lane holds the same sums a serial walk forms at its position.  Each lane
 // then forms its position's E[W], SD and term n P, and the terms ripple into
-// the queue's sum the same way, one round later (in the steps of the next
-// round's running sums).  A ripple always takes 63 steps: lanes beyond the
-// queue's end hold zeros, which leave every sum unchanged, and the code has
-// no branch between steps.  Loads run ahead: the next round's group fields
-// and swap costs, and the group ids of the round after.  Returns the queue's
-// score in every lane.  Group ids are clamped to [0, G), offsets to [0, G]
-// (malformed plans never read out of bounds).
+// the queue's sum the same way.  A ripple takes the round's positions less
+// one steps, rounded up to blocks of 8 (a step past the last position leaves
+// every position's sums unchanged), with the count in a scalar register so
+// that only a block ends in a branch.  Loads run ahead: the next round's group
+// fields and swap costs, and the group ids of the round after.  Returns the
+// queue's score in every lane.  Group ids are clamped to [0, G), offsets to
+// [0, G] (malformed plans never read out of bounds).
 struct RoundIn {
     int m;                    // model (0 where the lane holds no position)
     uint32_t n;               // requests (0 where none)
@@ -830,11 +830,9 @@ __device__ double wave_queue_exact(const ExactArgs &a, int64_t p, int g)
     int i2 = ids(bq + kWave);
     float sw = swap_in(f, i0 >= 0);
     double rA = 0.0, rV = 0.0, rK = 0.0, rC = 0.0;
-    double tprev = 0.0;       // the previous round's terms (none before the first)
     for (int v0 = bq; v0 < eq; v0 += kWave) {
         const int cnt = min(kWave, eq - v0);
         const bool on = lane < cnt;
-        // next round's fields, the ids of the round after
         const int i1 = i2;
         const RoundIn f1 = fields(i1, v0 + kWave);
         i2 = ids(v0 + 2 * kWave);
@@ -845,17 +843,17 @@ __device__ double wave_queue_exact(const ExactArgs &a, int64_t p, int g)
         const double c2 = (on && ((f.ev >> ((v0 + lane) & 31)) & 1u)) ? ecost : 0.0;
         const double la = from_left0(xa), lb = from_left0(xb);
         const double l1 = from_left0(c1), l2 = from_left0(c2);
-        const double lt = from_left0(tprev);
-        double A = rA, V = rV, K = rK, C = rC;
+        double A = rA, V = rV, K = rK;
+        const int steps = __builtin_amdgcn_readfirstlane(cnt - 1);
+        for (int j = 0; j < steps; j += 8) {
 #pragma unroll
-        for (int j = 1; j < kWave; ++j) {
-            A = from_left(A) + la;
-            V = from_left(V) + lb;
-            K = (from_left(K) + l1) + l2;
-            C = from_left(C) + lt;
+            for (int u = 0; u < 8; ++u) {
+                A = from_left(A) + la;
+                V = from_left(V) + lb;
+                K = (from_left(K) + l1) + l2;
+            }
         }
-        rC = lane_value(C, kWave - 1) + lane_value(tprev, kWave - 1);
-        K = K + c1;               // this position's swap, then its eviction
+        K = K + c1;
         K = K + c2;
         const double EW = A / theta + K;
         const double SD = sqrt(V) / theta;
@@ -865,20 +863,21 @@ __device__ double wave_queue_exact(const ExactArgs &a, int64_t p, int g)
             P = 0.5 * erfc((slo - EW) / (SD * 1.4142135623730951));
         else
             P = (EW > slo) ? 1.0 : 0.0;
-        tprev = on ? n * P : 0.0;
-        rA = lane_value(A, kWave - 1) + lane_value(xa, kWave - 1);
-        rV = lane_value(V, kWave - 1) + lane_value(xb, kWave - 1);
-        rK = lane_value(K, kWave - 1);
-        prev = __builtin_amdgcn_readlane(f.m, cnt - 1);
+        const double term = on ? n * P : 0.0;
+        const double lt = from_left0(term);
+        double C = rC;
+        for (int j = 0; j < steps; j += 8) {
+#pragma unroll
+            for (int u = 0; u < 8; ++u) C = from_left(C) + lt;
+        }
+        const int last = cnt - 1;
+        rA = lane_value(A, last) + lane_value(xa, last);
+        rV = lane_value(V, last) + lane_value(xb, last);
+        rK = lane_value(K, last);
+        rC = lane_value(C, last) + lane_value(term, last);
+        prev = __builtin_amdgcn_readlane(f.m, last);
         f = f1;
         sw = swap_in(f, i1 >= 0);
-    }
-    if (eq > bq) {            // the last round's terms
-        const double lt = from_left0(tprev);
-        double C = rC;
-#pragma unroll
-        for (int j = 1; j < kWave; ++j) C = from_left(C) + lt;
-        rC = lane_value(C, kWave - 1) + lane_value(tprev, kWave - 1);
     }
     return rC;
 }
