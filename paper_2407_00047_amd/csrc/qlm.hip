@@ -66,11 +66,20 @@ constexpr int kMaxScoreBlocks = 4096;
 // Row offsets of a block's prefetch (up to 67 rows of 4 * plan_stride bytes)
 // are 32-bit register operands.
 constexpr int64_t kMaxPlanStride = 1 << 22;
-// Request counts share the 32-bit record word with the model's cost-table
-// column (bits 3..10), so they are 21-bit.
+// Request counts are 21-bit (the interface's limit).
 constexpr uint32_t kCountMask = (1u << 21) - 1u;
-constexpr int kCountShift = 11;
-constexpr uint32_t kColMask = 0x7F8u;     // model * 8: byte column of the cost table
+// Compact group records of the scoring kernel's fast path (see stage_compact):
+// counts up to 2048 ride as half-precision numbers in the low 16 bits of the
+// double n mu, models below 64 in the low 6 bits of the single-precision
+// variance.
+constexpr uint32_t kCompactCountMax = 2048u;
+constexpr int kCompactModels = 64;
+constexpr uint32_t kModelBits = 63u;
+// The fast path finds a cost entry's eviction twin 2^10 doubles (8 KiB) on.
+constexpr int kTwinShift = 10;
+constexpr uint32_t kTwinEntries = 1u << kTwinShift;
+// General records (the exact walk): the count above the model's 8 bits.
+constexpr int kGenCountShift = 8;
 
 // Screening error bound per request: the tabulated tail (below 2.2e-6),
 // single-precision rounding of the standardised margin and of the block-wise
@@ -93,6 +102,7 @@ struct ScoreArgs {
     int32_t G, I, M, C;
     int32_t col_shift;        // log2(entries per cost-table row)
     int32_t ev_shift;         // log2(bytes from a cost entry to its evicted twin)
+    int32_t fast_ok;          // the fast path's shape conditions hold (M <= 64, twin at 8 KiB)
     uint32_t lut_bytes;       // bytes of the cost table (both halves), multiple of 16
     const int32_t *grp_count;
     const float *grp_mu, *grp_var, *grp_slo;
@@ -117,15 +127,19 @@ __device__ inline int clampi(int v, int lo, int hi) { return v < lo ? lo : (v > 
 
 // LDS of the scoring kernel.  The normal-tail table is a static array (8 KiB at
 // the start of LDS).  Dynamic part, byte addresses from `base`:
-//   group table   16 (G + 1) bytes: group i -> {mu, n var / kTailScale^2, slo,
-//                 (n << 11) | (model << 3)}; entry G is an all-zero record
-//                 (clamped out-of-range ids land there)
+//   group table   16 (G + 1) bytes, one record per group, in one of two forms
+//                 (the same for every workgroup of a launch):
+//                   compact (fast path): {n mu as a double whose low 16 bits
+//                   hold n, slo, n var / kTailScale^2 as a float whose low 6
+//                   bits hold the model}
+//                   general (exact walk): {mu, var, slo, (n << 8) | model}
+//                 Entry G is an all-zero record (clamped out-of-range ids land
+//                 there).
 //   cost table    lut_bytes of doubles.  Row r = c (M + 1) + previous model
 //                 (previous = M: none loaded) starts at byte r << (col_shift + 3);
 //                 its entry at + model * 8 holds the seconds of swapping to
 //                 `model` on class c (0 for the same model or none loaded).  The
-//                 twin at + (1 << ev_shift) adds the eviction cost.  A row offset is
-//                 the previous model's column offset shifted by col_shift.
+//                 twin at + (1 << ev_shift) adds the eviction cost.
 //   instances     16 bytes each: theta (double), the cost-table row base of its
 //                 class, the row of its head (initial model, or none)
 //   scratch       16 doubles for workgroup reductions
@@ -158,21 +172,46 @@ __device__ inline T *lds_ptr(uint32_t addr)
     return (T *)((__attribute__((address_space(3))) T *)(uintptr_t)addr);
 }
 
-__device__ void stage_tables(const ScoreArgs &a, const Lds &l)
+// Bit b of w moved to bit kTwinShift (other bits arbitrary): for b >= 10 a
+// right shift of the word, below that a left shift of its low half (16-bit
+// shifts keep the short issue form; b is a constant in the unrolled blocks).
+__device__ inline uint32_t twin_bit(uint32_t w, uint32_t b)
 {
-    uint4 *grp = lds_ptr<uint4>(l.grp);
-    for (int i = threadIdx.x; i <= a.G; i += blockDim.x) {
-        uint4 r = make_uint4(0u, 0u, 0u, 0u);
-        if (i < a.G) {
-            const uint32_t n = (uint32_t)clampi(a.grp_count[i], 0, (int)kCountMask);
-            const uint32_t m = (uint32_t)clampi(a.grp_model[i], 0, a.M - 1);
-            r.x = __float_as_uint(a.grp_mu[i]);
-            r.y = __float_as_uint((float)((double)n * (double)a.grp_var[i] * kVarScale));
-            r.z = __float_as_uint(a.grp_slo[i]);
-            r.w = (n << kCountShift) | (m << 3);
-        }
-        grp[i] = r;
-    }
+    if (b >= (uint32_t)kTwinShift) return w >> (b - kTwinShift);
+    return (uint32_t)(uint16_t)((uint16_t)w << (kTwinShift - b));
+}
+
+// Fields of a compact group record (stage_compact).
+__device__ inline double rec_nmu(const uint4 r)
+{
+    return __longlong_as_double((long long)(((uint64_t)r.y << 32) | r.x));
+}
+__device__ inline float rec_slo(const uint4 r) { return __uint_as_float(r.z); }
+__device__ inline float rec_nv(const uint4 r) { return __uint_as_float(r.w); }
+__device__ inline uint32_t rec_model(uint32_t w) { return w & kModelBits; }
+// S + n * p, n the record's count (the half-precision low half of x); the
+// compiler forms it as one v_fma_mix_f32, which widens the half on the way in.
+__device__ inline float fma_count(uint32_t x, float p, float S)
+{
+    return fmaf((float)__builtin_bit_cast(_Float16, (uint16_t)(x & 0xFFFFu)), p, S);
+}
+
+// Makes v opaque to the optimizer, in a vector register (no instruction): keeps
+// a uniform value out of scalar operands, and a sum from being regrouped.
+template <typename T>
+__device__ inline T in_vgpr(T v)
+{
+    asm volatile("" : "+v"(v));
+    return v;
+}
+
+// Cost table and instance records.  Returns whether every cost entry has at
+// most 29 significant bits (the low 24 bits of its mantissa clear), so that
+// its product with any single-precision throughput is exact in double
+// precision; the fast path needs that at queue heads (below).
+__device__ bool stage_costs(const ScoreArgs &a, const Lds &l)
+{
+    bool ok = true;
     double *lut = lds_ptr<double>(l.lut);
     const int Mp = 1 << a.col_shift;
     const int rows = a.M + 1;
@@ -192,6 +231,7 @@ __device__ void stage_tables(const ScoreArgs &a, const Lds &l)
             if (ev) v += (double)a.evict_cost;
         }
         lut[w] = v;
+        ok = ok && ((uint64_t)__double_as_longlong(v) & 0xFFFFFFull) == 0;
     }
     const uint32_t row_bytes = 8u << a.col_shift;
     for (int g = threadIdx.x; g < a.I; g += blockDim.x) {
@@ -205,6 +245,58 @@ __device__ void stage_tables(const ScoreArgs &a, const Lds &l)
         r.z = cb;
         r.w = cb + (uint32_t)(m0 >= 0 ? m0 : a.M) * row_bytes;
         lds_ptr<uint4>(l.inst)[g] = r;
+    }
+    return ok;
+}
+
+// Compact group records of the fast path.  n mu is exact in double precision
+// and, for n <= 2048, fills at most 36 of its 53 significand bits, so the low
+// 16 bits are free and carry n as a half-precision number (exact up to 2048):
+// the value read back differs from n mu by less than 2^-36 of it.  The scaled
+// variance is rounded to single precision and its low 6 mantissa bits carry
+// the model, which moves it by less than 2^-17 of itself.  Returns whether this
+// thread's groups fit the form: 0 < n <= 2048, a variance that is a normal
+// single-precision number (so every position after a queue head has SD > 0),
+// and a model below 64.
+__device__ bool stage_compact(const ScoreArgs &a, const Lds &l)
+{
+    bool ok = a.fast_ok != 0;
+    uint4 *grp = lds_ptr<uint4>(l.grp);
+    for (int i = threadIdx.x; i <= a.G; i += blockDim.x) {
+        uint4 r = make_uint4(0u, 0u, 0u, 0u);
+        if (i < a.G) {
+            const uint32_t n = (uint32_t)clampi(a.grp_count[i], 0, (int)kCountMask);
+            const uint32_t m = (uint32_t)clampi(a.grp_model[i], 0, a.M - 1);
+            const uint64_t nm = (uint64_t)__double_as_longlong((double)n * (double)a.grp_mu[i]);
+            const float nv = (float)((double)n * (double)a.grp_var[i] * kVarScale);
+            ok = ok && n >= 1u && n <= kCompactCountMax && nv >= 1.17549435e-38f &&
+                 nv <= 3.4028235e38f;
+            const uint32_t nh = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)(float)min(n, kCompactCountMax));
+            r.x = ((uint32_t)nm & 0xFFFF0000u) | nh;
+            r.y = (uint32_t)(nm >> 32);
+            r.z = __float_as_uint(a.grp_slo[i]);
+            r.w = (__float_as_uint(nv) & ~kModelBits) | (m & kModelBits);
+        }
+        grp[i] = r;
+    }
+    return ok;
+}
+
+// General group records of the exact walk: {mu, var, slo, (n << 8) | model}.
+__device__ void stage_general(const ScoreArgs &a, const Lds &l)
+{
+    uint4 *grp = lds_ptr<uint4>(l.grp);
+    for (int i = threadIdx.x; i <= a.G; i += blockDim.x) {
+        uint4 r = make_uint4(0u, 0u, 0u, 0u);
+        if (i < a.G) {
+            const uint32_t n = (uint32_t)clampi(a.grp_count[i], 0, (int)kCountMask);
+            const uint32_t m = (uint32_t)clampi(a.grp_model[i], 0, a.M - 1);
+            r.x = __float_as_uint(a.grp_mu[i]);
+            r.y = __float_as_uint(a.grp_var[i]);
+            r.z = __float_as_uint(a.grp_slo[i]);
+            r.w = (n << kGenCountShift) | m;
+        }
+        grp[i] = r;
     }
 }
 
@@ -225,6 +317,110 @@ __device__ inline double wave_min(double v)
     return v;
 }
 
+#pragma clang fp contract(off)
+// The exact walk of the scoring kernel, taken when the group records are in
+// the general form (a group with no requests or no variance, a count of 2^13
+// or more, 65 models or more, or a cost whose product with a throughput may
+// round).  One lane walks its plan's slots in order and forms the running sums
+// as the definition reads them: the tokens and the variance ahead as exact
+// products n mu and n var added in position order, the swap and then the
+// eviction seconds added one by one.  At a position whose variance ahead is
+// zero, P compares A / theta + K with the SLO in exactly that arithmetic, so
+// the indicator is the one the definition gives; where the scaled variance is
+// too small for single precision, P is the double-precision erfc; elsewhere
+// it comes from the tail table as in the fast path.
+template <bool EVICT, bool PEN, bool DETAIL>
+__device__ void walk_general(const ScoreArgs &a, const Lds &L, uint32_t tail0, int64_t tb, int lp,
+                             bool det, int64_t dq, double &S_out, double &PE_out)
+{
+    const int G = a.G;
+    const int I1 = a.I - 1;
+    const int64_t ld4 = a.ld * 4;
+    const uint32_t lpb = (uint32_t)lp * 4u;
+    const uint32_t row_bytes = 8u << a.col_shift;
+    auto at = [&](const void *base, int row) __attribute__((always_inline)) {
+        const unsigned char *rp =
+            reinterpret_cast<const unsigned char *>(base) + (int64_t)row * ld4 + tb * 4;
+        return *reinterpret_cast<const uint32_t *>(rp + lpb);
+    };
+    const double ecost = (double)a.evict_cost;
+    double A = 0.0, K = 0.0, V = 0.0, S = 0.0, PE = 0.0;
+    double theta = 1.0, inv_theta = 1.0;
+    uint32_t cbase = 0u, rowb = 0u;   // class row base; cost row of the slot before
+    int g = -1, nb = 0;               // current queue, the slot where the next starts
+    for (int s0 = 0; s0 < G; s0 += 8) {
+        uint32_t id[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) id[k] = at(a.perm, min(s0 + k, G - 1));
+        const uint32_t evw = EVICT ? at(a.evict, s0 >> 5) : 0u;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const int s = s0 + k;
+            if (s >= G) break;
+            if (s == nb) {
+                // the queue holding slot s: the next one not empty
+                int h = g, e_nb;
+                do {
+                    ++h;
+                    e_nb = h >= I1 ? INT_MAX : (int)at(a.qoff, h + 1);
+                } while (e_nb <= s && h < I1);
+                g = h;
+                nb = e_nb;
+                const uint4 ir = *lds_ptr<const uint4>(L.inst + 16u * (uint32_t)g);
+                theta = __longlong_as_double((long long)(((uint64_t)ir.y << 32) | ir.x));
+                inv_theta = 1.0 / theta;
+                cbase = ir.z;
+                rowb = ir.w;
+                A = 0.0;
+                K = 0.0;
+                V = 0.0;
+            }
+            const uint4 r = *lds_ptr<const uint4>((min(id[k], (uint32_t)G) << 4) + L.grp);
+            const double mu = (double)__uint_as_float(r.x);
+            const double var = (double)__uint_as_float(r.y);
+            const float slo = __uint_as_float(r.z);
+            const double n = (double)(r.w >> kGenCountShift);
+            const uint32_t m = r.w & 255u;
+            K = K + *lds_ptr<const double>(rowb + (m << 3));    // swap (0 when none)
+            if (EVICT && ((evw >> (s & 31)) & 1u)) K = K + ecost;
+            const double Yg = fma(K, theta, A);                  // theta E[W]
+            const double num = fma((double)slo, theta, -Yg);     // theta (slo - E[W])
+            const float vz = (float)(V * kVarScale);
+            float prob;
+            if (vz >= 1.17549435e-38f) {
+                const float rs = __builtin_amdgcn_rsqf(vz);
+                float tt = fmaf(-(float)num, rs, kTailMid);
+                tt = __builtin_amdgcn_fmed3f(tt, kTailLo, kTailHi);
+                const float2 c =
+                    *lds_ptr<const float2>(tail0 + ((__float_as_uint(tt) & kTailCellBits) >> 10));
+                prob = fmaf(c.y, tt, c.x);
+            } else {
+                const double EW = A / theta + K;
+                if (V > 0.0) {
+                    const double SD = sqrt(V) / theta;
+                    prob = (float)(0.5 * erfc(((double)slo - EW) / (SD * 1.4142135623730951)));
+                } else {
+                    prob = EW > (double)slo ? 1.0f : 0.0f;
+                }
+            }
+            S = fma(n, (double)prob, S);
+            if (PEN) PE = fma(-num, inv_theta, PE);
+            if (DETAIL && det) {
+                const int64_t o = (int64_t)s * a.d_count + dq;
+                if (a.d_mean) a.d_mean[o] = (float)(Yg * inv_theta);
+                if (a.d_sd) a.d_sd[o] = (float)(sqrt(V) * inv_theta);
+                if (a.d_prob) a.d_prob[o] = prob;
+            }
+            A = A + n * mu;
+            V = V + n * var;
+            rowb = cbase + m * row_bytes;
+        }
+    }
+    S_out = S;
+    PE_out = PE;
+}
+#pragma clang fp contract(on)
+
 // Screening score of every plan.  One lane = one plan; the slots of a plan are
 // walked in order, so every prefix sum is a running sum.  Per slot: the
 // group's record (one LDS gather), the tokens ahead and the swap/eviction
@@ -238,8 +434,20 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
     __shared__ __align__(16) float2 s_tail[kTailCells];
     extern __shared__ __align__(16) unsigned char lds[];
     const Lds L = lds_layout(a, lds);
-    stage_tables(a, L);
     stage_tail(s_tail);
+    // The form of the group records: compact when every group, model and cost
+    // fits it, else general (and every plan takes the exact walk).  Every
+    // workgroup stages the same tables, so all take the same decision.  (The
+    // flag goes through LDS and readfirstlane, so that the compiler knows it is
+    // uniform: the fast path's scalar row addressing depends on that.)
+    __shared__ int s_compact;
+    if (threadIdx.x == 0) s_compact = 1;
+    __syncthreads();
+    const bool fits = stage_costs(a, L) & stage_compact(a, L);
+    if (!fits) s_compact = 0;
+    __syncthreads();
+    const bool compact = __builtin_amdgcn_readfirstlane(s_compact) != 0;
+    if (!compact) stage_general(a, L);
     double *red = lds_ptr<double>(L.red);
     if (a.wg_nsum && blockIdx.x == 0) {
         if (threadIdx.x == 0 && a.ncand) *a.ncand = 0;
@@ -268,10 +476,13 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
     const int wpb = blockDim.x / kWave;
     const int64_t ntiles = (a.P + kWave - 1) / kWave;
     const int G = a.G;
+    // G held in a vector register (a scalar operand would cost the gather's
+    // clamp its short issue form)
+    const uint32_t Gv = in_vgpr((uint32_t)G);
     const int I1 = a.I - 1;
     const int64_t ld = a.ld;
     const int ev_shift = a.ev_shift;
-    const int col_shift = a.col_shift;
+    const int cs3 = a.col_shift + 3;          // log2(bytes per cost-table row)
     double lane_min = INFINITY;
 
     // When a.split < G every tile (64 plans) is scored by two wavefronts of the
@@ -286,6 +497,27 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
     const bool back = halves && (wave & 1);
     const int s_begin = back ? a.split : 0;
     const int s_end = halves && !back ? a.split : G;
+    if (!compact) {
+      // General records: the front wavefront of each tile walks the whole plan
+      // exactly (walk_general); the back one, if any, idles.
+      for (int64_t r0 = (int64_t)blockIdx.x * per_round; r0 < ntiles;
+           r0 += (int64_t)gridDim.x * per_round) {
+        const int64_t t = r0 + in_round;
+        if (back || t >= ntiles) continue;
+        const int64_t tb = t * kWave;
+        const bool live = tb + lane < a.P;
+        const int lp = live ? lane : (int)(a.P - 1 - tb);
+        const int64_t p = tb + lp;
+        const bool det = DETAIL && live && p >= a.d_begin && p < a.d_begin + a.d_count;
+        double S = 0.0, PE = 0.0;
+        walk_general<EVICT, PEN, DETAIL>(a, L, tail0, tb, lp, det, p - a.d_begin, S, PE);
+        if (live) {
+          a.score[p] = S;
+          if (PEN) a.penalty[p] = PE;
+          lane_min = fmin(lane_min, S);
+        }
+      }
+    } else
     for (int64_t r0 = (int64_t)blockIdx.x * per_round; r0 < ntiles; r0 += (int64_t)gridDim.x * per_round) {
       const int64_t t = r0 + in_round;
       double S_out = 0.0, PE_out = 0.0;
@@ -347,10 +579,14 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
 
         // Issued for every lane, never under a per-lane condition (clamped
         // index), so that the compiler counts the outstanding loads exactly.
+        // (the lane's queue-offset column: one 32 x 32 -> 64-bit multiply-add
+        // per row; plan_stride <= 2^22 keeps the row pitch within 32 bits)
+        const unsigned char *qcol = reinterpret_cast<const unsigned char *>(a.qoff) + tb * 4 + lpb;
+        const uint32_t ld4u = (uint32_t)ld4;
         auto load_qp = [&](int h) __attribute__((always_inline)) {
-            h = min(max(h, 0), I1);
+            h = min(h, I1);                   // g >= 0 wherever this is called
             QP q;
-            q.nb = (int)at(a.qoff, h + 1);
+            q.nb = (int)*reinterpret_cast<const uint32_t *>(qcol + (uint64_t)(uint32_t)(h + 1) * ld4u);
             const uint4 r = *lds_ptr<const uint4>(inst0 + 16u * (uint32_t)h);
             q.theta = __longlong_as_double((long long)(((uint64_t)r.y << 32) | r.x));
             q.inv = 1.0;
@@ -409,14 +645,13 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
             vblk = 0.0f;
         };
         // (In a fast block g, nb and the double variance sum are brought up to
-        // date at the end of the block, from whether nbr moved.)
-        int xnbr = 0;             // x.nb - base, set at the start of a fast block
+        // date at the end of the block, from whether the block held the head nbr
+        // names; nbr itself stays, as no second head can follow in the block.)
         auto enter_fast = [&](uint32_t &rowb) __attribute__((always_inline)) {
             theta = x.theta;
             if (PEN || DETAIL) inv_theta = x.inv;
             cbase = x.cbase;
             rowb = x.head;
-            nbr = xnbr;
             Y = 0.0;
             if (DETAIL) V = 0.0;
             vb = 0.0f;
@@ -461,8 +696,11 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
         constexpr int R = 16;
         int32_t ring[R];
         uint4 rec[4];                 // rec[s % 4] holds slot s's record
+        // (ids clamped to G in 16 bits: G < 2^16, and an id of 2^16 or more
+        // lands on some group, in bounds)
         auto gather = [&](int32_t gid) __attribute__((always_inline)) {
-            return *lds_ptr<const uint4>((min((uint32_t)gid, (uint32_t)G) << 4) + grp0);
+            const uint32_t c = (uint32_t)min((uint16_t)gid, (uint16_t)Gv);
+            return *lds_ptr<const uint4>((c << 4) + grp0);
         };
         // Back half: the state of the plan at slot s_begin (a multiple of 32,
         // > 0).  The queue holding it is the last one starting at or before it
@@ -510,15 +748,15 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
                 for (int k = 0; k < 16; ++k) {
                     const int s = c0 + k;
                     const uint4 r = gather((int32_t)id[k]);
-                    const uint32_t col = r.w & kColMask;
+                    const uint32_t col = rec_model(r.w);
                     if (s >= qs) {
                         const uint32_t evb =
                             EVICT ? __builtin_amdgcn_ubfe(evw, (uint32_t)(s & 31), 1u) << ev_shift : 0u;
-                        const uint32_t rb = s == qs ? ir.w : cbase + (colp << col_shift);
-                        const double cst = *lds_ptr<const double>(rb + col + evb);
+                        const uint32_t rb = s == qs ? ir.w : cbase + (colp << cs3);
+                        const double cst = *lds_ptr<const double>(rb + (col << 3) + evb);
                         Yw = fma(cst, theta, Yw);
-                        Yw = fma((double)(r.w >> kCountShift), (double)__uint_as_float(r.x), Yw);
-                        Vw += (double)__uint_as_float(r.y);
+                        Yw = Yw + rec_nmu(r);
+                        Vw += (double)rec_nv(r);
                     }
                     colp = col;
                 }
@@ -527,7 +765,7 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
             V = Vw;
             vb = (float)V;
             vblk = 0.0f;
-            rowb = qs == Gs ? ir.w : cbase + (colp << col_shift);
+            rowb = qs == Gs ? ir.w : cbase + (colp << cs3);
             // prefetch as if queue g had been entered during the block before
             q0 = g - 1;
             f1 = load_qp(g);
@@ -556,16 +794,16 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
         rec[D] = rec[0];
         uint32_t ev = EVICT ? ld_rel(rsrc_at(a.evict, s_begin >> 5), 0) : 0u;   // word of the block
         uint32_t ev_nx = 0u;                              // word of the next block
-        uint32_t colc = rec[0].w & kColMask;   // cost-table column of the current slot
-        double cost = *lds_ptr<const double>(rowb0 + colc + (EVICT ? (ev & 1u) << ev_shift : 0u));
+        uint32_t colc = rec_model(rec[0].w);    // cost-table column (model) of the current slot
+        double cost = *lds_ptr<const double>(rowb0 + (colc << 3) + (EVICT ? (ev & 1u) << ev_shift : 0u));
         float2 tc = make_float2(0.0f, 0.0f);   // tail cell of the previous slot (none yet)
         float tf = 0.0f;                       // and its t
-        float tn = 0.0f;                       // and its count
+        uint32_t tnx = 0u;                     // and its record word x (count in the low half)
 
         // The probability of the previous slot from its tail cell.
         auto finish = [&](int s_prev) __attribute__((always_inline)) {
             const float prob = fmaf(tc.y, tf, tc.x);
-            S32 = fmaf(tn, prob, S32);
+            S32 = fma_count(tnx, prob, S32);
             // settled here: sunk to the end of the block, the sums of all 32 slots
             // would keep their tail cells live in registers
             asm volatile("" : "+v"(S32));
@@ -581,17 +819,20 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
             // (0) slot s-1
             finish(s - 1);
             // (1) cost of slot s+1 if it stays in this queue
-            const uint32_t col1 = w1 & kColMask;
-            const uint32_t evb = EVICT ? __builtin_amdgcn_ubfe(evw, b1, 1u) << ev_shift : 0u;
-            double cost1 = *lds_ptr<const double>(cbase + (colc << col_shift) + col1 + evb);
+            const uint32_t col1 = rec_model(w1);
+            // entry of the row, in doubles, the eviction twin included (bit b1 of
+            // the eviction word moved to bit kTwinShift: a right shift, or a
+            // 16-bit left shift for the low bits)
+            const uint32_t off1 = EVICT ? (col1 | (twin_bit(evw, b1) & kTwinEntries)) : col1;
+            const uint32_t rb = in_vgpr(cbase + (colc << cs3));
+            double cost1 = *lds_ptr<const double>(rb + (off1 << 3));
 
             // (2) slot s
-            const float mu = __uint_as_float(r.x);
-            const float nv = __uint_as_float(r.y);
-            const float slo = __uint_as_float(r.z);
-            const double n = (double)(r.w >> kCountShift);
+            const double nmu = rec_nmu(r);
+            const float nv = rec_nv(r);
+            const float slo = rec_slo(r);
             Y = fma(cost, theta, Y);
-            const double num = fma((double)slo, theta, -Y);   // theta (slo - E[W])
+            const double nnum = fma(-(double)slo, theta, Y);  // theta (E[W] - slo)
             const float vz = vb + vblk;                       // scaled variance ahead
             if (DETAIL && det) {
                 const int64_t o = (int64_t)s * a.d_count + dq;
@@ -600,19 +841,19 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
             }
             vblk += nv;
             if (PEN) {
-                PE = fma(-num, inv_theta, PE);
+                PE = fma(nnum, inv_theta, PE);
                 asm volatile("" : "+v"(PE));     // not sunk to the end of the block
             }
-            Y = fma(n, (double)mu, Y);
+            Y = Y + nmu;
 
             // (3) tail cell of slot s
             const float rs = __builtin_amdgcn_rsqf(vz);       // cells per unit margin; inf if 0
-            float tt = fmaf(-(float)num, rs, kTailMid);
+            float tt = fmaf((float)nnum, rs, kTailMid);
             tt = __builtin_amdgcn_fmed3f(tt, kTailLo, kTailHi);   // NaN (0 / 0) -> low end
             const uint32_t cell = (__float_as_uint(tt) & kTailCellBits) >> 10;   // cell * 8
             tf = tt;
             tc = *lds_ptr<const float2>(tail0 + cell);
-            tn = (float)(r.w >> kCountShift);
+            tnx = r.x;
             // settled before the branch: nothing of slot s may sink into it
             asm volatile("" : "+v"(tf), "+v"(vblk));
 
@@ -623,7 +864,9 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
                     enter_fast(rowb);
                 else
                     enter_any(s + 1, rowb);
-                cost1 = *lds_ptr<const double>(rowb + col1 + evb);
+                // (its own shift: one v_lshl_add_u32 here and one above, not a
+                // shared shift and two adds)
+                cost1 = *lds_ptr<const double>(rowb + (in_vgpr(off1) << 3));
             }
             cost = cost1;
             colc = col1;
@@ -648,8 +891,6 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
             if (__builtin_amdgcn_ballot_w64(odd) == 0) {
                 rp = rsrc_at(a.perm, sb);
                 const int lim = G - 1 - sb;           // last row, relative to the block
-                const int nbr0 = nbr;
-                xnbr = x.nb - sb;
 #pragma unroll
                 for (int k = 0; k < 32; ++k) {
                     const int s = sb + k;
@@ -665,7 +906,7 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
                 }
                 // at most one queue entered in this block: bring g, nb and the
                 // double variance sum up to date
-                const bool moved = nbr != nbr0;
+                const bool moved = nbr >= 1 && nbr <= 32;
                 g += moved ? 1 : 0;
                 nb = moved ? x.nb : nb;
                 if (!DETAIL) V = moved ? 0.0 : V;
@@ -1246,7 +1487,8 @@ Geometry geometry(int G, int I, int M, int C, bool evict)
     Geometry g;
     g.col_shift = ceil_log2((uint32_t)M);
     const uint32_t half = (uint32_t)(C * (M + 1)) << (g.col_shift + 3);   // bytes of one half
-    g.ev_shift = ceil_log2(half < 16u ? 16u : half);
+    // the twin at 8 KiB (where the fast path expects it) when a half fits there
+    g.ev_shift = half <= (kTwinEntries << 3) ? kTwinShift + 3 : ceil_log2(half);
     const uint32_t bytes = evict ? (1u << g.ev_shift) + half : half;
     g.lut_bytes = (bytes + 15u) / 16u * 16u;
     // group table, cost table, instances, scratch
@@ -1263,6 +1505,8 @@ ScoreArgs score_args(const qlm_problem *pr, const qlm_plans *pl, const Geometry 
     a.C = pr->n_classes;
     a.col_shift = geo.col_shift;
     a.ev_shift = geo.ev_shift;
+    a.fast_ok = pr->n_models <= kCompactModels &&
+                (pl->evict_bits == nullptr || geo.ev_shift == kTwinShift + 3);
     a.lut_bytes = geo.lut_bytes;
     a.grp_count = pr->grp_count;
     a.grp_mu = pr->grp_mu;
