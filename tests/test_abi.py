@@ -96,8 +96,9 @@ def test_workspace_checks(lib):
 
 def test_max_groups(lib):
     # LDS budget 160 KiB: 16-byte group records plus cost and instance tables
+    # (the eviction twins 8 KiB on); the large workload's 8192 groups fit
     mg = lib.qlm_max_groups(8, 4, 64, 1)
-    assert 9000 < mg < 10240
+    assert 8192 <= mg < 10240
     assert lib.qlm_max_groups(1, 1, 1, 0) > mg
     assert lib.qlm_max_groups(0, 1, 1, 0) == 0
     assert lib.qlm_max_groups(256, 1, 1, 0) == 0
