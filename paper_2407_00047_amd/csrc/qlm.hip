@@ -553,6 +553,9 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
         double V = 0.0;        // scaled variance ahead, through the previous block
         float vb = 0.0f;       // V rounded to single precision
         float vblk = 0.0f;     // scaled variance ahead added within the current block
+        // rsqrt of the next slot's scaled variance ahead, formed one slot early
+        // (the reciprocal square root has a long latency; inf at a queue head)
+        float rsn = INFINITY;
         double S = 0.0;        // sum of n * P, through the previous block
         float S32 = 0.0f;      // sum of n * P within the current block
         double PE = 0.0;       // sum of (E[W] - slo)
@@ -643,6 +646,7 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
             V = 0.0;
             vb = 0.0f;
             vblk = 0.0f;
+            rsn = INFINITY;
         };
         // (In a fast block g, nb and the double variance sum are brought up to
         // date at the end of the block, from whether the block held the head nbr
@@ -656,6 +660,7 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
             if (DETAIL) V = 0.0;
             vb = 0.0f;
             vblk = 0.0f;
+            rsn = INFINITY;
         };
         auto enter_any = [&](int s, uint32_t &rowb) __attribute__((always_inline)) {
             if (fast) {
@@ -682,17 +687,19 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
 
         // Software pipeline over the slots of the plan:
         //   ring[16]  group ids of the next 16 slots (global loads, 16 slots ahead)
-        //   rec[4]    LDS records of slots s..s+3 (gathered D slots ahead)
+        //   rec[4]    LDS records of slots s..s+2 (gathered D = 2 slots ahead)
         //   cost      swap/eviction seconds of slot s, read during slot s-1
-        //   tc, tf    tail-table cell and position of slot s-1, read during s-1
-        // Slot s: (0) the probability of slot s-1, (1) the cost of s+1 read on the
-        // current queue's row, (2) waits and variances of slot s, (3) its tail cell,
-        // (4) if s+1 starts a queue: switch, and read the cost of s+1 again on the
-        // head row.  Every LDS read is consumed one slot after it is issued.
+        //   rsn       rsqrt of slot s's variance ahead, formed during slot s-1
+        //   tc, tcp   tail-table cells of slots s-1 and s-2 (with tf, tfp, tnx, tnxp)
+        // Slot s: (0) the probability of slot s-2, (1) the cost of s+1 read on the
+        // current queue's row, (2) waits and variances of slot s, (3) its tail
+        // position, (4) if s+1 starts a queue: switch, and read the cost of s+1
+        // again on the head row, (5) the tail cell of slot s.  A cost is used one
+        // slot after its read, a tail cell two.
         // At the start of a block at slot sb: ring[j] holds the group id of slot
         // sb + j (j >= D) or sb + 16 + j (j < D), rec[k] the record of slot sb + k
         // (k < D), cost and colc those of slot sb.
-        constexpr int D = 3;
+        constexpr int D = 2;
         constexpr int R = 16;
         int32_t ring[R];
         uint4 rec[4];                 // rec[s % 4] holds slot s's record
@@ -765,6 +772,7 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
             V = Vw;
             vb = (float)V;
             vblk = 0.0f;
+            rsn = __builtin_amdgcn_rsqf(vb);
             rowb = qs == Gs ? ir.w : cbase + (colp << cs3);
             // prefetch as if queue g had been entered during the block before
             q0 = g - 1;
@@ -796,18 +804,23 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
         uint32_t ev_nx = 0u;                              // word of the next block
         uint32_t colc = rec_model(rec[0].w);    // cost-table column (model) of the current slot
         double cost = *lds_ptr<const double>(rowb0 + (colc << 3) + (EVICT ? (ev & 1u) << ev_shift : 0u));
-        float2 tc = make_float2(0.0f, 0.0f);   // tail cell of the previous slot (none yet)
-        float tf = 0.0f;                       // and its t
-        uint32_t tnx = 0u;                     // and its record word x (count in the low half)
+        // Tail cells in flight: slot s's cell is read at the end of slot s, after
+        // the cost entries (so that waiting for a cost, or rereading it at a
+        // queue head, does not wait for the tail read) and used at the start of
+        // slot s + 2.  (tc, tf, tnx): slot s - 1's cell, t and record word x
+        // (count in the low half); (tcp, tfp, tnxp): slot s - 2's.
+        float2 tc = make_float2(0.0f, 0.0f), tcp = tc;
+        float tf = 0.0f, tfp = 0.0f;
+        uint32_t tnx = 0u, tnxp = 0u;
 
         // The probability of the previous slot from its tail cell.
         auto finish = [&](int s_prev) __attribute__((always_inline)) {
-            const float prob = fmaf(tc.y, tf, tc.x);
-            S32 = fma_count(tnx, prob, S32);
+            const float prob = fmaf(tcp.y, tfp, tcp.x);
+            S32 = fma_count(tnxp, prob, S32);
             // settled here: sunk to the end of the block, the sums of all 32 slots
             // would keep their tail cells live in registers
             asm volatile("" : "+v"(S32));
-            if (DETAIL && det && a.d_prob && s_prev >= 0)
+            if (DETAIL && det && a.d_prob && s_prev >= s_begin)
                 a.d_prob[(int64_t)s_prev * a.d_count + dq] = prob;
         };
 
@@ -816,8 +829,11 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
         // switch can happen here.
         auto step = [&](auto fast_block, int s, const uint4 r, uint32_t w1, uint32_t evw,
                         uint32_t b1) __attribute__((always_inline)) {
-            // (0) slot s-1
-            finish(s - 1);
+            // (0) the probability of slot s-2
+            finish(s - 2);
+            tcp = tc;
+            tfp = tf;
+            tnxp = tnx;
             // (1) cost of slot s+1 if it stays in this queue
             const uint32_t col1 = rec_model(w1);
             // entry of the row, in doubles, the eviction twin included (bit b1 of
@@ -833,13 +849,14 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
             const float slo = rec_slo(r);
             Y = fma(cost, theta, Y);
             const double nnum = fma(-(double)slo, theta, Y);  // theta (E[W] - slo)
-            const float vz = vb + vblk;                       // scaled variance ahead
             if (DETAIL && det) {
                 const int64_t o = (int64_t)s * a.d_count + dq;
                 if (a.d_mean) a.d_mean[o] = (float)(Y * inv_theta);
                 if (a.d_sd) a.d_sd[o] = (float)(sqrt(V + (double)vblk) * kTailScale * inv_theta);
             }
             vblk += nv;
+            const float rs = rsn;                 // cells per unit margin; inf if V = 0
+            rsn = __builtin_amdgcn_rsqf(vb + vblk);
             if (PEN) {
                 PE = fma(nnum, inv_theta, PE);
                 asm volatile("" : "+v"(PE));     // not sunk to the end of the block
@@ -847,12 +864,10 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
             Y = Y + nmu;
 
             // (3) tail cell of slot s
-            const float rs = __builtin_amdgcn_rsqf(vz);       // cells per unit margin; inf if 0
             float tt = fmaf((float)nnum, rs, kTailMid);
             tt = __builtin_amdgcn_fmed3f(tt, kTailLo, kTailHi);   // NaN (0 / 0) -> low end
             const uint32_t cell = (__float_as_uint(tt) & kTailCellBits) >> 10;   // cell * 8
             tf = tt;
-            tc = *lds_ptr<const float2>(tail0 + cell);
             tnx = r.x;
             // settled before the branch: nothing of slot s may sink into it
             asm volatile("" : "+v"(tf), "+v"(vblk));
@@ -868,6 +883,8 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
                 // shared shift and two adds)
                 cost1 = *lds_ptr<const double>(rowb + (in_vgpr(off1) << 3));
             }
+            // (5) the tail cell of slot s, read last
+            tc = *lds_ptr<const float2>(tail0 + cell);
             cost = cost1;
             colc = col1;
         };
@@ -952,6 +969,10 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
                 r = rn;
             }
         }
+        finish(s_end - 2);
+        tcp = tc;
+        tfp = tf;
+        tnxp = tnx;
         finish(s_end - 1);
         S += (double)S32;
         if (live) {
