@@ -161,6 +161,22 @@ int qlm_best_plan(const qlm_problem *problem, const qlm_plans *plans, void *ws,
                   qlm_stream stream);
 
 /*
+ * qlm_best_plan for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * the same computation and result, with the workspace in a static device
+ * array of the library (64 MiB, on each GPU the library runs on, held until
+ * the process ends) instead of a caller's buffer.  Allocates nothing and
+ * creates no events.  The caller still passes the problem, the plans and the
+ * two outputs (device pointers, as for qlm_best_plan).
+ *   QLM_ERR_CAPACITY  when qlm_best_plan_workspace_bytes(problem, n_plans)
+ *                     exceeds 64 MiB (nothing is enqueued)
+ * Every call on a GPU shares that GPU's array, and calls that overlap on one
+ * GPU (different streams or threads without ordering) race on it.
+ */
+int qlm_best_plan_static(const qlm_problem *problem, const qlm_plans *plans,
+                         int64_t *best_index, double *best_score, qlm_stream stream);
+
+/*
  * Checks plan structure (Eq. slot_assignment): qoff starts at 0, ends at G and
  * never decreases; perm is a permutation of 0..G-1; no eviction bit is set
  * beyond slot G-1.

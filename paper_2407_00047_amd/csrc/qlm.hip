@@ -1664,7 +1664,7 @@ int score_grid(ScoreKernel k, size_t lds, int64_t P, int G, int I, int *grid, in
 
 int launch_score(const qlm_problem *pr, const qlm_plans *pl, double *score, double *penalty,
                  const qlm_detail *det, double *wg_min, double *wg_nsum, int32_t *ncand,
-                 int *grid_out, hipStream_t stream)
+                 int *grid_out, hipStream_t stream, bool timed = true)
 {
     const bool ev = pl->evict_bits != nullptr;
     const Geometry geo = geometry(pr->n_groups, pr->n_instances, pr->n_models, pr->n_classes, ev);
@@ -1696,13 +1696,15 @@ int launch_score(const qlm_problem *pr, const qlm_plans *pl, double *score, doub
     if (rc) return rc;
     if (grid_out) *grid_out = grid;
 
-    qlm_internal::TimedLaunch tl;
-    rc = qlm_internal::timing_begin(stream, &tl);
-    if (rc) return rc;
+    qlm_internal::TimedLaunch tl{nullptr, nullptr};
+    if (timed) {
+        rc = qlm_internal::timing_begin(stream, &tl);
+        if (rc) return rc;
+    }
     hipLaunchKernelGGL(k, dim3(grid), dim3(kScoreThreads), geo.lds_bytes, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "k_score launch");
-    qlm_internal::timing_end(stream, &tl);
+    if (timed) qlm_internal::timing_end(stream, &tl);
     return QLM_OK;
 }
 
@@ -1715,6 +1717,43 @@ size_t best_plan_fixed_bytes(int64_t P)
 {
     return align256(8 * (size_t)P) + align256(8 * (size_t)kMaxScoreBlocks) + 256 +
            align256(8 * (size_t)P);
+}
+
+int best_plan_impl(const qlm_problem *problem, const qlm_plans *plans, void *ws, size_t ws_bytes,
+                   int64_t *best_index, double *best_score, hipStream_t stream, bool timed);
+
+// Scratch of qlm_best_plan_static, for callers that cannot allocate: a
+// file-scope device array (each GPU the library runs on holds its own copy
+// until the process ends).  Host code never passes the array's name to a
+// kernel or a copy: its device address comes from hipGetSymbolAddress, taken
+// once per device with that device current and kept per device.
+constexpr size_t kStaticScratchBytes = size_t(64) << 20;
+
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+namespace {
+
+std::mutex g_scratch_mu;
+std::vector<void *> g_scratch_ptr;   // by device ordinal; null until taken
+
+int static_scratch(void **out)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if ((size_t)dev >= g_scratch_ptr.size()) g_scratch_ptr.resize((size_t)dev + 1, nullptr);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+        if (!p) return fail(QLM_ERR_HIP, "hipGetSymbolAddress(scratch) gave no address");
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return QLM_OK;
 }
 
 }  // namespace
@@ -1776,7 +1815,40 @@ size_t qlm_best_plan_workspace_bytes(const qlm_problem *problem, int64_t n_plans
 int qlm_best_plan(const qlm_problem *problem, const qlm_plans *plans, void *ws, size_t ws_bytes,
                   int64_t *best_index, double *best_score, qlm_stream stream_)
 {
-    hipStream_t stream = (hipStream_t)stream_;
+    return best_plan_impl(problem, plans, ws, ws_bytes, best_index, best_score,
+                          (hipStream_t)stream_, true);
+}
+
+int qlm_best_plan_static(const qlm_problem *problem, const qlm_plans *plans,
+                         int64_t *best_index, double *best_score, qlm_stream stream_)
+{
+    int rc = check_problem(problem);
+    if (rc) return rc;
+    rc = check_plans(problem, plans);
+    if (rc) return rc;
+    if (!best_index || !best_score) return fail(QLM_ERR_ARG, "best_index and best_score are required");
+    const size_t need = qlm_best_plan_workspace_bytes(problem, plans->n_plans);
+    if (need > kStaticScratchBytes)
+        return fail(QLM_ERR_CAPACITY, "qlm_best_plan_static: " + std::to_string(plans->n_plans) +
+                                          " plans need " + std::to_string(need) +
+                                          " bytes of scratch; the static scratch holds " +
+                                          std::to_string(kStaticScratchBytes));
+    void *ws = nullptr;
+    rc = static_scratch(&ws);
+    if (rc) return rc;
+    // the same workspace size qlm_best_plan is given for these plans, so that
+    // both take the same path; no timing events are created
+    return best_plan_impl(problem, plans, ws, need, best_index, best_score, (hipStream_t)stream_,
+                          false);
+}
+
+}  // extern "C"
+
+namespace {
+
+int best_plan_impl(const qlm_problem *problem, const qlm_plans *plans, void *ws, size_t ws_bytes,
+                   int64_t *best_index, double *best_score, hipStream_t stream, bool timed)
+{
     int rc = check_problem(problem);
     if (rc) return rc;
     rc = check_plans(problem, plans);
@@ -1811,7 +1883,8 @@ int qlm_best_plan(const qlm_problem *problem, const qlm_plans *plans, void *ws, 
     int64_t cap = (int64_t)((ws_bytes - fixed) / (8 * (size_t)I));
     if (cap > P) cap = P;
     int grid = 0;
-    rc = launch_score(problem, plans, fast, nullptr, nullptr, wg_min, nsum, ncand, &grid, stream);
+    rc = launch_score(problem, plans, fast, nullptr, nullptr, wg_min, nsum, ncand, &grid, stream,
+                      timed);
     if (rc) return rc;
     int sgrid = (int)((P + kSelThreads - 1) / kSelThreads);
     if (sgrid > kSelBlocks) sgrid = kSelBlocks;
@@ -1831,6 +1904,10 @@ int qlm_best_plan(const qlm_problem *problem, const qlm_plans *plans, void *ws, 
     if (e != hipSuccess) return hip_fail(e, "k_gpick launch");
     return QLM_OK;
 }
+
+}  // namespace
+
+extern "C" {
 
 int qlm_validate_plans(const qlm_problem *problem, const qlm_plans *plans, int64_t *n_invalid,
                        int32_t *plan_status, qlm_stream stream_)

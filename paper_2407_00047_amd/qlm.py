@@ -84,6 +84,7 @@ def library():
             lib.qlm_best_plan_workspace_bytes.argtypes = [P, i64]
             lib.qlm_best_plan_workspace_bytes.restype = ctypes.c_size_t
             lib.qlm_best_plan.argtypes = [P, PL, vp, ctypes.c_size_t, vp, vp, vp]
+            lib.qlm_best_plan_static.argtypes = [P, PL, vp, vp, vp]
             lib.qlm_validate_plans.argtypes = [P, PL, vp, vp, vp]
             lib.qlm_validate_problem.argtypes = [P, vp, vp]
             lib.qlm_max_groups.argtypes = [ctypes.c_int32] * 4
@@ -120,7 +121,7 @@ def library():
             lib.qlm_place_begin.argtypes = [P, PL, vp, sz, vp]
             lib.qlm_place_step.argtypes = [P, i64, i32, vp, sz, vp, vp, vp]
             lib.qlm_place_end.argtypes = [P, i64, ctypes.POINTER(PlansOut), vp, sz, vp, vp]
-            for name in ("qlm_rwt_score", "qlm_rwt_score_exact", "qlm_best_plan",
+            for name in ("qlm_rwt_score", "qlm_rwt_score_exact", "qlm_best_plan", "qlm_best_plan_static",
                          "qlm_validate_plans", "qlm_validate_problem", "qlm_timing_enable",
                          "qlm_timing_read", "qlm_search_moves", "qlm_search_screen",
                          "qlm_local_search", "qlm_seed_plans", "qlm_place_group",
@@ -264,6 +265,21 @@ def best_plan(problem: DeviceProblem, plans: DevicePlans, ws=None, stream=None, 
         bi, bs = out
     _check(library().qlm_best_plan(ctypes.byref(problem.struct), ctypes.byref(plans.struct),
                                    _ptr(ws), ws.numel(), _ptr(bi), _ptr(bs), _stream(stream)))
+    return bi, bs
+
+
+def best_plan_static(problem: DeviceProblem, plans: DevicePlans, stream=None, out=None):
+    """qlm_best_plan_static: (best_index, best_score) as device tensors of
+    shape [1], with the library's static scratch as the workspace."""
+    import torch
+    dev = plans.perm.device
+    if out is None:
+        bi = torch.empty(1, dtype=torch.int64, device=dev)
+        bs = torch.empty(1, dtype=torch.float64, device=dev)
+    else:
+        bi, bs = out
+    _check(library().qlm_best_plan_static(ctypes.byref(problem.struct), ctypes.byref(plans.struct),
+                                          _ptr(bi), _ptr(bs), _stream(stream)))
     return bi, bs
 
 

@@ -94,6 +94,22 @@ def test_workspace_checks(lib):
     assert lib.qlm_best_plan(P(pr), P(pl), 0x1000, need, None, 0x1000, None) == qlm.QLM_ERR_ARG
 
 
+def test_static_best_plan_capacity(lib):
+    """qlm_best_plan_static refuses, on the host, a batch whose workspace would
+    not fit its 64 MiB static scratch, and takes the usual argument checks."""
+    from paper_2407_00047_amd import qlm
+    pr = _problem(qlm)
+    P = ctypes.byref
+    big = qlm.Plans(4000000, 4000000, 0x1000, 0x1000, None)
+    assert lib.qlm_best_plan_workspace_bytes(P(pr), 4000000) > 64 << 20
+    assert lib.qlm_best_plan_static(P(pr), P(big), 0x1000, 0x1000, None) == qlm.QLM_ERR_CAPACITY
+    assert b"static scratch" in lib.qlm_last_error()
+    pl = qlm.Plans(4, 4, 0x1000, 0x1000, None)
+    assert lib.qlm_best_plan_static(None, P(pl), 0x1000, 0x1000, None) == qlm.QLM_ERR_ARG
+    assert lib.qlm_best_plan_static(P(pr), P(qlm.Plans(-1, 4, 0x1000, 0x1000, None)),
+                                    0x1000, 0x1000, None) == qlm.QLM_ERR_ARG
+
+
 def test_max_groups(lib):
     # LDS budget 160 KiB: 16-byte group records plus cost and instance tables
     # (the eviction twins 8 KiB on); the large workload's 8192 groups fit
