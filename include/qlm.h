@@ -464,6 +464,21 @@ int32_t qlm_max_groups(int32_t n_models, int32_t n_classes, int32_t n_instances,
                        int32_t with_eviction);
 
 /* Text of a status code; the last error's detail for this host thread. */
+/*
+ * Which form of the scoring kernel a problem gets (qlm_rwt_score and
+ * qlm_best_plan decide it on the device, from the tables, at every launch):
+ *   form [1] device out: 1 the fast path -- every group with 0 < n <= 2048
+ *        requests and a variance that keeps n var / (1024/12)^2 a normal
+ *        single-precision number, at most 64 models, a cost table (swap
+ *        seconds, plus the eviction cost) whose entries have at most 29
+ *        significant bits, and with eviction a cost table whose half fits 8
+ *        KiB; 0 the general exact walk (the same results within the same
+ *        bounds, slower).
+ *   with_eviction  nonzero when the plans carry eviction bits
+ */
+int qlm_score_form(const qlm_problem *problem, int32_t with_eviction, int32_t *form,
+                   qlm_stream stream);
+
 const char *qlm_status_string(int status);
 const char *qlm_last_error(void);
 

@@ -205,33 +205,63 @@ __device__ inline T in_vgpr(T v)
     return v;
 }
 
-// Cost table and instance records.  Returns whether every cost entry has at
-// most 29 significant bits (the low 24 bits of its mantissa clear), so that
-// its product with any single-precision throughput is exact in double
-// precision; the fast path needs that at queue heads (below).
-__device__ bool stage_costs(const ScoreArgs &a, const Lds &l)
+// Entry w of the cost table (swap seconds, plus the eviction cost in the twin
+// half), 0 for the diagonal, no model loaded, padding and no swap table.
+__device__ inline double cost_entry(const ScoreArgs &a, int w)
 {
-    bool ok = true;
-    double *lut = lds_ptr<double>(l.lut);
     const int Mp = 1 << a.col_shift;
     const int rows = a.M + 1;
     const int half = a.C * rows * Mp;
     const int twin = 1 << (a.ev_shift - 3);
+    const int ev = w >= twin;
+    const int k = ev ? w - twin : w;
+    double v = 0.0;
+    if (k < half) {
+        const int col = k % Mp;
+        const int row = (k / Mp) % rows;
+        const int c = k / (Mp * rows);
+        if (a.swap_cost && row < a.M && col < a.M && row != col)
+            v = (double)a.swap_cost[((int64_t)c * a.M + row) * a.M + col];
+        if (ev) v += (double)a.evict_cost;
+    }
+    return v;
+}
+
+// The fast path's conditions.  A cost entry: at most 29 significant bits (the
+// low 24 bits of its mantissa clear), so that its product with any
+// single-precision throughput is exact in double precision (the fast path
+// needs that at queue heads, where SD = 0).  A group: 0 < n <= 2048 and a
+// scaled variance that is a normal single-precision number (so every position
+// after a queue head has SD > 0).
+__device__ inline bool cost_fits(double v)
+{
+    return ((uint64_t)__double_as_longlong(v) & 0xFFFFFFull) == 0;
+}
+__device__ inline uint32_t group_count(const ScoreArgs &a, int i)
+{
+    return (uint32_t)clampi(a.grp_count[i], 0, (int)kCountMask);
+}
+__device__ inline float group_scaled_var(const ScoreArgs &a, int i, uint32_t n)
+{
+    return (float)((double)n * (double)a.grp_var[i] * kVarScale);
+}
+__device__ inline bool group_fits(uint32_t n, float nv)
+{
+    return n >= 1u && n <= kCompactCountMax && nv >= 1.17549435e-38f && nv <= 3.4028235e38f;
+}
+
+// Cost table and instance records.  Returns whether every cost entry this
+// thread staged fits the fast path.
+__device__ bool stage_costs(const ScoreArgs &a, const Lds &l)
+{
+    bool ok = true;
+    double *lut = lds_ptr<double>(l.lut);
+    const int rows = a.M + 1;
     const int entries = (int)(a.lut_bytes / 8u);
     for (int w = threadIdx.x; w < entries; w += blockDim.x) {
-        const int ev = w >= twin;
-        const int k = ev ? w - twin : w;
-        double v = 0.0;
-        if (k < half) {
-            const int col = k % Mp;
-            const int row = (k / Mp) % rows;
-            const int c = k / (Mp * rows);
-            if (a.swap_cost && row < a.M && col < a.M && row != col)
-                v = (double)a.swap_cost[((int64_t)c * a.M + row) * a.M + col];
-            if (ev) v += (double)a.evict_cost;
-        }
+        const double v = cost_entry(a, w);
         lut[w] = v;
-        ok = ok && ((uint64_t)__double_as_longlong(v) & 0xFFFFFFull) == 0;
+        ok = ok && cost_fits(v);
     }
     const uint32_t row_bytes = 8u << a.col_shift;
     for (int g = threadIdx.x; g < a.I; g += blockDim.x) {
@@ -265,12 +295,11 @@ __device__ bool stage_compact(const ScoreArgs &a, const Lds &l)
     for (int i = threadIdx.x; i <= a.G; i += blockDim.x) {
         uint4 r = make_uint4(0u, 0u, 0u, 0u);
         if (i < a.G) {
-            const uint32_t n = (uint32_t)clampi(a.grp_count[i], 0, (int)kCountMask);
+            const uint32_t n = group_count(a, i);
             const uint32_t m = (uint32_t)clampi(a.grp_model[i], 0, a.M - 1);
             const uint64_t nm = (uint64_t)__double_as_longlong((double)n * (double)a.grp_mu[i]);
-            const float nv = (float)((double)n * (double)a.grp_var[i] * kVarScale);
-            ok = ok && n >= 1u && n <= kCompactCountMax && nv >= 1.17549435e-38f &&
-                 nv <= 3.4028235e38f;
+            const float nv = group_scaled_var(a, i, n);
+            ok = ok && group_fits(n, nv);
             const uint32_t nh = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)(float)min(n, kCompactCountMax));
             r.x = ((uint32_t)nm & 0xFFFF0000u) | nh;
             r.y = (uint32_t)(nm >> 32);
@@ -315,6 +344,22 @@ __device__ inline double wave_min(double v)
 {
     for (int o = 32; o > 0; o >>= 1) v = fmin(v, __shfl_xor(v, o, kWave));
     return v;
+}
+
+// qlm_score_form: 1 when the scoring kernel takes its fast path for this
+// problem (the conditions above, evaluated as its staging evaluates them),
+// else 0.  One workgroup.
+__global__ __launch_bounds__(1024) void k_score_form(ScoreArgs a, int32_t *form)
+{
+    bool ok = a.fast_ok != 0;
+    const int entries = (int)(a.lut_bytes / 8u);
+    for (int w = threadIdx.x; w < entries; w += blockDim.x) ok = ok && cost_fits(cost_entry(a, w));
+    for (int i = threadIdx.x; i < a.G; i += blockDim.x) {
+        const uint32_t n = group_count(a, i);
+        ok = ok && group_fits(n, group_scaled_var(a, i, n));
+    }
+    const int all = __syncthreads_and((int)ok);
+    if (threadIdx.x == 0) *form = all ? 1 : 0;
 }
 
 #pragma clang fp contract(off)
@@ -1960,6 +2005,24 @@ int32_t qlm_max_groups(int32_t n_models, int32_t n_classes, int32_t n_instances,
     const Geometry g0 = geometry(0, n_instances, n_models, n_classes, with_eviction != 0);
     if (g0.lds_bytes > kScoreLdsLimit) return 0;
     return (int32_t)((kScoreLdsLimit - g0.lds_bytes) / 16);
+}
+
+int qlm_score_form(const qlm_problem *problem, int32_t with_eviction, int32_t *form,
+                   qlm_stream stream)
+{
+    int rc = check_problem(problem);
+    if (rc) return rc;
+    if (!form) return fail(QLM_ERR_ARG, "form is NULL");
+    const bool ev = with_eviction != 0;
+    const Geometry geo = geometry(problem->n_groups, problem->n_instances, problem->n_models,
+                                  problem->n_classes, ev);
+    qlm_plans none{};
+    none.evict_bits = ev ? reinterpret_cast<const uint32_t *>(form) : nullptr;   // only tested for NULL
+    ScoreArgs a = score_args(problem, &none, geo);
+    hipLaunchKernelGGL(k_score_form, dim3(1), dim3(1024), 0, (hipStream_t)stream, a, form);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "k_score_form launch");
+    return QLM_OK;
 }
 
 const char *qlm_status_string(int status)

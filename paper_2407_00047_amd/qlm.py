@@ -85,6 +85,7 @@ def library():
             lib.qlm_best_plan_workspace_bytes.restype = ctypes.c_size_t
             lib.qlm_best_plan.argtypes = [P, PL, vp, ctypes.c_size_t, vp, vp, vp]
             lib.qlm_best_plan_static.argtypes = [P, PL, vp, vp, vp]
+            lib.qlm_score_form.argtypes = [P, ctypes.c_int32, vp, vp]
             lib.qlm_validate_plans.argtypes = [P, PL, vp, vp, vp]
             lib.qlm_validate_problem.argtypes = [P, vp, vp]
             lib.qlm_max_groups.argtypes = [ctypes.c_int32] * 4
@@ -122,6 +123,7 @@ def library():
             lib.qlm_place_step.argtypes = [P, i64, i32, vp, sz, vp, vp, vp]
             lib.qlm_place_end.argtypes = [P, i64, ctypes.POINTER(PlansOut), vp, sz, vp, vp]
             for name in ("qlm_rwt_score", "qlm_rwt_score_exact", "qlm_best_plan", "qlm_best_plan_static",
+                         "qlm_score_form",
                          "qlm_validate_plans", "qlm_validate_problem", "qlm_timing_enable",
                          "qlm_timing_read", "qlm_search_moves", "qlm_search_screen",
                          "qlm_local_search", "qlm_seed_plans", "qlm_place_group",
@@ -214,8 +216,10 @@ def rwt_score(problem: DeviceProblem, plans: DevicePlans, penalty: bool = False,
     import torch
     dev = plans.perm.device
     P = plans.n_plans
-    score = out if out is not None else torch.empty(P, dtype=torch.float64, device=dev)
-    pen = torch.empty(P, dtype=torch.float64, device=dev) if penalty else None
+    # outputs start as NaN, so that an entry the library failed to write shows
+    score = out if out is not None else torch.full((P,), float("nan"), dtype=torch.float64,
+                                                   device=dev)
+    pen = torch.full((P,), float("nan"), dtype=torch.float64, device=dev) if penalty else None
     det = None
     res = {"score": score, "penalty": pen}
     if detail is not None:
@@ -236,7 +240,7 @@ def rwt_score(problem: DeviceProblem, plans: DevicePlans, penalty: bool = False,
 def rwt_score_exact(problem: DeviceProblem, plans: DevicePlans, plan_index, stream=None):
     import torch
     idx = torch.as_tensor(plan_index, dtype=torch.int64).to(plans.perm.device)
-    out = torch.empty(idx.numel(), dtype=torch.float64, device=plans.perm.device)
+    out = torch.full((idx.numel(),), float("nan"), dtype=torch.float64, device=plans.perm.device)
     _check(library().qlm_rwt_score_exact(ctypes.byref(problem.struct), ctypes.byref(plans.struct),
                                          _ptr(idx), idx.numel(), _ptr(out), _stream(stream)))
     return out
@@ -259,8 +263,8 @@ def best_plan(problem: DeviceProblem, plans: DevicePlans, ws=None, stream=None, 
     if ws is None:
         ws = workspace(problem, plans.n_plans, dev)
     if out is None:
-        bi = torch.empty(1, dtype=torch.int64, device=dev)
-        bs = torch.empty(1, dtype=torch.float64, device=dev)
+        bi = torch.full((1,), -2, dtype=torch.int64, device=dev)
+        bs = torch.full((1,), float("nan"), dtype=torch.float64, device=dev)
     else:
         bi, bs = out
     _check(library().qlm_best_plan(ctypes.byref(problem.struct), ctypes.byref(plans.struct),
@@ -274,13 +278,23 @@ def best_plan_static(problem: DeviceProblem, plans: DevicePlans, stream=None, ou
     import torch
     dev = plans.perm.device
     if out is None:
-        bi = torch.empty(1, dtype=torch.int64, device=dev)
-        bs = torch.empty(1, dtype=torch.float64, device=dev)
+        bi = torch.full((1,), -2, dtype=torch.int64, device=dev)
+        bs = torch.full((1,), float("nan"), dtype=torch.float64, device=dev)
     else:
         bi, bs = out
     _check(library().qlm_best_plan_static(ctypes.byref(problem.struct), ctypes.byref(plans.struct),
                                           _ptr(bi), _ptr(bs), _stream(stream)))
     return bi, bs
+
+
+def score_form(problem: DeviceProblem, with_eviction: bool, stream=None) -> int:
+    """1 when qlm_rwt_score / qlm_best_plan take their fast path for this
+    problem, 0 when they take the general exact walk (synchronizes)."""
+    import torch
+    f = torch.full((1,), -1, dtype=torch.int32, device=problem.grp_count.device)
+    _check(library().qlm_score_form(ctypes.byref(problem.struct), int(bool(with_eviction)),
+                                    _ptr(f), _stream(stream)))
+    return int(f.item())
 
 
 def validate_plans(problem: DeviceProblem, plans: DevicePlans, stream=None):

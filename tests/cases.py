@@ -91,13 +91,14 @@ def subset_plans(pl, idx):
 
 
 def hand_case(rng, G, I, M=3, C=2, P=70, model0=True, evict=True, empty_queues=False,
-              skewed=False):
+              skewed=False, min_count=0):
     """Random groups, instances and plans drawn from rng (uniform sizes, SLOs
-    and costs; optional empty queues, skewed queue lengths, eviction flags)."""
+    and costs; optional empty queues, skewed queue lengths, eviction flags).
+    min_count=1 keeps every group non-empty (with a positive variance)."""
     groups = []
     for _ in range(G):
-        groups.append((int(rng.integers(0, 30)), float(rng.uniform(1, 600)),
-                       float(rng.uniform(0, 5e4)), int(rng.integers(0, M)),
+        groups.append((int(rng.integers(min_count, 30)), float(rng.uniform(1, 600)),
+                       float(rng.uniform(min_count, 5e4)), int(rng.integers(0, M)),
                        float(rng.uniform(0.1, 300))))
     inst = [(float(rng.choice([400.0, 1000.0, 5000.0])), int(rng.integers(0, C))) for _ in range(I)]
     S = rng.uniform(0.5, 30.0, (C, M, M)).astype(np.float32)
