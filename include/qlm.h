@@ -115,11 +115,17 @@ typedef struct qlm_detail {
  *   penalty [P] out or NULL: sum of (E[W] - slo) (Eq. penalty)
  *   detail  NULL or per-slot outputs for a plan range (must lie in [0, P))
  * Accuracy: per slot |dP| <= 1e-5 and E[W], SD[W] within 1e-5 relative of the
- * double-precision definition; |d score_p| <= 1e-5 * (total requests).  The
- * result is bit-for-bit reproducible for the same inputs.  Method: waits in
- * double precision, variances in single precision per block of 32 positions
- * on top of a double sum, and P from a 1024-cell linear table of the normal
- * tail over |z| <= 6 (error below 2.2e-6; beyond, P is exactly 0 or 1).
+ * double-precision definition; |d score_p| <= 8e-6 * (total requests).  At a
+ * position with SD = 0, P is the indicator [E[W] > slo] decided exactly as the
+ * definition decides it.  The result is bit-for-bit reproducible for the same
+ * inputs.  Method: waits in double precision, variances in single precision
+ * per block of 32 positions on top of a double sum, and P from a 1024-cell
+ * linear table of the normal tail over |z| <= 6 (error below 2.2e-6; beyond,
+ * P is exactly 0 or 1).  Two forms (qlm_score_form): the fast path, for
+ * problems whose groups all have requests and variance (SD = 0 then occurs
+ * only at queue heads, where the wait is the head's cost seconds and Theta
+ * times it is exact); and a general walk that forms A / Theta + K as the
+ * definition does, taken for every other problem.
  */
 int qlm_rwt_score(const qlm_problem *problem, const qlm_plans *plans, double *score,
                   double *penalty, const qlm_detail *detail, qlm_stream stream);
