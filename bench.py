@@ -30,8 +30,9 @@ SEARCH_METRIC = "plan-search moves scored/sec (screened + exact best) and % of V
 PEAK_VALU_LANES = 256 * 4 * 16 * 2.4e9
 # VALU instructions per slot in k_score's unrolled 32-slot block (gfx950 code of
 # the benchmarked variant, eviction words on; the queue-head path and the
-# per-block work excluded)
-VALU_PER_SLOT = 26
+# per-block work excluded); the measured count per slot, those included, comes
+# from the committed SQ counter summary when it matches the kernel source
+VALU_PER_SLOT = 22
 # VALU instructions per visited position in the main loop of the reassignment
 # screen (k_fmove), counted in its compiled loop body.
 VALU_PER_VISIT = 13
@@ -149,21 +150,109 @@ def summarize_counters(args):
     print(json.dumps(out, indent=1))
 
 
-def cpu_baseline(problem, plans, seconds: float):
+def summarize_sq(args):
+    """SQ and read-request counters of the scoring kernel from rocprofv3 --pmc
+    runs of bench.py (SQ_WAVES, SQ_INSTS_VALU, ...; and TCC_EA0_RDREQ_*_sum
+    of bench.py and of --copy-calibration): VALU instructions per slot, LDS
+    conflict cycles per slot, and the HBM read bytes from the request counts
+    (32, 64 and 128-byte requests) against the copy's known size.  Writes
+    profiles/k_score_<config>_counters.json and prints it."""
+    sq_dir, rd_dir, crd_dir = args.summarize_sq
+    from paper_2407_00047_amd import workload
+    cfg = workload.CONFIGS[args.config]
+    P = cfg["P"] if args.plans is None else args.plans
+    pr = workload.make_problem(args.config)
+
+    def avg(path, counter, pred):
+        vals = {}
+        for name, d, v in _counter_rows(path, counter):
+            if pred(name):
+                vals[d] = vals.get(d, 0.0) + v
+        return sum(vals.values()) / len(vals) if vals else None
+
+    def is_score(n):
+        return "k_score" in n
+
+    def is_copy(n):
+        return "copy" in n.lower()
+
+    out = {"config": args.config, "plans": P, "source_sha256": kernel_source_hash()}
+    names = ("SQ_WAVES", "SQ_INSTS_VALU", "SQ_ACTIVE_INST_VALU", "SQ_INSTS_LDS",
+             "SQ_LDS_BANK_CONFLICT", "SQ_LDS_IDX_ACTIVE", "SQ_WAVE_CYCLES", "GRBM_GUI_ACTIVE")
+    for c in names:
+        out[c] = avg(sq_dir, c, is_score)
+    wave_slots = P * pr["n_groups"] / 64.0          # one wave instruction covers 64 plans
+    out["valu_per_slot"] = out["SQ_INSTS_VALU"] / wave_slots
+    out["lds_insts_per_slot"] = out["SQ_INSTS_LDS"] / wave_slots
+    out["lds_conflict_cycles_per_slot"] = out["SQ_LDS_BANK_CONFLICT"] / wave_slots
+    reqs = ("TCC_EA0_RDREQ_sum", "TCC_EA0_RDREQ_32B_sum", "TCC_EA0_RDREQ_64B_sum",
+            "TCC_EA0_RDREQ_128B_sum")
+
+    def read_bytes(path, pred):
+        v = {c: avg(path, c, pred) for c in reqs}
+        v["bytes"] = (32.0 * v["TCC_EA0_RDREQ_32B_sum"] + 64.0 * v["TCC_EA0_RDREQ_64B_sum"] +
+                      128.0 * v["TCC_EA0_RDREQ_128B_sum"])
+        return v
+
+    def max_copy(path):
+        vals = {}
+        for c in reqs:
+            for name, d, val in _counter_rows(path, c):
+                if is_copy(name):
+                    vals.setdefault(d, {})[c] = vals.get(d, {}).get(c, 0.0) + val
+        best = max(vals.values(), key=lambda x: x["TCC_EA0_RDREQ_sum"])
+        best["bytes"] = (32.0 * best["TCC_EA0_RDREQ_32B_sum"] + 64.0 * best["TCC_EA0_RDREQ_64B_sum"] +
+                         128.0 * best["TCC_EA0_RDREQ_128B_sum"])
+        return best
+
+    k = read_bytes(rd_dir, is_score)
+    c = max_copy(crd_dir)
+    alg = algorithmic_bytes_per_plan(pr) * P
+    out["read_requests"] = k
+    out["copy_read_requests"] = c
+    out["copy_read_bytes_over_size"] = c["bytes"] / COPY_BYTES
+    out["read_bytes_per_launch"] = k["bytes"]
+    out["read_bytes_over_algorithmic_reads"] = k["bytes"] / (alg - 8 * P)
+    path = os.path.join(ROOT, "profiles", "k_score_%s_counters.json" % args.config)
+    with open(path, "w") as f:
+        json.dump(out, f, indent=1)
+        f.write("\n")
+    print(json.dumps(out, indent=1))
+
+
+def cpu_baseline(problem, plans, seconds: float, threads: int = 0):
+    """The oracle on a prefix of the same batch, sized to about `seconds` of
+    work: all host threads (threads=0) or the given count."""
     import oracle
     orc = oracle.default()
     P = plans["n_plans"]
-    n0 = min(P, 256)
+    used = orc.max_threads() if threads <= 0 else threads
+    n0 = min(P, max(16, 4 * used))
     t0 = time.perf_counter()
-    orc.score_plans(problem, plans, 0, n0)
+    orc.score_plans(problem, plans, 0, n0, threads=threads)
     dt = max(time.perf_counter() - t0, 1e-6)
     count = int(min(P, max(n0, seconds * n0 / dt)))
     t0 = time.perf_counter()
-    orc.score_plans(problem, plans, 0, count)
+    orc.score_plans(problem, plans, 0, count, threads=threads)
     dt = time.perf_counter() - t0
-    return {"value": count / dt, "unit": "plans/s", "cores": orc.max_threads(), "kind": "oracle",
-            "sample": "plans 0..%d of the same batch (%d of %d), all host threads, fp64 C oracle,"
-                      " %.1f s" % (count - 1, count, P, dt)}
+    N = sum(int(x) for x in problem["grp_count"])
+    return {"value": count / dt, "unit": "plans/s", "requests_per_s": count * N / dt,
+            "cores": used, "kind": "oracle",
+            "sample": "plans 0..%d of the same batch (%d of %d), %d host thread%s, fp64 C oracle,"
+                      " %.1f s" % (count - 1, count, P, used, "" if used == 1 else "s", dt)}
+
+
+def measured_counters(config: str, plans: int):
+    """SQ counter summary of the scoring kernel (VALU instructions per slot and
+    the like) when it was taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", "k_score_%s_counters.json" % config)
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    if t.get("source_sha256") != kernel_source_hash() or t.get("plans") != plans:
+        return None
+    return t
 
 
 def move_counts(problem, plans, p, window):
@@ -479,12 +568,15 @@ def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="large",
                     help="workload: tiny, mixed, hetero, heavy, large (default)")
     ap.add_argument("--plans", type=int, default=None, help="override the plan count")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--all-configs", action="store_true",
+                    help="best-plan benchmark of every workload in turn, one JSON line each "
+                         "(large last)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run a plain 1 GiB device copy (for HBM counter scaling) and exit")
     ap.add_argument("--search", action="store_true",
@@ -502,10 +594,16 @@ def main():
     ap.add_argument("--window", type=int, default=16, help="--search: swap window")
     ap.add_argument("--summarize-counters", nargs=4, metavar=("FETCH", "WRITE", "COPY_FETCH", "COPY_WRITE"),
                     help="rocprofv3 --pmc output folders: write the traffic summary and exit")
+    ap.add_argument("--summarize-sq", nargs=3, metavar=("SQ", "READS", "COPY_READS"),
+                    help="rocprofv3 --pmc output folders (SQ counters of bench.py, read requests "
+                         "of bench.py and of --copy-calibration): write the counter summary and exit")
     args = ap.parse_args()
 
     if args.summarize_counters:
         summarize_counters(args)
+        return
+    if args.summarize_sq:
+        summarize_sq(args)
         return
 
     if args.gpus != 1:
@@ -538,12 +636,26 @@ def main():
         bench_fcfs(args)
         return
 
-    cfg = workload.CONFIGS[args.config]
+    if args.all_configs:
+        for name in ("tiny", "mixed", "hetero", "heavy", "large"):
+            bench_best(args, name, dev)
+        return
+    bench_best(args, args.config, dev)
+
+
+def bench_best(args, config, dev):
+    """One step = one qlm_best_plan over the whole batch of `config`; prints
+    its JSON line."""
+    import torch
+
+    from paper_2407_00047_amd import qlm, workload
+
+    cfg = workload.CONFIGS[config]
     P = cfg["P"] if args.plans is None else args.plans
     t0 = time.perf_counter()
-    pr = workload.make_problem(args.config)
+    pr = workload.make_problem(config)
     pl = workload.make_plans(pr, 0, P)
-    log("generated %s: G=%d I=%d P=%d in %.1f s" % (args.config, pr["n_groups"],
+    log("generated %s: G=%d I=%d P=%d in %.1f s" % (config, pr["n_groups"],
                                                      pr["n_instances"], P,
                                                      time.perf_counter() - t0))
     dpr = qlm.DeviceProblem(pr, device=dev)
@@ -580,12 +692,16 @@ def main():
     stream = torch.cuda.current_stream()
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     e0.record(stream)
-    for _ in range(args.steps):
+    ev[0].record(stream)
+    for k in range(args.steps):
         qlm.best_plan(dpr, dpl, ws=ws, out=(bi, bs))
+        ev[k + 1].record(stream)
     e1.record(stream)
     torch.cuda.synchronize()
+    step_ms = sorted(ev[k].elapsed_time(ev[k + 1]) for k in range(args.steps))
     qlm.timing_enable(False)
     n_launch, k_ms = qlm.timing_read()
     total_ms = e0.elapsed_time(e1)
@@ -597,32 +713,41 @@ def main():
     bpp = algorithmic_bytes_per_plan(pr)
     k_avg_ms = k_ms / max(n_launch, 1)
     achieved = bpp * P / (k_avg_ms / 1e3) / 1e9
-    traffic = measured_traffic(args.config, P)
+    traffic = measured_traffic(config, P)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
                 "traffic": traffic, "kernel": "k_score", "kernel_avg_ms": round(k_avg_ms, 4),
                 "algorithmic_bytes_per_launch": bpp * P}
-    # the same kernel against its VALU issue bound (slot visits per second)
+    # the same kernel against its VALU issue bound (slot visits per second):
+    # one wave64 instruction per SIMD every 4 cycles, at the measured VALU
+    # count per slot when the counter summary matches the source, else the
+    # unrolled block's count
     slots = P * pr["n_groups"]
+    ctr = measured_counters(config, P)
+    vps = float(ctr["valu_per_slot"]) if ctr else float(VALU_PER_SLOT)
     s_achieved = slots / (k_avg_ms / 1e3) / 1e9
-    s_peak = PEAK_VALU_LANES / VALU_PER_SLOT / 1e9
+    s_peak = PEAK_VALU_LANES / vps / 1e9
     valu_issue = {"bound": "alu", "achieved": round(s_achieved, 1), "peak": round(s_peak, 1),
                   "unit": "Gslots/s", "frac": round(s_achieved / s_peak, 4), "kernel": "k_score",
-                  "slots_per_launch": slots, "valu_per_slot": VALU_PER_SLOT}
+                  "slots_per_launch": slots, "valu_per_slot": round(vps, 2),
+                  "valu_per_slot_from": "SQ counters" if ctr else "unrolled block"}
 
-    cpu = None
+    cpu = cpu1 = None
     if not args.no_cpu_baseline:
-        log("timing the CPU oracle ...")
+        log("timing the CPU oracle (all host threads, then one) ...")
         cpu = cpu_baseline(pr, pl, args.cpu_seconds)
+        cpu1 = cpu_baseline(pr, pl, args.cpu_seconds, threads=1)
 
     N = workload.total_requests(pr)
     out = {
         "metric": METRIC, "value": round(plans_per_s, 1), "unit": "plans/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
+        "ms_per_step": round(ms_step, 4),
+        "ms_per_step_median": round(step_ms[len(step_ms) // 2], 4),
+        "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "f32+f64", "data": "synthetic",
         "config": {"workload": "%s: %d groups (%d requests), %d instances in %d classes, "
-                               "%d models, %d plans" % (args.config, pr["n_groups"], N,
+                               "%d models, %d plans" % (config, pr["n_groups"], N,
                                                         pr["n_instances"], pr["n_classes"],
                                                         pr["n_models"], P),
                    "plans": P, "groups": pr["n_groups"], "instances": pr["n_instances"],
@@ -630,6 +755,7 @@ def main():
         "requests_per_s": round(plans_per_s * N, 1),
         "best_index": best_index, "best_score": best_score,
         "roofline": roofline, "valu_issue": valu_issue, "cpu_baseline": cpu,
+        "cpu_baseline_1core": cpu1,
     }
     if args.with_profile:
         out["config"]["workload"] += ", tables from a hardware profile"
