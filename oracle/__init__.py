@@ -74,6 +74,9 @@ class Oracle:
 
     def __init__(self, path: str | None = None):
         if path is None:
+            # QLM_ORACLE_LIB: another build of the same source (the sanitizer test)
+            path = os.environ.get("QLM_ORACLE_LIB")
+        if path is None:
             if not os.path.exists(_LIB):
                 build(force=False)
             path = _LIB

@@ -73,9 +73,13 @@ def _lib():
     global _gen
     with _lock:
         if _gen is None:
-            if not os.path.exists(_GEN_LIB):
-                build_generator(force=False)
-            lib = ctypes.CDLL(_GEN_LIB)
+            # QLM_GEN_LIB: another build of the same source (the sanitizer test)
+            path = os.environ.get("QLM_GEN_LIB")
+            if path is None:
+                if not os.path.exists(_GEN_LIB):
+                    build_generator(force=False)
+                path = _GEN_LIB
+            lib = ctypes.CDLL(path)
             lib.qlm_gen_plans.argtypes = [ctypes.c_uint64, ctypes.c_int64, ctypes.c_int64,
                                           ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                           ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
