@@ -302,16 +302,18 @@ class Oracle:
         return perm, qoff
 
     def place_group(self, problem, plans, p: int, group: int):
-        """Plan p with `group` moved to the EDF position of the queue giving the
-        lowest exact score (lowest queue on ties): dict perm, qoff, evict_bits,
-        score, queue."""
+        """Plan p with `group` moved to the place giving the lowest exact score:
+        the EDF position after the head of queue c, or (c >= I) the head of
+        queue c - I with its eviction flag set; the lowest c on ties.  A group
+        at its queue's head stays.  Returns a dict perm, qoff, evict_bits,
+        score, queue (= c)."""
         b = _Bound(problem, plans)
         if not 0 <= p < b.n_plans:
             raise ValueError("plan index out of range")
         G, I = b.G, int(problem["n_instances"])
         perm = np.empty(G, np.int32)
         qoff = np.empty(I + 1, np.int32)
-        ev = np.empty((G + 31) // 32, np.uint32) if plans.get("evict_bits") is not None else None
+        ev = np.empty((G + 31) // 32, np.uint32)
         sc = np.zeros(1)
         q = np.zeros(1, np.int32)
         if self.lib.oracle_place_group(ctypes.byref(b.problem), ctypes.byref(b.plans), p,
@@ -324,8 +326,9 @@ class Oracle:
     def local_search(self, problem, plans, p: int, window: int, max_steps: int,
                      threads: int = 0):
         """Steepest-descent search from plan p.  Returns a dict with the final
-        perm[G], qoff[I+1], evict_bits[ceil(G/32)] (None without flags), its
-        score, the number of steps applied and trace[max_steps]."""
+        perm[G], qoff[I+1], evict_bits[ceil(G/32)] (relocations set flags, so
+        they are returned even for start plans without), its score, the number
+        of steps applied and trace[max_steps]."""
         b = _Bound(problem, plans)
         if not 0 <= p < b.n_plans:
             raise ValueError("plan index out of range")
@@ -334,7 +337,7 @@ class Oracle:
         G, I = b.G, int(problem["n_instances"])
         perm = np.empty(G, np.int32)
         qoff = np.empty(I + 1, np.int32)
-        ev = np.empty((G + 31) // 32, np.uint32) if plans.get("evict_bits") is not None else None
+        ev = np.empty((G + 31) // 32, np.uint32)
         sc = np.zeros(1)
         steps = np.zeros(1, np.int32)
         trace = np.full(max(max_steps, 1), -1, np.int64)

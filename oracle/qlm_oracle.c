@@ -38,7 +38,7 @@
  *   best plan         argmin_p score_p, lowest p on ties.
  *
  * The plan search at the end of the file (local search with the scheduler's
- * reorder and reassign actions as moves) scores each move by building the
+ * reorder, reassign and evict actions as moves) scores each move by building the
  * moved plan and scoring it with the definition above, from scratch.
  *
  * The readings behind the choices that the paper leaves open (probability of
@@ -416,21 +416,32 @@ void oracle_apply_profile(const oracle_problem *pr, const oracle_profile *pf,
  * The paper's global scheduler places groups by solving the assignment
  * x_{g,i,j} of Sec. 7 as an LP and compares with EDF and with same-model
  * grouping (Secs. 2 and 8).  This library searches plans directly with the
- * scheduler's own actions on virtual queues as moves:
+ * scheduler's own actions on virtual queues as moves.  The first slot of a
+ * non-empty queue holds the group its instance is running; a group that has
+ * started does not go to another instance (Sec. 5, load balancing), and only
+ * an eviction puts a group ahead of it (Sec. 5, request eviction):
  *
- *   SWAP(s, d)  reordering within a queue: the groups at slots s and s + d
- *               (1 <= d <= W) trade places when both slots lie in one queue;
- *   MOVE(s, h)  reassignment (load balancing, Sec. 5): the group at slot s
- *               leaves its queue g and joins queue h != g, placed before the
- *               first group of h whose SLO is strictly later than its own
- *               (at the end of h when there is none).
+ *   SWAP(s, d)      reordering within a queue: the groups at slots s and
+ *                   s + d (1 <= d <= W) trade places when both slots lie in
+ *                   one queue and s is not its head;
+ *   MOVE(s, h)      reassignment (load balancing, Sec. 5): the group at slot s
+ *                   (not a head) leaves its queue g and joins queue h != g,
+ *                   placed before the first group of h after h's head whose
+ *                   SLO is strictly later than its own (at the end of h when
+ *                   there is none; the head of h when h is empty);
+ *   RELOCATE(s, h)  eviction: the group at slot s (not a head) leaves its
+ *                   queue and becomes the head of the non-empty queue h (its
+ *                   own queue or another), ahead of the running group, with
+ *                   its eviction flag set.
  *
- * A moved group keeps its eviction flag (the flag belongs to the group's
- * placement, not to the slot number).  Moves are numbered
- *   SWAP(s, d):  k = s*W + (d - 1)            s in [0, G), d in [1, W]
- *   MOVE(s, h):  k = G*W + s*I + h            s in [0, G), h in [0, I)
- * and a number whose partner slot lies in another queue (or beyond G), or
- * whose h is the group's own queue, names no move.
+ * Any other moved group keeps its eviction flag (the flag belongs to the
+ * group's placement, not to the slot number).  Moves are numbered
+ *   SWAP(s, d):      k = s*W + (d - 1)             s in [0, G), d in [1, W]
+ *   MOVE(s, h):      k = G*W + s*I + h             s in [0, G), h in [0, I)
+ *   RELOCATE(s, h):  k = G*W + G*I + s*I + h       s in [0, G), h in [0, I)
+ * and a number whose slot s is a queue's head, whose partner slot lies in
+ * another queue (or beyond G), whose h is the group's own queue (MOVE) or an
+ * empty queue (RELOCATE), names no move.
  *
  * One step scores every move (the exact score above of the plan the move
  * makes), takes the lowest score, the lowest k on ties, and applies that move
@@ -439,7 +450,7 @@ void oracle_apply_profile(const oracle_problem *pr, const oracle_profile *pf,
  */
 int64_t oracle_n_moves(int32_t G, int32_t I, int32_t W)
 {
-    return (int64_t)G * W + (int64_t)G * I;
+    return (int64_t)G * W + 2 * (int64_t)G * I;
 }
 
 /* queue holding slot s: the g with qoff[g] <= s < qoff[g+1] */
@@ -450,9 +461,42 @@ static int queue_of(const int32_t *qoff, int I, int32_t s)
     return -1;
 }
 
+/* The plan with the group at slot s (not a head) taken out of its queue and
+ * put into queue h: at the head with its flag set when `head`, else before
+ * the first group after h's head (as h stands without the group) whose SLO is
+ * strictly later, else at the end.  Written to (perm2, qoff2, flag2) queue by
+ * queue. */
+static void insert_into(const oracle_problem *pr, const int32_t *perm, const int32_t *qoff,
+                        const uint8_t *flag, int32_t s, int h, int head, int32_t *perm2,
+                        int32_t *qoff2, uint8_t *flag2)
+{
+    const int I = pr->n_instances;
+    const int32_t gi = perm[s];
+    const float slo_i = pr->grp_slo[gi];
+    int32_t out = 0;
+    for (int q = 0; q < I; ++q) {
+        qoff2[q] = out;
+        if (q == h && head) {
+            perm2[out] = gi;  flag2[out] = 1;  ++out;
+        }
+        int placed = (q != h) || head;
+        int seen = 0;                           /* groups of q already written */
+        for (int32_t u = qoff[q]; u < qoff[q + 1]; ++u) {
+            if (u == s) continue;                       /* the group leaves */
+            if (!placed && seen > 0 && pr->grp_slo[perm[u]] > slo_i) {
+                perm2[out] = gi;  flag2[out] = flag[s];  ++out;  placed = 1;
+            }
+            perm2[out] = perm[u];  flag2[out] = flag[u];  ++out;
+            ++seen;
+        }
+        if (!placed) { perm2[out] = gi;  flag2[out] = flag[s];  ++out; }
+    }
+    qoff2[I] = out;
+}
+
 /* Applies move k to the plan (perm, qoff, flag) of one plan; writes the new
  * plan to (perm2, qoff2, flag2).  Returns 1 when k names a move, else 0
- * (outputs untouched).  The new plan is built queue by queue as lists. */
+ * (outputs untouched). */
 int oracle_move_apply(const oracle_problem *pr, int32_t W, int64_t k,
                       const int32_t *perm, const int32_t *qoff, const uint8_t *flag,
                       int32_t *perm2, int32_t *qoff2, uint8_t *flag2)
@@ -463,7 +507,7 @@ int oracle_move_apply(const oracle_problem *pr, int32_t W, int64_t k,
         const int32_t s = (int32_t)(k / W), t = s + (int32_t)(k % W) + 1;
         if (t >= G) return 0;
         const int g = queue_of(qoff, I, s);
-        if (t >= qoff[g + 1]) return 0;
+        if (s == qoff[g] || t >= qoff[g + 1]) return 0;
         memcpy(perm2, perm, sizeof(int32_t) * G);
         memcpy(qoff2, qoff, sizeof(int32_t) * (I + 1));
         memcpy(flag2, flag, G);
@@ -471,33 +515,22 @@ int oracle_move_apply(const oracle_problem *pr, int32_t W, int64_t k,
         flag2[s] = flag[t];  flag2[t] = flag[s];
         return 1;
     }
-    const int64_t r = k - (int64_t)G * W;                        /* MOVE */
+    int64_t r = k - (int64_t)G * W;
+    const int relocate = r >= (int64_t)G * I;
+    if (relocate) r -= (int64_t)G * I;
     const int32_t s = (int32_t)(r / I);
     const int h = (int)(r % I);
     const int g = queue_of(qoff, I, s);
-    if (h == g) return 0;
-    const int32_t gi = perm[s];
-    const float slo_i = pr->grp_slo[gi];
-    int32_t out = 0;
-    for (int q = 0; q < I; ++q) {
-        qoff2[q] = out;
-        int placed = (q != h);
-        for (int32_t u = qoff[q]; u < qoff[q + 1]; ++u) {
-            if (u == s) continue;                       /* the group leaves g */
-            if (!placed && pr->grp_slo[perm[u]] > slo_i) {
-                perm2[out] = gi;  flag2[out] = flag[s];  ++out;  placed = 1;
-            }
-            perm2[out] = perm[u];  flag2[out] = flag[u];  ++out;
-        }
-        if (!placed) { perm2[out] = gi;  flag2[out] = flag[s];  ++out; }
-    }
-    qoff2[I] = out;
+    if (s == qoff[g]) return 0;                          /* the running group */
+    if (relocate ? qoff[h] == qoff[h + 1] : h == g) return 0;
+    insert_into(pr, perm, qoff, flag, s, h, relocate, perm2, qoff2, flag2);
     return 1;
 }
 
-/* Exact score of one plan given as arrays (flags one byte per slot). */
+/* Exact score of one plan given as arrays (flags one byte per slot; a search
+ * can set flags, so they are always passed). */
 static double score_one(const oracle_problem *pr, const int32_t *perm, const int32_t *qoff,
-                        const uint8_t *flag, int with_flags, uint32_t *words)
+                        const uint8_t *flag, uint32_t *words)
 {
     const int G = pr->n_groups;
     oracle_plans one;
@@ -505,13 +538,10 @@ static double score_one(const oracle_problem *pr, const int32_t *perm, const int
     one.ld = 1;
     one.perm = perm;
     one.qoff = qoff;
-    one.evict_bits = NULL;
-    if (with_flags) {
-        memset(words, 0, sizeof(uint32_t) * (size_t)((G + 31) / 32));
-        for (int s = 0; s < G; ++s)
-            if (flag[s]) words[s / 32] |= 1u << (s % 32);
-        one.evict_bits = words;
-    }
+    memset(words, 0, sizeof(uint32_t) * (size_t)((G + 31) / 32));
+    for (int s = 0; s < G; ++s)
+        if (flag[s]) words[s / 32] |= 1u << (s % 32);
+    one.evict_bits = words;
     double sc = NAN;
     if (oracle_plan(pr, &one, 0, NULL, NULL, NULL, &sc, NULL) != 0) return NAN;
     return sc;
@@ -531,8 +561,8 @@ static void take_plan(const oracle_problem *pr, const oracle_plans *pl, int64_t 
 /* Scores of moves of one plan given as arrays: ks[0..n) (NULL = every move,
  * n = oracle_n_moves).  A number that names no move scores +inf. */
 static void move_scores_of(const oracle_problem *pr, int32_t W, const int32_t *perm,
-                           const int32_t *qoff, const uint8_t *flag, int with_flags,
-                           const int64_t *ks, int64_t n, double *out, int n_threads)
+                           const int32_t *qoff, const uint8_t *flag, const int64_t *ks,
+                           int64_t n, double *out, int n_threads)
 {
     const int G = pr->n_groups, I = pr->n_instances;
 #ifdef _OPENMP
@@ -550,7 +580,7 @@ static void move_scores_of(const oracle_problem *pr, int32_t W, const int32_t *p
         for (int64_t j = 0; j < n; ++j) {
             const int64_t k = ks ? ks[j] : j;
             if (oracle_move_apply(pr, W, k, perm, qoff, flag, perm2, qoff2, flag2))
-                out[j] = score_one(pr, perm2, qoff2, flag2, with_flags, words);
+                out[j] = score_one(pr, perm2, qoff2, flag2, words);
             else
                 out[j] = INFINITY;
         }
@@ -569,7 +599,7 @@ int oracle_move_scores(const oracle_problem *pr, const oracle_plans *pl, int64_t
     uint8_t *flag = malloc(G);
     take_plan(pr, pl, p, perm, qoff, flag);
     if (!ks) n = oracle_n_moves(G, I, W);
-    move_scores_of(pr, W, perm, qoff, flag, pl->evict_bits != NULL, ks, n, out, n_threads);
+    move_scores_of(pr, W, perm, qoff, flag, ks, n, out, n_threads);
     free(perm); free(qoff); free(flag);
     return 0;
 }
@@ -584,7 +614,6 @@ int oracle_local_search(const oracle_problem *pr, const oracle_plans *pl, int64_
                         int n_threads)
 {
     const int G = pr->n_groups, I = pr->n_instances;
-    const int with_flags = pl->evict_bits != NULL;
     const int64_t nm = oracle_n_moves(G, I, W);
     int32_t *perm = malloc(sizeof(int32_t) * G), *perm2 = malloc(sizeof(int32_t) * G);
     int32_t *qoff = malloc(sizeof(int32_t) * (I + 1)), *qoff2 = malloc(sizeof(int32_t) * (I + 1));
@@ -592,11 +621,11 @@ int oracle_local_search(const oracle_problem *pr, const oracle_plans *pl, int64_
     uint32_t *words = malloc(sizeof(uint32_t) * ((G + 31) / 32));
     double *sc = malloc(sizeof(double) * (size_t)(nm > 0 ? nm : 1));
     take_plan(pr, pl, p, perm, qoff, flag);
-    double cur = score_one(pr, perm, qoff, flag, with_flags, words);
+    double cur = score_one(pr, perm, qoff, flag, words);
     int32_t done = 0;
     for (int32_t t = 0; t < max_steps; ++t) trace[t] = -1;
     for (int32_t t = 0; t < max_steps; ++t) {
-        move_scores_of(pr, W, perm, qoff, flag, with_flags, NULL, nm, sc, n_threads);
+        move_scores_of(pr, W, perm, qoff, flag, NULL, nm, sc, n_threads);
         int64_t best = -1;
         double bs = INFINITY;
         for (int64_t k = 0; k < nm; ++k)
@@ -606,7 +635,7 @@ int oracle_local_search(const oracle_problem *pr, const oracle_plans *pl, int64_
         memcpy(perm, perm2, sizeof(int32_t) * G);
         memcpy(qoff, qoff2, sizeof(int32_t) * (I + 1));
         memcpy(flag, flag2, G);
-        cur = score_one(pr, perm, qoff, flag, with_flags, words);
+        cur = score_one(pr, perm, qoff, flag, words);
         trace[t] = best;
         ++done;
     }
@@ -708,44 +737,27 @@ int oracle_seed_plan(const oracle_problem *pr, int32_t policy, int32_t *perm_out
 }
 
 /* ------------------------------------------------------------------------
- * Placement of one group (a new arrival parked anywhere in the plan, or a
- * group whose wait violates its SLO): the scheduler call of Sec. 5 for one
- * group.  The group leaves its queue and is put into queue h before the first
- * group of h (as h stands after the removal) whose SLO is strictly later (at
- * the end when there is none), keeping its eviction flag; the h giving the
- * lowest exact plan score wins, the lowest h on ties.
+ * Placement of one group (a new arrival parked behind the head of a queue, or
+ * a group whose wait violates its SLO): the scheduler call of Sec. 5 for one
+ * group.  The group leaves its slot and goes to one of 2I places c:
+ *   c = h       queue h before the first group after h's head (as h stands
+ *               without the group) whose SLO is strictly later, at the end
+ *               when there is none, at the head of an empty h; its flag kept
+ *               (the MOVE of the search; with h its own queue, a reinsertion);
+ *   c = I + h   the head of the non-empty queue h, ahead of the running
+ *               group, with its eviction flag set (the RELOCATE of the search).
+ * The c giving the lowest exact plan score wins, the lowest c on ties (c = 0
+ * when every score is NaN).  A group at its queue's head is running and stays
+ * where it is: the plan comes back unchanged and c is its queue.
  */
-static void place_into(const oracle_problem *pr, const int32_t *perm, const int32_t *qoff,
-                       const uint8_t *flag, int32_t s, int h, int32_t *perm2, int32_t *qoff2,
-                       uint8_t *flag2)
-{
-    const int I = pr->n_instances;
-    const int32_t gi = perm[s];
-    const float slo_i = pr->grp_slo[gi];
-    int32_t out = 0;
-    for (int q = 0; q < I; ++q) {
-        qoff2[q] = out;
-        int placed = (q != h);
-        for (int32_t u = qoff[q]; u < qoff[q + 1]; ++u) {
-            if (u == s) continue;
-            if (!placed && pr->grp_slo[perm[u]] > slo_i) {
-                perm2[out] = gi;  flag2[out] = flag[s];  ++out;  placed = 1;
-            }
-            perm2[out] = perm[u];  flag2[out] = flag[u];  ++out;
-        }
-        if (!placed) { perm2[out] = gi;  flag2[out] = flag[s];  ++out; }
-    }
-    qoff2[I] = out;
-}
 
 /* Places group `group` of plan p; writes the new plan, its exact score and the
- * chosen queue.  Returns 0, or -1 when the group is not in the plan. */
+ * chosen place c.  Returns 0, or -1 when the group is not in the plan. */
 int oracle_place_group(const oracle_problem *pr, const oracle_plans *pl, int64_t p, int32_t group,
                        int32_t *perm_out, int32_t *qoff_out, uint32_t *evict_out, double *score,
                        int32_t *queue)
 {
     const int G = pr->n_groups, I = pr->n_instances;
-    const int with_flags = pl->evict_bits != NULL;
     int32_t *perm = malloc(sizeof(int32_t) * G), *perm2 = malloc(sizeof(int32_t) * G);
     int32_t *qoff = malloc(sizeof(int32_t) * (I + 1)), *qoff2 = malloc(sizeof(int32_t) * (I + 1));
     uint8_t *flag = malloc(G), *flag2 = malloc(G);
@@ -754,16 +766,27 @@ int oracle_place_group(const oracle_problem *pr, const oracle_plans *pl, int64_t
     int32_t s = -1;
     for (int u = 0; u < G; ++u)
         if (perm[u] == group) s = u;
-    int best = -1;
-    double bs = INFINITY;
     if (s >= 0) {
-        for (int h = 0; h < I; ++h) {
-            place_into(pr, perm, qoff, flag, s, h, perm2, qoff2, flag2);
-            const double sc = score_one(pr, perm2, qoff2, flag2, with_flags, words);
-            if (sc < bs) { bs = sc; best = h; }
+        const int g = queue_of(qoff, I, s);
+        int best = -1;
+        if (s == qoff[g]) {                              /* running: it stays */
+            memcpy(perm2, perm, sizeof(int32_t) * G);
+            memcpy(qoff2, qoff, sizeof(int32_t) * (I + 1));
+            memcpy(flag2, flag, G);
+            best = g;
+        } else {
+            double bs = INFINITY;
+            for (int c = 0; c < 2 * I; ++c) {
+                const int head = c >= I, h = head ? c - I : c;
+                if (head && qoff[h] == qoff[h + 1]) continue;   /* nothing to evict */
+                insert_into(pr, perm, qoff, flag, s, h, head, perm2, qoff2, flag2);
+                const double sc = score_one(pr, perm2, qoff2, flag2, words);
+                if (sc < bs) { bs = sc; best = c; }
+            }
+            if (best < 0) best = 0;
+            insert_into(pr, perm, qoff, flag, s, best >= I ? best - I : best, best >= I, perm2,
+                        qoff2, flag2);
         }
-        if (best < 0) best = 0;
-        place_into(pr, perm, qoff, flag, s, best, perm2, qoff2, flag2);
         memcpy(perm_out, perm2, sizeof(int32_t) * G);
         memcpy(qoff_out, qoff2, sizeof(int32_t) * (I + 1));
         if (evict_out) {
@@ -771,7 +794,7 @@ int oracle_place_group(const oracle_problem *pr, const oracle_plans *pl, int64_t
             for (int u = 0; u < G; ++u)
                 if (flag2[u]) evict_out[u / 32] |= 1u << (u % 32);
         }
-        *score = score_one(pr, perm2, qoff2, flag2, with_flags, words);
+        *score = score_one(pr, perm2, qoff2, flag2, words);
         *queue = best;
     }
     free(perm); free(perm2); free(qoff); free(qoff2); free(flag); free(flag2); free(words);

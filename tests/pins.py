@@ -384,16 +384,32 @@ def pin_argmin_ties(orc):
 
 
 # ---------------------------------------------------------------------------
-# Plan search (local search with reorder and reassign moves)
+# Plan search (local search with reorder, reassign and evict moves)
 #
-# SWAP(s, d), k = s*W + d - 1: the groups at slots s and s+d trade places when
-# both are in one queue.  MOVE(s, h), k = G*W + s*I + h: the group at slot s
-# leaves its queue for queue h != g, placed before the first group of h with a
-# strictly later SLO (else at the end).  Eviction flags go with their group.
+# The first slot of a non-empty queue holds its running group, which no move
+# takes and only a relocation passes.  SWAP(s, d), k = s*W + d - 1: the groups
+# at slots s and s+d trade places when both are in one queue.  MOVE(s, h),
+# k = G*W + s*I + h: the group at slot s leaves its queue for queue h != g,
+# placed before the first group after h's head with a strictly later SLO
+# (else at the end; the head of an empty h).  RELOCATE(s, h),
+# k = G*W + G*I + s*I + h: the group at slot s becomes the head of the
+# non-empty queue h with its eviction flag set.  Other flags go with their
+# group.
 
 
 def _queues_of(perm, qoff):
     return [list(perm[qoff[g]:qoff[g + 1]]) for g in range(len(qoff) - 1)]
+
+
+def _n_moves(G, I, W):
+    return G * W + 2 * G * I
+
+
+def _edf_index(q, slo, item_slo):
+    """Where a group goes in the list q (its head excluded from the search):
+    before the first later SLO after the head, else the end."""
+    later = [j for j in range(1, len(q)) if slo[q[j][0]] > item_slo]
+    return later[0] if later else len(q)
 
 
 def _apply_move_py(pr, perm, qoff, flag, W, k):
@@ -405,24 +421,31 @@ def _apply_move_py(pr, perm, qoff, flag, W, k):
     for g in range(I):
         for s in range(qoff[g], qoff[g + 1]):
             owner[s] = g
+    heads = {int(qoff[g]) for g in range(I) if qoff[g] < qoff[g + 1]}
     # carry (group, flag) pairs per queue
     qs = [[(int(perm[s]), int(flag[s])) for s in range(qoff[g], qoff[g + 1])] for g in range(I)]
     if k < G * W:
         s, d = divmod(k, W)
         t = s + d + 1
-        if t >= G or owner[s] != owner[t]:
+        if t >= G or owner[s] != owner[t] or s in heads:
             return None
         g = owner[s]
         a, b = s - qoff[g], t - qoff[g]
         qs[g][a], qs[g][b] = qs[g][b], qs[g][a]
-    else:
+    elif k < G * W + G * I:
         s, h = divmod(k - G * W, I)
         g = owner[s]
-        if h == g:
+        if h == g or s in heads:
             return None
         item = qs[g].pop(s - qoff[g])
-        later = [j for j, (i, _) in enumerate(qs[h]) if slo[i] > slo[item[0]]]
-        qs[h].insert(later[0] if later else len(qs[h]), item)
+        qs[h].insert(_edf_index(qs[h], slo, slo[item[0]]), item)
+    else:
+        s, h = divmod(k - G * W - G * I, I)
+        g = owner[s]
+        if s in heads or not qs[h]:
+            return None
+        item = qs[g].pop(s - qoff[g])
+        qs[h].insert(0, (item[0], 1))
     flat = [x for q in qs for x in q]
     lens = [len(q) for q in qs]
     return (np.array([x[0] for x in flat], np.int32),
@@ -451,41 +474,62 @@ def _one_plan(perm, qoff, flag, with_flags):
 
 def pin_moves_by_hand(orc):
     """Moves worked by hand on one plan: queues [[0, 1, 2], [3], [4, 5, 6]] with
-    SLOs 0:5 1:1 2:9 3:3 4:5 5:1 6:9, group 2 flagged (slot 2), W = 2."""
+    SLOs 0:5 1:1 2:9 3:3 4:5 5:1 6:9, group 2 flagged (slot 2), W = 2.  Slots
+    0, 3 and 4 hold the running groups."""
     slo = [5, 1, 9, 3, 5, 1, 9]
     pr = problem([(1, 10.0, 0.0, 0, float(x)) for x in slo], [(100.0, 0)] * 3)
     perm = np.array([0, 1, 2, 3, 4, 5, 6], np.int32)
     qoff = np.array([0, 3, 4, 7], np.int32)
     flag = np.array([0, 0, 1, 0, 0, 0, 0], np.uint8)
     G, I, W = 7, 3, 2
+    MV, RL = G * W, G * W + G * I
 
     def mv(k):
         return orc.move_apply(pr, perm, qoff, flag, W, k)
-    # SWAP(0, 2) = k 1: groups 0 and 2 trade places, and the flag goes with group 2
-    p2, q2, f2 = mv(0 * W + 1)
-    assert list(p2) == [2, 1, 0, 3, 4, 5, 6] and list(q2) == [0, 3, 4, 7]
-    assert list(f2) == [1, 0, 0, 0, 0, 0, 0]
-    # SWAP(2, 1) = k 4: slot 3 is in the next queue, no move; SWAP(6, 1): beyond G
-    assert mv(2 * W + 0) is None and mv(6 * W + 0) is None
-    # MOVE(slot 3 = group 3, SLO 3, to queue 2 = [4(5), 5(1), 6(9)]): before group 4
-    p2, q2, f2 = mv(G * W + 3 * I + 2)
-    assert list(p2) == [0, 1, 2, 3, 4, 5, 6] and list(q2) == [0, 3, 3, 7]
-    # MOVE(slot 0 = group 0, SLO 5, to queue 2): 5 is not later than group 4's 5,
-    # nor 1; group 6 (9) is the first later one
-    p2, q2, f2 = mv(G * W + 0 * I + 2)
-    assert list(p2) == [1, 2, 3, 4, 5, 0, 6] and list(q2) == [0, 2, 3, 7]
-    assert list(f2) == [0, 1, 0, 0, 0, 0, 0]
+
+    def check(k, p, q, f):
+        r = mv(k)
+        assert r is not None, k
+        assert list(r[0]) == p and list(r[1]) == q and list(r[2]) == f, (k, r)
+    # SWAP(1, 1) = k 2: groups 1 and 2 trade places, and the flag goes with group 2
+    check(1 * W + 0, [0, 2, 1, 3, 4, 5, 6], [0, 3, 4, 7], [0, 1, 0, 0, 0, 0, 0])
+    check(5 * W + 0, [0, 1, 2, 3, 4, 6, 5], [0, 3, 4, 7], [0, 0, 1, 0, 0, 0, 0])
+    # SWAP(0, 1), SWAP(0, 2), SWAP(4, 1): a running group; SWAP(2, 1): slot 3 is
+    # in the next queue; SWAP(6, 1): beyond G
+    for k in (0, 1, 4 * W, 2 * W, 6 * W):
+        assert mv(k) is None, k
+    # MOVE(slot 1 = group 1, SLO 1, to queue 2 = [4(5), 5(1), 6(9)]): the head 4
+    # stays first; 5's SLO 1 is not later; before 6 (9)
+    check(MV + 1 * I + 2, [0, 2, 3, 4, 5, 1, 6], [0, 2, 3, 7], [0, 1, 0, 0, 0, 0, 0])
+    # MOVE(slot 5 = group 5, SLO 1, to queue 0 = [0(5), 1(1), 2(9)]): behind the
+    # running group 0 although its SLO is later; before 2 (9)
+    check(MV + 5 * I + 0, [0, 1, 5, 2, 3, 4, 6], [0, 4, 5, 7], [0, 0, 0, 1, 0, 0, 0])
     # MOVE(slot 2 = flagged group 2, SLO 9, to queue 1 = [3(3)]): at the end, flag kept
-    p2, q2, f2 = mv(G * W + 2 * I + 1)
-    assert list(p2) == [0, 1, 3, 2, 4, 5, 6] and list(q2) == [0, 2, 4, 7]
-    assert list(f2) == [0, 0, 0, 1, 0, 0, 0]
-    # MOVE(slot 5 = group 5, SLO 1, to queue 0 = [0(5), 1(1), 2(9)]): at the head
-    p2, q2, f2 = mv(G * W + 5 * I + 0)
-    assert list(p2) == [5, 0, 1, 2, 3, 4, 6] and list(q2) == [0, 4, 5, 7]
-    assert list(f2) == [0, 0, 0, 1, 0, 0, 0]
-    # MOVE to the group's own queue: no move
-    assert mv(G * W + 4 * I + 2) is None
-    assert orc.n_moves(G, I, W) == G * W + G * I
+    check(MV + 2 * I + 1, [0, 1, 3, 2, 4, 5, 6], [0, 2, 4, 7], [0, 0, 0, 1, 0, 0, 0])
+    # MOVE of a running group (slots 0, 3, 4), MOVE to the group's own queue: no move
+    for k in (MV + 0 * I + 1, MV + 3 * I + 2, MV + 4 * I + 0, MV + 5 * I + 2):
+        assert mv(k) is None, k
+    # RELOCATE(slot 2 = group 2, its own queue 0): ahead of the running group 0,
+    # flagged (it already was)
+    check(RL + 2 * I + 0, [2, 0, 1, 3, 4, 5, 6], [0, 3, 4, 7], [1, 0, 0, 0, 0, 0, 0])
+    # RELOCATE(slot 5 = group 5, queue 1 = [3]): [5*, 3]; the flag is set
+    check(RL + 5 * I + 1, [0, 1, 2, 5, 3, 4, 6], [0, 3, 5, 7], [0, 0, 1, 1, 0, 0, 0])
+    # RELOCATE(slot 1 = group 1, queue 2): [1*, 4, 5, 6]; group 2 keeps its flag
+    check(RL + 1 * I + 2, [0, 2, 3, 1, 4, 5, 6], [0, 2, 3, 7], [0, 1, 0, 1, 0, 0, 0])
+    # RELOCATE(slot 6 = group 6, its own queue 2): [6*, 4, 5]
+    check(RL + 6 * I + 2, [0, 1, 2, 3, 6, 4, 5], [0, 3, 4, 7], [0, 0, 1, 0, 1, 0, 0])
+    # RELOCATE of a running group: no move
+    for k in (RL + 0 * I + 0, RL + 3 * I + 0, RL + 4 * I + 1):
+        assert mv(k) is None, k
+    assert orc.n_moves(G, I, W) == G * W + 2 * G * I
+    # an empty queue: MOVE makes the group its head, RELOCATE names no move
+    pr2 = problem([(1, 10.0, 0.0, 0, 1.0), (1, 10.0, 0.0, 0, 2.0)], [(100.0, 0)] * 2)
+    p0, q0, f0 = np.array([0, 1], np.int32), np.array([0, 2, 2], np.int32), np.zeros(2, np.uint8)
+    r = orc.move_apply(pr2, p0, q0, f0, 1, 2 * 1 + 1 * 2 + 1)
+    assert list(r[0]) == [0, 1] and list(r[1]) == [0, 1, 2] and list(r[2]) == [0, 0]
+    assert orc.move_apply(pr2, p0, q0, f0, 1, 2 + 4 + 1 * 2 + 1) is None
+    r = orc.move_apply(pr2, p0, q0, f0, 1, 2 + 4 + 1 * 2 + 0)
+    assert list(r[0]) == [1, 0] and list(r[1]) == [0, 2, 2] and list(r[2]) == [1, 0]
 
 
 def _search_case(rng, G, I, M=2, C=2, evict=True):
@@ -499,13 +543,14 @@ def pin_moves_independent(orc):
     rng = np.random.default_rng(77)
     for G, I, W, evict in [(7, 3, 3, True), (9, 2, 9, False), (5, 4, 1, True)]:
         pr, pl = _search_case(rng, G, I, evict=evict)
+        nm = _n_moves(G, I, W)
         for p in range(pl["n_plans"]):
             perm = pl["perm"][:, p].copy()
             qoff = pl["qoff"][:, p].copy()
             flag = _flags_of(pl, p, G)
             sc = orc.move_scores(pr, pl, p, W)
-            assert sc.size == G * W + G * I
-            for k in range(G * W + G * I):
+            assert sc.size == nm
+            for k in range(nm):
                 a = orc.move_apply(pr, perm, qoff, flag, W, k)
                 b = _apply_move_py(pr, perm, qoff, flag, W, k)
                 if b is None:
@@ -514,34 +559,75 @@ def pin_moves_independent(orc):
                 assert a is not None, (G, I, W, p, k)
                 for x, y in zip(a, b):
                     assert np.array_equal(x, y), (G, I, W, p, k, a, b)
-                ref = orc.plan_detail(pr, _one_plan(*b, evict), 0)["score"]
+                ref = orc.plan_detail(pr, _one_plan(*b, True), 0)["score"]
                 assert sc[k] == ref, (k, sc[k], ref)
             # a sample of moves by number gives the same scores
-            ks = np.array([0, G * W + 1, G * W + G * I - 1, 2], np.int64)
+            ks = np.array([0, G * W + 1, G * W + G * I - 1, nm - 1, G * W + G * I + 2, 2],
+                          np.int64)
             assert np.array_equal(orc.move_scores(pr, pl, p, W, ks=ks), sc[ks])
 
 
 def pin_search_by_hand(orc):
     """Two identical instances (400 tok/s); queue 0 holds group 0 (2 x 200
-    tokens, 1 s) then group 1 (3 x 100 tokens), both with a 0.5 s SLO; queue 1
-    is empty.  Group 1 waits 1 s and misses: score 3.  With G = 2, W = 1, I = 2:
-    k0 SWAP(0,1): group 0 now waits 0.75 s and misses, score 2; k1 SWAP(1,1):
-    beyond G; k2 MOVE(0,0), k4 MOVE(1,0): own queue; k3 MOVE(0,1) and k5
-    MOVE(1,1): one group per queue, nobody waits, score 0.  The tie goes to
-    k3; after it nothing improves on 0."""
+    tokens, 1 s; running) then group 1 (3 x 100 tokens), both with a 0.5 s SLO;
+    queue 1 is empty.  Group 1 waits 1 s and misses: score 3.  With G = 2,
+    W = 1, I = 2 (MOVEs from k = 2, RELOCATEs from k = 6): k0 SWAP(0, 1), k2,
+    k3, k6, k7: the running group; k1: beyond G; k4 MOVE(1, 0): own queue;
+    k9 RELOCATE(1, 1): queue 1 is empty; k5 MOVE(1, 1): alone in queue 1,
+    nobody waits, score 0; k8 RELOCATE(1, 0): group 1 first (waits E = 0),
+    group 0 waits 0.75 s and misses, score 2.  The search takes k5, after which
+    nothing improves on 0."""
     pr = problem([(2, 200.0, 0.0, 0, 0.5), (3, 100.0, 0.0, 0, 0.5)], [(400.0, 0), (400.0, 0)])
     pl = plans([[[0, 1], []]], 2)
     sc = orc.move_scores(pr, pl, 0, 1)
-    assert list(sc) == [2.0, np.inf, np.inf, 0.0, np.inf, 0.0], sc
+    inf = np.inf
+    assert list(sc) == [inf, inf, inf, inf, inf, 0.0, inf, inf, 2.0, inf], sc
     r = orc.local_search(pr, pl, 0, 1, 4)
-    assert r["steps"] == 1 and list(r["trace"]) == [3, -1, -1, -1]
-    assert list(r["perm"]) == [1, 0] and list(r["qoff"]) == [0, 1, 2] and r["score"] == 0.0
-    # a plan that meets every SLO does not move; neither does one with no moves
+    assert r["steps"] == 1 and list(r["trace"]) == [5, -1, -1, -1]
+    assert list(r["perm"]) == [0, 1] and list(r["qoff"]) == [0, 1, 2] and r["score"] == 0.0
+    # a plan that meets every SLO does not move
     r = orc.local_search(pr, plans([[[0], [1]]], 2), 0, 1, 4)
     assert r["steps"] == 0 and list(r["perm"]) == [0, 1] and r["score"] == 0.0
-    pr1 = problem([(2, 200.0, 0.0, 0, 0.5), (3, 100.0, 0.0, 0, 0.5)], [(400.0, 0)])
-    r = orc.local_search(pr1, plans([[[0, 1]]], 2), 0, 0, 3)
-    assert r["steps"] == 0 and r["score"] == 3.0 and list(r["trace"]) == [-1, -1, -1]
+    # one instance: only RELOCATE(1, 0) = k 3 is a move.  With E = 0.25 s group 1
+    # waits 0.25 s (met) and group 0 1 s (misses): 2 < 3, taken.  With E = 0.6 s
+    # both miss: 5, not taken.
+    for E, steps, score in ((0.25, 1, 2.0), (0.6, 0, 3.0)):
+        pr1 = problem([(2, 200.0, 0.0, 0, 0.5), (3, 100.0, 0.0, 0, 0.5)], [(400.0, 0)],
+                      evict_cost=E)
+        assert list(orc.move_scores(pr1, plans([[[0, 1]]], 2), 0, 0)) == [inf, inf, inf,
+                                                                          5.0 - 3.0 * (E < 0.5)]
+        r = orc.local_search(pr1, plans([[[0, 1]]], 2), 0, 0, 3)
+        assert r["steps"] == steps and r["score"] == score, (E, r)
+        if steps:
+            assert list(r["trace"]) == [3, -1, -1] and list(r["perm"]) == [1, 0]
+            assert list(_flags_of({"evict_bits": r["evict_bits"].reshape(-1, 1)}, 0, 2)) == [1, 0]
+        else:
+            assert list(r["trace"]) == [-1, -1, -1] and list(r["perm"]) == [0, 1]
+
+
+def pin_relocate_by_hand(orc):
+    """Head-of-line blocking (Sec. 5, request eviction): one 100 tok/s instance
+    runs a batch group (1 request of 1000 tokens, 10 s, SLO 60 s); behind it an
+    interactive group (2 requests of 10 tokens, SLO 1 s) waits 10 s and both
+    its requests miss: score 2.  Relocating it to the head with E = 0.5 s: it
+    waits 0.5 s, the batch group 0.5 + 0.2 s, every SLO met: score 0.  With
+    E = 2 s the interactive group still misses (2 s > 1 s) and the batch group
+    meets its SLO: score 2, not below 2, so the plan stays.  With E = 1 s the
+    wait equals the SLO, which is met (a strict miss): score 0."""
+    for E, score, moved in ((0.5, 0.0, True), (2.0, 2.0, False), (1.0, 0.0, True)):
+        pr = problem([(1, 1000.0, 0.0, 0, 60.0), (2, 10.0, 0.0, 0, 1.0)], [(100.0, 0)],
+                     evict_cost=E)
+        pl = plans([[[0, 1]]], 2)
+        sc = orc.move_scores(pr, pl, 0, 1)
+        # k0 SWAP(0, 1): running; k1 beyond G; k2, k3 MOVE: running / own queue;
+        # k4 RELOCATE(0, 0): running; k5 RELOCATE(1, 0)
+        assert list(sc) == [np.inf] * 5 + [0.0 if moved else 2.0], (E, sc)
+        d = orc.plan_detail(pr, _one_plan([1, 0], [0, 2], [1, 0], True), 0)
+        assert d["wait_mean"][0] == E and d["wait_mean"][1] == E + 0.2, d["wait_mean"]
+        r = orc.local_search(pr, pl, 0, 1, 2)
+        assert r["score"] == score and r["steps"] == (1 if moved else 0), (E, r)
+        if moved:
+            assert list(r["perm"]) == [1, 0] and list(r["trace"]) == [5, -1]
 
 
 def pin_search_steepest(orc):
@@ -557,14 +643,14 @@ def pin_search_steepest(orc):
             perm = pl["perm"][:, p].copy()
             qoff = pl["qoff"][:, p].copy()
             flag = _flags_of(pl, p, G)
-            cur = orc.plan_detail(pr, _one_plan(perm, qoff, flag, evict), 0)["score"]
+            cur = orc.plan_detail(pr, _one_plan(perm, qoff, flag, True), 0)["score"]
             for t in range(13):
                 best, bs = -1, np.inf
-                for k in range(G * W + G * I):
+                for k in range(_n_moves(G, I, W)):
                     b = _apply_move_py(pr, perm, qoff, flag, W, k)
                     if b is None:
                         continue
-                    v = orc.plan_detail(pr, _one_plan(*b, evict), 0)["score"]
+                    v = orc.plan_detail(pr, _one_plan(*b, True), 0)["score"]
                     if v < bs:
                         best, bs = k, v
                 if t == 12 or not bs < cur:
@@ -575,9 +661,8 @@ def pin_search_steepest(orc):
             assert r["steps"] == t, (r["steps"], t)
             assert np.array_equal(r["perm"], perm) and np.array_equal(r["qoff"], qoff)
             assert r["score"] == cur
-            if evict:
-                assert np.array_equal(_flags_of({"evict_bits": r["evict_bits"].reshape(-1, 1)},
-                                                0, G), flag)
+            assert np.array_equal(_flags_of({"evict_bits": r["evict_bits"].reshape(-1, 1)}, 0, G),
+                                  flag)
 
 
 # ---------------------------------------------------------------------------
@@ -683,16 +768,22 @@ def pin_seed_restated(orc):
 # Placement of one group (arrival / violation trigger)
 
 
-def _place_py(pr, perm, qoff, flag, s, h):
-    """Group at slot s out of its queue, into queue h before the first later SLO
-    (as h stands after the removal), restated on Python lists."""
+def _place_py(pr, perm, qoff, flag, s, c):
+    """Group at slot s out of its queue, into place c (restated on Python
+    lists): c < I the EDF position of queue c after its head (as it stands
+    after the removal), c >= I the head of queue c - I, flagged.  None when
+    that queue is empty (nothing to evict)."""
     I = int(pr["n_instances"])
     slo = pr["grp_slo"]
     qs = [[(int(perm[u]), int(flag[u])) for u in range(qoff[g], qoff[g + 1])] for g in range(I)]
     g = next(q for q in range(I) if qoff[q] <= s < qoff[q + 1])
     item = qs[g].pop(s - qoff[g])
-    later = [j for j, (i, _) in enumerate(qs[h]) if slo[i] > slo[item[0]]]
-    qs[h].insert(later[0] if later else len(qs[h]), item)
+    if c < I:
+        qs[c].insert(_edf_index(qs[c], slo, slo[item[0]]), item)
+    else:
+        if not qs[c - I]:
+            return None
+        qs[c - I].insert(0, (item[0], 1))
     flat = [x for q in qs for x in q]
     return (np.array([x[0] for x in flat], np.int32),
             np.concatenate([[0], np.cumsum([len(q) for q in qs])]).astype(np.int32),
@@ -700,31 +791,43 @@ def _place_py(pr, perm, qoff, flag, s, h):
 
 
 def pin_place_by_hand(orc):
-    """Queue 0 holds groups 0, 1, 2 (1 s each, SLOs 0.5, 0.6, 0.7 s), queue 1 is
-    empty: groups 1 and 2 wait 1 and 2 s and miss.  Placing group 2: in queue 0
-    it goes back to the end (no later SLO), still missing (score 3 + 4); alone in
-    queue 1 it waits 0 s (score 3): queue 1.  With one instance, a group with a
-    0.5 s SLO behind two 10 s groups moves to the head and everything is met."""
+    """Queue 0 holds groups 0, 1, 2 (1.33, 1 and 1.33 s; SLOs 0.5, 0.6, 0.7 s),
+    queue 1 is empty: groups 1 and 2 miss (score 7).  Placing group 2: back at
+    the end of queue 0 (no later SLO; 7), alone in queue 1 (3), or at the head
+    of queue 0 (groups 0 and 1 miss: 5): queue 1.  With one instance, a group
+    with a 0.5 s SLO behind two 1 s groups with 10 s SLOs goes behind the
+    running group (it misses: 5) or, evicting it, ahead (everything met when
+    E = 0: c = I + 0 = 1; with E = 0.6 s it misses there too, a tie at 5 that
+    the lower c wins)."""
     pr = problem([(2, 200.0, 0.0, 0, 0.5), (3, 100.0, 0.0, 0, 0.6), (4, 100.0, 0.0, 0, 0.7)],
                  [(300.0, 0), (300.0, 0)])
     pl = plans([[[0, 1, 2], []]], 3)
     r = orc.place_group(pr, pl, 0, 2)
     assert r["queue"] == 1 and list(r["perm"]) == [0, 1, 2] and list(r["qoff"]) == [0, 2, 3]
     assert r["score"] == 3.0, r["score"]
-    pr = problem([(1, 100.0, 0.0, 0, 10.0), (1, 100.0, 0.0, 0, 10.0), (5, 20.0, 0.0, 0, 0.5)],
-                 [(100.0, 0)])
-    r = orc.place_group(pr, plans([[[0, 1, 2]]], 3), 0, 2)
-    assert r["queue"] == 0 and list(r["perm"]) == [2, 0, 1] and r["score"] == 0.0
-    # equal SLOs are not later: a group goes behind the groups that share its SLO
+    for E, c, perm, flags, score in ((0.0, 1, [2, 0, 1], [1, 0, 0], 0.0),
+                                     (0.6, 0, [0, 2, 1], [0, 0, 0], 5.0)):
+        pr = problem([(1, 100.0, 0.0, 0, 10.0), (1, 100.0, 0.0, 0, 10.0), (5, 20.0, 0.0, 0, 0.5)],
+                     [(100.0, 0)], evict_cost=E)
+        r = orc.place_group(pr, plans([[[0, 1, 2]]], 3), 0, 2)
+        assert r["queue"] == c and list(r["perm"]) == perm and r["score"] == score, (E, r)
+        assert list(_flags_of({"evict_bits": r["evict_bits"].reshape(-1, 1)}, 0, 3)) == flags
+    # equal SLOs are not later: group 0 goes behind the groups that share its
+    # SLO (waits 0, 1, 2 s against 1 s: one miss either way, so c = 0 wins
+    # the tie with the head place)
     pr = problem([(1, 100.0, 0.0, 0, 1.0)] * 3, [(100.0, 0)])
+    r = orc.place_group(pr, plans([[[2, 0, 1]]], 3), 0, 0)
+    assert list(r["perm"]) == [2, 1, 0] and r["queue"] == 0 and r["score"] == 1.0, r
+    # the running group stays where it is
     r = orc.place_group(pr, plans([[[2, 0, 1]]], 3), 0, 2)
-    assert list(r["perm"]) == [0, 1, 2], r["perm"]
+    assert list(r["perm"]) == [2, 0, 1] and r["queue"] == 0 and r["score"] == 1.0, r
 
 
 def pin_place_restated(orc):
-    """Random plans: the placed plan is the first minimum over every queue of
-    the placement restated in Python and scored as a plan; for other queues the
-    candidate is the reassignment move MOVE(s, h)."""
+    """Random plans: the placed plan is the first minimum over every place of
+    the placement restated in Python and scored as a plan; the places in other
+    queues are the moves MOVE(s, h), the head places RELOCATE(s, h); a running
+    group stays."""
     rng = np.random.default_rng(31)
     for G, I, evict in [(9, 3, True), (12, 4, False), (6, 1, True)]:
         pr, pl = _random_case(rng, G=G, I=I, M=2, C=2, P=3, evict=evict)
@@ -733,23 +836,31 @@ def pin_place_restated(orc):
             qoff = pl["qoff"][:, p].copy()
             flag = _flags_of(pl, p, G)
             ms = orc.move_scores(pr, pl, p, 0)
-            for group in (0, G - 1, G // 2):
+            assert ms.size == _n_moves(G, I, 0)
+            for group in range(G):
                 s = int(np.flatnonzero(perm == group)[0])
                 g = next(q for q in range(I) if qoff[q] <= s < qoff[q + 1])
-                best, bs, bplan = -1, np.inf, None
-                for h in range(I):
-                    c = _place_py(pr, perm, qoff, flag, s, h)
-                    v = orc.plan_detail(pr, _one_plan(*c, evict), 0)["score"]
-                    if h != g:
-                        assert v == ms[s * I + h], (h, v, ms[s * I + h])
-                    if v < bs:
-                        best, bs, bplan = h, v, c
                 r = orc.place_group(pr, pl, p, group)
+                got = _flags_of({"evict_bits": r["evict_bits"].reshape(-1, 1)}, 0, G)
+                if s == qoff[g]:
+                    assert r["queue"] == g and np.array_equal(r["perm"], perm)
+                    assert np.array_equal(r["qoff"], qoff) and np.array_equal(got, flag)
+                    continue
+                best, bs, bplan = -1, np.inf, None
+                for c in range(2 * I):
+                    cand = _place_py(pr, perm, qoff, flag, s, c)
+                    if cand is None:
+                        continue
+                    v = orc.plan_detail(pr, _one_plan(*cand, True), 0)["score"]
+                    if c < I and c != g:
+                        assert v == ms[s * I + c], (c, v, ms[s * I + c])
+                    if c >= I:
+                        assert v == ms[G * I + s * I + c - I], (c, v)
+                    if v < bs:
+                        best, bs, bplan = c, v, cand
                 assert r["queue"] == best and r["score"] == bs, (r["queue"], best, r["score"], bs)
                 assert np.array_equal(r["perm"], bplan[0]) and np.array_equal(r["qoff"], bplan[1])
-                if evict:
-                    assert np.array_equal(_flags_of({"evict_bits": r["evict_bits"].reshape(-1, 1)},
-                                                    0, G), bplan[2])
+                assert np.array_equal(got, bplan[2])
 
 
 # ---------------------------------------------------------------------------
@@ -984,6 +1095,6 @@ ALL_PINS = [pin_deterministic_queue, pin_variance_queue, pin_normal_table, pin_s
             pin_eviction_costs, pin_throughput_per_queue, pin_invariants, pin_half_at_mean,
             pin_identical_instances_symmetry, pin_monte_carlo, pin_edf_special_case,
             pin_grouping_special_case, pin_argmin_ties, pin_moves_by_hand, pin_moves_independent,
-            pin_search_by_hand, pin_search_steepest, pin_seed_by_hand, pin_seed_special_cases,
+            pin_search_by_hand, pin_relocate_by_hand, pin_search_steepest, pin_seed_by_hand, pin_seed_special_cases,
             pin_seed_restated, pin_place_by_hand, pin_place_restated, pin_fcfs_by_hand,
             pin_fcfs_exploded, pin_fcfs_monte_carlo, pin_profile_by_hand, pin_profile_scaling]

@@ -60,18 +60,36 @@ MUTANTS = [
     ("theta_of_first_queue", "const double theta = (double)pr->inst_tput[g];",
      "const double theta = (double)pr->inst_tput[0];"),
     # plan search
-    ("insert_before_equal_slo", "if (!placed && pr->grp_slo[perm[u]] > slo_i) {",
-     "if (!placed && pr->grp_slo[perm[u]] >= slo_i) {"),
-    ("insert_before_earlier_slo", "if (!placed && pr->grp_slo[perm[u]] > slo_i) {",
-     "if (!placed && pr->grp_slo[perm[u]] < slo_i) {"),
+    ("insert_before_equal_slo", "seen > 0 && pr->grp_slo[perm[u]] > slo_i) {",
+     "seen > 0 && pr->grp_slo[perm[u]] >= slo_i) {"),
+    ("insert_before_earlier_slo", "seen > 0 && pr->grp_slo[perm[u]] > slo_i) {",
+     "seen > 0 && pr->grp_slo[perm[u]] < slo_i) {"),
+    ("insert_passes_running_head", "if (!placed && seen > 0 && ", "if (!placed && "),
     ("swap_flags_stay", "flag2[s] = flag[t];  flag2[t] = flag[s];", "(void)0;"),
     ("move_flag_dropped", "perm2[out] = gi;  flag2[out] = flag[s];  ++out;  placed = 1;",
      "perm2[out] = gi;  flag2[out] = 0;  ++out;  placed = 1;"),
-    ("swap_across_queues", "if (t >= qoff[g + 1]) return 0;", "(void)g;"),
+    ("swap_across_queues", "if (s == qoff[g] || t >= qoff[g + 1]) return 0;",
+     "if (s == qoff[g]) return 0;"),
+    ("swap_takes_running_head", "if (s == qoff[g] || t >= qoff[g + 1]) return 0;",
+     "if (t >= qoff[g + 1]) return 0;"),
     ("swap_distance_short", "t = s + (int32_t)(k % W) + 1;", "t = s + (int32_t)(k % W);"),
     ("move_index_transposed",
      "const int32_t s = (int32_t)(r / I);\n    const int h = (int)(r % I);",
      "const int32_t s = (int32_t)(r % G);\n    const int h = (int)(r / G);"),
+    ("move_takes_running_head",
+     "if (s == qoff[g]) return 0;                          /* the running group */", "(void)0;"),
+    ("relocate_flag_not_set", "perm2[out] = gi;  flag2[out] = 1;  ++out;",
+     "perm2[out] = gi;  flag2[out] = flag[s];  ++out;"),
+    ("relocate_into_empty_queue", "if (relocate ? qoff[h] == qoff[h + 1] : h == g) return 0;",
+     "if (relocate ? 0 : h == g) return 0;"),
+    ("relocate_not_to_own_queue", "if (relocate ? qoff[h] == qoff[h + 1] : h == g) return 0;",
+     "if (relocate ? (qoff[h] == qoff[h + 1] || h == g) : h == g) return 0;"),
+    ("relocate_index_off_by_one", "if (relocate) r -= (int64_t)G * I;",
+     "if (relocate) r -= (int64_t)G * I - 1;"),
+    ("relocate_to_edf_place", "insert_into(pr, perm, qoff, flag, s, h, relocate, perm2, qoff2, flag2);",
+     "insert_into(pr, perm, qoff, flag, s, h, 0, perm2, qoff2, flag2);"),
+    ("relocate_moves_not_counted", "return (int64_t)G * W + 2 * (int64_t)G * I;",
+     "return (int64_t)G * W + (int64_t)G * I;"),
     ("last_move_on_ties", "if (sc[k] < bs) { bs = sc[k]; best = k; }",
      "if (sc[k] <= bs) { bs = sc[k]; best = k; }"),
     ("move_on_equal_score", "if (best < 0 || !(bs < cur)) break;",
@@ -89,15 +107,16 @@ MUTANTS = [
      "const double d = A[q] / (double)pr->inst_tput[q] + (K[q] + s);"),
     ("seed_swap_not_kept", "            K[best] += s;", "            (void)s;"),
     # placement of one group
-    ("place_last_queue_on_ties", "if (sc < bs) { bs = sc; best = h; }",
-     "if (sc <= bs) { bs = sc; best = h; }"),
+    ("place_last_place_on_ties", "if (sc < bs) { bs = sc; best = c; }",
+     "if (sc <= bs) { bs = sc; best = c; }"),
     ("place_own_queue_skipped",
-     "            place_into(pr, perm, qoff, flag, s, h, perm2, qoff2, flag2);\n            const double sc",
-     "            if (qoff[h] <= s && s < qoff[h + 1]) continue;\n"
-     "            place_into(pr, perm, qoff, flag, s, h, perm2, qoff2, flag2);\n            const double sc"),
-    ("place_before_equal_slo",
-     "            if (!placed && pr->grp_slo[perm[u]] > slo_i) {\n                perm2[out] = gi;  flag2[out] = flag[s];  ++out;  placed = 1;\n            }\n            perm2[out] = perm[u];  flag2[out] = flag[u];  ++out;\n        }\n        if (!placed) { perm2[out] = gi;  flag2[out] = flag[s];  ++out; }\n    }\n    qoff2[I] = out;\n}\n\n/* Places",
-     "            if (!placed && pr->grp_slo[perm[u]] >= slo_i) {\n                perm2[out] = gi;  flag2[out] = flag[s];  ++out;  placed = 1;\n            }\n            perm2[out] = perm[u];  flag2[out] = flag[u];  ++out;\n        }\n        if (!placed) { perm2[out] = gi;  flag2[out] = flag[s];  ++out; }\n    }\n    qoff2[I] = out;\n}\n\n/* Places"),
+     "                insert_into(pr, perm, qoff, flag, s, h, head, perm2, qoff2, flag2);\n",
+     "                if (!head && h == g) continue;\n"
+     "                insert_into(pr, perm, qoff, flag, s, h, head, perm2, qoff2, flag2);\n"),
+    ("place_without_head_places", "for (int c = 0; c < 2 * I; ++c) {",
+     "for (int c = 0; c < I; ++c) {"),
+    ("place_running_group_moved", "if (s == qoff[g]) {                              /* running: it stays */",
+     "if (0) {"),
     # per-request (FCFS) variant
     ("fcfs_own_requests_dropped", "const double Er  = EW + (double)r * (mu / theta);",
      "const double Er  = EW;"),
