@@ -256,32 +256,41 @@ def measured_counters(config: str, plans: int):
 
 
 def move_counts(problem, plans, p, window):
-    """Valid moves of plan p (swaps within a queue, reassignments) and the
-    positions the reassignment screen visits for them: for a group moving to
-    queue h, itself at its insertion point and every position of h from there
-    on (one position when it goes to the end or into an empty queue)."""
+    """Valid moves of plan p by kind (swaps within a queue, reassignments,
+    relocations to a queue's head) and the positions the reassignment screen
+    visits for them: for a group moving to queue h, itself at its insertion
+    point after h's head and every position of h from there on (one position
+    when it goes to the end or into an empty queue).  A queue's head (its
+    running group) takes part in no move."""
     import numpy as np
     G, I = problem["n_groups"], problem["n_instances"]
     perm = plans["perm"][:, p]
     qoff = plans["qoff"][:, p]
     slo = np.asarray(problem["grp_slo"], np.float32)
     lens = np.diff(qoff)
-    swaps = int(sum(max(int(L) - d, 0) for L in lens for d in range(1, window + 1)))
-    moves = G * (I - 1)
+    swaps = int(sum(max(int(L) - 1 - d, 0) for L in lens for d in range(1, window + 1)))
+    busy = int(np.sum(lens > 0))
+    movable = G - busy
+    moves = movable * (I - 1)
+    relocations = movable * busy
     owner = np.repeat(np.arange(I), lens)
     g_of = np.empty(G, np.int64)
     g_of[perm] = owner
+    head = np.zeros(G, bool)
+    head[perm[qoff[:-1][lens > 0]]] = True
     visits = 0
     for h in range(I):
         b, e = int(qoff[h]), int(qoff[h + 1])
-        x = slo[g_of != h]
+        x = slo[(g_of != h) & ~head]
         if e == b:
             visits += x.size
             continue
-        pmax = np.maximum.accumulate(slo[perm[b:e]])
-        pos = np.searchsorted(pmax, x, side="right")          # first pmax > slo
-        visits += int(np.sum(np.where(pos == e - b, 1, (e - b) - pos + 1)))
-    return swaps + moves, moves, visits
+        L = e - b
+        pmax = np.maximum.accumulate(slo[perm[b + 1:e]]) if L > 1 else np.zeros(0, np.float32)
+        pos = 1 + np.searchsorted(pmax, x, side="right")       # first later SLO after the head
+        visits += int(np.sum(np.where(pos == L, 1, L - pos + 1)))
+    return {"valid": swaps + moves + relocations, "swaps": swaps, "moves": moves,
+            "relocations": relocations, "visits": visits}
 
 
 def cpu_search_baseline(problem, plans, window, seconds: float):
@@ -308,8 +317,9 @@ def cpu_search_baseline(problem, plans, window, seconds: float):
 
 def bench_search(args):
     """One step = one step of the local search on every chain: cache the plan,
-    screen every move (removals, swaps, reassignments), re-score exactly the
-    moves that can still be the best, pick and apply."""
+    screen every move (removals, swaps, reassignments, relocations), re-score
+    exactly the moves that can still be the best, pick and apply."""
+    import numpy as np
     import torch
     from paper_2407_00047_amd import qlm, workload
     dev = torch.device("cuda:0")
@@ -322,12 +332,12 @@ def bench_search(args):
     ws = qlm.search_workspace(dpr, B, W, device=dev)
     nm = qlm.search_n_moves(G, I, W)
     counts = [move_counts(pr, pl, p, W) for p in range(B)]
-    valid = sum(c[0] for c in counts)
-    visits = sum(c[2] for c in counts)
-    log("search %s: G=%d I=%d chains=%d window=%d, %d valid moves per step" % (
-        args.config, G, I, B, W, valid))
-    out = qlm.DevicePlans(torch.empty_like(dpl.perm), torch.empty_like(dpl.qoff),
-                          None if dpl.evict_bits is None else torch.empty_like(dpl.evict_bits), B)
+    valid = sum(c["valid"] for c in counts)
+    visits = sum(c["visits"] for c in counts)
+    kinds = {k: sum(c[k] for c in counts) // B for k in ("swaps", "moves", "relocations")}
+    log("search %s: G=%d I=%d chains=%d window=%d, %d valid moves per step %s" % (
+        args.config, G, I, B, W, valid, kinds))
+    out = qlm.plans_like(dpl, G)
     for _ in range(max(args.warmup, 1)):
         r = qlm.local_search(dpr, dpl, W, K, ws=ws, out=out)
     torch.cuda.synchronize()
@@ -344,6 +354,9 @@ def bench_search(args):
     total_ms = e0.elapsed_time(e1)
     steps = r["steps"].cpu().numpy()
     applied = int(steps.sum())
+    # the same search again, untimed, for the kinds of the moves it applied
+    tr = qlm.local_search(dpr, dpl, W, K, trace=True, ws=ws, out=out)["trace"].cpu().numpy()
+    relocs = int(np.sum(tr >= G * W + G * I))
     # the reassignment screen on the start plans (the positions it visits are
     # known exactly there), timed over repeated launches
     reps = 10
@@ -375,11 +388,14 @@ def bench_search(args):
         "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "f32+f64", "data": "synthetic",
         "config": {"workload": "plan search on %s: %d groups (%d requests), %d instances, "
-                               "%d start plans, window %d, %d valid moves per plan and step"
-                               % (args.config, G, N, I, B, W, valid // B),
+                               "%d start plans, window %d, %d valid moves per plan and step "
+                               "(%d swaps, %d reassignments, %d relocations)"
+                               % (args.config, G, N, I, B, W, valid // B, kinds["swaps"],
+                                  kinds["moves"], kinds["relocations"]),
                    "chains": B, "window": W, "groups": G, "instances": I,
-                   "moves_per_step": valid},
+                   "moves_per_step": valid, "moves_per_plan_by_kind": kinds},
         "moves_applied": applied,
+        "relocations_applied": relocs,
         "score_start_to_end": [float(x) for x in r["score"].cpu().numpy()[:4]],
         "roofline": roofline, "cpu_baseline": cpu,
     }

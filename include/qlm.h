@@ -206,8 +206,9 @@ typedef struct qlm_plans_out {
     int64_t plan_stride;         /* elements between slot rows, >= n_plans      */
     int32_t  *perm;              /* [G][stride]                                  */
     int32_t  *qoff;              /* [I+1][stride]                                */
-    uint32_t *evict_bits;        /* [ceil(G/32)][stride]; required when the start
-                                    plans have eviction bits, else ignored      */
+    uint32_t *evict_bits;        /* [ceil(G/32)][stride]; required by the search
+                                    and the placements (a relocation sets flags,
+                                    also in plans that had none)                */
 } qlm_plans_out;
 
 /*
@@ -216,16 +217,27 @@ typedef struct qlm_plans_out {
  * and same-model grouping (Secs. 2, 8).  This library instead improves plans
  * by local search whose moves are the scheduler's actions on virtual queues
  * (Sec. 5: reordering within a queue, reassigning a group to another
- * instance), each scored exactly by the plan score above:
+ * instance, evicting the running group), each scored exactly by the plan
+ * score above.  The first slot of a non-empty queue holds the group its
+ * instance is running: a group that has started stays on its instance
+ * (Sec. 5), and only an eviction puts a group ahead of it.
  *
- *   SWAP(s, d)  k = s*W + d - 1     (s in [0,G), d in [1,W]): the groups at
- *               slots s and s + d trade places, if both slots lie in one queue;
- *   MOVE(s, h)  k = G*W + s*I + h   (h in [0,I)): the group at slot s leaves
- *               its queue g for queue h != g, placed before the first group of
- *               h whose SLO is strictly later than its own (else at the end).
+ *   SWAP(s, d)      k = s*W + d - 1          (s in [0,G), d in [1,W]): the
+ *                   groups at slots s and s + d trade places, if both slots
+ *                   lie in one queue and s is not its head;
+ *   MOVE(s, h)      k = G*W + s*I + h        (h in [0,I)): the group at slot s
+ *                   (not a head) leaves its queue g for queue h != g, placed
+ *                   before the first group after h's head whose SLO is
+ *                   strictly later than its own (else at the end; into an
+ *                   empty h, as its head);
+ *   RELOCATE(s, h)  k = G*W + G*I + s*I + h  (h in [0,I)): the group at slot s
+ *                   (not a head) becomes the head of the non-empty queue h
+ *                   (its own or another) ahead of the running group, and its
+ *                   eviction flag is set (it pays evict_cost at its start).
  *
- * A moved group keeps its eviction flag.  A number k whose partner slot lies
- * in another queue or beyond G, or whose h is the group's own queue, names no
+ * Any other moved group keeps its eviction flag.  A number k whose slot s is
+ * a queue's head, whose partner slot lies in another queue or beyond G, whose
+ * h is the group's own queue (MOVE) or an empty queue (RELOCATE), names no
  * move.  A move's score is the exact plan score (the arithmetic and summation
  * order of qlm_rwt_score_exact) of the plan the move makes; the library
  * computes it incrementally, from the first position the move changes.
@@ -273,7 +285,8 @@ int qlm_search_screen(const qlm_problem *problem, const qlm_plans *plans, int32_
  * the steps are those of a search that scores every move exactly.
  *   start   the start plans (read before any output is written, so `out` may
  *           name the same arrays)
- *   out     the final plans
+ *   out     the final plans, with their eviction words (required; QLM_ERR_ARG
+ *           when evict_bits is NULL)
  *   score   [P] device out or NULL: exact score of each final plan
  *   steps   [P] device out or NULL: moves applied
  *   trace   [P][max_steps] device out or NULL: the move applied at each step,
@@ -286,19 +299,27 @@ int qlm_local_search(const qlm_problem *problem, const qlm_plans *start,
 
 /*
  * Placement of one group in every plan: the scheduler call of Sec. 5 when a
- * group arrives (the caller parks it anywhere in the plan first) or when its
- * wait violates its SLO.  In plan p the group leaves its queue and goes into
- * queue h before the first group of h (as h stands after the removal) whose
- * SLO is strictly later, at the end when there is none, keeping its eviction
- * flag; of the I choices (its own queue included) the one with the lowest
- * exact plan score wins, the lowest h on ties.  Only the two queues that
- * change are walked, from the first position that changes.
- *   start/out  as for qlm_local_search (out may name the start arrays)
+ * group arrives (the caller parks it behind the head of any non-empty queue
+ * first) or when its wait violates its SLO (request eviction is how it can go
+ * ahead of a running group).  In plan p the group leaves its slot and goes to
+ * one of 2I places c:
+ *   c = h       (h in [0,I)) queue h before the first group after h's head (as
+ *               h stands without the group) whose SLO is strictly later, at
+ *               the end when there is none, at the head of an empty h; its
+ *               eviction flag kept (MOVE; with h its own queue, a reinsertion)
+ *   c = I + h   the head of the non-empty queue h, ahead of its running group,
+ *               with the group's eviction flag set (RELOCATE)
+ * The place with the lowest exact plan score wins, the lowest c on ties.  A
+ * group at its queue's head is running and stays: the plan is unchanged and c
+ * is its queue.  Only the two queues that change are walked, from the first
+ * position that changes.
+ *   start/out  as for qlm_local_search (out may name the start arrays; its
+ *              eviction words are required)
  *   group      the group's id; every plan holds it
  *   ws         device workspace of at least qlm_search_workspace_bytes(problem,
  *              P, 0), 256-byte aligned, scratch
  *   score [P]  device out or NULL: exact score of each placed plan
- *   queue [P]  device out or NULL: the queue chosen
+ *   queue [P]  device out or NULL: the place c chosen
  */
 int qlm_place_group(const qlm_problem *problem, const qlm_plans *start,
                     const qlm_plans_out *out, int32_t group, void *ws, size_t ws_bytes,
@@ -315,9 +336,9 @@ int qlm_place_group(const qlm_problem *problem, const qlm_plans *start,
  *                    problem, P, 0) bytes, 256-byte aligned)
  *   qlm_place_step   places `group` in every plan, as qlm_place_group does;
  *                    score [P] and queue [P] (device out or NULL): each
- *                    plan's exact score after the placement, the queue chosen
+ *                    plan's exact score after the placement, the place chosen
  *   qlm_place_end    writes the plans (as qlm_place_group writes them, with
- *                    eviction bits when out has them) and their exact scores
+ *                    their eviction words, required) and their exact scores
  *                    (score [P] or NULL); the session may continue after it
  * Every call names the same problem and plan count.  The workspace is the
  * session's state: between qlm_place_begin and the last call that uses it, no

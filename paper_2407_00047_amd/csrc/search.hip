@@ -3,14 +3,22 @@
 // include/qlm.h.
 //
 // Moves are the scheduler's actions on virtual queues (reordering within a
-// queue, reassignment to another instance: Sec. 5); the paper itself places
-// groups with an LP (Sec. 7) and compares with EDF and same-model grouping.
-//   SWAP(s, d)  k = s*W + d - 1     the groups at slots s and s + d (one queue)
-//                                   trade places
-//   MOVE(s, h)  k = G*W + s*I + h   the group at slot s joins queue h != its
-//                                   own, before the first group of h whose SLO
-//                                   is strictly later (else at the end)
-// A moved group keeps its eviction flag.
+// queue, reassignment to another instance, eviction: Sec. 5); the paper
+// itself places groups with an LP (Sec. 7) and compares with EDF and
+// same-model grouping.  The first slot of a non-empty queue holds the group
+// its instance is running: no move takes it, and only RELOCATE passes it.
+//   SWAP(s, d)      k = s*W + d - 1         the groups at slots s and s + d
+//                                           (one queue) trade places
+//   MOVE(s, h)      k = G*W + s*I + h       the group at slot s joins queue
+//                                           h != its own, before the first
+//                                           group after h's head whose SLO is
+//                                           strictly later (else at the end;
+//                                           the head of an empty h)
+//   RELOCATE(s, h)  k = G*W + G*I + s*I + h the group at slot s becomes the
+//                                           head of the non-empty queue h (its
+//                                           own or another), its eviction flag
+//                                           set
+// Any other moved group keeps its eviction flag.
 //
 // Exact scores.  A move changes at most two queues, each from one position
 // on.  For every chain (a plan being improved) k_sstate caches, per slot, the
@@ -43,8 +51,13 @@
 // D = infinity (re-scored exactly), as does one whose walk meets a variance
 // that single precision cannot hold.  A queue that loses the moved group is
 // screened with its variance ahead in double precision (no cancellation), and
-// a MOVE's bound adds the bounds of both its queues.  Exact scores (of the
-// candidates) walk both queues exactly.
+// a MOVE's or another queue's RELOCATE's bound adds the bounds of both its
+// queues.  A RELOCATE within one queue walks two shifted stretches (the
+// groups it passes gain its tokens and variance; past its old slot only the
+// costs change) and forms the position after its old slot afresh; where
+// nothing ahead of that position has variance its indicator would not be
+// formed from the exact score's sums, so the move is re-scored exactly.
+// Exact scores (of the candidates) walk both queues exactly.
 //
 // Kernels
 //   k_srank    once per call: the groups ranked by SLO (partial counts per
@@ -59,19 +72,22 @@
 //              s without s (for the MOVEs of s), and screened SWAP(s, d); the
 //              positions past the changes are walked in step by the wavefront
 //   k_fmove    one wavefront per (target queue h, 64 groups adjacent in SLO
-//              order): screened MOVE; the positions past the insertion points
-//              are walked in step by the whole wavefront (one record read per
+//              order): screened MOVE, and (a second launch) screened RELOCATE
+//              into another queue; the positions past the insertion points are
+//              walked in step by the whole wavefront (one record read per
 //              position for all 64 moves)
+//   k_frel     one lane per slot: screened RELOCATE within the slot's queue
 //   k_sbound / k_sselect / k_sexact   the bound min(F + D), the candidates,
 //              their exact scores
 //   k_spick    lowest (exact score, k) of the candidates; applied when it
 //              improves on the plan, else the chain has converged
 //   k_sout     final plans back to the caller's slot-major layout
-//   k_sswap / k_smove   exact scores of every move, one lane per move
-//              (qlm_search_moves)
+//   k_sswap / k_smove / k_sreloc   exact scores of every move, one lane per
+//              move (qlm_search_moves)
 //   k_place_eval / k_place_pick   placement of one group (qlm_place_group):
-//              one wavefront per (plan, queue) scores the group placed there
-//              exactly; the lowest score is applied
+//              one wavefront per (plan, place) scores the group placed there
+//              (the EDF position after a queue's head, or a queue's head with
+//              eviction) exactly; the lowest score is applied
 //   k_seedrank / k_seedassign / k_seedwrite   seed plans (qlm_seed_plans):
 //              EDF or same-model order, each group to the queue with the
 //              smallest drain time after it (one wavefront per seed)
@@ -126,8 +142,8 @@ struct GRec {
 };
 
 // A chain's slot record, in slot order: the group's record with its eviction
-// flag in bit 8, the running maximum of the SLOs of the queue up to this slot,
-// and the slot's queue.
+// flag in bit 8, the running maximum of the SLOs of the queue's groups after
+// its head up to this slot (-inf at the head), and the slot's queue.
 struct SRec {
     double a, b;
     float slo;
@@ -196,8 +212,10 @@ struct SearchArgs {
     int32_t *dq;                  // [4] placement: the queues a placement changed
                                   // (every queue from the lower to the higher),
                                   // the group's slot and queue
-    int32_t nwg_a, nwg_b, nwg;    // per chain: k_sswap, k_smove (per queue), total
-    int32_t nwg_f, nws;           // per chain: k_fswap (d = 0..W), all screen workgroups
+    int32_t nwg_a, nwg_b, nwg;    // per chain: k_sswap, k_smove and k_sreloc (per
+                                  // queue), total
+    int32_t nwg_f, nwg_r, nws;    // per chain: k_fswap (d = 0..W), k_frel, all screen
+                                  // workgroups
     int64_t n_moves;
     double *move_score;           // [B][n_moves] or null (exact kernels)
     int64_t *trace;               // [B][max_steps] or null
@@ -351,6 +369,14 @@ __device__ inline int insertion_point_wave(const SRec *sr, int bq, int eq, float
         if (m) return u0 + (int)__builtin_ctzll(m);
     }
     return eq;
+}
+
+// The EDF position of queue [bq, eq) for a group with SLO slo: the insertion
+// point among the groups after the head (the running maxima leave the head
+// out), or the head of an empty queue.
+__device__ inline int edf_point(const SRec *sr, int bq, int eq, float slo)
+{
+    return bq == eq ? bq : insertion_point(sr, bq + 1, eq, slo);
 }
 
 // (score, k) is better than (s2, k2): lower score, then lower k.  A NaN score
@@ -654,7 +680,7 @@ __global__ __launch_bounds__(kThreads) void k_sstate(SearchArgs a, int force)
             x.slo = gr.slo;
             x.nmf = gr.nm | (flag[u] ? kFlagBit : 0u);
             x.q = (uint32_t)g;
-            mx = gr.slo;
+            mx = u == bq ? -INFINITY : gr.slo;     // the running head is never passed
             inv[i] = u;
         }
         for (int o = 1; o < kWave; o <<= 1) {
@@ -749,7 +775,7 @@ __global__ __launch_bounds__(kThreads) void k_sswap(SearchArgs a)
         } else {
             const int64_t k = (int64_t)s * W + (d - 1);
             double score = INFINITY;
-            if (s + d < eq) {
+            if (s + d < eq && s != bq) {
                 Run r = start_at(a, sr, ss, s, bq, g);
                 for (int u = s; u < eq; ++u) {
                     const int v = u == s ? s + d : (u == s + d ? s : u);
@@ -794,7 +820,7 @@ __global__ __launch_bounds__(kThreads) void k_smove(SearchArgs a)
         const int g = (int)x.q;
         const int64_t k = (int64_t)G * a.W + (int64_t)s * I + h;
         double score = INFINITY;
-        if (g != h) {
+        if (g != h && s != qof[g]) {
             const int bq = qof[h], eq = qof[h + 1];
             const double theta = (double)a.inst_tput[h];
             const int cls = clampi(a.inst_class[h], 0, a.C - 1);
@@ -803,7 +829,7 @@ __global__ __launch_bounds__(kThreads) void k_smove(SearchArgs a)
                 w = Run{0.0, 0.0, 0.0, 0.0, model0_of(a, h)};
                 visit(w, x, theta, cls, a);
             } else {
-                const int p = insertion_point(sr, bq, eq, x.slo);
+                const int p = edf_point(sr, bq, eq, x.slo);
                 if (p == eq) {
                     w = start_at(a, sr, ss, eq - 1, bq, h);
                     visit(w, sr[eq - 1], theta, cls, a);
@@ -825,6 +851,56 @@ __global__ __launch_bounds__(kThreads) void k_smove(SearchArgs a)
     block_best(best, bk, ls, lk);
     if (threadIdx.x == 0) {
         const int64_t o = b * a.nwg + a.nwg_a + (int64_t)h * a.nwg_b + wg;
+        a.wmin_s[o] = best;
+        a.wmin_i[o] = bk;
+    }
+}
+
+// RELOCATE(s, h): one lane per (slot s, queue h); the group goes first in h,
+// flagged, and h's groups follow it in order (its own slot left out when h is
+// its own queue).
+__global__ __launch_bounds__(kThreads) void k_sreloc(SearchArgs a)
+{
+    __shared__ double ls[kWaves];
+    __shared__ int64_t lk[kWaves];
+    const int G = a.G, I = a.I;
+    const int per_chain = I * a.nwg_b;
+    const int64_t b = blockIdx.x / per_chain;
+    const int h = (blockIdx.x % per_chain) / a.nwg_b;
+    const int wg = blockIdx.x % a.nwg_b;
+    if (a.done[b]) return;
+    const SRec *__restrict__ sr = a.srec + b * G;
+    const int32_t *__restrict__ qof = a.qof + b * (I + 1);
+    const int s = wg * kThreads + threadIdx.x;
+    double best = INFINITY;
+    int64_t bk = INT64_MAX;
+    if (s < G) {
+        SRec x = sr[s];
+        const int g = (int)x.q;
+        const int64_t k = (int64_t)G * a.W + (int64_t)G * I + (int64_t)s * I + h;
+        const int bq = qof[h], eq = qof[h + 1];
+        double score = INFINITY;
+        if (s != qof[g] && bq < eq) {
+            x.nmf |= kFlagBit;
+            const double theta = (double)a.inst_tput[h];
+            const int cls = clampi(a.inst_class[h], 0, a.C - 1);
+            Run w{0.0, 0.0, 0.0, 0.0, model0_of(a, h)};
+            visit(w, x, theta, cls, a);
+            for (int u = bq; u < eq; ++u)
+                if (u != s) visit(w, sr[u], theta, cls, a);
+            score = g == h ? total_with(a.T + b * (I + 1), a.Q + b * I, I, g, w.sc)
+                           : total_with2(a.T + b * (I + 1), a.Q + b * I, I, g, a.R[b * G + s], h,
+                                         w.sc);
+            if (better(score, k, best, bk)) {
+                best = score;
+                bk = k;
+            }
+        }
+        if (a.move_score) a.move_score[b * a.n_moves + k] = score;
+    }
+    block_best(best, bk, ls, lk);
+    if (threadIdx.x == 0) {
+        const int64_t o = b * a.nwg + a.nwg_a + (int64_t)(I + h) * a.nwg_b + wg;
         a.wmin_s[o] = best;
         a.wmin_i[o] = bk;
     }
@@ -1021,7 +1097,7 @@ __global__ __launch_bounds__(kThreads) void k_fswap(SearchArgs a)
                     on = true;
                 }
             }
-        } else if (s + d < eq) {
+        } else if (s + d < eq && s != bq) {
             valid = true;
             screen_visit(r, rec(s + d), theta, inv_theta, cls, vscale, eps, tab, a, force, swc);
             for (int u = s + 1; u < s + d; ++u)
@@ -1088,11 +1164,13 @@ __global__ __launch_bounds__(kThreads) void k_fswap(SearchArgs a)
     if (threadIdx.x == 0) a.smin[b * a.nws + wg] = m;
 }
 
-// Screened MOVE: one wavefront per (target queue h, 64 groups adjacent in SLO
-// order).  Each lane scores its group's insertion point and the position after
-// it with running sums; past that, the queue is the old one shifted by the
-// group's tokens, variance and the change of costs, walked by the whole
-// wavefront in step from the earliest insertion point.
+// Screened MOVE (REL: RELOCATE into another queue, whose insertion point is
+// the head of h and whose group is flagged): one wavefront per (target queue
+// h, 64 groups adjacent in SLO order).  Each lane scores its group's insertion
+// point and the position after it with running sums; past that, the queue is
+// the old one shifted by the group's tokens, variance and the change of costs,
+// walked by the whole wavefront in step from the earliest insertion point.
+template <bool REL>
 __global__ __launch_bounds__(kThreads) void k_fmove(SearchArgs a)
 {
     __shared__ float2 tab[qlm_tail::kCells];
@@ -1114,7 +1192,7 @@ __global__ __launch_bounds__(kThreads) void k_fmove(SearchArgs a)
     // the tail records' staging buffer (the tails are staged after a barrier)
     float *pmax = reinterpret_cast<float *>(stage);
     constexpr int kPmaxSlots = (int)(kStage * sizeof(TRec) / sizeof(float));
-    const bool pm_lds = eq - bq <= kPmaxSlots;
+    const bool pm_lds = !REL && eq - bq <= kPmaxSlots;
     for (int k = threadIdx.x; k < qlm_tail::kCells; k += kThreads) tab[k] = a.tail[k];
     if (pm_lds)
         for (int u = bq + (int)threadIdx.x; u < eq; u += kThreads) pmax[u - bq] = sr[u].pmax;
@@ -1133,17 +1211,22 @@ __global__ __launch_bounds__(kThreads) void k_fmove(SearchArgs a)
     if (r < G) {
         const int i = a.by_slo[r];
         s = clampi(a.inv[b * G + i], 0, G - 1);
-        const SRec x = sr[s];
+        SRec x = sr[s];
         g = (int)x.q;
-        valid = g != h;
+        // a running group never moves; RELOCATE needs a group to evict
+        valid = g != h && s != qof[g] && (!REL || bq < eq);
+        if (REL) x.nmf |= kFlagBit;
         if (valid) {
             Run w;
             if (bq == eq) {
                 w = Run{0.0, 0.0, 0.0, 0.0, model0_of(a, h)};
                 screen_visit(w, x, theta, inv_theta, cls, vscale, eps, tab, a, force);
             } else {
-                p = pm_lds ? insertion_point_lds(pmax, bq, eq, x.slo)
-                           : insertion_point(sr, bq, eq, x.slo);
+                if (REL)
+                    p = bq;
+                else
+                    p = pm_lds ? insertion_point_lds(pmax + 1, bq + 1, eq, x.slo)   // pmax from bq
+                               : insertion_point(sr, bq + 1, eq, x.slo);
                 if (p == eq) {
                     const SSt t = ss[eq - 1];
                     const SRec y = sr[eq - 1];
@@ -1210,13 +1293,110 @@ __global__ __launch_bounds__(kThreads) void k_fmove(SearchArgs a)
         F = cur + (a.R[b * G + s] - a.Q[b * I + g]) + (N - Qh);
         D = force ? INFINITY : a.RD[b * G + s] + kEpsP * nq + 1e-12 * (fabs(cur) + nq);
     }
-    if (r < G) {
-        const int64_t k = (int64_t)G * a.W + (int64_t)s * I + h;
+    if (r < G && (!REL || g != h)) {          // k_frel screens RELOCATE into the own queue
+        const int64_t k = (int64_t)G * a.W + (REL ? (int64_t)G * I : 0) + (int64_t)s * I + h;
         a.F[b * a.n_moves + k] = F;
         a.D[b * a.n_moves + k] = D;
     }
     const double m = block_min(F + D, lmin);
-    if (threadIdx.x == 0) a.smin[b * a.nws + a.nwg_f + (int64_t)h * a.nwg_b + wg] = m;
+    if (threadIdx.x == 0)
+        a.smin[b * a.nws + a.nwg_f + (int64_t)((REL ? I : 0) + h) * a.nwg_b + wg] = m;
+}
+
+// Screened RELOCATE within the group's own queue, one lane per slot s: the
+// group goes first, flagged, then the evicted head; the groups between the
+// head and s are the old ones shifted by the group's tokens, variance and the
+// change of costs at the head; the position after s is formed afresh (its
+// tokens and variance ahead are the old ones: the group is ahead of it either
+// way); past it only the costs change.
+__global__ __launch_bounds__(kThreads) void k_frel(SearchArgs a)
+{
+    __shared__ float2 tab[qlm_tail::kCells];
+    __shared__ double lmin[kWaves];
+    const int64_t b = blockIdx.x / a.nwg_r;
+    const int wg = blockIdx.x % a.nwg_r;
+    if (a.done[b]) return;                    // the same in the whole workgroup
+    const int G = a.G, I = a.I;
+    const SRec *__restrict__ sr = a.srec + b * G;
+    const SSt *__restrict__ ss = a.sst + b * G;
+    const TRec *__restrict__ tr = a.trec + b * G;
+    const int32_t *__restrict__ qof = a.qof + b * (I + 1);
+    for (int k = threadIdx.x; k < qlm_tail::kCells; k += kThreads) tab[k] = a.tail[k];
+    __syncthreads();
+    const int s = wg * kThreads + threadIdx.x;
+    bool valid = false, force = false, on1 = false, on2 = false;
+    int g = 0, lo1 = 0, hi1 = 0, lo2 = 0, hi2 = 0;
+    double q = 0.0, dE1 = 0.0, dE2 = 0.0, vscale = 0.0;
+    float dvz1 = 0.0f;
+    if (s < G) {
+        SRec x = sr[s];
+        g = (int)min(x.q, (uint32_t)(I - 1));
+        const int bq = qof[g], eq = qof[g + 1];
+        if (s > bq) {
+            valid = true;
+            x.nmf |= kFlagBit;
+            const double theta = (double)a.inst_tput[g];
+            const double inv_theta = 1.0 / theta;
+            vscale = qlm_tail::kVarScale / (theta * theta);
+            const int cls = clampi(a.inst_class[g], 0, a.C - 1);
+            const double eps = margin_eps(eq - bq);
+            const double es = a.Es[b * I + g];
+            Run r{0.0, 0.0, 0.0, 0.0, model0_of(a, g)};
+            screen_visit(r, x, theta, inv_theta, cls, vscale, eps, tab, a, force);
+            screen_visit(r, sr[bq], theta, inv_theta, cls, vscale, eps, tab, a, force);
+            q = r.sc;
+            const double dK1 = r.K - ss[bq].K;
+            if (bq + 1 < s) {
+                dE1 = x.a * inv_theta + dK1;
+                dvz1 = (float)(x.b * vscale);
+                lo1 = bq + 1;
+                hi1 = s;
+                on1 = true;
+                force = force || !((double)(tr[lo1].vz + dvz1) >= vz_floor(eps, es + fabs(dE1)));
+            }
+            if (s + 1 < eq) {
+                const SSt t = ss[s + 1];
+                const SRec y = sr[s - 1];
+                Run r2{t.A, t.V, s - 1 == bq ? r.K : ss[s - 1].K + dK1, 0.0,
+                       (int)(y.nmf & 0xFFu)};
+                // its sums ahead come from the cache, not from the exact walk's
+                // order: an indicator (nothing ahead with variance) is not trusted
+                force = force || !(t.V > 0.0);
+                screen_visit(r2, sr[s + 1], theta, inv_theta, cls, vscale, eps, tab, a, force);
+                q += r2.sc;
+                const double dK2 = r2.K - t.K;
+                if (s + 2 < eq) {
+                    lo2 = s + 2;
+                    hi2 = eq;
+                    force = force || !((double)tr[lo2].vz >= vz_floor(eps, es + fabs(dK2)));
+                    if (dK2 == 0.0)
+                        q += a.Q[b * I + g] - ss[lo2].C;
+                    else {
+                        dE2 = dK2;
+                        on2 = true;
+                    }
+                }
+            }
+        }
+    }
+    auto tr_at = [&](int u) { return tr[u]; };
+    auto v_at = [&](int u) { return ss[u].V; };
+    q += tail_walk(tr_at, v_at, tab, on1, lo1, hi1, dE1, dvz1, 0.0, vscale, false);
+    q += tail_walk(tr_at, v_at, tab, on2, lo2, hi2, dE2, 0.0f, 0.0, vscale, false);
+    double F = INFINITY, D = 0.0;
+    if (valid) {
+        const double cur = a.cur[b];
+        const double nq = a.Nq[b * I + g];
+        F = cur - a.Q[b * I + g] + q;
+        D = force ? INFINITY : kEpsP * nq + 1e-12 * (fabs(cur) + nq);
+    }
+    if (s < G) {
+        const int64_t k = (int64_t)G * a.W + (int64_t)G * I + (int64_t)s * I + g;
+        a.F[b * a.n_moves + k] = F;
+        a.D[b * a.n_moves + k] = D;
+    }
+    const double m = block_min(F + D, lmin);
+    if (threadIdx.x == 0) a.smin[b * a.nws + a.nwg_f + (int64_t)2 * I * a.nwg_b + wg] = m;
 }
 
 // The bound of the chain's lowest exact score, min(F + D); the candidate list
@@ -1281,7 +1461,7 @@ __global__ __launch_bounds__(kThreads) void k_sexact(SearchArgs a)
             const int s = (int)(k / W), d = (int)(k % W) + 1;
             const int g = (int)sr[s].q;
             const int bq = qof[g], eq = qof[g + 1];
-            if (s + d >= eq) {
+            if (s + d >= eq || s == bq) {
                 if (lane == 0) a.cex[b * a.n_moves + c] = score;
                 continue;
             }
@@ -1291,12 +1471,43 @@ __global__ __launch_bounds__(kThreads) void k_sexact(SearchArgs a)
                       (double)a.inst_tput[g], clampi(a.inst_class[g], 0, a.C - 1), a,
                       NoOut{});
             score = total_with(T, Q, I, g, r.sc);
+        } else if (k >= (int64_t)G * W + (int64_t)G * I) {
+            // RELOCATE(s, h): the group first in h, flagged, then h's groups
+            const int64_t rr = k - (int64_t)G * W - (int64_t)G * I;
+            const int s = (int)(rr / I), h = (int)(rr % I);
+            SRec x = sr[s];
+            x.nmf |= kFlagBit;
+            const int g = (int)x.q;
+            const int bq = qof[h], eq = qof[h + 1];
+            if (s == qof[g] || bq == eq) {
+                if (lane == 0) a.cex[b * a.n_moves + c] = score;
+                continue;
+            }
+            const double theta = (double)a.inst_tput[h];
+            const int cls = clampi(a.inst_class[h], 0, a.C - 1);
+            Run r{0.0, 0.0, 0.0, 0.0, model0_of(a, h)};
+            if (g == h) {
+                wave_walk(r, eq - bq, [&](int v) {
+                    return v == 0 ? x : (bq + v - 1 < s ? sr[bq + v - 1] : sr[bq + v]);
+                }, theta, cls, a, NoOut{});
+                score = total_with(T, Q, I, g, r.sc);
+            } else {
+                wave_walk(r, eq - bq + 1, [&](int v) { return v == 0 ? x : sr[bq + v - 1]; },
+                          theta, cls, a, NoOut{});
+                const double nh = r.sc;
+                const int bg = qof[g], eg = qof[g + 1];
+                Run rg = start_at(a, sr, ss, s, bg, g);
+                wave_walk(rg, eg - s - 1, [&](int v) { return sr[s + 1 + v]; },
+                          (double)a.inst_tput[g], clampi(a.inst_class[g], 0, a.C - 1), a,
+                          NoOut{});
+                score = total_with2(T, Q, I, g, rg.sc, h, nh);
+            }
         } else {
             const int64_t rr = k - (int64_t)G * W;
             const int s = (int)(rr / I), h = (int)(rr % I);
             const SRec x = sr[s];
             const int g = (int)x.q;
-            if (g == h) {
+            if (g == h || s == qof[g]) {
                 if (lane == 0) a.cex[b * a.n_moves + c] = score;
                 continue;
             }
@@ -1308,7 +1519,7 @@ __global__ __launch_bounds__(kThreads) void k_sexact(SearchArgs a)
                 r = Run{0.0, 0.0, 0.0, 0.0, model0_of(a, h)};
                 wave_walk(r, 1, [&](int) { return x; }, theta, cls, a, NoOut{});
             } else {
-                const int p = insertion_point(sr, bq, eq, x.slo);
+                const int p = edf_point(sr, bq, eq, x.slo);
                 if (p == eq) {
                     r = start_at(a, sr, ss, eq - 1, bq, h);
                     wave_walk(r, 2, [&](int v) { return v == 0 ? sr[eq - 1] : x; }, theta, cls,
@@ -1333,12 +1544,14 @@ __global__ __launch_bounds__(kThreads) void k_sexact(SearchArgs a)
 
 #pragma clang fp contract(on)
 
-// Moves the group at slot s of chain b to queue h, before the first group of h
-// whose SLO is strictly later (a reassignment, or with h its own queue a
-// re-insertion): the slots between its old and new place rotate by one, and
-// the queue offsets between the two queues shift.  Run by a whole workgroup.
+// Moves the group at slot s of chain b to queue h, at insertion point p_known
+// (by default its EDF position after h's head: a reassignment, or with h its
+// own queue a re-insertion; a relocation passes h's head slot and `evict`,
+// which sets the group's flag): the slots between its old and new place
+// rotate by one, and the queue offsets between the two queues shift.  Run by
+// a whole workgroup.
 __device__ void place_apply(const SearchArgs &a, int64_t b, int s, int h, int p_known = -1,
-                            int g_known = -1)
+                            int g_known = -1, bool evict = false)
 {
     // the slots that move, staged in LDS when they fit (else in the workspace)
     __shared__ int32_t st_perm[kStageSlots];
@@ -1349,7 +1562,7 @@ __device__ void place_apply(const SearchArgs &a, int64_t b, int s, int h, int p_
     int32_t *qof = a.qof + b * (I + 1);
     const SRec *sr = a.srec + b * G;
     const int g = g_known >= 0 ? g_known : (int)sr[s].q;
-    const int p = p_known >= 0 ? p_known : insertion_point(sr, qof[h], qof[h + 1], sr[s].slo);
+    const int p = p_known >= 0 ? p_known : edf_point(sr, qof[h], qof[h + 1], sr[s].slo);
     // left: the group goes later (to slot p - 1); right: earlier (to slot p)
     const bool left = h > g || (h == g && p > s);
     const int lo = left ? s : p;
@@ -1383,6 +1596,10 @@ __device__ void place_apply(const SearchArgs &a, int64_t b, int s, int h, int p_
         for (int q = g + 1 + threadIdx.x; q <= h; q += kThreads) qof[q] -= 1;
     } else if (h < g) {
         for (int q = h + 1 + threadIdx.x; q <= g; q += kThreads) qof[q] += 1;
+    }
+    if (evict) {
+        __syncthreads();                     // every slot of the rotation written
+        if (threadIdx.x == 0) flag[left ? p - 1 : p] = 1;
     }
 }
 
@@ -1438,7 +1655,12 @@ __global__ __launch_bounds__(kThreads) void k_spick(SearchArgs a, int step)
         return;
     }
     const int64_t r = k - (int64_t)G * W;
-    place_apply(a, b, (int)(r / I), (int)(r % I));
+    if (r < (int64_t)G * I) {
+        place_apply(a, b, (int)(r / I), (int)(r % I));
+    } else {
+        const int s = (int)((r - (int64_t)G * I) / I), h = (int)((r - (int64_t)G * I) % I);
+        place_apply(a, b, s, h, a.qof[b * (I + 1) + h], -1, true);
+    }
 }
 
 // Final plans to the caller's slot-major arrays, with their scores and steps.
@@ -1475,101 +1697,130 @@ __global__ __launch_bounds__(kThreads) void k_sout(SearchArgs a, qlm_plans_out o
 
 #pragma clang fp contract(off)
 
-// Exact score of each plan with its group `group` placed in queue h, one
-// wavefront per (plan, h).
-// One wavefront per (chain, queue h), and one more per chain (h = I) for the
-// group's own queue without it, which every other queue's score shares: the
-// score of the plan with the group placed in h (h = the group's queue), or
-// the score of queue h with the group inserted (other h; k_place_pick
-// completes it with the own queue's score without the group), or the own
-// queue's score without the group (h = I, in U).
+// Exact score of each plan with its group `group` at each of its 2I places:
+// c < I the EDF position of queue c after its head (as the queue stands
+// without the group), c >= I the head of the non-empty queue c - I with the
+// group flagged.  One wavefront per (chain, w), w in [0, 2I]: w < I the place
+// c = w, w = I the group's own queue without it (which every other queue's
+// score shares, in U), w > I the place c = w - 1.  A place in the group's own
+// queue is scored as a plan; a place in another queue h as the score of h
+// with the group (k_place_pick completes it).  A group at its queue's head is
+// running and is not placed (k_place_pick keeps the plan).
 __global__ __launch_bounds__(kThreads) void k_place_eval(SearchArgs a, int group)
 {
     const int G = a.G, I = a.I;
-    const int nblk = (I + 1 + kWaves - 1) / kWaves;
+    const int nblk = (2 * I + 1 + kWaves - 1) / kWaves;
     const int64_t b = blockIdx.x / nblk;
-    const int h = (blockIdx.x % nblk) * kWaves + wave_id();
-    if (h > I) return;
+    const int w = (blockIdx.x % nblk) * kWaves + wave_id();
+    if (w > 2 * I) return;
     const SRec *__restrict__ sr = a.srec + b * G;
     const SSt *__restrict__ ss = a.sst + b * G;
     const int32_t *__restrict__ qof = a.qof + b * (I + 1);
     const double *T = a.T + b * (I + 1);
     const double *Q = a.Q + b * I;
     const int s = __builtin_amdgcn_readfirstlane(clampi(a.inv[b * G + group], 0, G - 1));
-    const SRec x = sr[s];
+    SRec x = sr[s];
     const int g = clampi((int)x.q, 0, I - 1);
-    if (h == I) {
-        const int bg = clampi(qof[g], 0, G), eg = clampi(qof[g + 1], bg, G);
-        Run rg = start_at(a, sr, ss, s, bg, g);
-        wave_walk(rg, eg - s - 1, [&](int v) { return sr[s + 1 + v]; }, (double)a.inst_tput[g],
-                  clampi(a.inst_class[g], 0, a.C - 1), a, NoOut{});
-        if ((threadIdx.x & (kWave - 1)) == 0) {
-            a.U[b] = rg.sc;
+    const int bg = clampi(qof[g], 0, G), eg = clampi(qof[g + 1], bg, G);
+    const bool lead = (threadIdx.x & (kWave - 1)) == 0;
+    if (w == I) {
+        if (lead) {
             a.dq[b * 4 + 2] = s;
             a.dq[b * 4 + 3] = g;
         }
+        if (s == bg) return;
+        Run rg = start_at(a, sr, ss, s, bg, g);
+        wave_walk(rg, eg - s - 1, [&](int v) { return sr[s + 1 + v]; }, (double)a.inst_tput[g],
+                  clampi(a.inst_class[g], 0, a.C - 1), a, NoOut{});
+        if (lead) a.U[b] = rg.sc;
         return;
     }
+    if (s == bg) return;                       // running: it stays
+    const int c = w < I ? w : w - 1;
+    const bool head = c >= I;
+    const int h = head ? c - I : c;
     const int bq = clampi(qof[h], 0, G), eq = clampi(qof[h + 1], bq, G);
     const double theta = (double)a.inst_tput[h];
     const int cls = clampi(a.inst_class[h], 0, a.C - 1);
-    const int p = insertion_point_wave(sr, bq, eq, x.slo);
-    double score;
-    if (h == g) {
-        // its own queue: from the first position that changes, the queue without
-        // s with the group at the insertion point
-        const int st = min(s, p);
-        Run r = start_at(a, sr, ss, st, bq, g);
-        if (p <= s)
-            wave_walk(r, eq - st, [&](int v) { return v == 0 ? x : (v <= s - p ? sr[p + v - 1] : sr[p + v]); },
-                      theta, cls, a, NoOut{});
-        else
-            wave_walk(r, eq - st, [&](int v) {
-                return v < p - s - 1 ? sr[s + 1 + v] : (v == p - s - 1 ? x : sr[s + v]);
-            }, theta, cls, a, NoOut{});
-        score = total_with(T, Q, I, g, r.sc);
-    } else {
-        Run r;
-        if (bq == eq) {
-            r = Run{0.0, 0.0, 0.0, 0.0, model0_of(a, h)};
-            wave_walk(r, 1, [&](int) { return x; }, theta, cls, a, NoOut{});
-        } else if (p == eq) {
-            r = start_at(a, sr, ss, eq - 1, bq, h);
-            wave_walk(r, 2, [&](int v) { return v == 0 ? sr[eq - 1] : x; }, theta, cls, a, NoOut{});
-        } else {
-            r = start_at(a, sr, ss, p, bq, h);
-            wave_walk(r, eq - p + 1, [&](int v) { return v == 0 ? x : sr[p + v - 1]; }, theta, cls,
-                      a, NoOut{});
+    double score = INFINITY;
+    int p = bq;
+    if (head) {
+        // at the head, ahead of the running group (an empty queue has none to
+        // evict: no place)
+        x.nmf |= kFlagBit;
+        if (bq < eq) {
+            Run r{0.0, 0.0, 0.0, 0.0, model0_of(a, h)};
+            if (h == g) {
+                wave_walk(r, eq - bq, [&](int v) {
+                    return v == 0 ? x : (bq + v - 1 < s ? sr[bq + v - 1] : sr[bq + v]);
+                }, theta, cls, a, NoOut{});
+                score = total_with(T, Q, I, g, r.sc);
+            } else {
+                wave_walk(r, eq - bq + 1, [&](int v) { return v == 0 ? x : sr[bq + v - 1]; },
+                          theta, cls, a, NoOut{});
+                score = r.sc;                // completed by k_place_pick
+            }
         }
-        score = r.sc;                    // completed by k_place_pick
+    } else {
+        p = bq == eq ? bq : insertion_point_wave(sr, bq + 1, eq, x.slo);
+        if (h == g) {
+            // its own queue: from the first position that changes, the queue
+            // without s with the group at the insertion point
+            const int st = min(s, p);
+            Run r = start_at(a, sr, ss, st, bq, g);
+            if (p <= s)
+                wave_walk(r, eq - st, [&](int v) { return v == 0 ? x : (v <= s - p ? sr[p + v - 1] : sr[p + v]); },
+                          theta, cls, a, NoOut{});
+            else
+                wave_walk(r, eq - st, [&](int v) {
+                    return v < p - s - 1 ? sr[s + 1 + v] : (v == p - s - 1 ? x : sr[s + v]);
+                }, theta, cls, a, NoOut{});
+            score = total_with(T, Q, I, g, r.sc);
+        } else {
+            Run r;
+            if (bq == eq) {
+                r = Run{0.0, 0.0, 0.0, 0.0, model0_of(a, h)};
+                wave_walk(r, 1, [&](int) { return x; }, theta, cls, a, NoOut{});
+            } else if (p == eq) {
+                r = start_at(a, sr, ss, eq - 1, bq, h);
+                wave_walk(r, 2, [&](int v) { return v == 0 ? sr[eq - 1] : x; }, theta, cls, a, NoOut{});
+            } else {
+                r = start_at(a, sr, ss, p, bq, h);
+                wave_walk(r, eq - p + 1, [&](int v) { return v == 0 ? x : sr[p + v - 1]; }, theta, cls,
+                          a, NoOut{});
+            }
+            score = r.sc;                    // completed by k_place_pick
+        }
     }
-    if ((threadIdx.x & (kWave - 1)) == 0) {
-        a.cex[b * a.n_moves + h] = score;
-        a.cand[b * a.n_moves + h] = p;   // the insertion point, for the pick
+    if (lead) {
+        a.cex[b * a.n_moves + c] = score;
+        a.cand[b * a.n_moves + c] = p;       // the insertion point, for the pick
     }
 }
 
 #pragma clang fp contract(on)
 
-// The queue with the lowest exact score (lowest h on ties), applied.
+// The place with the lowest exact score (lowest c on ties), applied; a running
+// group stays, and the plan keeps its score.
 __global__ __launch_bounds__(kThreads) void k_place_pick(SearchArgs a, int group, int32_t *queue,
                                                          double *score)
 {
     __shared__ double ls[kWaves];
     __shared__ int64_t lk[kWaves];
     __shared__ int64_t kk;
-    __shared__ int kp, kg;
+    __shared__ int kp, kg, stay;
     // the queue scores and their running sums, staged for the totals
     __shared__ double sT[kMaxSearchInstances + 1], sQ[kMaxSearchInstances];
     __shared__ int scand[kThreads];
     const int64_t b = blockIdx.x;
     const int G = a.G, I = a.I;
+    const int n = 2 * I;
     // every independent load at once: the queue scores, the moved group's
-    // slot and queue, and (up to kThreads queues) each thread's candidate
+    // slot and queue, and (up to kThreads places) each thread's candidate
     // score and insertion point
-    const bool one = I <= kThreads;
+    const bool one = n <= kThreads;
     double v1 = 0.0;
-    if (one && threadIdx.x < I) {
+    if (one && threadIdx.x < n) {
         v1 = a.cex[b * a.n_moves + threadIdx.x];
         scand[threadIdx.x] = a.cand[b * a.n_moves + threadIdx.x];
     }
@@ -1579,39 +1830,54 @@ __global__ __launch_bounds__(kThreads) void k_place_pick(SearchArgs a, int group
     }
     const int s0 = clampi(a.dq[b * 4 + 2], 0, G - 1);
     const int g0 = clampi(a.dq[b * 4 + 3], 0, I - 1);
-    if (threadIdx.x == 0) kg = (int)a.srec[b * G + s0].q;
+    if (threadIdx.x == 0) {
+        kg = (int)a.srec[b * G + s0].q;
+        stay = s0 == a.qof[b * (I + 1) + g0];
+    }
     __syncthreads();
+    if (stay) {
+        if (threadIdx.x == 0) {
+            if (queue) queue[b] = g0;
+            if (score) score[b] = a.cur[b];
+            a.dq[b * 4] = g0;
+            a.dq[b * 4 + 1] = g0;
+        }
+        return;
+    }
     const double *T = sT;
     const double *Q = sQ;
     const double rg = a.U[b];
     double best = INFINITY;
     int64_t bk = INT64_MAX;
-    for (int h = threadIdx.x; h < I; h += kThreads) {
-        double v = one ? v1 : a.cex[b * a.n_moves + h];
+    for (int c = threadIdx.x; c < n; c += kThreads) {
+        double v = one ? v1 : a.cex[b * a.n_moves + c];
+        const int h = c < I ? c : c - I;
         if (h != g0) {
             v = total_with2(T, Q, I, g0, rg, h, v);
-            a.cex[b * a.n_moves + h] = v;
+            a.cex[b * a.n_moves + c] = v;
         }
-        if (better(v, h, best, bk)) {
+        if (better(v, c, best, bk)) {
             best = v;
-            bk = h;
+            bk = c;
         }
     }
     block_best(best, bk, ls, lk);
     if (threadIdx.x == 0) {
-        const bool none = bk < 0 || bk >= I;
-        if (none) bk = 0;                         // every score NaN: the first queue
+        const bool none = bk < 0 || bk >= n;
+        if (none) bk = 0;                         // every score NaN: the first place
         kk = bk;
         const double cur = none ? a.cex[b * a.n_moves + bk] : best;
         a.cur[b] = cur;
         if (queue) queue[b] = (int32_t)bk;
         if (score) score[b] = cur;
-        a.dq[b * 4] = min(g0, (int)bk);
-        a.dq[b * 4 + 1] = max(g0, (int)bk);
+        const int h = (int)(bk < I ? bk : bk - I);
+        a.dq[b * 4] = min(g0, h);
+        a.dq[b * 4 + 1] = max(g0, h);
         kp = clampi(one ? scand[bk] : a.cand[b * a.n_moves + bk], 0, G);
     }
     __syncthreads();
-    place_apply(a, b, s0, (int)kk, kp, kg);
+    const int c = (int)kk;
+    place_apply(a, b, s0, c < I ? c : c - I, kp, kg, c >= I);
 }
 
 // ---------------------------------------------------------------------------
@@ -1794,7 +2060,7 @@ __global__ __launch_bounds__(kThreads) void k_seedwrite(SeedArgs a)
 size_t align256(size_t v) { return (v + 255) / 256 * 256; }
 
 struct Layout {
-    int nwg_a, nwg_b, nwg, nwg_f, nws;
+    int nwg_a, nwg_b, nwg, nwg_f, nwg_r, nws;
     int64_t n_moves;
     size_t grec, by_slo, rank_part, perm, flag, qof, inv, srec, sst, trec, R, RD, Q, Nq, Es, T, cur, done, steps,
         wmin_s, wmin_i, smin, F, D, cand, cex, ncand, U, scratch, dq, tail, total;
@@ -1805,10 +2071,11 @@ Layout layout(int G, int I, int W, int64_t B)
     Layout L{};
     L.nwg_a = (int)(((int64_t)G * (W + 1) + kThreads - 1) / kThreads);
     L.nwg_b = (G + kThreads - 1) / kThreads;
-    L.nwg = L.nwg_a + I * L.nwg_b;
+    L.nwg = L.nwg_a + 2 * I * L.nwg_b;
     L.nwg_f = (int)(((int64_t)G * (W + 1) + kThreads - 1) / kThreads);
-    L.nws = L.nwg_f + I * L.nwg_b;
-    L.n_moves = (int64_t)G * W + (int64_t)G * I;
+    L.nwg_r = (G + kThreads - 1) / kThreads;
+    L.nws = L.nwg_f + 2 * I * L.nwg_b + L.nwg_r;
+    L.n_moves = (int64_t)G * W + 2 * (int64_t)G * I;
     size_t o = 0;
     auto take = [&](size_t bytes) {
         const size_t at = o;
@@ -1928,6 +2195,7 @@ SearchArgs search_args(const qlm_problem *pr, int64_t B, int32_t W, unsigned cha
     a.nwg_b = L.nwg_b;
     a.nwg = L.nwg;
     a.nwg_f = L.nwg_f;
+    a.nwg_r = L.nwg_r;
     a.nws = L.nws;
     a.n_moves = L.n_moves;
     return a;
@@ -2006,22 +2274,28 @@ int exact_moves(SearchArgs &a, hipStream_t stream)
                        stream, a);
     if ((rc = launched("k_smove launch"))) return rc;
     qlm_internal::timing_end(stream, &tl);
-    return QLM_OK;
+    hipLaunchKernelGGL(k_sreloc, dim3((unsigned)((int64_t)a.I * a.nwg_b * a.B)), dim3(kThreads), 0,
+                       stream, a);
+    return launched("k_sreloc launch");
 }
 
-// The screens of every move (removals and swaps, then reassignments).
+// The screens of every move (removals and swaps, then reassignments, then
+// relocations into other queues and within a queue).
 int screen_moves(SearchArgs &a, hipStream_t stream)
 {
     hipLaunchKernelGGL(k_fswap, dim3((unsigned)(a.nwg_f * a.B)), dim3(kThreads), 0, stream, a);
     int rc = launched("k_fswap launch");
     if (rc) return rc;
+    const dim3 mgrid((unsigned)((int64_t)a.I * a.nwg_b * a.B));
     qlm_internal::TimedLaunch tl;
     if ((rc = qlm_internal::timing_begin(stream, &tl))) return rc;
-    hipLaunchKernelGGL(k_fmove, dim3((unsigned)((int64_t)a.I * a.nwg_b * a.B)), dim3(kThreads), 0,
-                       stream, a);
+    hipLaunchKernelGGL(k_fmove<false>, mgrid, dim3(kThreads), 0, stream, a);
     if ((rc = launched("k_fmove launch"))) return rc;
     qlm_internal::timing_end(stream, &tl);
-    return QLM_OK;
+    hipLaunchKernelGGL(k_fmove<true>, mgrid, dim3(kThreads), 0, stream, a);
+    if ((rc = launched("k_fmove (relocate) launch"))) return rc;
+    hipLaunchKernelGGL(k_frel, dim3((unsigned)(a.nwg_r * a.B)), dim3(kThreads), 0, stream, a);
+    return launched("k_frel launch");
 }
 
 // The placement of one group in every chain: the candidate queues scored
@@ -2033,7 +2307,7 @@ int place_step(SearchArgs &a, int32_t group, int32_t *queue, double *score, bool
     int rc;
     qlm_internal::TimedLaunch tl;
     if ((rc = qlm_internal::timing_begin(stream, &tl))) return rc;
-    const int eblk = (a.I + 1 + kWaves - 1) / kWaves;
+    const int eblk = (2 * a.I + 1 + kWaves - 1) / kWaves;
     hipLaunchKernelGGL(k_place_eval, dim3((unsigned)(eblk * a.B)), dim3(kThreads), 0, stream, a,
                        group);
     if ((rc = launched("k_place_eval launch"))) return rc;
@@ -2183,11 +2457,11 @@ int qlm_place_group(const qlm_problem *problem, const qlm_plans *start, const ql
     if (!problem || group < 0 || group >= problem->n_groups)
         return fail(QLM_ERR_ARG, "group must be in [0, n_groups)");
     if (start && start->n_plans > 0) {
-        if (!out->perm || !out->qoff) return fail(QLM_ERR_ARG, "out perm and qoff are required");
+        if (!out->perm || !out->qoff || !out->evict_bits)
+            return fail(QLM_ERR_ARG, "out perm, qoff and evict_bits are required (a relocation "
+                                     "sets eviction flags)");
         if (out->plan_stride < start->n_plans)
             return fail(QLM_ERR_ARG, "out plan_stride must be >= n_plans");
-        if (start->evict_bits && !out->evict_bits)
-            return fail(QLM_ERR_ARG, "out evict_bits is required when the plans have eviction bits");
     }
     SearchArgs a;
     int rc = search_begin(problem, start, 0, ws, ws_bytes, &a, stream, false);
@@ -2196,9 +2470,7 @@ int qlm_place_group(const qlm_problem *problem, const qlm_plans *start, const ql
     rc = load_and_state(a, start, stream);
     if (rc) return rc;
     if ((rc = place_step(a, group, queue, nullptr, false, stream))) return rc;
-    qlm_plans_out o = *out;
-    if (!start->evict_bits) o.evict_bits = nullptr;
-    return write_plans(a, o, score, stream);
+    return write_plans(a, *out, score, stream);
 }
 
 int qlm_place_begin(const qlm_problem *problem, const qlm_plans *plans, void *ws, size_t ws_bytes,
@@ -2234,7 +2506,9 @@ int qlm_place_end(const qlm_problem *problem, int64_t n_plans, const qlm_plans_o
     int rc = session_args(problem, n_plans, ws, ws_bytes, &a);
     if (rc) return rc;
     if (a.B == 0) return QLM_OK;
-    if (!out->perm || !out->qoff) return fail(QLM_ERR_ARG, "out perm and qoff are required");
+    if (!out->perm || !out->qoff || !out->evict_bits)
+        return fail(QLM_ERR_ARG, "out perm, qoff and evict_bits are required (a relocation sets "
+                                 "eviction flags)");
     if (out->plan_stride < n_plans) return fail(QLM_ERR_ARG, "out plan_stride must be >= n_plans");
     return write_plans(a, *out, score, stream);
 }
@@ -2242,7 +2516,7 @@ int qlm_place_end(const qlm_problem *problem, int64_t n_plans, const qlm_plans_o
 int64_t qlm_search_n_moves(int32_t n_groups, int32_t n_instances, int32_t window)
 {
     if (n_groups < 1 || n_instances < 1 || window < 0) return 0;
-    return (int64_t)n_groups * window + (int64_t)n_groups * n_instances;
+    return (int64_t)n_groups * window + 2 * (int64_t)n_groups * n_instances;
 }
 
 size_t qlm_search_workspace_bytes(const qlm_problem *problem, int64_t n_plans, int32_t window)
@@ -2292,11 +2566,11 @@ int qlm_local_search(const qlm_problem *problem, const qlm_plans *start, const q
     if (!out) return fail(QLM_ERR_ARG, "out is NULL");
     if (max_steps < 0) return fail(QLM_ERR_ARG, "max_steps must be >= 0");
     if (start && start->n_plans > 0) {
-        if (!out->perm || !out->qoff) return fail(QLM_ERR_ARG, "out perm and qoff are required");
+        if (!out->perm || !out->qoff || !out->evict_bits)
+            return fail(QLM_ERR_ARG, "out perm, qoff and evict_bits are required (a relocation "
+                                     "sets eviction flags)");
         if (out->plan_stride < start->n_plans)
             return fail(QLM_ERR_ARG, "out plan_stride must be >= n_plans");
-        if (start->evict_bits && !out->evict_bits)
-            return fail(QLM_ERR_ARG, "out evict_bits is required when the plans have eviction bits");
     }
     SearchArgs a;
     int rc = search_begin(problem, start, window, ws, ws_bytes, &a, stream);
@@ -2312,8 +2586,7 @@ int qlm_local_search(const qlm_problem *problem, const qlm_plans *start, const q
         if ((rc = pick_step(a, t, stream))) return rc;
     }
     if (max_steps > 0 && (rc = launch_state(a, 1, stream))) return rc;
-    qlm_plans_out o = *out;
-    if (!start->evict_bits) o.evict_bits = nullptr;
+    const qlm_plans_out o = *out;
     const int64_t rows = (int64_t)a.G + a.I + 1 + (o.evict_bits ? (a.G + 31) / 32 : 0) + 1;
     int64_t grid = (rows * a.B + kThreads - 1) / kThreads;
     if (grid > 65536) grid = 65536;

@@ -333,6 +333,17 @@ def timing_read():
 
 # -- plan search --------------------------------------------------------------
 
+def plans_like(plans: DevicePlans, n_groups: int) -> DevicePlans:
+    """Output plans shaped like `plans`, always with eviction words (a
+    relocation sets flags even in plans that had none)."""
+    import torch
+    ev = plans.evict_bits
+    ev = torch.empty_like(ev) if ev is not None else torch.empty(
+        ((n_groups + 31) // 32, plans.perm.shape[1]), dtype=torch.int32, device=plans.perm.device)
+    return DevicePlans(torch.empty_like(plans.perm), torch.empty_like(plans.qoff), ev,
+                       plans.n_plans)
+
+
 def search_n_moves(n_groups: int, n_instances: int, window: int) -> int:
     return int(library().qlm_search_n_moves(n_groups, n_instances, window))
 
@@ -392,9 +403,7 @@ def local_search(problem: DeviceProblem, plans: DevicePlans, window: int, max_st
     if ws is None:
         ws = search_workspace(problem, P, window, dev)
     if out is None:
-        out = DevicePlans(torch.empty_like(plans.perm), torch.empty_like(plans.qoff),
-                          None if plans.evict_bits is None else torch.empty_like(plans.evict_bits),
-                          P)
+        out = plans_like(plans, problem.n_groups)
     o = PlansOut(int(out.perm.shape[1]), _ptr(out.perm), _ptr(out.qoff), _ptr(out.evict_bits))
     score = torch.empty(P, dtype=torch.float64, device=dev)
     steps = torch.empty(P, dtype=torch.int32, device=dev)
@@ -436,18 +445,18 @@ def seed_plans(problem: DeviceProblem, policies=(EDF, GROUPED), evict: bool = Fa
 
 def place_group(problem: DeviceProblem, plans: DevicePlans, group: int, ws=None, stream=None,
                 out: DevicePlans | None = None):
-    """Every plan with `group` moved to the EDF position of its best queue:
-    dict with the placed plans (DevicePlans), their exact scores [P] f64 and
-    the chosen queues [P] int32."""
+    """Every plan with `group` moved to its best place: the EDF position after
+    the head of queue c, or (c >= I) the head of queue c - I with its eviction
+    flag set; a group at its queue's head stays.  Returns a dict with the
+    placed plans (DevicePlans, with eviction words), their exact scores [P] f64
+    and the chosen places c [P] int32."""
     import torch
     dev = plans.perm.device
     P = plans.n_plans
     if ws is None:
         ws = search_workspace(problem, P, 0, dev)
     if out is None:
-        out = DevicePlans(torch.empty_like(plans.perm), torch.empty_like(plans.qoff),
-                          None if plans.evict_bits is None else torch.empty_like(plans.evict_bits),
-                          P)
+        out = plans_like(plans, problem.n_groups)
     o = PlansOut(int(out.perm.shape[1]), _ptr(out.perm), _ptr(out.qoff), _ptr(out.evict_bits))
     score = torch.empty(P, dtype=torch.float64, device=dev)
     queue = torch.empty(P, dtype=torch.int32, device=dev)
@@ -595,7 +604,7 @@ class PlaceSession:
         self.queue = torch.empty(max(self.n_plans, 1), dtype=torch.int32, device=self.dev)
 
     def step(self, group: int):
-        """Places `group` in every plan; returns (scores [P], queues [P]) (device)."""
+        """Places `group` in every plan; returns (scores [P], places [P]) (device)."""
         _check(library().qlm_place_step(ctypes.byref(self.problem.struct), self.n_plans,
                                         int(group), _ptr(self.ws), self.ws.numel(),
                                         _ptr(self.score), _ptr(self.queue), _stream(self.stream)))
@@ -604,11 +613,8 @@ class PlaceSession:
     def end(self, out: DevicePlans | None = None):
         """The plans as they stand (DevicePlans) and their exact scores."""
         import torch
-        p = self.like
         if out is None:
-            out = DevicePlans(torch.empty_like(p.perm), torch.empty_like(p.qoff),
-                              None if p.evict_bits is None else torch.empty_like(p.evict_bits),
-                              self.n_plans)
+            out = plans_like(self.like, self.problem.n_groups)
         o = PlansOut(int(out.perm.shape[1]), _ptr(out.perm), _ptr(out.qoff), _ptr(out.evict_bits))
         score = torch.empty(max(self.n_plans, 1), dtype=torch.float64, device=self.dev)
         _check(library().qlm_place_end(ctypes.byref(self.problem.struct), self.n_plans,

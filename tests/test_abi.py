@@ -127,13 +127,13 @@ def test_search_argument_checks(lib):
     P = ctypes.byref
     pr = _problem(qlm, G=8, I=2)
     pl = qlm.Plans(3, 3, 0x1000, 0x1000, None)
-    assert lib.qlm_search_n_moves(8, 2, 3) == 8 * 3 + 8 * 2
+    assert lib.qlm_search_n_moves(8, 2, 3) == 8 * 3 + 2 * 8 * 2     # SWAP, MOVE, RELOCATE
     assert lib.qlm_search_n_moves(8, 2, -1) == 0
     need = lib.qlm_search_workspace_bytes(P(pr), 3, 4)
     assert need > 0 and lib.qlm_search_workspace_bytes(P(pr), 6, 4) > need
     assert lib.qlm_search_workspace_bytes(P(pr), 3, -1) == 0
     ws = 0x10000
-    out = qlm.PlansOut(3, 0x1000, 0x1000, None)
+    out = qlm.PlansOut(3, 0x1000, 0x1000, 0x1000)
     ms = lib.qlm_search_moves
     assert ms(P(pr), P(pl), -1, ws, need, 0x1000, None) == qlm.QLM_ERR_ARG
     assert ms(P(pr), P(pl), 1025, ws, need, 0x1000, None) == qlm.QLM_ERR_ARG
@@ -148,10 +148,13 @@ def test_search_argument_checks(lib):
     ls = lib.qlm_local_search
     assert ls(P(pr), P(pl), None, 4, 5, ws, need, None, None, None, None) == qlm.QLM_ERR_ARG
     assert ls(P(pr), P(pl), P(out), 4, -1, ws, need, None, None, None, None) == qlm.QLM_ERR_ARG
-    short = qlm.PlansOut(2, 0x1000, 0x1000, None)
+    short = qlm.PlansOut(2, 0x1000, 0x1000, 0x1000)
     assert ls(P(pr), P(pl), P(short), 4, 5, ws, need, None, None, None, None) == qlm.QLM_ERR_ARG
+    # the eviction words of the output are required, with or without start ones
+    noev = qlm.PlansOut(3, 0x1000, 0x1000, None)
     plev = qlm.Plans(3, 3, 0x1000, 0x1000, 0x1000)
-    assert ls(P(pr), P(plev), P(out), 4, 5, ws, need, None, None, None, None) == qlm.QLM_ERR_ARG
+    assert ls(P(pr), P(plev), P(noev), 4, 5, ws, need, None, None, None, None) == qlm.QLM_ERR_ARG
+    assert ls(P(pr), P(pl), P(noev), 4, 5, ws, need, None, None, None, None) == qlm.QLM_ERR_ARG
     assert ls(P(pr), P(pl), P(out), 4, 5, ws, need - 1, None, None, None, None) == \
         qlm.QLM_ERR_WORKSPACE
     sc = lib.qlm_search_screen
@@ -193,8 +196,10 @@ def test_place_argument_checks(lib):
     pr = _problem(qlm, G=8, I=2)
     pl = qlm.Plans(3, 3, 0x1000, 0x1000, None)
     need = lib.qlm_search_workspace_bytes(P(pr), 3, 0)
-    out = qlm.PlansOut(3, 0x1000, 0x1000, None)
+    out = qlm.PlansOut(3, 0x1000, 0x1000, 0x1000)
     pg = lib.qlm_place_group
+    noev = qlm.PlansOut(3, 0x1000, 0x1000, None)
+    assert pg(P(pr), P(pl), P(noev), 1, 0x10000, need, None, None, None) == qlm.QLM_ERR_ARG
     assert pg(P(pr), P(pl), None, 0, 0x10000, need, None, None, None) == qlm.QLM_ERR_ARG
     assert pg(P(pr), P(pl), P(out), 8, 0x10000, need, None, None, None) == qlm.QLM_ERR_ARG
     assert pg(P(pr), P(pl), P(out), -1, 0x10000, need, None, None, None) == qlm.QLM_ERR_ARG
@@ -273,10 +278,12 @@ def test_place_session_argument_checks(lib):
     assert st(P(pr), 3, 1, ws, need - 1, None, None, None) == qlm.QLM_ERR_WORKSPACE
     assert st(P(pr), -1, 1, ws, need, None, None, None) == qlm.QLM_ERR_ARG
     assert st(P(pr), 0, 1, ws, need, None, None, None) == qlm.QLM_OK
-    out = qlm.PlansOut(3, 0x1000, 0x1000, None)
+    out = qlm.PlansOut(3, 0x1000, 0x1000, 0x1000)
     en = lib.qlm_place_end
     assert en(P(pr), 3, None, ws, need, None, None) == qlm.QLM_ERR_ARG
     assert en(P(pr), 3, P(out), ws, need - 1, None, None) == qlm.QLM_ERR_WORKSPACE
-    short = qlm.PlansOut(2, 0x1000, 0x1000, None)
+    noev = qlm.PlansOut(3, 0x1000, 0x1000, None)
+    assert en(P(pr), 3, P(noev), ws, need, None, None) == qlm.QLM_ERR_ARG
+    short = qlm.PlansOut(2, 0x1000, 0x1000, 0x1000)
     assert en(P(pr), 3, P(short), ws, need, None, None) == qlm.QLM_ERR_ARG
 

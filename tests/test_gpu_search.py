@@ -96,15 +96,19 @@ def test_move_scores(qlm, orc, kw):
     torch.cuda.synchronize()
     ms = ms.cpu().numpy()
     G, I = pr["n_groups"], pr["n_instances"]
-    assert ms.shape == (pl["n_plans"], G * W + G * I)
+    assert ms.shape == (pl["n_plans"], G * W + 2 * G * I)
     exact = 0
+    kinds = np.zeros(3, np.int64)
     for p in range(pl["n_plans"]):
         ref = orc.move_scores(pr, pl, p, W)
         ok = _close(ms[p], ref)
         bad = np.flatnonzero(~ok)
         assert ok.all(), (p, bad[:5], ms[p][bad[:5]], ref[bad[:5]])
         exact += int(np.sum(ms[p] == ref))
-    print("bit-identical move scores: %d of %d" % (exact, ms.size))
+        fin = np.isfinite(ref)
+        kinds += [fin[:G * W].sum(), fin[G * W:G * W + G * I].sum(), fin[G * W + G * I:].sum()]
+    print("bit-identical move scores: %d of %d; moves SWAP %d MOVE %d RELOCATE %d"
+          % (exact, ms.size, *kinds))
 
 
 def _check_screen(F, D, ref, label):
@@ -194,15 +198,13 @@ def _check_search(orc, pr, pl, p, W, T, g_trace, g_steps, g_perm, g_qoff, g_ev, 
     """Compares one chain's search with the oracle's; returns the step where a
     near-tie let the two sides part (None when they agree throughout)."""
     G = pr["n_groups"]
-    with_flags = pl.get("evict_bits") is not None
     o = orc.local_search(pr, pl, p, W, T)
     ot = o["trace"]
     diff = np.flatnonzero(g_trace != ot)
     if diff.size == 0:
         assert g_steps == o["steps"]
         assert np.array_equal(g_perm, o["perm"]) and np.array_equal(g_qoff, o["qoff"])
-        if with_flags:
-            assert np.array_equal(g_ev, o["evict_bits"])
+        assert np.array_equal(g_ev, o["evict_bits"])
         assert _close(g_score, o["score"]), (g_score, o["score"])
         return None
     t = int(diff[0])
@@ -210,7 +212,7 @@ def _check_search(orc, pr, pl, p, W, T, g_trace, g_steps, g_perm, g_qoff, g_ev, 
     perm, qoff, flag = pl["perm"][:, p].copy(), pl["qoff"][:, p].copy(), _flags(pl, p, G)
     for k in ot[:t]:
         perm, qoff, flag = orc.move_apply(pr, perm, qoff, flag, W, int(k))
-    one = _one(perm, qoff, flag, with_flags)
+    one = _one(perm, qoff, flag, True)
     cur = orc.plan_detail(pr, one, 0)["score"]
     allm = orc.move_scores(pr, one, 0, W)
     best = float(allm.min())
@@ -237,21 +239,56 @@ def test_local_search(qlm, orc, kw):
     out = r["plans"]
     g_perm = out.perm.cpu().numpy()
     g_qoff = out.qoff.cpu().numpy()
-    g_ev = None if out.evict_bits is None else out.evict_bits.cpu().numpy().view(np.uint32)
+    g_ev = out.evict_bits.cpu().numpy().view(np.uint32)
     g_trace = r["trace"].cpu().numpy()
     g_steps = r["steps"].cpu().numpy()
     g_score = r["score"].cpu().numpy()
     moved = 0
     for p in range(pl["n_plans"]):
         t = _check_search(orc, pr, pl, p, W, T, g_trace[p], int(g_steps[p]), g_perm[:, p],
-                          g_qoff[:, p], None if g_ev is None else g_ev[:, p], float(g_score[p]))
+                          g_qoff[:, p], g_ev[:, p], float(g_score[p]))
         if t is not None:
             print("plan %d: near-tie at step %d" % (p, t))
         moved += int(g_steps[p])
-    print("moves applied over all plans:", moved)
+    G, I = pr["n_groups"], pr["n_instances"]
+    print("moves applied over all plans: %d (relocations %d)"
+          % (moved, int(np.sum(g_trace >= G * W + G * I))))
     # scores never rise, and the final scores are those of the final plans
     ex = qlm.rwt_score_exact(dpr, out, np.arange(pl["n_plans"]))
     assert np.array_equal(ex.cpu().numpy(), g_score)
+
+
+def test_relocate_by_hand(qlm, orc):
+    """Head-of-line blocking on one 100 tok/s instance: a running batch group
+    (1000 tokens, SLO 60 s), behind it an interactive group (2 x 10 tokens,
+    SLO 1 s) that misses (score 2).  Its relocation to the head, paying E, is
+    the one move (k 5; the others touch the running group or lie beyond G):
+    score 0 for E = 0.5 s and E = 1 s (a wait equal to the SLO meets it), 2
+    for E = 2 s, where the search keeps the plan.  Placement of the
+    interactive group: the head place c = 1 wins unless E = 2 s."""
+    import torch
+    from cases import plans as hplans, problem as hproblem
+    for E, sc in ((0.5, 0.0), (2.0, 2.0), (1.0, 0.0)):
+        pr = hproblem([(1, 1000.0, 0.0, 0, 60.0), (2, 10.0, 0.0, 0, 1.0)], [(100.0, 0)],
+                      evict_cost=E)
+        pl = hplans([[[0, 1]]], 2)
+        dpr, dpl = device_inputs(pr, pl)
+        ms = qlm.search_moves(dpr, dpl, 1).cpu().numpy()[0]
+        assert list(ms) == [np.inf] * 5 + [sc], (E, ms)
+        F, D = qlm.search_screen(dpr, dpl, 1)
+        _check_screen(F.cpu().numpy()[0], D.cpu().numpy()[0], ms, ("hand", E))
+        r = qlm.local_search(dpr, dpl, 1, 2, trace=True)
+        pg = qlm.place_group(dpr, dpl, 1)
+        torch.cuda.synchronize()
+        moved = sc < 2.0
+        assert float(r["score"][0]) == sc and int(r["steps"][0]) == int(moved), (E, r)
+        assert list(r["trace"].cpu().numpy()[0]) == ([5, -1] if moved else [-1, -1])
+        assert list(r["plans"].perm.cpu().numpy()[:, 0]) == ([1, 0] if moved else [0, 1])
+        assert int(r["plans"].evict_bits.cpu().numpy()[0, 0]) == (1 if moved else 0)
+        o = orc.place_group(pr, pl, 0, 1)
+        assert int(pg["queue"][0]) == o["queue"] == (1 if moved else 0), (E, o["queue"])
+        assert float(pg["score"][0]) == o["score"]
+        assert list(pg["plans"].perm.cpu().numpy()[:, 0]) == list(o["perm"])
 
 
 def test_search_edge_calls(qlm, orc):
@@ -311,8 +348,7 @@ def test_search_workloads(qlm, orc):
             _check_search(orc, pr, pl, p, W, 5, r["trace"].cpu().numpy()[p],
                           int(r["steps"][p]), out.perm.cpu().numpy()[:, p],
                           out.qoff.cpu().numpy()[:, p],
-                          None if out.evict_bits is None
-                          else out.evict_bits.cpu().numpy().view(np.uint32)[:, p],
+                          out.evict_bits.cpu().numpy().view(np.uint32)[:, p],
                           float(r["score"][p]))
 
 
@@ -359,13 +395,12 @@ def test_search_full_size(qlm, orc, name, W):
     # the first step takes the oracle's best move (lowest number on ties)
     assert tr[0] == first_min, (tr[0], first_min)
     perm, qoff, flag = pl["perm"][:, 0].copy(), pl["qoff"][:, 0].copy(), _flags(pl, 0, G)
-    with_flags = pl.get("evict_bits") is not None
-    cur = orc.plan_detail(pr, _one(perm, qoff, flag, with_flags), 0)["score"]
+    cur = orc.plan_detail(pr, _one(perm, qoff, flag, True), 0)["score"]
     for t in range(T):
         k = int(tr[t])
         if k < 0:
             break
-        v = orc.move_scores(pr, _one(perm, qoff, flag, with_flags), 0, W, ks=[k])[0]
+        v = orc.move_scores(pr, _one(perm, qoff, flag, True), 0, W, ks=[k])[0]
         assert v < cur
         perm, qoff, flag = orc.move_apply(pr, perm, qoff, flag, W, k)
         cur = v
@@ -446,9 +481,8 @@ def test_place_group(qlm, orc, kw):
                 assert _close(sc[p], o["score"]), (kw, group, p, qu[p], o["queue"])
                 continue
             assert np.array_equal(perm[:, p], o["perm"]) and np.array_equal(qoff[:, p], o["qoff"])
-            if out.evict_bits is not None:
-                assert np.array_equal(out.evict_bits.cpu().numpy().view(np.uint32)[:, p],
-                                      o["evict_bits"])
+            assert np.array_equal(out.evict_bits.cpu().numpy().view(np.uint32)[:, p],
+                                  o["evict_bits"])
             assert _close(sc[p], o["score"]), (sc[p], o["score"])
         ex = qlm.rwt_score_exact(dpr, out, np.arange(pl["n_plans"])).cpu().numpy()
         assert np.array_equal(ex, sc)
@@ -492,9 +526,9 @@ def test_place_group_arrival(qlm, orc):
 def test_place_group_long_move(qlm, orc, fast):
     """A placement that moves more slots than a workgroup stages in LDS (8192):
     9000 groups on 3 queues, one instance 100 times faster than the others.
-    fast = 2: the group heads queue 0, which holds 8301 groups (the slots
-    shift left); fast = 0: the group ends queue 2 and queue 0 holds 100 groups
-    (they shift right)."""
+    fast = 2: the group is second in queue 0, which holds 8301 groups (the
+    slots shift left); fast = 0: the group ends queue 2 and queue 0 holds 100
+    groups (they shift right)."""
     import torch
     from cases import plans as make_plans_by_hand, problem as make_problem_by_hand
     rng = np.random.default_rng(31 + fast)
@@ -506,7 +540,7 @@ def test_place_group_long_move(qlm, orc, fast):
     pr = make_problem_by_hand(groups, inst)
     order = [int(x) for x in rng.permutation(G)]
     if fast == 2:
-        group = order[0]
+        group = order[1]
         queues = [order[:8301], order[8301:8311], order[8311:]]
     else:
         group = order[-1]
@@ -553,13 +587,11 @@ def test_place_session(qlm, orc, kw):
             if int(qu[p]) == o["queue"]:
                 assert _close(float(sc[p]), o["score"]), (k, p)
         host = {"n_plans": P, "perm": cur.perm.cpu().numpy(), "qoff": cur.qoff.cpu().numpy(),
-                "evict_bits": None if cur.evict_bits is None
-                else cur.evict_bits.cpu().numpy().view(np.uint32)}
+                "evict_bits": cur.evict_bits.cpu().numpy().view(np.uint32)}
     out, score = ses.end()
     torch.cuda.synchronize()
     assert np.array_equal(out.perm.cpu().numpy(), cur.perm.cpu().numpy())
     assert np.array_equal(out.qoff.cpu().numpy(), cur.qoff.cpu().numpy())
-    if cur.evict_bits is not None:
-        assert np.array_equal(out.evict_bits.cpu().numpy(), cur.evict_bits.cpu().numpy())
+    assert np.array_equal(out.evict_bits.cpu().numpy(), cur.evict_bits.cpu().numpy())
     ex = qlm.rwt_score_exact(dpr, out, np.arange(P)).cpu().numpy()
     assert np.array_equal(score.cpu().numpy(), ex)
