@@ -369,7 +369,8 @@ def search_moves(problem: DeviceProblem, plans: DevicePlans, window: int, ws=Non
     if ws is None:
         ws = search_workspace(problem, plans.n_plans, window, dev)
     if out is None:
-        out = torch.empty((plans.n_plans, nm), dtype=torch.float64, device=dev)
+        # NaN until written: an entry the library leaves unwritten shows
+        out = torch.full((plans.n_plans, nm), float("nan"), dtype=torch.float64, device=dev)
     _check(library().qlm_search_moves(ctypes.byref(problem.struct), ctypes.byref(plans.struct),
                                       window, _ptr(ws), ws.numel(), _ptr(out), _stream(stream)))
     return out
@@ -384,8 +385,8 @@ def search_screen(problem: DeviceProblem, plans: DevicePlans, window: int, ws=No
     nm = search_n_moves(problem.n_groups, problem.n_instances, window)
     if ws is None:
         ws = search_workspace(problem, plans.n_plans, window, dev)
-    score = torch.empty((plans.n_plans, nm), dtype=torch.float64, device=dev)
-    bound = torch.empty((plans.n_plans, nm), dtype=torch.float64, device=dev)
+    score = torch.full((plans.n_plans, nm), float("nan"), dtype=torch.float64, device=dev)
+    bound = torch.full((plans.n_plans, nm), float("nan"), dtype=torch.float64, device=dev)
     _check(library().qlm_search_screen(ctypes.byref(problem.struct), ctypes.byref(plans.struct),
                                        window, _ptr(ws), ws.numel(), _ptr(score), _ptr(bound),
                                        _stream(stream)))
@@ -405,9 +406,10 @@ def local_search(problem: DeviceProblem, plans: DevicePlans, window: int, max_st
     if out is None:
         out = plans_like(plans, problem.n_groups)
     o = PlansOut(int(out.perm.shape[1]), _ptr(out.perm), _ptr(out.qoff), _ptr(out.evict_bits))
-    score = torch.empty(P, dtype=torch.float64, device=dev)
-    steps = torch.empty(P, dtype=torch.int32, device=dev)
-    tr = torch.empty((P, max(max_steps, 1)), dtype=torch.int64, device=dev) if trace else None
+    # sentinels until written: NaN scores, -2 steps and moves
+    score = torch.full((P,), float("nan"), dtype=torch.float64, device=dev)
+    steps = torch.full((P,), -2, dtype=torch.int32, device=dev)
+    tr = torch.full((P, max(max_steps, 1)), -2, dtype=torch.int64, device=dev) if trace else None
     _check(library().qlm_local_search(ctypes.byref(problem.struct), ctypes.byref(plans.struct),
                                       ctypes.byref(o), window, max_steps, _ptr(ws), ws.numel(),
                                       _ptr(score), _ptr(steps), _ptr(tr), _stream(stream)))
@@ -458,8 +460,8 @@ def place_group(problem: DeviceProblem, plans: DevicePlans, group: int, ws=None,
     if out is None:
         out = plans_like(plans, problem.n_groups)
     o = PlansOut(int(out.perm.shape[1]), _ptr(out.perm), _ptr(out.qoff), _ptr(out.evict_bits))
-    score = torch.empty(P, dtype=torch.float64, device=dev)
-    queue = torch.empty(P, dtype=torch.int32, device=dev)
+    score = torch.full((P,), float("nan"), dtype=torch.float64, device=dev)
+    queue = torch.full((P,), -2, dtype=torch.int32, device=dev)
     _check(library().qlm_place_group(ctypes.byref(problem.struct), ctypes.byref(plans.struct),
                                      ctypes.byref(o), int(group), _ptr(ws), ws.numel(),
                                      _ptr(score), _ptr(queue), _stream(stream)))
@@ -497,7 +499,7 @@ def fcfs_score(problem: DeviceProblem, plans: DevicePlans, req_slo, ws=None, str
     if ws is None:
         ws = fcfs_workspace(problem, plans.n_plans, req_slo.numel(), dev)
     if out is None:
-        out = torch.empty(max(plans.n_plans, 1), dtype=torch.float64, device=dev)
+        out = torch.full((max(plans.n_plans, 1),), float("nan"), dtype=torch.float64, device=dev)
     _check(library().qlm_fcfs_score(ctypes.byref(problem.struct), ctypes.byref(plans.struct),
                                     _ptr(req_slo), req_slo.numel(), _ptr(ws), ws.numel(),
                                     _ptr(out), _stream(stream)))
@@ -512,7 +514,7 @@ def fcfs_score_exact(problem: DeviceProblem, plans: DevicePlans, req_slo, plan_i
     idx = torch.as_tensor(plan_index, dtype=torch.int64).to(dev)
     if ws is None:
         ws = fcfs_workspace(problem, plans.n_plans, req_slo.numel(), dev)
-    out = torch.empty(max(idx.numel(), 1), dtype=torch.float64, device=dev)
+    out = torch.full((max(idx.numel(), 1),), float("nan"), dtype=torch.float64, device=dev)
     _check(library().qlm_fcfs_score_exact(ctypes.byref(problem.struct),
                                           ctypes.byref(plans.struct), _ptr(req_slo),
                                           req_slo.numel(), _ptr(idx), idx.numel(), _ptr(ws),
@@ -528,8 +530,8 @@ def fcfs_best_plan(problem: DeviceProblem, plans: DevicePlans, req_slo, ws=None,
     if ws is None:
         ws = fcfs_workspace(problem, plans.n_plans, req_slo.numel(), dev)
     if out is None:
-        bi = torch.empty(1, dtype=torch.int64, device=dev)
-        bs = torch.empty(1, dtype=torch.float64, device=dev)
+        bi = torch.full((1,), -2, dtype=torch.int64, device=dev)
+        bs = torch.full((1,), float("nan"), dtype=torch.float64, device=dev)
     else:
         bi, bs = out
     _check(library().qlm_fcfs_best_plan(ctypes.byref(problem.struct), ctypes.byref(plans.struct),
@@ -600,8 +602,9 @@ class PlaceSession:
         self.stream = stream
         _check(library().qlm_place_begin(ctypes.byref(problem.struct), ctypes.byref(plans.struct),
                                          _ptr(self.ws), self.ws.numel(), _stream(stream)))
-        self.score = torch.empty(max(self.n_plans, 1), dtype=torch.float64, device=self.dev)
-        self.queue = torch.empty(max(self.n_plans, 1), dtype=torch.int32, device=self.dev)
+        self.score = torch.full((max(self.n_plans, 1),), float("nan"), dtype=torch.float64,
+                                device=self.dev)
+        self.queue = torch.full((max(self.n_plans, 1),), -2, dtype=torch.int32, device=self.dev)
 
     def step(self, group: int):
         """Places `group` in every plan; returns (scores [P], places [P]) (device)."""
