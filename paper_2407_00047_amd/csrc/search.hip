@@ -121,7 +121,9 @@ constexpr int kSwapStageBytes = kSwapStage * 24;   // 16-byte records and 8-byte
 constexpr int kSwapRecs = kSwapStageBytes / 32;    // or that many 32-byte slot records
 constexpr int kSwapCostStage = 1024;         // swap-cost entries it stages
 constexpr int kExactBlocks = 64;           // per chain, for the exact re-scores
-constexpr int kStage = 1024;               // tail records staged in LDS at a time
+constexpr int kStage = 256;                // tail records k_fmove stages in LDS at a time
+constexpr int kRelThreads = 64;            // k_frel: one wavefront per workgroup
+constexpr int kRelStage = 1024;            // tail records a k_frel wavefront stages
 constexpr int32_t kMaxSearchGroups = 1 << 16;
 constexpr int32_t kMaxSearchInstances = 4096;
 constexpr int32_t kMaxWindow = 1024;
@@ -1303,16 +1305,17 @@ __global__ __launch_bounds__(kThreads) void k_fmove(SearchArgs a)
         a.smin[b * a.nws + a.nwg_f + (int64_t)((REL ? I : 0) + h) * a.nwg_b + wg] = m;
 }
 
-// Screened RELOCATE within the group's own queue, one lane per slot s: the
-// group goes first, flagged, then the evicted head; the groups between the
-// head and s are the old ones shifted by the group's tokens, variance and the
-// change of costs at the head; the position after s is formed afresh (its
-// tokens and variance ahead are the old ones: the group is ahead of it either
-// way); past it only the costs change.
-__global__ __launch_bounds__(kThreads) void k_frel(SearchArgs a)
+// Screened RELOCATE within the group's own queue, one lane per slot s, one
+// wavefront per workgroup: the group goes first, flagged, then the evicted
+// head; the groups between the head and s are the old ones shifted by the
+// group's tokens, variance and the change of costs at the head; the position
+// after s is formed afresh (its tokens and variance ahead are the old ones:
+// the group is ahead of it either way); past it only the costs change.  The
+// tail records of the wavefront's queues are staged in LDS when they fit.
+__global__ __launch_bounds__(kRelThreads) void k_frel(SearchArgs a)
 {
     __shared__ float2 tab[qlm_tail::kCells];
-    __shared__ double lmin[kWaves];
+    __shared__ TRec st[kRelStage];
     const int64_t b = blockIdx.x / a.nwg_r;
     const int wg = blockIdx.x % a.nwg_r;
     if (a.done[b]) return;                    // the same in the whole workgroup
@@ -1321,9 +1324,9 @@ __global__ __launch_bounds__(kThreads) void k_frel(SearchArgs a)
     const SSt *__restrict__ ss = a.sst + b * G;
     const TRec *__restrict__ tr = a.trec + b * G;
     const int32_t *__restrict__ qof = a.qof + b * (I + 1);
-    for (int k = threadIdx.x; k < qlm_tail::kCells; k += kThreads) tab[k] = a.tail[k];
+    for (int k = threadIdx.x; k < qlm_tail::kCells; k += kRelThreads) tab[k] = a.tail[k];
     __syncthreads();
-    const int s = wg * kThreads + threadIdx.x;
+    const int s = wg * kRelThreads + threadIdx.x;
     bool valid = false, force = false, on1 = false, on2 = false;
     int g = 0, lo1 = 0, hi1 = 0, lo2 = 0, hi2 = 0;
     double q = 0.0, dE1 = 0.0, dE2 = 0.0, vscale = 0.0;
@@ -1379,10 +1382,25 @@ __global__ __launch_bounds__(kThreads) void k_frel(SearchArgs a)
             }
         }
     }
-    auto tr_at = [&](int u) { return tr[u]; };
-    auto v_at = [&](int u) { return ss[u].V; };
-    q += tail_walk(tr_at, v_at, tab, on1, lo1, hi1, dE1, dvz1, 0.0, vscale, false);
-    q += tail_walk(tr_at, v_at, tab, on2, lo2, hi2, dE2, 0.0f, 0.0, vscale, false);
+    // the positions the wavefront walks, staged in LDS when they fit
+    const int wlo = __builtin_amdgcn_readfirstlane((int)wave_min(
+        on1 ? (double)lo1 : (on2 ? (double)lo2 : 1e9)));
+    const int whi = __builtin_amdgcn_readfirstlane((int)wave_max(
+        on2 ? (double)hi2 : (on1 ? (double)hi1 : -1.0)));
+    const bool staged = wlo < whi && whi - wlo <= kRelStage;
+    if (staged)
+        for (int u = wlo + (int)threadIdx.x; u < whi; u += kRelThreads) st[u - wlo] = tr[u];
+    __syncthreads();
+    auto v_at = [&](int u) { return ss[u].V; };    // (not read: exactv is off)
+    if (staged) {
+        auto st_at = [&](int u) { return st[u - wlo]; };
+        q += tail_walk(st_at, v_at, tab, on1, lo1, hi1, dE1, dvz1, 0.0, vscale, false);
+        q += tail_walk(st_at, v_at, tab, on2, lo2, hi2, dE2, 0.0f, 0.0, vscale, false);
+    } else {
+        auto tr_at = [&](int u) { return tr[u]; };
+        q += tail_walk(tr_at, v_at, tab, on1, lo1, hi1, dE1, dvz1, 0.0, vscale, false);
+        q += tail_walk(tr_at, v_at, tab, on2, lo2, hi2, dE2, 0.0f, 0.0, vscale, false);
+    }
     double F = INFINITY, D = 0.0;
     if (valid) {
         const double cur = a.cur[b];
@@ -1395,7 +1413,7 @@ __global__ __launch_bounds__(kThreads) void k_frel(SearchArgs a)
         a.F[b * a.n_moves + k] = F;
         a.D[b * a.n_moves + k] = D;
     }
-    const double m = block_min(F + D, lmin);
+    const double m = wave_min(F + D);
     if (threadIdx.x == 0) a.smin[b * a.nws + a.nwg_f + (int64_t)2 * I * a.nwg_b + wg] = m;
 }
 
@@ -1568,9 +1586,28 @@ __device__ void place_apply(const SearchArgs &a, int64_t b, int s, int h, int p_
     const int lo = left ? s : p;
     const int hi = left ? p - 1 : s;
     if (hi - lo < kStageSlots) {
-        for (int u = lo + threadIdx.x; u <= hi; u += kThreads) {
-            st_perm[u - lo] = perm[u];
-            st_flag[u - lo] = flag[u];
+        // 16 reads in flight per thread before any is stored: the slots
+        // between two far queues are thousands
+        constexpr int kBatch = 16;
+        for (int u0 = lo + (int)threadIdx.x; u0 <= hi; u0 += kBatch * kThreads) {
+            int32_t pv[kBatch];
+            uint8_t fv[kBatch];
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j) {
+                const int u = u0 + j * kThreads;
+                if (u <= hi) {
+                    pv[j] = perm[u];
+                    fv[j] = flag[u];
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j) {
+                const int u = u0 + j * kThreads;
+                if (u <= hi) {
+                    st_perm[u - lo] = pv[j];
+                    st_flag[u - lo] = fv[j];
+                }
+            }
         }
         __syncthreads();
         for (int u = lo + threadIdx.x; u <= hi; u += kThreads) {
@@ -1702,10 +1739,11 @@ __global__ __launch_bounds__(kThreads) void k_sout(SearchArgs a, qlm_plans_out o
 // without the group), c >= I the head of the non-empty queue c - I with the
 // group flagged.  One wavefront per (chain, w), w in [0, 2I]: w < I the place
 // c = w, w = I the group's own queue without it (which every other queue's
-// score shares, in U), w > I the place c = w - 1.  A place in the group's own
-// queue is scored as a plan; a place in another queue h as the score of h
-// with the group (k_place_pick completes it).  A group at its queue's head is
-// running and is not placed (k_place_pick keeps the plan).
+// score shares, in U), w > I the place c = w - 1.  Each place is scored as
+// the score of the queue that receives the group (its own queue without it
+// and with it, or queue h with it); k_place_pick completes the plan scores.
+// A group at its queue's head is running and is not placed (k_place_pick
+// keeps the plan).
 __global__ __launch_bounds__(kThreads) void k_place_eval(SearchArgs a, int group)
 {
     const int G = a.G, I = a.I;
@@ -1716,8 +1754,6 @@ __global__ __launch_bounds__(kThreads) void k_place_eval(SearchArgs a, int group
     const SRec *__restrict__ sr = a.srec + b * G;
     const SSt *__restrict__ ss = a.sst + b * G;
     const int32_t *__restrict__ qof = a.qof + b * (I + 1);
-    const double *T = a.T + b * (I + 1);
-    const double *Q = a.Q + b * I;
     const int s = __builtin_amdgcn_readfirstlane(clampi(a.inv[b * G + group], 0, G - 1));
     SRec x = sr[s];
     const int g = clampi((int)x.q, 0, I - 1);
@@ -1750,16 +1786,14 @@ __global__ __launch_bounds__(kThreads) void k_place_eval(SearchArgs a, int group
         x.nmf |= kFlagBit;
         if (bq < eq) {
             Run r{0.0, 0.0, 0.0, 0.0, model0_of(a, h)};
-            if (h == g) {
+            if (h == g)
                 wave_walk(r, eq - bq, [&](int v) {
                     return v == 0 ? x : (bq + v - 1 < s ? sr[bq + v - 1] : sr[bq + v]);
                 }, theta, cls, a, NoOut{});
-                score = total_with(T, Q, I, g, r.sc);
-            } else {
+            else
                 wave_walk(r, eq - bq + 1, [&](int v) { return v == 0 ? x : sr[bq + v - 1]; },
                           theta, cls, a, NoOut{});
-                score = r.sc;                // completed by k_place_pick
-            }
+            score = r.sc;                    // completed by k_place_pick
         }
     } else {
         p = bq == eq ? bq : insertion_point_wave(sr, bq + 1, eq, x.slo);
@@ -1775,7 +1809,7 @@ __global__ __launch_bounds__(kThreads) void k_place_eval(SearchArgs a, int group
                 wave_walk(r, eq - st, [&](int v) {
                     return v < p - s - 1 ? sr[s + 1 + v] : (v == p - s - 1 ? x : sr[s + v]);
                 }, theta, cls, a, NoOut{});
-            score = total_with(T, Q, I, g, r.sc);
+            score = r.sc;                    // completed by k_place_pick
         } else {
             Run r;
             if (bq == eq) {
@@ -1801,7 +1835,8 @@ __global__ __launch_bounds__(kThreads) void k_place_eval(SearchArgs a, int group
 #pragma clang fp contract(on)
 
 // The place with the lowest exact score (lowest c on ties), applied; a running
-// group stays, and the plan keeps its score.
+// group stays, and the plan keeps its score.  The plan's queue scores are
+// summed here, in queue order (the running sums the totals need).
 __global__ __launch_bounds__(kThreads) void k_place_pick(SearchArgs a, int group, int32_t *queue,
                                                          double *score)
 {
@@ -1824,10 +1859,7 @@ __global__ __launch_bounds__(kThreads) void k_place_pick(SearchArgs a, int group
         v1 = a.cex[b * a.n_moves + threadIdx.x];
         scand[threadIdx.x] = a.cand[b * a.n_moves + threadIdx.x];
     }
-    for (int q = threadIdx.x; q <= I; q += kThreads) {
-        sT[q] = a.T[b * (I + 1) + q];
-        if (q < I) sQ[q] = a.Q[b * I + q];
-    }
+    for (int q = threadIdx.x; q < I; q += kThreads) sQ[q] = a.Q[b * I + q];
     const int s0 = clampi(a.dq[b * 4 + 2], 0, G - 1);
     const int g0 = clampi(a.dq[b * 4 + 3], 0, I - 1);
     if (threadIdx.x == 0) {
@@ -1835,10 +1867,20 @@ __global__ __launch_bounds__(kThreads) void k_place_pick(SearchArgs a, int group
         stay = s0 == a.qof[b * (I + 1) + g0];
     }
     __syncthreads();
+    if (threadIdx.x == 0) {
+        double t = 0.0;
+        sT[0] = 0.0;
+        for (int q = 0; q < I; ++q) {
+            t += sQ[q];
+            sT[q + 1] = t;
+        }
+    }
+    __syncthreads();
     if (stay) {
         if (threadIdx.x == 0) {
+            a.cur[b] = sT[I];
             if (queue) queue[b] = g0;
-            if (score) score[b] = a.cur[b];
+            if (score) score[b] = sT[I];
             a.dq[b * 4] = g0;
             a.dq[b * 4 + 1] = g0;
         }
@@ -1852,10 +1894,8 @@ __global__ __launch_bounds__(kThreads) void k_place_pick(SearchArgs a, int group
     for (int c = threadIdx.x; c < n; c += kThreads) {
         double v = one ? v1 : a.cex[b * a.n_moves + c];
         const int h = c < I ? c : c - I;
-        if (h != g0) {
-            v = total_with2(T, Q, I, g0, rg, h, v);
-            a.cex[b * a.n_moves + c] = v;
-        }
+        v = h != g0 ? total_with2(T, Q, I, g0, rg, h, v) : total_with(T, Q, I, g0, v);
+        a.cex[b * a.n_moves + c] = v;
         if (better(v, c, best, bk)) {
             best = v;
             bk = c;
@@ -2073,7 +2113,7 @@ Layout layout(int G, int I, int W, int64_t B)
     L.nwg_b = (G + kThreads - 1) / kThreads;
     L.nwg = L.nwg_a + 2 * I * L.nwg_b;
     L.nwg_f = (int)(((int64_t)G * (W + 1) + kThreads - 1) / kThreads);
-    L.nwg_r = (G + kThreads - 1) / kThreads;
+    L.nwg_r = (G + kRelThreads - 1) / kRelThreads;
     L.nws = L.nwg_f + 2 * I * L.nwg_b + L.nwg_r;
     L.n_moves = (int64_t)G * W + 2 * (int64_t)G * I;
     size_t o = 0;
@@ -2294,7 +2334,7 @@ int screen_moves(SearchArgs &a, hipStream_t stream)
     qlm_internal::timing_end(stream, &tl);
     hipLaunchKernelGGL(k_fmove<true>, mgrid, dim3(kThreads), 0, stream, a);
     if ((rc = launched("k_fmove (relocate) launch"))) return rc;
-    hipLaunchKernelGGL(k_frel, dim3((unsigned)(a.nwg_r * a.B)), dim3(kThreads), 0, stream, a);
+    hipLaunchKernelGGL(k_frel, dim3((unsigned)(a.nwg_r * a.B)), dim3(kRelThreads), 0, stream, a);
     return launched("k_frel launch");
 }
 
@@ -2316,7 +2356,10 @@ int place_step(SearchArgs &a, int32_t group, int32_t *queue, double *score, bool
                        queue, score);
     if ((rc = launched("k_place_pick launch"))) return rc;
     if (!refresh) return QLM_OK;
-    return launch_state(a, 2, stream);
+    // k_place_pick sums the queue scores itself: the cache alone
+    const int nblk = (a.I + kWaves - 1) / kWaves;
+    hipLaunchKernelGGL(k_sstate, dim3((unsigned)(nblk * a.B)), dim3(kThreads), 0, stream, a, 2);
+    return launched("k_sstate launch");
 }
 
 // The chains' plans back to the caller's layout, with their scores.
