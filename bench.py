@@ -33,9 +33,12 @@ PEAK_VALU_LANES = 256 * 4 * 16 * 2.4e9
 # per-block work excluded); the measured count per slot, those included, comes
 # from the committed SQ counter summary when it matches the kernel source
 VALU_PER_SLOT = 22
-# VALU instructions per visited position in the main loop of the reassignment
-# screen (k_fmove), counted in its compiled loop body.
-VALU_PER_VISIT = 13
+# VALU instructions per visited position in the main loop of the screen of
+# moves into another queue (k_fmove), counted in its compiled loop body: margin
+# (v_add_f64, v_cvt_f32_f64), variance (v_add_f32), v_rsq_f32, cell coordinate
+# (v_fma_f32, v_med3_f32), cell address (v_lshrrev_b32, v_and_b32), the cell's
+# line and the weighted sum (two v_fma_f32)
+VALU_PER_VISIT = 10
 
 
 def log(*a):
@@ -257,11 +260,14 @@ def measured_counters(config: str, plans: int):
 
 def move_counts(problem, plans, p, window):
     """Valid moves of plan p by kind (swaps within a queue, reassignments,
-    relocations to a queue's head) and the positions the reassignment screen
-    visits for them: for a group moving to queue h, itself at its insertion
-    point after h's head and every position of h from there on (one position
-    when it goes to the end or into an empty queue).  A queue's head (its
-    running group) takes part in no move."""
+    relocations to a queue's head) and the positions the screen of moves into
+    another queue (k_fmove) visits for them: for a group moving to queue h,
+    itself at its insertion point after h's head and every position of h from
+    there on (one position when it goes to the end or into an empty queue);
+    for a group relocated to the head of another queue h, itself and every
+    position of h; for a group relocated to the head of its own queue, every
+    position of it.  A queue's head (its running group) takes part in no
+    move."""
     import numpy as np
     G, I = problem["n_groups"], problem["n_instances"]
     perm = plans["perm"][:, p]
@@ -289,6 +295,8 @@ def move_counts(problem, plans, p, window):
         pmax = np.maximum.accumulate(slo[perm[b + 1:e]]) if L > 1 else np.zeros(0, np.float32)
         pos = 1 + np.searchsorted(pmax, x, side="right")       # first later SLO after the head
         visits += int(np.sum(np.where(pos == L, 1, L - pos + 1)))
+        visits += int(x.size) * (L + 1)                        # relocations to its head
+        visits += (L - 1) * L                                  # relocations within h
     return {"valid": swaps + moves + relocations, "swaps": swaps, "moves": moves,
             "relocations": relocations, "visits": visits}
 

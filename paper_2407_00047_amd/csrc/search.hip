@@ -72,11 +72,11 @@
 //              s without s (for the MOVEs of s), and screened SWAP(s, d); the
 //              positions past the changes are walked in step by the wavefront
 //   k_fmove    one wavefront per (target queue h, 64 groups adjacent in SLO
-//              order): screened MOVE, and (a second launch) screened RELOCATE
-//              into another queue; the positions past the insertion points are
-//              walked in step by the whole wavefront (one record read per
-//              position for all 64 moves)
-//   k_frel     one lane per slot: screened RELOCATE within the slot's queue
+//              order): screened MOVE and screened RELOCATE into another
+//              queue; the positions past the insertion points are walked in
+//              step by the whole wavefront (one record read per position for
+//              all 64 moves); in the same launch, one lane per slot: screened
+//              RELOCATE within the slot's queue
 //   k_sbound / k_sselect / k_sexact   the bound min(F + D), the candidates,
 //              their exact scores
 //   k_spick    lowest (exact score, k) of the candidates; applied when it
@@ -122,8 +122,8 @@ constexpr int kSwapRecs = kSwapStageBytes / 32;    // or that many 32-byte slot 
 constexpr int kSwapCostStage = 1024;         // swap-cost entries it stages
 constexpr int kExactBlocks = 64;           // per chain, for the exact re-scores
 constexpr int kStage = 256;                // tail records k_fmove stages in LDS at a time
-constexpr int kRelThreads = 64;            // k_frel: one wavefront per workgroup
-constexpr int kRelStage = 1024;            // tail records a k_frel wavefront stages
+constexpr int kRelStage = 128;             // tail records each wavefront of the
+                                           // own-queue relocation screen stages
 constexpr int32_t kMaxSearchGroups = 1 << 16;
 constexpr int32_t kMaxSearchInstances = 4096;
 constexpr int32_t kMaxWindow = 1024;
@@ -216,8 +216,8 @@ struct SearchArgs {
                                   // the group's slot and queue
     int32_t nwg_a, nwg_b, nwg;    // per chain: k_sswap, k_smove and k_sreloc (per
                                   // queue), total
-    int32_t nwg_f, nwg_r, nws;    // per chain: k_fswap (d = 0..W), k_frel, all screen
-                                  // workgroups
+    int32_t nwg_f, nwg_r, nws;    // per chain: k_fswap (d = 0..W), k_fmove's own-queue
+                                  // relocations, all screen workgroups
     int64_t n_moves;
     double *move_score;           // [B][n_moves] or null (exact kernels)
     int64_t *trace;               // [B][max_steps] or null
@@ -1173,17 +1173,14 @@ __global__ __launch_bounds__(kThreads) void k_fswap(SearchArgs a)
 // the old one shifted by the group's tokens, variance and the change of costs,
 // walked by the whole wavefront in step from the earliest insertion point.
 template <bool REL>
-__global__ __launch_bounds__(kThreads) void k_fmove(SearchArgs a)
+__device__ inline void fmove_body(const SearchArgs &a, int bid, float2 *tab, double *lmin,
+                                  int *lint, TRec *stage)
 {
-    __shared__ float2 tab[qlm_tail::kCells];
-    __shared__ double lmin[kWaves];
-    __shared__ int lint[kWaves];
-    __shared__ TRec stage[kStage];
     const int G = a.G, I = a.I;
     const int per_chain = I * a.nwg_b;
-    const int64_t b = blockIdx.x / per_chain;
-    const int h = (blockIdx.x % per_chain) / a.nwg_b;
-    const int wg = blockIdx.x % a.nwg_b;
+    const int64_t b = bid / per_chain;
+    const int h = (bid % per_chain) / a.nwg_b;
+    const int wg = bid % a.nwg_b;
     if (a.done[b]) return;                    // the same in the whole workgroup
     const SRec *__restrict__ sr = a.srec + b * G;
     const SSt *__restrict__ ss = a.sst + b * G;
@@ -1265,6 +1262,9 @@ __global__ __launch_bounds__(kThreads) void k_fmove(SearchArgs a)
             const int c1 = min(c0 + kStage, eq);
             __syncthreads();
             for (int u = c0 + (int)threadIdx.x; u < c1; u += kThreads) stage[u - c0] = tr[u];
+            // seven blank records past the chunk (no requests, a finite margin
+            // and variance): the unrolled walk reads up to seven past its end
+            if (threadIdx.x < 7) stage[c1 - c0 + threadIdx.x] = TRec{0.0, 1.0f, 0.0f};
             __syncthreads();
             int u = max(c0, ulo);
             // masked part: some lanes' tails start later
@@ -1273,15 +1273,16 @@ __global__ __launch_bounds__(kThreads) void k_fmove(SearchArgs a)
                 const float q = qlm_tail::q_of(tab, (float)(x.m - dE), x.vz + dvz);
                 acc += (double)((tail && u > p) ? x.n * q : 0.0f);
             }
-            // every lane with a tail is in it now
+            // every lane with a tail is in it now: blocks of eight records at
+            // one address and fixed offsets
             for (; u < c1; u += 8) {
+                const TRec *xs = stage + (u - c0);
                 float s32 = 0.0f;
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
-                    const int uu = min(u + j, c1 - 1);
-                    const TRec x = stage[uu - c0];
+                    const TRec x = xs[j];
                     const float q = qlm_tail::q_of(tab, (float)(x.m - dE), x.vz + dvz);
-                    s32 = fmaf(u + j < c1 ? x.n : 0.0f, q, s32);
+                    s32 = fmaf(x.n, q, s32);
                 }
                 acc += (double)s32;
             }
@@ -1295,7 +1296,7 @@ __global__ __launch_bounds__(kThreads) void k_fmove(SearchArgs a)
         F = cur + (a.R[b * G + s] - a.Q[b * I + g]) + (N - Qh);
         D = force ? INFINITY : a.RD[b * G + s] + kEpsP * nq + 1e-12 * (fabs(cur) + nq);
     }
-    if (r < G && (!REL || g != h)) {          // k_frel screens RELOCATE into the own queue
+    if (r < G && (!REL || g != h)) {          // frel_body screens RELOCATE into the own queue
         const int64_t k = (int64_t)G * a.W + (REL ? (int64_t)G * I : 0) + (int64_t)s * I + h;
         a.F[b * a.n_moves + k] = F;
         a.D[b * a.n_moves + k] = D;
@@ -1305,28 +1306,28 @@ __global__ __launch_bounds__(kThreads) void k_fmove(SearchArgs a)
         a.smin[b * a.nws + a.nwg_f + (int64_t)((REL ? I : 0) + h) * a.nwg_b + wg] = m;
 }
 
-// Screened RELOCATE within the group's own queue, one lane per slot s, one
-// wavefront per workgroup: the group goes first, flagged, then the evicted
-// head; the groups between the head and s are the old ones shifted by the
-// group's tokens, variance and the change of costs at the head; the position
-// after s is formed afresh (its tokens and variance ahead are the old ones:
-// the group is ahead of it either way); past it only the costs change.  The
-// tail records of the wavefront's queues are staged in LDS when they fit.
-__global__ __launch_bounds__(kRelThreads) void k_frel(SearchArgs a)
+// Screened RELOCATE within the group's own queue, one lane per slot s: the
+// group goes first, flagged, then the evicted head; the groups between the
+// head and s are the old ones shifted by the group's tokens, variance and the
+// change of costs at the head; the position after s is formed afresh (its
+// tokens and variance ahead are the old ones: the group is ahead of it either
+// way); past it only the costs change.  Each wavefront stages the tail
+// records of its queues in LDS when they fit (st: kRelStage per wavefront).
+__device__ inline void frel_body(const SearchArgs &a, int bid, float2 *tab, double *lmin,
+                                 TRec *stall)
 {
-    __shared__ float2 tab[qlm_tail::kCells];
-    __shared__ TRec st[kRelStage];
-    const int64_t b = blockIdx.x / a.nwg_r;
-    const int wg = blockIdx.x % a.nwg_r;
+    const int64_t b = bid / a.nwg_r;
+    const int wg = bid % a.nwg_r;
     if (a.done[b]) return;                    // the same in the whole workgroup
     const int G = a.G, I = a.I;
     const SRec *__restrict__ sr = a.srec + b * G;
     const SSt *__restrict__ ss = a.sst + b * G;
     const TRec *__restrict__ tr = a.trec + b * G;
     const int32_t *__restrict__ qof = a.qof + b * (I + 1);
-    for (int k = threadIdx.x; k < qlm_tail::kCells; k += kRelThreads) tab[k] = a.tail[k];
+    TRec *st = stall + wave_id() * kRelStage;
+    for (int k = threadIdx.x; k < qlm_tail::kCells; k += kThreads) tab[k] = a.tail[k];
     __syncthreads();
-    const int s = wg * kRelThreads + threadIdx.x;
+    const int s = wg * kThreads + threadIdx.x;
     bool valid = false, force = false, on1 = false, on2 = false;
     int g = 0, lo1 = 0, hi1 = 0, lo2 = 0, hi2 = 0;
     double q = 0.0, dE1 = 0.0, dE2 = 0.0, vscale = 0.0;
@@ -1389,7 +1390,8 @@ __global__ __launch_bounds__(kRelThreads) void k_frel(SearchArgs a)
         on2 ? (double)hi2 : (on1 ? (double)hi1 : -1.0)));
     const bool staged = wlo < whi && whi - wlo <= kRelStage;
     if (staged)
-        for (int u = wlo + (int)threadIdx.x; u < whi; u += kRelThreads) st[u - wlo] = tr[u];
+        for (int u = wlo + (int)(threadIdx.x & (kWave - 1)); u < whi; u += kWave)
+            st[u - wlo] = tr[u];
     __syncthreads();
     auto v_at = [&](int u) { return ss[u].V; };    // (not read: exactv is off)
     if (staged) {
@@ -1413,8 +1415,32 @@ __global__ __launch_bounds__(kRelThreads) void k_frel(SearchArgs a)
         a.F[b * a.n_moves + k] = F;
         a.D[b * a.n_moves + k] = D;
     }
-    const double m = wave_min(F + D);
+    const double m = block_min(F + D, lmin);
     if (threadIdx.x == 0) a.smin[b * a.nws + a.nwg_f + (int64_t)2 * I * a.nwg_b + wg] = m;
+}
+
+// The screens of moves into another queue and of relocations, in one launch
+// (more wavefronts to hide each one's set-up; the short own-queue relocation
+// screens run beside the long ones).  Per launch: nwg_r * B workgroups screen
+// the relocations within a queue, then I * nwg_b * B the MOVEs, then as many
+// the RELOCATEs into another queue.
+__global__ __launch_bounds__(kThreads) void k_fmove(SearchArgs a)
+{
+    __shared__ float2 tab[qlm_tail::kCells];
+    __shared__ double lmin[kWaves];
+    __shared__ int lint[kWaves];
+    // (the move screens stage kStage records and seven blank ones)
+    static_assert(kWaves * kRelStage >= kStage + 7, "the screens' staging buffer");
+    __shared__ TRec stage[kWaves * kRelStage];
+    const int nrel = (int)((int64_t)a.nwg_r * a.B);
+    const int half = (int)((int64_t)a.I * a.nwg_b * a.B);
+    const int bid = (int)blockIdx.x;
+    if (bid < nrel)
+        frel_body(a, bid, tab, lmin, stage);
+    else if (bid < nrel + half)
+        fmove_body<false>(a, bid - nrel, tab, lmin, lint, stage);
+    else
+        fmove_body<true>(a, bid - nrel - half, tab, lmin, lint, stage);
 }
 
 // The bound of the chain's lowest exact score, min(F + D); the candidate list
@@ -2113,7 +2139,7 @@ Layout layout(int G, int I, int W, int64_t B)
     L.nwg_b = (G + kThreads - 1) / kThreads;
     L.nwg = L.nwg_a + 2 * I * L.nwg_b;
     L.nwg_f = (int)(((int64_t)G * (W + 1) + kThreads - 1) / kThreads);
-    L.nwg_r = (G + kRelThreads - 1) / kRelThreads;
+    L.nwg_r = (G + kThreads - 1) / kThreads;
     L.nws = L.nwg_f + 2 * I * L.nwg_b + L.nwg_r;
     L.n_moves = (int64_t)G * W + 2 * (int64_t)G * I;
     size_t o = 0;
@@ -2326,16 +2352,13 @@ int screen_moves(SearchArgs &a, hipStream_t stream)
     hipLaunchKernelGGL(k_fswap, dim3((unsigned)(a.nwg_f * a.B)), dim3(kThreads), 0, stream, a);
     int rc = launched("k_fswap launch");
     if (rc) return rc;
-    const dim3 mgrid((unsigned)((int64_t)a.I * a.nwg_b * a.B));
+    const dim3 mgrid((unsigned)((2 * (int64_t)a.I * a.nwg_b + a.nwg_r) * a.B));
     qlm_internal::TimedLaunch tl;
     if ((rc = qlm_internal::timing_begin(stream, &tl))) return rc;
-    hipLaunchKernelGGL(k_fmove<false>, mgrid, dim3(kThreads), 0, stream, a);
+    hipLaunchKernelGGL(k_fmove, mgrid, dim3(kThreads), 0, stream, a);
     if ((rc = launched("k_fmove launch"))) return rc;
     qlm_internal::timing_end(stream, &tl);
-    hipLaunchKernelGGL(k_fmove<true>, mgrid, dim3(kThreads), 0, stream, a);
-    if ((rc = launched("k_fmove (relocate) launch"))) return rc;
-    hipLaunchKernelGGL(k_frel, dim3((unsigned)(a.nwg_r * a.B)), dim3(kRelThreads), 0, stream, a);
-    return launched("k_frel launch");
+    return QLM_OK;
 }
 
 // The placement of one group in every chain: the candidate queues scored
