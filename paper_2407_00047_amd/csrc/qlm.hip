@@ -909,13 +909,11 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
             Y = Y + nmu;
 
             // (3) tail cell of slot s
-            float tt = fmaf((float)nnum, rs, kTailMid);
-            tt = __builtin_amdgcn_fmed3f(tt, kTailLo, kTailHi);   // NaN (0 / 0) -> low end
-            const uint32_t cell = (__float_as_uint(tt) & kTailCellBits) >> 10;   // cell * 8
-            tf = tt;
+            tf = __builtin_amdgcn_fmed3f(fmaf((float)nnum, rs, kTailMid), kTailLo, kTailHi);
             tnx = r.x;
             // settled before the branch: nothing of slot s may sink into it
             asm volatile("" : "+v"(tf), "+v"(vblk));
+            const uint32_t cell = (__float_as_uint(tf) & kTailCellBits) >> 10;   // cell * 8
 
             // (4) queue head at s+1?
             if (s + 1 - base == nbr) {       // s + 1 == nb, compared block-relative
