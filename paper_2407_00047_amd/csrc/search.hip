@@ -1893,12 +1893,25 @@ __global__ __launch_bounds__(kThreads) void k_place_pick(SearchArgs a, int group
         stay = s0 == a.qof[b * (I + 1) + g0];
     }
     __syncthreads();
-    if (threadIdx.x == 0) {
-        double t = 0.0;
-        sT[0] = 0.0;
-        for (int q = 0; q < I; ++q) {
-            t += sQ[q];
-            sT[q + 1] = t;
+    // the running sums of the queue scores, in queue order (the additions of a
+    // serial sum, rippled across the first wavefront's lanes)
+    if (threadIdx.x < kWave) {
+        const int lane = threadIdx.x;
+        double carry = 0.0;
+        if (lane == 0) sT[0] = 0.0;
+        for (int q0 = 0; q0 < I; q0 += kWave) {
+            const int cnt = min(kWave, I - q0);
+            const double x = lane < cnt ? sQ[q0 + lane] : 0.0;
+            const double lx = from_left0(x);
+            double t = carry;
+            const int steps = __builtin_amdgcn_readfirstlane(cnt - 1);
+            for (int j = 0; j < steps; j += 8) {
+#pragma unroll
+                for (int u = 0; u < 8; ++u) t = from_left(t) + lx;
+            }
+            const double t1 = t + x;
+            if (lane < cnt) sT[q0 + lane + 1] = t1;
+            carry = lane_value(t1, cnt - 1);
         }
     }
     __syncthreads();
