@@ -543,16 +543,21 @@ def bench_place(args):
     for g in groups[:max(args.warmup, 1)]:
         ses.step(g)
     torch.cuda.synchronize()
-    qlm.timing_enable(True)
-    qlm.timing_read()
     e0.record(stream)
     for g in groups[max(args.warmup, 1):max(args.warmup, 1) + K]:
         ses.step(g)
     e1.record(stream)
     torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / K
+    # the candidate kernel's own duration, in further steps (the events the
+    # library then records around it are kept out of the timed steps above)
+    qlm.timing_enable(True)
+    qlm.timing_read()
+    for g in groups[:K]:
+        ses.step(g)
+    torch.cuda.synchronize()
     n_launch, k_ms = qlm.timing_read()
     qlm.timing_enable(False)
-    ms = e0.elapsed_time(e1) / K
     ses.end()
     # the single call, for comparison
     K1 = min(K, 20)

@@ -328,9 +328,8 @@ int qlm_place_group(const qlm_problem *problem, const qlm_plans *start,
 /*
  * A placement session: the plans stay in the workspace between placements, so
  * that a stream of arrivals and violations is placed one group after another
- * without reloading the plans, and each placement re-forms only the cache of
- * the queues it changed (every queue from the group's old queue to its new
- * one; the others keep theirs).
+ * without reloading the plans; each placement changes the plan in place and
+ * keeps the queue scores and every group's slot up to date.
  *   qlm_place_begin  loads the plans (as qlm_place_group reads them) and
  *                    forms their cache in ws (qlm_search_workspace_bytes(
  *                    problem, P, 0) bytes, 256-byte aligned)

@@ -211,9 +211,8 @@ struct SearchArgs {
     int32_t *ncand;               // [1]
     double *U;                    // [1] min(F + D)
     int32_t *scratch;             // [2 G] shifts of k_spick
-    int32_t *dq;                  // [4] placement: the queues a placement changed
-                                  // (every queue from the lower to the higher),
-                                  // the group's slot and queue
+    int32_t *dq;                  // [4] placement: the group's slot and queue, and
+                                  // whether it is running (stays)
     int32_t nwg_a, nwg_b, nwg;    // per chain: k_sswap, k_smove and k_sreloc (per
                                   // queue), total
     int32_t nwg_f, nwg_r, nws;    // per chain: k_fswap (d = 0..W), k_fmove's own-queue
@@ -494,14 +493,20 @@ __device__ void wave_walk_rounds(Run &r, int nv, const LoadRound &load, double t
     }
 }
 
+// wave_walk takes position v's record from rec(v); the next round's records
+// are read while a round ripples.
 template <class RecOf, class Out>
 __device__ void wave_walk(Run &r, int nv, const RecOf &rec, double theta, int cls,
                           const SearchArgs &a, const Out &out)
 {
     const int lane = threadIdx.x & (kWave - 1);
-    wave_walk_rounds(r, nv, [&](int v0, bool on) {
-        SRec x{};
-        if (on) x = rec(v0 + lane);
+    SRec nxt{};
+    if (lane < nv) nxt = rec(lane);
+    wave_walk_rounds(r, nv, [&](int v0, bool) {
+        const SRec x = nxt;
+        const int v1 = v0 + kWave + lane;
+        nxt = SRec{};
+        if (v1 < nv) nxt = rec(v1);
         return x;
     }, theta, cls, a, out);
 }
@@ -654,8 +659,6 @@ __global__ __launch_bounds__(kThreads) void k_sstate(SearchArgs a, int force)
     const int g = (blockIdx.x % nblk) * kWaves + wave_id();
     const int lane = threadIdx.x & (kWave - 1);
     if (g >= I || (!force && a.done[b])) return;
-    // force == 2: only the queues a placement changed
-    if (force == 2 && (g < a.dq[b * 4] || g > a.dq[b * 4 + 1])) return;
     const int32_t *__restrict__ perm = a.perm + b * G;
     const uint8_t *__restrict__ flag = a.flag + b * G;
     SRec *__restrict__ sr = a.srec + b * G;
@@ -1592,8 +1595,8 @@ __global__ __launch_bounds__(kThreads) void k_sexact(SearchArgs a)
 // (by default its EDF position after h's head: a reassignment, or with h its
 // own queue a re-insertion; a relocation passes h's head slot and `evict`,
 // which sets the group's flag): the slots between its old and new place
-// rotate by one, and the queue offsets between the two queues shift.  Run by
-// a whole workgroup.
+// rotate by one (with the slot index of each group moved), and the queue
+// offsets between the two queues shift.  Run by a whole workgroup.
 __device__ void place_apply(const SearchArgs &a, int64_t b, int s, int h, int p_known = -1,
                             int g_known = -1, bool evict = false)
 {
@@ -1604,6 +1607,7 @@ __device__ void place_apply(const SearchArgs &a, int64_t b, int s, int h, int p_
     int32_t *perm = a.perm + b * G;
     uint8_t *flag = a.flag + b * G;
     int32_t *qof = a.qof + b * (I + 1);
+    int32_t *inv = a.inv + b * G;
     const SRec *sr = a.srec + b * G;
     const int g = g_known >= 0 ? g_known : (int)sr[s].q;
     const int p = p_known >= 0 ? p_known : edf_point(sr, qof[h], qof[h + 1], sr[s].slo);
@@ -1638,8 +1642,10 @@ __device__ void place_apply(const SearchArgs &a, int64_t b, int s, int h, int p_
         __syncthreads();
         for (int u = lo + threadIdx.x; u <= hi; u += kThreads) {
             const int v = left ? (u == hi ? s : u + 1) : (u == lo ? s : u - 1);
-            perm[u] = st_perm[v - lo];
+            const int32_t i = st_perm[v - lo];
+            perm[u] = i;
             flag[u] = st_flag[v - lo];
+            inv[clampi(i, 0, G - 1)] = u;
         }
     } else {
         int32_t *sp = a.scratch + b * 2 * G;
@@ -1651,8 +1657,10 @@ __device__ void place_apply(const SearchArgs &a, int64_t b, int s, int h, int p_
         __syncthreads();
         for (int u = lo + threadIdx.x; u <= hi; u += kThreads) {
             const int v = left ? (u == hi ? s : u + 1) : (u == lo ? s : u - 1);
-            perm[u] = sp[v];
+            const int32_t i = sp[v];
+            perm[u] = i;
             flag[u] = (uint8_t)sf[v];
+            inv[clampi(i, 0, G - 1)] = u;
         }
     }
     if (h > g) {
@@ -1768,8 +1776,10 @@ __global__ __launch_bounds__(kThreads) void k_sout(SearchArgs a, qlm_plans_out o
 // score shares, in U), w > I the place c = w - 1.  Each place is scored as
 // the score of the queue that receives the group (its own queue without it
 // and with it, or queue h with it); k_place_pick completes the plan scores.
-// A group at its queue's head is running and is not placed (k_place_pick
-// keeps the plan).
+// The walks read the plan itself (group ids, flags, group records): a
+// placement session keeps only the plan, the slot of every group and the
+// queue scores up to date between its steps.  A group at its queue's head is
+// running and is not placed (k_place_pick keeps the plan).
 __global__ __launch_bounds__(kThreads) void k_place_eval(SearchArgs a, int group)
 {
     const int G = a.G, I = a.I;
@@ -1777,84 +1787,93 @@ __global__ __launch_bounds__(kThreads) void k_place_eval(SearchArgs a, int group
     const int64_t b = blockIdx.x / nblk;
     const int w = (blockIdx.x % nblk) * kWaves + wave_id();
     if (w > 2 * I) return;
-    const SRec *__restrict__ sr = a.srec + b * G;
-    const SSt *__restrict__ ss = a.sst + b * G;
+    const int32_t *__restrict__ perm = a.perm + b * G;
+    const uint8_t *__restrict__ flag = a.flag + b * G;
     const int32_t *__restrict__ qof = a.qof + b * (I + 1);
+    const int lane = threadIdx.x & (kWave - 1);
     const int s = __builtin_amdgcn_readfirstlane(clampi(a.inv[b * G + group], 0, G - 1));
-    SRec x = sr[s];
-    const int g = clampi((int)x.q, 0, I - 1);
-    const int bg = clampi(qof[g], 0, G), eg = clampi(qof[g + 1], bg, G);
-    const bool lead = (threadIdx.x & (kWave - 1)) == 0;
-    if (w == I) {
-        if (lead) {
-            a.dq[b * 4 + 2] = s;
-            a.dq[b * 4 + 3] = g;
+    // the group's queue: the last g with qof[g] <= s
+    int g = 0;
+    {
+        int lo = 0, hi = I - 1;
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (qof[mid] <= s)
+                lo = mid;
+            else
+                hi = mid - 1;
         }
-        if (s == bg) return;
-        Run rg = start_at(a, sr, ss, s, bg, g);
-        wave_walk(rg, eg - s - 1, [&](int v) { return sr[s + 1 + v]; }, (double)a.inst_tput[g],
-                  clampi(a.inst_class[g], 0, a.C - 1), a, NoOut{});
-        if (lead) a.U[b] = rg.sc;
-        return;
+        g = __builtin_amdgcn_readfirstlane(lo);
+    }
+    const int bg = clampi(qof[g], 0, G);
+    const bool lead = lane == 0;
+    if (w == I && lead) {
+        a.dq[b * 4] = s;
+        a.dq[b * 4 + 1] = g;
+        a.dq[b * 4 + 2] = s == bg;             // running: it stays
     }
     if (s == bg) return;                       // running: it stays
+    auto rec_at = [&](int u) __attribute__((always_inline)) {
+        const GRec gr = a.grec[clampi(perm[u], 0, G - 1)];
+        SRec x{};
+        x.a = gr.a;
+        x.b = gr.b;
+        x.slo = gr.slo;
+        x.nmf = gr.nm | (flag[u] ? kFlagBit : 0u);
+        return x;
+    };
+    SRec x = rec_at(s);
+    // the place: w = I its own queue without it; else queue h, the group at the
+    // head (flagged) or at its EDF position
     const int c = w < I ? w : w - 1;
-    const bool head = c >= I;
-    const int h = head ? c - I : c;
+    const bool head = w != I && c >= I;
+    const int h = w == I ? g : (head ? c - I : c);
     const int bq = clampi(qof[h], 0, G), eq = clampi(qof[h + 1], bq, G);
+    const bool own = h == g;
+    const int L = eq - bq - (own ? 1 : 0);     // the queue's positions without the group
+    auto src = [&](int v) __attribute__((always_inline)) {
+        return bq + v + (own && bq + v >= s ? 1 : 0);
+    };
+    auto raw = [&](int v) __attribute__((always_inline)) { return rec_at(src(v)); };
     const double theta = (double)a.inst_tput[h];
     const int cls = clampi(a.inst_class[h], 0, a.C - 1);
+    Run r{0.0, 0.0, 0.0, 0.0, model0_of(a, h)};
+    if (w == I) {
+        wave_walk(r, L, raw, theta, cls, a, NoOut{});
+        if (lead) a.U[b] = r.sc;
+        return;
+    }
     double score = INFINITY;
-    int p = bq;
+    int p = bq;                                // insertion slot, in the plan as it stands
+    int ip = 0;                                // the group's position in the walk
     if (head) {
         // at the head, ahead of the running group (an empty queue has none to
         // evict: no place)
         x.nmf |= kFlagBit;
-        if (bq < eq) {
-            Run r{0.0, 0.0, 0.0, 0.0, model0_of(a, h)};
-            if (h == g)
-                wave_walk(r, eq - bq, [&](int v) {
-                    return v == 0 ? x : (bq + v - 1 < s ? sr[bq + v - 1] : sr[bq + v]);
-                }, theta, cls, a, NoOut{});
-            else
-                wave_walk(r, eq - bq + 1, [&](int v) { return v == 0 ? x : sr[bq + v - 1]; },
-                          theta, cls, a, NoOut{});
-            score = r.sc;                    // completed by k_place_pick
-        }
     } else {
-        p = bq == eq ? bq : insertion_point_wave(sr, bq + 1, eq, x.slo);
-        if (h == g) {
-            // its own queue: from the first position that changes, the queue
-            // without s with the group at the insertion point
-            const int st = min(s, p);
-            Run r = start_at(a, sr, ss, st, bq, g);
-            if (p <= s)
-                wave_walk(r, eq - st, [&](int v) { return v == 0 ? x : (v <= s - p ? sr[p + v - 1] : sr[p + v]); },
-                          theta, cls, a, NoOut{});
-            else
-                wave_walk(r, eq - st, [&](int v) {
-                    return v < p - s - 1 ? sr[s + 1 + v] : (v == p - s - 1 ? x : sr[s + v]);
-                }, theta, cls, a, NoOut{});
-            score = r.sc;                    // completed by k_place_pick
-        } else {
-            Run r;
-            if (bq == eq) {
-                r = Run{0.0, 0.0, 0.0, 0.0, model0_of(a, h)};
-                wave_walk(r, 1, [&](int) { return x; }, theta, cls, a, NoOut{});
-            } else if (p == eq) {
-                r = start_at(a, sr, ss, eq - 1, bq, h);
-                wave_walk(r, 2, [&](int v) { return v == 0 ? sr[eq - 1] : x; }, theta, cls, a, NoOut{});
-            } else {
-                r = start_at(a, sr, ss, p, bq, h);
-                wave_walk(r, eq - p + 1, [&](int v) { return v == 0 ? x : sr[p + v - 1]; }, theta, cls,
-                          a, NoOut{});
+        // the EDF position: before the first group after the head whose SLO
+        // is strictly later (position ip of the queue without the group)
+        ip = L;
+        for (int v0 = 0; v0 < L; v0 += kWave) {
+            const int v = v0 + lane;
+            const uint64_t m =
+                __builtin_amdgcn_ballot_w64(v >= 1 && v < L && raw(min(v, L - 1)).slo > x.slo);
+            if (m) {
+                ip = v0 + (int)__builtin_ctzll(m);
+                break;
             }
-            score = r.sc;                    // completed by k_place_pick
         }
+        ip = __builtin_amdgcn_readfirstlane(ip);
+        p = ip < L ? src(ip) : eq;
+    }
+    if (!head || L > 0) {
+        wave_walk(r, L + 1, [&](int v) { return v == ip ? x : raw(v < ip ? v : v - 1); }, theta,
+                  cls, a, NoOut{});
+        score = r.sc;
     }
     if (lead) {
-        a.cex[b * a.n_moves + c] = score;
-        a.cand[b * a.n_moves + c] = p;       // the insertion point, for the pick
+        a.cex[b * a.n_moves + c] = score;      // completed by k_place_pick
+        a.cand[b * a.n_moves + c] = p;         // the insertion point, for the pick
     }
 }
 
@@ -1863,7 +1882,7 @@ __global__ __launch_bounds__(kThreads) void k_place_eval(SearchArgs a, int group
 // The place with the lowest exact score (lowest c on ties), applied; a running
 // group stays, and the plan keeps its score.  The plan's queue scores are
 // summed here, in queue order (the running sums the totals need).
-__global__ __launch_bounds__(kThreads) void k_place_pick(SearchArgs a, int group, int32_t *queue,
+__global__ __launch_bounds__(kThreads) void k_place_pick(SearchArgs a, int32_t *queue,
                                                          double *score)
 {
     __shared__ double ls[kWaves];
@@ -1873,6 +1892,7 @@ __global__ __launch_bounds__(kThreads) void k_place_pick(SearchArgs a, int group
     // the queue scores and their running sums, staged for the totals
     __shared__ double sT[kMaxSearchInstances + 1], sQ[kMaxSearchInstances];
     __shared__ int scand[kThreads];
+    __shared__ double scex[kThreads];
     const int64_t b = blockIdx.x;
     const int G = a.G, I = a.I;
     const int n = 2 * I;
@@ -1883,14 +1903,15 @@ __global__ __launch_bounds__(kThreads) void k_place_pick(SearchArgs a, int group
     double v1 = 0.0;
     if (one && threadIdx.x < n) {
         v1 = a.cex[b * a.n_moves + threadIdx.x];
+        scex[threadIdx.x] = v1;
         scand[threadIdx.x] = a.cand[b * a.n_moves + threadIdx.x];
     }
     for (int q = threadIdx.x; q < I; q += kThreads) sQ[q] = a.Q[b * I + q];
-    const int s0 = clampi(a.dq[b * 4 + 2], 0, G - 1);
-    const int g0 = clampi(a.dq[b * 4 + 3], 0, I - 1);
+    const int s0 = clampi(a.dq[b * 4], 0, G - 1);
+    const int g0 = clampi(a.dq[b * 4 + 1], 0, I - 1);
     if (threadIdx.x == 0) {
-        kg = (int)a.srec[b * G + s0].q;
-        stay = s0 == a.qof[b * (I + 1) + g0];
+        kg = g0;
+        stay = a.dq[b * 4 + 2];
     }
     __syncthreads();
     // the running sums of the queue scores, in queue order (the additions of a
@@ -1920,8 +1941,6 @@ __global__ __launch_bounds__(kThreads) void k_place_pick(SearchArgs a, int group
             a.cur[b] = sT[I];
             if (queue) queue[b] = g0;
             if (score) score[b] = sT[I];
-            a.dq[b * 4] = g0;
-            a.dq[b * 4 + 1] = g0;
         }
         return;
     }
@@ -1930,11 +1949,14 @@ __global__ __launch_bounds__(kThreads) void k_place_pick(SearchArgs a, int group
     const double rg = a.U[b];
     double best = INFINITY;
     int64_t bk = INT64_MAX;
-    for (int c = threadIdx.x; c < n; c += kThreads) {
-        double v = one ? v1 : a.cex[b * a.n_moves + c];
+    // a place's plan score: its queue's new score (the candidate's) with the
+    // group's own queue without it, the other queues as they stand
+    auto total = [&](int c, double v) __attribute__((always_inline)) {
         const int h = c < I ? c : c - I;
-        v = h != g0 ? total_with2(T, Q, I, g0, rg, h, v) : total_with(T, Q, I, g0, v);
-        a.cex[b * a.n_moves + c] = v;
+        return h != g0 ? total_with2(T, Q, I, g0, rg, h, v) : total_with(T, Q, I, g0, v);
+    };
+    for (int c = threadIdx.x; c < n; c += kThreads) {
+        const double v = total(c, one ? v1 : a.cex[b * a.n_moves + c]);
         if (better(v, c, best, bk)) {
             best = v;
             bk = c;
@@ -1945,14 +1967,20 @@ __global__ __launch_bounds__(kThreads) void k_place_pick(SearchArgs a, int group
         const bool none = bk < 0 || bk >= n;
         if (none) bk = 0;                         // every score NaN: the first place
         kk = bk;
-        const double cur = none ? a.cex[b * a.n_moves + bk] : best;
+        const double vq = one ? scex[bk] : a.cex[b * a.n_moves + bk];   // its queue's new score
+        const double cur = none ? total((int)bk, vq) : best;
         a.cur[b] = cur;
         if (queue) queue[b] = (int32_t)bk;
         if (score) score[b] = cur;
         const int h = (int)(bk < I ? bk : bk - I);
-        a.dq[b * 4] = min(g0, h);
-        a.dq[b * 4 + 1] = max(g0, h);
         kp = clampi(one ? scand[bk] : a.cand[b * a.n_moves + bk], 0, G);
+        // the queue scores of the plan after the move
+        if (h != g0) {
+            a.Q[b * I + g0] = rg;
+            a.Q[b * I + h] = vq;
+        } else {
+            a.Q[b * I + g0] = vq;
+        }
     }
     __syncthreads();
     const int c = (int)kk;
@@ -2374,11 +2402,10 @@ int screen_moves(SearchArgs &a, hipStream_t stream)
     return QLM_OK;
 }
 
-// The placement of one group in every chain: the candidate queues scored
-// exactly, the lowest applied; with `refresh`, the cache of the queues the
-// placement changed is formed again (the session's next step reads it).
-int place_step(SearchArgs &a, int32_t group, int32_t *queue, double *score, bool refresh,
-               hipStream_t stream)
+// The placement of one group in every chain: the candidate places scored
+// exactly, the lowest applied (the plan, the slot of every group and the queue
+// scores kept up to date, which is all the next placement reads).
+int place_step(SearchArgs &a, int32_t group, int32_t *queue, double *score, hipStream_t stream)
 {
     int rc;
     qlm_internal::TimedLaunch tl;
@@ -2388,14 +2415,9 @@ int place_step(SearchArgs &a, int32_t group, int32_t *queue, double *score, bool
                        group);
     if ((rc = launched("k_place_eval launch"))) return rc;
     qlm_internal::timing_end(stream, &tl);
-    hipLaunchKernelGGL(k_place_pick, dim3((unsigned)a.B), dim3(kThreads), 0, stream, a, group,
-                       queue, score);
-    if ((rc = launched("k_place_pick launch"))) return rc;
-    if (!refresh) return QLM_OK;
-    // k_place_pick sums the queue scores itself: the cache alone
-    const int nblk = (a.I + kWaves - 1) / kWaves;
-    hipLaunchKernelGGL(k_sstate, dim3((unsigned)(nblk * a.B)), dim3(kThreads), 0, stream, a, 2);
-    return launched("k_sstate launch");
+    hipLaunchKernelGGL(k_place_pick, dim3((unsigned)a.B), dim3(kThreads), 0, stream, a, queue,
+                       score);
+    return launched("k_place_pick launch");
 }
 
 // The chains' plans back to the caller's layout, with their scores.
@@ -2548,7 +2570,7 @@ int qlm_place_group(const qlm_problem *problem, const qlm_plans *start, const ql
     if (a.B == 0) return QLM_OK;
     rc = load_and_state(a, start, stream);
     if (rc) return rc;
-    if ((rc = place_step(a, group, queue, nullptr, false, stream))) return rc;
+    if ((rc = place_step(a, group, queue, nullptr, stream))) return rc;
     return write_plans(a, *out, score, stream);
 }
 
@@ -2573,7 +2595,7 @@ int qlm_place_step(const qlm_problem *problem, int64_t n_plans, int32_t group, v
     int rc = session_args(problem, n_plans, ws, ws_bytes, &a);
     if (rc) return rc;
     if (a.B == 0) return QLM_OK;
-    return place_step(a, group, queue, score, true, stream);
+    return place_step(a, group, queue, score, stream);
 }
 
 int qlm_place_end(const qlm_problem *problem, int64_t n_plans, const qlm_plans_out *out, void *ws,

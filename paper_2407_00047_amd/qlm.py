@@ -589,10 +589,13 @@ def apply_profile(problem: DeviceProblem, profile, inst_model=None, req_slo=None
 
 class PlaceSession:
     """A placement session (qlm_place_begin / step / end): the plans stay in
-    the workspace while groups are placed one after another."""
+    the workspace while groups are placed one after another, on one stream
+    (`stream`, or the current stream when the session begins)."""
 
     def __init__(self, problem: DeviceProblem, plans: DevicePlans, ws=None, stream=None):
         import torch
+        if stream is None:
+            stream = torch.cuda.current_stream()
         self.problem = problem
         self.n_plans = plans.n_plans
         self.has_evict = plans.evict_bits is not None
@@ -605,13 +608,18 @@ class PlaceSession:
         self.score = torch.full((max(self.n_plans, 1),), float("nan"), dtype=torch.float64,
                                 device=self.dev)
         self.queue = torch.full((max(self.n_plans, 1),), -2, dtype=torch.int32, device=self.dev)
+        # a step's arguments but the group, formed once (a step is a few tens of
+        # microseconds of GPU work; marshalling them per call would add as much)
+        self._fn = library().qlm_place_step
+        self._args = (ctypes.byref(problem.struct), self.n_plans)
+        self._rest = (_ptr(self.ws), self.ws.numel(), _ptr(self.score), _ptr(self.queue),
+                      _stream(stream))
+        self._out = (self.score[:self.n_plans], self.queue[:self.n_plans])
 
     def step(self, group: int):
         """Places `group` in every plan; returns (scores [P], places [P]) (device)."""
-        _check(library().qlm_place_step(ctypes.byref(self.problem.struct), self.n_plans,
-                                        int(group), _ptr(self.ws), self.ws.numel(),
-                                        _ptr(self.score), _ptr(self.queue), _stream(self.stream)))
-        return self.score[:self.n_plans], self.queue[:self.n_plans]
+        _check(self._fn(*self._args, int(group), *self._rest))
+        return self._out
 
     def end(self, out: DevicePlans | None = None):
         """The plans as they stand (DevicePlans) and their exact scores."""
