@@ -504,8 +504,11 @@ __global__ __launch_bounds__(kThreads) void k_fstart(FArgs a, int64_t pc)
 // queue (the queue < 4096 in bits 0-11, the group in bits 12-18, the lane in
 // bits 19-24, kNoVar in bit 31).
 struct WaveBuf {
-    FRec rec[kSub * kWave];
-    uint16_t sidx[kSub * kWave];    // sorted position -> entry
+    // the records as four arrays of 32-bit words (c0's low and high words, v0,
+    // q): a gather of records in sorted order then spreads its lanes over the
+    // banks by entry, where 16-byte records would give it 16 bank groups
+    uint32_t rw[4][kSub * kWave];
+    uint32_t sidx[kSub * kWave];    // sorted position -> entry | group block << 16
     uint16_t sgb[kSub * kWave];     // entry -> group block
     uint8_t val[kSub * kWave];      // entry holds a record
     int cnt[kMaxBlocks];
@@ -554,14 +557,24 @@ __device__ inline void flush(const FArgs &a, WaveBuf &wb, int64_t tile, int nblk
 #pragma unroll
     for (int j = 0; j < kSub; ++j) {
         const int e = j * kWave + lane;
-        if (wb.val[e]) wb.sidx[wb.boff[wb.sgb[e]] + rank[j]] = (uint16_t)e;
+        if (wb.val[e]) {
+            const uint32_t k = wb.sgb[e];
+            wb.sidx[wb.boff[k] + rank[j]] = (uint32_t)e | (k << 16);
+        }
     }
     wave_sync();
     for (int pos = lane; pos < run; pos += kWave) {
-        const int e = wb.sidx[pos];
-        const int k = wb.sgb[e];
+        const uint32_t se = wb.sidx[pos];
+        const int e = (int)(se & 0xFFFFu);
+        const int k = (int)(se >> 16);
         const int dst = wb.gbase[k] + (pos - wb.boff[k]);
-        if (dst < kBlkCap) a.bucket[(tile * nblk + k) * (int64_t)kBlkCap + dst] = wb.rec[e];
+        if (dst < kBlkCap) {
+            FRec r;
+            r.c0 = __hiloint2double((int)wb.rw[1][e], (int)wb.rw[0][e]);
+            r.v0 = __uint_as_float(wb.rw[2][e]);
+            r.q = wb.rw[3][e];
+            a.bucket[(tile * nblk + k) * (int64_t)kBlkCap + dst] = r;
+        }
     }
     wave_sync();
 #pragma unroll
@@ -617,7 +630,10 @@ __global__ __launch_bounds__(kRecWaves * kWave) void k_frec(FArgs a, int64_t p0,
             r.v0 = (float)(x.V * x.vscale);
             r.q = (uint32_t)x.q | ((uint32_t)(i & (kBlk - 1)) << 12) |
                   ((uint32_t)lane << 19) | (x.V == 0.0 ? kNoVar : 0u);
-            wb.rec[e] = r;
+            wb.rw[0][e] = (uint32_t)__double2loint(r.c0);
+            wb.rw[1][e] = (uint32_t)__double2hiint(r.c0);
+            wb.rw[2][e] = __float_as_uint(r.v0);
+            wb.rw[3][e] = r.q;
             wb.sgb[e] = (uint16_t)(i / kBlk);
             wb.val[e] = 1;
         }
@@ -628,13 +644,20 @@ __global__ __launch_bounds__(kRecWaves * kWave) void k_frec(FArgs a, int64_t p0,
 }
 
 // One workgroup per bucket (tile, group block): its records into LDS at their
-// (group, lane) place, then out to the groups' rows, 64 plans a row.
+// (group, lane) place, then out to the groups' rows, 64 plans a row.  The
+// records sit in LDS as four arrays of 32-bit words (the low and high words of
+// c0, v0, q), so that a scattered store's lanes land in banks by their plan's
+// lane alone: a 16-byte record per place would give the 64 lanes of a store
+// only 16 bank groups.
 constexpr int kTransThreads = 1024;
 
 __global__ __launch_bounds__(kTransThreads) void k_ftrans(FArgs a, int64_t pc)
 {
     extern __shared__ __align__(16) unsigned char dyn[];
-    FRec *tile_rec = reinterpret_cast<FRec *>(dyn);
+    uint32_t *w0 = reinterpret_cast<uint32_t *>(dyn);      // [kBlkCap] each
+    uint32_t *w1 = w0 + kBlkCap;
+    uint32_t *w2 = w1 + kBlkCap;
+    uint32_t *w3 = w2 + kBlkCap;
     const int nblk = (a.G + kBlk - 1) / kBlk;
     const int64_t tile = blockIdx.x / nblk;
     const int gb = (int)(blockIdx.x % nblk);
@@ -655,15 +678,22 @@ __global__ __launch_bounds__(kTransThreads) void k_ftrans(FArgs a, int64_t pc)
         if (r < n) {
             const int gi = (int)((x[u].q >> 12) & (kBlk - 1));
             const int ln = (int)((x[u].q >> 19) & (kWave - 1));
-            x[u].q &= 0xFFFu | kNoVar;
-            tile_rec[gi * kWave + ln] = x[u];
+            const int at = gi * kWave + ln;
+            w0[at] = (uint32_t)__double2loint(x[u].c0);
+            w1[at] = (uint32_t)__double2hiint(x[u].c0);
+            w2[at] = __float_as_uint(x[u].v0);
+            w3[at] = x[u].q & (0xFFFu | kNoVar);
         }
     }
     __syncthreads();
     for (int idx = threadIdx.x; idx < ng * kWave; idx += kTransThreads) {
         const int gi = idx / kWave, ln = idx % kWave;
         const int64_t col = tile * kWave + ln;
-        if (col < pc) a.rec[(int64_t)(i0 + gi) * a.rld + col] = tile_rec[idx];
+        FRec y;
+        y.c0 = __hiloint2double((int)w1[idx], (int)w0[idx]);
+        y.v0 = __uint_as_float(w2[idx]);
+        y.q = w3[idx];
+        if (col < pc) a.rec[(int64_t)(i0 + gi) * a.rld + col] = y;
     }
 }
 
