@@ -346,6 +346,18 @@ __device__ inline double wave_min(double v)
     return v;
 }
 
+// Bitwise or of v over the 64 lanes (every lane active), as a scalar: within
+// quads, half rows and rows by DPP, then the four rows' results read out.
+__device__ inline uint32_t wave_or(uint32_t v)
+{
+    v |= (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xF, 0xF, false);    // quad_perm 1,0,3,2
+    v |= (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4E, 0xF, 0xF, false);    // quad_perm 2,3,0,1
+    v |= (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x141, 0xF, 0xF, false);   // row_half_mirror
+    v |= (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x140, 0xF, 0xF, false);   // row_mirror
+    return (uint32_t)(__builtin_amdgcn_readlane((int)v, 0) | __builtin_amdgcn_readlane((int)v, 16) |
+                      __builtin_amdgcn_readlane((int)v, 32) | __builtin_amdgcn_readlane((int)v, 48));
+}
+
 // qlm_score_form: 1 when the scoring kernel takes its fast path for this
 // problem (the conditions above, evaluated as its staging evaluates them),
 // else 0.  One workgroup.
@@ -599,7 +611,8 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
         float vb = 0.0f;       // V rounded to single precision
         float vblk = 0.0f;     // scaled variance ahead added within the current block
         // rsqrt of the next slot's scaled variance ahead, formed one slot early
-        // (the reciprocal square root has a long latency; inf at a queue head)
+        // (the reciprocal square root has a long latency; inf at a queue head,
+        // where the variance ahead is 0)
         float rsn = INFINITY;
         double S = 0.0;        // sum of n * P, through the previous block
         float S32 = 0.0f;      // sum of n * P within the current block
@@ -622,6 +635,9 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
         };
         int g = -1, nb = 0, q0 = -1;
         int base = 0, nbr = 0;    // current block start, nb - base
+        // In a fast block: bit k set when some lane's next queue starts at slot
+        // base + k + 1 (the or over the wavefront of each lane's one head)
+        uint32_t hm = 0u;
         QP x{0, 1.0, 1.0, 0u, 0u}, f1 = x, f2 = x;
         bool fast = false;
 
@@ -691,7 +707,6 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
             V = 0.0;
             vb = 0.0f;
             vblk = 0.0f;
-            rsn = INFINITY;
         };
         // (In a fast block g, nb and the double variance sum are brought up to
         // date at the end of the block, from whether the block held the head nbr
@@ -705,7 +720,6 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
             if (DETAIL) V = 0.0;
             vb = 0.0f;
             vblk = 0.0f;
-            rsn = INFINITY;
         };
         auto enter_any = [&](int s, uint32_t &rowb) __attribute__((always_inline)) {
             if (fast) {
@@ -734,12 +748,13 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
         //   ring[16]  group ids of the next 16 slots (global loads, 16 slots ahead)
         //   rec[4]    LDS records of slots s..s+2 (gathered D = 2 slots ahead)
         //   cost      swap/eviction seconds of slot s, read during slot s-1
-        //   rsn       rsqrt of slot s's variance ahead, formed during slot s-1
+        //   rsn       rsqrt of slot s's variance ahead, formed at the end of slot s-1
         //   tc, tcp   tail-table cells of slots s-1 and s-2 (with tf, tfp, tnx, tnxp)
         // Slot s: (0) the probability of slot s-2, (1) the cost of s+1 read on the
         // current queue's row, (2) waits and variances of slot s, (3) its tail
         // position, (4) if s+1 starts a queue: switch, and read the cost of s+1
-        // again on the head row, (5) the tail cell of slot s.  A cost is used one
+        // again on the head row, (5) the rsqrt of s+1's variance ahead and the
+        // tail cell of slot s.  A cost is used one
         // slot after its read, a tail cell two.
         // At the start of a block at slot sb: ring[j] holds the group id of slot
         // sb + j (j >= D) or sb + 16 + j (j < D), rec[k] the record of slot sb + k
@@ -901,7 +916,6 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
             }
             vblk += nv;
             const float rs = rsn;                 // cells per unit margin; inf if V = 0
-            rsn = __builtin_amdgcn_rsqf(vb + vblk);
             if (PEN) {
                 PE = fma(nnum, inv_theta, PE);
                 asm volatile("" : "+v"(PE));     // not sunk to the end of the block
@@ -915,18 +929,27 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
             asm volatile("" : "+v"(tf), "+v"(vblk));
             const uint32_t cell = (__float_as_uint(tf) & kTailCellBits) >> 10;   // cell * 8
 
-            // (4) queue head at s+1?
-            if (s + 1 - base == nbr) {       // s + 1 == nb, compared block-relative
-                uint32_t rowb;
-                if constexpr (decltype(fast_block)::value)
-                    enter_fast(rowb);
-                else
-                    enter_any(s + 1, rowb);
-                // (its own shift: one v_lshl_add_u32 here and one above, not a
-                // shared shift and two adds)
-                cost1 = *lds_ptr<const double>(rowb + (in_vgpr(off1) << 3));
+            // (4) queue head at s+1?  In a fast block only where the block's head
+            // mask says so: a scalar test, the comparison of every lane made in
+            // those slots alone.
+            if (!decltype(fast_block)::value || ((hm >> (uint32_t)(s - base)) & 1u)) {
+                // (a branch of its own: the comparison is not to be merged into
+                // the scalar test and made in every slot)
+                asm volatile("");
+                if (s + 1 - base == nbr) {       // s + 1 == nb, compared block-relative
+                    uint32_t rowb;
+                    if constexpr (decltype(fast_block)::value)
+                        enter_fast(rowb);
+                    else
+                        enter_any(s + 1, rowb);
+                    // (its own shift: one v_lshl_add_u32 here and one above, not a
+                    // shared shift and two adds)
+                    cost1 = *lds_ptr<const double>(rowb + (in_vgpr(off1) << 3));
+                }
             }
-            // (5) the tail cell of slot s, read last
+            // (5) the variance ahead of slot s+1 (0 after a queue head, where its
+            // reciprocal square root is inf) and the tail cell of slot s, read last
+            rsn = __builtin_amdgcn_rsqf(vb + vblk);
             tc = *lds_ptr<const float2>(tail0 + cell);
             cost = cost1;
             colc = col1;
@@ -949,6 +972,7 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
             nbr = nb - sb;
             const bool odd = nbr >= 1 && nbr <= 32 && (!fast || x.nb <= sb + 32);
             if (__builtin_amdgcn_ballot_w64(odd) == 0) {
+                hm = wave_or(nbr >= 1 && nbr <= 32 ? 1u << (uint32_t)(nbr - 1) : 0u);
                 rp = rsrc_at(a.perm, sb);
                 const int lim = G - 1 - sb;           // last row, relative to the block
 #pragma unroll
