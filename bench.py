@@ -606,6 +606,9 @@ def main():
     ap.add_argument("--all-configs", action="store_true",
                     help="best-plan benchmark of every workload in turn, one JSON line each "
                          "(large last)")
+    ap.add_argument("--clock-check", action="store_true",
+                    help="time the scoring kernel back to back and after idle gaps (the "
+                         "sustained clock), print one JSON line and exit")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run a plain 1 GiB device copy (for HBM counter scaling) and exit")
     ap.add_argument("--search", action="store_true",
@@ -665,11 +668,61 @@ def main():
         bench_fcfs(args)
         return
 
+    if args.clock_check:
+        bench_clock(args, args.config, dev)
+        return
     if args.all_configs:
         for name in ("tiny", "mixed", "hetero", "heavy", "large"):
             bench_best(args, name, dev)
         return
     bench_best(args, args.config, dev)
+
+
+def bench_clock(args, config, dev):
+    """k_score's average launch time with qlm_best_plan called back to back (as
+    the benchmark times it) and with the device idle for a few milliseconds
+    before each call: the difference is the clock the device holds under
+    sustained load. Prints one JSON line."""
+    import torch
+
+    from paper_2407_00047_amd import qlm, workload
+
+    cfg = workload.CONFIGS[config]
+    P = cfg["P"] if args.plans is None else args.plans
+    pr = workload.make_problem(config)
+    pl = workload.make_plans(pr, 0, P)
+    dpr = qlm.DeviceProblem(pr, device=dev)
+    dpl = qlm.DevicePlans.from_host(pl, device=dev)
+    ws = qlm.workspace(dpr, P, device=dev)
+    bi = torch.empty(1, dtype=torch.int64, device=dev)
+    bs = torch.empty(1, dtype=torch.float64, device=dev)
+    for _ in range(args.warmup):
+        qlm.best_plan(dpr, dpl, ws=ws, out=(bi, bs))
+    torch.cuda.synchronize()
+
+    def k_avg(gap_s):
+        qlm.timing_enable(True)
+        qlm.timing_read()
+        for _ in range(args.steps):
+            if gap_s:
+                torch.cuda.synchronize()
+                time.sleep(gap_s)
+            qlm.best_plan(dpr, dpl, ws=ws, out=(bi, bs))
+        torch.cuda.synchronize()
+        n, ms = qlm.timing_read()
+        qlm.timing_enable(False)
+        return ms / max(n, 1)
+
+    runs = []
+    for _ in range(2):
+        runs.append({"back_to_back_ms": round(k_avg(0.0), 4), "after_idle_ms": round(k_avg(0.005), 4)})
+    bpp = algorithmic_bytes_per_plan(pr)
+    best = {k: min(r[k] for r in runs) for k in runs[0]}
+    print(json.dumps({"kernel": "k_score", "config": config, "plans": P, "launches": args.steps,
+                      "idle_gap_ms": 5.0, "runs": runs,
+                      "frac_back_to_back": round(bpp * P / (best["back_to_back_ms"] / 1e3) / 1e9 / PEAK_HBM_GBS, 4),
+                      "frac_after_idle": round(bpp * P / (best["after_idle_ms"] / 1e3) / 1e9 / PEAK_HBM_GBS, 4)}),
+          flush=True)
 
 
 def bench_best(args, config, dev):

@@ -745,7 +745,9 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
         };
 
         // Software pipeline over the slots of the plan:
-        //   ring[16]  group ids of the next 16 slots (global loads, 16 slots ahead)
+        //   ring[8]   group ids of the next 8 slots (buffer loads, 8 slots ahead: with
+        //             four wavefronts per SIMD that covers the memory latency, and
+        //             leaves the kernel within 128 registers without spills)
         //   rec[4]    LDS records of slots s..s+2 (gathered D = 2 slots ahead)
         //   cost      swap/eviction seconds of slot s, read during slot s-1
         //   rsn       rsqrt of slot s's variance ahead, formed at the end of slot s-1
@@ -757,10 +759,10 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
         // tail cell of slot s.  A cost is used one
         // slot after its read, a tail cell two.
         // At the start of a block at slot sb: ring[j] holds the group id of slot
-        // sb + j (j >= D) or sb + 16 + j (j < D), rec[k] the record of slot sb + k
+        // sb + j (j >= D) or sb + R + j (j < D), rec[k] the record of slot sb + k
         // (k < D), cost and colc those of slot sb.
         constexpr int D = 2;
-        constexpr int R = 16;
+        constexpr int R = 8;
         int32_t ring[R];
         uint4 rec[4];                 // rec[s % 4] holds slot s's record
         // (ids clamped to G in 16 bits: G < 2^16, and an id of 2^16 or more
