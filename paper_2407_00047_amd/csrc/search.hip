@@ -72,11 +72,12 @@
 //              s without s (for the MOVEs of s), and screened SWAP(s, d); the
 //              positions past the changes are walked in step by the wavefront
 //   k_fmove    one wavefront per (target queue h, 64 groups adjacent in SLO
-//              order): screened MOVE and screened RELOCATE into another
-//              queue; the positions past the insertion points are walked in
-//              step by the whole wavefront (one record read per position for
-//              all 64 moves); in the same launch, one lane per slot: screened
-//              RELOCATE within the slot's queue
+//              order), each lane both moves of its group into h: screened
+//              MOVE and screened RELOCATE into another queue; the positions
+//              past the insertion points are walked in step by the whole
+//              wavefront (one record read per position for all 128 moves); in
+//              the same launch, one lane per slot: screened RELOCATE within
+//              the slot's queue
 //   k_sbound / k_sselect / k_sexact   the bound min(F + D), the candidates,
 //              their exact scores
 //   k_spick    lowest (exact score, k) of the candidates; applied when it
@@ -1169,15 +1170,18 @@ __global__ __launch_bounds__(kThreads) void k_fswap(SearchArgs a)
     if (threadIdx.x == 0) a.smin[b * a.nws + wg] = m;
 }
 
-// Screened MOVE (REL: RELOCATE into another queue, whose insertion point is
-// the head of h and whose group is flagged): one wavefront per (target queue
-// h, 64 groups adjacent in SLO order).  Each lane scores its group's insertion
-// point and the position after it with running sums; past that, the queue is
-// the old one shifted by the group's tokens, variance and the change of costs,
-// walked by the whole wavefront in step from the earliest insertion point.
-template <bool REL>
-__device__ inline void fmove_body(const SearchArgs &a, int bid, float2 *tab, double *lmin,
-                                  int *lint, TRec *stage)
+// Screened MOVE and RELOCATE into another queue h: one workgroup per (target
+// queue h, 256 groups adjacent in SLO order), each lane one group and both of
+// its moves into h.  MOVE puts the group at its insertion point in h;
+// RELOCATE puts it, flagged, at the head of h, ahead of the running group.
+// Each lane scores each move's position and the position after it with
+// running sums; past that, the queue is the old one shifted by the group's
+// tokens, variance and the change of costs.  The whole wavefront walks those
+// positions in step from the earliest of its lanes' tails, forming both
+// moves' terms at each position (a lane's MOVE term only past its insertion
+// point).
+__device__ inline void fmove_body(const SearchArgs &a, int bid, float2 *tab, float *st_c,
+                                  double *lmin, int *lint, TRec *stage)
 {
     const int G = a.G, I = a.I;
     const int per_chain = I * a.nwg_b;
@@ -1194,11 +1198,16 @@ __device__ inline void fmove_body(const SearchArgs &a, int bid, float2 *tab, dou
     // the tail records' staging buffer (the tails are staged after a barrier)
     float *pmax = reinterpret_cast<float *>(stage);
     constexpr int kPmaxSlots = (int)(kStage * sizeof(TRec) / sizeof(float));
-    const bool pm_lds = !REL && eq - bq <= kPmaxSlots;
+    const bool pm_lds = eq - bq <= kPmaxSlots;
+    const int ncost = a.swap_cost ? a.C * a.M * a.M : 0;
+    const bool cost_lds = ncost <= kSwapCostStage;
     for (int k = threadIdx.x; k < qlm_tail::kCells; k += kThreads) tab[k] = a.tail[k];
     if (pm_lds)
         for (int u = bq + (int)threadIdx.x; u < eq; u += kThreads) pmax[u - bq] = sr[u].pmax;
+    if (cost_lds)
+        for (int k = threadIdx.x; k < ncost; k += kThreads) st_c[k] = a.swap_cost[k];
     __syncthreads();
+    const float *swc = cost_lds ? st_c : nullptr;
     const double theta = (double)a.inst_tput[h];
     const double inv_theta = 1.0 / theta;
     const double vscale = qlm_tail::kVarScale / (theta * theta);
@@ -1206,61 +1215,77 @@ __device__ inline void fmove_body(const SearchArgs &a, int bid, float2 *tab, dou
     const double eps = margin_eps(eq - bq + 1);
     const double Qh = a.Q[b * I + h];
     const int r = wg * kThreads + threadIdx.x;
-    bool valid = false, tail = false, force = false;
+    bool valid_m = false, valid_r = false, tail_m = false, tail_r = false;
+    bool force_m = false, force_r = false;
     int s = 0, g = 0, p = eq;
-    double N = 0.0, dE = 0.0;
+    double N_m = 0.0, N_r = 0.0, dE_m = 0.0, dE_r = 0.0;
     float dvz = 0.0f;
     if (r < G) {
         const int i = a.by_slo[r];
         s = clampi(a.inv[b * G + i], 0, G - 1);
-        SRec x = sr[s];
+        const SRec x = sr[s];
         g = (int)x.q;
         // a running group never moves; RELOCATE needs a group to evict
-        valid = g != h && s != qof[g] && (!REL || bq < eq);
-        if (REL) x.nmf |= kFlagBit;
-        if (valid) {
+        valid_m = g != h && s != qof[g];
+        valid_r = valid_m && bq < eq;
+        dvz = (float)(x.b * vscale);
+        if (valid_m) {
             Run w;
             if (bq == eq) {
                 w = Run{0.0, 0.0, 0.0, 0.0, model0_of(a, h)};
-                screen_visit(w, x, theta, inv_theta, cls, vscale, eps, tab, a, force);
+                screen_visit(w, x, theta, inv_theta, cls, vscale, eps, tab, a, force_m, swc);
             } else {
-                if (REL)
-                    p = bq;
-                else
-                    p = pm_lds ? insertion_point_lds(pmax + 1, bq + 1, eq, x.slo)   // pmax from bq
-                               : insertion_point(sr, bq + 1, eq, x.slo);
+                p = pm_lds ? insertion_point_lds(pmax + 1, bq + 1, eq, x.slo)   // pmax from bq
+                           : insertion_point(sr, bq + 1, eq, x.slo);
                 if (p == eq) {
                     const SSt t = ss[eq - 1];
                     const SRec y = sr[eq - 1];
                     w = Run{t.A + y.a, t.V + y.b, t.K, Qh, (int)(y.nmf & 0xFFu)};
-                    screen_visit(w, x, theta, inv_theta, cls, vscale, eps, tab, a, force);
+                    screen_visit(w, x, theta, inv_theta, cls, vscale, eps, tab, a, force_m, swc);
                 } else {
                     w = start_at(a, sr, ss, p, bq, h);
-                    screen_visit(w, x, theta, inv_theta, cls, vscale, eps, tab, a, force);
-                    screen_visit(w, sr[p], theta, inv_theta, cls, vscale, eps, tab, a, force);
+                    screen_visit(w, x, theta, inv_theta, cls, vscale, eps, tab, a, force_m, swc);
+                    screen_visit(w, sr[p], theta, inv_theta, cls, vscale, eps, tab, a, force_m, swc);
                     const double dK = w.K - ss[p].K;
-                    dE = x.a * inv_theta + dK;
-                    dvz = (float)(x.b * vscale);
-                    tail = p + 1 < eq;
-                    if (tail) {
-                        const double floor = vz_floor(eps, a.Es[b * I + h] + fabs(dE));
-                        force = force || !((double)(tr[p + 1].vz + dvz) >= floor);
+                    dE_m = x.a * inv_theta + dK;
+                    tail_m = p + 1 < eq;
+                    if (tail_m) {
+                        const double floor = vz_floor(eps, a.Es[b * I + h] + fabs(dE_m));
+                        force_m = force_m || !((double)(tr[p + 1].vz + dvz) >= floor);
                     }
                 }
             }
-            N = w.sc;
+            N_m = w.sc;
+        }
+        if (valid_r) {
+            SRec xr = x;
+            xr.nmf |= kFlagBit;
+            Run w = start_at(a, sr, ss, bq, bq, h);
+            screen_visit(w, xr, theta, inv_theta, cls, vscale, eps, tab, a, force_r, swc);
+            screen_visit(w, sr[bq], theta, inv_theta, cls, vscale, eps, tab, a, force_r, swc);
+            const double dK = w.K - ss[bq].K;
+            dE_r = xr.a * inv_theta + dK;
+            tail_r = bq + 1 < eq;
+            if (tail_r) {
+                const double floor = vz_floor(eps, a.Es[b * I + h] + fabs(dE_r));
+                force_r = force_r || !((double)(tr[bq + 1].vz + dvz) >= floor);
+            }
+            N_r = w.sc;
         }
     }
     // the shifted tails: queue h's tail records pass through LDS in chunks
     // (every wavefront of the workgroup targets h); each wavefront walks its
-    // lanes' tails in step, masked until its last lane's tail has begun
+    // lanes' tails in step from the earliest, a lane's MOVE terms masked
+    // until its insertion point is passed (a RELOCATE's tail starts at the
+    // first position after the head, where the walk starts)
     {
-        const int lo = tail ? p + 1 : eq;
+        const int lo_m = tail_m ? p + 1 : eq;
+        const int lo = min(lo_m, tail_r ? bq + 1 : eq);
         const int ulo = __builtin_amdgcn_readfirstlane((int)wave_min((double)lo));
         const int umask = __builtin_amdgcn_readfirstlane(
-            (int)wave_max(tail ? (double)lo : -1.0));            // from here no lane waits
+            (int)wave_max(tail_m ? (double)lo_m : -1.0));        // from here no MOVE lane waits
         const int wlo = __builtin_amdgcn_readfirstlane(block_min_int(ulo, lint));   // the workgroup's earliest
-        double acc = 0.0;
+        double acc_m = 0.0, acc_r = 0.0;
         for (int c0 = wlo; c0 < eq; c0 += kStage) {
             const int c1 = min(c0 + kStage, eq);
             __syncthreads();
@@ -1270,43 +1295,58 @@ __device__ inline void fmove_body(const SearchArgs &a, int bid, float2 *tab, dou
             if (threadIdx.x < 7) stage[c1 - c0 + threadIdx.x] = TRec{0.0, 1.0f, 0.0f};
             __syncthreads();
             int u = max(c0, ulo);
-            // masked part: some lanes' tails start later
+            // masked part: some lanes' MOVE tails start later
             for (; u < c1 && u <= umask; ++u) {
                 const TRec x = stage[u - c0];
-                const float q = qlm_tail::q_of(tab, (float)(x.m - dE), x.vz + dvz);
-                acc += (double)((tail && u > p) ? x.n * q : 0.0f);
+                const float q_m = qlm_tail::q_of(tab, (float)(x.m - dE_m), x.vz + dvz);
+                const float q_r = qlm_tail::q_of(tab, (float)(x.m - dE_r), x.vz + dvz);
+                acc_m += (double)((tail_m && u > p) ? x.n * q_m : 0.0f);
+                acc_r += (double)(x.n * q_r);
             }
             // every lane with a tail is in it now: blocks of eight records at
             // one address and fixed offsets
             for (; u < c1; u += 8) {
                 const TRec *xs = stage + (u - c0);
-                float s32 = 0.0f;
+                float s_m = 0.0f, s_r = 0.0f;
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
                     const TRec x = xs[j];
-                    const float q = qlm_tail::q_of(tab, (float)(x.m - dE), x.vz + dvz);
-                    s32 = fmaf(x.n, q, s32);
+                    const float q_m = qlm_tail::q_of(tab, (float)(x.m - dE_m), x.vz + dvz);
+                    const float q_r = qlm_tail::q_of(tab, (float)(x.m - dE_r), x.vz + dvz);
+                    s_m = fmaf(x.n, q_m, s_m);
+                    s_r = fmaf(x.n, q_r, s_r);
                 }
-                acc += (double)s32;
+                acc_m += (double)s_m;
+                acc_r += (double)s_r;
             }
         }
-        N += tail ? acc : 0.0;
+        N_m += tail_m ? acc_m : 0.0;
+        N_r += tail_r ? acc_r : 0.0;
     }
-    double F = INFINITY, D = 0.0;
-    if (valid) {
+    double F_m = INFINITY, D_m = 0.0, F_r = INFINITY, D_r = 0.0;
+    if (valid_m) {
         const double cur = a.cur[b];
         const double nq = a.Nq[b * I + h];
-        F = cur + (a.R[b * G + s] - a.Q[b * I + g]) + (N - Qh);
-        D = force ? INFINITY : a.RD[b * G + s] + kEpsP * nq + 1e-12 * (fabs(cur) + nq);
+        const double base = a.R[b * G + s] - a.Q[b * I + g];
+        const double rd = a.RD[b * G + s] + kEpsP * nq + 1e-12 * (fabs(cur) + nq);
+        F_m = cur + base + (N_m - Qh);
+        D_m = force_m ? INFINITY : rd;
+        if (valid_r) {
+            F_r = cur + base + (N_r - Qh);
+            D_r = force_r ? INFINITY : rd;
+        }
     }
-    if (r < G && (!REL || g != h)) {          // frel_body screens RELOCATE into the own queue
-        const int64_t k = (int64_t)G * a.W + (REL ? (int64_t)G * I : 0) + (int64_t)s * I + h;
-        a.F[b * a.n_moves + k] = F;
-        a.D[b * a.n_moves + k] = D;
+    if (r < G) {
+        const int64_t k = (int64_t)G * a.W + (int64_t)s * I + h;
+        a.F[b * a.n_moves + k] = F_m;
+        a.D[b * a.n_moves + k] = D_m;
+        if (g != h) {                         // frel_body screens RELOCATE into the own queue
+            a.F[b * a.n_moves + k + (int64_t)G * I] = F_r;
+            a.D[b * a.n_moves + k + (int64_t)G * I] = D_r;
+        }
     }
-    const double m = block_min(F + D, lmin);
-    if (threadIdx.x == 0)
-        a.smin[b * a.nws + a.nwg_f + (int64_t)((REL ? I : 0) + h) * a.nwg_b + wg] = m;
+    const double m = block_min(fmin(F_m + D_m, F_r + D_r), lmin);
+    if (threadIdx.x == 0) a.smin[b * a.nws + a.nwg_f + (int64_t)h * a.nwg_b + wg] = m;
 }
 
 // Screened RELOCATE within the group's own queue, one lane per slot s: the
@@ -1316,8 +1356,8 @@ __device__ inline void fmove_body(const SearchArgs &a, int bid, float2 *tab, dou
 // tokens and variance ahead are the old ones: the group is ahead of it either
 // way); past it only the costs change.  Each wavefront stages the tail
 // records of its queues in LDS when they fit (st: kRelStage per wavefront).
-__device__ inline void frel_body(const SearchArgs &a, int bid, float2 *tab, double *lmin,
-                                 TRec *stall)
+__device__ inline void frel_body(const SearchArgs &a, int bid, float2 *tab, float *st_c,
+                                 double *lmin, TRec *stall)
 {
     const int64_t b = bid / a.nwg_r;
     const int wg = bid % a.nwg_r;
@@ -1328,8 +1368,13 @@ __device__ inline void frel_body(const SearchArgs &a, int bid, float2 *tab, doub
     const TRec *__restrict__ tr = a.trec + b * G;
     const int32_t *__restrict__ qof = a.qof + b * (I + 1);
     TRec *st = stall + wave_id() * kRelStage;
+    const int ncost = a.swap_cost ? a.C * a.M * a.M : 0;
+    const bool cost_lds = ncost <= kSwapCostStage;
     for (int k = threadIdx.x; k < qlm_tail::kCells; k += kThreads) tab[k] = a.tail[k];
+    if (cost_lds)
+        for (int k = threadIdx.x; k < ncost; k += kThreads) st_c[k] = a.swap_cost[k];
     __syncthreads();
+    const float *swc = cost_lds ? st_c : nullptr;
     const int s = wg * kThreads + threadIdx.x;
     bool valid = false, force = false, on1 = false, on2 = false;
     int g = 0, lo1 = 0, hi1 = 0, lo2 = 0, hi2 = 0;
@@ -1349,8 +1394,8 @@ __device__ inline void frel_body(const SearchArgs &a, int bid, float2 *tab, doub
             const double eps = margin_eps(eq - bq);
             const double es = a.Es[b * I + g];
             Run r{0.0, 0.0, 0.0, 0.0, model0_of(a, g)};
-            screen_visit(r, x, theta, inv_theta, cls, vscale, eps, tab, a, force);
-            screen_visit(r, sr[bq], theta, inv_theta, cls, vscale, eps, tab, a, force);
+            screen_visit(r, x, theta, inv_theta, cls, vscale, eps, tab, a, force, swc);
+            screen_visit(r, sr[bq], theta, inv_theta, cls, vscale, eps, tab, a, force, swc);
             q = r.sc;
             const double dK1 = r.K - ss[bq].K;
             if (bq + 1 < s) {
@@ -1369,7 +1414,7 @@ __device__ inline void frel_body(const SearchArgs &a, int bid, float2 *tab, doub
                 // its sums ahead come from the cache, not from the exact walk's
                 // order: an indicator (nothing ahead with variance) is not trusted
                 force = force || !(t.V > 0.0);
-                screen_visit(r2, sr[s + 1], theta, inv_theta, cls, vscale, eps, tab, a, force);
+                screen_visit(r2, sr[s + 1], theta, inv_theta, cls, vscale, eps, tab, a, force, swc);
                 q += r2.sc;
                 const double dK2 = r2.K - t.K;
                 if (s + 2 < eq) {
@@ -1419,14 +1464,14 @@ __device__ inline void frel_body(const SearchArgs &a, int bid, float2 *tab, doub
         a.D[b * a.n_moves + k] = D;
     }
     const double m = block_min(F + D, lmin);
-    if (threadIdx.x == 0) a.smin[b * a.nws + a.nwg_f + (int64_t)2 * I * a.nwg_b + wg] = m;
+    if (threadIdx.x == 0) a.smin[b * a.nws + a.nwg_f + (int64_t)I * a.nwg_b + wg] = m;
 }
 
 // The screens of moves into another queue and of relocations, in one launch
 // (more wavefronts to hide each one's set-up; the short own-queue relocation
 // screens run beside the long ones).  Per launch: nwg_r * B workgroups screen
-// the relocations within a queue, then I * nwg_b * B the MOVEs, then as many
-// the RELOCATEs into another queue.
+// the relocations within a queue, then I * nwg_b * B the MOVEs and RELOCATEs
+// into another queue.
 __global__ __launch_bounds__(kThreads) void k_fmove(SearchArgs a)
 {
     __shared__ float2 tab[qlm_tail::kCells];
@@ -1435,15 +1480,13 @@ __global__ __launch_bounds__(kThreads) void k_fmove(SearchArgs a)
     // (the move screens stage kStage records and seven blank ones)
     static_assert(kWaves * kRelStage >= kStage + 7, "the screens' staging buffer");
     __shared__ TRec stage[kWaves * kRelStage];
+    __shared__ float st_c[kSwapCostStage];    // the swap costs, when they fit
     const int nrel = (int)((int64_t)a.nwg_r * a.B);
-    const int half = (int)((int64_t)a.I * a.nwg_b * a.B);
     const int bid = (int)blockIdx.x;
     if (bid < nrel)
-        frel_body(a, bid, tab, lmin, stage);
-    else if (bid < nrel + half)
-        fmove_body<false>(a, bid - nrel, tab, lmin, lint, stage);
+        frel_body(a, bid, tab, st_c, lmin, stage);
     else
-        fmove_body<true>(a, bid - nrel - half, tab, lmin, lint, stage);
+        fmove_body(a, bid - nrel, tab, st_c, lmin, lint, stage);
 }
 
 // The bound of the chain's lowest exact score, min(F + D); the candidate list
@@ -2181,7 +2224,7 @@ Layout layout(int G, int I, int W, int64_t B)
     L.nwg = L.nwg_a + 2 * I * L.nwg_b;
     L.nwg_f = (int)(((int64_t)G * (W + 1) + kThreads - 1) / kThreads);
     L.nwg_r = (G + kThreads - 1) / kThreads;
-    L.nws = L.nwg_f + 2 * I * L.nwg_b + L.nwg_r;
+    L.nws = L.nwg_f + I * L.nwg_b + L.nwg_r;
     L.n_moves = (int64_t)G * W + 2 * (int64_t)G * I;
     size_t o = 0;
     auto take = [&](size_t bytes) {
@@ -2393,7 +2436,7 @@ int screen_moves(SearchArgs &a, hipStream_t stream)
     hipLaunchKernelGGL(k_fswap, dim3((unsigned)(a.nwg_f * a.B)), dim3(kThreads), 0, stream, a);
     int rc = launched("k_fswap launch");
     if (rc) return rc;
-    const dim3 mgrid((unsigned)((2 * (int64_t)a.I * a.nwg_b + a.nwg_r) * a.B));
+    const dim3 mgrid((unsigned)(((int64_t)a.I * a.nwg_b + a.nwg_r) * a.B));
     qlm_internal::TimedLaunch tl;
     if ((rc = qlm_internal::timing_begin(stream, &tl))) return rc;
     hipLaunchKernelGGL(k_fmove, mgrid, dim3(kThreads), 0, stream, a);
