@@ -669,7 +669,12 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
             fast = c <= 1 && g < I1 && x.nb > nb;
             q0 = g;
             __builtin_amdgcn_sched_barrier(0);        // select before the reload
-            f1 = load_qp(g + 1);
+            // queue g + 1 is x itself when every lane entered at most one queue
+            // in the block before: only queue g + 2 is loaded then
+            if (__builtin_amdgcn_ballot_w64(c > 1) == 0)
+                f1 = x;
+            else
+                f1 = load_qp(g + 1);
             f2 = load_qp(g + 2);
         };
         // Enter queue g + 1 (or the first non-empty queue after it) at slot s,
