@@ -114,7 +114,8 @@ struct ScoreArgs {
     int64_t P, ld;
     const int32_t *perm, *qoff;
     const uint32_t *evict;
-    int32_t split;            // slot where the second half of every plan starts, or G
+    int32_t nparts;           // wavefronts per tile: 1, 2 or 4
+    int32_t bound[3];         // slots where parts 1, 2, 3 of every plan start (multiples of 32)
     double *score, *penalty;
     int64_t d_begin, d_count;
     float *d_mean, *d_sd, *d_prob;
@@ -542,18 +543,22 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
     const int cs3 = a.col_shift + 3;          // log2(bytes per cost-table row)
     double lane_min = INFINITY;
 
-    // When a.split < G every tile (64 plans) is scored by two wavefronts of the
-    // workgroup: the front one takes slots [0, split), the back one [split, G),
-    // after a warm-up that rebuilds the running sums of the queue holding slot
-    // split.  The back one leaves its partial sums in the outputs; after a
-    // barrier the front one adds its own.  Tiles are taken in rounds, the same
-    // number for every wavefront of the workgroup.
-    const bool halves = a.split < G;
-    const int per_round = halves ? wpb / 2 : wpb;
-    const int in_round = halves ? (wave >> 1) : wave;
-    const bool back = halves && (wave & 1);
-    const int s_begin = back ? a.split : 0;
-    const int s_end = halves && !back ? a.split : G;
+    // With a.nparts = 2 or 4 every tile (64 plans) is scored by that many
+    // wavefronts of the workgroup: part k takes slots [bound[k-1], bound[k])
+    // (bound[-1] = 0, bound[nparts-1] = G), each part after the first after a
+    // warm-up that rebuilds the running sums of the queue holding its first
+    // slot.  The partial sums pass through the outputs from the last part to
+    // the first, one barrier apart; the first part adds its own last.  Tiles
+    // are taken in rounds, the same number for every wavefront of the
+    // workgroup.
+    const int np = a.nparts;
+    const bool halves = np > 1;
+    const int per_round = wpb / np;
+    const int in_round = wave / np;
+    const int part = wave & (np - 1);
+    const bool back = part > 0;
+    const int s_begin = back ? a.bound[part - 1] : 0;
+    const int s_end = part < np - 1 ? a.bound[part] : G;
     if (!compact) {
       // General records: the front wavefront of each tile walks the whole plan
       // exactly (walk_general); the back one, if any, idles.
@@ -968,7 +973,7 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
         // wavefront takes the generic path for that block, slot by slot with
         // plain loads, and then refills the pipeline for the next block.
         const int G32 = G & ~31;
-        const int s_full = s_end & ~31;       // split is a multiple of 32
+        const int s_full = s_end & ~31;       // the part bounds are multiples of 32
         for (int sb0 = s_begin; sb0 < s_full; sb0 += 32) {
             // uniform by construction; said explicitly so that the row offsets and
             // buffer resources below stay scalar
@@ -1056,12 +1061,18 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
         }
       }
       if (halves) {
-          // the back half's sums go through the outputs to the front half
-          if (back && p_out >= 0) {
-              a.score[p_out] = S_out;
-              if (PEN) a.penalty[p_out] = PE_out;
+          // the later parts' sums go through the outputs to the first part
+          for (int k = np - 1; k >= 1; --k) {
+              if (part == k && p_out >= 0) {
+                  if (k < np - 1) {
+                      S_out += a.score[p_out];
+                      if (PEN) PE_out += a.penalty[p_out];
+                  }
+                  a.score[p_out] = S_out;
+                  if (PEN) a.penalty[p_out] = PE_out;
+              }
+              __syncthreads();
           }
-          __syncthreads();
           if (!back && p_out >= 0) {
               S_out += a.score[p_out];
               if (PEN) PE_out += a.penalty[p_out];
@@ -1709,11 +1720,32 @@ int occupancy(ScoreKernel k, size_t lds, int *cus, int *per_cu)
     return QLM_OK;
 }
 
+// Slots where parts 1 .. n-1 of every plan start when each plan is split
+// into n parts: multiples of 32, each part at least 64 slots.  A part after
+// the first also rebuilds about one queue's running sums (w slots), so it is
+// given that much less: the first part takes (G + (n - 1) w) / n slots.
+// Returns false when no such split exists.
+bool part_bounds(int G, int I, int n, int32_t *bound)
+{
+    const int w = G / I;
+    const int first = (G + (n - 1) * w) / n;
+    int prev = 0;
+    for (int k = 1; k < n; ++k) {
+        const int b = (first + (k - 1) * (first - w)) & ~31;
+        if (b - prev < 64) return false;
+        bound[k - 1] = b;
+        prev = b;
+    }
+    return G - prev >= 64;
+}
+
 // Grid of the scoring kernel: persistent, at most as many workgroups as fit.
-// When the tiles (64 plans each) fill at most half of the wavefronts the chip
-// holds at once, every tile is split between two wavefronts at *split (a
-// multiple of 32); otherwise *split = G.
-int score_grid(ScoreKernel k, size_t lds, int64_t P, int G, int I, int *grid, int *split)
+// When the tiles (64 plans each) fill at most a quarter (or half) of the
+// wavefronts the chip holds at once, every tile is split between four (or
+// two) wavefronts (part_bounds); four only where the queues are short against
+// a part (a part's warm-up rebuilds one queue's sums).
+int score_grid(ScoreKernel k, size_t lds, int64_t P, int G, int I, int *grid, int *nparts,
+               int32_t *bound)
 {
     int cus = 0, per_cu = 0;
     int rc = occupancy(k, lds, &cus, &per_cu);
@@ -1721,12 +1753,14 @@ int score_grid(ScoreKernel k, size_t lds, int64_t P, int G, int I, int *grid, in
     const int wpb = kScoreThreads / kWave;
     const int64_t tiles = (P + kWave - 1) / kWave;
     const int64_t resident = (int64_t)per_cu * cus * wpb;
-    const bool halves = G >= 256 && 2 * tiles <= resident;
-    // the back half also rebuilds about one queue's running sums: give it a
-    // little less
-    const int mean_queue = G / I;
-    *split = halves ? min((G + mean_queue) / 2, G - 64) & ~31 : G;
-    const int per_round = halves ? wpb / 2 : wpb;
+    int np = 1;
+    if (G >= 512 && 8 * (G / I) <= G && 4 * tiles <= resident && part_bounds(G, I, 4, bound))
+        np = 4;
+    else if (G >= 256 && 2 * tiles <= resident && part_bounds(G, I, 2, bound))
+        np = 2;
+    for (int k = np - 1; k < 3; ++k) bound[k] = G;
+    *nparts = np;
+    const int per_round = wpb / np;
     const int64_t need = (tiles + per_round - 1) / per_round;
     int64_t g = (int64_t)per_cu * cus;
     if (g > need) g = need;
@@ -1764,9 +1798,8 @@ int launch_score(const qlm_problem *pr, const qlm_plans *pl, double *score, doub
                          (det->wait_mean || det->wait_sd || det->prob);
     ScoreKernel k = pick_kernel(ev, penalty != nullptr, use_det);
     int grid = 1;
-    int split = pr->n_groups;
-    int rc = score_grid(k, geo.lds_bytes, pl->n_plans, pr->n_groups, pr->n_instances, &grid, &split);
-    a.split = split;
+    int rc = score_grid(k, geo.lds_bytes, pl->n_plans, pr->n_groups, pr->n_instances, &grid,
+                        &a.nparts, a.bound);
     if (rc) return rc;
     if (grid_out) *grid_out = grid;
 
