@@ -3,9 +3,15 @@
 Each case below plants one mistake in a copy of oracle/qlm_oracle.c (on the CPU,
 in a temporary directory), builds it with gcc, and runs every pin against it; at
 least one pin must fail.  A mutant that survives means a blind spot in the pins.
+The pins run in a child process: a mistake in an index can make the mutant
+read out of bounds, and a crash there (reported as such) must not take the
+test run down with it.
 """
+import json
 import os
+import signal
 import subprocess
+import sys
 
 import pytest
 
@@ -186,19 +192,62 @@ def _mutant_source(name, old, new):
     return src
 
 
-@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
-def test_mutant_is_caught(tmp_path, name, old, new):
+def _run_mutant(tmp, name, old, new):
+    """Builds the mutant and runs the pins on it in a child process; returns
+    (return code, failed pins or the child's error output)."""
     src = _mutant_source(name, old, new)
-    c = tmp_path / "mutant.c"
-    so = tmp_path / "libmutant.so"
-    c.write_text(src)
+    c = os.path.join(tmp, name + ".c")
+    so = os.path.join(tmp, "lib" + name + ".so")
+    with open(c, "w") as f:
+        f.write(src)
     subprocess.run(["gcc", "-O1", "-fopenmp", "-ffp-contract=off", "-std=c11", "-shared", "-fPIC",
-                    "-w", "-o", str(so), str(c), "-lm"], check=True)
-    orc = oracle.Oracle(str(so))
-    failed = []
-    for pin in pins.ALL_PINS:
-        try:
-            pin(orc)
-        except (AssertionError, ValueError, FloatingPointError):
-            failed.append(pin.__name__)
-    assert failed, "mutant %s survived every pin" % name
+                    "-w", "-o", so, c, "-lm"], check=True)
+    here = os.path.dirname(os.path.abspath(__file__))
+    env = dict(os.environ, OMP_NUM_THREADS="1",
+               PYTHONPATH=os.pathsep.join([here, os.path.dirname(here),
+                                           os.environ.get("PYTHONPATH", "")]))
+    child = subprocess.run([sys.executable, "-c", _CHILD, so], capture_output=True, text=True,
+                           cwd=here, timeout=900, env=env)
+    if child.returncode != 0:
+        return child.returncode, child.stderr[-2000:]
+    return 0, json.loads(child.stdout.strip().splitlines()[-1])
+
+
+@pytest.fixture(scope="module")
+def mutant_results(tmp_path_factory):
+    """Every mutant's result, the children run side by side."""
+    from concurrent.futures import ThreadPoolExecutor
+    tmp = str(tmp_path_factory.mktemp("mutants"))
+    workers = max(1, min(8, os.cpu_count() or 1))
+    with ThreadPoolExecutor(workers) as ex:
+        futs = {m[0]: ex.submit(_run_mutant, tmp, *m) for m in MUTANTS}
+        return {k: f.result() for k, f in futs.items()}
+
+
+@pytest.mark.parametrize("name", [m[0] for m in MUTANTS])
+def test_mutant_is_caught(mutant_results, name):
+    rc, out = mutant_results[name]
+    if rc < 0:
+        # killed by a signal inside the mutant (an access out of bounds): the
+        # mistake did not pass unnoticed
+        print("mutant %s crashed the oracle (%s)" % (name, signal.Signals(-rc).name))
+        return
+    assert rc == 0, out
+    print("mutant %s caught by %s" % (name, ", ".join(out)))
+    assert out, "mutant %s survived every pin" % name
+
+
+# Runs every pin against the oracle library named on the command line and
+# prints the names of the pins that failed, as one JSON line.
+_CHILD = """
+import json, sys
+import oracle, pins
+orc = oracle.Oracle(sys.argv[1])
+failed = []
+for pin in pins.ALL_PINS:
+    try:
+        pin(orc)
+    except (AssertionError, ValueError, FloatingPointError):
+        failed.append(pin.__name__)
+print(json.dumps(failed))
+"""
