@@ -37,7 +37,7 @@
 // again from them and forms the records.  The records belong in the rows of
 // the groups, a different row in every lane: this transposition from the
 // plans' slot order to group order is the price of the screen's shared SLOs.
-// It runs in two passes: k_frec sorts every 8 slots' records by block of 128
+// It runs in two passes: k_frec sorts every 4 slots' records by block of 128
 // groups in LDS and appends each block's run to the block's bucket of the
 // tile; k_ftrans places each bucket's records in LDS by (group, plan) and
 // writes whole rows.
@@ -107,7 +107,7 @@ constexpr int kSeg = 128;                   // slots per segment of the queue wa
 constexpr int kRecPad = 24;                 // plans of padding per record row
 constexpr int kBlk = 128;                   // groups per bucket of the transposition
 constexpr int kBlkCap = kBlk * 64;          // records per bucket (a tile's plans)
-constexpr int kSub = 8;                     // slots a walk sorts into buckets at a time
+constexpr int kSub = 4;                     // slots a walk sorts into buckets at a time
 constexpr int kRecWaves = 4;                // wavefronts of a k_frec workgroup
 constexpr int kMaxFcfsGroups = 1 << 16;
 constexpr int kMaxFcfsInstances = 4096;
