@@ -104,6 +104,9 @@ constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / kWave;
 constexpr int kGroupsPerWave = 64;          // groups of one k_fscreen wavefront
 constexpr int kSeg = 128;                   // slots per segment of the queue walks
+constexpr int kSegThreads = 1024;           // k_fseg: 16 wavefronts, one workgroup per CU
+constexpr int kSegWaves = kSegThreads / kWave;
+constexpr size_t kSegLdsLimit = 160 * 1024; // LDS of one workgroup
 constexpr int kRecPad = 24;                 // plans of padding per record row
 constexpr int kBlk = 128;                   // groups per bucket of the transposition
 constexpr int kBlkCap = kBlk * 64;          // records per bucket (a tile's plans)
@@ -340,7 +343,8 @@ __device__ inline int queue_at(const FArgs &a, int64_t p, int s)
 // empty queues skipped) the sums restart; then the slot's model-change and
 // eviction costs; visit(s, i, w) sees the sums on entry to the slot (fixed
 // costs included); then the group's tokens and variance join the sums.  Ids
-// out of range (a malformed plan) are skipped.
+// out of range (a malformed plan) are skipped.  The group records and swap
+// costs are read from grp and swc: the problem's own arrays, or copies in LDS.
 template <int B>
 struct Batch {
     int ids[B];
@@ -359,12 +363,12 @@ __device__ inline void batch_ids(const FArgs &a, int64_t p, int sb, int s1, Batc
 }
 
 template <int B>
-__device__ inline void batch_groups(const FArgs &a, const Batch<B> &b, FGrp *gr)
+__device__ inline void batch_groups(const FArgs &a, const FGrp *grp, const Batch<B> &b, FGrp *gr)
 {
 #pragma unroll
     for (int u = 0; u < B; ++u) {
         const int i = b.ids[u];
-        gr[u] = (i >= 0 && i < a.G) ? a.grp[i] : FGrp{0.0f, 0.0f, 0u, 0u};
+        gr[u] = (i >= 0 && i < a.G) ? grp[i] : FGrp{0.0f, 0.0f, 0u, 0u};
     }
 }
 
@@ -373,8 +377,9 @@ struct NoPost {
 };
 
 template <int B, bool kPipe, class Visit, class Post = NoPost>
-__device__ inline void walk(const FArgs &a, int64_t p, int s0, int s1, Walk &w, bool *fresh,
-                            const Visit &visit, const Post &post = Post{})
+__device__ inline void walk(const FArgs &a, const FGrp *grp, const float *swc, int64_t p, int s0,
+                            int s1, Walk &w, bool *fresh, const Visit &visit,
+                            const Post &post = Post{})
 {
     static_assert(B <= 32 && (B & (B - 1)) == 0, "a batch lies in one eviction word");
     if (s0 >= s1) return;
@@ -382,7 +387,7 @@ __device__ inline void walk(const FArgs &a, int64_t p, int s0, int s1, Walk &w, 
     Batch<B> cur;
     FGrp gr[B];
     batch_ids<B>(a, p, sb, s1, cur);
-    batch_groups<B>(a, cur, gr);
+    batch_groups<B>(a, grp, cur, gr);
     for (; sb < s1; sb += B) {
         Batch<B> nxt;
         const bool more = sb + B < s1;
@@ -402,7 +407,7 @@ __device__ inline void walk(const FArgs &a, int64_t p, int s0, int s1, Walk &w, 
             if (i < 0 || i >= a.G) continue;
             const int m = (int)gr[u].model;
             if (w.prev >= 0 && w.prev != m && a.swap_cost)
-                w.K += (double)a.swap_cost[((int64_t)w.cls * a.M + w.prev) * a.M + m];
+                w.K += (double)swc[((int64_t)w.cls * a.M + w.prev) * a.M + m];
             if ((cur.ev >> (s & 31)) & 1u) w.K += (double)a.evict_cost;
             visit(s, i, w);
             const double n = (double)gr[u].cnt;
@@ -416,7 +421,7 @@ __device__ inline void walk(const FArgs &a, int64_t p, int s0, int s1, Walk &w, 
                 cur = nxt;
             else
                 batch_ids<B>(a, p, sb + B, s1, cur);
-            batch_groups<B>(a, cur, gr);
+            batch_groups<B>(a, grp, cur, gr);
         }
     }
 }
@@ -425,15 +430,31 @@ struct NoVisit {
     __device__ void operator()(int, int, const Walk &) const {}
 };
 
-// Grid: ceil(chunk/64) tiles x ceil(nseg/4); wavefront = (tile, segment).
+// Grid: ceil(chunk/64) tiles x ceil(nseg/16); wavefront = (tile, segment).
 // Pass 1: each segment's trailing piece (the sums of its last queue over the
-// segment's slots).
-__global__ __launch_bounds__(kThreads) void k_fseg(FArgs a, int64_t p0, int64_t pc)
+// segment's slots).  With kLds the group records and swap costs are first
+// copied into LDS (dynamic, 16 G bytes and the costs), so that every slot's
+// gather is an LDS read, not a random L2 access.
+template <bool kLds>
+__global__ __launch_bounds__(kSegThreads) void k_fseg(FArgs a, int64_t p0, int64_t pc)
 {
+    extern __shared__ __align__(16) unsigned char fseg_lds[];
+    const FGrp *grp = a.grp;
+    const float *swc = a.swap_cost;
+    if (kLds) {
+        FGrp *sg = reinterpret_cast<FGrp *>(fseg_lds);
+        float *sc = reinterpret_cast<float *>(fseg_lds + sizeof(FGrp) * (size_t)a.G);
+        for (int i = threadIdx.x; i < a.G; i += kSegThreads) sg[i] = a.grp[i];
+        if (a.swap_cost)
+            for (int k = threadIdx.x; k < a.C * a.M * a.M; k += kSegThreads) sc[k] = a.swap_cost[k];
+        __syncthreads();
+        grp = sg;
+        swc = sc;
+    }
     const int nseg = (a.G + kSeg - 1) / kSeg;
-    const int sq = (nseg + kWaves - 1) / kWaves;
+    const int sq = (nseg + kSegWaves - 1) / kSegWaves;
     const int64_t tile = blockIdx.x / sq;
-    const int k = (int)(blockIdx.x % sq) * kWaves + wave_id();
+    const int k = (int)(blockIdx.x % sq) * kSegWaves + wave_id();
     if (k >= nseg) return;
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t col = tile * kWave + lane;
@@ -446,9 +467,9 @@ __global__ __launch_bounds__(kThreads) void k_fseg(FArgs a, int64_t p0, int64_t 
     bool fresh = s0 == 0 || a.qoff[(int64_t)q0 * a.ld + p] >= s0;
     if (!fresh) {
         const int i = a.perm[(int64_t)(s0 - 1) * a.ld + p];
-        if (i >= 0 && i < a.G) w.prev = (int)a.grp[i].model;
+        if (i >= 0 && i < a.G) w.prev = (int)grp[i].model;
     }
-    walk<8, true>(a, p, s0, s1, w, &fresh, NoVisit{});
+    walk<8, true>(a, grp, swc, p, s0, s1, w, &fresh, NoVisit{});
     if (on) {
         Piece t;
         t.A = w.A;
@@ -609,7 +630,7 @@ __global__ __launch_bounds__(kRecWaves * kWave) void k_frec(FArgs a, int64_t p0,
         if (st.V == 0.0) {
             // nothing varies ahead: form the sums again in the oracle's order
             bool f = false;
-            walk<8, true>(a, p, max(b, 0), s0, w, &f, NoVisit{});
+            walk<8, true>(a, a.grp, a.swap_cost, p, max(b, 0), s0, w, &f, NoVisit{});
         } else {
             w.A = st.A;
             w.V = st.V;
@@ -622,7 +643,7 @@ __global__ __launch_bounds__(kRecWaves * kWave) void k_frec(FArgs a, int64_t p0,
     bool f = false;
     // batches of kSub slots (s0 is a multiple of kSub); the next batch's reads
     // are in flight while a batch's records are sorted into the buckets
-    walk<kSub, true>(a, p, s0, s1, w, &f, [&](int s, int i, const Walk &x) {
+    walk<kSub, true>(a, a.grp, a.swap_cost, p, s0, s1, w, &f, [&](int s, int i, const Walk &x) {
         if (on) {
             const int e = (s & (kSub - 1)) * kWave + lane;
             FRec r;
@@ -1174,9 +1195,20 @@ int screen_all(const FArgs &a, hipStream_t stream)
     for (int64_t p0 = 0; p0 < a.P; p0 += a.chunk) {
         const int64_t pc = a.P - p0 < a.chunk ? a.P - p0 : a.chunk;
         const int64_t tiles = (pc + kWave - 1) / kWave;
-        const int64_t sq = ((a.G + kSeg - 1) / kSeg + kWaves - 1) / kWaves;
-        hipLaunchKernelGGL(k_fseg, dim3((unsigned)(tiles * sq)), dim3(kThreads), 0, stream, a, p0,
-                           pc);
+        const int64_t sq = ((a.G + kSeg - 1) / kSeg + kSegWaves - 1) / kSegWaves;
+        const size_t seg_lds = sizeof(FGrp) * (size_t)a.G +
+                               (a.swap_cost ? sizeof(float) * (size_t)a.C * a.M * a.M : 0);
+        if (seg_lds <= kSegLdsLimit) {
+            const hipError_t e = hipFuncSetAttribute((const void *)k_fseg<true>,
+                                                     hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                     (int)seg_lds);
+            if (e != hipSuccess) return hip_fail(e, "hipFuncSetAttribute");
+            hipLaunchKernelGGL(k_fseg<true>, dim3((unsigned)(tiles * sq)), dim3(kSegThreads),
+                               seg_lds, stream, a, p0, pc);
+        } else {
+            hipLaunchKernelGGL(k_fseg<false>, dim3((unsigned)(tiles * sq)), dim3(kSegThreads), 0,
+                               stream, a, p0, pc);
+        }
         if ((rc = launched("k_fseg launch"))) return rc;
         hipLaunchKernelGGL(k_fstart, dim3((unsigned)((pc + kThreads - 1) / kThreads)),
                            dim3(kThreads), 0, stream, a, pc);
