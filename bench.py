@@ -32,7 +32,7 @@ PEAK_VALU_LANES = 256 * 4 * 16 * 2.4e9
 # the benchmarked variant, eviction words on; the queue-head path and the
 # per-block work excluded); the measured count per slot, those included, comes
 # from the committed SQ counter summary when it matches the kernel source
-VALU_PER_SLOT = 22
+VALU_PER_SLOT = 21
 # VALU instructions per visited position in the main loop of the screen of
 # moves into another queue (k_fmove), counted in its compiled loop body: margin
 # (v_add_f64, v_cvt_f32_f64), variance (v_add_f32), v_rsq_f32, cell coordinate
