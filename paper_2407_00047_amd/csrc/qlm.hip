@@ -607,8 +607,10 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
                 reinterpret_cast<const unsigned char *>(base) + (int64_t)row * ld4 + tb * 4;
             return __builtin_amdgcn_make_buffer_rsrc((void *)rp, (short)0, 0x7FFFFFFF, 0x00020000);
         };
+        // (non-temporal: every plan row is read once, and streaming it past the
+        // caches leaves them to the queue offsets and tables that are reused)
         auto ld_rel = [&](__amdgpu_buffer_rsrc_t r, int rel_row) __attribute__((always_inline)) {
-            return (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(r, (int)lpb, rel_row * (int)ld4, 0);
+            return (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(r, (int)lpb, rel_row * (int)ld4, 2);
         };
 
         double Y = 0.0;        // tokens ahead + theta * (swap and eviction seconds so far)
