@@ -148,6 +148,30 @@ struct FRec {
     uint32_t q;
 };
 
+// The transposition's streaming accesses (each bucket record read once, each
+// row written once): non-temporal.  Stores past the caches took k_ftrans from
+// 443 to 406 us per chunk at large; for k_frec's bucket appends (runs of a
+// few records, merged into lines in L2) they were slower.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+__device__ inline FRec ld_rec_nt(const FRec *p)
+{
+    const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
+    FRec r;
+    r.c0 = __hiloint2double((int)v.y, (int)v.x);
+    r.v0 = __uint_as_float(v.z);
+    r.q = v.w;
+    return r;
+}
+__device__ inline void st_rec_nt(FRec *p, const FRec &r)
+{
+    u32x4 v;
+    v.x = (uint32_t)__double2loint(r.c0);
+    v.y = (uint32_t)__double2hiint(r.c0);
+    v.z = __float_as_uint(r.v0);
+    v.w = r.q;
+    __builtin_nontemporal_store(v, reinterpret_cast<u32x4 *>(p));
+}
+
 // Sums over the slots of one segment of a plan that belong to the queue open
 // at the segment's end (tokens, variance, fixed costs), whether that queue
 // starts inside the segment, and the queue open at the segment's start.
@@ -691,7 +715,7 @@ __global__ __launch_bounds__(kTransThreads) void k_ftrans(FArgs a, int64_t pc)
 #pragma unroll
     for (int u = 0; u < kU; ++u) {
         const int r = u * kTransThreads + (int)threadIdx.x;
-        if (r < n) x[u] = src[r];
+        if (r < n) x[u] = ld_rec_nt(src + r);
     }
 #pragma unroll
     for (int u = 0; u < kU; ++u) {
@@ -714,7 +738,7 @@ __global__ __launch_bounds__(kTransThreads) void k_ftrans(FArgs a, int64_t pc)
         y.c0 = __hiloint2double((int)w1[idx], (int)w0[idx]);
         y.v0 = __uint_as_float(w2[idx]);
         y.q = w3[idx];
-        if (col < pc) a.rec[(int64_t)(i0 + gi) * a.rld + col] = y;
+        if (col < pc) st_rec_nt(a.rec + (int64_t)(i0 + gi) * a.rld + col, y);
     }
 }
 
