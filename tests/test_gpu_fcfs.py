@@ -50,6 +50,9 @@ CASES = [
     dict(G=97, I=1, P=5, evict=False),
     dict(G=64, I=64, P=9),
     dict(G=300, I=12, P=66, skewed=True),
+    # more groups than the segment sums' LDS copy of the group table holds
+    # (16 B a group, 160 KiB): they read the problem's own arrays instead
+    dict(G=10500, I=40, P=70),
 ]
 
 
