@@ -501,7 +501,10 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
     __shared__ int s_compact;
     if (threadIdx.x == 0) s_compact = 1;
     __syncthreads();
-    const bool fits = stage_costs(a, L) & stage_compact(a, L);
+    // (both tables are staged whatever the first one's answer)
+    const bool costs_fit = stage_costs(a, L);
+    const bool groups_fit = stage_compact(a, L);
+    const bool fits = costs_fit && groups_fit;
     if (!fits) s_compact = 0;
     __syncthreads();
     const bool compact = __builtin_amdgcn_readfirstlane(s_compact) != 0;
