@@ -878,10 +878,11 @@ __global__ __launch_bounds__(kThreads) void k_fselect(FArgs a, int nbmin)
 // ---------------------------------------------------------------------------
 // Exact scores
 
-// The oracle's terms for one group in double: the slot sum starts at 0 and
-// adds P_0, P_1, ... in arrival order.
+// The oracle's terms for one group in double, for its requests in slice j of
+// nsl (consecutive arrivals): the slice's sum starts at 0 and adds its P_r in
+// arrival order.
 __device__ inline double slot_exact(const FArgs &a, int i, double A, double V, double K,
-                                    double theta)
+                                    double theta, int j, int nsl)
 {
     const int n = (int)a.req[i].n;
     const double mu = (double)a.grp[i].mu;
@@ -889,7 +890,8 @@ __device__ inline double slot_exact(const FArgs &a, int i, double A, double V, d
     const float *slo = a.req_slo + a.first[i];
     const double EW = A / theta + K;
     double slot = 0.0;
-    for (int r = 0; r < n; ++r) {
+    const int r0 = (int)((int64_t)n * j / nsl), r1 = (int)((int64_t)n * (j + 1) / nsl);
+    for (int r = r0; r < r1; ++r) {
         const double sl = (double)slo[r];
         const double Er = EW + (double)r * (mu / theta);
         const double SDr = sqrt(V + (double)r * var) / theta;
@@ -903,19 +905,29 @@ __device__ inline double slot_exact(const FArgs &a, int i, double A, double V, d
     return slot;
 }
 
-// One wavefront per (candidate k, queue g), over a fixed grid: the queue's
-// positions 64 at a time, one per lane; the running sums ripple from lane to
-// lane in position order, then each lane forms its group's requests' terms,
-// and the slot sums ripple into the queue score the same way.
-__global__ __launch_bounds__(kThreads) void k_fexact(FArgs a, const int64_t *plan_index,
-                                                      const int32_t *count_dev, int64_t count)
+// One workgroup per (candidate k, queue g), over a fixed grid; each of its 16
+// wavefronts takes one slice of every group's requests (consecutive
+// arrivals).  A wavefront walks the queue's positions 64 at a time, one per
+// lane; the running sums ripple from lane to lane in position order, then each
+// lane forms its slice of its group's requests' terms, and those sums ripple
+// into the slice's queue sum the same way.  The queue score is the slices'
+// sums added in slice order (the oracle's sum reassociated: equal to within
+// the rounding of a sum of that many terms).  Sixteen wavefronts per queue
+// instead of one keep the requests' erfc chains short and the chip busy when
+// only a few plans are re-scored.
+constexpr int kExactThreads = 1024;
+constexpr int kExactSlices = kExactThreads / kWave;
+
+__global__ __launch_bounds__(kExactThreads) void k_fexact(FArgs a, const int64_t *plan_index,
+                                                           const int32_t *count_dev, int64_t count)
 {
+    __shared__ double part[kExactSlices];
     const int lane = threadIdx.x & (kWave - 1);
+    const int js = wave_id();
     const int64_t n = count_dev ? (int64_t)__builtin_amdgcn_readfirstlane(count_dev[0]) : count;
     const int64_t tasks = n * a.I;
-    const int64_t nw = (int64_t)gridDim.x * kWaves;
     const double ecost = (double)a.evict_cost;
-    for (int64_t t = (int64_t)blockIdx.x * kWaves + wave_id(); t < tasks; t += nw) {
+    for (int64_t t = blockIdx.x; t < tasks; t += gridDim.x) {
         const int64_t k = t / a.I;
         const int g = (int)(t % a.I);
         int64_t p = plan_index[k];
@@ -968,7 +980,7 @@ __global__ __launch_bounds__(kThreads) void k_fexact(FArgs a, const int64_t *pla
             }
             double K = K0 + c1;
             K = K + c2;
-            const double term = i >= 0 ? slot_exact(a, i, A, V, K, theta) : 0.0;
+            const double term = i >= 0 ? slot_exact(a, i, A, V, K, theta, js, kExactSlices) : 0.0;
             const double lt = from_left0(term);
             double C = rC;
             for (int j = 0; j < steps; j += 8) {
@@ -984,7 +996,14 @@ __global__ __launch_bounds__(kThreads) void k_fexact(FArgs a, const int64_t *pla
             int carry = __builtin_amdgcn_readlane(mm, last);
             prev = carry;
         }
-        if (lane == 0) a.Q[k * a.I + g] = rC;
+        if (lane == 0) part[js] = rC;
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            double q = 0.0;
+            for (int j = 0; j < kExactSlices; ++j) q += part[j];
+            a.Q[k * a.I + g] = q;
+        }
+        __syncthreads();
     }
 }
 
@@ -1269,7 +1288,7 @@ int screen_all(const FArgs &a, hipStream_t stream)
 
 int exact_grid(int64_t tasks)
 {
-    int64_t b = (tasks + kWaves - 1) / kWaves;
+    int64_t b = tasks;                         // a workgroup per task
     if (b > kExactBlocks) b = kExactBlocks;
     return (int)(b < 1 ? 1 : b);
 }
@@ -1320,7 +1339,7 @@ int qlm_fcfs_score_exact(const qlm_problem *problem, const qlm_plans *plans, con
                     stream);
     if (rc) return rc;
     if (n == 0) return QLM_OK;
-    hipLaunchKernelGGL(k_fexact, dim3((unsigned)exact_grid(n * a.I)), dim3(kThreads), 0, stream, a,
+    hipLaunchKernelGGL(k_fexact, dim3((unsigned)exact_grid(n * a.I)), dim3(kExactThreads), 0, stream, a,
                        plan_index, (const int32_t *)nullptr, n);
     if ((rc = launched("k_fexact launch"))) return rc;
     int64_t blocks = (n + kThreads - 1) / kThreads;
@@ -1346,7 +1365,7 @@ int qlm_fcfs_best_plan(const qlm_problem *problem, const qlm_plans *plans, const
         if ((rc = screen_all(a, stream))) return rc;
         hipLaunchKernelGGL(k_fselect, dim3(kSumBlocks), dim3(kThreads), 0, stream, a, kSumBlocks);
         if ((rc = launched("k_fselect launch"))) return rc;
-        hipLaunchKernelGGL(k_fexact, dim3(kExactBlocks), dim3(kThreads), 0, stream, a,
+        hipLaunchKernelGGL(k_fexact, dim3(kExactBlocks), dim3(kExactThreads), 0, stream, a,
                            (const int64_t *)a.cand, (const int32_t *)a.ncand, (int64_t)0);
         if ((rc = launched("k_fexact launch"))) return rc;
     }
