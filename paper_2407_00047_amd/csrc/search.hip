@@ -1533,9 +1533,15 @@ __global__ __launch_bounds__(kThreads) void k_sselect(SearchArgs a)
     }
 }
 
-// Exact scores of the candidates, one wavefront per candidate.
+// Exact scores of the candidates, two wavefronts per candidate: a move into
+// another queue walks the target queue (the first wavefront) and the source
+// queue from the moved slot on (the second) side by side, and the first adds
+// the two into the plan score; a move within one queue is one walk (the second
+// idles).  Every walk is the one a single wavefront made in turn, so the
+// scores do not change.
 __global__ __launch_bounds__(kThreads) void k_sexact(SearchArgs a)
 {
+    __shared__ double src_part[kWaves];
     const int64_t b = blockIdx.x / kExactBlocks;
     if (a.done[b]) return;
     const int G = a.G, I = a.I, W = a.W;
@@ -1546,92 +1552,118 @@ __global__ __launch_bounds__(kThreads) void k_sexact(SearchArgs a)
     const double *Q = a.Q + b * I;
     const int nc = a.ncand[b];
     const int lane = threadIdx.x & (kWave - 1);
-    for (int c = (int)(blockIdx.x % kExactBlocks) * kWaves + wave_id(); c < nc;
-         c += kExactBlocks * kWaves) {
-        const int64_t k = __builtin_amdgcn_readfirstlane(a.cand[b * a.n_moves + c]);
+    constexpr int kPairs = kWaves / 2;
+    const int pair = wave_id() >> 1;
+    const bool second = (wave_id() & 1) != 0;
+    // (the loop's trip count is the same in the whole workgroup: barriers)
+    for (int c0 = (int)(blockIdx.x % kExactBlocks) * kPairs; c0 < nc;
+         c0 += kExactBlocks * kPairs) {
+        const int c = c0 + pair;
         double score = INFINITY;              // for a number that names no move
-        if (k < (int64_t)G * W) {
-            const int s = (int)(k / W), d = (int)(k % W) + 1;
-            const int g = (int)sr[s].q;
-            const int bq = qof[g], eq = qof[g + 1];
-            if (s + d >= eq || s == bq) {
-                if (lane == 0) a.cex[b * a.n_moves + c] = score;
-                continue;
-            }
-            Run r = start_at(a, sr, ss, s, bq, g);
-            wave_walk(r, eq - s,
-                      [&](int v) { return sr[v == 0 ? s + d : (v == d ? s : s + v)]; },
-                      (double)a.inst_tput[g], clampi(a.inst_class[g], 0, a.C - 1), a,
-                      NoOut{});
-            score = total_with(T, Q, I, g, r.sc);
-        } else if (k >= (int64_t)G * W + (int64_t)G * I) {
-            // RELOCATE(s, h): the group first in h, flagged, then h's groups
-            const int64_t rr = k - (int64_t)G * W - (int64_t)G * I;
-            const int s = (int)(rr / I), h = (int)(rr % I);
-            SRec x = sr[s];
-            x.nmf |= kFlagBit;
-            const int g = (int)x.q;
-            const int bq = qof[h], eq = qof[h + 1];
-            if (s == qof[g] || bq == eq) {
-                if (lane == 0) a.cex[b * a.n_moves + c] = score;
-                continue;
-            }
-            const double theta = (double)a.inst_tput[h];
-            const int cls = clampi(a.inst_class[h], 0, a.C - 1);
-            Run r{0.0, 0.0, 0.0, 0.0, model0_of(a, h)};
-            if (g == h) {
-                wave_walk(r, eq - bq, [&](int v) {
-                    return v == 0 ? x : (bq + v - 1 < s ? sr[bq + v - 1] : sr[bq + v]);
-                }, theta, cls, a, NoOut{});
-                score = total_with(T, Q, I, g, r.sc);
+        bool two = false;                     // a move into another queue
+        int g2 = 0, h2 = 0;
+        double nh2 = 0.0;                     // (first wavefront) the target queue's sum
+        double mine = 0.0;                    // (second wavefront) the source queue's sum
+        if (c < nc) {
+            const int64_t k = __builtin_amdgcn_readfirstlane(a.cand[b * a.n_moves + c]);
+            if (k < (int64_t)G * W) {
+                const int s = (int)(k / W), d = (int)(k % W) + 1;
+                const int g = (int)sr[s].q;
+                const int bq = qof[g], eq = qof[g + 1];
+                if (!(s + d >= eq || s == bq) && !second) {
+                    Run r = start_at(a, sr, ss, s, bq, g);
+                    wave_walk(r, eq - s,
+                              [&](int v) { return sr[v == 0 ? s + d : (v == d ? s : s + v)]; },
+                              (double)a.inst_tput[g], clampi(a.inst_class[g], 0, a.C - 1), a,
+                              NoOut{});
+                    score = total_with(T, Q, I, g, r.sc);
+                }
+            } else if (k >= (int64_t)G * W + (int64_t)G * I) {
+                // RELOCATE(s, h): the group first in h, flagged, then h's groups
+                const int64_t rr = k - (int64_t)G * W - (int64_t)G * I;
+                const int s = (int)(rr / I), h = (int)(rr % I);
+                SRec x = sr[s];
+                x.nmf |= kFlagBit;
+                const int g = (int)x.q;
+                const int bq = qof[h], eq = qof[h + 1];
+                if (!(s == qof[g] || bq == eq)) {
+                    const double theta = (double)a.inst_tput[h];
+                    const int cls = clampi(a.inst_class[h], 0, a.C - 1);
+                    Run r{0.0, 0.0, 0.0, 0.0, model0_of(a, h)};
+                    if (g == h) {
+                        if (!second) {
+                            wave_walk(r, eq - bq, [&](int v) {
+                                return v == 0 ? x : (bq + v - 1 < s ? sr[bq + v - 1] : sr[bq + v]);
+                            }, theta, cls, a, NoOut{});
+                            score = total_with(T, Q, I, g, r.sc);
+                        }
+                    } else {
+                        two = true;
+                        g2 = g;
+                        h2 = h;
+                        if (!second) {
+                            wave_walk(r, eq - bq + 1, [&](int v) { return v == 0 ? x : sr[bq + v - 1]; },
+                                      theta, cls, a, NoOut{});
+                            nh2 = r.sc;
+                        } else {
+                            const int bg = qof[g], eg = qof[g + 1];
+                            Run rg = start_at(a, sr, ss, s, bg, g);
+                            wave_walk(rg, eg - s - 1, [&](int v) { return sr[s + 1 + v]; },
+                                      (double)a.inst_tput[g], clampi(a.inst_class[g], 0, a.C - 1),
+                                      a, NoOut{});
+                            mine = rg.sc;
+                        }
+                    }
+                }
             } else {
-                wave_walk(r, eq - bq + 1, [&](int v) { return v == 0 ? x : sr[bq + v - 1]; },
-                          theta, cls, a, NoOut{});
-                const double nh = r.sc;
-                const int bg = qof[g], eg = qof[g + 1];
-                Run rg = start_at(a, sr, ss, s, bg, g);
-                wave_walk(rg, eg - s - 1, [&](int v) { return sr[s + 1 + v]; },
-                          (double)a.inst_tput[g], clampi(a.inst_class[g], 0, a.C - 1), a,
-                          NoOut{});
-                score = total_with2(T, Q, I, g, rg.sc, h, nh);
-            }
-        } else {
-            const int64_t rr = k - (int64_t)G * W;
-            const int s = (int)(rr / I), h = (int)(rr % I);
-            const SRec x = sr[s];
-            const int g = (int)x.q;
-            if (g == h || s == qof[g]) {
-                if (lane == 0) a.cex[b * a.n_moves + c] = score;
-                continue;
-            }
-            const int bq = qof[h], eq = qof[h + 1];
-            const double theta = (double)a.inst_tput[h];
-            const int cls = clampi(a.inst_class[h], 0, a.C - 1);
-            Run r;
-            if (bq == eq) {
-                r = Run{0.0, 0.0, 0.0, 0.0, model0_of(a, h)};
-                wave_walk(r, 1, [&](int) { return x; }, theta, cls, a, NoOut{});
-            } else {
-                const int p = edf_point(sr, bq, eq, x.slo);
-                if (p == eq) {
-                    r = start_at(a, sr, ss, eq - 1, bq, h);
-                    wave_walk(r, 2, [&](int v) { return v == 0 ? sr[eq - 1] : x; }, theta, cls,
-                              a, NoOut{});
-                } else {
-                    r = start_at(a, sr, ss, p, bq, h);
-                    wave_walk(r, eq - p + 1, [&](int v) { return v == 0 ? x : sr[p + v - 1]; },
-                              theta, cls, a, NoOut{});
+                const int64_t rr = k - (int64_t)G * W;
+                const int s = (int)(rr / I), h = (int)(rr % I);
+                const SRec x = sr[s];
+                const int g = (int)x.q;
+                if (!(g == h || s == qof[g])) {
+                    two = true;
+                    g2 = g;
+                    h2 = h;
+                    if (!second) {
+                        const int bq = qof[h], eq = qof[h + 1];
+                        const double theta = (double)a.inst_tput[h];
+                        const int cls = clampi(a.inst_class[h], 0, a.C - 1);
+                        Run r;
+                        if (bq == eq) {
+                            r = Run{0.0, 0.0, 0.0, 0.0, model0_of(a, h)};
+                            wave_walk(r, 1, [&](int) { return x; }, theta, cls, a, NoOut{});
+                        } else {
+                            const int p = edf_point(sr, bq, eq, x.slo);
+                            if (p == eq) {
+                                r = start_at(a, sr, ss, eq - 1, bq, h);
+                                wave_walk(r, 2, [&](int v) { return v == 0 ? sr[eq - 1] : x; }, theta,
+                                          cls, a, NoOut{});
+                            } else {
+                                r = start_at(a, sr, ss, p, bq, h);
+                                wave_walk(r, eq - p + 1,
+                                          [&](int v) { return v == 0 ? x : sr[p + v - 1]; }, theta,
+                                          cls, a, NoOut{});
+                            }
+                        }
+                        nh2 = r.sc;
+                    } else {
+                        const int bg = qof[g], eg = qof[g + 1];
+                        Run rg = start_at(a, sr, ss, s, bg, g);
+                        wave_walk(rg, eg - s - 1, [&](int v) { return sr[s + 1 + v]; },
+                                  (double)a.inst_tput[g], clampi(a.inst_class[g], 0, a.C - 1), a,
+                                  NoOut{});
+                        mine = rg.sc;
+                    }
                 }
             }
-            const double nh = r.sc;
-            const int bg = qof[g], eg = qof[g + 1];
-            Run rg = start_at(a, sr, ss, s, bg, g);
-            wave_walk(rg, eg - s - 1, [&](int v) { return sr[s + 1 + v]; },
-                      (double)a.inst_tput[g], clampi(a.inst_class[g], 0, a.C - 1), a,
-                      NoOut{});
-            score = total_with2(T, Q, I, g, rg.sc, h, nh);
         }
-        if (lane == 0) a.cex[b * a.n_moves + c] = score;
+        if (second && lane == 0) src_part[wave_id()] = mine;
+        __syncthreads();
+        if (!second && c < nc) {
+            if (two) score = total_with2(T, Q, I, g2, src_part[wave_id() + 1], h2, nh2);
+            if (lane == 0) a.cex[b * a.n_moves + c] = score;
+        }
+        __syncthreads();
     }
 }
 
