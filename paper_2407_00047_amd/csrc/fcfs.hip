@@ -37,7 +37,7 @@
 // again from them and forms the records.  The records belong in the rows of
 // the groups, a different row in every lane: this transposition from the
 // plans' slot order to group order is the price of the screen's shared SLOs.
-// It runs in two passes: k_frec sorts every 4 slots' records by block of 128
+// It runs in two passes: k_frec sorts every 8 slots' records by block of 128
 // groups in LDS and appends each block's run to the block's bucket of the
 // tile; k_ftrans places each bucket's records in LDS by (group, plan) and
 // writes whole rows.
@@ -63,13 +63,15 @@
 //
 // Kernels
 //   k_fprep     per group: clamped count, request offset, statistics; the
-//               request total; k_fslo: the SLOs widened to double; k_ftail:
+//               request total; per instance: Theta, the variance scale, class
+//               and first model; k_fslo: the SLOs widened to double; k_ftail:
 //               the normal-tail table
 //   k_fseg      one lane per plan, one wavefront per (64 plans, segment):
 //               each segment's trailing queue piece
 //   k_fstart    one lane per plan: the sums at each segment's first slot
 //   k_frec      as k_fseg: the records of the segment's groups, into the
-//               buckets of their group blocks (k_fbzero clears the counts)
+//               buckets of their group blocks (k_fbzero clears the counts);
+//               a tile's workgroups on one XCD
 //   k_ftrans    one workgroup per (64 plans, 128 groups): the bucket to rows
 //   k_fscreen   one lane per plan, one wavefront per (64 plans, 64 groups):
 //               partial screened scores
@@ -110,8 +112,11 @@ constexpr size_t kSegLdsLimit = 160 * 1024; // LDS of one workgroup
 constexpr int kRecPad = 24;                 // plans of padding per record row
 constexpr int kBlk = 128;                   // groups per bucket of the transposition
 constexpr int kBlkCap = kBlk * 64;          // records per bucket (a tile's plans)
-constexpr int kSub = 4;                     // slots a walk sorts into buckets at a time
+constexpr int kSub = 8;                     // slots a walk sorts into buckets at a time
 constexpr int kRecWaves = 4;                // wavefronts of a k_frec workgroup
+constexpr int kXcds = 8;                    // XCDs of the device (workgroups dealt in turn)
+constexpr size_t kFrecTabLimit = 16 * 1024; // k_frec: most bytes of tables copied into LDS
+constexpr size_t kCuLds = 160 * 1024;       // LDS of one CU
 constexpr int kMaxFcfsGroups = 1 << 16;
 constexpr int kMaxFcfsInstances = 4096;
 constexpr int kMaxBlocks = kMaxFcfsGroups / kBlk;
@@ -137,6 +142,14 @@ struct FReq {
     float mu, var;
     uint32_t n;
     uint32_t pad;
+};
+
+// Per instance, for the walks: Theta, the table scale over Theta^2, the class
+// clamped to [0, C), the model loaded at the start (-1: none).
+struct FInst {
+    double theta, vscale;
+    int32_t cls, m0;
+    int32_t pad[2];
 };
 
 // A slot's group start in one plan: E[W] of its first request, its variance
@@ -203,6 +216,7 @@ struct FArgs {
     // workspace
     FGrp *grp;                // [G]
     FReq *req;                // [G]
+    FInst *inst;              // [I]
     int32_t *first;           // [G + 1] request offsets in req_slo
     double *slo64;            // [n_req] the SLOs in double
     float2 *tail;             // [kCells]
@@ -297,6 +311,15 @@ __global__ __launch_bounds__(kThreads) void k_fprep(FArgs a)
         a.req[i] = r;
         off += want;
     }
+    for (int q = t; q < a.I; q += kThreads) {
+        FInst v;
+        v.theta = (double)a.inst_tput[q];
+        v.vscale = qlm_tail::kVarScale / (v.theta * v.theta);
+        v.cls = clampi(a.inst_class[q], 0, a.C - 1);
+        v.m0 = a.inst_model0 ? clampi(a.inst_model0[q], -1, a.M - 1) : -1;
+        v.pad[0] = v.pad[1] = 0;
+        a.inst[q] = v;
+    }
     // the last thread's range ends at G: its offset is then the total
     if (t == kThreads - 1) {
         a.first[a.G] = (int32_t)(off < a.n_req ? off : a.n_req);
@@ -327,22 +350,41 @@ __global__ __launch_bounds__(kThreads) void k_ftail(FArgs a)
 // Queues are contiguous slot ranges; at a queue's first slot the running sums
 // restart.  The sums and costs are formed with the oracle's operations in the
 // oracle's order.
+constexpr int kAhead = 3;      // queue boundaries a walk holds beyond the open queue's
+static_assert(kAhead == 3, "open_queue settles nh and three boundaries");
+
 struct Walk {
     int q, nh;                 // open queue, first slot of the next queue
+    int nx[kAhead];            // qoff[q + 2 + j] (j < kAhead), -1 where not read
     double theta, vscale;
     int cls, prev;
     double A, V, K;
 };
 
-__device__ inline void open_queue(const FArgs &a, int64_t p, int q, Walk &w)
+__device__ inline void set_queue(const FInst *inst, int q, Walk &w)
 {
+    const FInst v = inst[q];
     w.q = q;
-    w.nh = a.qoff[(int64_t)(q + 1) * a.ld + p];
-    w.theta = (double)a.inst_tput[q];
-    w.vscale = qlm_tail::kVarScale / (w.theta * w.theta);
-    w.cls = clampi(a.inst_class[q], 0, a.C - 1);
-    w.prev = a.inst_model0 ? clampi(a.inst_model0[q], -1, a.M - 1) : -1;
+    w.theta = v.theta;
+    w.vscale = v.vscale;
+    w.cls = v.cls;
+    w.prev = v.m0;
     w.A = w.V = w.K = 0.0;
+}
+
+// Open queue q: its end boundary and the next kAhead ones are read together
+// and waited for at once, so that no later read of the walk waits behind
+// them (memory reads complete in order), and the switches to the next
+// queues read nothing.  inst: the per-instance table (in LDS or global
+// memory).
+__device__ inline void open_queue(const FArgs &a, const FInst *inst, int64_t p, int q, Walk &w)
+{
+    w.nh = a.qoff[(int64_t)(q + 1) * a.ld + p];
+#pragma unroll
+    for (int j = 0; j < kAhead; ++j)
+        w.nx[j] = q + 2 + j <= a.I ? a.qoff[(int64_t)(q + 2 + j) * a.ld + p] : -1;
+    asm volatile("" ::"v"(w.nh), "v"(w.nx[0]), "v"(w.nx[1]), "v"(w.nx[2]));
+    set_queue(inst, q, w);
 }
 
 // The queue holding slot s: the largest q with qoff[q] <= s.
@@ -378,22 +420,20 @@ struct Batch {
 template <int B>
 __device__ inline void batch_ids(const FArgs &a, int64_t p, int sb, int s1, Batch<B> &b)
 {
+    // (rows past s1 clamp to its last one: the walk stops at s1, and no read
+    // waits behind a conditional one)
 #pragma unroll
-    for (int u = 0; u < B; ++u) {
-        const int s = sb + u;
-        b.ids[u] = s < s1 ? a.perm[(int64_t)s * a.ld + p] : -1;
-    }
+    for (int u = 0; u < B; ++u) b.ids[u] = a.perm[(int64_t)min(sb + u, s1 - 1) * a.ld + p];
     b.ev = a.evict_bits ? a.evict_bits[(int64_t)(sb >> 5) * a.ld + p] : 0u;
 }
 
+// (every gather is issued, at a clamped id, so that all of a batch's are in
+// flight together; the walk does not use the record of an id out of range)
 template <int B>
 __device__ inline void batch_groups(const FArgs &a, const FGrp *grp, const Batch<B> &b, FGrp *gr)
 {
 #pragma unroll
-    for (int u = 0; u < B; ++u) {
-        const int i = b.ids[u];
-        gr[u] = (i >= 0 && i < a.G) ? grp[i] : FGrp{0.0f, 0.0f, 0u, 0u};
-    }
+    for (int u = 0; u < B; ++u) gr[u] = grp[clampi(b.ids[u], 0, a.G - 1)];
 }
 
 struct NoPost {
@@ -401,8 +441,8 @@ struct NoPost {
 };
 
 template <int B, bool kPipe, class Visit, class Post = NoPost>
-__device__ inline void walk(const FArgs &a, const FGrp *grp, const float *swc, int64_t p, int s0,
-                            int s1, Walk &w, bool *fresh, const Visit &visit,
+__device__ inline void walk(const FArgs &a, const FGrp *grp, const float *swc, const FInst *inst,
+                            int64_t p, int s0, int s1, Walk &w, bool *fresh, const Visit &visit,
                             const Post &post = Post{})
 {
     static_assert(B <= 32 && (B & (B - 1)) == 0, "a batch lies in one eviction word");
@@ -422,9 +462,19 @@ __device__ inline void walk(const FArgs &a, const FGrp *grp, const float *swc, i
             if (s < s0) continue;
             if (s >= s1) break;
             if (s >= w.nh) {
-                int q = w.q;
-                while (q + 1 < a.I && a.qoff[(int64_t)(q + 1) * a.ld + p] <= s) ++q;
-                open_queue(a, p, q, w);
+                if (w.q + 1 < a.I && w.nx[0] >= 0 && (w.q + 2 >= a.I || w.nx[0] > s)) {
+                    // the next queue (qoff[q+1] <= s < qoff[q+2]), from the
+                    // boundaries held (a negative one is taken as not held)
+                    w.nh = w.nx[0];
+#pragma unroll
+                    for (int j = 0; j + 1 < kAhead; ++j) w.nx[j] = w.nx[j + 1];
+                    w.nx[kAhead - 1] = -1;
+                    set_queue(inst, w.q + 1, w);
+                } else {
+                    int q = w.q;
+                    while (q + 1 < a.I && a.qoff[(int64_t)(q + 1) * a.ld + p] <= s) ++q;
+                    open_queue(a, inst, p, q, w);
+                }
                 *fresh = true;
             }
             const int i = cur.ids[u];
@@ -439,7 +489,8 @@ __device__ inline void walk(const FArgs &a, const FGrp *grp, const float *swc, i
             w.V += n * (double)gr[u].var;
             w.prev = m;
         }
-        post(sb);                       // every lane, after each batch
+        // the next batch's gathers go out before post: waiting for them then
+        // waits for none of post's stores
         if (more) {
             if (kPipe)
                 cur = nxt;
@@ -447,7 +498,28 @@ __device__ inline void walk(const FArgs &a, const FGrp *grp, const float *swc, i
                 batch_ids<B>(a, p, sb + B, s1, cur);
             batch_groups<B>(a, grp, cur, gr);
         }
+        post(sb);                       // every lane, after each batch
     }
+}
+
+// Bytes of the swap-cost table, rounded up to 16.
+__device__ __host__ inline size_t swap_bytes(const FArgs &a)
+{
+    return a.swap_cost ? ((sizeof(float) * (size_t)a.C * a.M * a.M + 15) & ~(size_t)15) : 0;
+}
+
+// Copies of the swap costs and the instance table in LDS at t (swap_bytes(a)
+// then I FInst); every thread of the workgroup takes part.
+__device__ inline void stage_tables(const FArgs &a, unsigned char *t, int nthreads,
+                                    const float **swc, const FInst **inst)
+{
+    float *sc = reinterpret_cast<float *>(t);
+    FInst *si = reinterpret_cast<FInst *>(t + swap_bytes(a));
+    if (a.swap_cost)
+        for (int k = threadIdx.x; k < a.C * a.M * a.M; k += nthreads) sc[k] = a.swap_cost[k];
+    for (int q = threadIdx.x; q < a.I; q += nthreads) si[q] = a.inst[q];
+    *swc = a.swap_cost ? sc : nullptr;
+    *inst = si;
 }
 
 struct NoVisit {
@@ -456,24 +528,23 @@ struct NoVisit {
 
 // Grid: ceil(chunk/64) tiles x ceil(nseg/16); wavefront = (tile, segment).
 // Pass 1: each segment's trailing piece (the sums of its last queue over the
-// segment's slots).  With kLds the group records and swap costs are first
-// copied into LDS (dynamic, 16 G bytes and the costs), so that every slot's
-// gather is an LDS read, not a random L2 access.
+// segment's slots).  With kLds the group records, the swap costs and the
+// instance table are first copied into LDS (dynamic: 16 G bytes, the costs,
+// 32 I bytes), so that every slot's gather is an LDS read, not a random L2
+// access.
 template <bool kLds>
 __global__ __launch_bounds__(kSegThreads) void k_fseg(FArgs a, int64_t p0, int64_t pc)
 {
     extern __shared__ __align__(16) unsigned char fseg_lds[];
     const FGrp *grp = a.grp;
     const float *swc = a.swap_cost;
+    const FInst *inst = a.inst;
     if (kLds) {
         FGrp *sg = reinterpret_cast<FGrp *>(fseg_lds);
-        float *sc = reinterpret_cast<float *>(fseg_lds + sizeof(FGrp) * (size_t)a.G);
         for (int i = threadIdx.x; i < a.G; i += kSegThreads) sg[i] = a.grp[i];
-        if (a.swap_cost)
-            for (int k = threadIdx.x; k < a.C * a.M * a.M; k += kSegThreads) sc[k] = a.swap_cost[k];
+        stage_tables(a, fseg_lds + sizeof(FGrp) * (size_t)a.G, kSegThreads, &swc, &inst);
         __syncthreads();
         grp = sg;
-        swc = sc;
     }
     const int nseg = (a.G + kSeg - 1) / kSeg;
     const int sq = (nseg + kSegWaves - 1) / kSegWaves;
@@ -487,13 +558,13 @@ __global__ __launch_bounds__(kSegThreads) void k_fseg(FArgs a, int64_t p0, int64
     const int s0 = k * kSeg, s1 = min(a.G, s0 + kSeg);
     Walk w;
     const int q0 = queue_at(a, p, s0);
-    open_queue(a, p, q0, w);
+    open_queue(a, inst, p, q0, w);
     bool fresh = s0 == 0 || a.qoff[(int64_t)q0 * a.ld + p] >= s0;
     if (!fresh) {
         const int i = a.perm[(int64_t)(s0 - 1) * a.ld + p];
         if (i >= 0 && i < a.G) w.prev = (int)grp[i].model;
     }
-    walk<8, true>(a, grp, swc, p, s0, s1, w, &fresh, NoVisit{});
+    walk<8, true>(a, grp, swc, inst, p, s0, s1, w, &fresh, NoVisit{});
     if (on) {
         Piece t;
         t.A = w.A;
@@ -548,6 +619,7 @@ __global__ __launch_bounds__(kThreads) void k_fstart(FArgs a, int64_t pc)
 // record carries its group within the block and its lane in the word of its
 // queue (the queue < 4096 in bits 0-11, the group in bits 12-18, the lane in
 // bits 19-24, kNoVar in bit 31).
+template <int kNB>
 struct WaveBuf {
     // the records as four arrays of 32-bit words (c0's low and high words, v0,
     // q): a gather of records in sorted order then spreads its lanes over the
@@ -556,8 +628,8 @@ struct WaveBuf {
     uint32_t sidx[kSub * kWave];    // sorted position -> entry | group block << 16
     uint16_t sgb[kSub * kWave];     // entry -> group block
     uint8_t val[kSub * kWave];      // entry holds a record
-    int cnt[kMaxBlocks];
-    uint16_t boff[kMaxBlocks], gbase[kMaxBlocks];
+    int cnt[kNB];                   // per group block (nblk <= kNB)
+    uint16_t boff[kNB], gbase[kNB];
 };
 
 __device__ inline void wave_sync()
@@ -568,7 +640,8 @@ __device__ inline void wave_sync()
 }
 
 // The wavefront's buffered records into the buckets of tile `tile`.
-__device__ inline void flush(const FArgs &a, WaveBuf &wb, int64_t tile, int nblk)
+template <int kNB>
+__device__ inline void flush(const FArgs &a, WaveBuf<kNB> &wb, int64_t tile, int nblk)
 {
     const int lane = threadIdx.x & (kWave - 1);
     for (int k = lane; k < nblk; k += kWave) wb.cnt[k] = 0;
@@ -627,16 +700,32 @@ __device__ inline void flush(const FArgs &a, WaveBuf &wb, int64_t tile, int nblk
     wave_sync();
 }
 
+// kNB: group blocks the wavefront buffers hold (64 or kMaxBlocks); kTab: the
+// swap costs and the instance table copied into (dynamic) LDS.
+template <int kNB, bool kTab>
 __global__ __launch_bounds__(kRecWaves * kWave) void k_frec(FArgs a, int64_t p0, int64_t pc)
 {
-    __shared__ WaveBuf bufs[kRecWaves];
+    __shared__ WaveBuf<kNB> bufs[kRecWaves];
+    extern __shared__ __align__(16) unsigned char frec_lds[];
+    const float *swc = a.swap_cost;
+    const FInst *inst = a.inst;
+    if (kTab) {
+        stage_tables(a, frec_lds, kRecWaves * kWave, &swc, &inst);
+        __syncthreads();
+    }
     const int nseg = (a.G + kSeg - 1) / kSeg;
     const int nblk = (a.G + kBlk - 1) / kBlk;
     const int sq = (nseg + kRecWaves - 1) / kRecWaves;
-    const int64_t tile = blockIdx.x / sq;
-    const int k = (int)(blockIdx.x % sq) * kRecWaves + wave_id();
-    if (k >= nseg) return;
-    WaveBuf &wb = bufs[wave_id()];
+    // Workgroups are dealt to the XCDs in turn; all workgroups of a tile get
+    // the same XCD (xcd = blockIdx mod kXcds), so that the bucket lines their
+    // appends share fill up in that XCD's L2 before they are written back
+    // (from several L2s they went out in pieces).  The grid holds the tiles
+    // rounded up to a multiple of kXcds.
+    const int64_t local = blockIdx.x / kXcds;
+    const int64_t tile = (local / sq) * kXcds + blockIdx.x % kXcds;
+    const int k = (int)(local % sq) * kRecWaves + wave_id();
+    if (tile * kWave >= pc || k >= nseg) return;
+    WaveBuf<kNB> &wb = bufs[wave_id()];
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t col = tile * kWave + lane;
     const bool on = col < pc;
@@ -647,14 +736,14 @@ __global__ __launch_bounds__(kRecWaves * kWave) void k_frec(FArgs a, int64_t p0,
     for (int j = 0; j < kSub; ++j) wb.val[j * kWave + lane] = 0;
     Walk w;
     const int q0 = a.piece[(int64_t)k * a.chunk + c].q0;
-    open_queue(a, p, q0, w);
+    open_queue(a, inst, p, q0, w);
     const int b = a.qoff[(int64_t)q0 * a.ld + p];
     if (s0 > 0 && b < s0) {
         const Start st = a.start[(int64_t)k * a.chunk + c];
         if (st.V == 0.0) {
             // nothing varies ahead: form the sums again in the oracle's order
             bool f = false;
-            walk<8, true>(a, a.grp, a.swap_cost, p, max(b, 0), s0, w, &f, NoVisit{});
+            walk<8, true>(a, a.grp, swc, inst, p, max(b, 0), s0, w, &f, NoVisit{});
         } else {
             w.A = st.A;
             w.V = st.V;
@@ -667,7 +756,7 @@ __global__ __launch_bounds__(kRecWaves * kWave) void k_frec(FArgs a, int64_t p0,
     bool f = false;
     // batches of kSub slots (s0 is a multiple of kSub); the next batch's reads
     // are in flight while a batch's records are sorted into the buckets
-    walk<kSub, true>(a, a.grp, a.swap_cost, p, s0, s1, w, &f, [&](int s, int i, const Walk &x) {
+    walk<kSub, true>(a, a.grp, swc, inst, p, s0, s1, w, &f, [&](int s, int i, const Walk &x) {
         if (on) {
             const int e = (s & (kSub - 1)) * kWave + lane;
             FRec r;
@@ -1081,7 +1170,7 @@ int64_t chunk_of(int32_t G, int64_t P, int64_t want)
 }
 
 struct FLayout {
-    size_t grp, req, first, slo64, tail, nreq, rec, bucket, bcnt, piece, start, part, F, bmin, ncand,
+    size_t grp, req, inst, first, slo64, tail, nreq, rec, bucket, bcnt, piece, start, part, F, bmin, ncand,
         cand, Q, total;
     int64_t chunk;
 };
@@ -1100,6 +1189,7 @@ FLayout flayout(const qlm_problem *pr, int64_t P, int64_t n_req, int64_t chunk)
     };
     put(L.grp, sizeof(FGrp) * (size_t)G);
     put(L.req, sizeof(FReq) * (size_t)G);
+    put(L.inst, sizeof(FInst) * (size_t)I);
     put(L.first, 4 * ((size_t)G + 1));
     put(L.slo64, 8 * ((size_t)n_req + 1));
     put(L.tail, 8 * (size_t)qlm_tail::kCells);
@@ -1158,6 +1248,7 @@ FArgs fargs(const qlm_problem *pr, const qlm_plans *pl, const float *req_slo, in
     unsigned char *w = (unsigned char *)ws;
     a.grp = (FGrp *)(w + L.grp);
     a.req = (FReq *)(w + L.req);
+    a.inst = (FInst *)(w + L.inst);
     a.first = (int32_t *)(w + L.first);
     a.slo64 = (double *)(w + L.slo64);
     a.tail = (float2 *)(w + L.tail);
@@ -1230,6 +1321,33 @@ int fbegin(const qlm_problem *problem, const qlm_plans *plans, const float *req_
     return QLM_OK;
 }
 
+// k_frec in the form the problem allows: wavefront buffers for 64 group
+// blocks where they suffice, and the tables in LDS where they leave as many
+// workgroups on a CU as there are without them.
+template <int kNB>
+int launch_frec_nb(const FArgs &a, size_t tab_bytes, dim3 grid, hipStream_t stream, int64_t p0,
+                   int64_t pc)
+{
+    const size_t fixed = sizeof(WaveBuf<kNB>) * kRecWaves;
+    if (tab_bytes <= kFrecTabLimit &&
+        kCuLds / (fixed + tab_bytes) == kCuLds / fixed) {
+        hipLaunchKernelGGL((k_frec<kNB, true>), grid, dim3(kRecWaves * kWave), tab_bytes, stream, a,
+                           p0, pc);
+    } else {
+        hipLaunchKernelGGL((k_frec<kNB, false>), grid, dim3(kRecWaves * kWave), 0, stream, a, p0,
+                           pc);
+    }
+    return launched("k_frec launch");
+}
+
+int launch_frec(const FArgs &a, size_t tab_bytes, dim3 grid, hipStream_t stream, int64_t p0,
+                int64_t pc)
+{
+    const int nblk = (a.G + kBlk - 1) / kBlk;
+    if (nblk <= 64) return launch_frec_nb<64>(a, tab_bytes, grid, stream, p0, pc);
+    return launch_frec_nb<kMaxBlocks>(a, tab_bytes, grid, stream, p0, pc);
+}
+
 // The screen over every plan, chunk by chunk: F and the per-block minima.
 int screen_all(const FArgs &a, hipStream_t stream)
 {
@@ -1239,8 +1357,8 @@ int screen_all(const FArgs &a, hipStream_t stream)
         const int64_t pc = a.P - p0 < a.chunk ? a.P - p0 : a.chunk;
         const int64_t tiles = (pc + kWave - 1) / kWave;
         const int64_t sq = ((a.G + kSeg - 1) / kSeg + kSegWaves - 1) / kSegWaves;
-        const size_t seg_lds = sizeof(FGrp) * (size_t)a.G +
-                               (a.swap_cost ? sizeof(float) * (size_t)a.C * a.M * a.M : 0);
+        const size_t tab_bytes = swap_bytes(a) + sizeof(FInst) * (size_t)a.I;
+        const size_t seg_lds = sizeof(FGrp) * (size_t)a.G + tab_bytes;
         if (seg_lds <= kSegLdsLimit) {
             const hipError_t e = hipFuncSetAttribute((const void *)k_fseg<true>,
                                                      hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -1262,9 +1380,9 @@ int screen_all(const FArgs &a, hipStream_t stream)
         hipLaunchKernelGGL(k_fbzero, dim3((unsigned)zb), dim3(kThreads), 0, stream, a, tiles * nblk);
         if ((rc = launched("k_fbzero launch"))) return rc;
         const int64_t sq2 = ((a.G + kSeg - 1) / kSeg + kRecWaves - 1) / kRecWaves;
-        hipLaunchKernelGGL(k_frec, dim3((unsigned)(tiles * sq2)), dim3(kRecWaves * kWave), 0,
-                           stream, a, p0, pc);
-        if ((rc = launched("k_frec launch"))) return rc;
+        const int64_t tiles8 = (tiles + kXcds - 1) / kXcds * kXcds;
+        if ((rc = launch_frec(a, tab_bytes, dim3((unsigned)(tiles8 * sq2)), stream, p0, pc)))
+            return rc;
         const hipError_t ea = hipFuncSetAttribute((const void *)k_ftrans,
                                                   hipFuncAttributeMaxDynamicSharedMemorySize,
                                                   (int)(sizeof(FRec) * kBlkCap));
