@@ -668,6 +668,8 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
             q.head = r.w;
             return q;
         };
+        int c_in = 0;                 // queues entered in the block before
+        uint32_t ev_nx = 0u;          // eviction word of the next block
         auto block_start = [&]() __attribute__((always_inline)) {
             const int c = g - q0;     // queues entered since the previous start
             x.nb = c == 0 ? f1.nb : f2.nb;
@@ -678,14 +680,24 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
             if (PEN || DETAIL) x.inv = 1.0 / x.theta;
             fast = c <= 1 && g < I1 && x.nb > nb;
             q0 = g;
+            c_in = c;
+        };
+        // The reads for the next block (queue parameters, eviction word), issued
+        // at the start of either path of a block, not before the choice: where
+        // the two paths join, a read issued before the choice looks just issued
+        // on the path that consumed it long ago, and the wait for it there
+        // waited for every later read too (memory reads complete in order), the
+        // fast path's ring of group ids included.
+        auto prefetch = [&](int sb) __attribute__((always_inline)) {
             __builtin_amdgcn_sched_barrier(0);        // select before the reload
             // queue g + 1 is x itself when every lane entered at most one queue
             // in the block before: only queue g + 2 is loaded then
-            if (__builtin_amdgcn_ballot_w64(c > 1) == 0)
+            if (__builtin_amdgcn_ballot_w64(c_in > 1) == 0)
                 f1 = x;
             else
                 f1 = load_qp(g + 1);
             f2 = load_qp(g + 2);
+            if (EVICT) ev_nx = ld_rel(rsrc_at(a.evict, min((sb >> 5) + 1, (G - 1) >> 5)), 0);
         };
         // Enter queue g + 1 (or the first non-empty queue after it) at slot s,
         // loading its parameters on the spot and waiting for them.
@@ -878,7 +890,6 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
         }
         rec[D] = rec[0];
         uint32_t ev = EVICT ? ld_rel(rsrc_at(a.evict, s_begin >> 5), 0) : 0u;   // word of the block
-        uint32_t ev_nx = 0u;                              // word of the next block
         uint32_t colc = rec_model(rec[0].w);    // cost-table column (model) of the current slot
         double cost = *lds_ptr<const double>(rowb0 + (colc << 3) + (EVICT ? (ev & 1u) << ev_shift : 0u));
         // Tail cells in flight: slot s's cell is read at the end of slot s, after
@@ -984,11 +995,11 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
             // buffer resources below stay scalar
             const int sb = __builtin_amdgcn_readfirstlane(sb0);
             block_start();
-            if (EVICT) ev_nx = ld_rel(rsrc_at(a.evict, min((sb >> 5) + 1, (G - 1) >> 5)), 0);
             base = sb;
             nbr = nb - sb;
             const bool odd = nbr >= 1 && nbr <= 32 && (!fast || x.nb <= sb + 32);
             if (__builtin_amdgcn_ballot_w64(odd) == 0) {
+                prefetch(sb);
                 hm = wave_or(nbr >= 1 && nbr <= 32 ? 1u << (uint32_t)(nbr - 1) : 0u);
                 rp = rsrc_at(a.perm, sb);
                 const int lim = G - 1 - sb;           // last row, relative to the block
@@ -1012,6 +1023,7 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(4
                 nb = moved ? x.nb : nb;
                 if (!DETAIL) V = moved ? 0.0 : V;
             } else {
+                prefetch(sb);
                 uint4 r = rec[0];                     // slot sb (sb % 4 == 0)
                 for (int k = 0; k < 32; ++k) {
                     const int s = sb + k;
