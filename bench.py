@@ -412,7 +412,7 @@ def bench_search(args):
 
 FCFS_METRIC = "plans scored per second, per-request FCFS variant (exact argmin), 1 GPU"
 FCFS_PLANS = 16384
-# VALU instructions per request in k_fscreen's unrolled loop (compiled code):
+# VALU instructions per request in k_fbscreen's unrolled loop (compiled code):
 # margin (v_add_f64, v_fmac_f64, v_cvt_f32_f64), variance (v_fmamk_f32),
 # v_rsq_f32, cell coordinate (v_fma_f32, v_med3_f32), cell address
 # (v_lshrrev_b32, v_and_b32), the line (v_fmac_f32), the sum (v_add_f32)
@@ -491,7 +491,7 @@ def bench_fcfs(args):
         "best": [int(bi.item()), float(bs.item())],
         "roofline": {"bound": "alu", "achieved": round(achieved, 1), "peak": round(peak, 1),
                      "unit": "Grequests/s", "frac": round(achieved / peak, 4), "traffic": None,
-                     "kernel": "k_fscreen", "kernel_avg_ms": round(k_avg, 4),
+                     "kernel": "k_fbscreen", "kernel_avg_ms": round(k_avg, 4),
                      "requests_per_launch": int(per_launch),
                      "valu_per_request": VALU_PER_REQUEST},
         "cpu_baseline": cpu,

@@ -22,9 +22,9 @@
 // Screen.  The running sums are per position (one walk of each plan), the
 // tails are per request.  The walk produces, for every group and plan, the
 // group's start E[W] = A/Theta + K (double), its variance ahead (single,
-// scaled for the tail table) and its queue, stored group-major; the screen
-// then takes one lane per plan and one wavefront per (64 plans, 64 groups):
-// all 64 lanes work on the same group at a time, so the request SLOs are the
+// scaled for the tail table) and its queue, gathered group by group; the
+// screen then takes one lane per plan and one wavefront per (64 plans, one
+// group): all 64 lanes work on the same group at a time, so the request SLOs are the
 // same across the wavefront and come through the scalar cache, the request's
 // position in its group is a constant of the unrolled loop, and each request
 // costs a margin in double, a variance in single and one read of the
@@ -39,8 +39,8 @@
 // plans' slot order to group order is the price of the screen's shared SLOs.
 // It runs in two passes: k_frec sorts every 8 slots' records by block of 128
 // groups in LDS and appends each block's run to the block's bucket of the
-// tile; k_ftrans places each bucket's records in LDS by (group, plan) and
-// writes whole rows.
+// tile; k_fbscreen places each bucket's records in LDS by (group, plan) and
+// screens them there.
 //
 // Screening bound, per request: table error below 2.2e-6; single-precision
 // rounding of the cell coordinate, of the line's evaluation, of the margin and
@@ -72,9 +72,9 @@
 //   k_frec      as k_fseg: the records of the segment's groups, into the
 //               buckets of their group blocks (k_fbzero clears the counts);
 //               a tile's workgroups on one XCD
-//   k_ftrans    one workgroup per (64 plans, 128 groups): the bucket to rows
-//   k_fscreen   one lane per plan, one wavefront per (64 plans, 64 groups):
-//               partial screened scores
+//   k_fbscreen  one workgroup per (64 plans, 128 groups): the bucket into LDS
+//               by (group, plan), then the partial screened scores, one
+//               wavefront per group at a time (lane = plan)
 //   k_fsum      partial scores -> screened plan scores, and the per-block
 //               minimum
 //   k_fselect   the plans within the bound of the lowest -> candidates
@@ -104,12 +104,10 @@ using qlm_ripple::wave_id;
 constexpr int kWave = 64;
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / kWave;
-constexpr int kGroupsPerWave = 64;          // groups of one k_fscreen wavefront
 constexpr int kSeg = 128;                   // slots per segment of the queue walks
 constexpr int kSegThreads = 1024;           // k_fseg: 16 wavefronts, one workgroup per CU
 constexpr int kSegWaves = kSegThreads / kWave;
 constexpr size_t kSegLdsLimit = 160 * 1024; // LDS of one workgroup
-constexpr int kRecPad = 24;                 // plans of padding per record row
 constexpr int kBlk = 128;                   // groups per bucket of the transposition
 constexpr int kBlkCap = kBlk * 64;          // records per bucket (a tile's plans)
 constexpr int kSub = 8;                     // slots a walk sorts into buckets at a time
@@ -161,10 +159,9 @@ struct FRec {
     uint32_t q;
 };
 
-// The transposition's streaming accesses (each bucket record read once, each
-// row written once): non-temporal.  Stores past the caches took k_ftrans from
-// 443 to 406 us per chunk at large; for k_frec's bucket appends (runs of a
-// few records, merged into lines in L2) they were slower.
+// The transposition's streaming reads (each bucket record read once):
+// non-temporal.  (For k_frec's bucket appends, runs of a few records merged
+// into lines in L2, non-temporal stores were slower.)
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 __device__ inline FRec ld_rec_nt(const FRec *p)
 {
@@ -174,15 +171,6 @@ __device__ inline FRec ld_rec_nt(const FRec *p)
     r.v0 = __uint_as_float(v.z);
     r.q = v.w;
     return r;
-}
-__device__ inline void st_rec_nt(FRec *p, const FRec &r)
-{
-    u32x4 v;
-    v.x = (uint32_t)__double2loint(r.c0);
-    v.y = (uint32_t)__double2hiint(r.c0);
-    v.z = __float_as_uint(r.v0);
-    v.w = r.q;
-    __builtin_nontemporal_store(v, reinterpret_cast<u32x4 *>(p));
 }
 
 // Sums over the slots of one segment of a plan that belong to the queue open
@@ -221,21 +209,17 @@ struct FArgs {
     double *slo64;            // [n_req] the SLOs in double
     float2 *tail;             // [kCells]
     double *nreq;             // [1] requests scored
-    FRec *rec;                // [G][rld] group-major
     FRec *bucket;             // [tiles][nblk][kBlkCap] the transposition's buckets
     int32_t *bcnt;            // [tiles][nblk] records in each bucket
     Piece *piece;             // [nseg][chunk]
     Start *start;             // [nseg][chunk]
-    double *part;             // [ceil(G / kGroupsPerWave)][chunk]
+    double *part;             // [ceil(G / kBlk)][chunk] partial screened scores
     double *F;                // [P] screened scores
     double *bmin;             // [kSumBlocks]
     int32_t *ncand;           // [1]
     int64_t *cand;            // [P]
     double *Q;                // [P][I] exact queue scores
     int64_t chunk;
-    int64_t rld;              // row stride of rec: chunk plus a pad, so that the
-                              // rows a scattered store touches fall on different
-                              // memory channels
 };
 
 __device__ inline int clampi(int v, int lo, int hi) { return v < lo ? lo : (v > hi ? hi : v); }
@@ -615,7 +599,7 @@ __global__ __launch_bounds__(kThreads) void k_fstart(FArgs a, int64_t pc)
 // not stored directly (every store would be a partial line).  Every kSub
 // slots the wavefront sorts its records by group block (kBlk groups) in LDS
 // and appends each block's run to that block's bucket of the tile, in
-// consecutive addresses; k_ftrans then turns each bucket into its rows.  A
+// consecutive addresses; k_fbscreen then places each bucket by group.  A
 // record carries its group within the block and its lane in the word of its
 // queue (the queue < 4096 in bits 0-11, the group in bits 12-18, the lane in
 // bits 19-24, kNoVar in bit 31).
@@ -777,24 +761,100 @@ __global__ __launch_bounds__(kRecWaves * kWave) void k_frec(FArgs a, int64_t p0,
     });
 }
 
-// One workgroup per bucket (tile, group block): its records into LDS at their
-// (group, lane) place, then out to the groups' rows, 64 plans a row.  The
-// records sit in LDS as four arrays of 32-bit words (the low and high words of
-// c0, v0, q), so that a scattered store's lanes land in banks by their plan's
-// lane alone: a 16-byte record per place would give the 64 lanes of a store
-// only 16 bank groups.
+__global__ __launch_bounds__(kThreads) void k_fbzero(FArgs a, int64_t n)
+{
+    for (int64_t k = (int64_t)blockIdx.x * kThreads + threadIdx.x; k < n;
+         k += (int64_t)gridDim.x * kThreads)
+        a.bcnt[k] = 0;
+}
+
+// Q of the margin m (seconds) at scaled variance vz, from the table in LDS.
+__device__ inline float tail_q(const float2 *tab, float m, float vz)
+{
+    return qlm_tail::q_of(tab, m, vz);
+}
+
+// The screened sum of P over the requests of group i in one plan (lane = plan;
+// every lane of a wavefront at the same request of the same group, whose SLO
+// is read through the scalar cache), from the group's start record rc.
+__device__ inline double group_screen(const FArgs &a, const float2 *tab, int i, const FRec &rc)
+{
+    const auto req = as_const(a.req);
+    const auto first = as_const(a.first);
+    const int n = (int)req[i].n;
+    if (n == 0) return 0.0;
+    const float mu = req[i].mu, var = req[i].var;
+    const auto slo = as_const(a.slo64 + first[i]);
+    const int g = min((int)(rc.q & ~kNoVar), a.I - 1);
+    const bool novar = (rc.q & kNoVar) != 0u;
+    const double theta = (double)a.inst_tput[g];
+    const double c1 = (double)mu / theta;
+    const float v1 = (float)((double)var * (qlm_tail::kVarScale / (theta * theta)));
+    const double c0 = rc.c0;
+    const float v0 = rc.v0;
+    const double s0 = slo[0];
+    double Sg = novar ? (c0 > s0 ? 1.0 : 0.0) : (double)tail_q(tab, (float)(s0 - c0), v0);
+    if (var == 0.0f) {
+        for (int r = 1; r < n; ++r) {
+            const double Er = c0 + (double)r * c1;
+            const double sr = slo[r];
+            Sg += novar ? (Er > sr ? 1.0 : 0.0) : (double)tail_q(tab, (float)(sr - Er), v0);
+        }
+    } else {
+        int r = 1;
+        for (; r + 32 <= n; r += 32) {
+            const double eb = c0 + (double)r * c1;
+            const float vb = fmaf((float)r, v1, v0);
+            float S = 0.0f;
+#pragma unroll
+            for (int k = 0; k < 32; ++k) {
+                const float m = (float)fma(-(double)k, c1, slo[r + k] - eb);
+                const float v = fmaf((float)k, v1, vb);
+                S += tail_q(tab, m, v);
+            }
+            Sg += (double)S;
+        }
+        float S = 0.0f;
+        for (; r < n; ++r) {
+            const double e = c0 + (double)r * c1;
+            const float m = (float)(slo[r] - e);
+            const float v = fmaf((float)r, v1, v0);
+            S += tail_q(tab, m, v);
+        }
+        Sg += (double)S;
+    }
+    return Sg;
+}
+
+// The second pass of the transposition and the screen in one: one workgroup
+// per bucket (tile, block of kBlk groups), group block major (the workgroups
+// running at one time share their groups' SLOs in the caches).  The bucket's
+// records go into LDS at their (group, plan) place; the 16 wavefronts then
+// take the block's groups one at a time from a counter in LDS and screen each
+// from LDS, leaving the group's sum for every plan in the place of its record;
+// one wavefront adds them in group order, the block's partial score of each
+// plan.  The records sit in LDS as four arrays of 32-bit words (the low and
+// high words of c0, v0, q), so that a scattered store's lanes land in banks by
+// their plan's lane alone: a 16-byte record per place would give the 64 lanes
+// of a store only 16 bank groups.  (Writing the records out as group rows for
+// a separate screen moved 2 GiB more per chunk at large.)
 constexpr int kTransThreads = 1024;
 
-__global__ __launch_bounds__(kTransThreads) void k_ftrans(FArgs a, int64_t pc)
+__global__ __launch_bounds__(kTransThreads) void k_fbscreen(FArgs a, int64_t pc)
 {
     extern __shared__ __align__(16) unsigned char dyn[];
     uint32_t *w0 = reinterpret_cast<uint32_t *>(dyn);      // [kBlkCap] each
     uint32_t *w1 = w0 + kBlkCap;
     uint32_t *w2 = w1 + kBlkCap;
     uint32_t *w3 = w2 + kBlkCap;
+    __shared__ float2 tab[qlm_tail::kCells];
+    __shared__ int next;
+    for (int k = threadIdx.x; k < qlm_tail::kCells; k += kTransThreads) tab[k] = a.tail[k];
+    if (threadIdx.x == 0) next = 0;
     const int nblk = (a.G + kBlk - 1) / kBlk;
-    const int64_t tile = blockIdx.x / nblk;
-    const int gb = (int)(blockIdx.x % nblk);
+    const int64_t tiles = (pc + kWave - 1) / kWave;
+    const int gb = (int)(blockIdx.x / tiles);
+    const int64_t tile = blockIdx.x % tiles;
     const int i0 = gb * kBlk;
     const int ng = min(kBlk, a.G - i0);
     const int n = min(a.bcnt[tile * nblk + gb], kBlkCap);
@@ -820,99 +880,34 @@ __global__ __launch_bounds__(kTransThreads) void k_ftrans(FArgs a, int64_t pc)
         }
     }
     __syncthreads();
-    for (int idx = threadIdx.x; idx < ng * kWave; idx += kTransThreads) {
-        const int gi = idx / kWave, ln = idx % kWave;
-        const int64_t col = tile * kWave + ln;
-        FRec y;
-        y.c0 = __hiloint2double((int)w1[idx], (int)w0[idx]);
-        y.v0 = __uint_as_float(w2[idx]);
-        y.q = w3[idx];
-        if (col < pc) st_rec_nt(a.rec + (int64_t)(i0 + gi) * a.rld + col, y);
-    }
-}
-
-__global__ __launch_bounds__(kThreads) void k_fbzero(FArgs a, int64_t n)
-{
-    for (int64_t k = (int64_t)blockIdx.x * kThreads + threadIdx.x; k < n;
-         k += (int64_t)gridDim.x * kThreads)
-        a.bcnt[k] = 0;
-}
-
-// Q of the margin m (seconds) at scaled variance vz, from the table in LDS.
-__device__ inline float tail_q(const float2 *tab, float m, float vz)
-{
-    return qlm_tail::q_of(tab, m, vz);
-}
-
-// Grid: ceil(G / 64) group blocks x ceil(tiles / 4), group block major (the
-// wavefronts running at one time share their groups' SLOs in the caches).
-// Lane = plan; every lane of a wavefront is at the same request of the same
-// group, whose SLO is read through the scalar cache.
-__global__ __launch_bounds__(kThreads) void k_fscreen(FArgs a, int64_t p0, int64_t pc)
-{
-    __shared__ float2 tab[qlm_tail::kCells];
-    for (int k = threadIdx.x; k < qlm_tail::kCells; k += kThreads) tab[k] = a.tail[k];
-    __syncthreads();
-    const int64_t tiles = (pc + kWave - 1) / kWave;
-    const int64_t quads = (tiles + kWaves - 1) / kWaves;
-    const int gb = (int)(blockIdx.x / quads);
-    const int64_t tile = (blockIdx.x % quads) * kWaves + wave_id();
-    if (tile >= tiles) return;
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t col0 = tile * kWave + lane;
     const bool on = col0 < pc;
-    const int64_t col = on ? col0 : pc - 1;
-    const int i0 = gb * kGroupsPerWave, i1 = min(a.G, i0 + kGroupsPerWave);
-    const auto req = as_const(a.req);
-    const auto first = as_const(a.first);
-    double tot = 0.0;
-    for (int i = i0; i < i1; ++i) {
-        const int n = (int)req[i].n;
-        if (n == 0) continue;
-        const float mu = req[i].mu, var = req[i].var;
-        const auto slo = as_const(a.slo64 + first[i]);
-        const FRec rc = a.rec[(int64_t)i * a.rld + col];
-        const int g = min((int)(rc.q & ~kNoVar), a.I - 1);
-        const bool novar = (rc.q & kNoVar) != 0u;
-        const double theta = (double)a.inst_tput[g];
-        const double c1 = (double)mu / theta;
-        const float v1 = (float)((double)var * (qlm_tail::kVarScale / (theta * theta)));
-        const double c0 = rc.c0;
-        const float v0 = rc.v0;
-        const double s0 = slo[0];
-        double Sg = novar ? (c0 > s0 ? 1.0 : 0.0) : (double)tail_q(tab, (float)(s0 - c0), v0);
-        if (var == 0.0f) {
-            for (int r = 1; r < n; ++r) {
-                const double Er = c0 + (double)r * c1;
-                const double sr = slo[r];
-                Sg += novar ? (Er > sr ? 1.0 : 0.0) : (double)tail_q(tab, (float)(sr - Er), v0);
-            }
-        } else {
-            int r = 1;
-            for (; r + 32 <= n; r += 32) {
-                const double eb = c0 + (double)r * c1;
-                const float vb = fmaf((float)r, v1, v0);
-                float S = 0.0f;
-#pragma unroll
-                for (int k = 0; k < 32; ++k) {
-                    const float m = (float)fma(-(double)k, c1, slo[r + k] - eb);
-                    const float v = fmaf((float)k, v1, vb);
-                    S += tail_q(tab, m, v);
-                }
-                Sg += (double)S;
-            }
-            float S = 0.0f;
-            for (; r < n; ++r) {
-                const double e = c0 + (double)r * c1;
-                const float m = (float)(slo[r] - e);
-                const float v = fmaf((float)r, v1, v0);
-                S += tail_q(tab, m, v);
-            }
-            Sg += (double)S;
-        }
-        tot += Sg;
+    // a lane past the chunk takes the record of the tile's last plan
+    const int ln = on ? lane : (int)(pc - 1 - tile * kWave);
+    for (;;) {
+        int gi = 0;
+        if (lane == 0) gi = atomicAdd(&next, 1);
+        gi = __builtin_amdgcn_readfirstlane(__shfl(gi, 0, kWave));
+        if (gi >= ng) break;
+        const int at = gi * kWave + ln;
+        FRec rc;
+        rc.c0 = __hiloint2double((int)w1[at], (int)w0[at]);
+        rc.v0 = __uint_as_float(w2[at]);
+        rc.q = w3[at];
+        const double Sg = group_screen(a, tab, i0 + gi, rc);
+        // (every lane has read its record: the wavefront moves in step)
+        const int me = gi * kWave + lane;
+        w0[me] = (uint32_t)__double2loint(Sg);
+        w1[me] = (uint32_t)__double2hiint(Sg);
     }
-    if (on) a.part[(int64_t)gb * a.chunk + col0] = tot;
+    __syncthreads();
+    if (threadIdx.x < kWave) {
+        double tot = 0.0;
+        for (int gi = 0; gi < ng; ++gi)
+            tot += __hiloint2double((int)w1[gi * kWave + lane], (int)w0[gi * kWave + lane]);
+        if (on) a.part[(int64_t)gb * a.chunk + col0] = tot;
+    }
 }
 
 // Screened plan scores of the chunk (partials in group-block order) and the
@@ -920,7 +915,7 @@ __global__ __launch_bounds__(kThreads) void k_fscreen(FArgs a, int64_t p0, int64
 __global__ __launch_bounds__(kThreads) void k_fsum(FArgs a, int64_t p0, int64_t pc, int first_chunk)
 {
     __shared__ double lmin[kWaves];
-    const int nb = (a.G + kGroupsPerWave - 1) / kGroupsPerWave;
+    const int nb = (a.G + kBlk - 1) / kBlk;
     double mn = first_chunk ? INFINITY : a.bmin[blockIdx.x];
     for (int64_t c = (int64_t)blockIdx.x * kThreads + threadIdx.x; c < pc;
          c += (int64_t)gridDim.x * kThreads) {
@@ -1170,7 +1165,7 @@ int64_t chunk_of(int32_t G, int64_t P, int64_t want)
 }
 
 struct FLayout {
-    size_t grp, req, inst, first, slo64, tail, nreq, rec, bucket, bcnt, piece, start, part, F, bmin, ncand,
+    size_t grp, req, inst, first, slo64, tail, nreq, bucket, bcnt, piece, start, part, F, bmin, ncand,
         cand, Q, total;
     int64_t chunk;
 };
@@ -1181,7 +1176,7 @@ FLayout flayout(const qlm_problem *pr, int64_t P, int64_t n_req, int64_t chunk)
     const int32_t G = pr->n_groups, I = pr->n_instances;
     L.chunk = chunk_of(G, P, chunk);
     const int64_t Pn = P > 0 ? P : 1;
-    const int nb = (G + kGroupsPerWave - 1) / kGroupsPerWave;
+    const int nb = (G + kBlk - 1) / kBlk;
     size_t o = 0;
     auto put = [&](size_t &field, size_t bytes) {
         field = o;
@@ -1194,7 +1189,6 @@ FLayout flayout(const qlm_problem *pr, int64_t P, int64_t n_req, int64_t chunk)
     put(L.slo64, 8 * ((size_t)n_req + 1));
     put(L.tail, 8 * (size_t)qlm_tail::kCells);
     put(L.nreq, 8);
-    put(L.rec, sizeof(FRec) * (size_t)G * (size_t)(L.chunk + kRecPad));
     const size_t tiles = (size_t)(L.chunk / kWave);
     const size_t nblk = (size_t)((G + kBlk - 1) / kBlk);
     put(L.bucket, sizeof(FRec) * tiles * nblk * (size_t)kBlkCap);
@@ -1253,7 +1247,6 @@ FArgs fargs(const qlm_problem *pr, const qlm_plans *pl, const float *req_slo, in
     a.slo64 = (double *)(w + L.slo64);
     a.tail = (float2 *)(w + L.tail);
     a.nreq = (double *)(w + L.nreq);
-    a.rec = (FRec *)(w + L.rec);
     a.bucket = (FRec *)(w + L.bucket);
     a.bcnt = (int32_t *)(w + L.bcnt);
     a.piece = (Piece *)(w + L.piece);
@@ -1265,7 +1258,6 @@ FArgs fargs(const qlm_problem *pr, const qlm_plans *pl, const float *req_slo, in
     a.cand = (int64_t *)(w + L.cand);
     a.Q = (double *)(w + L.Q);
     a.chunk = L.chunk;
-    a.rld = L.chunk + kRecPad;
     return a;
 }
 
@@ -1352,7 +1344,6 @@ int launch_frec(const FArgs &a, size_t tab_bytes, dim3 grid, hipStream_t stream,
 int screen_all(const FArgs &a, hipStream_t stream)
 {
     int rc;
-    const int nb = (a.G + kGroupsPerWave - 1) / kGroupsPerWave;
     for (int64_t p0 = 0; p0 < a.P; p0 += a.chunk) {
         const int64_t pc = a.P - p0 < a.chunk ? a.P - p0 : a.chunk;
         const int64_t tiles = (pc + kWave - 1) / kWave;
@@ -1383,19 +1374,15 @@ int screen_all(const FArgs &a, hipStream_t stream)
         const int64_t tiles8 = (tiles + kXcds - 1) / kXcds * kXcds;
         if ((rc = launch_frec(a, tab_bytes, dim3((unsigned)(tiles8 * sq2)), stream, p0, pc)))
             return rc;
-        const hipError_t ea = hipFuncSetAttribute((const void *)k_ftrans,
+        const hipError_t ea = hipFuncSetAttribute((const void *)k_fbscreen,
                                                   hipFuncAttributeMaxDynamicSharedMemorySize,
                                                   (int)(sizeof(FRec) * kBlkCap));
         if (ea != hipSuccess) return hip_fail(ea, "hipFuncSetAttribute");
-        hipLaunchKernelGGL(k_ftrans, dim3((unsigned)(tiles * nblk)), dim3(kTransThreads),
-                           sizeof(FRec) * kBlkCap, stream, a, pc);
-        if ((rc = launched("k_ftrans launch"))) return rc;
-        const int64_t quads = (tiles + kWaves - 1) / kWaves;
         qlm_internal::TimedLaunch tl;
         if ((rc = qlm_internal::timing_begin(stream, &tl))) return rc;
-        hipLaunchKernelGGL(k_fscreen, dim3((unsigned)(quads * nb)), dim3(kThreads), 0, stream, a,
-                           p0, pc);
-        if ((rc = launched("k_fscreen launch"))) return rc;
+        hipLaunchKernelGGL(k_fbscreen, dim3((unsigned)(tiles * nblk)), dim3(kTransThreads),
+                           sizeof(FRec) * kBlkCap, stream, a, pc);
+        if ((rc = launched("k_fbscreen launch"))) return rc;
         qlm_internal::timing_end(stream, &tl);
         hipLaunchKernelGGL(k_fsum, dim3(kSumBlocks), dim3(kThreads), 0, stream, a, p0, pc,
                            p0 == 0 ? 1 : 0);
