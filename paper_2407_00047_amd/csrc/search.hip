@@ -1475,7 +1475,10 @@ __device__ inline void frel_body(const SearchArgs &a, int bid, float2 *tab, floa
 // screens run beside the long ones).  Per launch: nwg_r * B workgroups screen
 // the relocations within a queue, then I * nwg_b * B the MOVEs and RELOCATEs
 // into another queue.
-__global__ __launch_bounds__(kThreads) void k_fmove(SearchArgs a)
+// (six wavefronts per SIMD: the compiler keeps it within 80 registers, and
+// more wavefronts cover the lanes' chain of dependent reads before the walk)
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(6))) void k_fmove(
+    SearchArgs a)
 {
     __shared__ float2 tab[qlm_tail::kCells];
     __shared__ double lmin[kWaves];
