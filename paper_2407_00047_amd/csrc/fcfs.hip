@@ -24,11 +24,11 @@
 // group's start E[W] = A/Theta + K (double), its variance ahead (single,
 // scaled for the tail table) and its queue, gathered group by group; the
 // screen then takes one lane per plan and one wavefront per (64 plans, one
-// group): all 64 lanes work on the same group at a time, so the request SLOs are the
-// same across the wavefront and come through the scalar cache, the request's
-// position in its group is a constant of the unrolled loop, and each request
-// costs a margin in double, a variance in single and one read of the
-// normal-tail table (11 vector instructions).
+// group): all 64 lanes work on the same group at a time, so the request SLOs
+// are the same across the wavefront and come through the scalar cache, the
+// request's position in its group is a constant of the unrolled loop, and
+// each request costs a margin in double, a variance in single and one read of
+// the normal-tail table (11 vector instructions).
 //
 // The walk reads the plans slot-major with every lane (plan) of a wavefront at
 // the same slot, so its reads are coalesced.  It is cut into segments of 128
@@ -56,10 +56,10 @@
 // walked with exact comparisons throughout.
 //
 // Exact argmin.  Plans whose screened score is within twice the bound of the
-// lowest are re-scored exactly (k_fexact: one wavefront per queue, the running
+// lowest are re-scored exactly (k_fexact: one workgroup per queue, the running
 // sums rippled from lane to lane in position order, each request's term in
-// double with erfc, in the oracle's order), and the lowest exact score, the
-// lowest index on ties, wins.
+// double with erfc, its 16 wavefronts over slices of every group's requests),
+// and the lowest exact score, the lowest index on ties, wins.
 //
 // Kernels
 //   k_fprep     per group: clamped count, request offset, statistics; the
@@ -78,7 +78,7 @@
 //   k_fsum      partial scores -> screened plan scores, and the per-block
 //               minimum
 //   k_fselect   the plans within the bound of the lowest -> candidates
-//   k_fexact    one wavefront per (candidate, queue): exact queue scores
+//   k_fexact    one workgroup per (candidate, queue): exact queue scores
 //   k_fpick / k_fplan   exact plan scores; the lowest (score, index)
 #include <hip/hip_runtime.h>
 
