@@ -832,8 +832,8 @@ __device__ inline double group_screen(const FArgs &a, const float2 *tab, int i, 
 // records go into LDS at their (group, plan) place; the 16 wavefronts then
 // take the block's groups one at a time from a counter in LDS and screen each
 // from LDS, leaving the group's sum for every plan in the place of its record;
-// one wavefront adds them in group order, the block's partial score of each
-// plan.  The records sit in LDS as four arrays of 32-bit words (the low and
+// these are added in a fixed order (blocks of consecutive groups, then the
+// blocks), the block's partial score of each plan.  The records sit in LDS as four arrays of 32-bit words (the low and
 // high words of c0, v0, q), so that a scattered store's lanes land in banks by
 // their plan's lane alone: a 16-byte record per place would give the 64 lanes
 // of a store only 16 bank groups.  (Writing the records out as group rows for
@@ -902,10 +902,21 @@ __global__ __launch_bounds__(kTransThreads) void k_fbscreen(FArgs a, int64_t pc)
         w1[me] = (uint32_t)__double2hiint(Sg);
     }
     __syncthreads();
+    // the sums in a fixed order: each wavefront adds kBlk / 16 consecutive
+    // groups, then one wavefront adds the 16 partials (in the record words
+    // v0, q, free now)
+    constexpr int kPer = kBlk / (kTransThreads / kWave);
+    const int wv = wave_id();
+    double part = 0.0;
+    for (int gi = wv * kPer; gi < min(ng, wv * kPer + kPer); ++gi)
+        part += __hiloint2double((int)w1[gi * kWave + lane], (int)w0[gi * kWave + lane]);
+    w2[wv * kWave + lane] = (uint32_t)__double2loint(part);
+    w3[wv * kWave + lane] = (uint32_t)__double2hiint(part);
+    __syncthreads();
     if (threadIdx.x < kWave) {
         double tot = 0.0;
-        for (int gi = 0; gi < ng; ++gi)
-            tot += __hiloint2double((int)w1[gi * kWave + lane], (int)w0[gi * kWave + lane]);
+        for (int k = 0; k < kTransThreads / kWave; ++k)
+            tot += __hiloint2double((int)w3[k * kWave + lane], (int)w2[k * kWave + lane]);
         if (on) a.part[(int64_t)gb * a.chunk + col0] = tot;
     }
 }
